@@ -1,0 +1,184 @@
+"""Python access to the plain CPU oracle (``liboracle.so``).
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()``
+and the ``cpu_baseline`` leg of ``bench.py``; never by the product package.
+Arguments are numpy arrays in host memory; every function is argument
+marshalling around the C oracle in ``wm_oracle.c``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liboracle.so")
+SOURCES = [os.path.join(HERE, "wm_oracle.c")]
+
+CRC32_ZLIB = 0
+CRC32C = 1
+
+V_HEADER, V_TABLE, V_RECORD, V_DATA, V_STAGING = 1, 2, 4, 8, 16
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc into oracle/liboracle.so."""
+    if not force and os.path.exists(LIB_PATH):
+        return LIB_PATH
+    tmp = LIB_PATH + ".tmp"
+    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-shared", "-fPIC",
+           "-pthread", *SOURCES, "-o", tmp]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB_PATH)
+    return LIB_PATH
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        L = ctypes.CDLL(LIB_PATH)
+        u8p = ctypes.POINTER(ctypes.c_uint8)
+        u32p = ctypes.POINTER(ctypes.c_uint32)
+        u64p = ctypes.POINTER(ctypes.c_uint64)
+        L.orc_crc_bitwise.argtypes = [ctypes.c_int, u8p, ctypes.c_uint64]
+        L.orc_crc_bitwise.restype = ctypes.c_uint32
+        L.orc_crc.argtypes = [ctypes.c_int, u8p, ctypes.c_uint64]
+        L.orc_crc.restype = ctypes.c_uint32
+        L.orc_checksum_chunks.argtypes = [ctypes.c_int, u8p, ctypes.c_uint64,
+                                          ctypes.c_uint32, u32p, u32p,
+                                          ctypes.c_int]
+        L.orc_checksum_chunks.restype = ctypes.c_int
+        L.orc_diff_dirty.argtypes = [u8p, u8p, ctypes.c_uint64, ctypes.c_uint32,
+                                     u32p, ctypes.c_int]
+        L.orc_diff_dirty.restype = ctypes.c_uint32
+        L.orc_payload_bound.argtypes = [ctypes.c_uint64, ctypes.c_uint32,
+                                        ctypes.c_uint32]
+        L.orc_payload_bound.restype = ctypes.c_uint64
+        L.orc_encode.argtypes = [ctypes.c_int, u8p, ctypes.c_uint64,
+                                 ctypes.c_uint32, u32p, ctypes.c_uint32, u8p,
+                                 ctypes.c_uint64, ctypes.c_int]
+        L.orc_encode.restype = ctypes.c_int64
+        L.orc_plan_chunk.argtypes = [u8p, ctypes.c_uint32, u32p, u32p, u32p,
+                                     u32p, u64p]
+        L.orc_plan_chunk.restype = ctypes.c_int
+        L.orc_decode_verify.argtypes = [ctypes.c_int, u8p, ctypes.c_uint64,
+                                        ctypes.c_uint64, ctypes.c_uint32, u8p,
+                                        ctypes.c_uint64, u32p, ctypes.c_uint32,
+                                        ctypes.c_int]
+        L.orc_decode_verify.restype = ctypes.c_uint32
+        L.orc_commit.argtypes = [u8p, ctypes.c_uint64, ctypes.c_uint32, u8p,
+                                 u8p, ctypes.c_uint32]
+        L.orc_commit.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _bytes(a) -> np.ndarray:
+    a = np.ascontiguousarray(a)
+    return a.reshape(-1).view(np.uint8)
+
+
+def _p8(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8))
+
+
+def _p32(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))
+
+
+def crc(kind: int, data) -> int:
+    b = _bytes(data)
+    return int(lib().orc_crc(kind, _p8(b), b.size))
+
+
+def crc_bitwise(kind: int, data) -> int:
+    b = _bytes(data)
+    return int(lib().orc_crc_bitwise(kind, _p8(b), b.size))
+
+
+def n_chunks(nbytes: int, chunk: int) -> int:
+    return (nbytes + chunk - 1) // chunk
+
+
+def checksum_chunks(kind: int, data, chunk: int = 65536, threads: int = 1):
+    """Per-chunk CRCs (uint32 array) and the whole-buffer CRC."""
+    b = _bytes(data)
+    out = np.zeros(max(n_chunks(b.size, chunk), 1), np.uint32)
+    g = np.zeros(1, np.uint32)
+    rc = lib().orc_checksum_chunks(kind, _p8(b), b.size, chunk, _p32(out),
+                                   _p32(g), threads)
+    if rc != 0:
+        raise ValueError("orc_checksum_chunks rejected its arguments")
+    return out[: n_chunks(b.size, chunk)], int(g[0])
+
+
+def diff_dirty(cur, prev, chunk: int = 65536, threads: int = 1) -> np.ndarray:
+    c, p = _bytes(cur), _bytes(prev)
+    assert c.size == p.size
+    idx = np.zeros(max(n_chunks(c.size, chunk), 1), np.uint32)
+    m = lib().orc_diff_dirty(_p8(c), _p8(p), c.size, chunk, _p32(idx), threads)
+    return idx[:m].copy()
+
+
+def payload_bound(nbytes: int, chunk: int, n_records: int) -> int:
+    return int(lib().orc_payload_bound(nbytes, chunk, n_records))
+
+
+def encode(kind: int, state, chunk: int = 65536, idx=None,
+           threads: int = 1) -> np.ndarray:
+    """Payload bytes (uint8 array of exactly payload_bytes)."""
+    b = _bytes(state)
+    if idx is None:
+        n_rec, pidx = n_chunks(b.size, chunk), None
+        idx_arr = None
+    else:
+        idx_arr = np.ascontiguousarray(idx, dtype=np.uint32)
+        n_rec = idx_arr.size
+        pidx = _p32(idx_arr) if idx_arr.size else _p32(np.zeros(1, np.uint32))
+    cap = payload_bound(b.size, chunk, n_rec)
+    out = np.zeros(max(cap, 64), np.uint8)
+    n = lib().orc_encode(kind, _p8(b), b.size, chunk, pidx, n_rec, _p8(out),
+                         out.size, threads)
+    if n < 0:
+        raise ValueError(f"orc_encode failed ({n})")
+    return out[:n].copy()
+
+
+def plan_chunk(chunk_bytes) -> dict:
+    b = _bytes(chunk_bytes)
+    m, k, base, esc = (np.zeros(1, np.uint32) for _ in range(4))
+    size = np.zeros(1, np.uint64)
+    lib().orc_plan_chunk(_p8(b), b.size, _p32(m), _p32(k), _p32(base),
+                         _p32(esc),
+                         size.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)))
+    return dict(mode=int(m[0]), k=int(k[0]), base=int(base[0]),
+                n_esc=int(esc[0]), size=int(size[0]))
+
+
+def decode_verify(kind: int, payload, nbytes: int, chunk: int = 65536,
+                  staging_cap: int | None = None, threads: int = 1):
+    """Returns (verdict, staging uint8 array, per-record status array)."""
+    p = _bytes(payload)
+    if staging_cap is None:
+        staging_cap = n_chunks(nbytes, chunk) * chunk
+    staging = np.zeros(max(staging_cap, 1), np.uint8)
+    nst = max(n_chunks(nbytes, chunk), 1)
+    status = np.zeros(nst, np.uint32)
+    v = lib().orc_decode_verify(kind, _p8(p), p.size, nbytes, chunk,
+                                _p8(staging), staging_cap, _p32(status), nst,
+                                threads)
+    return int(v), staging[:staging_cap], status
+
+
+def commit(live: np.ndarray, chunk: int, staging, payload, verdict: int) -> int:
+    """In-place install into `live` (uint8 array). 0 = installed, 1 = refused."""
+    assert live.dtype == np.uint8 and live.flags.c_contiguous
+    s, p = _bytes(staging), _bytes(payload)
+    return int(lib().orc_commit(_p8(live), live.size, chunk, _p8(s), _p8(p),
+                                verdict))

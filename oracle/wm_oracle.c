@@ -1,0 +1,610 @@
+/*
+ * wm_oracle.c -- plain CPU oracle for the exact-state mover's data path.
+ *
+ * TEST INFRASTRUCTURE ONLY (see wm_oracle.h).  Slow on purpose: every step is
+ * written the way its definition reads.  Threads only split the loop over
+ * independent chunks; outputs do not depend on the thread count.
+ *
+ * Payload format v1 (this project's own definition; the paper names a lossless
+ * codec but fixes no byte layout, §6.4 codec paragraph).  All integers are
+ * little-endian, all sections are padded with zero bytes to a multiple of 16.
+ *
+ *   header (64 B)
+ *     0 u32 magic 'W','M','V','1'     4 u16 version = 1
+ *     6 u8  crc kind                  7 u8  codec = 1
+ *     8 u32 chunk_bytes              12 u32 n_chunks = ceil(state_bytes/chunk)
+ *    16 u64 state_bytes              24 u32 n_records
+ *    28 u32 flags (bit0 FULL)        32 u64 payload_bytes
+ *    40 u32 global_crc (CRC of the whole source state)
+ *    44 u32 table_crc  (CRC of the 16*n_records table bytes)
+ *    48..59 zero                     60 u32 header_crc = CRC(bytes 0..59)
+ *   table (16 B per record): u32 chunk_idx, u32 src_crc, u64 record_offset
+ *   records, contiguous, in table order.  Record:
+ *     0 u8 mode (0 RAW, 1 PACK)  1 u8 k  2 u8 base  3 u8 0
+ *     4 u32 n_words  8 u32 n_esc  12 u32 rec_crc = CRC(record bytes 0..11)
+ *     RAW : the chunk's bytes
+ *     PACK: codes (ceil(n*k/8) B, LSB-first k-bit codes) | escapes (n_esc B)
+ *           | sign/mantissa plane (n B)
+ *   A bf16 word w splits into sign w>>15, exponent e = (w>>7)&255 and
+ *   mantissa w&127; sm = sign<<7 | mantissa.  PACK with k >= 1 codes e as
+ *   e - base when 0 <= e - base < 2^k - 1, else as ESC = 2^k - 1 with e
+ *   appended to the escapes; PACK with k = 0 means every e equals base.
+ */
+#include "wm_oracle.h"
+
+#include <pthread.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------ CRC -- */
+
+static uint32_t poly_of(int kind) {
+  return kind == ORC_CRC32C ? 0x82F63B78u : 0xEDB88320u;
+}
+
+/* The reflected CRC-32 register update, one message bit at a time. */
+uint32_t orc_crc_bitwise(int kind, const uint8_t *p, uint64_t n) {
+  uint32_t poly = poly_of(kind);
+  uint32_t c = 0xFFFFFFFFu;
+  for (uint64_t i = 0; i < n; i++) {
+    c ^= p[i];
+    for (int b = 0; b < 8; b++) c = (c >> 1) ^ (poly & (0u - (c & 1u)));
+  }
+  return c ^ 0xFFFFFFFFu;
+}
+
+static uint32_t byte_table[2][256];
+static pthread_once_t table_once = PTHREAD_ONCE_INIT;
+
+/* Entry v is the register after feeding byte v into a zero register through
+ * the bitwise step; a byte step is then c = table[(c ^ b) & 255] ^ (c >> 8). */
+static void build_tables(void) {
+  for (int kind = 0; kind < 2; kind++) {
+    uint32_t poly = poly_of(kind);
+    for (uint32_t v = 0; v < 256; v++) {
+      uint32_t c = v;
+      for (int b = 0; b < 8; b++) c = (c >> 1) ^ (poly & (0u - (c & 1u)));
+      byte_table[kind][v] = c;
+    }
+  }
+}
+
+uint32_t orc_crc(int kind, const uint8_t *p, uint64_t n) {
+  pthread_once(&table_once, build_tables);
+  const uint32_t *t = byte_table[kind == ORC_CRC32C ? 1 : 0];
+  uint32_t c = 0xFFFFFFFFu;
+  for (uint64_t i = 0; i < n; i++) c = t[(c ^ p[i]) & 255u] ^ (c >> 8);
+  return c ^ 0xFFFFFFFFu;
+}
+
+/* -------------------------------------------------------------- threads -- */
+
+typedef void (*range_fn)(void *ctx, uint64_t lo, uint64_t hi);
+typedef struct {
+  range_fn fn;
+  void *ctx;
+  uint64_t lo, hi;
+} range_job;
+
+static void *range_thread(void *arg) {
+  range_job *j = (range_job *)arg;
+  j->fn(j->ctx, j->lo, j->hi);
+  return NULL;
+}
+
+/* Run fn over [0, n) split into `threads` contiguous ranges. */
+static void parallel_for(uint64_t n, int threads, range_fn fn, void *ctx) {
+  if (threads < 1) threads = 1;
+  if (threads > 256) threads = 256;
+  if ((uint64_t)threads > n) threads = n ? (int)n : 1;
+  if (threads == 1) {
+    fn(ctx, 0, n);
+    return;
+  }
+  pthread_t tid[256];
+  range_job job[256];
+  for (int t = 0; t < threads; t++) {
+    job[t].fn = fn;
+    job[t].ctx = ctx;
+    job[t].lo = n * (uint64_t)t / (uint64_t)threads;
+    job[t].hi = n * (uint64_t)(t + 1) / (uint64_t)threads;
+    pthread_create(&tid[t], NULL, range_thread, &job[t]);
+  }
+  for (int t = 0; t < threads; t++) pthread_join(tid[t], NULL);
+}
+
+/* ------------------------------------------------------------- chunking -- */
+
+static uint64_t n_chunks_of(uint64_t nbytes, uint32_t chunk) {
+  return (nbytes + chunk - 1) / chunk;
+}
+static uint32_t chunk_len(uint64_t nbytes, uint32_t chunk, uint64_t c) {
+  uint64_t start = c * (uint64_t)chunk;
+  uint64_t left = nbytes - start;
+  return left < chunk ? (uint32_t)left : chunk;
+}
+static int chunk_ok(uint32_t chunk) {
+  /* a power of two between 4 KiB and 16 MiB */
+  return chunk >= 4096u && chunk <= (16u << 20) && (chunk & (chunk - 1)) == 0;
+}
+static uint64_t pad16(uint64_t x) { return (x + 15u) & ~(uint64_t)15u; }
+
+/* --------------------------------------------------------- checksumming -- */
+
+typedef struct {
+  int kind;
+  const uint8_t *data;
+  uint64_t nbytes;
+  uint32_t chunk;
+  uint32_t *crc;
+} ck_ctx;
+
+static void ck_range(void *vp, uint64_t lo, uint64_t hi) {
+  ck_ctx *x = (ck_ctx *)vp;
+  for (uint64_t c = lo; c < hi; c++)
+    x->crc[c] = orc_crc(x->kind, x->data + c * (uint64_t)x->chunk,
+                        chunk_len(x->nbytes, x->chunk, c));
+}
+
+int orc_checksum_chunks(int kind, const uint8_t *data, uint64_t nbytes,
+                        uint32_t chunk_bytes, uint32_t *crc_out,
+                        uint32_t *global_out, int threads) {
+  if (!chunk_ok(chunk_bytes) || (kind != 0 && kind != 1)) return -1;
+  ck_ctx x = {kind, data, nbytes, chunk_bytes, crc_out};
+  parallel_for(n_chunks_of(nbytes, chunk_bytes), threads, ck_range, &x);
+  /* the global CRC is the plain CRC of the whole buffer, read again */
+  if (global_out) *global_out = orc_crc(kind, data, nbytes);
+  return 0;
+}
+
+/* ----------------------------------------------------------------- diff -- */
+
+typedef struct {
+  const uint8_t *cur, *prev;
+  uint64_t nbytes;
+  uint32_t chunk;
+  uint8_t *dirty;
+} df_ctx;
+
+static void df_range(void *vp, uint64_t lo, uint64_t hi) {
+  df_ctx *x = (df_ctx *)vp;
+  for (uint64_t c = lo; c < hi; c++) {
+    uint64_t off = c * (uint64_t)x->chunk;
+    x->dirty[c] = memcmp(x->cur + off, x->prev + off,
+                         chunk_len(x->nbytes, x->chunk, c)) != 0;
+  }
+}
+
+uint32_t orc_diff_dirty(const uint8_t *cur, const uint8_t *prev,
+                        uint64_t nbytes, uint32_t chunk_bytes,
+                        uint32_t *idx_out, int threads) {
+  if (!chunk_ok(chunk_bytes)) return 0;
+  uint64_t n = n_chunks_of(nbytes, chunk_bytes);
+  uint8_t *dirty = (uint8_t *)calloc(n ? n : 1, 1);
+  df_ctx x = {cur, prev, nbytes, chunk_bytes, dirty};
+  parallel_for(n, threads, df_range, &x);
+  uint32_t m = 0;
+  for (uint64_t c = 0; c < n; c++)
+    if (dirty[c]) idx_out[m++] = (uint32_t)c;
+  free(dirty);
+  return m;
+}
+
+/* ---------------------------------------------------------------- codec -- */
+
+static uint16_t word_at(const uint8_t *p, uint32_t i) {
+  return (uint16_t)(p[2 * i] | (p[2 * i + 1] << 8));
+}
+static uint32_t exponent_of(uint16_t w) { return (w >> 7) & 255u; }
+static uint8_t sm_of(uint16_t w) {
+  return (uint8_t)(((w >> 15) << 7) | (w & 127u));
+}
+
+static uint64_t raw_size(uint32_t n) { return 16 + pad16(2 * (uint64_t)n); }
+static uint64_t pack_size(uint32_t n, uint32_t k, uint32_t n_esc) {
+  return 16 + pad16(((uint64_t)n * k + 7) / 8) + pad16(n_esc) + pad16(n);
+}
+
+/* Mode choice for one chunk of len bytes (len even).  Candidates, in the
+ * order that also breaks ties: RAW, PACK k=0 (only when every exponent is the
+ * same), PACK k=1..7 with the base that puts the most words inside the
+ * window [base, base + 2^k - 2] (smallest base on ties).  The smallest
+ * record wins. */
+int orc_plan_chunk(const uint8_t *chunk, uint32_t len, uint32_t *mode,
+                   uint32_t *k, uint32_t *base, uint32_t *n_esc,
+                   uint64_t *size) {
+  uint32_t n = len / 2;
+  uint64_t hist[256];
+  memset(hist, 0, sizeof(hist));
+  for (uint32_t i = 0; i < n; i++) hist[exponent_of(word_at(chunk, i))]++;
+
+  uint32_t distinct = 0, only = 0;
+  for (uint32_t e = 0; e < 256; e++)
+    if (hist[e]) {
+      distinct++;
+      only = e;
+    }
+
+  uint32_t best_mode = 0, best_k = 0, best_base = 0, best_esc = 0;
+  uint64_t best = raw_size(n);
+
+  if (distinct == 1) {
+    uint64_t s = pack_size(n, 0, 0);
+    if (s < best) {
+      best = s;
+      best_mode = 1;
+      best_k = 0;
+      best_base = only;
+      best_esc = 0;
+    }
+  }
+  for (uint32_t kk = 1; kk <= 7; kk++) {
+    uint32_t window = (1u << kk) - 1u;
+    uint64_t top = 0;
+    uint32_t top_base = 0;
+    for (uint32_t b = 0; b < 256; b++) {
+      uint64_t inside = 0;
+      for (uint32_t e = b; e < b + window && e < 256; e++) inside += hist[e];
+      if (inside > top) {
+        top = inside;
+        top_base = b;
+      }
+    }
+    uint32_t esc = n - (uint32_t)top;
+    uint64_t s = pack_size(n, kk, esc);
+    if (s < best) {
+      best = s;
+      best_mode = 1;
+      best_k = kk;
+      best_base = top_base;
+      best_esc = esc;
+    }
+  }
+  *mode = best_mode;
+  *k = best_k;
+  *base = best_base;
+  *n_esc = best_esc;
+  *size = best;
+  return 0;
+}
+
+static void put_u16(uint8_t *p, uint16_t v) {
+  p[0] = (uint8_t)v;
+  p[1] = (uint8_t)(v >> 8);
+}
+static void put_u32(uint8_t *p, uint32_t v) {
+  for (int i = 0; i < 4; i++) p[i] = (uint8_t)(v >> (8 * i));
+}
+static void put_u64(uint8_t *p, uint64_t v) {
+  for (int i = 0; i < 8; i++) p[i] = (uint8_t)(v >> (8 * i));
+}
+static uint32_t get_u32(const uint8_t *p) {
+  return (uint32_t)p[0] | ((uint32_t)p[1] << 8) | ((uint32_t)p[2] << 16) |
+         ((uint32_t)p[3] << 24);
+}
+static uint64_t get_u64(const uint8_t *p) {
+  return (uint64_t)get_u32(p) | ((uint64_t)get_u32(p + 4) << 32);
+}
+
+/* Write one record (size bytes, already zeroed by the caller). */
+static void write_record(int kind, const uint8_t *chunk, uint32_t len,
+                         uint32_t mode, uint32_t k, uint32_t base,
+                         uint32_t n_esc, uint8_t *out) {
+  uint32_t n = len / 2;
+  out[0] = (uint8_t)mode;
+  out[1] = (uint8_t)k;
+  out[2] = (uint8_t)base;
+  out[3] = 0;
+  put_u32(out + 4, n);
+  put_u32(out + 8, n_esc);
+  put_u32(out + 12, orc_crc(kind, out, 12));
+  uint8_t *body = out + 16;
+  if (mode == 0) {
+    memcpy(body, chunk, len);
+    return;
+  }
+  uint8_t *codes = body;
+  uint8_t *escapes = codes + pad16(((uint64_t)n * k + 7) / 8);
+  uint8_t *sm = escapes + pad16(n_esc);
+  uint32_t esc_code = (1u << k) - 1u;
+  uint32_t esc_written = 0;
+  for (uint32_t i = 0; i < n; i++) {
+    uint16_t w = word_at(chunk, i);
+    uint32_t e = exponent_of(w);
+    sm[i] = sm_of(w);
+    if (k == 0) continue; /* every exponent equals base */
+    uint32_t code;
+    if (e >= base && e - base < esc_code) {
+      code = e - base;
+    } else {
+      code = esc_code;
+      escapes[esc_written++] = (uint8_t)e;
+    }
+    /* stream bit i*k + b is bit b of code i; stream bit j lives in bit
+     * j % 8 of byte j / 8 */
+    for (uint32_t b = 0; b < k; b++) {
+      uint64_t j = (uint64_t)i * k + b;
+      if ((code >> b) & 1u) codes[j / 8] |= (uint8_t)(1u << (j % 8));
+    }
+  }
+}
+
+typedef struct {
+  int kind;
+  const uint8_t *state;
+  uint64_t nbytes;
+  uint32_t chunk;
+  const uint32_t *idx; /* NULL: record r is chunk r */
+  uint32_t *mode, *k, *base, *esc;
+  uint64_t *size, *offset;
+  uint8_t *payload;
+} en_ctx;
+
+static uint64_t en_chunk(const en_ctx *x, uint64_t r) {
+  return x->idx ? x->idx[r] : r;
+}
+
+static void en_plan_range(void *vp, uint64_t lo, uint64_t hi) {
+  en_ctx *x = (en_ctx *)vp;
+  for (uint64_t r = lo; r < hi; r++) {
+    uint64_t c = en_chunk(x, r);
+    orc_plan_chunk(x->state + c * (uint64_t)x->chunk,
+                   chunk_len(x->nbytes, x->chunk, c), &x->mode[r], &x->k[r],
+                   &x->base[r], &x->esc[r], &x->size[r]);
+  }
+}
+
+static void en_write_range(void *vp, uint64_t lo, uint64_t hi) {
+  en_ctx *x = (en_ctx *)vp;
+  for (uint64_t r = lo; r < hi; r++) {
+    uint64_t c = en_chunk(x, r);
+    const uint8_t *src = x->state + c * (uint64_t)x->chunk;
+    uint32_t len = chunk_len(x->nbytes, x->chunk, c);
+    uint8_t *entry = x->payload + 64 + 16 * r;
+    put_u32(entry, (uint32_t)c);
+    put_u32(entry + 4, orc_crc(x->kind, src, len));
+    put_u64(entry + 8, x->offset[r]);
+    write_record(x->kind, src, len, x->mode[r], x->k[r], x->base[r],
+                 x->esc[r], x->payload + x->offset[r]);
+  }
+}
+
+uint64_t orc_payload_bound(uint64_t nbytes, uint32_t chunk_bytes,
+                           uint32_t n_records) {
+  (void)nbytes; /* every record is bounded by a full RAW chunk */
+  if (!chunk_ok(chunk_bytes)) return 0;
+  return 64 + 16 * (uint64_t)n_records +
+         (uint64_t)n_records * raw_size(chunk_bytes / 2);
+}
+
+int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
+                   uint32_t chunk_bytes, const uint32_t *idx, uint32_t n_idx,
+                   uint8_t *payload, uint64_t cap, int threads) {
+  if (!chunk_ok(chunk_bytes) || (kind != 0 && kind != 1) || (nbytes & 1))
+    return -1;
+  uint64_t n_chunks = n_chunks_of(nbytes, chunk_bytes);
+  uint64_t n_rec = idx ? n_idx : n_chunks;
+  if (n_rec > n_chunks) return -1;
+  for (uint64_t r = 0; idx && r < n_rec; r++)
+    if (idx[r] >= n_chunks || (r && idx[r] <= idx[r - 1])) return -1;
+  if (cap < orc_payload_bound(nbytes, chunk_bytes, (uint32_t)n_rec)) return -2;
+
+  uint64_t m = n_rec ? n_rec : 1;
+  en_ctx x;
+  x.kind = kind;
+  x.state = state;
+  x.nbytes = nbytes;
+  x.chunk = chunk_bytes;
+  x.idx = idx;
+  x.mode = (uint32_t *)calloc(m, 4);
+  x.k = (uint32_t *)calloc(m, 4);
+  x.base = (uint32_t *)calloc(m, 4);
+  x.esc = (uint32_t *)calloc(m, 4);
+  x.size = (uint64_t *)calloc(m, 8);
+  x.offset = (uint64_t *)calloc(m, 8);
+  x.payload = payload;
+
+  /* 1. plan every record; 2. record offsets are the exclusive prefix sum of
+   * record sizes after the table; 3. write table entries and records. */
+  parallel_for(n_rec, threads, en_plan_range, &x);
+  uint64_t at = 64 + 16 * n_rec;
+  for (uint64_t r = 0; r < n_rec; r++) {
+    x.offset[r] = at;
+    at += x.size[r];
+  }
+  uint64_t total = at;
+  memset(payload, 0, total);
+  parallel_for(n_rec, threads, en_write_range, &x);
+
+  uint8_t *h = payload;
+  h[0] = 'W';
+  h[1] = 'M';
+  h[2] = 'V';
+  h[3] = '1';
+  put_u16(h + 4, 1);
+  h[6] = (uint8_t)kind;
+  h[7] = 1;
+  put_u32(h + 8, chunk_bytes);
+  put_u32(h + 12, (uint32_t)n_chunks);
+  put_u64(h + 16, nbytes);
+  put_u32(h + 24, (uint32_t)n_rec);
+  put_u32(h + 28, idx ? 0u : 1u);
+  put_u64(h + 32, total);
+  put_u32(h + 40, orc_crc(kind, state, nbytes));
+  put_u32(h + 44, orc_crc(kind, payload + 64, 16 * n_rec));
+  put_u32(h + 60, orc_crc(kind, h, 60));
+
+  free(x.mode);
+  free(x.k);
+  free(x.base);
+  free(x.esc);
+  free(x.size);
+  free(x.offset);
+  return (int64_t)total;
+}
+
+/* --------------------------------------------------------------- decode -- */
+
+static int all_zero(const uint8_t *p, uint64_t n) {
+  for (uint64_t i = 0; i < n; i++)
+    if (p[i]) return 0;
+  return 1;
+}
+
+/* Structure checks and decode of one record occupying rec[0..L).  Returns 0,
+ * ORC_V_RECORD or ORC_V_DATA; on 0 the chunk's len bytes are in out. */
+static uint32_t decode_record(int kind, const uint8_t *rec, uint64_t L,
+                              uint32_t len, uint32_t src_crc, uint8_t *out) {
+  uint32_t n = len / 2;
+  if (L < 16) return ORC_V_RECORD;
+  if (orc_crc(kind, rec, 12) != get_u32(rec + 12)) return ORC_V_RECORD;
+  uint32_t mode = rec[0], k = rec[1], base = rec[2];
+  uint32_t n_words = get_u32(rec + 4), n_esc = get_u32(rec + 8);
+  if (rec[3] != 0 || n_words != n || mode > 1) return ORC_V_RECORD;
+  const uint8_t *body = rec + 16;
+
+  if (mode == 0) {
+    if (k != 0 || base != 0 || n_esc != 0) return ORC_V_RECORD;
+    if (L != raw_size(n)) return ORC_V_RECORD;
+    if (!all_zero(body + 2 * (uint64_t)n, pad16(2 * (uint64_t)n) - 2 * n))
+      return ORC_V_RECORD;
+    memcpy(out, body, len);
+  } else {
+    if (k > 7 || n_esc > n || (k == 0 && n_esc != 0)) return ORC_V_RECORD;
+    if (L != pack_size(n, k, n_esc)) return ORC_V_RECORD;
+    uint64_t code_bytes = ((uint64_t)n * k + 7) / 8;
+    const uint8_t *codes = body;
+    const uint8_t *escapes = codes + pad16(code_bytes);
+    const uint8_t *sm = escapes + pad16(n_esc);
+    /* padding: whole bytes after each section, and stream bits past n*k */
+    if (!all_zero(codes + code_bytes, pad16(code_bytes) - code_bytes) ||
+        !all_zero(escapes + n_esc, pad16(n_esc) - n_esc) ||
+        !all_zero(sm + n, pad16(n) - n))
+      return ORC_V_RECORD;
+    uint64_t used_bits = (uint64_t)n * k;
+    if (used_bits % 8 && (codes[used_bits / 8] >> (used_bits % 8)))
+      return ORC_V_RECORD;
+    uint32_t esc_code = (1u << k) - 1u;
+    uint32_t esc_read = 0;
+    for (uint32_t i = 0; i < n; i++) {
+      uint32_t e;
+      if (k == 0) {
+        e = base;
+      } else {
+        uint32_t code = 0;
+        for (uint32_t b = 0; b < k; b++) {
+          uint64_t j = (uint64_t)i * k + b;
+          code |= (uint32_t)((codes[j / 8] >> (j % 8)) & 1u) << b;
+        }
+        if (code == esc_code) {
+          if (esc_read >= n_esc) return ORC_V_RECORD;
+          e = escapes[esc_read++];
+        } else {
+          if (base + code > 255u) return ORC_V_RECORD;
+          e = base + code;
+        }
+      }
+      uint16_t w = (uint16_t)(((uint32_t)(sm[i] >> 7) << 15) | (e << 7) |
+                              (sm[i] & 127u));
+      put_u16(out + 2 * (uint64_t)i, w);
+    }
+    if (esc_read != n_esc) return ORC_V_RECORD;
+  }
+  return orc_crc(kind, out, len) == src_crc ? 0u : ORC_V_DATA;
+}
+
+typedef struct {
+  int kind;
+  const uint8_t *payload;
+  uint64_t payload_bytes, nbytes;
+  uint32_t chunk, n_rec;
+  uint8_t *staging;
+  uint32_t *status;
+} de_ctx;
+
+static void de_range(void *vp, uint64_t lo, uint64_t hi) {
+  de_ctx *x = (de_ctx *)vp;
+  for (uint64_t r = lo; r < hi; r++) {
+    const uint8_t *e = x->payload + 64 + 16 * r;
+    uint32_t c = get_u32(e);
+    uint64_t off = get_u64(e + 8);
+    uint64_t end = r + 1 < x->n_rec ? get_u64(e + 16 + 8) : x->payload_bytes;
+    x->status[r] = decode_record(x->kind, x->payload + off, end - off,
+                                 chunk_len(x->nbytes, x->chunk, c),
+                                 get_u32(e + 4),
+                                 x->staging + r * (uint64_t)x->chunk);
+  }
+}
+
+uint32_t orc_decode_verify(int kind, const uint8_t *payload, uint64_t cap,
+                           uint64_t nbytes, uint32_t chunk_bytes,
+                           uint8_t *staging, uint64_t staging_cap,
+                           uint32_t *rec_status, uint32_t n_status,
+                           int threads) {
+  if (!chunk_ok(chunk_bytes) || (kind != 0 && kind != 1)) return ORC_V_HEADER;
+  uint64_t n_chunks = n_chunks_of(nbytes, chunk_bytes);
+
+  /* header */
+  if (cap < 64) return ORC_V_HEADER;
+  const uint8_t *h = payload;
+  if (orc_crc(kind, h, 60) != get_u32(h + 60)) return ORC_V_HEADER;
+  if (h[0] != 'W' || h[1] != 'M' || h[2] != 'V' || h[3] != '1')
+    return ORC_V_HEADER;
+  if ((h[4] | (h[5] << 8)) != 1 || h[6] != (uint8_t)kind || h[7] != 1)
+    return ORC_V_HEADER;
+  if (get_u32(h + 8) != chunk_bytes || get_u32(h + 12) != n_chunks ||
+      get_u64(h + 16) != nbytes)
+    return ORC_V_HEADER;
+  uint32_t n_rec = get_u32(h + 24), flags = get_u32(h + 28);
+  uint64_t payload_bytes = get_u64(h + 32);
+  if ((flags & ~1u) || !all_zero(h + 48, 12)) return ORC_V_HEADER;
+  if (n_rec > n_chunks) return ORC_V_HEADER;
+  if (64 + 16 * (uint64_t)n_rec > payload_bytes || payload_bytes > cap)
+    return ORC_V_HEADER;
+  if ((flags & 1u) && n_rec != n_chunks) return ORC_V_HEADER;
+  if ((uint64_t)n_rec * chunk_bytes > staging_cap) return ORC_V_STAGING;
+
+  /* table */
+  const uint8_t *t = payload + 64;
+  uint64_t table_end = 64 + 16 * (uint64_t)n_rec;
+  if (orc_crc(kind, t, 16 * (uint64_t)n_rec) != get_u32(h + 44))
+    return ORC_V_TABLE;
+  if (n_rec == 0 && payload_bytes != table_end) return ORC_V_TABLE;
+  for (uint32_t r = 0; r < n_rec; r++) {
+    uint32_t c = get_u32(t + 16 * (uint64_t)r);
+    uint64_t off = get_u64(t + 16 * (uint64_t)r + 8);
+    uint64_t end = r + 1 < n_rec ? get_u64(t + 16 * (uint64_t)(r + 1) + 8)
+                                 : payload_bytes;
+    if (c >= n_chunks) return ORC_V_TABLE;
+    if (r && c <= get_u32(t + 16 * (uint64_t)(r - 1))) return ORC_V_TABLE;
+    if (r == 0 && off != table_end) return ORC_V_TABLE;
+    if (off % 16 || off >= end) return ORC_V_TABLE;
+  }
+
+  /* records */
+  uint32_t *status = (uint32_t *)calloc(n_rec ? n_rec : 1, 4);
+  de_ctx x = {kind,   payload,    payload_bytes, nbytes, chunk_bytes,
+              n_rec,  staging,    status};
+  parallel_for(n_rec, threads, de_range, &x);
+  uint32_t verdict = 0;
+  for (uint32_t r = 0; r < n_rec; r++) {
+    verdict |= status[r];
+    if (rec_status && r < n_status) rec_status[r] = status[r];
+  }
+  free(status);
+  return verdict;
+}
+
+int orc_commit(uint8_t *live, uint64_t nbytes, uint32_t chunk_bytes,
+               const uint8_t *staging, const uint8_t *payload,
+               uint32_t verdict) {
+  if (verdict != 0) return 1;
+  uint32_t n_rec = get_u32(payload + 24);
+  for (uint32_t r = 0; r < n_rec; r++) {
+    uint32_t c = get_u32(payload + 64 + 16 * (uint64_t)r);
+    memcpy(live + (uint64_t)c * chunk_bytes,
+           staging + (uint64_t)r * chunk_bytes,
+           chunk_len(nbytes, chunk_bytes, c));
+  }
+  return 0;
+}

@@ -1,0 +1,102 @@
+/*
+ * wm_oracle.h -- plain CPU oracle for the exact-state mover's data path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may include, link,
+ * load or call this code; it exists so that tests, the smoke check and the
+ * CPU-baseline leg of the benchmark can compare the HIP library against an
+ * independent, slow, obviously-correct implementation.  It shares no source
+ * with the HIP library: every constant below is restated here from the
+ * written payload-format definition, not taken from the library's headers.
+ *
+ * Paper passages followed (arXiv 2607.10389):
+ *   - Contract: the destination is bit-identical to the source or nothing is
+ *     installed (§1 Introduction; §4 "Sufficiency": commit only on a
+ *     byte-identical fingerprint).
+ *   - Checksum: per-chunk CRC of the flattened state, the CRC being zlib's
+ *     (§6.5 verification plane: "CPU-side zlib CRC"; hardware CRC is a fold
+ *     "of the same polynomial"), per-chunk CRCs combined into one global CRC
+ *     (§6.5; Appendix I "single global CRC").
+ *   - Dirty set: chunks rewritten since the last shipped round (§6.2
+ *     Exhibit 2 and Appendix H, iterative pre-copy).
+ *   - Codec: lossless, bf16 exponent plane carries the redundancy, receipts
+ *     bind to the decoded bytes so decode sits inside the verified envelope
+ *     (§6.4 codec paragraph).  The paper fixes no codec format; the byte
+ *     layout implemented here is this project's payload format v1.
+ *   - Shadow slot, verify, then commit or roll back (Table 1, session API).
+ *
+ * Functions return plain integers; no function allocates memory visible to
+ * the caller.  Buffers are host memory owned by the caller.
+ */
+#ifndef WM_ORACLE_H
+#define WM_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* CRC kinds */
+#define ORC_CRC32_ZLIB 0 /* reflected 0xEDB88320, init/xorout 0xFFFFFFFF */
+#define ORC_CRC32C 1     /* reflected 0x82F63B78, init/xorout 0xFFFFFFFF */
+
+/* verdict bits */
+#define ORC_V_HEADER 1u   /* header rejected (nothing else examined) */
+#define ORC_V_TABLE 2u    /* table rejected (records not examined) */
+#define ORC_V_RECORD 4u   /* a record's structure is invalid */
+#define ORC_V_DATA 8u     /* a decoded chunk's CRC differs from its receipt */
+#define ORC_V_STAGING 16u /* receiver staging too small for the records */
+
+/* CRC by its definition: one bit at a time. */
+uint32_t orc_crc_bitwise(int kind, const uint8_t *p, uint64_t n);
+/* Same function, one byte at a time through a 256-entry table that is
+ * derived from the bitwise step (Sarwate's method). */
+uint32_t orc_crc(int kind, const uint8_t *p, uint64_t n);
+
+/* Per-chunk CRCs over chunks of chunk_bytes (last chunk may be short) and
+ * the CRC of the whole buffer (global_out may be NULL). */
+int orc_checksum_chunks(int kind, const uint8_t *data, uint64_t nbytes,
+                        uint32_t chunk_bytes, uint32_t *crc_out,
+                        uint32_t *global_out, int threads);
+
+/* Ascending indices of chunks whose bytes differ; returns the count. */
+uint32_t orc_diff_dirty(const uint8_t *cur, const uint8_t *prev,
+                        uint64_t nbytes, uint32_t chunk_bytes,
+                        uint32_t *idx_out, int threads);
+
+/* Upper bound on the payload size for n_records records. */
+uint64_t orc_payload_bound(uint64_t nbytes, uint32_t chunk_bytes,
+                           uint32_t n_records);
+
+/* Encode the chunks listed in idx (ascending; idx == NULL means every chunk,
+ * which also sets the FULL flag) into payload.  Returns payload bytes, or
+ * -1 on invalid arguments, -2 when cap is too small. */
+int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
+                   uint32_t chunk_bytes, const uint32_t *idx, uint32_t n_idx,
+                   uint8_t *payload, uint64_t cap, int threads);
+
+/* Plan of one chunk's record (exposed for tests): mode, k, base, n_esc and
+ * record size in bytes. */
+int orc_plan_chunk(const uint8_t *chunk, uint32_t len, uint32_t *mode,
+                   uint32_t *k, uint32_t *base, uint32_t *n_esc,
+                   uint64_t *size);
+
+/* Validate and decode a payload into staging (record i at i*chunk_bytes).
+ * rec_status (may be NULL) receives 0, ORC_V_RECORD or ORC_V_DATA per
+ * record when the header and table are valid.  Returns the verdict. */
+uint32_t orc_decode_verify(int kind, const uint8_t *payload, uint64_t cap,
+                           uint64_t nbytes, uint32_t chunk_bytes,
+                           uint8_t *staging, uint64_t staging_cap,
+                           uint32_t *rec_status, uint32_t n_status,
+                           int threads);
+
+/* Install: verdict 0 copies each staged record to its chunk of live and
+ * returns 0; any other verdict leaves live untouched and returns 1. */
+int orc_commit(uint8_t *live, uint64_t nbytes, uint32_t chunk_bytes,
+               const uint8_t *staging, const uint8_t *payload,
+               uint32_t verdict);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,222 @@
+"""Pins for the oracle's payload codec (no GPU).
+
+The codec is this project's payload format v1 (the paper fixes no byte
+layout; its codec is lossless, splits bf16 planes and keeps decode inside the
+verified envelope: §6.4 codec paragraph).  Pins here do not reuse the oracle's
+code paths:
+  * round-trip identity on random, constant and all-65536-bit-pattern inputs;
+  * closed-form record sizes (constant chunk -> PACK k=0; uniform random
+    16-bit words -> RAW);
+  * a brute-force argmin over every (k, base) on tiny chunks;
+  * hand-built expected bytes for a two-chunk payload, with CRCs from zlib.
+"""
+import struct
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+
+CH = 4096  # smallest legal chunk; keeps brute force cheap
+
+
+def pad16(x):
+    return (x + 15) // 16 * 16
+
+
+def roundtrip(state_u8, chunk=CH, kind=0, idx=None):
+    payload = oracle.encode(kind, state_u8, chunk, idx)
+    v, staging, st = oracle.decode_verify(kind, payload, state_u8.size, chunk)
+    assert v == 0, (v, st)
+    live = np.zeros_like(state_u8) if idx is None else state_u8.copy()
+    assert oracle.commit(live, chunk, staging, payload, v) == 0
+    return payload, live
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+def test_roundtrip_random_bf16(kind):
+    rng = np.random.default_rng(0)
+    x = (rng.standard_normal(5 * CH // 2 + 7) *
+         np.exp(0.5 * rng.standard_normal(1))).astype(np.float32)
+    bf = (x.view(np.uint32) >> 16).astype(np.uint16)
+    state = bf.view(np.uint8)
+    payload, live = roundtrip(state, kind=kind)
+    assert np.array_equal(live, state)
+    assert payload.size < state.size  # normal data compresses
+
+
+def test_roundtrip_all_bit_patterns():
+    allw = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    for order in ("sorted", "shuffled"):
+        w = allw if order == "sorted" else np.random.default_rng(3).permutation(allw)
+        state = w.view(np.uint8)
+        _, live = roundtrip(state)
+        assert np.array_equal(live, state)
+
+
+def test_roundtrip_special_values():
+    # NaN payloads, +-Inf, +-0, denormals, max finite: bit patterns only
+    vals = np.array([0x7FC0, 0x7F81, 0xFFC1, 0x7F80, 0xFF80, 0x0000, 0x8000,
+                     0x0001, 0x807F, 0x7F7F, 0xFF7F], np.uint16)
+    w = np.resize(vals, CH // 2 * 3)
+    state = w.view(np.uint8)
+    _, live = roundtrip(state)
+    assert np.array_equal(live, state)
+
+
+def test_constant_chunk_closed_form():
+    n = CH // 2
+    w = np.full(n, 0x3F80, np.uint16)  # 1.0 everywhere: one exponent, sm = 0
+    plan = oracle.plan_chunk(w.view(np.uint8))
+    assert plan == dict(mode=1, k=0, base=127, n_esc=0, size=16 + pad16(n))
+    payload, live = roundtrip(w.view(np.uint8))
+    assert np.array_equal(live, w.view(np.uint8))
+
+
+def test_random_bits_choose_raw():
+    rng = np.random.default_rng(11)
+    n = CH // 2
+    w = rng.integers(0, 65536, n, dtype=np.uint32).astype(np.uint16)
+    plan = oracle.plan_chunk(w.view(np.uint8))
+    assert plan["mode"] == 0 and plan["size"] == 16 + 2 * n
+    assert plan["k"] == 0 and plan["base"] == 0 and plan["n_esc"] == 0
+
+
+def brute_force_plan(words):
+    """Smallest record over every candidate; ties RAW < k=0 < k=1 < ... < 7,
+    and for a given k the smallest base.  Counts escapes word by word."""
+    n = len(words)
+    e = [(int(w) >> 7) & 255 for w in words]
+    best = (16 + pad16(2 * n), 0, 0, 0, 0)  # size, mode, k, base, n_esc
+    if len(set(e)) == 1:
+        s = 16 + pad16(n)
+        if s < best[0]:
+            best = (s, 1, 0, e[0], 0)
+    for k in range(1, 8):
+        width = (1 << k) - 1
+        kbest = None
+        for base in range(256):
+            esc = sum(1 for x in e if not (base <= x < base + width))
+            if kbest is None or esc < kbest[1]:
+                kbest = (base, esc)
+        base, esc = kbest
+        s = 16 + pad16((n * k + 7) // 8) + pad16(esc) + pad16(n)
+        if s < best[0]:
+            best = (s, 1, k, base, esc)
+    return dict(size=best[0], mode=best[1], k=best[2], base=best[3],
+                n_esc=best[4])
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_plan_matches_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 400))
+    kind = seed % 4
+    if kind == 0:  # normal-ish values, a few exponents
+        x = rng.standard_normal(n).astype(np.float32) * float(rng.uniform(0.01, 100))
+        w = (x.view(np.uint32) >> 16).astype(np.uint16)
+    elif kind == 1:  # exponents from a narrow random set
+        es = rng.integers(0, 256, int(rng.integers(1, 9)))
+        e = rng.choice(es, n)
+        w = ((rng.integers(0, 2, n) << 15) | (e << 7) |
+             rng.integers(0, 128, n)).astype(np.uint16)
+    elif kind == 2:  # random bits
+        w = rng.integers(0, 65536, n).astype(np.uint16)
+    else:  # near the top and bottom of the exponent range
+        e = rng.choice([0, 1, 2, 253, 254, 255], n)
+        w = ((e << 7) | rng.integers(0, 128, n)).astype(np.uint16)
+    assert oracle.plan_chunk(w.view(np.uint8)) == brute_force_plan(w)
+
+
+def test_hand_built_payload():
+    """Two 4 KiB chunks: chunk 0 constant 1.0 (PACK k=0), chunk 1 exponents
+    cycling base..base+2 with k=2.  Expected bytes are written out here from
+    the format text, CRCs from zlib."""
+    n = CH // 2
+    c0 = np.full(n, 0x3F80, np.uint16)
+    e1 = 120 + (np.arange(n) % 3)
+    sm1 = (np.arange(n) * 37) % 256
+    c1 = (((sm1 >> 7) << 15) | (e1 << 7) | (sm1 & 127)).astype(np.uint16)
+    state = np.concatenate([c0, c1]).view(np.uint8)
+
+    def rec(mode, k, base, n_esc, body):
+        h = struct.pack("<BBBBII", mode, k, base, 0, n, n_esc)
+        return h + struct.pack("<I", zlib.crc32(h)) + body
+
+    r0 = rec(1, 0, 127, 0, bytes(pad16(n)))  # sm plane of zeros
+    codes = bytearray(n * 2 // 8)
+    for i in range(n):
+        code = i % 3
+        for b in range(2):
+            if (code >> b) & 1:
+                j = i * 2 + b
+                codes[j // 8] |= 1 << (j % 8)
+    r1 = rec(1, 2, 120, 0, bytes(codes) + sm1.astype(np.uint8).tobytes())
+    table_end = 64 + 32
+    table = struct.pack("<IIQ", 0, zlib.crc32(c0.tobytes()), table_end)
+    table += struct.pack("<IIQ", 1, zlib.crc32(c1.tobytes()),
+                         table_end + len(r0))
+    total = table_end + len(r0) + len(r1)
+    head = b"WMV1" + struct.pack("<HBBIIQIIQII", 1, 0, 1, CH, 2, state.size,
+                                 2, 1, total, zlib.crc32(state.tobytes()),
+                                 zlib.crc32(table)) + bytes(12)
+    head += struct.pack("<I", zlib.crc32(head))
+    want = head + table + r0 + r1
+    got = oracle.encode(0, state, CH).tobytes()
+    assert len(got) == len(want) == total
+    assert got == want
+
+
+def test_escapes_and_partial_tail():
+    # 3 chunks + a short tail; a wide exponent spread forces escapes
+    rng = np.random.default_rng(21)
+    n = (3 * CH + 1234) // 2
+    x = (rng.standard_t(3, n) * 1e3).astype(np.float32)
+    w = (x.view(np.uint32) >> 16).astype(np.uint16)
+    state = w.view(np.uint8)
+    payload, live = roundtrip(state)
+    assert np.array_equal(live, state)
+    # some record used escapes
+    plans = [oracle.plan_chunk(state[i:i + CH]) for i in range(0, state.size, CH)]
+    assert any(p["n_esc"] > 0 for p in plans)
+
+
+def test_dirty_subset_payload_and_install():
+    rng = np.random.default_rng(5)
+    prev = rng.standard_normal(8 * CH // 2).astype(np.float32)
+    prev = (prev.view(np.uint32) >> 16).astype(np.uint16).view(np.uint8)
+    cur = prev.copy()
+    for c in (1, 4, 7):
+        cur[c * CH:(c + 1) * CH] = rng.integers(0, 256, CH, dtype=np.uint8)
+    idx = oracle.diff_dirty(cur, prev, CH)
+    assert idx.tolist() == [1, 4, 7]
+    payload = oracle.encode(0, cur, CH, idx)
+    v, staging, _ = oracle.decode_verify(0, payload, cur.size, CH,
+                                         staging_cap=3 * CH)
+    assert v == 0
+    live = prev.copy()
+    assert oracle.commit(live, CH, staging, payload, v) == 0
+    assert np.array_equal(live, cur)
+    # empty dirty set: header-only payload, nothing to install
+    payload = oracle.encode(0, cur, CH, np.zeros(0, np.uint32))
+    assert payload.size == 64
+    v, staging, _ = oracle.decode_verify(0, payload, cur.size, CH)
+    assert v == 0
+
+
+def test_empty_state():
+    state = np.zeros(0, np.uint8)
+    payload = oracle.encode(0, state, CH)
+    assert payload.size == 64
+    v, _, _ = oracle.decode_verify(0, payload, 0, CH)
+    assert v == 0
+
+
+def test_thread_count_does_not_change_bytes():
+    rng = np.random.default_rng(8)
+    x = rng.standard_normal(9 * CH // 2).astype(np.float32)
+    state = (x.view(np.uint32) >> 16).astype(np.uint16).view(np.uint8)
+    a = oracle.encode(0, state, CH, threads=1)
+    b = oracle.encode(0, state, CH, threads=4)
+    assert np.array_equal(a, b)
