@@ -18,8 +18,10 @@
  *    40 u32 global_crc (CRC of the whole source state)
  *    44 u32 table_crc  (CRC of the 16*n_records table bytes)
  *    48..59 zero                     60 u32 header_crc = CRC(bytes 0..59)
- *   table (16 B per record): u32 chunk_idx, u32 src_crc, u64 record_offset
- *   records, contiguous, in table order.  Record:
+ *   records, contiguous from offset 64, in ascending chunk order
+ *   table (16 B per record, after the last record, ending at payload_bytes):
+ *     u32 chunk_idx, u32 src_crc, u64 record_offset
+ *   Record:
  *     0 u8 mode (0 RAW, 1 PACK)  1 u8 k  2 u8 base  3 u8 0
  *     4 u32 n_words  8 u32 n_esc  12 u32 rec_crc = CRC(record bytes 0..11)
  *     RAW : the chunk's bytes
@@ -337,6 +339,7 @@ typedef struct {
   const uint32_t *idx; /* NULL: record r is chunk r */
   uint32_t *mode, *k, *base, *esc;
   uint64_t *size, *offset;
+  uint64_t table; /* byte offset of the table */
   uint8_t *payload;
 } en_ctx;
 
@@ -360,7 +363,7 @@ static void en_write_range(void *vp, uint64_t lo, uint64_t hi) {
     uint64_t c = en_chunk(x, r);
     const uint8_t *src = x->state + c * (uint64_t)x->chunk;
     uint32_t len = chunk_len(x->nbytes, x->chunk, c);
-    uint8_t *entry = x->payload + 64 + 16 * r;
+    uint8_t *entry = x->payload + x->table + 16 * r;
     put_u32(entry, (uint32_t)c);
     put_u32(entry + 4, orc_crc(x->kind, src, len));
     put_u64(entry + 8, x->offset[r]);
@@ -405,14 +408,16 @@ int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
   x.payload = payload;
 
   /* 1. plan every record; 2. record offsets are the exclusive prefix sum of
-   * record sizes after the table; 3. write table entries and records. */
+   * record sizes, starting right after the header; the table follows the
+   * last record; 3. write records and table entries. */
   parallel_for(n_rec, threads, en_plan_range, &x);
-  uint64_t at = 64 + 16 * n_rec;
+  uint64_t at = 64;
   for (uint64_t r = 0; r < n_rec; r++) {
     x.offset[r] = at;
     at += x.size[r];
   }
-  uint64_t total = at;
+  x.table = at;
+  uint64_t total = at + 16 * n_rec;
   memset(payload, 0, total);
   parallel_for(n_rec, threads, en_write_range, &x);
 
@@ -431,7 +436,7 @@ int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
   put_u32(h + 28, idx ? 0u : 1u);
   put_u64(h + 32, total);
   put_u32(h + 40, orc_crc(kind, state, nbytes));
-  put_u32(h + 44, orc_crc(kind, payload + 64, 16 * n_rec));
+  put_u32(h + 44, orc_crc(kind, payload + x.table, 16 * n_rec));
   put_u32(h + 60, orc_crc(kind, h, 60));
 
   free(x.mode);
@@ -516,7 +521,7 @@ static uint32_t decode_record(int kind, const uint8_t *rec, uint64_t L,
 typedef struct {
   int kind;
   const uint8_t *payload;
-  uint64_t payload_bytes, nbytes;
+  uint64_t table, nbytes;
   uint32_t chunk, n_rec;
   uint8_t *staging;
   uint32_t *status;
@@ -525,10 +530,10 @@ typedef struct {
 static void de_range(void *vp, uint64_t lo, uint64_t hi) {
   de_ctx *x = (de_ctx *)vp;
   for (uint64_t r = lo; r < hi; r++) {
-    const uint8_t *e = x->payload + 64 + 16 * r;
+    const uint8_t *e = x->payload + x->table + 16 * r;
     uint32_t c = get_u32(e);
     uint64_t off = get_u64(e + 8);
-    uint64_t end = r + 1 < x->n_rec ? get_u64(e + 16 + 8) : x->payload_bytes;
+    uint64_t end = r + 1 < x->n_rec ? get_u64(e + 16 + 8) : x->table;
     x->status[r] = decode_record(x->kind, x->payload + off, end - off,
                                  chunk_len(x->nbytes, x->chunk, c),
                                  get_u32(e + 4),
@@ -564,27 +569,27 @@ uint32_t orc_decode_verify(int kind, const uint8_t *payload, uint64_t cap,
   if ((flags & 1u) && n_rec != n_chunks) return ORC_V_HEADER;
   if ((uint64_t)n_rec * chunk_bytes > staging_cap) return ORC_V_STAGING;
 
-  /* table */
-  const uint8_t *t = payload + 64;
-  uint64_t table_end = 64 + 16 * (uint64_t)n_rec;
+  /* table: the last 16*n_records bytes of the payload */
+  uint64_t table = payload_bytes - 16 * (uint64_t)n_rec;
+  const uint8_t *t = payload + table;
   if (orc_crc(kind, t, 16 * (uint64_t)n_rec) != get_u32(h + 44))
     return ORC_V_TABLE;
-  if (n_rec == 0 && payload_bytes != table_end) return ORC_V_TABLE;
+  if (n_rec == 0 && payload_bytes != 64) return ORC_V_TABLE;
   for (uint32_t r = 0; r < n_rec; r++) {
     uint32_t c = get_u32(t + 16 * (uint64_t)r);
     uint64_t off = get_u64(t + 16 * (uint64_t)r + 8);
-    uint64_t end = r + 1 < n_rec ? get_u64(t + 16 * (uint64_t)(r + 1) + 8)
-                                 : payload_bytes;
+    uint64_t end =
+        r + 1 < n_rec ? get_u64(t + 16 * (uint64_t)(r + 1) + 8) : table;
     if (c >= n_chunks) return ORC_V_TABLE;
     if (r && c <= get_u32(t + 16 * (uint64_t)(r - 1))) return ORC_V_TABLE;
-    if (r == 0 && off != table_end) return ORC_V_TABLE;
+    if (r == 0 && off != 64) return ORC_V_TABLE;
     if (off % 16 || off >= end) return ORC_V_TABLE;
   }
 
   /* records */
   uint32_t *status = (uint32_t *)calloc(n_rec ? n_rec : 1, 4);
-  de_ctx x = {kind,   payload,    payload_bytes, nbytes, chunk_bytes,
-              n_rec,  staging,    status};
+  de_ctx x = {kind,  payload, table,   nbytes, chunk_bytes,
+              n_rec, staging, status};
   parallel_for(n_rec, threads, de_range, &x);
   uint32_t verdict = 0;
   for (uint32_t r = 0; r < n_rec; r++) {
@@ -600,8 +605,9 @@ int orc_commit(uint8_t *live, uint64_t nbytes, uint32_t chunk_bytes,
                uint32_t verdict) {
   if (verdict != 0) return 1;
   uint32_t n_rec = get_u32(payload + 24);
+  uint64_t table = get_u64(payload + 32) - 16 * (uint64_t)n_rec;
   for (uint32_t r = 0; r < n_rec; r++) {
-    uint32_t c = get_u32(payload + 64 + 16 * (uint64_t)r);
+    uint32_t c = get_u32(payload + table + 16 * (uint64_t)r);
     memcpy(live + (uint64_t)c * chunk_bytes,
            staging + (uint64_t)r * chunk_bytes,
            chunk_len(nbytes, chunk_bytes, c));

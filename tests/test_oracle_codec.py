@@ -131,8 +131,8 @@ def test_plan_matches_brute_force(seed):
 
 def test_hand_built_payload():
     """Two 4 KiB chunks: chunk 0 constant 1.0 (PACK k=0), chunk 1 exponents
-    cycling base..base+2 with k=2.  Expected bytes are written out here from
-    the format text, CRCs from zlib."""
+    cycling base..base+2 with k=2.  Expected bytes (header, records, then the
+    table) are written out here from the format text, CRCs from zlib."""
     n = CH // 2
     c0 = np.full(n, 0x3F80, np.uint16)
     e1 = 120 + (np.arange(n) % 3)
@@ -153,16 +153,14 @@ def test_hand_built_payload():
                 j = i * 2 + b
                 codes[j // 8] |= 1 << (j % 8)
     r1 = rec(1, 2, 120, 0, bytes(codes) + sm1.astype(np.uint8).tobytes())
-    table_end = 64 + 32
-    table = struct.pack("<IIQ", 0, zlib.crc32(c0.tobytes()), table_end)
-    table += struct.pack("<IIQ", 1, zlib.crc32(c1.tobytes()),
-                         table_end + len(r0))
-    total = table_end + len(r0) + len(r1)
+    table = struct.pack("<IIQ", 0, zlib.crc32(c0.tobytes()), 64)
+    table += struct.pack("<IIQ", 1, zlib.crc32(c1.tobytes()), 64 + len(r0))
+    total = 64 + len(r0) + len(r1) + len(table)
     head = b"WMV1" + struct.pack("<HBBIIQIIQII", 1, 0, 1, CH, 2, state.size,
                                  2, 1, total, zlib.crc32(state.tobytes()),
                                  zlib.crc32(table)) + bytes(12)
     head += struct.pack("<I", zlib.crc32(head))
-    want = head + table + r0 + r1
+    want = head + r0 + r1 + table
     got = oracle.encode(0, state, CH).tobytes()
     assert len(got) == len(want) == total
     assert got == want

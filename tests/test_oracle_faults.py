@@ -48,7 +48,8 @@ def test_flip_classes_set_expected_bits():
     state = small_state()
     payload = oracle.encode(0, state, CH)
     n_rec = 3
-    rec0 = 64 + 16 * n_rec
+    rec0 = 64
+    table = payload.size - 16 * n_rec
 
     def verdict_after_flip(pos):
         bad = payload.copy()
@@ -56,9 +57,9 @@ def test_flip_classes_set_expected_bits():
         return oracle.decode_verify(0, bad, state.size, CH)
 
     assert verdict_after_flip(5)[0] == oracle.V_HEADER
-    assert verdict_after_flip(64 + 3)[0] == oracle.V_TABLE
+    assert verdict_after_flip(table + 3)[0] == oracle.V_TABLE
     assert verdict_after_flip(rec0 + 1)[0] == oracle.V_RECORD  # record k field
-    v, _, st = verdict_after_flip(payload.size - 100)  # sm plane of record 2
+    v, _, st = verdict_after_flip(table - 100)  # sm plane of record 2
     assert v == oracle.V_DATA and st[:3].tolist() == [0, 0, oracle.V_DATA]
 
 
