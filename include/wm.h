@@ -1,0 +1,189 @@
+/*
+ * wm.h -- C ABI of libwm, the exact-state mover's device hot path on MI355X.
+ *
+ * The library implements, for a flat multi-gigabyte bf16 state (an attention
+ * KV cache) resident in device memory, the mover's data path from
+ * arXiv 2607.10389 ("Stateful Worlds, Stateless Elasticity"):
+ *
+ *   source side       wm_checksum_chunks -> wm_diff_dirty -> wm_encode
+ *                     (or the single-pass wm_encode_step)
+ *   destination side  wm_decode_verify -> wm_commit_or_abort
+ *
+ * under the paper's contract: the destination is bit-identical to the source
+ * or nothing is installed (§1; §4 "Sufficiency": commit only on a
+ * byte-identical fingerprint; Table 1: migrate stages into a shadow slot,
+ * commit re-verifies then swaps, rollback drops the staged copy).
+ *
+ * Conventions for every call:
+ *   - Buffer pointers are DEVICE pointers owned by the caller, unless a
+ *     comment says "host".  The library never allocates, frees or keeps a
+ *     pointer after returning.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Calls only enqueue work on it and return without waiting, except
+ *     wm_commit_or_abort, which waits for the stream.
+ *   - Argument errors are detected on the host before anything is enqueued;
+ *     the call then returns a negative status and writes nothing.
+ *   - Problems found on the device (a malformed or corrupted payload) are
+ *     never crashes: they become bits of the device verdict word.
+ *   - Calls on different streams must use different workspaces; calls that
+ *     share a workspace must be ordered (same stream).
+ *   - All functions are thread-safe.  The first call on a device uploads the
+ *     library's constant CRC tables to it (wm_init does this eagerly).
+ *   - The kernels support chunk_bytes == 65536 only; other values return
+ *     WM_ERR_UNSUPPORTED.
+ */
+#ifndef WM_H
+#define WM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t wm_status;
+#define WM_OK 0
+#define WM_VERIFY_FAILED 1       /* verdict: nothing was installed */
+#define WM_ERR_INVALID_ARG (-1)  /* null/misaligned pointer, bad size/param */
+#define WM_ERR_CAPACITY (-2)     /* payload_cap below wm_payload_bound() */
+#define WM_ERR_HIP (-3)          /* HIP runtime or launch failure */
+#define WM_ERR_WORKSPACE (-4)    /* ws_bytes below wm_workspace_bytes() */
+#define WM_ERR_UNSUPPORTED (-5)  /* valid but not implemented (chunk size) */
+
+#define WM_CRC32_ZLIB 0 /* reflected 0xEDB88320, init/xorout 0xFFFFFFFF */
+#define WM_CRC32C 1     /* reflected 0x82F63B78, init/xorout 0xFFFFFFFF */
+#define WM_CODEC_EXPFOR 1
+
+/* Bits of the device verdict word written by wm_decode_verify. */
+#define WM_V_HEADER 1u  /* header rejected; nothing else examined */
+#define WM_V_TABLE 2u   /* record table rejected; records not examined */
+#define WM_V_RECORD 4u  /* some record's structure is invalid */
+#define WM_V_DATA 8u    /* some decoded chunk's CRC differs from its receipt */
+#define WM_V_STAGING 16u /* staging_cap too small for the payload's records */
+
+/* wm_commit_or_abort modes */
+#define WM_COMMIT_NONE 0    /* only read the verdict (full ship: caller swaps) */
+#define WM_COMMIT_SCATTER 1 /* copy each staged record into its chunk of live */
+
+typedef struct wm_params {
+  uint32_t chunk_bytes; /* bytes per chunk; 65536 */
+  uint32_t crc_kind;    /* WM_CRC32_ZLIB or WM_CRC32C */
+  uint32_t codec;       /* WM_CODEC_EXPFOR */
+  uint32_t flags;       /* must be 0 */
+} wm_params;
+
+/* Human-readable name of a status code (static string; never NULL). */
+const char *wm_status_str(wm_status s);
+
+/* Upload the constant tables to `device` (the current HIP device if < 0).
+ * Optional: every other call does it on first use. */
+wm_status wm_init(int device);
+
+/* Bytes of device workspace needed by wm_diff_dirty, wm_encode,
+ * wm_encode_step and wm_decode_verify for a state of nbytes.  0 if p is
+ * invalid. */
+uint64_t wm_workspace_bytes(uint64_t nbytes, const wm_params *p);
+
+/* Largest payload that n_records records of a state of nbytes can produce
+ * (header + every record RAW + table).  0 if p is invalid. */
+uint64_t wm_payload_bound(uint64_t nbytes, uint32_t n_records,
+                          const wm_params *p);
+
+/* Per-chunk CRC of the flat state (§4 "Sufficiency"; §6.5: zlib's CRC per
+ * chunk, chunk CRCs GF(2)-combined into one global CRC).
+ *   data       : nbytes of state, 16-byte aligned; any nbytes (last chunk
+ *                may be short)
+ *   crc_out    : ceil(nbytes / chunk_bytes) u32, CRC of each chunk
+ *   global_crc : 1 u32, CRC of the whole state, or NULL
+ * No workspace.  Errors: WM_ERR_INVALID_ARG, WM_ERR_UNSUPPORTED, WM_ERR_HIP. */
+wm_status wm_checksum_chunks(const void *data, uint64_t nbytes,
+                             const wm_params *p, uint32_t *crc_out,
+                             uint32_t *global_crc, void *stream);
+
+/* Dirty chunks: those whose bytes differ between cur and prev (the last
+ * shipped snapshot; §6.2 Exhibit 2 and App. H, iterative pre-copy).  A chunk
+ * rewritten with identical bytes is clean.
+ *   cur, prev  : nbytes each, 16-byte aligned
+ *   dirty_idx  : ceil(nbytes / chunk_bytes) u32; receives the dirty chunk
+ *                indices in ascending order
+ *   n_dirty    : 1 u32, the number of dirty chunks
+ *   ws         : workspace of ws_bytes >= wm_workspace_bytes() */
+wm_status wm_diff_dirty(const void *cur, const void *prev, uint64_t nbytes,
+                        const wm_params *p, uint32_t *dirty_idx,
+                        uint32_t *n_dirty, void *ws, uint64_t ws_bytes,
+                        void *stream);
+
+/* Encode chunks of the state into a payload (format v1: 64-byte header,
+ * records from offset 64 in ascending chunk order, then the record table;
+ * each record RAW or exponent-window PACK, whichever is smaller; §6.4: a
+ * lossless codec whose receipts bind to the decoded bytes).
+ *   state      : nbytes (even), 16-byte aligned
+ *   idx, n_idx : device list of *n_idx ascending chunk indices to encode, or
+ *                both NULL to encode every chunk (sets the FULL flag)
+ *   crc        : ceil(nbytes/chunk_bytes) u32 chunk CRCs from
+ *                wm_checksum_chunks (used as receipts and for the header's
+ *                global CRC), or NULL to compute them in the same pass; NULL
+ *                is only allowed when idx is NULL
+ *   payload    : payload_cap bytes, 16-byte aligned; payload_cap must be at
+ *                least wm_payload_bound(nbytes, n_chunks, p)
+ *   payload_bytes : 1 u64, the payload size written
+ * Errors: WM_ERR_INVALID_ARG, WM_ERR_CAPACITY, WM_ERR_WORKSPACE,
+ *         WM_ERR_UNSUPPORTED, WM_ERR_HIP. */
+wm_status wm_encode(const void *state, uint64_t nbytes, const wm_params *p,
+                    const uint32_t *idx, const uint32_t *n_idx,
+                    const uint32_t *crc, void *payload, uint64_t payload_cap,
+                    uint64_t *payload_bytes, void *ws, uint64_t ws_bytes,
+                    void *stream);
+
+/* Single pass over cur (and prev) with outputs byte-identical to
+ * wm_checksum_chunks(cur) + wm_diff_dirty(cur, prev) + wm_encode(cur, dirty
+ * list, crc).  prev == NULL ships every chunk (outputs identical to
+ * wm_checksum_chunks + wm_encode(cur, NULL, NULL, crc); dirty_idx then lists
+ * every chunk).
+ *   crc_out    : n_chunks u32, or NULL
+ *   global_crc : 1 u32, or NULL
+ *   dirty_idx  : n_chunks u32, or NULL;  n_dirty : 1 u32, or NULL
+ * Other arguments as wm_encode. */
+wm_status wm_encode_step(const void *cur, const void *prev, uint64_t nbytes,
+                         const wm_params *p, uint32_t *crc_out,
+                         uint32_t *global_crc, uint32_t *dirty_idx,
+                         uint32_t *n_dirty, void *payload, uint64_t payload_cap,
+                         uint64_t *payload_bytes, void *ws, uint64_t ws_bytes,
+                         void *stream);
+
+/* Validate and decode a payload into staging, re-checksumming every decoded
+ * chunk against its receipt (§6.4: decode sits inside the verified
+ * envelope; Table 1: verify).  Reads never leave [payload, payload +
+ * payload_cap).
+ *   nbytes     : the receiver's state size (must match the header)
+ *   staging    : staging_cap bytes, 16-byte aligned; record i is decoded to
+ *                staging + i*chunk_bytes (a full ship's staging is therefore
+ *                the shadow copy of the state)
+ *   verdict    : 1 u32, 0 when every check passed, else WM_V_* bits
+ *   rec_status : n_chunks u32 (0, WM_V_RECORD or WM_V_DATA per record when
+ *                header and table are valid), or NULL
+ * After a nonzero verdict the staging contents are unspecified. */
+wm_status wm_decode_verify(const void *payload, uint64_t payload_cap,
+                           uint64_t nbytes, const wm_params *p, void *staging,
+                           uint64_t staging_cap, uint32_t *verdict,
+                           uint32_t *rec_status, void *ws, uint64_t ws_bytes,
+                           void *stream);
+
+/* Install or abort (Table 1: commit / rollback).  Enqueues, for
+ * WM_COMMIT_SCATTER, a copy of each staged record into live that runs only
+ * if *verdict == 0 on the device, then waits for the stream and returns
+ * WM_OK (installed) or WM_VERIFY_FAILED (live untouched).  WM_COMMIT_NONE
+ * copies nothing (a full ship's caller then swaps the staging buffer in).
+ *   live     : nbytes, 16-byte aligned (SCATTER only)
+ *   staging, payload : as passed to wm_decode_verify (SCATTER only)
+ *   verdict  : the device verdict word from wm_decode_verify */
+wm_status wm_commit_or_abort(void *live, uint64_t nbytes, const wm_params *p,
+                             const void *staging, const void *payload,
+                             const uint32_t *verdict, uint32_t mode,
+                             void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WM_H */

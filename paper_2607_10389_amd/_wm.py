@@ -1,0 +1,187 @@
+"""ctypes binding of libwm (include/wm.h).
+
+Argument marshalling only: every step of the hot path runs in the HIP
+kernels of libwm.so.  Tensors are torch CUDA (HIP) tensors; the binding
+passes their device pointers, sizes and the current stream's handle.  There
+is no CPU fallback: if libwm.so is missing or cannot load, importing this
+module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libwm.so")
+
+WM_OK = 0
+WM_VERIFY_FAILED = 1
+WM_ERR_INVALID_ARG = -1
+WM_ERR_CAPACITY = -2
+WM_ERR_HIP = -3
+WM_ERR_WORKSPACE = -4
+WM_ERR_UNSUPPORTED = -5
+
+WM_CRC32_ZLIB = 0
+WM_CRC32C = 1
+WM_CODEC_EXPFOR = 1
+
+V_HEADER, V_TABLE, V_RECORD, V_DATA, V_STAGING = 1, 2, 4, 8, 16
+
+WM_COMMIT_NONE = 0
+WM_COMMIT_SCATTER = 1
+
+CHUNK = 65536
+
+# every symbol declared in include/wm.h
+EXPORTS = (
+    "wm_status_str", "wm_init", "wm_workspace_bytes", "wm_payload_bound",
+    "wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_encode_step",
+    "wm_decode_verify", "wm_commit_or_abort",
+)
+
+
+class WmError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_str(status)} ({status})")
+        self.status = status
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("chunk_bytes", ctypes.c_uint32), ("crc_kind", ctypes.c_uint32),
+                ("codec", ctypes.c_uint32), ("flags", ctypes.c_uint32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing; build it with "
+            "`python -m paper_2607_10389_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, u64, u32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32
+    pp = ctypes.POINTER(Params)
+    sig = {
+        "wm_status_str": ([ctypes.c_int32], ctypes.c_char_p),
+        "wm_init": ([ctypes.c_int], ctypes.c_int32),
+        "wm_workspace_bytes": ([u64, pp], u64),
+        "wm_payload_bound": ([u64, u32, pp], u64),
+        "wm_checksum_chunks": ([vp, u64, pp, vp, vp, vp], ctypes.c_int32),
+        "wm_diff_dirty": ([vp, vp, u64, pp, vp, vp, vp, u64, vp], ctypes.c_int32),
+        "wm_encode": ([vp, u64, pp, vp, vp, vp, vp, u64, vp, vp, u64, vp],
+                      ctypes.c_int32),
+        "wm_encode_step": ([vp, vp, u64, pp, vp, vp, vp, vp, vp, u64, vp, vp,
+                            u64, vp], ctypes.c_int32),
+        "wm_decode_verify": ([vp, u64, u64, pp, vp, u64, vp, vp, vp, u64, vp],
+                             ctypes.c_int32),
+        "wm_commit_or_abort": ([vp, u64, pp, vp, vp, vp, u32, vp],
+                               ctypes.c_int32),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+LIB = _load()
+
+
+def status_str(s: int) -> str:
+    return LIB.wm_status_str(s).decode()
+
+
+def params(crc_kind: int = WM_CRC32_ZLIB, chunk_bytes: int = CHUNK) -> Params:
+    return Params(chunk_bytes, crc_kind, WM_CODEC_EXPFOR, 0)
+
+
+def _p(t):
+    """Device pointer of a tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("libwm takes device tensors")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(status: int, where: str) -> int:
+    if status < 0:
+        raise WmError(status, where)
+    return status
+
+
+def n_chunks(nbytes: int, chunk: int = CHUNK) -> int:
+    return (nbytes + chunk - 1) // chunk
+
+
+def workspace_bytes(nbytes: int, p: Params | None = None) -> int:
+    p = p or params()
+    return int(LIB.wm_workspace_bytes(nbytes, ctypes.byref(p)))
+
+
+def payload_bound(nbytes: int, n_records: int, p: Params | None = None) -> int:
+    p = p or params()
+    return int(LIB.wm_payload_bound(nbytes, n_records, ctypes.byref(p)))
+
+
+def init(device: int = -1) -> None:
+    _check(LIB.wm_init(device), "wm_init")
+
+
+def checksum_chunks(data, nbytes, p, crc_out, global_crc=None, stream=None):
+    return _check(LIB.wm_checksum_chunks(_p(data), nbytes, ctypes.byref(p),
+                                         _p(crc_out), _p(global_crc),
+                                         _stream(stream)), "wm_checksum_chunks")
+
+
+def diff_dirty(cur, prev, nbytes, p, dirty_idx, n_dirty, ws, stream=None):
+    return _check(LIB.wm_diff_dirty(_p(cur), _p(prev), nbytes, ctypes.byref(p),
+                                    _p(dirty_idx), _p(n_dirty), _p(ws),
+                                    _nbytes(ws), _stream(stream)),
+                  "wm_diff_dirty")
+
+
+def encode(state, nbytes, p, idx, n_idx, crc, payload, payload_bytes, ws,
+           stream=None):
+    return _check(LIB.wm_encode(_p(state), nbytes, ctypes.byref(p), _p(idx),
+                                _p(n_idx), _p(crc), _p(payload),
+                                _nbytes(payload), _p(payload_bytes), _p(ws),
+                                _nbytes(ws), _stream(stream)), "wm_encode")
+
+
+def encode_step(cur, prev, nbytes, p, crc_out, global_crc, dirty_idx, n_dirty,
+                payload, payload_bytes, ws, stream=None):
+    return _check(LIB.wm_encode_step(_p(cur), _p(prev), nbytes, ctypes.byref(p),
+                                     _p(crc_out), _p(global_crc),
+                                     _p(dirty_idx), _p(n_dirty), _p(payload),
+                                     _nbytes(payload), _p(payload_bytes),
+                                     _p(ws), _nbytes(ws), _stream(stream)),
+                  "wm_encode_step")
+
+
+def decode_verify(payload, payload_cap, nbytes, p, staging, verdict,
+                  rec_status, ws, stream=None):
+    return _check(LIB.wm_decode_verify(_p(payload), payload_cap, nbytes,
+                                       ctypes.byref(p), _p(staging),
+                                       _nbytes(staging) if staging is not None
+                                       else 0, _p(verdict), _p(rec_status),
+                                       _p(ws), _nbytes(ws), _stream(stream)),
+                  "wm_decode_verify")
+
+
+def commit_or_abort(live, nbytes, p, staging, payload, verdict, mode,
+                    stream=None) -> int:
+    return _check(LIB.wm_commit_or_abort(_p(live), nbytes, ctypes.byref(p),
+                                         _p(staging), _p(payload), _p(verdict),
+                                         mode, _stream(stream)),
+                  "wm_commit_or_abort")

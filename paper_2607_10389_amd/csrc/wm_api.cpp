@@ -1,0 +1,258 @@
+// wm_api.cpp -- the C ABI of libwm (declared in include/wm.h).
+//
+// Host side only: argument validation (before anything is enqueued),
+// per-call geometry, workspace layout, and the launches.  Constant CRC tables
+// are built once on the host and uploaded once per device.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <map>
+#include <mutex>
+
+#include "wm.h"
+#include "wm_internal.h"
+
+using namespace wm;
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+struct DeviceState {
+  bool ready = false;
+  int n_cu = 0;
+};
+
+std::mutex g_mu;
+DeviceState g_dev[kMaxDevices];
+CrcTables g_tables_host[2];
+bool g_tables_built = false;
+
+struct TailGeom {
+  uint32_t k_tail;
+  uint32_t mat[32];
+};
+std::map<uint64_t, TailGeom> g_tail_cache;
+
+wm_status ensure_device(int *n_cu) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return WM_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_mu);
+  if (!g_tables_built) {
+    build_crc_tables(poly_of(0), &g_tables_host[0]);
+    build_crc_tables(poly_of(1), &g_tables_host[1]);
+    g_tables_built = true;
+  }
+  DeviceState &st = g_dev[dev];
+  if (!st.ready) {
+    if (upload_tables(dev, g_tables_host) != 0) return WM_ERR_HIP;
+    if (set_kernel_attributes() != 0) return WM_ERR_HIP;
+    int cu = 0;
+    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cu <= 0)
+      return WM_ERR_HIP;
+    st.n_cu = cu;
+    st.ready = true;
+  }
+  *n_cu = st.n_cu;
+  return WM_OK;
+}
+
+wm_status check_params(const wm_params *p) {
+  if (!p) return WM_ERR_INVALID_ARG;
+  if (p->crc_kind > 1 || p->codec != WM_CODEC_EXPFOR || p->flags != 0) return WM_ERR_INVALID_ARG;
+  uint32_t c = p->chunk_bytes;
+  bool pow2 = c >= 4096u && c <= (16u << 20) && (c & (c - 1)) == 0;
+  if (!pow2) return WM_ERR_INVALID_ARG;
+  if (c != kChunk) return WM_ERR_UNSUPPORTED;
+  return WM_OK;
+}
+
+wm_status make_geom(uint64_t nbytes, const wm_params *p, ChunkGeom *g) {
+  wm_status s = check_params(p);
+  if (s != WM_OK) return s;
+  uint64_t n = (nbytes + kChunk - 1) / kChunk;
+  if (n >= (1ull << 24)) return WM_ERR_INVALID_ARG;  // look-back field width
+  g->nbytes = nbytes;
+  g->n_chunks = (uint32_t)n;
+  g->tail_len = n ? (uint32_t)(nbytes - (n - 1) * kChunk) : kChunk;
+  g->crc_kind = p->crc_kind;
+  g->k_tail = 0;
+  for (int i = 0; i < 32; ++i) g->tail_mat[i] = 1u << i;
+  if (g->tail_len != kChunk) {
+    uint64_t key = ((uint64_t)p->crc_kind << 32) | g->tail_len;
+    std::lock_guard<std::mutex> lock(g_mu);
+    auto it = g_tail_cache.find(key);
+    if (it == g_tail_cache.end()) {
+      uint32_t poly = poly_of(p->crc_kind);
+      TailGeom t;
+      t.k_tail = shift_apply(poly, g->tail_len, 0xFFFFFFFFu) ^ 0xFFFFFFFFu;
+      shift_matrix(poly, -(int64_t)(kChunk - g->tail_len), t.mat);
+      it = g_tail_cache.emplace(key, t).first;
+    }
+    g->k_tail = it->second.k_tail;
+    for (int i = 0; i < 32; ++i) g->tail_mat[i] = it->second.mat[i];
+  }
+  return WM_OK;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+wm_status hip_status(int e) { return e == 0 ? WM_OK : WM_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char *wm_status_str(wm_status s) {
+  switch (s) {
+    case WM_OK: return "WM_OK";
+    case WM_VERIFY_FAILED: return "WM_VERIFY_FAILED";
+    case WM_ERR_INVALID_ARG: return "WM_ERR_INVALID_ARG";
+    case WM_ERR_CAPACITY: return "WM_ERR_CAPACITY";
+    case WM_ERR_HIP: return "WM_ERR_HIP";
+    case WM_ERR_WORKSPACE: return "WM_ERR_WORKSPACE";
+    case WM_ERR_UNSUPPORTED: return "WM_ERR_UNSUPPORTED";
+    default: return "WM_UNKNOWN_STATUS";
+  }
+}
+
+wm_status wm_init(int device) {
+  if (device >= 0 && hipSetDevice(device) != hipSuccess) return WM_ERR_HIP;
+  int n_cu = 0;
+  return ensure_device(&n_cu);
+}
+
+uint64_t wm_workspace_bytes(uint64_t nbytes, const wm_params *p) {
+  ChunkGeom g;
+  if (check_params(p) != WM_OK) return 0;
+  uint64_t n = (nbytes + p->chunk_bytes - 1) / p->chunk_bytes;
+  if (n >= (1ull << 24)) return 0;
+  (void)g;
+  return ws_layout((uint32_t)n).total;
+}
+
+uint64_t wm_payload_bound(uint64_t nbytes, uint32_t n_records, const wm_params *p) {
+  (void)nbytes;
+  if (check_params(p) != WM_OK) return 0;
+  return 64u + 16ull * n_records + (uint64_t)n_records * (16u + p->chunk_bytes);
+}
+
+wm_status wm_checksum_chunks(const void *data, uint64_t nbytes, const wm_params *p,
+                             uint32_t *crc_out, uint32_t *global_crc, void *stream) {
+  ChunkGeom g;
+  wm_status s = make_geom(nbytes, p, &g);
+  if (s != WM_OK) return s;
+  if ((nbytes && (!data || !crc_out)) || !aligned16(data)) return WM_ERR_INVALID_ARG;
+  if (!nbytes && !global_crc) return WM_OK;
+  if (!crc_out && global_crc) return WM_ERR_INVALID_ARG;
+  int n_cu = 0;
+  if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  return hip_status(launch_checksum(data, g, crc_out, global_crc, n_cu, stream));
+}
+
+wm_status wm_diff_dirty(const void *cur, const void *prev, uint64_t nbytes, const wm_params *p,
+                        uint32_t *dirty_idx, uint32_t *n_dirty, void *ws, uint64_t ws_bytes,
+                        void *stream) {
+  ChunkGeom g;
+  wm_status s = make_geom(nbytes, p, &g);
+  if (s != WM_OK) return s;
+  if (!n_dirty || (nbytes && (!cur || !prev || !dirty_idx))) return WM_ERR_INVALID_ARG;
+  if (!aligned16(cur) || !aligned16(prev)) return WM_ERR_INVALID_ARG;
+  WsLayout L = ws_layout(g.n_chunks);
+  if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
+  int n_cu = 0;
+  if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  return hip_status(launch_diff(cur, prev, g, dirty_idx, n_dirty, ws, L, stream));
+}
+
+wm_status wm_encode(const void *state, uint64_t nbytes, const wm_params *p, const uint32_t *idx,
+                    const uint32_t *n_idx, const uint32_t *crc, void *payload,
+                    uint64_t payload_cap, uint64_t *payload_bytes, void *ws, uint64_t ws_bytes,
+                    void *stream) {
+  ChunkGeom g;
+  wm_status s = make_geom(nbytes, p, &g);
+  if (s != WM_OK) return s;
+  if (nbytes & 1u) return WM_ERR_INVALID_ARG;
+  if ((nbytes && !state) || !aligned16(state)) return WM_ERR_INVALID_ARG;
+  if ((idx == nullptr) != (n_idx == nullptr)) return WM_ERR_INVALID_ARG;
+  if (idx && !crc) return WM_ERR_INVALID_ARG;
+  if (!payload || !payload_bytes || !aligned16(payload)) return WM_ERR_INVALID_ARG;
+  if (payload_cap < wm_payload_bound(nbytes, g.n_chunks, p)) return WM_ERR_CAPACITY;
+  WsLayout L = ws_layout(g.n_chunks);
+  if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
+  int n_cu = 0;
+  if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  uint32_t *crc_scratch =
+      crc ? nullptr : reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + L.flags);
+  int mode = idx ? 0 : 1;
+  return hip_status(launch_encode(mode, state, nullptr, g, idx, n_idx, crc, crc_scratch, nullptr,
+                                  nullptr, nullptr, payload, payload_bytes, ws, L, n_cu, stream));
+}
+
+wm_status wm_encode_step(const void *cur, const void *prev, uint64_t nbytes, const wm_params *p,
+                         uint32_t *crc_out, uint32_t *global_crc, uint32_t *dirty_idx,
+                         uint32_t *n_dirty, void *payload, uint64_t payload_cap,
+                         uint64_t *payload_bytes, void *ws, uint64_t ws_bytes, void *stream) {
+  ChunkGeom g;
+  wm_status s = make_geom(nbytes, p, &g);
+  if (s != WM_OK) return s;
+  if (nbytes & 1u) return WM_ERR_INVALID_ARG;
+  if ((nbytes && !cur) || !aligned16(cur) || !aligned16(prev)) return WM_ERR_INVALID_ARG;
+  if (!payload || !payload_bytes || !aligned16(payload)) return WM_ERR_INVALID_ARG;
+  if (payload_cap < wm_payload_bound(nbytes, g.n_chunks, p)) return WM_ERR_CAPACITY;
+  WsLayout L = ws_layout(g.n_chunks);
+  if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
+  int n_cu = 0;
+  if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  uint32_t *crcs =
+      crc_out ? crc_out : reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + L.flags);
+  return hip_status(launch_encode(2, cur, prev, g, nullptr, nullptr, nullptr, crcs, global_crc,
+                                  dirty_idx, n_dirty, payload, payload_bytes, ws, L, n_cu,
+                                  stream));
+}
+
+wm_status wm_decode_verify(const void *payload, uint64_t payload_cap, uint64_t nbytes,
+                           const wm_params *p, void *staging, uint64_t staging_cap,
+                           uint32_t *verdict, uint32_t *rec_status, void *ws, uint64_t ws_bytes,
+                           void *stream) {
+  ChunkGeom g;
+  wm_status s = make_geom(nbytes, p, &g);
+  if (s != WM_OK) return s;
+  if (nbytes & 1u) return WM_ERR_INVALID_ARG;
+  if (!payload || !verdict || !aligned16(payload)) return WM_ERR_INVALID_ARG;
+  if ((staging_cap && !staging) || !aligned16(staging)) return WM_ERR_INVALID_ARG;
+  WsLayout L = ws_layout(g.n_chunks);
+  if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
+  int n_cu = 0;
+  if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  return hip_status(launch_decode(payload, payload_cap, g, staging, staging_cap, verdict,
+                                  rec_status, ws, L, n_cu, stream));
+}
+
+wm_status wm_commit_or_abort(void *live, uint64_t nbytes, const wm_params *p, const void *staging,
+                             const void *payload, const uint32_t *verdict, uint32_t mode,
+                             void *stream) {
+  ChunkGeom g;
+  wm_status s = make_geom(nbytes, p, &g);
+  if (s != WM_OK) return s;
+  if (!verdict || mode > WM_COMMIT_SCATTER) return WM_ERR_INVALID_ARG;
+  if (mode == WM_COMMIT_SCATTER) {
+    if ((nbytes && (!live || !staging || !payload)) || !aligned16(live) || !aligned16(staging) ||
+        !aligned16(payload))
+      return WM_ERR_INVALID_ARG;
+  }
+  int n_cu = 0;
+  if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (mode == WM_COMMIT_SCATTER) {
+    if (launch_commit(live, g, staging, payload, verdict, n_cu, stream) != 0) return WM_ERR_HIP;
+  }
+  uint32_t v = 0xFFFFFFFFu;
+  if (hipMemcpyAsync(&v, verdict, sizeof(v), hipMemcpyDeviceToHost, st) != hipSuccess)
+    return WM_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return WM_ERR_HIP;
+  return v == 0 ? WM_OK : WM_VERIFY_FAILED;
+}
+
+}  // extern "C"

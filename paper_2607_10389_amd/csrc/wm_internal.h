@@ -1,0 +1,108 @@
+// wm_internal.h -- shared constants and launch interfaces of libwm.
+//
+// CRC arithmetic used throughout.  For a reflected CRC with polynomial P the
+// register update after one message bit is Z(c) = (c >> 1) ^ (P & -(c & 1)),
+// a linear map over GF(2).  F^m denotes m zero bytes (8m applications of Z).
+// Feeding four message bytes d (little-endian word) into register c gives
+// F^4(c ^ d).  With R(M) the register after M from a zero register, the
+// standard CRC with init = xorout = 0xFFFFFFFF is
+//     CRC(M) = R(M) ^ F^|M|(0xFFFFFFFF) ^ 0xFFFFFFFF,
+// and CRC(A|B) = F^|B|(CRC(A)) ^ CRC(B) (how chunk CRCs combine, §6.5).
+// A linear map is stored either as four byte tables (tab[j][b] = M(b << 8j))
+// or as its 32 columns (col[i] = M(1 << i)).
+#pragma once
+#include <cstdint>
+
+namespace wm {
+
+constexpr uint32_t kChunk = 65536;  // bytes per chunk the kernels process
+constexpr int kWaves = 8;           // waves per workgroup
+constexpr int kThreads = kWaves * 64;
+constexpr uint32_t kRow = 1024;             // bytes per wave row: 64 lanes x 16 B
+constexpr uint32_t kSub = kChunk / kWaves;  // bytes of a chunk per wave
+constexpr int kRows = kSub / kRow;          // rows per lane
+constexpr int kTree = 6;                    // log2(64) lanes
+
+// Constant tables for one CRC kind (built on the host, uploaded once).
+struct CrcTables {
+  uint32_t row[4][256];          // F^kRow   (column-stream step, hot)
+  uint32_t f4[4][256];           // F^4      (standard 4-byte step)
+  uint32_t f8[4][256];           // F^8
+  uint32_t tree[kTree][4][256];  // F^(16 << l): lane-tree levels
+  uint32_t byte1[256];           // one-byte step of the table method
+  uint32_t wave_mat[kWaves][32]; // F^(kSub*(kWaves-1-w) + 4 - kRow), columns
+  uint32_t pow2[48][32];         // F^(2^i) bytes, columns
+  uint32_t k_full;               // F^kChunk(~0) ^ ~0
+  uint32_t pad_[3];
+};
+
+// Host-side table construction (wm_tables.cpp).
+void build_crc_tables(uint32_t poly, CrcTables *t);
+// Columns of F^m (m may be negative: the inverse shift).
+void shift_matrix(uint32_t poly, int64_t m, uint32_t cols[32]);
+// F^m applied to v.
+uint32_t shift_apply(uint32_t poly, int64_t m, uint32_t v);
+uint32_t poly_of(uint32_t crc_kind);
+
+// Per-call parameters passed by value to every kernel.
+struct ChunkGeom {
+  uint64_t nbytes;      // state bytes
+  uint32_t n_chunks;    // ceil(nbytes / kChunk)
+  uint32_t tail_len;    // length of the last chunk (kChunk if full)
+  uint32_t crc_kind;
+  uint32_t k_tail;      // F^tail_len(~0) ^ ~0
+  uint32_t tail_mat[32];// F^-(kChunk - tail_len), columns
+};
+
+// Workspace layout (bytes from the workspace base).
+struct WsLayout {
+  uint64_t ctl;        // 256 B of counters and flags
+  uint64_t status;     // n_chunks x u64 look-back words
+  uint64_t table;      // n_chunks x 16 B staged table entries
+  uint64_t entry_crc;  // n_chunks x u32 CRC of each table entry
+  uint64_t flags;      // n_chunks x u32 (diff flags / record bits)
+  uint64_t total;
+};
+WsLayout ws_layout(uint32_t n_chunks);
+
+// Control block at the start of the workspace.
+struct WsCtl {
+  uint32_t ticket;       // dynamic work counter
+  uint32_t error;        // encode: 1 = look-back gave up, 2 = bad chunk index
+  uint32_t hdr_ok;       // decode: header passed
+  uint32_t table_bad;    // decode: a table-local rule failed
+  uint32_t rec_bits;     // decode: OR of record status bits
+  uint32_t n_rec;        // decode: records in the payload
+  uint64_t payload_bytes;// decode: from the header
+  uint64_t table_off;    // decode: table start
+  uint32_t table_crc;    // decode: expected table CRC
+  uint32_t verdict_pre;  // decode: header/staging verdict
+  uint32_t pad_[52];
+};
+static_assert(sizeof(WsCtl) == 256, "control block is 256 bytes");
+
+// Kernel launchers (wm_kernels.hip).  All return a hipError_t as int.
+int upload_tables(int device, const CrcTables tabs[2]);
+int launch_checksum(const void *data, const ChunkGeom &g, uint32_t *crc_out,
+                    uint32_t *global_crc, int n_cu, void *stream);
+int launch_diff(const void *cur, const void *prev, const ChunkGeom &g,
+                uint32_t *dirty_idx, uint32_t *n_dirty, void *ws,
+                const WsLayout &L, void *stream);
+// mode: 0 = list (idx/n_idx), 1 = all chunks, 2 = step (prev may be NULL)
+int launch_encode(int mode, const void *cur, const void *prev,
+                  const ChunkGeom &g, const uint32_t *idx,
+                  const uint32_t *n_idx, const uint32_t *crc_in,
+                  uint32_t *crc_out, uint32_t *global_crc,
+                  uint32_t *dirty_idx, uint32_t *n_dirty, void *payload,
+                  uint64_t *payload_bytes, void *ws, const WsLayout &L,
+                  int n_cu, void *stream);
+int launch_decode(const void *payload, uint64_t payload_cap,
+                  const ChunkGeom &g, void *staging, uint64_t staging_cap,
+                  uint32_t *verdict, uint32_t *rec_status, void *ws,
+                  const WsLayout &L, int n_cu, void *stream);
+int launch_commit(void *live, const ChunkGeom &g, const void *staging,
+                  const void *payload, const uint32_t *verdict, int n_cu,
+                  void *stream);
+int set_kernel_attributes();
+
+}  // namespace wm

@@ -1,0 +1,221 @@
+"""GPU parity: every libwm output equals the oracle's, bit for bit.
+
+Runs through the C ABI (ctypes) on device buffers; the oracle runs on host
+copies of the same bytes.  Checksums, dirty lists, payload bytes, decoded
+bytes and verdicts are compared exactly (integer work: tolerance 0).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import wm_inputs
+
+pytestmark = pytest.mark.gpu
+
+CH = 65536
+
+
+@pytest.fixture(scope="module")
+def wm():
+    from paper_2607_10389_amd import _wm
+    _wm.init(-1)
+    return _wm
+
+
+def mover(nbytes, kind=0, **kw):
+    from paper_2607_10389_amd import Mover
+    return Mover(nbytes, kind, **kw)
+
+
+from gpu_helpers import (ORACLE_THREADS, check_full_ship, host_bytes,  # noqa: E402
+                         random_bytes, say, u32)
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+def test_tiny_checksum(wm, kind):
+    state = wm_inputs.make_cache(wm_inputs.TINY, "cuda")
+    m = mover(state.numel() * 2, kind)
+    m.checksum(state)
+    torch.cuda.synchronize()
+    crcs, g = oracle.checksum_chunks(kind, host_bytes(state), CH)
+    assert np.array_equal(m.crc_host(), crcs)
+    assert int(u32(m.global_crc)[0]) == g
+
+
+@pytest.mark.parametrize("n", [1, 15, 16, 17, 4095, 65535, 65536, 65537,
+                               2 * CH + 5536, 5 * CH + 1, 7 * CH - 2])
+def test_ragged_checksum(wm, n):
+    say(f"[ragged checksum] n={n}")
+    data = random_bytes(n, seed=n)
+    m = mover(n)
+    m.checksum(data)
+    torch.cuda.synchronize()
+    crcs, g = oracle.checksum_chunks(0, host_bytes(data), CH)
+    assert np.array_equal(m.crc_host(), crcs)
+    assert int(u32(m.global_crc)[0]) == g
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+@pytest.mark.parametrize("fused", [True, False])
+def test_tiny_full_ship(wm, kind, fused):
+    state = wm_inputs.make_cache(wm_inputs.TINY, "cuda")
+    m = mover(state.numel() * 2, kind)
+    check_full_ship(m, state, kind, "tiny", fused)
+
+
+def test_tiny_full_ship_crc_in_pass(wm):
+    """wm_encode with crc = NULL computes the receipts in the same pass."""
+    state = wm_inputs.make_cache(wm_inputs.TINY, "cuda")
+    m = mover(state.numel() * 2)
+    m.encode(state, with_crc=False)
+    torch.cuda.synchronize()
+    want = oracle.encode(0, host_bytes(state), CH)
+    assert np.array_equal(m.payload_host(), want)
+
+
+def test_tiny_step(wm):
+    prev, cur, ids = wm_inputs.tiny_step("cuda")
+    nbytes = cur.numel() * 2
+    hc, hp = host_bytes(cur), host_bytes(prev)
+    want_idx = oracle.diff_dirty(hc, hp, CH)
+    assert want_idx.tolist() == ids.cpu().tolist()
+    crcs, _ = oracle.checksum_chunks(0, hc, CH)
+    want_payload = oracle.encode(0, hc, CH, want_idx)
+
+    # separate calls
+    m = mover(nbytes)
+    m.checksum(cur)
+    m.diff(cur, prev)
+    m.encode(cur, dirty_only=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(m.dirty_host(), want_idx)
+    assert np.array_equal(m.crc_host(), crcs)
+    assert np.array_equal(m.payload_host(), want_payload)
+
+    # fused step
+    m2 = mover(nbytes)
+    m2.encode_step(cur, prev)
+    torch.cuda.synchronize()
+    assert np.array_equal(m2.dirty_host(), want_idx)
+    assert np.array_equal(m2.crc_host(), crcs)
+    assert np.array_equal(m2.payload_host(), want_payload)
+
+    # destination: decode into compact staging, scatter-install into live
+    live = prev.clone()
+    m2.decode()
+    assert m2.commit(live, scatter=True) == 0
+    assert torch.equal(live, cur)
+    v, staging, _ = oracle.decode_verify(0, want_payload, nbytes, CH)
+    assert v == 0
+    n = want_idx.size
+    assert np.array_equal(host_bytes(m2.staging[: n * CH]), staging[: n * CH])
+
+
+def _words_state(words: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(words.astype(np.uint16).view(np.int16).copy()).cuda()
+
+
+def edge_states():
+    rng = np.random.default_rng(17)
+    n = CH // 2
+    yield "constant", np.full(3 * n, 0x3F80)
+    yield "random_bits", rng.integers(0, 65536, 3 * n)
+    yield "all_patterns", np.arange(65536 * 2) % 65536
+    yield "special", np.resize(np.array([0x7FC0, 0x7F81, 0xFFC1, 0x7F80, 0xFF80,
+                                         0, 0x8000, 1, 0x807F, 0x7F7F]), 2 * n)
+    t = (rng.standard_t(3, 4 * n) * 10).astype(np.float32)
+    yield "student_t", (t.view(np.uint32) >> 16)
+    x = rng.standard_normal(3 * n + 2768).astype(np.float32)
+    yield "ragged_tail", (x.view(np.uint32) >> 16)
+    wide = np.concatenate([rng.integers(0, 256, 16) << 7, np.full(n - 16, 127 << 7)])
+    yield "few_escapes", wide
+    yield "top_exponents", (np.resize([254, 255, 253], n) << 7) | rng.integers(0, 128, n)
+    yield "one_word_tail", np.concatenate([np.full(n, 0x4000), [0x1234]])
+
+
+@pytest.mark.parametrize("label,words", list(edge_states()),
+                         ids=[s[0] for s in edge_states()])
+def test_codec_edge_cases(wm, label, words):
+    state = _words_state(np.asarray(words))
+    m = mover(state.numel() * 2)
+    check_full_ship(m, state, 0, label, fused=True)
+
+
+def test_empty_state(wm):
+    from paper_2607_10389_amd import _wm
+    m = mover(0)
+    state = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    m.encode_step(state, None)
+    torch.cuda.synchronize()
+    want = oracle.encode(0, np.zeros(0, np.uint8), CH)
+    assert np.array_equal(m.payload_host(), want)
+    m.decode()
+    assert m.commit(None, scatter=False) == _wm.WM_OK
+
+
+def test_bit_flips_abort_and_match_oracle(wm):
+    """Flipped payload bits: the GPU verdict equals the oracle's, and a
+    scatter commit after a nonzero verdict leaves live untouched."""
+    rng = np.random.default_rng(4)
+    n = CH // 2
+    x = rng.standard_normal(n).astype(np.float32)
+    words = np.concatenate([x.view(np.uint32) >> 16, rng.integers(0, 65536, n),
+                            np.full(700, 0xBF80)])
+    state = _words_state(words)
+    nbytes = state.numel() * 2
+    m = mover(nbytes)
+    m.encode_step(state, None)
+    torch.cuda.synchronize()
+    good = m.payload_host()
+    assert np.array_equal(good, oracle.encode(0, host_bytes(state), CH))
+    n_rec = 3
+    table = good.size - 16 * n_rec
+    positions = list(range(0, 64)) + list(range(64, 64 + 16)) + \
+        list(range(table, good.size)) + \
+        rng.integers(0, good.size, 120).tolist()
+    live0 = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    for pos in positions:
+        bit = int(rng.integers(0, 8))
+        bad = good.copy()
+        bad[pos] ^= 1 << bit
+        m.payload[: bad.size].copy_(torch.from_numpy(bad))
+        m.decode(payload_cap=bad.size)
+        live = live0.clone()
+        rc = m.commit(live, scatter=True)
+        v_gpu = int(m.verdict.item())
+        v_orc, _, st = oracle.decode_verify(0, bad, nbytes, CH)
+        assert v_orc != 0 and v_gpu == v_orc, (pos, bit, v_gpu, v_orc)
+        assert rc == 1
+        assert not live.any()
+        if v_orc & (oracle.V_RECORD | oracle.V_DATA):
+            assert np.array_equal(u32(m.rec_status)[:n_rec], st[:n_rec]), pos
+
+
+def test_truncation_and_wrong_params(wm):
+    from paper_2607_10389_amd import _wm
+    state = wm_inputs.make_cache(wm_inputs.TINY, "cuda")
+    nbytes = state.numel() * 2
+    m = mover(nbytes)
+    m.encode_step(state, None)
+    size = int(m.payload_bytes.item())
+    m.decode(payload_cap=size - 16)
+    assert m.commit(None, scatter=False) == _wm.WM_VERIFY_FAILED
+    assert int(m.verdict.item()) == oracle.V_HEADER
+    # receiver expecting another size
+    m2 = mover(nbytes - 2)
+    m2.decode(payload=m.payload, payload_cap=size)
+    assert m2.commit(None, scatter=False) == _wm.WM_VERIFY_FAILED
+    # staging too small
+    m3 = mover(nbytes, staging_chunks=4)
+    m3.decode(payload=m.payload, payload_cap=size)
+    assert m3.commit(None, scatter=False) == _wm.WM_VERIFY_FAILED
+    assert int(m3.verdict.item()) == oracle.V_STAGING
+
+
+def test_production_full_ship(wm):
+    state = wm_inputs.make_cache(wm_inputs.PRODUCTION, "cuda")
+    say("[production] generated")
+    m = mover(state.numel() * 2)
+    got = check_full_ship(m, state, 0, "production", fused=True)
+    say(f"[production] payload {got.size} bytes, ratio {got.size / (state.numel() * 2):.4f}")
