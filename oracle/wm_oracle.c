@@ -564,7 +564,8 @@ uint32_t orc_decode_verify(int kind, const uint8_t *payload, uint64_t cap,
   uint64_t payload_bytes = get_u64(h + 32);
   if ((flags & ~1u) || !all_zero(h + 48, 12)) return ORC_V_HEADER;
   if (n_rec > n_chunks) return ORC_V_HEADER;
-  if (64 + 16 * (uint64_t)n_rec > payload_bytes || payload_bytes > cap)
+  if (64 + 16 * (uint64_t)n_rec > payload_bytes || payload_bytes > cap ||
+      payload_bytes % 16)
     return ORC_V_HEADER;
   if ((flags & 1u) && n_rec != n_chunks) return ORC_V_HEADER;
   if ((uint64_t)n_rec * chunk_bytes > staging_cap) return ORC_V_STAGING;

@@ -32,6 +32,7 @@ struct CrcTables {
   uint32_t byte1[256];           // one-byte step of the table method
   uint32_t wave_mat[kWaves][32]; // F^(kSub*(kWaves-1-w) + 4 - kRow), columns
   uint32_t pow2[48][32];         // F^(2^i) bytes, columns
+  uint32_t unrow_mat[32];        // F^(4 - kRow): chunk from a one-wave tree
   uint32_t k_full;               // F^kChunk(~0) ^ ~0
   uint32_t pad_[3];
 };

@@ -583,6 +583,44 @@ __device__ Plan chunk_plan(uint32_t n_words) {
   return p;
 }
 
+// Exclusive prefix (records, record bytes / 16) of `item` by decoupled
+// look-back: wave 0 reads 64 predecessors per round trip and stops at the
+// nearest inclusive one.  Every item publishes its aggregate before its own
+// look-back, and tickets are taken in order by running workgroups, so every
+// predecessor publishes eventually; the spin bound only guarantees
+// termination if that were ever violated.
+__device__ uint64_t lookback(const uint64_t *status, uint32_t item, WsCtl *ctl) {
+  const uint32_t lane = threadIdx.x & 63u;
+  uint64_t excl = 0;
+  int64_t top = (int64_t)item - 1;
+  uint32_t spins = 0;
+  while (top >= 0) {
+    const int64_t j = top - (int64_t)lane;
+    const uint64_t s = j >= 0 ? status_load(&status[j]) : kFlagIncl;
+    const uint32_t f = (uint32_t)(s & 3u);
+    const unsigned long long incl = __ballot(f == kFlagIncl);
+    const unsigned long long empty = __ballot(f == 0u);
+    const uint32_t stop = incl ? (uint32_t)__ffsll((long long)incl) - 1u : 64u;
+    const unsigned long long need = stop >= 63u ? ~0ull : ((2ull << stop) - 1ull);
+    if (empty & need) {
+      if (++spins > (1u << 22)) {
+        if (lane == 0) atomicOr(&ctl->error, 1u);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+      continue;
+    }
+    uint64_t v = lane <= stop ? (s >> 2) : 0ull;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    excl += v;
+    if (stop < 64u) break;
+    top -= 64;
+  }
+  return excl;
+}
+
+template <bool HAS_PREV>
 __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(a.ws + a.L.ctl);
   uint64_t *status = reinterpret_cast<uint64_t *>(a.ws + a.L.status);
@@ -590,7 +628,7 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
   uint32_t *ecrc = reinterpret_cast<uint32_t *>(a.ws + a.L.entry_crc);
   const uint32_t n_items = a.mode == kModeList ? min(*a.n_idx, g.n_chunks) : g.n_chunks;
   const bool need_crc = a.crc_in == nullptr;
-  const bool has_prev = a.mode == kModeStep && a.prev != nullptr;
+  constexpr bool has_prev = HAS_PREV;
 
   load_crc_tables(g.crc_kind);
   const CrcTables &T = g_tables[g.crc_kind];
@@ -599,9 +637,13 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
   uint32_t *M = misc();
   uint8_t *codes = lds + kLdsCodes;
 
-  if (threadIdx.x == 0) M[M_BCAST + 8] = atomicAdd(&ctl->ticket, 1u);
+  if (threadIdx.x == 0) {
+    M[M_BCAST + 8] = atomicAdd(&ctl->ticket, 1u);
+    M[M_BCAST + 13] = atomicAdd(&ctl->ticket, 1u);
+  }
   __syncthreads();
   uint32_t item = M[M_BCAST + 8];
+  uint32_t next = M[M_BCAST + 13];
   uint4 d[kRows], p[kRows];
   if (item < n_items) {
     uint32_t c = item_chunk(a, item, g);
@@ -612,10 +654,6 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
   }
 
   while (item < n_items) {
-    __syncthreads();
-    if (threadIdx.x == 0) M[M_BCAST + 8] = atomicAdd(&ctl->ticket, 1u);
-    __syncthreads();
-    const uint32_t next = M[M_BCAST + 8];
     uint4 dn[kRows], pn[kRows];
     if (next < n_items) {
       uint32_t cn = item_chunk(a, next, g);
@@ -701,30 +739,14 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
     }
     __syncthreads();
 
-    // look-back for the exclusive prefix (records, bytes / 16)
+    // look-back for the exclusive prefix (records, bytes / 16); the next
+    // ticket is taken here so its latency overlaps the look-back
+    uint64_t excl = 0;
+    uint32_t ticket = 0;
+    if (threadIdx.x == 0) ticket = atomicAdd(&ctl->ticket, 1u);
+    if (threadIdx.x < 64u) excl = lookback(status, item, ctl);
     if (threadIdx.x == 0) {
-      uint64_t excl = 0;
-      if (item != 0) {
-        uint32_t j = item - 1;
-        uint32_t spins = 0;
-        while (true) {
-          uint64_t s = status_load(&status[j]);
-          uint64_t f = s & 3u;
-          if (f == 0) {
-            // a predecessor always publishes; the bound only guarantees
-            // that a fault elsewhere cannot keep this wave spinning
-            if (++spins > (1u << 24)) {
-              atomicOr(&ctl->error, 1u);
-              break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-            continue;
-          }
-          excl += s >> 2;
-          if (f == kFlagIncl) break;
-          --j;
-        }
-      }
+      M[M_BCAST + 13] = ticket;
       const uint64_t incl = excl + (agg >> 2);
       status_store(&status[item], (incl << 2) | kFlagIncl);
       if (item + 1 == n_items) {
@@ -802,9 +824,11 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
 #pragma unroll
     for (int h = 0; h < kRows; ++h) {
       d[h] = dn[h];
-      p[h] = pn[h];
+      if (HAS_PREV) p[h] = pn[h];
     }
     item = next;
+    next = M[M_BCAST + 13];
+    __syncthreads();  // everyone has read the ticket before it is rewritten
   }
 }
 
@@ -905,7 +929,7 @@ __global__ __launch_bounds__(256) void k_decode_prepare(
   uint64_t total = ld_u64(payload + 32);
   if ((flags & ~1u) || ld_u32(payload + 48) || ld_u32(payload + 52) || ld_u32(payload + 56)) return;
   if (n_rec > g.n_chunks) return;
-  if (64u + 16ull * n_rec > total || total > cap) return;
+  if (64u + 16ull * n_rec > total || total > cap || (total & 15u)) return;
   if ((flags & 1u) && n_rec != g.n_chunks) return;
   if ((uint64_t)n_rec * kChunk > staging_cap) {
     ctl->verdict_pre = 16u;
@@ -920,7 +944,42 @@ __global__ __launch_bounds__(256) void k_decode_prepare(
   if (n_rec == 0 && total != 64u) ctl->table_bad = 1;
 }
 
-__global__ __launch_bounds__(kThreads) void k_decode(
+// One wave decodes one record: no barriers, so the 16 waves of a workgroup
+// overlap each other's memory latency.  Lane t of the wave owns bytes
+// [16t, 16t+16) of every 1 KiB row of the chunk (rows processed in order);
+// the CRC column streams run down the rows exactly as in the encoder.
+constexpr int kDecWaves = 16;
+constexpr uint32_t kLdsDecScratch = kLdsCrcEnd;  // per wave: 64 u32 row bases
+constexpr uint32_t kLdsDecode = kLdsDecScratch + kDecWaves * 256;
+constexpr int kChunkRows = kChunk / kRow;  // 64
+
+// 8 codes of k bits for the 8 words of group `grp` (12-byte window load).
+__device__ __forceinline__ uint64_t load_codes(const uint8_t *codes, uint32_t grp,
+                                               uint32_t k) {
+  uint64_t start = (uint64_t)grp * k;
+  uint64_t a4 = start & ~3ull;
+  const uint3 x = *reinterpret_cast<const uint3 *>(codes + a4);
+  uint32_t sh = (uint32_t)(start - a4) * 8u;
+  uint64_t lo = ((uint64_t)x.y << 32) | x.x;
+  return sh ? (lo >> sh) | ((uint64_t)x.z << (64 - sh)) : lo;
+}
+
+// CRC of the wave's chunk from its four column states (valid in lane 0).
+__device__ __forceinline__ uint32_t wave_chunk_crc(uint32_t v0, uint32_t v1, uint32_t v2,
+                                                   uint32_t v3, uint32_t len,
+                                                   const ChunkGeom &g, const CrcTables &T) {
+  uint32_t u = tab4(kLdsF8, tab4(kLdsF4, v0) ^ v1) ^ tab4(kLdsF4, v2) ^ v3;
+#pragma unroll
+  for (int lv = 0; lv < kTree; ++lv) {
+    uint32_t s = tab4(kLdsTree + lv * 4096u, u);
+    uint32_t o = __shfl_down(u, 1u << lv, 64);
+    u = s ^ o;
+  }
+  uint32_t raw = mat_apply(T.unrow_mat, u);
+  return len == kChunk ? raw ^ T.k_full : mat_apply(g.tail_mat, raw) ^ g.k_tail;
+}
+
+__global__ __launch_bounds__(kDecWaves * 64) void k_decode(
     const uint8_t *__restrict__ payload, ChunkGeom g, uint8_t *__restrict__ staging,
     uint32_t *__restrict__ rec_status, uint8_t *ws, WsLayout L) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(ws + L.ctl);
@@ -932,186 +991,179 @@ __global__ __launch_bounds__(kThreads) void k_decode(
   __syncthreads();
   const CrcTables &T = g_tables[g.crc_kind];
   const GLane gl = glane_make();
-  const Lane l = lane_info();
-  uint32_t *M = misc();
+  const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
+  uint32_t *rowbase = reinterpret_cast<uint32_t *>(lds + kLdsDecScratch + wave * 256u);
+  const uint32_t stride = gridDim.x * kDecWaves;
 
-  for (uint32_t r = blockIdx.x; r < n_rec; r += gridDim.x) {
-    // ---- table entry and record header (thread 0)
-    if (threadIdx.x == 0) {
-      const uint8_t *e = payload + table_off + 16ull * r;
-      uint32_t ew[4] = {ld_u32(e), ld_u32(e + 4), ld_u32(e + 8), ld_u32(e + 12)};
-      ecrc[r] = crc_words(ew, 4);
-      uint32_t c = ew[0];
-      uint64_t off = (uint64_t)ew[2] | ((uint64_t)ew[3] << 32);
-      uint64_t end = r + 1 < n_rec ? ld_u64(e + 16 + 8) : table_off;
-      bool tbad = c >= g.n_chunks || (r == 0 && off != 64u) || (off & 15u) ||
-                  off >= end || end > table_off;
-      if (r + 1 < n_rec && !tbad && ld_u32(e + 16) <= c) tbad = true;
-      uint32_t st = 0, mode = 0, k = 0, base = 0, n_esc = 0;
-      uint32_t len = 0;
-      if (tbad) {
-        atomicOr(&ctl->table_bad, 1u);
-      } else {
-        len = chunk_len(g, c);
-        uint32_t n_words = len / 2;
-        uint64_t reclen = end - off;
-        const uint8_t *rec = payload + off;
-        if (reclen < 16) {
-          st = 4;
-        } else {
-          uint32_t hw[4] = {ld_u32(rec), ld_u32(rec + 4), ld_u32(rec + 8), ld_u32(rec + 12)};
-          mode = hw[0] & 255u;
-          k = (hw[0] >> 8) & 255u;
-          base = (hw[0] >> 16) & 255u;
-          n_esc = hw[2];
-          if (crc_words(hw, 3) != hw[3] || (hw[0] >> 24) || hw[1] != n_words || mode > 1) {
-            st = 4;
-          } else if (mode == 0) {
-            if (k || base || n_esc || reclen != 16u + pad16(2ull * n_words)) st = 4;
-          } else {
-            if (k > 7 || n_esc > n_words || (k == 0 && n_esc) ||
-                reclen != 16u + pad16(((uint64_t)n_words * k + 7) / 8) + pad16(n_esc) +
-                              pad16(n_words))
-              st = 4;
-          }
-        }
-      }
-      M[M_BCAST + 0] = tbad ? 1u : 0u;
-      M[M_BCAST + 1] = st;
-      M[M_BCAST + 2] = mode;
-      M[M_BCAST + 3] = k;
-      M[M_BCAST + 4] = base;
-      M[M_BCAST + 5] = n_esc;
-      M[M_BCAST + 6] = c;
-      M[M_BCAST + 7] = (uint32_t)off;
-      M[M_BCAST + 8] = (uint32_t)(off >> 32);
-      M[M_BCAST + 9] = ew[1];
-      M[M_BCAST + 10] = len;
-      M[M_BCAST + 11] = 0;  // structure flags raised by the decode below
+  for (uint32_t r = blockIdx.x * kDecWaves + wave; r < n_rec; r += stride) {
+    // ---- table entry, table-local rules (uniform across the wave)
+    const uint8_t *e = payload + table_off + 16ull * r;
+    const uint4 ent = *reinterpret_cast<const uint4 *>(e);
+    const uint32_t c = ent.x, src_crc = ent.y;
+    const uint64_t off = (uint64_t)ent.z | ((uint64_t)ent.w << 32);
+    uint64_t end = table_off;
+    bool tbad = false;
+    if (r + 1 < n_rec) {
+      const uint4 nx = *reinterpret_cast<const uint4 *>(e + 16);
+      end = (uint64_t)nx.z | ((uint64_t)nx.w << 32);
+      tbad = nx.x <= c;
     }
-    __syncthreads();
-    if (M[M_BCAST + 0]) {  // table-local rule failed: record not examined
-      __syncthreads();
+    {
+      uint32_t ew[4] = {ent.x, ent.y, ent.z, ent.w};
+      uint32_t ec = crc_words(ew, 4);
+      if (lane == 0) ecrc[r] = ec;
+    }
+    tbad = tbad || c >= g.n_chunks || (r == 0 && off != 64u) || (off & 15u) || off >= end ||
+           end > table_off;
+    if (tbad) {
+      if (lane == 0) atomicOr(&ctl->table_bad, 1u);
       continue;
     }
-    uint32_t st = M[M_BCAST + 1];
-    const uint32_t mode = M[M_BCAST + 2], k = M[M_BCAST + 3], base = M[M_BCAST + 4];
-    const uint32_t n_esc = M[M_BCAST + 5];
-    const uint64_t off = (uint64_t)M[M_BCAST + 7] | ((uint64_t)M[M_BCAST + 8] << 32);
-    const uint32_t src_crc = M[M_BCAST + 9], len = M[M_BCAST + 10];
-    const uint32_t n_words = len / 2;
+    // ---- record header
+    const uint32_t len = chunk_len(g, c), n_words = len / 2;
+    const uint64_t reclen = end - off;
     const uint8_t *rec = payload + off;
-    uint4 d[kRows];
+    uint32_t st = 0, mode = 0, k = 0, base = 0, n_esc = 0;
+    if (reclen < 16) {
+      st = 4;
+    } else {
+      const uint4 h4 = *reinterpret_cast<const uint4 *>(rec);
+      uint32_t hw[4] = {h4.x, h4.y, h4.z, h4.w};
+      mode = hw[0] & 255u;
+      k = (hw[0] >> 8) & 255u;
+      base = (hw[0] >> 16) & 255u;
+      n_esc = hw[2];
+      if (crc_words(hw, 3) != hw[3] || (hw[0] >> 24) || hw[1] != n_words || mode > 1) {
+        st = 4;
+      } else if (mode == 0) {
+        if (k || base || n_esc || reclen != 16u + pad16(2ull * n_words)) st = 4;
+      } else if (k > 7 || n_esc > n_words || (k == 0 && n_esc) ||
+                 reclen != 16u + pad16(((uint64_t)n_words * k + 7) / 8) + pad16(n_esc) +
+                               pad16(n_words)) {
+        st = 4;
+      }
+    }
     if (st == 0) {
-      uint32_t bad = 0;
+      uint8_t *dst = staging + (uint64_t)r * kChunk;
+      uint32_t v0 = 0, v1 = 0, v2 = 0, v3 = 0;
+      bool bad = false;
       if (mode == 0) {
-        load_chunk(rec + 16, len, l, d);
-        if (threadIdx.x < 16u) {
-          uint64_t at = 16u + 2ull * n_words + threadIdx.x;
-          if (at < 16u + pad16(2ull * n_words) && rec[at]) bad = 1;
+        const uint8_t *body = rec + 16;
+#pragma unroll 4
+        for (int row = 0; row < kChunkRows; ++row) {
+          const uint32_t o = row * kRow + lane * 16u;
+          uint4 d;
+          if (len == kChunk) d = ldg_nt(body + o);
+          else if (o + 16u <= len) d = *reinterpret_cast<const uint4 *>(body + o);
+          else if (o < len) d = load16_partial(body + o, len - o);
+          else d = make_uint4(0, 0, 0, 0);
+          v0 = g_step(v0 ^ d.x, gl);
+          v1 = g_step(v1 ^ d.y, gl);
+          v2 = g_step(v2 ^ d.z, gl);
+          v3 = g_step(v3 ^ d.w, gl);
+          if (o + 16u <= len) {
+            *reinterpret_cast<uint4 *>(dst + o) = d;
+          } else if (o < len) {
+            const uint32_t w[4] = {d.x, d.y, d.z, d.w};
+            for (uint32_t b = 0; b < len - o; ++b) dst[o + b] = (uint8_t)(w[b >> 2] >> (8 * (b & 3)));
+          }
+        }
+        if (lane < 16u) {
+          uint64_t at = 16u + 2ull * n_words + lane;
+          if (at < 16u + pad16(2ull * n_words) && rec[at]) bad = true;
         }
       } else {
         const uint64_t code_bytes = ((uint64_t)n_words * k + 7) / 8;
         const uint64_t esc_off = 16 + pad16(code_bytes);
         const uint64_t sm_off = esc_off + pad16(n_esc);
         const uint32_t esc_code = (1u << k) - 1u;
-        uint32_t codes_w[kRows][2];
-        uint32_t row_rank[kRows];
-        uint32_t wave_esc = 0;
-        // codes of each lane's 8-word groups, escape ranks within the wave
+        const uint8_t *codes = rec + 16;
+        // pass 1: escapes per row (row bases into LDS), literal range check
+        if (k) {
+          uint32_t acc = 0;
+#pragma unroll 4
+          for (int row = 0; row < kChunkRows; ++row) {
+            const uint32_t w0 = row * (kRow / 2) + lane * 8u;
+            uint64_t v = 0;
+            if (w0 < n_words) v = load_codes(codes, w0 >> 3, k);
+            uint32_t s = 0;
 #pragma unroll
-        for (int h = 0; h < kRows; ++h) {
-          const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-          uint64_t v = 0;
-          if (k && w0 < n_words) {
-            uint64_t start = (uint64_t)(w0 >> 3) * k;
-            uint64_t a4 = start & ~3ull;
-            const uint8_t *q = rec + 16 + a4;
-            uint32_t x0 = ld_u32(q), x1 = ld_u32(q + 4), x2 = ld_u32(q + 8);
-            uint32_t sh = (uint32_t)(start - a4) * 8u;
-            uint64_t lo = ((uint64_t)x1 << 32) | x0;
-            v = sh ? (lo >> sh) | ((uint64_t)x2 << (64 - sh)) : lo;
+            for (int u = 0; u < 8; ++u) {
+              uint32_t code = (uint32_t)(v >> (u * k)) & esc_code;
+              bool valid = w0 + u < n_words;
+              if (valid && code != esc_code && base + code > 255u) bad = true;
+              s += (uint32_t)__popcll(__ballot(valid && code == esc_code));
+            }
+            if (lane == 0) rowbase[row] = acc;
+            acc += s;
           }
-          codes_w[h][0] = (uint32_t)v;
-          codes_w[h][1] = (uint32_t)(v >> 32);
-          uint32_t before = 0, lane_esc = 0;
+          if (acc != n_esc) bad = true;
+        }
+        // pass 2: rebuild words, CRC, store
+#pragma unroll 2
+        for (int row = 0; row < kChunkRows; ++row) {
+          const uint32_t o = row * kRow + lane * 16u;
+          const uint32_t w0 = o >> 1;
+          uint32_t out[4] = {0, 0, 0, 0};
+          uint64_t v = 0;
+          if (k && w0 < n_words) v = load_codes(codes, w0 >> 3, k);
+          uint32_t flags = 0;
 #pragma unroll
           for (int u = 0; u < 8; ++u) {
             uint32_t code = (uint32_t)(v >> (u * k)) & esc_code;
-            bool valid = w0 + u < n_words;
-            bool esc = k && valid && code == esc_code;
-            if (k && valid && !esc && base + code > 255u) bad = 1;
-            unsigned long long m = __ballot(esc);
-            before += lanes_below(m);
-            lane_esc += (uint32_t)__popcll(m);
+            if (k && w0 + u < n_words && code == esc_code) flags |= 1u << u;
           }
-          row_rank[h] = wave_esc + before;
-          wave_esc += lane_esc;
-        }
-        if (l.lane == 0) M[M_ESCW + l.wave] = wave_esc;
-        __syncthreads();
-        uint32_t esc_before = 0, esc_total = 0;
-        for (uint32_t w = 0; w < kWaves; ++w) {
-          esc_total += M[M_ESCW + w];
-          if (w < l.wave) esc_before += M[M_ESCW + w];
-        }
-        if (esc_total != n_esc) bad = 1;
-        // rebuild the words
+          // escapes in lower lanes of this row
+          uint32_t below = 0;
 #pragma unroll
-        for (int h = 0; h < kRows; ++h) {
-          const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-          uint32_t out[4] = {0, 0, 0, 0};
+          for (int u = 0; u < 8; ++u) below += lanes_below(__ballot((flags >> u) & 1u));
           if (w0 < n_words) {
-            uint2 smv = *reinterpret_cast<const uint2 *>(rec + sm_off + w0);
-            uint64_t sm8 = ((uint64_t)smv.y << 32) | smv.x;
-            uint64_t v = ((uint64_t)codes_w[h][1] << 32) | codes_w[h][0];
-            uint32_t rank = esc_before + row_rank[h];
+            const uint2 smv = *reinterpret_cast<const uint2 *>(rec + sm_off + w0);
+            const uint64_t sm8 = ((uint64_t)smv.y << 32) | smv.x;
+            uint32_t rank = (k ? rowbase[row] : 0u) + below;
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
               if (w0 + u >= n_words) break;
-              uint32_t code = k ? (uint32_t)(v >> (u * k)) & esc_code : 0u;
-              uint32_t e;
-              if (k && code == esc_code) {
-                e = rank < n_esc ? rec[esc_off + rank] : 0u;
+              uint32_t code = (uint32_t)(v >> (u * k)) & esc_code;
+              uint32_t ex;
+              if ((flags >> u) & 1u) {
+                ex = rank < n_esc ? rec[esc_off + rank] : 0u;
                 ++rank;
               } else {
-                e = (base + code) & 255u;
+                ex = (base + code) & 255u;
               }
               uint32_t sm = (uint32_t)(sm8 >> (8 * u)) & 255u;
-              uint32_t w = ((sm & 0x80u) << 8) | (e << 7) | (sm & 0x7Fu);
+              uint32_t w = ((sm & 0x80u) << 8) | (ex << 7) | (sm & 0x7Fu);
               out[u >> 1] |= w << (16 * (u & 1));
             }
           }
-          d[h] = make_uint4(out[0], out[1], out[2], out[3]);
+          v0 = g_step(v0 ^ out[0], gl);
+          v1 = g_step(v1 ^ out[1], gl);
+          v2 = g_step(v2 ^ out[2], gl);
+          v3 = g_step(v3 ^ out[3], gl);
+          if (o + 16u <= len) {
+            *reinterpret_cast<uint4 *>(dst + o) = make_uint4(out[0], out[1], out[2], out[3]);
+          } else if (o < len) {
+            for (uint32_t b = 0; b < len - o; ++b) dst[o + b] = (uint8_t)(out[b >> 2] >> (8 * (b & 3)));
+          }
         }
         // padding: codes (whole bytes and unused bits), escapes, sm plane
-        if (threadIdx.x < 16u) {
-          uint32_t t = threadIdx.x;
-          if (code_bytes + t < pad16(code_bytes) && rec[16 + code_bytes + t]) bad = 1;
-          if (n_esc + t < pad16(n_esc) && rec[esc_off + n_esc + t]) bad = 1;
-          if (n_words + t < pad16(n_words) && rec[sm_off + n_words + t]) bad = 1;
+        if (lane < 16u) {
+          if (code_bytes + lane < pad16(code_bytes) && codes[code_bytes + lane]) bad = true;
+          if (n_esc + lane < pad16(n_esc) && rec[esc_off + n_esc + lane]) bad = true;
+          if (n_words + lane < pad16(n_words) && rec[sm_off + n_words + lane]) bad = true;
           uint64_t used = (uint64_t)n_words * k;
-          if (t == 0 && (used & 7u) && (rec[16 + used / 8] >> (used & 7u))) bad = 1;
+          if (lane == 0 && (used & 7u) && (codes[used / 8] >> (used & 7u))) bad = true;
         }
       }
-      if (__syncthreads_or(bad)) st = 4;
-    } else {
-      __syncthreads();
-      __syncthreads();
+      const uint32_t crc = wave_chunk_crc(v0, v1, v2, v3, len, g, T);
+      if (__ballot(bad)) st = 4;
+      else if (__shfl(crc, 0, 64) != src_crc) st = 8;
     }
-    if (st == 0) {
-      uint32_t crc = chunk_crc(d, gl, l, len, g, T);
-      store_chunk(staging + (uint64_t)r * kChunk, len, l, d, false);
-      if (threadIdx.x == 0 && crc != src_crc) st = 8;
-    } else {
-      __syncthreads();
-      __syncthreads();
-    }
-    if (threadIdx.x == 0) {
+    if (lane == 0) {
       if (rec_status) rec_status[r] = st;
       if (st) atomicOr(&ctl->rec_bits, st);
     }
-    __syncthreads();
   }
 }
 
@@ -1168,11 +1220,14 @@ int set_kernel_attributes() {
   e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_checksum),
                           hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBase);
   if (e != hipSuccess) return (int)e;
-  e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_encode),
+  e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_encode<false>),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, kLdsEncode);
+  if (e != hipSuccess) return (int)e;
+  e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_encode<true>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, kLdsEncode);
   if (e != hipSuccess) return (int)e;
   e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_decode),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBase);
+                          hipFuncAttributeMaxDynamicSharedMemorySize, kLdsDecode);
   return (int)e;
 }
 
@@ -1237,7 +1292,10 @@ int launch_encode(int mode, const void *cur, const void *prev, const ChunkGeom &
   a.mode = mode;
   if (g.n_chunks) {
     uint32_t grid = min((uint32_t)n_cu, g.n_chunks);
-    hipLaunchKernelGGL(k_encode, dim3(grid), dim3(kThreads), kLdsEncode, S(stream), a, g);
+    if (mode == kModeStep && prev != nullptr)
+      hipLaunchKernelGGL(k_encode<true>, dim3(grid), dim3(kThreads), kLdsEncode, S(stream), a, g);
+    else
+      hipLaunchKernelGGL(k_encode<false>, dim3(grid), dim3(kThreads), kLdsEncode, S(stream), a, g);
     e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
   }
@@ -1276,8 +1334,9 @@ int launch_decode(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
   if (e != hipSuccess) return (int)e;
   if (g.n_chunks) {
     uint32_t grid = min((uint32_t)n_cu, g.n_chunks);
-    hipLaunchKernelGGL(k_decode, dim3(grid), dim3(kThreads), kLdsBase, S(stream), pl, g,
-                       static_cast<uint8_t *>(staging), rec_status, wsb, L);
+    uint32_t grid_d = min((uint32_t)n_cu, (g.n_chunks + kDecWaves - 1) / kDecWaves);
+    hipLaunchKernelGGL(k_decode, dim3(grid_d), dim3(kDecWaves * 64), kLdsDecode, S(stream), pl,
+                       g, static_cast<uint8_t *>(staging), rec_status, wsb, L);
     e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
   }

@@ -110,6 +110,8 @@ void build_crc_tables(uint32_t poly, CrcTables *t) {
     std::memcpy(t->pow2[i], p.c, sizeof(p.c));
     p = compose(p, p);
   }
+  Mat un = byte_shift(poly, 4 - (int64_t)kRow);
+  std::memcpy(t->unrow_mat, un.c, sizeof(un.c));
   t->k_full = apply(byte_shift(poly, kChunk), 0xFFFFFFFFu) ^ 0xFFFFFFFFu;
 }
 
