@@ -25,8 +25,10 @@
  *     0 u8 mode (0 RAW, 1 PACK)  1 u8 k  2 u8 base  3 u8 0
  *     4 u32 n_words  8 u32 n_esc  12 u32 rec_crc = CRC(record bytes 0..11)
  *     RAW : the chunk's bytes
- *     PACK: codes (ceil(n*k/8) B, LSB-first k-bit codes) | escapes (n_esc B)
- *           | sign/mantissa plane (n B)
+ *     PACK: codes (ceil(n*k/8) B, LSB-first k-bit codes) | escape index
+ *           (ceil(n/512) u16: escaped words before each 512-word block)
+ *           | escapes (n_esc B) | sign/mantissa plane (n B); k = 0 has only
+ *           the sign/mantissa plane
  *   A bf16 word w splits into sign w>>15, exponent e = (w>>7)&255 and
  *   mantissa w&127; sm = sign<<7 | mantissa.  PACK with k >= 1 codes e as
  *   e - base when 0 <= e - base < 2^k - 1, else as ESC = 2^k - 1 with e
@@ -203,8 +205,13 @@ static uint8_t sm_of(uint16_t w) {
 }
 
 static uint64_t raw_size(uint32_t n) { return 16 + pad16(2 * (uint64_t)n); }
+/* escape-index entries: one per block of 512 words (k >= 1 only) */
+static uint64_t index_bytes(uint32_t n, uint32_t k) {
+  return k ? 2 * (((uint64_t)n + 511) / 512) : 0;
+}
 static uint64_t pack_size(uint32_t n, uint32_t k, uint32_t n_esc) {
-  return 16 + pad16(((uint64_t)n * k + 7) / 8) + pad16(n_esc) + pad16(n);
+  return 16 + pad16(((uint64_t)n * k + 7) / 8) + pad16(index_bytes(n, k)) +
+         pad16(n_esc) + pad16(n);
 }
 
 /* Mode choice for one chunk of len bytes (len even).  Candidates, in the
@@ -306,7 +313,8 @@ static void write_record(int kind, const uint8_t *chunk, uint32_t len,
     return;
   }
   uint8_t *codes = body;
-  uint8_t *escapes = codes + pad16(((uint64_t)n * k + 7) / 8);
+  uint8_t *index = codes + pad16(((uint64_t)n * k + 7) / 8);
+  uint8_t *escapes = index + pad16(index_bytes(n, k));
   uint8_t *sm = escapes + pad16(n_esc);
   uint32_t esc_code = (1u << k) - 1u;
   uint32_t esc_written = 0;
@@ -315,6 +323,7 @@ static void write_record(int kind, const uint8_t *chunk, uint32_t len,
     uint32_t e = exponent_of(w);
     sm[i] = sm_of(w);
     if (k == 0) continue; /* every exponent equals base */
+    if (i % 512 == 0) put_u16(index + 2 * (i / 512), (uint16_t)esc_written);
     uint32_t code;
     if (e >= base && e - base < esc_code) {
       code = e - base;
@@ -478,11 +487,14 @@ static uint32_t decode_record(int kind, const uint8_t *rec, uint64_t L,
     if (k > 7 || n_esc > n || (k == 0 && n_esc != 0)) return ORC_V_RECORD;
     if (L != pack_size(n, k, n_esc)) return ORC_V_RECORD;
     uint64_t code_bytes = ((uint64_t)n * k + 7) / 8;
+    uint64_t ib = index_bytes(n, k);
     const uint8_t *codes = body;
-    const uint8_t *escapes = codes + pad16(code_bytes);
+    const uint8_t *index = codes + pad16(code_bytes);
+    const uint8_t *escapes = index + pad16(ib);
     const uint8_t *sm = escapes + pad16(n_esc);
     /* padding: whole bytes after each section, and stream bits past n*k */
     if (!all_zero(codes + code_bytes, pad16(code_bytes) - code_bytes) ||
+        !all_zero(index + ib, pad16(ib) - ib) ||
         !all_zero(escapes + n_esc, pad16(n_esc) - n_esc) ||
         !all_zero(sm + n, pad16(n) - n))
       return ORC_V_RECORD;
@@ -493,6 +505,11 @@ static uint32_t decode_record(int kind, const uint8_t *rec, uint64_t L,
     uint32_t esc_read = 0;
     for (uint32_t i = 0; i < n; i++) {
       uint32_t e;
+      /* each index entry must equal the escapes decoded before its block */
+      if (k && i % 512 == 0 &&
+          (uint32_t)(index[2 * (i / 512)] | (index[2 * (i / 512) + 1] << 8)) !=
+              esc_read)
+        return ORC_V_RECORD;
       if (k == 0) {
         e = base;
       } else {

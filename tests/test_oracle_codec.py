@@ -8,6 +8,7 @@ code paths:
   * closed-form record sizes (constant chunk -> PACK k=0; uniform random
     16-bit words -> RAW);
   * a brute-force argmin over every (k, base) on tiny chunks;
+  * escape-index entries counted word by word;
   * hand-built expected bytes for a two-chunk payload, with CRCs from zlib.
 """
 import struct
@@ -101,7 +102,8 @@ def brute_force_plan(words):
             if kbest is None or esc < kbest[1]:
                 kbest = (base, esc)
         base, esc = kbest
-        s = 16 + pad16((n * k + 7) // 8) + pad16(esc) + pad16(n)
+        s = 16 + pad16((n * k + 7) // 8) + pad16(2 * ((n + 511) // 512)) + \
+            pad16(esc) + pad16(n)
         if s < best[0]:
             best = (s, 1, k, base, esc)
     return dict(size=best[0], mode=best[1], k=best[2], base=best[3],
@@ -152,7 +154,8 @@ def test_hand_built_payload():
             if (code >> b) & 1:
                 j = i * 2 + b
                 codes[j // 8] |= 1 << (j % 8)
-    r1 = rec(1, 2, 120, 0, bytes(codes) + sm1.astype(np.uint8).tobytes())
+    index = bytes(16)  # 4 blocks of 512 words, no escapes: four zero u16
+    r1 = rec(1, 2, 120, 0, bytes(codes) + index + sm1.astype(np.uint8).tobytes())
     table = struct.pack("<IIQ", 0, zlib.crc32(c0.tobytes()), 64)
     table += struct.pack("<IIQ", 1, zlib.crc32(c1.tobytes()), 64 + len(r0))
     total = 64 + len(r0) + len(r1) + len(table)
@@ -218,3 +221,23 @@ def test_thread_count_does_not_change_bytes():
     a = oracle.encode(0, state, CH, threads=1)
     b = oracle.encode(0, state, CH, threads=4)
     assert np.array_equal(a, b)
+
+
+def test_escape_index_counts():
+    """Index entry b = escaped words before block b (512 words per block),
+    counted here word by word from the record's own codes."""
+    rng = np.random.default_rng(12)
+    n = 3 * 512 + 100
+    e = np.where(rng.random(n) < 0.1, rng.integers(0, 256, n), 127 + rng.integers(0, 3, n))
+    w = ((e << 7) | rng.integers(0, 128, n)).astype(np.uint16)
+    plan = oracle.plan_chunk(w.view(np.uint8))
+    k, base = plan["k"], plan["base"]
+    assert plan["mode"] == 1 and k >= 1 and plan["n_esc"] > 0
+    payload = oracle.encode(0, np.concatenate([w, np.zeros(CH // 2 - n, np.uint16)]).view(np.uint8)[: 2 * n], CH)
+    rec = payload[64:]
+    code_bytes = (n * k + 7) // 8
+    idx_off = 16 + pad16(code_bytes)
+    index = rec[idx_off: idx_off + 2 * 4].view(np.uint16)
+    esc = [not (base <= x < base + (1 << k) - 1) for x in e]
+    want = [sum(esc[: 512 * b]) for b in range(4)]
+    assert index.tolist() == want
