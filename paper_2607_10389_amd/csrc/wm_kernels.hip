@@ -31,10 +31,6 @@ constexpr uint32_t kLdsTree = kLdsF8 + 4096;        // 6 x 4 KiB
 constexpr uint32_t kLdsCrcEnd = kLdsTree + kTree * 4096;  // 98304
 constexpr uint32_t kLdsMisc = kLdsCrcEnd;           // 8 KiB of small scratch
 constexpr uint32_t kLdsMiscBytes = 8192;
-constexpr uint32_t kLdsHist = kLdsMisc + kLdsMiscBytes;  // 16 KiB histogram
-constexpr uint32_t kLdsCodes = kLdsHist + 16384;         // 28 KiB code staging
-constexpr uint32_t kLdsCodesBytes = 7 * (kChunk / 2) / 8;
-constexpr uint32_t kLdsEncode = kLdsCodes + kLdsCodesBytes;  // 147456
 constexpr uint32_t kLdsBase = kLdsMisc + kLdsMiscBytes;      // 106496
 
 // misc scratch (u32 index into kLdsMisc)
@@ -48,7 +44,6 @@ constexpr uint32_t M_H = 256;       // [256] histogram
 constexpr uint32_t M_P = 512;       // [257] prefix of the histogram
 constexpr uint32_t M_QP = 1024;     // [4][128] quarter partials
 
-static_assert(kLdsEncode <= 163840, "encoder LDS must fit one CU");
 
 extern __shared__ __align__(16) uint8_t lds[];
 
@@ -415,6 +410,7 @@ __global__ __launch_bounds__(1024) void k_compact(const uint32_t *__restrict__ f
 
 constexpr int kModeList = 0, kModeAll = 1, kModeStep = 2;
 constexpr uint64_t kFlagAgg = 1, kFlagIncl = 2;
+constexpr uint32_t kLookbackWindow = 256;  // predecessors read per round trip
 
 struct EncArgs {
   const uint8_t *cur;
@@ -430,17 +426,28 @@ struct EncArgs {
   int mode;
 };
 
-__device__ __forceinline__ uint64_t pad16(uint64_t x) { return (x + 15u) & ~15ull; }
+// Encoder LDS beyond the CRC tables.
+struct EncShared {
+  uint32_t part[kWaves];     // wave CRC partials
+  uint32_t dirty_w[kWaves];  // per-wave "differs from prev"
+  uint32_t esc_w[kWaves];    // escapes per wave
+  uint32_t mode, k, base, n_esc, size, crc, dirty, pad0;
+  uint32_t rec_idx, off_lo, off_hi, ticket;
+  uint32_t H[256];           // histogram
+  uint32_t P[260];           // exclusive prefix of H (P[256] = n)
+};
+static_assert(sizeof(EncShared) <= kLdsMiscBytes, "encoder scratch fits");
+constexpr uint32_t kLdsHistE = kLdsMisc + kLdsMiscBytes;  // 256 bins x 16 copies
+constexpr uint32_t kLdsStage = kLdsHistE + 16384;         // code staging
+constexpr uint32_t kLdsStageBytes = 7 * (kChunk / 2) / 8;
+constexpr uint32_t kLdsEncode = kLdsStage + kLdsStageBytes;
+static_assert(kLdsEncode <= 163840, "encoder LDS fits one CU");
 
-// Chunk of a work item; a caller's list must be ascending and in range, a
-// violation returns an out-of-range index (the item is then flagged).
-__device__ __forceinline__ uint32_t item_chunk(const EncArgs &a, uint32_t item,
-                                               const ChunkGeom &g) {
-  if (a.mode != kModeList) return item;
-  uint32_t c = a.idx[item];
-  if (c >= g.n_chunks || (item > 0 && a.idx[item - 1] >= c)) return 0xFFFFFFFFu;
-  return c;
+__device__ __forceinline__ EncShared &enc_shared() {
+  return *reinterpret_cast<EncShared *>(lds + kLdsMisc);
 }
+
+__device__ __forceinline__ uint64_t pad16(uint64_t x) { return (x + 15u) & ~15ull; }
 
 __device__ __forceinline__ void status_store(uint64_t *p, uint64_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -455,167 +462,116 @@ __device__ __forceinline__ uint32_t lanes_below(unsigned long long m) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
-// Exponent histogram of the chunk's valid words into H[256] (misc).  Uses the
-// 32-copy packed histogram; contains barriers.
-__device__ void chunk_histogram(const uint4 (&d)[kRows], const Lane &l,
-                                uint32_t n_words) {
-  uint32_t *hist = reinterpret_cast<uint32_t *>(lds + kLdsHist);
-  uint4 *h4 = reinterpret_cast<uint4 *>(hist);
-  for (uint32_t i = threadIdx.x; i < 1024u; i += kThreads) h4[i] = make_uint4(0, 0, 0, 0);
-  __syncthreads();
-  const uint32_t copy = threadIdx.x & 31u;
-  const bool full = n_words == kChunk / 2;
+// Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts and row
+// broadcasts).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
 #pragma unroll
-  for (int h = 0; h < kRows; ++h) {
-    const uint32_t w0 = (l.off0 + h * kRow) >> 1;  // first word of the piece
-    const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        if (full || w0 + 2 * j + half < n_words) {
-          uint32_t e = (x[j] >> (7 + 16 * half)) & 255u;
-          atomicAdd(&hist[(e >> 1) * 32u + copy], 1u << ((e & 1u) * 16u));
-        }
-      }
-    }
-  }
-  __syncthreads();
-  // sum the 32 copies: thread (pair p, quarter q) sums 8 copies
-  {
-    uint32_t t = threadIdx.x;
-    uint32_t p = t & 127u, q = t >> 7;
-    uint32_t s = 0;
-#pragma unroll
-    for (uint32_t c = 8 * q; c < 8 * q + 8; ++c) s += hist[p * 32u + ((c + p) & 31u)];
-    misc()[M_QP + q * 128u + p] = s;
-  }
-  __syncthreads();
-  if (threadIdx.x < 128u) {
-    uint32_t p = threadIdx.x;
-    uint32_t s = misc()[M_QP + p] + misc()[M_QP + 128 + p] + misc()[M_QP + 256 + p] +
-                 misc()[M_QP + 384 + p];
-    misc()[M_H + 2 * p] = s & 0xFFFFu;
-    misc()[M_H + 2 * p + 1] = s >> 16;
-  }
-  __syncthreads();
+  for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, 64));
+  return v;
 }
 
-struct Plan {
-  uint32_t mode, k, base, n_esc;
-  uint64_t size;
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pk_sub_min(uint32_t ex, uint32_t base2, uint32_t esc2) {
+  u16x2 a = __builtin_bit_cast(u16x2, ex), b = __builtin_bit_cast(u16x2, base2);
+  u16x2 e = __builtin_bit_cast(u16x2, esc2);
+  u16x2 d = a - b;
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_min(d, e));
+}
+
+// The 8 sign/mantissa bytes of a 16-byte piece: byte u = (w_u >> 8 & 0x80) |
+// (w_u & 0x7F).
+__device__ __forceinline__ uint2 sm_bytes(const uint4 &x) {
+  uint32_t s0 = (x.x & 0x007F007Fu) | ((x.x >> 8) & 0x00800080u);
+  uint32_t s1 = (x.y & 0x007F007Fu) | ((x.y >> 8) & 0x00800080u);
+  uint32_t s2 = (x.z & 0x007F007Fu) | ((x.z >> 8) & 0x00800080u);
+  uint32_t s3 = (x.w & 0x007F007Fu) | ((x.w >> 8) & 0x00800080u);
+  // gather bytes 0 and 2 of each word pair
+  uint32_t lo = __builtin_amdgcn_perm(s1, s0, 0x06040200u);
+  uint32_t hi = __builtin_amdgcn_perm(s3, s2, 0x06040200u);
+  return make_uint2(lo, hi);
+}
+
+// Chunk of a work item; a caller's list must be ascending and in range, a
+// violation returns an out-of-range index (the item is then flagged).
+__device__ __forceinline__ uint32_t item_chunk(const EncArgs &a, uint32_t item,
+                                               const ChunkGeom &g) {
+  if (a.mode != kModeList) return item;
+  uint32_t c = a.idx[item];
+  if (c >= g.n_chunks || (item > 0 && a.idx[item - 1] >= c)) return 0xFFFFFFFFu;
+  return c;
+}
+
+// Look-back (wave 0).  The first window is loaded by lookback_issue before
+// other work; lookback_finish consumes it and reads further windows only if
+// needed.  Every item publishes its aggregate before its own look-back and
+// tickets are handed out in order to running workgroups, so each
+// predecessor publishes eventually; the spin bound only guarantees that the
+// kernel terminates if that were ever violated (the call then reports an
+// empty payload).
+struct Window {
+  uint64_t s[kLookbackWindow / 64];
 };
 
-// Mode choice from H (payload format v1 §3.3); result broadcast in misc.
-__device__ Plan chunk_plan(uint32_t n_words) {
-  uint32_t t = threadIdx.x, lane = t & 63u, wave = t >> 6;
-  uint32_t *M = misc();
-  if (t < 256u) {
-    // inclusive scan of H over the 256 bins
-    uint32_t h = M[M_H + t];
-    uint32_t s = h;
+__device__ __forceinline__ Window lookback_issue(const uint64_t *status, int64_t top) {
+  Window w;
+  const uint32_t lane = threadIdx.x & 63u;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      uint32_t y = __shfl_up(s, o, 64);
-      if (lane >= (uint32_t)o) s += y;
-    }
-    if (lane == 63u) M[M_WSUM + wave] = s;
-    unsigned long long nz = __ballot(h > 0);
-    if (lane == 0) {
-      M[M_WMISC + 2 * wave] = (uint32_t)__popcll(nz);
-      M[M_WMISC + 2 * wave + 1] = nz ? wave * 64u + 63u - __clzll(nz) : 0u;
-    }
-    M[M_P + 1 + t] = s;
+  for (int q = 0; q < (int)(kLookbackWindow / 64); ++q) {
+    int64_t j = top - (int64_t)(lane * (kLookbackWindow / 64) + q);
+    w.s[q] = j >= 0 ? status_load(&status[j]) : kFlagIncl;
   }
-  if (t == 0) M[M_P] = 0;
-  __syncthreads();
-  if (t < 256u) {
-    uint32_t add = 0;
-    for (uint32_t w = 0; w < wave; ++w) add += M[M_WSUM + w];
-    M[M_P + 1 + t] += add;
-  }
-  __syncthreads();
-  if (t < 256u) {
-    uint32_t pb = M[M_P + t];
-#pragma unroll
-    for (int k = 1; k <= 7; ++k) {
-      uint32_t end = min(t + (1u << k) - 1u, 256u);
-      uint32_t key = ((M[M_P + end] - pb) << 8) | (255u - t);
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) key = max(key, (uint32_t)__shfl_xor(key, o, 64));
-      if (lane == 0) M[M_WKEY + wave * 8 + k] = key;
-    }
-  }
-  __syncthreads();
-  if (t == 0) {
-    uint32_t distinct = 0, only = 0;
-    for (int w = 0; w < 4; ++w) {
-      distinct += M[M_WMISC + 2 * w];
-      if (M[M_WMISC + 2 * w]) only = max(only, M[M_WMISC + 2 * w + 1]);
-    }
-    uint64_t n = n_words;
-    Plan best = {0u, 0u, 0u, 0u, 16u + pad16(2 * n)};
-    if (distinct == 1) {
-      uint64_t s = 16u + pad16(n);
-      if (s < best.size) best = Plan{1u, 0u, only, 0u, s};
-    }
-    for (uint32_t k = 1; k <= 7; ++k) {
-      uint32_t key = 0;
-      for (int w = 0; w < 4; ++w) key = max(key, M[M_WKEY + w * 8 + k]);
-      uint32_t inside = key >> 8, base = 255u - (key & 255u);
-      uint32_t esc = n_words - inside;
-      uint64_t s = 16u + pad16((n * k + 7) / 8) + pad16(esc) + pad16(n);
-      if (s < best.size) best = Plan{1u, k, base, esc, s};
-    }
-    M[M_BCAST + 0] = best.mode;
-    M[M_BCAST + 1] = best.k;
-    M[M_BCAST + 2] = best.base;
-    M[M_BCAST + 3] = best.n_esc;
-    M[M_BCAST + 4] = (uint32_t)best.size;
-  }
-  __syncthreads();
-  Plan p;
-  p.mode = M[M_BCAST + 0];
-  p.k = M[M_BCAST + 1];
-  p.base = M[M_BCAST + 2];
-  p.n_esc = M[M_BCAST + 3];
-  p.size = M[M_BCAST + 4];
-  return p;
+  return w;
 }
 
-// Exclusive prefix (records, record bytes / 16) of `item` by decoupled
-// look-back: wave 0 reads 64 predecessors per round trip and stops at the
-// nearest inclusive one.  Every item publishes its aggregate before its own
-// look-back, and tickets are taken in order by running workgroups, so every
-// predecessor publishes eventually; the spin bound only guarantees
-// termination if that were ever violated.
-__device__ uint64_t lookback(const uint64_t *status, uint32_t item, WsCtl *ctl) {
+__device__ uint64_t lookback_finish(const uint64_t *status, int64_t top, Window w,
+                                    WsCtl *ctl) {
+  constexpr int Q = kLookbackWindow / 64;
   const uint32_t lane = threadIdx.x & 63u;
   uint64_t excl = 0;
-  int64_t top = (int64_t)item - 1;
   uint32_t spins = 0;
   while (top >= 0) {
-    const int64_t j = top - (int64_t)lane;
-    const uint64_t s = j >= 0 ? status_load(&status[j]) : kFlagIncl;
-    const uint32_t f = (uint32_t)(s & 3u);
-    const unsigned long long incl = __ballot(f == kFlagIncl);
-    const unsigned long long empty = __ballot(f == 0u);
-    const uint32_t stop = incl ? (uint32_t)__ffsll((long long)incl) - 1u : 64u;
-    const unsigned long long need = stop >= 63u ? ~0ull : ((2ull << stop) - 1ull);
-    if (empty & need) {
+    // distance of an entry from `top` is lane*Q + q
+    uint32_t first = 0xFFFFFFFFu;  // nearest inclusive distance held by this lane
+#pragma unroll
+    for (int q = Q - 1; q >= 0; --q)
+      if ((w.s[q] & 3u) == kFlagIncl) first = lane * Q + q;
+    uint32_t stop = first;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) stop = min(stop, (uint32_t)__shfl_xor((int)stop, o, 64));
+    bool missing = false;
+    uint64_t v = 0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      uint32_t dist = lane * Q + q;
+      if (dist <= stop) {
+        if ((w.s[q] & 3u) == 0) missing = true;
+        v += w.s[q] >> 2;
+      }
+    }
+    if (__ballot(missing)) {
       if (++spins > (1u << 22)) {
         if (lane == 0) atomicOr(&ctl->error, 1u);
         break;
       }
       __builtin_amdgcn_s_sleep(2);
+      w = lookback_issue(status, top);
       continue;
     }
-    uint64_t v = lane <= stop ? (s >> 2) : 0ull;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
     excl += v;
-    if (stop < 64u) break;
-    top -= 64;
+    if (stop != 0xFFFFFFFFu) break;
+    top -= kLookbackWindow;
+    w = lookback_issue(status, top);
   }
   return excl;
 }
@@ -628,149 +584,289 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
   uint32_t *ecrc = reinterpret_cast<uint32_t *>(a.ws + a.L.entry_crc);
   const uint32_t n_items = a.mode == kModeList ? min(*a.n_idx, g.n_chunks) : g.n_chunks;
   const bool need_crc = a.crc_in == nullptr;
-  constexpr bool has_prev = HAS_PREV;
 
   load_crc_tables(g.crc_kind);
   const CrcTables &T = g_tables[g.crc_kind];
   const GLane gl = glane_make();
   const Lane l = lane_info();
-  uint32_t *M = misc();
-  uint8_t *codes = lds + kLdsCodes;
-
+  EncShared &sh = enc_shared();
+  uint8_t *stage = lds + kLdsStage;
+  uint32_t *hist = reinterpret_cast<uint32_t *>(lds + kLdsHistE);
+  const uint32_t copy4 = (threadIdx.x & 15u) * 4u;
+  {
+    uint4 *h4 = reinterpret_cast<uint4 *>(hist);
+    for (uint32_t i = threadIdx.x; i < 1024u; i += kThreads) h4[i] = make_uint4(0, 0, 0, 0);
+  }
   if (threadIdx.x == 0) {
-    M[M_BCAST + 8] = atomicAdd(&ctl->ticket, 1u);
-    M[M_BCAST + 13] = atomicAdd(&ctl->ticket, 1u);
+    sh.rec_idx = atomicAdd(&ctl->ticket, 1u);
+    sh.ticket = atomicAdd(&ctl->ticket, 1u);
   }
   __syncthreads();
-  uint32_t item = M[M_BCAST + 8];
-  uint32_t next = M[M_BCAST + 13];
-  uint4 d[kRows], p[kRows];
+  uint32_t item = sh.rec_idx;
+  uint32_t next = sh.ticket;
+  uint4 d[kRows];
   if (item < n_items) {
     uint32_t c = item_chunk(a, item, g);
-    if (c < g.n_chunks) {
-      load_chunk(a.cur + (uint64_t)c * kChunk, chunk_len(g, c), l, d);
-      if (has_prev) load_chunk(a.prev + (uint64_t)c * kChunk, chunk_len(g, c), l, p);
-    }
+    if (c < g.n_chunks) load_chunk(a.cur + (uint64_t)c * kChunk, chunk_len(g, c), l, d);
   }
+  __syncthreads();
 
   while (item < n_items) {
-    uint4 dn[kRows], pn[kRows];
+    // ---- 1. prefetch the next chunk; prev of this chunk; next ticket
+    uint4 dn[kRows];
     if (next < n_items) {
       uint32_t cn = item_chunk(a, next, g);
-      if (cn < g.n_chunks) {
-        load_chunk(a.cur + (uint64_t)cn * kChunk, chunk_len(g, cn), l, dn);
-        if (has_prev) load_chunk(a.prev + (uint64_t)cn * kChunk, chunk_len(g, cn), l, pn);
-      }
+      if (cn < g.n_chunks) load_chunk(a.cur + (uint64_t)cn * kChunk, chunk_len(g, cn), l, dn);
     }
-
-    // ---- one chunk (an invalid caller index is flagged and encoded as an
-    // empty item so that the scan still completes)
     uint32_t c = item_chunk(a, item, g);
     const bool bad_index = c >= g.n_chunks;
-    if (bad_index) {
-      if (threadIdx.x == 0) atomicOr(&ctl->error, 2u);
-      c = 0;
-    }
+    if (bad_index) c = 0;
     const uint32_t len = bad_index ? 0u : chunk_len(g, c);
     const uint32_t n_words = len / 2;
-    uint32_t crc = 0;
-    if (need_crc) crc = chunk_crc(d, gl, l, bad_index ? kChunk : len, g, T);
-    else if (threadIdx.x == 0) crc = a.crc_in[c];
+    uint4 p[kRows];
+    if (HAS_PREV && !bad_index) load_chunk(a.prev + (uint64_t)c * kChunk, len, l, p);
+    uint32_t ticket = 0;
+    if (threadIdx.x == 0) ticket = atomicAdd(&ctl->ticket, 1u);
 
+    // ---- 2. CRC (and the diff against prev)
+    if (need_crc) {
+      uint32_t q = wave_q(d, gl);
+      if (l.lane == 0) sh.part[l.wave] = mat_apply(T.wave_mat[l.wave], q);
+    }
     bool dirty = !bad_index;
-    if (has_prev && !bad_index) {
+    if (HAS_PREV) {
       uint32_t diff = 0;
 #pragma unroll
       for (int h = 0; h < kRows; ++h)
         diff |= (d[h].x ^ p[h].x) | (d[h].y ^ p[h].y) | (d[h].z ^ p[h].z) | (d[h].w ^ p[h].w);
-      dirty = __syncthreads_or(diff != 0) != 0;
+      unsigned long long any = __ballot(diff != 0);
+      if (l.lane == 0) sh.dirty_w[l.wave] = any ? 1u : 0u;
+      __syncthreads();
+      uint32_t dw = 0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) dw |= sh.dirty_w[w];
+      dirty = dirty && dw != 0;
     }
 
-    Plan plan = {0u, 0u, 0u, 0u, 0u};
+    // ---- 3. exponent histogram (16 copies x 256 bins)
+    const bool full = len == kChunk;
     if (dirty) {
-      chunk_histogram(d, l, n_words);
-      plan = chunk_plan(n_words);
+#pragma unroll
+      for (int h = 0; h < kRows; ++h) {
+        const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+        const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (full || w0 + 2 * j < n_words)
+            atomicAdd(reinterpret_cast<uint32_t *>(lds + kLdsHistE + (((x[j] >> 1) & 0x3FC0u) | copy4)), 1u);
+          if (full || w0 + 2 * j + 1 < n_words)
+            atomicAdd(reinterpret_cast<uint32_t *>(lds + kLdsHistE + (((x[j] >> 17) & 0x3FC0u) | copy4)), 1u);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
-    // publish this item's aggregate (records, record bytes / 16)
-    const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) |
-                         ((uint64_t)(plan.size >> 4) << 26);
-    if (threadIdx.x == 0 && item != 0) status_store(&status[item], agg | kFlagAgg);
+    __syncthreads();  // B1: histogram and CRC partials complete
 
-    // codes into LDS staging, escape counts per row
-    const uint32_t k = plan.k;
+    // ---- 4. histogram reduce (all waves, 32 bins each)
+    if (dirty) {
+      const uint32_t bin = l.wave * 32u + (l.lane >> 1), half = l.lane & 1u;
+      uint32_t s = 0;
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) {
+        uint32_t cp = (half * 8u + ((cc + (l.lane >> 1)) & 7u));
+        s += hist[bin * 16u + cp];
+      }
+      s += __shfl_xor((int)s, 1, 64);
+      if (half == 0) sh.H[bin] = s;
+    }
+    __syncthreads();  // B2: H complete; the histogram copies are free
+
+    // ---- 5. wave 0: chunk CRC, plan, aggregate, first look-back window
+    Window win;
+    if (l.wave == 0) {
+      uint32_t crc = 0;
+      if (need_crc) {
+        uint32_t raw = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) raw ^= sh.part[w];
+        crc = bad_index ? 0u : (full ? raw ^ T.k_full : mat_apply(g.tail_mat, raw) ^ g.k_tail);
+      } else {
+        crc = a.crc_in[c];
+      }
+      uint32_t mode = 0, k = 0, base = 0, n_esc = 0;
+      uint64_t size = 0;
+      if (dirty) {
+        // exclusive prefix P over the 256 bins (4 per lane)
+        const uint32_t b0 = l.lane * 4u;
+        const uint32_t h0 = sh.H[b0], h1 = sh.H[b0 + 1], h2 = sh.H[b0 + 2], h3 = sh.H[b0 + 3];
+        const uint32_t t4 = h0 + h1 + h2 + h3;
+        const uint32_t ex = wave_incl_scan(t4) - t4;
+        sh.P[b0] = ex;
+        sh.P[b0 + 1] = ex + h0;
+        sh.P[b0 + 2] = ex + h0 + h1;
+        sh.P[b0 + 3] = ex + h0 + h1 + h2;
+        if (l.lane == 63u) sh.P[256] = ex + t4;
+        const uint32_t nzmask = (h0 ? 1u : 0u) | (h1 ? 2u : 0u) | (h2 ? 4u : 0u) | (h3 ? 8u : 0u);
+        const uint32_t distinct = wave_incl_scan(__popc(nzmask));
+        const uint32_t n_distinct = __builtin_amdgcn_readlane(distinct, 63);
+        const uint32_t only = wave_max(nzmask ? b0 + 31u - __clz(nzmask) : 0u);
+        const uint64_t n = n_words;
+        // candidates: lane 0 RAW, lane 1 k=0, lanes 2..8 k = lane-1
+        uint64_t cand = ~0ull;
+        uint32_t c_base = 0, c_esc = 0;
+#pragma unroll
+        for (uint32_t kk = 1; kk <= 7; ++kk) {
+          const uint32_t win_w = (1u << kk) - 1u;
+          uint32_t key = 0;
+#pragma unroll
+          for (uint32_t j = 0; j < 4; ++j) {
+            uint32_t b = b0 + j;
+            uint32_t end = min(b + win_w, 256u);
+            uint32_t inside = sh.P[end] - sh.P[b];
+            key = max(key, (inside << 8) | (255u - b));
+          }
+          key = wave_max(key);
+          if (l.lane == kk + 1) {
+            uint32_t inside = key >> 8;
+            c_base = 255u - (key & 255u);
+            c_esc = n_words - inside;
+            cand = 16u + pad16((n * kk + 7) / 8) + pad16(2 * ((n + 511) / 512)) + pad16(c_esc) +
+                   pad16(n);
+          }
+        }
+        if (l.lane == 0) cand = 16u + pad16(2 * n);
+        if (l.lane == 1 && n_distinct == 1) {
+          cand = 16u + pad16(n);
+          c_base = only;
+        }
+        // smallest size, then lowest lane
+        uint64_t key = (cand << 8) | l.lane;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+          uint64_t y = __shfl_xor(key, o, 64);
+          key = y < key ? y : key;
+        }
+        const uint32_t win_lane = (uint32_t)(key & 255u);
+        size = key >> 8;
+        mode = win_lane == 0 ? 0u : 1u;
+        k = win_lane <= 1 ? 0u : win_lane - 1u;
+        base = __shfl((int)c_base, (int)win_lane, 64);
+        n_esc = __shfl((int)c_esc, (int)win_lane, 64);
+      }
+      const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((size >> 4) << 26);
+      if (l.lane == 0) {
+        if (item != 0) status_store(&status[item], agg | kFlagAgg);
+        sh.mode = mode;
+        sh.k = k;
+        sh.base = base;
+        sh.n_esc = n_esc;
+        sh.size = (uint32_t)size;
+        sh.crc = crc;
+        sh.dirty = dirty ? 1u : 0u;
+      }
+      win = lookback_issue(status, (int64_t)item - 1);
+    }
+    __syncthreads();  // B3: plan known
+
+    // ---- 6. codes into staging, escape counts, sign/mantissa bytes
+    const uint32_t mode = sh.mode, k = sh.k, base = sh.base, n_esc = sh.n_esc;
+    dirty = sh.dirty != 0;
+    const bool pack = dirty && mode == 1u && k > 0u;
     const uint32_t esc_code = (1u << k) - 1u;
-    const bool pack = dirty && plan.mode == 1 && k > 0;
-    uint32_t row_rank[kRows];
+    const uint32_t base2 = base | (base << 16), esc2 = esc_code | (esc_code << 16);
+    uint32_t escm[2] = {0, 0};      // escape flags, 8 bits per row
+    uint32_t row_base[kRows];      // escapes in earlier rows of this wave
     uint32_t wave_esc = 0;
     if (pack) {
-      if (len != kChunk) {
-        uint4 *c4 = reinterpret_cast<uint4 *>(codes);
-        for (uint32_t i = threadIdx.x; i < kLdsCodesBytes / 16; i += kThreads)
-          c4[i] = make_uint4(0, 0, 0, 0);
+      if (!full) {
+        uint4 *s4 = reinterpret_cast<uint4 *>(stage);
+        for (uint32_t i = threadIdx.x; i < kLdsStageBytes / 16; i += kThreads)
+          s4[i] = make_uint4(0, 0, 0, 0);
         __syncthreads();
       }
 #pragma unroll
       for (int h = 0; h < kRows; ++h) {
         const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-        const uint32_t grp = w0 >> 3;
         const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
-        uint64_t packed = 0;
-        uint32_t lane_esc = 0;
-        uint32_t before = 0;
+        uint32_t cp[4];
+        uint32_t flags = 0;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          uint32_t e = (x[u >> 1] >> (7 + 16 * (u & 1))) & 255u;
-          bool valid = w0 + u < n_words;
-          uint32_t code = valid ? min(e - plan.base, esc_code) : 0u;
-          packed |= (uint64_t)code << (u * k);
-          bool esc = valid && code == esc_code;
-          unsigned long long m = __ballot(esc);
-          before += lanes_below(m);
-          lane_esc += (uint32_t)__popcll(m);
+        for (int j = 0; j < 4; ++j) {
+          cp[j] = pk_sub_min((x[j] >> 7) & 0x00FF00FFu, base2, esc2);
+          if (!full) {  // words past the chunk code as 0, never escape
+            if (w0 + 2 * j >= n_words) cp[j] &= 0xFFFF0000u;
+            if (w0 + 2 * j + 1 >= n_words) cp[j] &= 0x0000FFFFu;
+          }
+          uint32_t lo = cp[j] & 0xFFFFu, hi = cp[j] >> 16;
+          bool vlo = full || w0 + 2 * j < n_words, vhi = full || w0 + 2 * j + 1 < n_words;
+          flags |= ((vlo && lo == esc_code) ? 1u : 0u) << (2 * j);
+          flags |= ((vhi && hi == esc_code) ? 1u : 0u) << (2 * j + 1);
         }
-        row_rank[h] = wave_esc + before;
-        wave_esc += lane_esc;
+        // 8 codes of k bits
+        uint64_t packed = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          uint64_t pair = (uint64_t)(cp[j] & 0xFFFFu) | ((uint64_t)(cp[j] >> 16) << k);
+          packed |= pair << (2 * j * k);
+        }
         if (w0 < n_words) {
-          uint32_t at = grp * k;
-          for (uint32_t b = 0; b < k; ++b) codes[at + b] = (uint8_t)(packed >> (8 * b));
+          const uint32_t at = (w0 >> 3) * k;
+          if (k == 4u) {
+            *reinterpret_cast<uint32_t *>(stage + at) = (uint32_t)packed;
+          } else if (k == 2u) {
+            *reinterpret_cast<uint16_t *>(stage + at) = (uint16_t)packed;
+          } else if (k == 1u) {
+            stage[at] = (uint8_t)packed;
+          } else {
+            for (uint32_t b = 0; b < k; ++b) stage[at + b] = (uint8_t)(packed >> (8 * b));
+          }
         }
+        const uint32_t cnt = __popc(flags);
+        const uint32_t incl = wave_incl_scan(cnt);
+        row_base[h] = wave_esc;
+        wave_esc += __builtin_amdgcn_readlane(incl, 63);
+        escm[h >> 2] |= flags << (8 * (h & 3));
+        __builtin_amdgcn_sched_barrier(0);
       }
-      if (l.lane == 0) M[M_ESCW + l.wave] = wave_esc;
+      if (l.lane == 0) sh.esc_w[l.wave] = wave_esc;
     }
-    __syncthreads();
-
-    // look-back for the exclusive prefix (records, bytes / 16); the next
-    // ticket is taken here so its latency overlaps the look-back
-    uint64_t excl = 0;
-    uint32_t ticket = 0;
-    if (threadIdx.x == 0) ticket = atomicAdd(&ctl->ticket, 1u);
-    if (threadIdx.x < 64u) excl = lookback(status, item, ctl);
-    if (threadIdx.x == 0) {
-      M[M_BCAST + 13] = ticket;
-      const uint64_t incl = excl + (agg >> 2);
-      status_store(&status[item], (incl << 2) | kFlagIncl);
-      if (item + 1 == n_items) {
-        ctl->n_rec = (uint32_t)(incl & 0xFFFFFFu);
-        ctl->payload_bytes = (incl >> 24) << 4;  // total record bytes
+    // zero the histogram copies for the next chunk
+    {
+      uint4 *h4 = reinterpret_cast<uint4 *>(hist);
+      for (uint32_t i = threadIdx.x; i < 1024u; i += kThreads) h4[i] = make_uint4(0, 0, 0, 0);
+    }
+    // wave 0: finish the look-back, publish the inclusive prefix
+    if (l.wave == 0) {
+      const uint64_t excl = lookback_finish(status, (int64_t)item - 1, win, ctl);
+      if (l.lane == 0) {
+        const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(sh.size >> 4) << 26);
+        const uint64_t incl = excl + (agg >> 2);
+        status_store(&status[item], (incl << 2) | kFlagIncl);
+        if (item + 1 == n_items) {
+          ctl->n_rec = (uint32_t)(incl & 0xFFFFFFu);
+          ctl->payload_bytes = (incl >> 24) << 4;  // total record bytes
+        }
+        sh.rec_idx = (uint32_t)(excl & 0xFFFFFFu);
+        const uint64_t off = 64u + ((excl >> 24) << 4);
+        sh.off_lo = (uint32_t)off;
+        sh.off_hi = (uint32_t)(off >> 32);
+        sh.ticket = ticket;
+        if (bad_index) atomicOr(&ctl->error, 2u);
       }
-      M[M_BCAST + 9] = (uint32_t)(excl & 0xFFFFFFu);      // record index
-      M[M_BCAST + 10] = (uint32_t)(excl >> 24);           // bytes/16 low
-      M[M_BCAST + 11] = (uint32_t)(excl >> 56);           // bytes/16 high
-      M[M_BCAST + 12] = crc;
     }
-    __syncthreads();
-    const uint32_t rec_idx = M[M_BCAST + 9];
-    const uint64_t rec_off =
-        64u + (((uint64_t)M[M_BCAST + 10] | ((uint64_t)M[M_BCAST + 11] << 32)) << 4);
-    crc = M[M_BCAST + 12];
+    __syncthreads();  // B4: offset known, codes staged, escape totals known
 
+    // ---- 7. write the record
+    const uint32_t rec_idx = sh.rec_idx;
+    const uint64_t rec_off = (uint64_t)sh.off_lo | ((uint64_t)sh.off_hi << 32);
+    const uint32_t crc = sh.crc;
     if (dirty) {
       uint8_t *rec = a.payload + rec_off;
       if (threadIdx.x == 0) {
         uint32_t hw[4];
-        hw[0] = plan.mode | (k << 8) | (plan.base << 16);
+        hw[0] = mode | (k << 8) | (base << 16);
         hw[1] = n_words;
-        hw[2] = plan.n_esc;
+        hw[2] = n_esc;
         hw[3] = crc_words(hw, 3);
         *reinterpret_cast<uint4 *>(rec) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
         uint32_t ew[4] = {c, crc, (uint32_t)rec_off, (uint32_t)(rec_off >> 32)};
@@ -778,57 +874,63 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
         ecrc[rec_idx] = crc_words(ew, 4);
         if (a.dirty_idx) a.dirty_idx[rec_idx] = c;
       }
-      if (plan.mode == 0) {
+      if (mode == 0) {
         store_chunk(rec + 16, len, l, d, true);
       } else {
-        const uint64_t code_bytes = ((uint64_t)n_words * k + 7) / 8;
-        const uint64_t esc_off = 16 + pad16(code_bytes);
-        const uint64_t sm_off = esc_off + pad16(plan.n_esc);
-        // codes (whole 16-byte pieces, zero padding included)
+        const uint64_t n = n_words;
+        const uint64_t code_bytes = (n * k + 7) / 8;
+        const uint64_t n_blocks = k ? (n + 511) / 512 : 0;
+        const uint64_t idx_off = 16 + pad16(code_bytes);
+        const uint64_t esc_off = idx_off + pad16(2 * n_blocks);
+        const uint64_t sm_off = esc_off + pad16(n_esc);
         for (uint32_t i = threadIdx.x; i < pad16(code_bytes) / 16; i += kThreads)
           *reinterpret_cast<uint4 *>(rec + 16 + 16 * i) =
-              *reinterpret_cast<const uint4 *>(codes + 16 * i);
-        uint32_t esc_before = 0;
-        for (uint32_t w = 0; w < l.wave; ++w) esc_before += pack ? M[M_ESCW + w] : 0u;
-        // escapes and the sign/mantissa plane
+              *reinterpret_cast<const uint4 *>(stage + 16 * i);
+        uint32_t wave_base = 0;
+        if (pack) {
+          for (uint32_t w = 0; w < l.wave; ++w) wave_base += sh.esc_w[w];
+        }
 #pragma unroll
         for (int h = 0; h < kRows; ++h) {
           const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-          const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
-          uint32_t smw[2] = {0, 0};
-          uint32_t rank = esc_before + (pack ? row_rank[h] : 0u);
+          if (w0 < n_words) *reinterpret_cast<uint2 *>(rec + sm_off + w0) = sm_bytes(d[h]);
+          if (pack) {
+            // escape index entry of this row's 512-word block
+            if (l.lane == 0 && (w0 >> 9) < n_blocks)
+              *reinterpret_cast<uint16_t *>(rec + idx_off + 2 * (w0 >> 9)) =
+                  (uint16_t)(wave_base + row_base[h]);
+            const uint32_t flags = (escm[h >> 2] >> (8 * (h & 3))) & 255u;
+            const uint32_t cnt = __popc(flags);
+            const uint32_t lane_before = wave_incl_scan(cnt) - cnt;
+            if (flags) {
+              const uint32_t xx[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
+              uint32_t rank = wave_base + row_base[h] + lane_before;
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            uint32_t w = (x[u >> 1] >> (16 * (u & 1))) & 0xFFFFu;
-            uint32_t e = (w >> 7) & 255u;
-            bool valid = w0 + u < n_words;
-            uint32_t sm = ((w >> 8) & 0x80u) | (w & 0x7Fu);
-            if (valid) smw[u >> 2] |= sm << (8 * (u & 3));
-            if (pack && valid && min(e - plan.base, esc_code) == esc_code) {
-              rec[esc_off + rank] = (uint8_t)e;
-              ++rank;
+              for (int u = 0; u < 8; ++u) {
+                if ((flags >> u) & 1u) {
+                  rec[esc_off + rank] = (uint8_t)((xx[u >> 1] >> (7 + 16 * (u & 1))) & 255u);
+                  ++rank;
+                }
+              }
             }
           }
-          if (w0 < n_words)
-            *reinterpret_cast<uint2 *>(rec + sm_off + w0) = make_uint2(smw[0], smw[1]);
+          __builtin_amdgcn_sched_barrier(0);
         }
         if (threadIdx.x < 16u) {
-          uint32_t t = threadIdx.x;
-          if (plan.n_esc + t < pad16(plan.n_esc)) rec[esc_off + plan.n_esc + t] = 0;
-          if (n_words + t < pad16(n_words)) rec[sm_off + n_words + t] = 0;
+          const uint32_t t = threadIdx.x;
+          if (2 * n_blocks + t < pad16(2 * n_blocks)) rec[idx_off + 2 * n_blocks + t] = 0;
+          if (n_esc + t < pad16(n_esc)) rec[esc_off + n_esc + t] = 0;
+          if (n + t < pad16(n)) rec[sm_off + n + t] = 0;
         }
       }
     }
-    if (threadIdx.x == 0 && a.crc_out) a.crc_out[c] = crc;
+    if (threadIdx.x == 0 && a.crc_out && !bad_index) a.crc_out[c] = crc;
 
 #pragma unroll
-    for (int h = 0; h < kRows; ++h) {
-      d[h] = dn[h];
-      if (HAS_PREV) p[h] = pn[h];
-    }
+    for (int h = 0; h < kRows; ++h) d[h] = dn[h];
     item = next;
-    next = M[M_BCAST + 13];
-    __syncthreads();  // everyone has read the ticket before it is rewritten
+    next = sh.ticket;
+    __syncthreads();  // B5: scratch may be rewritten
   }
 }
 
@@ -944,18 +1046,21 @@ __global__ __launch_bounds__(256) void k_decode_prepare(
   if (n_rec == 0 && total != 64u) ctl->table_bad = 1;
 }
 
-// One wave decodes one record: no barriers, so the 16 waves of a workgroup
-// overlap each other's memory latency.  Lane t of the wave owns bytes
-// [16t, 16t+16) of every 1 KiB row of the chunk (rows processed in order);
-// the CRC column streams run down the rows exactly as in the encoder.
-constexpr int kDecWaves = 16;
-constexpr uint32_t kLdsDecScratch = kLdsCrcEnd;  // per wave: 64 u32 row bases
-constexpr uint32_t kLdsDecode = kLdsDecScratch + kDecWaves * 256;
-constexpr int kChunkRows = kChunk / kRow;  // 64
+// One wave decodes one record with no barriers, so the 16 waves of a
+// workgroup overlap each other's memory latency.  Lane t owns bytes
+// [16t, 16t+16) of every 1 KiB row (one 512-word escape-index block); rows are
+// decoded in batches of 2 while the next batch's codes, sign/mantissa bytes
+// and escape bytes are already being fetched.
+constexpr int kDecWaves = 12;
+constexpr int kBatch = 2;                       // rows per batch
+constexpr uint32_t kEscPieces = 2;              // 16-byte escape pieces per lane
+constexpr uint32_t kEscStage = 64 * 16 * kEscPieces;  // escape staging per wave
+constexpr uint32_t kLdsDecStage = kLdsCrcEnd;
+constexpr uint32_t kLdsDecode = kLdsDecStage + kDecWaves * kEscStage;
+constexpr int kChunkRows = kChunk / kRow;       // 64
+static_assert(kLdsDecode <= 163840, "decoder LDS fits one CU");
 
-// 8 codes of k bits for the 8 words of group `grp` (12-byte window load).
-__device__ __forceinline__ uint64_t load_codes(const uint8_t *codes, uint32_t grp,
-                                               uint32_t k) {
+__device__ __forceinline__ uint64_t load_codes(const uint8_t *codes, uint32_t grp, uint32_t k) {
   uint64_t start = (uint64_t)grp * k;
   uint64_t a4 = start & ~3ull;
   const uint3 x = *reinterpret_cast<const uint3 *>(codes + a4);
@@ -964,7 +1069,6 @@ __device__ __forceinline__ uint64_t load_codes(const uint8_t *codes, uint32_t gr
   return sh ? (lo >> sh) | ((uint64_t)x.z << (64 - sh)) : lo;
 }
 
-// CRC of the wave's chunk from its four column states (valid in lane 0).
 __device__ __forceinline__ uint32_t wave_chunk_crc(uint32_t v0, uint32_t v1, uint32_t v2,
                                                    uint32_t v3, uint32_t len,
                                                    const ChunkGeom &g, const CrcTables &T) {
@@ -977,6 +1081,132 @@ __device__ __forceinline__ uint32_t wave_chunk_crc(uint32_t v0, uint32_t v1, uin
   }
   uint32_t raw = mat_apply(T.unrow_mat, u);
   return len == kChunk ? raw ^ T.k_full : mat_apply(g.tail_mat, raw) ^ g.k_tail;
+}
+
+struct PackRec {
+  const uint8_t *rec;
+  uint64_t code_off, idx_off, esc_off, sm_off;
+  uint32_t k, base, n_esc, n_words, n_blocks, esc_code;
+  uint32_t blk;  // lane b holds escape-index entry b (lane n_blocks: n_esc)
+};
+
+struct DecBatch {
+  uint3 code[kBatch];
+  uint2 sm[kBatch];
+  uint4 esc[kEscPieces];
+  uint32_t lo, lo_al, hi;
+};
+
+__device__ __forceinline__ uint32_t blk_at(const PackRec &R, uint32_t b) {
+  if (b >= R.n_blocks) return R.n_esc;
+  return (uint32_t)__shfl((int)R.blk, (int)b, 64);
+}
+
+__device__ __forceinline__ void dec_load(DecBatch &B, const PackRec &R, int j, uint32_t lane,
+                                         uint64_t reclen) {
+#pragma unroll
+  for (int q = 0; q < kBatch; ++q) {
+    const uint32_t row = j * kBatch + q;
+    const uint32_t w0 = row * (kRow / 2) + lane * 8u;
+    B.code[q] = make_uint3(0, 0, 0);
+    B.sm[q] = make_uint2(0, 0);
+    if (w0 < R.n_words) {
+      if (R.k) {
+        uint64_t a4 = ((uint64_t)(w0 >> 3) * R.k) & ~3ull;
+        B.code[q] = *reinterpret_cast<const uint3 *>(R.rec + R.code_off + a4);
+      }
+      B.sm[q] = *reinterpret_cast<const uint2 *>(R.rec + R.sm_off + w0);
+    }
+  }
+  // escape bytes of the batch: [index[4j], index[4j+4]) from the index
+  B.lo = B.lo_al = B.hi = 0;
+  if (R.k) {
+    uint32_t lo = blk_at(R, j * kBatch), hi = blk_at(R, j * kBatch + kBatch);
+    lo = min(lo, R.n_esc);
+    hi = min(max(hi, lo), R.n_esc);
+    if (hi - lo > kBatch * (kRow / 2)) hi = lo;  // inconsistent index: rejected later
+    B.lo = lo;
+    B.hi = hi;
+    B.lo_al = lo & ~15u;
+#pragma unroll
+    for (int p = 0; p < (int)kEscPieces; ++p) {
+      const uint32_t piece = lane + 64u * p;
+      B.esc[p] = make_uint4(0, 0, 0, 0);
+      const uint64_t at = R.esc_off + B.lo_al + 16u * piece;
+      if (B.lo_al + 16u * piece < hi && at + 16 <= reclen)
+        B.esc[p] = *reinterpret_cast<const uint4 *>(R.rec + at);
+    }
+  }
+}
+
+// Decode one batch; returns whether any structure rule failed.
+__device__ __forceinline__ bool dec_process(const DecBatch &B, const PackRec &R, int j,
+                                            uint32_t lane, uint8_t *stage, uint32_t &acc,
+                                            uint32_t &v0, uint32_t &v1, uint32_t &v2,
+                                            uint32_t &v3, const GLane &gl, uint8_t *dst,
+                                            uint32_t len) {
+  bool bad = false;
+  if (R.k) {
+#pragma unroll
+    for (int p = 0; p < (int)kEscPieces; ++p)
+      *reinterpret_cast<uint4 *>(stage + 16u * (lane + 64u * p)) = B.esc[p];
+  }
+#pragma unroll
+  for (int q = 0; q < kBatch; ++q) {
+    const uint32_t row = j * kBatch + q;
+    const uint32_t w0 = row * (kRow / 2) + lane * 8u;
+    const uint32_t o = w0 * 2u;
+    uint32_t out[4] = {0, 0, 0, 0};
+    if (row * (kRow / 2) < R.n_words) {
+      uint64_t v = 0;
+      if (R.k) {
+        const uint64_t start = (uint64_t)(w0 >> 3) * R.k;
+        const uint32_t sh = (uint32_t)(start & 3u) * 8u;
+        const uint64_t lo = ((uint64_t)B.code[q].y << 32) | B.code[q].x;
+        v = sh ? (lo >> sh) | ((uint64_t)B.code[q].z << (64 - sh)) : lo;
+      }
+      uint32_t flags = 0;
+      uint32_t codes[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        codes[u] = (uint32_t)(v >> (u * R.k)) & R.esc_code;
+        bool valid = w0 + u < R.n_words;
+        if (R.k && valid && codes[u] == R.esc_code) flags |= 1u << u;
+        if (R.k && valid && codes[u] != R.esc_code && R.base + codes[u] > 255u) bad = true;
+      }
+      const uint32_t cnt = __popc(flags);
+      const uint32_t incl = wave_incl_scan(cnt);
+      // the index entry of this block must equal the escapes decoded so far
+      if (R.k && blk_at(R, row) != acc) bad = true;
+      uint32_t rank = acc + incl - cnt;
+      acc += __builtin_amdgcn_readlane(incl, 63);
+      const uint64_t sm8 = ((uint64_t)B.sm[q].y << 32) | B.sm[q].x;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        uint32_t ex = (R.base + codes[u]) & 255u;
+        if ((flags >> u) & 1u) {
+          uint32_t at = rank - B.lo_al;
+          ex = (rank >= B.lo && rank < B.hi && at < kEscStage) ? stage[at] : 0u;
+          if (!(rank >= B.lo && rank < B.hi)) bad = true;
+          ++rank;
+        }
+        const uint32_t sm = (uint32_t)(sm8 >> (8 * u)) & 255u;
+        const uint32_t w = ((sm & 0x80u) << 8) | (ex << 7) | (sm & 0x7Fu);
+        if (w0 + u < R.n_words) out[u >> 1] |= w << (16 * (u & 1));
+      }
+    }
+    v0 = g_step(v0 ^ out[0], gl);
+    v1 = g_step(v1 ^ out[1], gl);
+    v2 = g_step(v2 ^ out[2], gl);
+    v3 = g_step(v3 ^ out[3], gl);
+    if (o + 16u <= len) {
+      *reinterpret_cast<uint4 *>(dst + o) = make_uint4(out[0], out[1], out[2], out[3]);
+    } else if (o < len) {
+      for (uint32_t b = 0; b < len - o; ++b) dst[o + b] = (uint8_t)(out[b >> 2] >> (8 * (b & 3)));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  return bad;
 }
 
 __global__ __launch_bounds__(kDecWaves * 64) void k_decode(
@@ -992,7 +1222,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void k_decode(
   const CrcTables &T = g_tables[g.crc_kind];
   const GLane gl = glane_make();
   const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
-  uint32_t *rowbase = reinterpret_cast<uint32_t *>(lds + kLdsDecScratch + wave * 256u);
+  uint8_t *stage = lds + kLdsDecStage + wave * kEscStage;
   const uint32_t stride = gridDim.x * kDecWaves;
 
   for (uint32_t r = blockIdx.x * kDecWaves + wave; r < n_rec; r += stride) {
@@ -1024,6 +1254,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void k_decode(
     const uint64_t reclen = end - off;
     const uint8_t *rec = payload + off;
     uint32_t st = 0, mode = 0, k = 0, base = 0, n_esc = 0;
+    uint64_t code_bytes = 0, n_blocks = 0;
     if (reclen < 16) {
       st = 4;
     } else {
@@ -1033,12 +1264,14 @@ __global__ __launch_bounds__(kDecWaves * 64) void k_decode(
       k = (hw[0] >> 8) & 255u;
       base = (hw[0] >> 16) & 255u;
       n_esc = hw[2];
+      code_bytes = ((uint64_t)n_words * k + 7) / 8;
+      n_blocks = k ? ((uint64_t)n_words + 511) / 512 : 0;
       if (crc_words(hw, 3) != hw[3] || (hw[0] >> 24) || hw[1] != n_words || mode > 1) {
         st = 4;
       } else if (mode == 0) {
         if (k || base || n_esc || reclen != 16u + pad16(2ull * n_words)) st = 4;
       } else if (k > 7 || n_esc > n_words || (k == 0 && n_esc) ||
-                 reclen != 16u + pad16(((uint64_t)n_words * k + 7) / 8) + pad16(n_esc) +
+                 reclen != 16u + pad16(code_bytes) + pad16(2 * n_blocks) + pad16(n_esc) +
                                pad16(n_words)) {
         st = 4;
       }
@@ -1049,7 +1282,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void k_decode(
       bool bad = false;
       if (mode == 0) {
         const uint8_t *body = rec + 16;
-#pragma unroll 4
+#pragma unroll 8
         for (int row = 0; row < kChunkRows; ++row) {
           const uint32_t o = row * kRow + lane * 16u;
           uint4 d;
@@ -1073,92 +1306,54 @@ __global__ __launch_bounds__(kDecWaves * 64) void k_decode(
           if (at < 16u + pad16(2ull * n_words) && rec[at]) bad = true;
         }
       } else {
-        const uint64_t code_bytes = ((uint64_t)n_words * k + 7) / 8;
-        const uint64_t esc_off = 16 + pad16(code_bytes);
-        const uint64_t sm_off = esc_off + pad16(n_esc);
-        const uint32_t esc_code = (1u << k) - 1u;
-        const uint8_t *codes = rec + 16;
-        // pass 1: escapes per row (row bases into LDS), literal range check
-        if (k) {
-          uint32_t acc = 0;
-#pragma unroll 4
-          for (int row = 0; row < kChunkRows; ++row) {
-            const uint32_t w0 = row * (kRow / 2) + lane * 8u;
-            uint64_t v = 0;
-            if (w0 < n_words) v = load_codes(codes, w0 >> 3, k);
-            uint32_t s = 0;
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-              uint32_t code = (uint32_t)(v >> (u * k)) & esc_code;
-              bool valid = w0 + u < n_words;
-              if (valid && code != esc_code && base + code > 255u) bad = true;
-              s += (uint32_t)__popcll(__ballot(valid && code == esc_code));
-            }
-            if (lane == 0) rowbase[row] = acc;
-            acc += s;
-          }
-          if (acc != n_esc) bad = true;
+        PackRec R;
+        R.rec = rec;
+        R.k = k;
+        R.base = base;
+        R.n_esc = n_esc;
+        R.n_words = n_words;
+        R.n_blocks = (uint32_t)n_blocks;
+        R.esc_code = (1u << k) - 1u;
+        R.code_off = 16;
+        R.idx_off = 16 + pad16(code_bytes);
+        R.esc_off = R.idx_off + pad16(2 * n_blocks);
+        R.sm_off = R.esc_off + pad16(n_esc);
+        R.blk = (k && lane < n_blocks)
+                    ? (uint32_t)(*reinterpret_cast<const uint16_t *>(rec + R.idx_off + 2 * lane))
+                    : n_esc;
+        const int n_batches = (int)((n_words + kBatch * (kRow / 2) - 1) / (kBatch * (kRow / 2)));
+        uint32_t acc = 0;
+        DecBatch A, B2;
+        dec_load(A, R, 0, lane, reclen);
+        for (int j = 0; j < n_batches; j += 2) {
+          if (j + 1 < n_batches) dec_load(B2, R, j + 1, lane, reclen);
+          bad |= dec_process(A, R, j, lane, stage, acc, v0, v1, v2, v3, gl, dst, len);
+          if (j + 1 >= n_batches) break;
+          if (j + 2 < n_batches) dec_load(A, R, j + 2, lane, reclen);
+          bad |= dec_process(B2, R, j + 1, lane, stage, acc, v0, v1, v2, v3, gl, dst, len);
         }
-        // pass 2: rebuild words, CRC, store
-#pragma unroll 2
-        for (int row = 0; row < kChunkRows; ++row) {
-          const uint32_t o = row * kRow + lane * 16u;
-          const uint32_t w0 = o >> 1;
-          uint32_t out[4] = {0, 0, 0, 0};
-          uint64_t v = 0;
-          if (k && w0 < n_words) v = load_codes(codes, w0 >> 3, k);
-          uint32_t flags = 0;
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            uint32_t code = (uint32_t)(v >> (u * k)) & esc_code;
-            if (k && w0 + u < n_words && code == esc_code) flags |= 1u << u;
-          }
-          // escapes in lower lanes of this row
-          uint32_t below = 0;
-#pragma unroll
-          for (int u = 0; u < 8; ++u) below += lanes_below(__ballot((flags >> u) & 1u));
-          if (w0 < n_words) {
-            const uint2 smv = *reinterpret_cast<const uint2 *>(rec + sm_off + w0);
-            const uint64_t sm8 = ((uint64_t)smv.y << 32) | smv.x;
-            uint32_t rank = (k ? rowbase[row] : 0u) + below;
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-              if (w0 + u >= n_words) break;
-              uint32_t code = (uint32_t)(v >> (u * k)) & esc_code;
-              uint32_t ex;
-              if ((flags >> u) & 1u) {
-                ex = rank < n_esc ? rec[esc_off + rank] : 0u;
-                ++rank;
-              } else {
-                ex = (base + code) & 255u;
-              }
-              uint32_t sm = (uint32_t)(sm8 >> (8 * u)) & 255u;
-              uint32_t w = ((sm & 0x80u) << 8) | (ex << 7) | (sm & 0x7Fu);
-              out[u >> 1] |= w << (16 * (u & 1));
-            }
-          }
-          v0 = g_step(v0 ^ out[0], gl);
-          v1 = g_step(v1 ^ out[1], gl);
-          v2 = g_step(v2 ^ out[2], gl);
-          v3 = g_step(v3 ^ out[3], gl);
-          if (o + 16u <= len) {
-            *reinterpret_cast<uint4 *>(dst + o) = make_uint4(out[0], out[1], out[2], out[3]);
-          } else if (o < len) {
-            for (uint32_t b = 0; b < len - o; ++b) dst[o + b] = (uint8_t)(out[b >> 2] >> (8 * (b & 3)));
-          }
+        // rows past the chunk: zero data, as in the zero-padded CRC layout
+        for (int row = n_batches * kBatch; row < kChunkRows; ++row) {
+          v0 = g_step(v0, gl);
+          v1 = g_step(v1, gl);
+          v2 = g_step(v2, gl);
+          v3 = g_step(v3, gl);
         }
-        // padding: codes (whole bytes and unused bits), escapes, sm plane
+        if (acc != n_esc) bad = true;
+        // padding: codes (whole bytes and unused bits), index, escapes, sm
         if (lane < 16u) {
+          const uint8_t *codes = rec + R.code_off;
           if (code_bytes + lane < pad16(code_bytes) && codes[code_bytes + lane]) bad = true;
-          if (n_esc + lane < pad16(n_esc) && rec[esc_off + n_esc + lane]) bad = true;
-          if (n_words + lane < pad16(n_words) && rec[sm_off + n_words + lane]) bad = true;
+          if (2 * n_blocks + lane < pad16(2 * n_blocks) && rec[R.idx_off + 2 * n_blocks + lane]) bad = true;
+          if (n_esc + lane < pad16(n_esc) && rec[R.esc_off + n_esc + lane]) bad = true;
+          if (n_words + lane < pad16(n_words) && rec[R.sm_off + n_words + lane]) bad = true;
           uint64_t used = (uint64_t)n_words * k;
           if (lane == 0 && (used & 7u) && (codes[used / 8] >> (used & 7u))) bad = true;
         }
       }
       const uint32_t crc = wave_chunk_crc(v0, v1, v2, v3, len, g, T);
       if (__ballot(bad)) st = 4;
-      else if (__shfl(crc, 0, 64) != src_crc) st = 8;
+      else if ((uint32_t)__shfl((int)crc, 0, 64) != src_crc) st = 8;
     }
     if (lane == 0) {
       if (rec_status) rec_status[r] = st;
@@ -1166,6 +1361,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void k_decode(
     }
   }
 }
+
 
 // Final verdict after the table CRC has been combined.
 __global__ void k_decode_verdict(const uint8_t *ws, WsLayout L,
@@ -1333,7 +1529,6 @@ int launch_decode(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
   if (g.n_chunks) {
-    uint32_t grid = min((uint32_t)n_cu, g.n_chunks);
     uint32_t grid_d = min((uint32_t)n_cu, (g.n_chunks + kDecWaves - 1) / kDecWaves);
     hipLaunchKernelGGL(k_decode, dim3(grid_d), dim3(kDecWaves * 64), kLdsDecode, S(stream), pl,
                        g, static_cast<uint8_t *>(staging), rec_status, wsb, L);
