@@ -1,20 +1,27 @@
 // wm_kernels.hip -- CDNA4 (gfx950) kernels of the exact-state mover.
 //
-// Data layout.  A 64 KiB chunk is processed by one 512-thread workgroup with
-// the chunk held in registers: wave w owns bytes [w*8K, (w+1)*8K); lane t of
-// the wave owns 16 bytes of each 1 KiB row h (offset w*8K + h*1K + 16t), so
-// every load and store is a coalesced 128-bit access.
+// Data layout.  A 64 KiB chunk is split into 64 rows of 1 KiB; lane t of a
+// wave owns bytes [16t, 16t+16) of each row it handles, so every load and
+// store is a coalesced 128-bit access.  The encoder gives each of 8 data
+// waves 8 consecutive rows of a chunk; the decoder gives one wave a whole
+// record.
 //
 // CRC (§4 "Sufficiency", §6.5: per-chunk zlib CRC, GF(2)-combined).  Each lane
 // runs four independent dword "column" streams down its rows:
 //     v <- F^1024(v ^ d)
 // (the next dword of the column is 1 KiB further on).  A lane's four columns
 // merge into one value, the 64 lane values of a wave merge through a 6-level
-// shuffle tree of byte-table shifts, and the 8 wave values merge through one
-// GF(2) matrix per wave.  The F^1024 tables are the hot ones: 16 copies in
-// LDS, addressed as byte*256 + slot*64 + copy*4 with v_perm, where each group
-// of 16 lanes starts at a different table slot so that one ds_read touches
-// every bank once.  All other shift tables are read rarely and kept single.
+// shuffle tree of byte-table shifts, and wave values merge through one GF(2)
+// matrix per wave.  The F^1024 tables are the hot ones: 16 copies in LDS,
+// addressed as byte*256 + slot*64 + copy*4 with v_perm, where each group of
+// 16 lanes starts at a different table slot so that one ds_read touches every
+// bank once.  All other shift tables are read rarely and kept single.
+//
+// Memory ordering rule followed by the streaming loops: a wave that has
+// issued its prefetch of the next rows issues no other vector-memory load
+// until it consumes that prefetch (vector-memory loads retire in order, so
+// any later load would wait for the whole prefetch).  Uniform data (tables,
+// matrices) therefore comes through scalar loads.
 #include <hip/hip_runtime.h>
 
 #include "wm_internal.h"
@@ -31,19 +38,10 @@ constexpr uint32_t kLdsTree = kLdsF8 + 4096;        // 6 x 4 KiB
 constexpr uint32_t kLdsCrcEnd = kLdsTree + kTree * 4096;  // 98304
 constexpr uint32_t kLdsMisc = kLdsCrcEnd;           // 8 KiB of small scratch
 constexpr uint32_t kLdsMiscBytes = 8192;
-constexpr uint32_t kLdsBase = kLdsMisc + kLdsMiscBytes;      // 106496
+constexpr uint32_t kLdsBase = kLdsMisc + kLdsMiscBytes;  // 106496
 
-// misc scratch (u32 index into kLdsMisc)
-constexpr uint32_t M_PART = 0;      // [kWaves] wave CRC partials
-constexpr uint32_t M_BCAST = 16;    // [32] broadcast words
-constexpr uint32_t M_ESCW = 64;     // [kWaves] escapes per wave
-constexpr uint32_t M_WKEY = 80;     // [4][8] window keys per wave
-constexpr uint32_t M_WMISC = 120;   // [4][2] distinct / single per wave
-constexpr uint32_t M_WSUM = 136;    // [4] wave sums of the histogram scan
-constexpr uint32_t M_H = 256;       // [256] histogram
-constexpr uint32_t M_P = 512;       // [257] prefix of the histogram
-constexpr uint32_t M_QP = 1024;     // [4][128] quarter partials
-
+// checksum-kernel scratch (u32 index into kLdsMisc)
+constexpr uint32_t M_PART = 0;  // [kWaves] wave CRC partials
 
 extern __shared__ __align__(16) uint8_t lds[];
 
@@ -60,6 +58,9 @@ __device__ __forceinline__ uint32_t lds_u32(uint32_t off) {
 }
 __device__ __forceinline__ uint32_t *misc() {
   return reinterpret_cast<uint32_t *>(lds + kLdsMisc);
+}
+__device__ __forceinline__ uint32_t uniform(uint32_t v) {
+  return __builtin_amdgcn_readfirstlane(v);
 }
 
 // Byte-table application of a shift stored at LDS offset `off`.
@@ -109,12 +110,13 @@ __device__ void load_crc_tables(uint32_t kind) {
     dst[i] = src[i];
 }
 
-// Columns applied to v (uniform matrix, scalar loads).
+// Columns applied to v; `m` must be wave-uniform (the columns then arrive
+// through scalar loads).
 __device__ __forceinline__ uint32_t mat_apply(const uint32_t *__restrict__ m,
                                               uint32_t v) {
   uint32_t r = 0;
 #pragma unroll
-  for (int i = 0; i < 32; ++i) r ^= ((v >> i) & 1u) ? m[i] : 0u;
+  for (int i = 0; i < 32; ++i) r ^= m[i] & (0u - ((v >> i) & 1u));  // no load under a branch
   return r;
 }
 
@@ -126,23 +128,56 @@ __device__ uint32_t shift_bytes(const CrcTables &T, uint64_t m, uint32_t v) {
 }
 
 // Standard CRC (init/xorout ~0) of 4*nw bytes held as words, with F^4 tables
-// in LDS.  One lane; used for headers and table entries.
+// in LDS.  Used for headers and table entries.
 __device__ __forceinline__ uint32_t crc_words(const uint32_t *w, int nw) {
   uint32_t s = 0xFFFFFFFFu;
   for (int i = 0; i < nw; ++i) s = tab4(kLdsF4, s ^ w[i]);
   return s ^ 0xFFFFFFFFu;
 }
 
+__device__ __forceinline__ uint64_t pad16(uint64_t x) { return (x + 15u) & ~15ull; }
+
+__device__ __forceinline__ uint32_t lanes_below(unsigned long long m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts and row
+// broadcasts).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, 64));
+  return v;
+}
+
 // -------------------------------------------------------- chunk movement --
 
 struct Lane {
-  uint32_t wave, lane, off0;  // off0: chunk offset of row 0
+  uint32_t wave, lane, off0;  // off0: chunk offset of the lane's first row
 };
 __device__ __forceinline__ Lane lane_info() {
   Lane l;
-  l.wave = threadIdx.x >> 6;
+  l.wave = uniform(threadIdx.x >> 6);
   l.lane = threadIdx.x & 63u;
   l.off0 = l.wave * kSub + l.lane * 16u;
+  return l;
+}
+
+// The same lane offsets, hidden from loop-invariant code motion: per-row
+// addresses derived from them are then recomputed in each iteration of a
+// chunk loop instead of being hoisted out of it and held in registers for its
+// whole duration (dozens of them with the k-specialised paths).
+__device__ __forceinline__ Lane lane_fresh(Lane l) {
+  asm volatile("" : "+v"(l.lane), "+v"(l.off0));
   return l;
 }
 
@@ -156,14 +191,13 @@ __device__ __forceinline__ uint4 load16_partial(const uint8_t *p, uint32_t n) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// Load a chunk of `len` bytes into registers; bytes past len read as zero.
+// Load a wave's 8 rows of a chunk of `len` bytes; bytes past len read 0.
 __device__ __forceinline__ void load_chunk(const uint8_t *__restrict__ base,
                                            uint32_t len, const Lane &l,
                                            uint4 (&d)[kRows]) {
   if (len == kChunk) {
 #pragma unroll
-    for (int h = 0; h < kRows; ++h)
-      d[h] = ldg_nt(base + l.off0 + h * kRow);
+    for (int h = 0; h < kRows; ++h) d[h] = ldg_nt(base + l.off0 + h * kRow);
   } else {
 #pragma unroll
     for (int h = 0; h < kRows; ++h) {
@@ -178,8 +212,8 @@ __device__ __forceinline__ void load_chunk(const uint8_t *__restrict__ base,
   }
 }
 
-// Store the first `len` bytes of a chunk held in registers (pieces that start
-// below len are stored whole; their bytes past len are zero in registers).
+// Store the first `len` bytes of a wave's rows (pieces that start below len
+// are stored whole when pad_ok; their bytes past len are zero).
 __device__ __forceinline__ void store_chunk(uint8_t *__restrict__ base,
                                             uint32_t len, const Lane &l,
                                             const uint4 (&d)[kRows],
@@ -197,17 +231,10 @@ __device__ __forceinline__ void store_chunk(uint8_t *__restrict__ base,
   }
 }
 
-// Wave-level CRC value Q of the wave's 8 KiB (valid in lane 0).
-__device__ __forceinline__ uint32_t wave_q(const uint4 (&d)[kRows],
-                                           const GLane &gl) {
-  uint32_t v0 = 0, v1 = 0, v2 = 0, v3 = 0;
-#pragma unroll
-  for (int h = 0; h < kRows; ++h) {
-    v0 = g_step(v0 ^ d[h].x, gl);
-    v1 = g_step(v1 ^ d[h].y, gl);
-    v2 = g_step(v2 ^ d[h].z, gl);
-    v3 = g_step(v3 ^ d[h].w, gl);
-  }
+// Lane merge of the four column states and the 6-level lane tree; the wave
+// value Q is valid in lane 0.
+__device__ __forceinline__ uint32_t lane_tree(uint32_t v0, uint32_t v1, uint32_t v2,
+                                              uint32_t v3) {
   // u = F^12 v0 ^ F^8 v1 ^ F^4 v2 ^ v3
   uint32_t u = tab4(kLdsF8, tab4(kLdsF4, v0) ^ v1) ^ tab4(kLdsF4, v2) ^ v3;
 #pragma unroll
@@ -219,25 +246,24 @@ __device__ __forceinline__ uint32_t wave_q(const uint4 (&d)[kRows],
   return u;
 }
 
-// Whole-workgroup chunk CRC.  Contains two barriers; the result is valid in
-// thread 0 only.
-__device__ __forceinline__ uint32_t chunk_crc(const uint4 (&d)[kRows],
-                                              const GLane &gl, const Lane &l,
-                                              uint32_t len, const ChunkGeom &g,
-                                              const CrcTables &T) {
-  uint32_t q = wave_q(d, gl);
-  if (l.lane == 0) misc()[M_PART + l.wave] = mat_apply(T.wave_mat[l.wave], q);
-  __syncthreads();
-  uint32_t crc = 0;
-  if (threadIdx.x == 0) {
-    uint32_t raw = 0;
+// Wave-level CRC value Q of the wave's 8 rows (valid in lane 0).
+__device__ __forceinline__ uint32_t wave_q(const uint4 (&d)[kRows],
+                                           const GLane &gl) {
+  uint32_t v0 = 0, v1 = 0, v2 = 0, v3 = 0;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) raw ^= misc()[M_PART + w];
-    crc = (len == kChunk) ? raw ^ T.k_full
-                          : mat_apply(g.tail_mat, raw) ^ g.k_tail;
+  for (int h = 0; h < kRows; ++h) {
+    v0 = g_step(v0 ^ d[h].x, gl);
+    v1 = g_step(v1 ^ d[h].y, gl);
+    v2 = g_step(v2 ^ d[h].z, gl);
+    v3 = g_step(v3 ^ d[h].w, gl);
   }
-  __syncthreads();
-  return crc;
+  return lane_tree(v0, v1, v2, v3);
+}
+
+// Chunk CRC from the raw (zero-init, padded) value of the whole chunk.
+__device__ __forceinline__ uint32_t finish_crc(uint32_t raw, uint32_t len,
+                                               const ChunkGeom &g, const CrcTables &T) {
+  return len == kChunk ? raw ^ T.k_full : mat_apply(g.tail_mat, raw) ^ g.k_tail;
 }
 
 // -------------------------------------------------------------- checksum --
@@ -254,11 +280,19 @@ __global__ __launch_bounds__(kThreads) void k_checksum(
   uint4 d[kRows];
   if (c < g.n_chunks) load_chunk(data + (uint64_t)c * kChunk, chunk_len(g, c), l, d);
   while (c < g.n_chunks) {
-    uint32_t cn = c + gridDim.x;
+    const uint32_t cn = c + gridDim.x;
     uint4 dn[kRows];
     if (cn < g.n_chunks) load_chunk(data + (uint64_t)cn * kChunk, chunk_len(g, cn), l, dn);
-    uint32_t crc = chunk_crc(d, gl, l, chunk_len(g, c), g, T);
-    if (threadIdx.x == 0) crc_out[c] = crc;
+    const uint32_t q = wave_q(d, gl);
+    if (l.lane == 0) misc()[M_PART + l.wave] = mat_apply(T.wave_mat[l.wave], q);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t raw = 0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) raw ^= misc()[M_PART + w];
+      crc_out[c] = finish_crc(raw, chunk_len(g, c), g, T);
+    }
+    __syncthreads();
 #pragma unroll
     for (int h = 0; h < kRows; ++h) d[h] = dn[h];
     c = cn;
@@ -406,11 +440,27 @@ __global__ __launch_bounds__(1024) void k_compact(const uint32_t *__restrict__ f
   if (threadIdx.x == 0) *count = carry;
 }
 
+
 // ---------------------------------------------------------------- encode --
+//
+// One 576-thread workgroup per CU: 8 data waves hold a chunk in registers
+// (8 rows each) and a dedicated control wave owns everything that waits on
+// global memory other than the data itself (tickets, the decoupled
+// look-back of record offsets, the plan, headers).  Per chunk:
+//   data   : prefetch next chunk | CRC streams | exponent histogram  [B1]
+//            reduce histogram                                         [B2]
+//            clear histogram                                          [B3]
+//            k-bit codes into LDS, escape flags                       [B4]
+//            write sign/mantissa plane, codes, escape index, escapes
+//   control:                                                          [B1]
+//                                                                     [B2]
+//            chunk CRC, plan, publish aggregate, first look-back read [B3]
+//            finish look-back, publish prefix, header, table entry    [B4]
 
 constexpr int kModeList = 0, kModeAll = 1, kModeStep = 2;
 constexpr uint64_t kFlagAgg = 1, kFlagIncl = 2;
 constexpr uint32_t kLookbackWindow = 256;  // predecessors read per round trip
+constexpr int kEncThreads = kThreads + 64;
 
 struct EncArgs {
   const uint8_t *cur;
@@ -426,28 +476,28 @@ struct EncArgs {
   int mode;
 };
 
-// Encoder LDS beyond the CRC tables.
 struct EncShared {
   uint32_t part[kWaves];     // wave CRC partials
   uint32_t dirty_w[kWaves];  // per-wave "differs from prev"
   uint32_t esc_w[kWaves];    // escapes per wave
-  uint32_t mode, k, base, n_esc, size, crc, dirty, pad0;
-  uint32_t rec_idx, off_lo, off_hi, ticket;
+  uint32_t mode, k, base, n_esc, size, dirty, crc;
+  uint32_t first, next;      // tickets
+  uint32_t off_lo, off_hi;   // record offset
   uint32_t H[256];           // histogram
   uint32_t P[260];           // exclusive prefix of H (P[256] = n)
 };
 static_assert(sizeof(EncShared) <= kLdsMiscBytes, "encoder scratch fits");
 constexpr uint32_t kLdsHistE = kLdsMisc + kLdsMiscBytes;  // 256 bins x 16 copies
-constexpr uint32_t kLdsStage = kLdsHistE + 16384;         // code staging
-constexpr uint32_t kLdsStageBytes = 7 * (kChunk / 2) / 8;
+constexpr uint32_t kLdsStage = kLdsHistE + 16384;         // record body staging
+// codes + escape index + escapes of a chosen packed record: the plan only
+// packs when the record is smaller than RAW, so they stay below half a chunk
+constexpr uint32_t kLdsStageBytes = kChunk / 2;
 constexpr uint32_t kLdsEncode = kLdsStage + kLdsStageBytes;
 static_assert(kLdsEncode <= 163840, "encoder LDS fits one CU");
 
 __device__ __forceinline__ EncShared &enc_shared() {
   return *reinterpret_cast<EncShared *>(lds + kLdsMisc);
 }
-
-__device__ __forceinline__ uint64_t pad16(uint64_t x) { return (x + 15u) & ~15ull; }
 
 __device__ __forceinline__ void status_store(uint64_t *p, uint64_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -457,34 +507,12 @@ __device__ __forceinline__ uint64_t status_load(const uint64_t *p) {
                            __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ uint32_t lanes_below(unsigned long long m) {
-  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                   __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-}
-
-// Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts and row
-// broadcasts).
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);
-  return v;
-}
-__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, 64));
-  return v;
-}
-
 typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+// Per 16-bit half: min((e - base) mod 2^16, esc).
 __device__ __forceinline__ uint32_t pk_sub_min(uint32_t ex, uint32_t base2, uint32_t esc2) {
   u16x2 a = __builtin_bit_cast(u16x2, ex), b = __builtin_bit_cast(u16x2, base2);
   u16x2 e = __builtin_bit_cast(u16x2, esc2);
-  u16x2 d = a - b;
-  return __builtin_bit_cast(uint32_t, __builtin_elementwise_min(d, e));
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_min(a - b, e));
 }
 
 // The 8 sign/mantissa bytes of a 16-byte piece: byte u = (w_u >> 8 & 0x80) |
@@ -494,10 +522,8 @@ __device__ __forceinline__ uint2 sm_bytes(const uint4 &x) {
   uint32_t s1 = (x.y & 0x007F007Fu) | ((x.y >> 8) & 0x00800080u);
   uint32_t s2 = (x.z & 0x007F007Fu) | ((x.z >> 8) & 0x00800080u);
   uint32_t s3 = (x.w & 0x007F007Fu) | ((x.w >> 8) & 0x00800080u);
-  // gather bytes 0 and 2 of each word pair
-  uint32_t lo = __builtin_amdgcn_perm(s1, s0, 0x06040200u);
-  uint32_t hi = __builtin_amdgcn_perm(s3, s2, 0x06040200u);
-  return make_uint2(lo, hi);
+  return make_uint2(__builtin_amdgcn_perm(s1, s0, 0x06040200u),
+                    __builtin_amdgcn_perm(s3, s2, 0x06040200u));
 }
 
 // Chunk of a work item; a caller's list must be ascending and in range, a
@@ -510,10 +536,10 @@ __device__ __forceinline__ uint32_t item_chunk(const EncArgs &a, uint32_t item,
   return c;
 }
 
-// Look-back (wave 0).  The first window is loaded by lookback_issue before
-// other work; lookback_finish consumes it and reads further windows only if
-// needed.  Every item publishes its aggregate before its own look-back and
-// tickets are handed out in order to running workgroups, so each
+// Look-back (control wave).  lookback_issue reads a window of predecessors
+// before other work; lookback_finish consumes it and reads further windows
+// only if needed.  Every item publishes its aggregate before its own
+// look-back and tickets go to running workgroups in order, so each
 // predecessor publishes eventually; the spin bound only guarantees that the
 // kernel terminates if that were ever violated (the call then reports an
 // empty payload).
@@ -540,7 +566,7 @@ __device__ uint64_t lookback_finish(const uint64_t *status, int64_t top, Window 
   uint32_t spins = 0;
   while (top >= 0) {
     // distance of an entry from `top` is lane*Q + q
-    uint32_t first = 0xFFFFFFFFu;  // nearest inclusive distance held by this lane
+    uint32_t first = 0xFFFFFFFFu;
 #pragma unroll
     for (int q = Q - 1; q >= 0; --q)
       if ((w.s[q] & 3u) == kFlagIncl) first = lane * Q + q;
@@ -576,81 +602,155 @@ __device__ uint64_t lookback_finish(const uint64_t *status, int64_t top, Window 
   return excl;
 }
 
+// k-bit codes of the data wave's 8 rows into LDS staging; escape flags per
+// row (8 bits each) and each row's escape count before it within the wave.
+template <uint32_t K>
+__device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &l,
+                                           uint32_t n_words, bool full, uint32_t base,
+                                           uint8_t *stage, uint32_t (&escm)[2],
+                                           uint32_t (&row_base)[kRows], uint32_t &wave_esc) {
+  constexpr uint32_t esc = (1u << K) - 1u;
+  constexpr uint32_t esc2 = esc | (esc << 16);
+  const uint32_t base2 = base | (base << 16);
+#pragma unroll
+  for (int h = 0; h < kRows; ++h) {
+    const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+    const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
+    uint32_t lo[4], hi[4];
+    uint32_t flags = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t cp = pk_sub_min((x[j] >> 7) & 0x00FF00FFu, base2, esc2);
+      lo[j] = cp & 0xFFFFu;
+      hi[j] = cp >> 16;
+      if (!full) {  // words past the chunk code as 0 and never escape
+        if (w0 + 2 * j >= n_words) lo[j] = 0;
+        if (w0 + 2 * j + 1 >= n_words) hi[j] = 0;
+      }
+      flags |= (lo[j] == esc ? 1u : 0u) << (2 * j);
+      flags |= (hi[j] == esc ? 1u : 0u) << (2 * j + 1);
+    }
+    if (!full) {
+      const uint32_t valid = w0 >= n_words ? 0u : (n_words - w0 >= 8 ? 8u : n_words - w0);
+      flags &= (1u << valid) - 1u;
+    }
+    if (w0 < n_words) {
+      uint8_t *at = stage + (w0 >> 3) * K;
+      if constexpr (K * 8 <= 32) {
+        uint32_t p = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) p |= (lo[j] << (2 * j * K)) | (hi[j] << ((2 * j + 1) * K));
+        if constexpr (K == 4) *reinterpret_cast<uint32_t *>(at) = p;
+        else if constexpr (K == 2) *reinterpret_cast<uint16_t *>(at) = (uint16_t)p;
+        else if constexpr (K == 1) *at = (uint8_t)p;
+        else {
+#pragma unroll
+          for (uint32_t b = 0; b < K; ++b) at[b] = (uint8_t)(p >> (8 * b));
+        }
+      } else {
+        uint64_t p = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          p |= ((uint64_t)lo[j] << (2 * j * K)) | ((uint64_t)hi[j] << ((2 * j + 1) * K));
+        if constexpr (K == 6) {
+#pragma unroll
+          for (uint32_t b = 0; b < 3; ++b)
+            reinterpret_cast<uint16_t *>(at)[b] = (uint16_t)(p >> (16 * b));
+        } else {
+#pragma unroll
+          for (uint32_t b = 0; b < K; ++b) at[b] = (uint8_t)(p >> (8 * b));
+        }
+      }
+    }
+    const uint32_t cnt = __popc(flags);
+    const uint32_t incl = wave_incl_scan(cnt);
+    row_base[h] = wave_esc;
+    wave_esc += __builtin_amdgcn_readlane(incl, 63);
+    escm[h >> 2] |= flags << (8 * (h & 3));
+  }
+}
+
 template <bool HAS_PREV>
-__global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
+__global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(a.ws + a.L.ctl);
   uint64_t *status = reinterpret_cast<uint64_t *>(a.ws + a.L.status);
   uint4 *tab_ws = reinterpret_cast<uint4 *>(a.ws + a.L.table);
   uint32_t *ecrc = reinterpret_cast<uint32_t *>(a.ws + a.L.entry_crc);
-  const uint32_t n_items = a.mode == kModeList ? min(*a.n_idx, g.n_chunks) : g.n_chunks;
+  const uint32_t n_items =
+      uniform(a.mode == kModeList ? min(*a.n_idx, g.n_chunks) : g.n_chunks);
   const bool need_crc = a.crc_in == nullptr;
+  const bool is_ctl = threadIdx.x >= (uint32_t)kThreads;
 
   load_crc_tables(g.crc_kind);
   const CrcTables &T = g_tables[g.crc_kind];
-  const GLane gl = glane_make();
-  const Lane l = lane_info();
   EncShared &sh = enc_shared();
   uint8_t *stage = lds + kLdsStage;
   uint32_t *hist = reinterpret_cast<uint32_t *>(lds + kLdsHistE);
-  const uint32_t copy4 = (threadIdx.x & 15u) * 4u;
   {
     uint4 *h4 = reinterpret_cast<uint4 *>(hist);
-    for (uint32_t i = threadIdx.x; i < 1024u; i += kThreads) h4[i] = make_uint4(0, 0, 0, 0);
+    for (uint32_t i = threadIdx.x; i < 1024u; i += kEncThreads) h4[i] = make_uint4(0, 0, 0, 0);
   }
-  if (threadIdx.x == 0) {
-    sh.rec_idx = atomicAdd(&ctl->ticket, 1u);
-    sh.ticket = atomicAdd(&ctl->ticket, 1u);
-  }
-  __syncthreads();
-  uint32_t item = sh.rec_idx;
-  uint32_t next = sh.ticket;
-  uint4 d[kRows];
-  if (item < n_items) {
-    uint32_t c = item_chunk(a, item, g);
-    if (c < g.n_chunks) load_chunk(a.cur + (uint64_t)c * kChunk, chunk_len(g, c), l, d);
+  if (threadIdx.x == (uint32_t)kThreads) {
+    sh.first = atomicAdd(&ctl->ticket, 1u);
+    sh.next = atomicAdd(&ctl->ticket, 1u);
   }
   __syncthreads();
+  uint32_t item = uniform(sh.first);
+  uint32_t next = uniform(sh.next);
 
+  // data-wave state
+  const GLane gl = glane_make();
+  const Lane l0 = lane_info();
+  uint4 d[kRows];
+  if (!is_ctl && item < n_items) {
+    const uint32_t c = uniform(item_chunk(a, item, g));
+    if (c < g.n_chunks) load_chunk(a.cur + (uint64_t)c * kChunk, chunk_len(g, c), l0, d);
+  }
   while (item < n_items) {
-    // ---- 1. prefetch the next chunk; prev of this chunk; next ticket
-    uint4 dn[kRows];
-    if (next < n_items) {
-      uint32_t cn = item_chunk(a, next, g);
-      if (cn < g.n_chunks) load_chunk(a.cur + (uint64_t)cn * kChunk, chunk_len(g, cn), l, dn);
-    }
-    uint32_t c = item_chunk(a, item, g);
+    Window win;           // control wave: look-back window in flight
+    uint32_t ticket = 0;  // control wave: the ticket after `next`
+    const Lane l = lane_fresh(l0);
+    const uint32_t copy4 = (l.lane & 15u) * 4u;
+    uint32_t c = uniform(item_chunk(a, item, g));
     const bool bad_index = c >= g.n_chunks;
     if (bad_index) c = 0;
     const uint32_t len = bad_index ? 0u : chunk_len(g, c);
     const uint32_t n_words = len / 2;
-    uint4 p[kRows];
-    if (HAS_PREV && !bad_index) load_chunk(a.prev + (uint64_t)c * kChunk, len, l, p);
-    uint32_t ticket = 0;
-    if (threadIdx.x == 0) ticket = atomicAdd(&ctl->ticket, 1u);
+    const bool full = len == kChunk;
+    uint4 dn[kRows];
 
-    // ---- 2. CRC (and the diff against prev)
-    if (need_crc) {
-      uint32_t q = wave_q(d, gl);
-      if (l.lane == 0) sh.part[l.wave] = mat_apply(T.wave_mat[l.wave], q);
+    // ---- data: prefetch, CRC streams, diff
+    if (!is_ctl) {
+      uint4 p[kRows];
+      if (HAS_PREV && !bad_index) load_chunk(a.prev + (uint64_t)c * kChunk, len, l, p);
+      if (next < n_items) {
+        const uint32_t cn = uniform(item_chunk(a, next, g));
+        if (cn < g.n_chunks) load_chunk(a.cur + (uint64_t)cn * kChunk, chunk_len(g, cn), l, dn);
+      }
+      if (need_crc) {
+        const uint32_t q = wave_q(d, gl);
+        if (l.lane == 0) sh.part[l.wave] = mat_apply(T.wave_mat[l.wave], q);
+      }
+      if (HAS_PREV) {
+        uint32_t diff = 0;
+#pragma unroll
+        for (int h = 0; h < kRows; ++h)
+          diff |= (d[h].x ^ p[h].x) | (d[h].y ^ p[h].y) | (d[h].z ^ p[h].z) | (d[h].w ^ p[h].w);
+        const unsigned long long any = __ballot(diff != 0);
+        if (l.lane == 0) sh.dirty_w[l.wave] = (any && !bad_index) ? 1u : 0u;
+      }
     }
     bool dirty = !bad_index;
     if (HAS_PREV) {
-      uint32_t diff = 0;
-#pragma unroll
-      for (int h = 0; h < kRows; ++h)
-        diff |= (d[h].x ^ p[h].x) | (d[h].y ^ p[h].y) | (d[h].z ^ p[h].z) | (d[h].w ^ p[h].w);
-      unsigned long long any = __ballot(diff != 0);
-      if (l.lane == 0) sh.dirty_w[l.wave] = any ? 1u : 0u;
-      __syncthreads();
+      __syncthreads();  // B0: per-wave diff flags
       uint32_t dw = 0;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) dw |= sh.dirty_w[w];
-      dirty = dirty && dw != 0;
+      dirty = uniform(dw) != 0;
     }
 
-    // ---- 3. exponent histogram (16 copies x 256 bins)
-    const bool full = len == kChunk;
-    if (dirty) {
+    // ---- data: exponent histogram (16 copies x 256 bins)
+    if (!is_ctl && dirty) {
 #pragma unroll
       for (int h = 0; h < kRows; ++h) {
         const uint32_t w0 = (l.off0 + h * kRow) >> 1;
@@ -662,42 +762,37 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
           if (full || w0 + 2 * j + 1 < n_words)
             atomicAdd(reinterpret_cast<uint32_t *>(lds + kLdsHistE + (((x[j] >> 17) & 0x3FC0u) | copy4)), 1u);
         }
-        __builtin_amdgcn_sched_barrier(0);
       }
     }
-    __syncthreads();  // B1: histogram and CRC partials complete
+    __syncthreads();  // B1: histogram copies and CRC partials complete
 
-    // ---- 4. histogram reduce (all waves, 32 bins each)
-    if (dirty) {
+    // ---- data: reduce the copies, 32 bins per wave
+    if (!is_ctl && dirty) {
       const uint32_t bin = l.wave * 32u + (l.lane >> 1), half = l.lane & 1u;
       uint32_t s = 0;
 #pragma unroll
-      for (int cc = 0; cc < 8; ++cc) {
-        uint32_t cp = (half * 8u + ((cc + (l.lane >> 1)) & 7u));
-        s += hist[bin * 16u + cp];
-      }
-      s += __shfl_xor((int)s, 1, 64);
+      for (int cc = 0; cc < 8; ++cc) s += hist[bin * 16u + half * 8u + ((cc + (l.lane >> 1)) & 7u)];
+      s += (uint32_t)__shfl_xor((int)s, 1, 64);
       if (half == 0) sh.H[bin] = s;
     }
-    __syncthreads();  // B2: H complete; the histogram copies are free
+    __syncthreads();  // B2: H complete
 
-    // ---- 5. wave 0: chunk CRC, plan, aggregate, first look-back window
-    Window win;
-    if (l.wave == 0) {
-      uint32_t crc = 0;
+    if (is_ctl) {
+      // ---- control: chunk CRC, plan, aggregate, first look-back window
+      if (l.lane == 0) ticket = atomicAdd(&ctl->ticket, 1u);  // handed out after B4
+      uint32_t crc;
       if (need_crc) {
         uint32_t raw = 0;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) raw ^= sh.part[w];
-        crc = bad_index ? 0u : (full ? raw ^ T.k_full : mat_apply(g.tail_mat, raw) ^ g.k_tail);
+        crc = bad_index ? 0u : finish_crc(raw, len, g, T);
       } else {
         crc = a.crc_in[c];
       }
       uint32_t mode = 0, k = 0, base = 0, n_esc = 0;
       uint64_t size = 0;
       if (dirty) {
-        // exclusive prefix P over the 256 bins (4 per lane)
-        const uint32_t b0 = l.lane * 4u;
+        const uint32_t lane = l.lane, b0 = lane * 4u;
         const uint32_t h0 = sh.H[b0], h1 = sh.H[b0 + 1], h2 = sh.H[b0 + 2], h3 = sh.H[b0 + 3];
         const uint32_t t4 = h0 + h1 + h2 + h3;
         const uint32_t ex = wave_incl_scan(t4) - t4;
@@ -705,53 +800,49 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
         sh.P[b0 + 1] = ex + h0;
         sh.P[b0 + 2] = ex + h0 + h1;
         sh.P[b0 + 3] = ex + h0 + h1 + h2;
-        if (l.lane == 63u) sh.P[256] = ex + t4;
-        const uint32_t nzmask = (h0 ? 1u : 0u) | (h1 ? 2u : 0u) | (h2 ? 4u : 0u) | (h3 ? 8u : 0u);
-        const uint32_t distinct = wave_incl_scan(__popc(nzmask));
-        const uint32_t n_distinct = __builtin_amdgcn_readlane(distinct, 63);
-        const uint32_t only = wave_max(nzmask ? b0 + 31u - __clz(nzmask) : 0u);
+        if (lane == 63u) sh.P[256] = ex + t4;
+        const uint32_t nz = (h0 ? 1u : 0u) | (h1 ? 2u : 0u) | (h2 ? 4u : 0u) | (h3 ? 8u : 0u);
+        const uint32_t n_distinct = __builtin_amdgcn_readlane(wave_incl_scan(__popc(nz)), 63);
+        const uint32_t only = wave_max(nz ? b0 + 31u - __clz(nz) : 0u);
         const uint64_t n = n_words;
         // candidates: lane 0 RAW, lane 1 k=0, lanes 2..8 k = lane-1
         uint64_t cand = ~0ull;
         uint32_t c_base = 0, c_esc = 0;
-#pragma unroll
+#pragma unroll 1
         for (uint32_t kk = 1; kk <= 7; ++kk) {
-          const uint32_t win_w = (1u << kk) - 1u;
+          const uint32_t width = (1u << kk) - 1u;
           uint32_t key = 0;
 #pragma unroll
           for (uint32_t j = 0; j < 4; ++j) {
-            uint32_t b = b0 + j;
-            uint32_t end = min(b + win_w, 256u);
-            uint32_t inside = sh.P[end] - sh.P[b];
+            const uint32_t b = b0 + j;
+            const uint32_t inside = sh.P[min(b + width, 256u)] - sh.P[b];
             key = max(key, (inside << 8) | (255u - b));
           }
           key = wave_max(key);
-          if (l.lane == kk + 1) {
-            uint32_t inside = key >> 8;
+          if (lane == kk + 1) {
             c_base = 255u - (key & 255u);
-            c_esc = n_words - inside;
+            c_esc = n_words - (key >> 8);
             cand = 16u + pad16((n * kk + 7) / 8) + pad16(2 * ((n + 511) / 512)) + pad16(c_esc) +
                    pad16(n);
           }
         }
-        if (l.lane == 0) cand = 16u + pad16(2 * n);
-        if (l.lane == 1 && n_distinct == 1) {
+        if (lane == 0) cand = 16u + pad16(2 * n);
+        if (lane == 1 && n_distinct == 1) {
           cand = 16u + pad16(n);
           c_base = only;
         }
-        // smallest size, then lowest lane
-        uint64_t key = (cand << 8) | l.lane;
+        uint64_t key = (cand << 8) | lane;  // smallest size, then lowest lane
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) {
-          uint64_t y = __shfl_xor(key, o, 64);
+          const uint64_t y = __shfl_xor(key, o, 64);
           key = y < key ? y : key;
         }
         const uint32_t win_lane = (uint32_t)(key & 255u);
         size = key >> 8;
         mode = win_lane == 0 ? 0u : 1u;
         k = win_lane <= 1 ? 0u : win_lane - 1u;
-        base = __shfl((int)c_base, (int)win_lane, 64);
-        n_esc = __shfl((int)c_esc, (int)win_lane, 64);
+        base = (uint32_t)__shfl((int)c_base, (int)win_lane, 64);
+        n_esc = (uint32_t)__shfl((int)c_esc, (int)win_lane, 64);
       }
       const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((size >> 4) << 26);
       if (l.lane == 0) {
@@ -761,178 +852,140 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a, ChunkGeom g) {
         sh.base = base;
         sh.n_esc = n_esc;
         sh.size = (uint32_t)size;
-        sh.crc = crc;
         sh.dirty = dirty ? 1u : 0u;
+        sh.crc = crc;
       }
       win = lookback_issue(status, (int64_t)item - 1);
-    }
-    __syncthreads();  // B3: plan known
-
-    // ---- 6. codes into staging, escape counts, sign/mantissa bytes
-    const uint32_t mode = sh.mode, k = sh.k, base = sh.base, n_esc = sh.n_esc;
-    dirty = sh.dirty != 0;
-    const bool pack = dirty && mode == 1u && k > 0u;
-    const uint32_t esc_code = (1u << k) - 1u;
-    const uint32_t base2 = base | (base << 16), esc2 = esc_code | (esc_code << 16);
-    uint32_t escm[2] = {0, 0};      // escape flags, 8 bits per row
-    uint32_t row_base[kRows];      // escapes in earlier rows of this wave
-    uint32_t wave_esc = 0;
-    if (pack) {
-      if (!full) {
-        uint4 *s4 = reinterpret_cast<uint4 *>(stage);
-        for (uint32_t i = threadIdx.x; i < kLdsStageBytes / 16; i += kThreads)
-          s4[i] = make_uint4(0, 0, 0, 0);
-        __syncthreads();
-      }
-#pragma unroll
-      for (int h = 0; h < kRows; ++h) {
-        const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-        const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
-        uint32_t cp[4];
-        uint32_t flags = 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          cp[j] = pk_sub_min((x[j] >> 7) & 0x00FF00FFu, base2, esc2);
-          if (!full) {  // words past the chunk code as 0, never escape
-            if (w0 + 2 * j >= n_words) cp[j] &= 0xFFFF0000u;
-            if (w0 + 2 * j + 1 >= n_words) cp[j] &= 0x0000FFFFu;
-          }
-          uint32_t lo = cp[j] & 0xFFFFu, hi = cp[j] >> 16;
-          bool vlo = full || w0 + 2 * j < n_words, vhi = full || w0 + 2 * j + 1 < n_words;
-          flags |= ((vlo && lo == esc_code) ? 1u : 0u) << (2 * j);
-          flags |= ((vhi && hi == esc_code) ? 1u : 0u) << (2 * j + 1);
-        }
-        // 8 codes of k bits
-        uint64_t packed = 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          uint64_t pair = (uint64_t)(cp[j] & 0xFFFFu) | ((uint64_t)(cp[j] >> 16) << k);
-          packed |= pair << (2 * j * k);
-        }
-        if (w0 < n_words) {
-          const uint32_t at = (w0 >> 3) * k;
-          if (k == 4u) {
-            *reinterpret_cast<uint32_t *>(stage + at) = (uint32_t)packed;
-          } else if (k == 2u) {
-            *reinterpret_cast<uint16_t *>(stage + at) = (uint16_t)packed;
-          } else if (k == 1u) {
-            stage[at] = (uint8_t)packed;
-          } else {
-            for (uint32_t b = 0; b < k; ++b) stage[at + b] = (uint8_t)(packed >> (8 * b));
-          }
-        }
-        const uint32_t cnt = __popc(flags);
-        const uint32_t incl = wave_incl_scan(cnt);
-        row_base[h] = wave_esc;
-        wave_esc += __builtin_amdgcn_readlane(incl, 63);
-        escm[h >> 2] |= flags << (8 * (h & 3));
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      if (l.lane == 0) sh.esc_w[l.wave] = wave_esc;
-    }
-    // zero the histogram copies for the next chunk
-    {
+    } else if (dirty) {
+      // ---- data: clear the copies for the next chunk
       uint4 *h4 = reinterpret_cast<uint4 *>(hist);
       for (uint32_t i = threadIdx.x; i < 1024u; i += kThreads) h4[i] = make_uint4(0, 0, 0, 0);
     }
-    // wave 0: finish the look-back, publish the inclusive prefix
-    if (l.wave == 0) {
+    __syncthreads();  // B3: plan known
+
+    const uint32_t mode = uniform(sh.mode), k = uniform(sh.k), base = uniform(sh.base);
+    const uint32_t n_esc = uniform(sh.n_esc);
+    const bool pack = dirty && mode == 1u && k > 0u;
+    uint32_t escm[2] = {0, 0};
+    uint32_t row_base[kRows];
+    if (is_ctl) {
+      // ---- control: offset, header, table entry
+      const uint32_t crc = uniform(sh.crc);
       const uint64_t excl = lookback_finish(status, (int64_t)item - 1, win, ctl);
+      const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(sh.size >> 4) << 26);
+      const uint64_t incl = excl + (agg >> 2);
+      const uint32_t rec_idx = (uint32_t)(excl & 0xFFFFFFu);
+      const uint64_t rec_off = 64u + ((excl >> 24) << 4);
+      uint32_t hw[4] = {mode | (k << 8) | (base << 16), n_words, n_esc, 0};
+      hw[3] = crc_words(hw, 3);
+      uint32_t ew[4] = {c, crc, (uint32_t)rec_off, (uint32_t)(rec_off >> 32)};
+      const uint32_t eck = crc_words(ew, 4);
       if (l.lane == 0) {
-        const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(sh.size >> 4) << 26);
-        const uint64_t incl = excl + (agg >> 2);
         status_store(&status[item], (incl << 2) | kFlagIncl);
         if (item + 1 == n_items) {
           ctl->n_rec = (uint32_t)(incl & 0xFFFFFFu);
           ctl->payload_bytes = (incl >> 24) << 4;  // total record bytes
         }
-        sh.rec_idx = (uint32_t)(excl & 0xFFFFFFu);
-        const uint64_t off = 64u + ((excl >> 24) << 4);
-        sh.off_lo = (uint32_t)off;
-        sh.off_hi = (uint32_t)(off >> 32);
-        sh.ticket = ticket;
         if (bad_index) atomicOr(&ctl->error, 2u);
+        sh.off_lo = (uint32_t)rec_off;
+        sh.off_hi = (uint32_t)(rec_off >> 32);
+        sh.next = ticket;
+        if (dirty) {
+          *reinterpret_cast<uint4 *>(a.payload + rec_off) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+          tab_ws[rec_idx] = make_uint4(ew[0], ew[1], ew[2], ew[3]);
+          ecrc[rec_idx] = eck;
+          if (a.dirty_idx) a.dirty_idx[rec_idx] = c;
+        }
+        if (a.crc_out && !bad_index) a.crc_out[c] = crc;
       }
+    } else if (pack) {
+      // ---- data: codes into staging, escape flags and counts
+      if (!full) {  // the wave's own code bytes; lanes past the chunk write none
+        uint4 *s4 = reinterpret_cast<uint4 *>(stage + l.wave * 512u * k);
+        for (uint32_t i = l.lane; i < 32u * k; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
+      }
+      uint32_t wave_esc = 0;
+      switch (k) {
+        case 1: pack_codes<1>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
+        case 2: pack_codes<2>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
+        case 3: pack_codes<3>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
+        case 4: pack_codes<4>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
+        case 5: pack_codes<5>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
+        case 6: pack_codes<6>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
+        default: pack_codes<7>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
+      }
+      if (l.lane == 0) sh.esc_w[l.wave] = wave_esc;
     }
     __syncthreads();  // B4: offset known, codes staged, escape totals known
 
-    // ---- 7. write the record
-    const uint32_t rec_idx = sh.rec_idx;
-    const uint64_t rec_off = (uint64_t)sh.off_lo | ((uint64_t)sh.off_hi << 32);
-    const uint32_t crc = sh.crc;
-    if (dirty) {
-      uint8_t *rec = a.payload + rec_off;
-      if (threadIdx.x == 0) {
-        uint32_t hw[4];
-        hw[0] = mode | (k << 8) | (base << 16);
-        hw[1] = n_words;
-        hw[2] = n_esc;
-        hw[3] = crc_words(hw, 3);
-        *reinterpret_cast<uint4 *>(rec) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-        uint32_t ew[4] = {c, crc, (uint32_t)rec_off, (uint32_t)(rec_off >> 32)};
-        tab_ws[rec_idx] = make_uint4(ew[0], ew[1], ew[2], ew[3]);
-        ecrc[rec_idx] = crc_words(ew, 4);
-        if (a.dirty_idx) a.dirty_idx[rec_idx] = c;
-      }
+    // ---- data: sign/mantissa plane to the payload; escape index and
+    // escapes into staging behind the codes
+    const uint64_t n = n_words;
+    const uint32_t code_bytes = (uint32_t)((n * k + 7) / 8);
+    const uint32_t n_blocks = k ? (n_words + 511u) / 512u : 0u;
+    const uint32_t s_idx = (uint32_t)pad16(code_bytes);          // staging offsets
+    const uint32_t s_esc = s_idx + (uint32_t)pad16(2 * n_blocks);
+    const uint32_t s_end = s_esc + (uint32_t)pad16(n_esc);
+    const uint64_t rec_off = (uint64_t)uniform(sh.off_lo) | ((uint64_t)uniform(sh.off_hi) << 32);
+    uint8_t *rec = a.payload + rec_off;
+    if (!is_ctl && dirty) {
       if (mode == 0) {
         store_chunk(rec + 16, len, l, d, true);
       } else {
-        const uint64_t n = n_words;
-        const uint64_t code_bytes = (n * k + 7) / 8;
-        const uint64_t n_blocks = k ? (n + 511) / 512 : 0;
-        const uint64_t idx_off = 16 + pad16(code_bytes);
-        const uint64_t esc_off = idx_off + pad16(2 * n_blocks);
-        const uint64_t sm_off = esc_off + pad16(n_esc);
-        for (uint32_t i = threadIdx.x; i < pad16(code_bytes) / 16; i += kThreads)
-          *reinterpret_cast<uint4 *>(rec + 16 + 16 * i) =
-              *reinterpret_cast<const uint4 *>(stage + 16 * i);
-        uint32_t wave_base = 0;
-        if (pack) {
-          for (uint32_t w = 0; w < l.wave; ++w) wave_base += sh.esc_w[w];
-        }
+        uint8_t *sm_at = rec + 16 + s_end;
 #pragma unroll
         for (int h = 0; h < kRows; ++h) {
           const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-          if (w0 < n_words) *reinterpret_cast<uint2 *>(rec + sm_off + w0) = sm_bytes(d[h]);
-          if (pack) {
-            // escape index entry of this row's 512-word block
-            if (l.lane == 0 && (w0 >> 9) < n_blocks)
-              *reinterpret_cast<uint16_t *>(rec + idx_off + 2 * (w0 >> 9)) =
+          if (w0 < n_words) *reinterpret_cast<uint2 *>(sm_at + w0) = sm_bytes(d[h]);
+        }
+        if (pack) {
+          uint32_t wave_base = 0;
+          for (uint32_t w = 0; w < l.wave; ++w) wave_base += sh.esc_w[w];
+          wave_base = uniform(wave_base);
+#pragma unroll
+          for (int h = 0; h < kRows; ++h) {
+            const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+            if (l.lane == 0 && w0 < n_words)  // this row is escape-index block w0/512
+              *reinterpret_cast<uint16_t *>(stage + s_idx + 2 * (w0 >> 9)) =
                   (uint16_t)(wave_base + row_base[h]);
             const uint32_t flags = (escm[h >> 2] >> (8 * (h & 3))) & 255u;
             const uint32_t cnt = __popc(flags);
-            const uint32_t lane_before = wave_incl_scan(cnt) - cnt;
+            uint32_t rank = wave_base + row_base[h] + wave_incl_scan(cnt) - cnt;
             if (flags) {
               const uint32_t xx[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
-              uint32_t rank = wave_base + row_base[h] + lane_before;
 #pragma unroll
               for (int u = 0; u < 8; ++u) {
                 if ((flags >> u) & 1u) {
-                  rec[esc_off + rank] = (uint8_t)((xx[u >> 1] >> (7 + 16 * (u & 1))) & 255u);
+                  stage[s_esc + rank] = (uint8_t)((xx[u >> 1] >> (7 + 16 * (u & 1))) & 255u);
                   ++rank;
                 }
               }
             }
           }
-          __builtin_amdgcn_sched_barrier(0);
         }
-        if (threadIdx.x < 16u) {
+        if (threadIdx.x < 16u) {  // zero padding of index, escapes and sm plane
           const uint32_t t = threadIdx.x;
-          if (2 * n_blocks + t < pad16(2 * n_blocks)) rec[idx_off + 2 * n_blocks + t] = 0;
-          if (n_esc + t < pad16(n_esc)) rec[esc_off + n_esc + t] = 0;
-          if (n + t < pad16(n)) rec[sm_off + n + t] = 0;
+          if (2 * n_blocks + t < s_esc - s_idx) stage[s_idx + 2 * n_blocks + t] = 0;
+          if (n_esc + t < s_end - s_esc) stage[s_esc + n_esc + t] = 0;
+          if (n_words + t < pad16(n)) sm_at[n_words + t] = 0;
         }
       }
     }
-    if (threadIdx.x == 0 && a.crc_out && !bad_index) a.crc_out[c] = crc;
-
+    __syncthreads();  // B5: staging complete
+    if (!is_ctl && dirty && mode == 1u) {
+      for (uint32_t i = threadIdx.x; i < s_end / 16u; i += kThreads)
+        *reinterpret_cast<uint4 *>(rec + 16 + 16 * i) =
+            *reinterpret_cast<const uint4 *>(stage + 16 * i);
+    }
+    if (!is_ctl) {
 #pragma unroll
-    for (int h = 0; h < kRows; ++h) d[h] = dn[h];
+      for (int h = 0; h < kRows; ++h) d[h] = dn[h];
+    }
     item = next;
-    next = sh.ticket;
-    __syncthreads();  // B5: scratch may be rewritten
+    next = uniform(sh.next);
   }
 }
+
 
 // Zero the control block and the look-back words before an encode.
 __global__ void k_encode_prepare(uint8_t *ws, WsLayout L, uint32_t n) {
@@ -994,6 +1047,7 @@ __global__ __launch_bounds__(256) void k_encode_finish(
   }
 }
 
+
 // ---------------------------------------------------------------- decode --
 
 __device__ __forceinline__ uint32_t ld_u32(const uint8_t *p) {
@@ -1004,7 +1058,7 @@ __device__ __forceinline__ uint64_t ld_u64(const uint8_t *p) {
 }
 
 // Header validation and control-block setup (one workgroup).
-__global__ __launch_bounds__(256) void k_decode_prepare(
+__global__ __launch_bounds__(64) void k_decode_prepare(
     const uint8_t *__restrict__ payload, uint64_t cap, ChunkGeom g,
     uint64_t staging_cap, uint8_t *ws, WsLayout L) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(ws + L.ctl);
@@ -1046,322 +1100,454 @@ __global__ __launch_bounds__(256) void k_decode_prepare(
   if (n_rec == 0 && total != 64u) ctl->table_bad = 1;
 }
 
-// One wave decodes one record with no barriers, so the 16 waves of a
-// workgroup overlap each other's memory latency.  Lane t owns bytes
-// [16t, 16t+16) of every 1 KiB row (one 512-word escape-index block); rows are
-// decoded in batches of 2 while the next batch's codes, sign/mantissa bytes
-// and escape bytes are already being fetched.
-constexpr int kDecWaves = 12;
-constexpr int kBatch = 2;                       // rows per batch
-constexpr uint32_t kEscPieces = 2;              // 16-byte escape pieces per lane
-constexpr uint32_t kEscStage = 64 * 16 * kEscPieces;  // escape staging per wave
-constexpr uint32_t kLdsDecStage = kLdsCrcEnd;
-constexpr uint32_t kLdsDecode = kLdsDecStage + kDecWaves * kEscStage;
-constexpr int kChunkRows = kChunk / kRow;       // 64
+// One 576-thread workgroup per CU, laid out like the encoder: 8 data waves
+// decode one record (wave w: rows 8w..8w+7, which are escape-index blocks
+// 8w..8w+7, so each wave finds its escapes from the index alone) while the
+// control wave validates the table entry, header, padding and index of the
+// record two steps ahead and publishes its layout in LDS.  Data waves hold
+// the current record in registers and have the next one's loads in flight
+// while they decode; the control wave also settles the previous record
+// (chunk CRC from the wave partials, status).
+constexpr int kDecThreads = kThreads + 64;
+constexpr uint32_t kDecEscBytes = 1024;  // escape window prefetched per data wave
+constexpr uint32_t kMetaSkip = 0xFFu;    // table entry rejected: no record status
+
+struct DecMeta {
+  uint32_t st;  // 0 decode, kMetaSkip, else the record's status
+  uint32_t mode, k, base, n_words, n_esc, c, src_crc, r;
+  uint32_t off_lo, off_hi, code_off, esc_off, sm_off;
+  uint32_t pad_[2];
+  uint32_t ent[68];  // escape index; entries from n_blocks on read n_esc
+};
+struct DecShared {
+  DecMeta meta[3];
+  uint32_t part[2][kWaves];  // wave CRC partials
+  uint32_t bad[2][kWaves];   // wave structure failures
+};
+static_assert(sizeof(DecShared) <= kLdsMiscBytes, "decoder scratch fits");
+constexpr uint32_t kLdsDecEsc = kLdsMisc + kLdsMiscBytes;
+constexpr uint32_t kLdsDecode = kLdsDecEsc + kWaves * kDecEscBytes;
 static_assert(kLdsDecode <= 163840, "decoder LDS fits one CU");
 
-__device__ __forceinline__ uint64_t load_codes(const uint8_t *codes, uint32_t grp, uint32_t k) {
-  uint64_t start = (uint64_t)grp * k;
-  uint64_t a4 = start & ~3ull;
-  const uint3 x = *reinterpret_cast<const uint3 *>(codes + a4);
-  uint32_t sh = (uint32_t)(start - a4) * 8u;
-  uint64_t lo = ((uint64_t)x.y << 32) | x.x;
-  return sh ? (lo >> sh) | ((uint64_t)x.z << (64 - sh)) : lo;
+__device__ __forceinline__ DecShared &dec_shared() {
+  return *reinterpret_cast<DecShared *>(lds + kLdsMisc);
 }
 
-__device__ __forceinline__ uint32_t wave_chunk_crc(uint32_t v0, uint32_t v1, uint32_t v2,
-                                                   uint32_t v3, uint32_t len,
-                                                   const ChunkGeom &g, const CrcTables &T) {
-  uint32_t u = tab4(kLdsF8, tab4(kLdsF4, v0) ^ v1) ^ tab4(kLdsF4, v2) ^ v3;
-#pragma unroll
-  for (int lv = 0; lv < kTree; ++lv) {
-    uint32_t s = tab4(kLdsTree + lv * 4096u, u);
-    uint32_t o = __shfl_down(u, 1u << lv, 64);
-    u = s ^ o;
+// Control wave: checks of table entry r and of its record, layout into M.
+__device__ void dec_prepare(const uint8_t *__restrict__ payload, uint64_t table_off,
+                            uint32_t n_rec, uint32_t r, const ChunkGeom &g,
+                            uint32_t *__restrict__ ecrc, WsCtl *ctl, DecMeta &M) {
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint8_t *e = payload + table_off + 16ull * r;
+  const uint4 ent = *reinterpret_cast<const uint4 *>(e);
+  const uint32_t c = ent.x;
+  const uint64_t off = (uint64_t)ent.z | ((uint64_t)ent.w << 32);
+  uint64_t end = table_off;
+  bool tbad = false;
+  if (r + 1 < n_rec) {
+    const uint4 nx = *reinterpret_cast<const uint4 *>(e + 16);
+    end = (uint64_t)nx.z | ((uint64_t)nx.w << 32);
+    tbad = nx.x <= c;
   }
-  uint32_t raw = mat_apply(T.unrow_mat, u);
-  return len == kChunk ? raw ^ T.k_full : mat_apply(g.tail_mat, raw) ^ g.k_tail;
+  {
+    uint32_t ew[4] = {ent.x, ent.y, ent.z, ent.w};
+    const uint32_t ec = crc_words(ew, 4);
+    if (lane == 0) ecrc[r] = ec;
+  }
+  tbad = tbad || c >= g.n_chunks || (r == 0 && off != 64u) || (off & 15u) || off >= end ||
+         end > table_off;
+  if (tbad) {
+    if (lane == 0) {
+      atomicOr(&ctl->table_bad, 1u);
+      M.st = kMetaSkip;
+    }
+    return;
+  }
+  const uint32_t len = chunk_len(g, c), n_words = len / 2;
+  const uint64_t reclen = end - off;
+  const uint8_t *rec = payload + off;
+  uint32_t st = 0, mode = 0, k = 0, base = 0, n_esc = 0;
+  uint64_t code_bytes = 0, n_blocks = 0, idx_off = 16, esc_off = 16, sm_off = 16;
+  if (reclen < 16) {
+    st = 4;
+  } else {
+    const uint4 h4 = *reinterpret_cast<const uint4 *>(rec);
+    uint32_t hw[4] = {h4.x, h4.y, h4.z, h4.w};
+    mode = hw[0] & 255u;
+    k = (hw[0] >> 8) & 255u;
+    base = (hw[0] >> 16) & 255u;
+    n_esc = hw[2];
+    code_bytes = ((uint64_t)n_words * k + 7) / 8;
+    n_blocks = k ? ((uint64_t)n_words + 511) / 512 : 0;
+    idx_off = 16 + pad16(code_bytes);
+    esc_off = idx_off + pad16(2 * n_blocks);
+    sm_off = esc_off + pad16(n_esc);
+    if (crc_words(hw, 3) != hw[3] || (hw[0] >> 24) || hw[1] != n_words || mode > 1) {
+      st = 4;
+    } else if (mode == 0) {
+      if (k || base || n_esc || reclen != 16u + pad16(2ull * n_words)) st = 4;
+    } else if (k > 7 || n_esc > n_words || (k == 0 && n_esc) ||
+               reclen != sm_off + pad16(n_words)) {
+      st = 4;
+    }
+  }
+  uint32_t entry = n_esc;
+  if (st == 0) {
+    bool bad = false;
+    if (mode == 0) {
+      const uint64_t at = 16u + 2ull * n_words + lane;
+      if (lane < 16u && at < 16u + pad16(2ull * n_words) && rec[at]) bad = true;
+    } else {
+      // padding: whole bytes after each section, code bits past n*k
+      if (lane < 16u) {
+        if (code_bytes + lane < pad16(code_bytes) && rec[16 + code_bytes + lane]) bad = true;
+        if (2 * n_blocks + lane < pad16(2 * n_blocks) && rec[idx_off + 2 * n_blocks + lane])
+          bad = true;
+        if (n_esc + lane < pad16(n_esc) && rec[esc_off + n_esc + lane]) bad = true;
+        if (n_words + lane < pad16(n_words) && rec[sm_off + n_words + lane]) bad = true;
+        const uint64_t used = (uint64_t)n_words * k;
+        if (lane == 0 && (used & 7u) && (rec[16 + used / 8] >> (used & 7u))) bad = true;
+      }
+      if (lane < n_blocks) entry = *reinterpret_cast<const uint16_t *>(rec + idx_off + 2 * lane);
+      if (lane == 0 && n_blocks && entry != 0) bad = true;  // the first block starts at 0
+    }
+    if (__ballot(bad)) st = 4;
+  }
+  M.ent[lane] = entry;
+  if (lane == 0) {
+    M.ent[64] = n_esc;
+    M.st = st;
+    M.mode = mode;
+    M.k = k;
+    M.base = base;
+    M.n_words = n_words;
+    M.n_esc = n_esc;
+    M.c = c;
+    M.src_crc = ent.y;
+    M.r = r;
+    M.off_lo = (uint32_t)off;
+    M.off_hi = (uint32_t)(off >> 32);
+    M.code_off = 16;
+    M.esc_off = (uint32_t)esc_off;
+    M.sm_off = (uint32_t)sm_off;
+  }
 }
 
-struct PackRec {
+// A data wave's share of a record: RAW rows in a[], or codes (a[].xyz) and
+// sign/mantissa bytes (b[]) plus the head of the wave's escape range (e).
+struct DecBuf {
+  uint4 a[kRows];
+  uint2 b[kRows];
+  uint4 e;
+};
+
+struct DecView {  // uniform fields of a record as a data wave needs them
   const uint8_t *rec;
-  uint64_t code_off, idx_off, esc_off, sm_off;
-  uint32_t k, base, n_esc, n_words, n_blocks, esc_code;
-  uint32_t blk;  // lane b holds escape-index entry b (lane n_blocks: n_esc)
+  uint32_t mode, k, base, n_words, n_esc, len;
+  uint32_t E0, Ee;  // the wave's escape range from the index
+  uint32_t al;      // 16-byte aligned start of the prefetched escape window
+  uint32_t esc_off, sm_off, r;
 };
 
-struct DecBatch {
-  uint3 code[kBatch];
-  uint2 sm[kBatch];
-  uint4 esc[kEscPieces];
-  uint32_t lo, lo_al, hi;
-};
-
-__device__ __forceinline__ uint32_t blk_at(const PackRec &R, uint32_t b) {
-  if (b >= R.n_blocks) return R.n_esc;
-  return (uint32_t)__shfl((int)R.blk, (int)b, 64);
+__device__ __forceinline__ DecView dec_view(const uint8_t *payload, const DecMeta &M,
+                                            const Lane &l, const ChunkGeom &g) {
+  DecView v;
+  const uint64_t off = (uint64_t)uniform(M.off_lo) | ((uint64_t)uniform(M.off_hi) << 32);
+  v.rec = payload + off;
+  v.mode = uniform(M.mode);
+  v.k = uniform(M.k);
+  v.base = uniform(M.base);
+  v.n_words = uniform(M.n_words);
+  v.n_esc = uniform(M.n_esc);
+  v.len = chunk_len(g, uniform(M.c));
+  v.E0 = uniform(M.ent[l.wave * kRows]);
+  v.Ee = uniform(M.ent[l.wave * kRows + kRows]);
+  const uint32_t e0c = min(v.E0, v.n_esc);
+  v.al = e0c & ~15u;
+  v.esc_off = uniform(M.esc_off);
+  v.sm_off = uniform(M.sm_off);
+  v.r = uniform(M.r);
+  return v;
 }
 
-__device__ __forceinline__ void dec_load(DecBatch &B, const PackRec &R, int j, uint32_t lane,
-                                         uint64_t reclen) {
+__device__ __forceinline__ void dec_load(DecBuf &B, const DecView &v, const Lane &l) {
+  if (v.mode == 0) {
+    load_chunk(v.rec + 16, v.len, l, B.a);
+    return;
+  }
 #pragma unroll
-  for (int q = 0; q < kBatch; ++q) {
-    const uint32_t row = j * kBatch + q;
-    const uint32_t w0 = row * (kRow / 2) + lane * 8u;
-    B.code[q] = make_uint3(0, 0, 0);
-    B.sm[q] = make_uint2(0, 0);
-    if (w0 < R.n_words) {
-      if (R.k) {
-        uint64_t a4 = ((uint64_t)(w0 >> 3) * R.k) & ~3ull;
-        B.code[q] = *reinterpret_cast<const uint3 *>(R.rec + R.code_off + a4);
+  for (int h = 0; h < kRows; ++h) {
+    const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+    B.a[h] = make_uint4(0, 0, 0, 0);
+    B.b[h] = make_uint2(0, 0);
+    if (w0 < v.n_words) {
+      if (v.k) {
+        const uint32_t a4 = ((w0 >> 3) * v.k) & ~3u;
+        const uint3 x = *reinterpret_cast<const uint3 *>(v.rec + 16 + a4);
+        B.a[h] = make_uint4(x.x, x.y, x.z, 0);
       }
-      B.sm[q] = *reinterpret_cast<const uint2 *>(R.rec + R.sm_off + w0);
+      B.b[h] = *reinterpret_cast<const uint2 *>(v.rec + v.sm_off + w0);
     }
   }
-  // escape bytes of the batch: [index[4j], index[4j+4]) from the index
-  B.lo = B.lo_al = B.hi = 0;
-  if (R.k) {
-    uint32_t lo = blk_at(R, j * kBatch), hi = blk_at(R, j * kBatch + kBatch);
-    lo = min(lo, R.n_esc);
-    hi = min(max(hi, lo), R.n_esc);
-    if (hi - lo > kBatch * (kRow / 2)) hi = lo;  // inconsistent index: rejected later
-    B.lo = lo;
-    B.hi = hi;
-    B.lo_al = lo & ~15u;
-#pragma unroll
-    for (int p = 0; p < (int)kEscPieces; ++p) {
-      const uint32_t piece = lane + 64u * p;
-      B.esc[p] = make_uint4(0, 0, 0, 0);
-      const uint64_t at = R.esc_off + B.lo_al + 16u * piece;
-      if (B.lo_al + 16u * piece < hi && at + 16 <= reclen)
-        B.esc[p] = *reinterpret_cast<const uint4 *>(R.rec + at);
-    }
+  B.e = make_uint4(0, 0, 0, 0);
+  if (v.k) {
+    const uint32_t e0c = min(v.E0, v.n_esc), eec = min(max(v.Ee, e0c), v.n_esc);
+    const uint32_t at = v.al + 16u * l.lane;
+    if (at < eec) B.e = *reinterpret_cast<const uint4 *>(v.rec + v.esc_off + at);
   }
 }
 
-// Decode one batch; returns whether any structure rule failed.
-__device__ __forceinline__ bool dec_process(const DecBatch &B, const PackRec &R, int j,
-                                            uint32_t lane, uint8_t *stage, uint32_t &acc,
-                                            uint32_t &v0, uint32_t &v1, uint32_t &v2,
-                                            uint32_t &v3, const GLane &gl, uint8_t *dst,
-                                            uint32_t len) {
+__device__ __forceinline__ void dec_store(uint8_t *dst, uint32_t o, uint32_t len,
+                                          const uint32_t (&out)[4]) {
+  if (o + 16u <= len) {
+    *reinterpret_cast<uint4 *>(dst + o) = make_uint4(out[0], out[1], out[2], out[3]);
+  } else if (o < len) {
+    for (uint32_t b = 0; b < len - o; ++b) dst[o + b] = (uint8_t)(out[b >> 2] >> (8 * (b & 3)));
+  }
+}
+
+__device__ __forceinline__ uint32_t bfi(uint32_t m, uint32_t a, uint32_t b) {
+  return (a & m) | (b & ~m);
+}
+
+// The lane's 8 K-bit codes, which start at bit `sh` of a.x, one per byte
+// (codes 0..3 in .x, 4..7 in .y).
+template <uint32_t K>
+__device__ __forceinline__ uint2 unpack_codes(const uint4 &a, uint32_t sh) {
+  uint2 c = make_uint2(0, 0);
+  if constexpr (K == 0) {
+    return c;
+  } else {
+    const uint32_t v0 = __builtin_amdgcn_alignbit(a.y, a.x, sh);
+    if constexpr (K == 4) {
+      const uint32_t t0 = __builtin_amdgcn_perm(0u, v0, 0x01010000u);  // b0 b0 b1 b1
+      const uint32_t t1 = __builtin_amdgcn_perm(0u, v0, 0x03030202u);  // b2 b2 b3 b3
+      c.x = (t0 & 0x000F000Fu) | ((t0 >> 4) & 0x0F000F00u);
+      c.y = (t1 & 0x000F000Fu) | ((t1 >> 4) & 0x0F000F00u);
+    } else {
+      const uint32_t v1 = K > 4 ? __builtin_amdgcn_alignbit(a.z, a.y, sh) : 0u;
+      constexpr uint32_t m = (1u << K) - 1u;
+#pragma unroll
+      for (uint32_t u = 0; u < 8; ++u) {
+        const uint32_t lo = u * K;
+        uint32_t f;
+        if (lo + K <= 32) f = (v0 >> lo) & m;
+        else if (lo >= 32) f = (v1 >> (lo - 32)) & m;
+        else f = __builtin_amdgcn_alignbit(v1, v0, lo) & m;
+        if (u < 4) c.x |= f << (8 * u);
+        else c.y |= f << (8 * (u - 4));
+      }
+    }
+    return c;
+  }
+}
+
+// Four words from their exponent bytes e and sign/mantissa bytes s:
+// word i = (s_i & 0x80) << 8 | e_i << 7 | (s_i & 0x7F).
+__device__ __forceinline__ uint2 assemble4(uint32_t e, uint32_t s) {
+  const uint32_t b0 = bfi(0x7F7F7F7Fu, s, e << 7);   // low bytes
+  const uint32_t b1 = bfi(0x80808080u, s, e >> 1);   // high bytes
+  return make_uint2(__builtin_amdgcn_perm(b1, b0, 0x05010400u),
+                    __builtin_amdgcn_perm(b1, b0, 0x07030602u));
+}
+
+// Decode a packed share with K-bit codes; returns whether a structure rule
+// failed.  Works on four words per instruction (one byte each); escapes,
+// codes that can overflow the exponent byte and the chunk tail take uniform
+// branches.  CRC column streams are advanced over all 8 rows.
+template <uint32_t K>
+__device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, const DecMeta &M,
+                                           const Lane &l, uint8_t *stage, uint8_t *dst,
+                                           uint32_t (&cv)[4], const GLane &gl) {
+  constexpr uint32_t esc = (1u << K) - 1u;
   bool bad = false;
-  if (R.k) {
+  uint32_t acc = v.E0;
+  const uint32_t e0c = min(v.E0, v.n_esc), eec = min(max(v.Ee, e0c), v.n_esc);
+  const uint32_t sh = ((l.lane * K) & 3u) * 8u;
+  const uint32_t base4 = v.base * 0x01010101u;
+  const bool wrap = v.base + esc > 255u;  // a code can carry out of its byte
+  const bool full = v.n_words == kChunk / 2;
+  if (K) *reinterpret_cast<uint4 *>(stage + 16u * l.lane) = B.e;
 #pragma unroll
-    for (int p = 0; p < (int)kEscPieces; ++p)
-      *reinterpret_cast<uint4 *>(stage + 16u * (lane + 64u * p)) = B.esc[p];
-  }
-#pragma unroll
-  for (int q = 0; q < kBatch; ++q) {
-    const uint32_t row = j * kBatch + q;
-    const uint32_t w0 = row * (kRow / 2) + lane * 8u;
-    const uint32_t o = w0 * 2u;
+  for (int h = 0; h < kRows; ++h) {
+    const uint32_t row = l.wave * kRows + h;
+    const uint32_t w0 = (l.off0 + h * kRow) >> 1;
     uint32_t out[4] = {0, 0, 0, 0};
-    if (row * (kRow / 2) < R.n_words) {
-      uint64_t v = 0;
-      if (R.k) {
-        const uint64_t start = (uint64_t)(w0 >> 3) * R.k;
-        const uint32_t sh = (uint32_t)(start & 3u) * 8u;
-        const uint64_t lo = ((uint64_t)B.code[q].y << 32) | B.code[q].x;
-        v = sh ? (lo >> sh) | ((uint64_t)B.code[q].z << (64 - sh)) : lo;
+    if (row * (kRow / 2) < v.n_words) {
+      uint2 c = unpack_codes<K>(B.a[h], sh);
+      uint32_t vm0 = ~0u, vm1 = ~0u;  // valid code bytes
+      if (!full) {
+        const uint32_t vw = w0 >= v.n_words ? 0u : min(v.n_words - w0, 8u);
+        vm0 = vw >= 4 ? ~0u : (1u << (8 * vw)) - 1u;
+        vm1 = vw >= 8 ? ~0u : (vw <= 4 ? 0u : (1u << (8 * (vw - 4))) - 1u);
+        c.x &= vm0;
+        c.y &= vm1;
       }
-      uint32_t flags = 0;
-      uint32_t codes[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        codes[u] = (uint32_t)(v >> (u * R.k)) & R.esc_code;
-        bool valid = w0 + u < R.n_words;
-        if (R.k && valid && codes[u] == R.esc_code) flags |= 1u << u;
-        if (R.k && valid && codes[u] != R.esc_code && R.base + codes[u] > 255u) bad = true;
+      uint2 f = make_uint2(0, 0);  // escape flags at bit 8u+K
+      if (K) {
+        f.x = (c.x + 0x01010101u) & (0x01010101u << K);
+        f.y = (c.y + 0x01010101u) & (0x01010101u << K);
       }
-      const uint32_t cnt = __popc(flags);
-      const uint32_t incl = wave_incl_scan(cnt);
-      // the index entry of this block must equal the escapes decoded so far
-      if (R.k && blk_at(R, row) != acc) bad = true;
-      uint32_t rank = acc + incl - cnt;
-      acc += __builtin_amdgcn_readlane(incl, 63);
-      const uint64_t sm8 = ((uint64_t)B.sm[q].y << 32) | B.sm[q].x;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        uint32_t ex = (R.base + codes[u]) & 255u;
-        if ((flags >> u) & 1u) {
-          uint32_t at = rank - B.lo_al;
-          ex = (rank >= B.lo && rank < B.hi && at < kEscStage) ? stage[at] : 0u;
-          if (!(rank >= B.lo && rank < B.hi)) bad = true;
-          ++rank;
+      uint2 e;
+      if (!wrap) {
+        e = make_uint2(c.x + base4, c.y + base4);
+      } else {  // bytewise sum; a non-escape code past 255 is invalid
+        const uint32_t s0 = ((c.x & 0x7F7F7F7Fu) + (base4 & 0x7F7F7F7Fu)) ^ ((c.x ^ base4) & 0x80808080u);
+        const uint32_t s1 = ((c.y & 0x7F7F7F7Fu) + (base4 & 0x7F7F7F7Fu)) ^ ((c.y ^ base4) & 0x80808080u);
+        const uint32_t k0 = ((c.x & base4) | ((c.x | base4) & ~s0)) & 0x80808080u;
+        const uint32_t k1 = ((c.y & base4) | ((c.y | base4) & ~s1)) & 0x80808080u;
+        if ((k0 & ~(f.x << (7 - K)) & vm0) | (k1 & ~(f.y << (7 - K)) & vm1)) bad = true;
+        e = make_uint2(s0, s1);
+      }
+      if (K) {
+        // the index entry of this block equals the escapes before it
+        if (uniform(M.ent[row]) != acc) bad = true;
+        if (__ballot((f.x | f.y) != 0)) {
+          const uint32_t cnt = __popc(f.x) + __popc(f.y);
+          const uint32_t incl = wave_incl_scan(cnt);
+          uint32_t rank = acc + incl - cnt;
+          acc += __builtin_amdgcn_readlane(incl, 63);
+          uint64_t ff = (uint64_t)f.x | ((uint64_t)f.y << 32);
+          uint64_t ev = (uint64_t)e.x | ((uint64_t)e.y << 32);
+          while (ff) {
+            const uint32_t bit = (uint32_t)__builtin_ctzll(ff) & ~7u;
+            ff &= ff - 1;
+            uint32_t x = 0;
+            if (rank < eec) {
+              const uint32_t at = rank - v.al;
+              x = at < kDecEscBytes ? stage[at] : v.rec[v.esc_off + rank];
+            } else {
+              bad = true;
+            }
+            ++rank;
+            ev = (ev & ~(0xFFull << bit)) | ((uint64_t)x << bit);
+          }
+          e = make_uint2((uint32_t)ev, (uint32_t)(ev >> 32));
         }
-        const uint32_t sm = (uint32_t)(sm8 >> (8 * u)) & 255u;
-        const uint32_t w = ((sm & 0x80u) << 8) | (ex << 7) | (sm & 0x7Fu);
-        if (w0 + u < R.n_words) out[u >> 1] |= w << (16 * (u & 1));
+      }
+      const uint2 lo = assemble4(e.x, B.b[h].x), hi = assemble4(e.y, B.b[h].y);
+      out[0] = lo.x;
+      out[1] = lo.y;
+      out[2] = hi.x;
+      out[3] = hi.y;
+      if (!full) {  // words past the chunk are zero
+        const uint32_t vw = w0 >= v.n_words ? 0u : min(v.n_words - w0, 8u);
+#pragma unroll
+        for (uint32_t j = 0; j < 4; ++j)
+          out[j] &= vw >= 2 * j + 2 ? ~0u : (vw == 2 * j + 1 ? 0xFFFFu : 0u);
       }
     }
-    v0 = g_step(v0 ^ out[0], gl);
-    v1 = g_step(v1 ^ out[1], gl);
-    v2 = g_step(v2 ^ out[2], gl);
-    v3 = g_step(v3 ^ out[3], gl);
-    if (o + 16u <= len) {
-      *reinterpret_cast<uint4 *>(dst + o) = make_uint4(out[0], out[1], out[2], out[3]);
-    } else if (o < len) {
-      for (uint32_t b = 0; b < len - o; ++b) dst[o + b] = (uint8_t)(out[b >> 2] >> (8 * (b & 3)));
-    }
-    __builtin_amdgcn_sched_barrier(0);
+    cv[0] = g_step(cv[0] ^ out[0], gl);
+    cv[1] = g_step(cv[1] ^ out[1], gl);
+    cv[2] = g_step(cv[2] ^ out[2], gl);
+    cv[3] = g_step(cv[3] ^ out[3], gl);
+    dec_store(dst, l.off0 + h * kRow, v.len, out);
   }
+  if (K && acc != v.Ee) bad = true;  // the wave's escapes end where the next block's begin
   return bad;
 }
 
-__global__ __launch_bounds__(kDecWaves * 64) void k_decode(
+__global__ __launch_bounds__(kDecThreads) void k_decode(
     const uint8_t *__restrict__ payload, ChunkGeom g, uint8_t *__restrict__ staging,
     uint32_t *__restrict__ rec_status, uint8_t *ws, WsLayout L) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(ws + L.ctl);
   uint32_t *ecrc = reinterpret_cast<uint32_t *>(ws + L.entry_crc);
-  if (!ctl->hdr_ok) return;
-  const uint32_t n_rec = ctl->n_rec;
+  if (!uniform(ctl->hdr_ok)) return;
+  const uint32_t n_rec = uniform(ctl->n_rec);
   const uint64_t table_off = ctl->table_off;
   load_crc_tables(g.crc_kind);
   __syncthreads();
   const CrcTables &T = g_tables[g.crc_kind];
+  DecShared &sh = dec_shared();
+  const bool is_ctl = threadIdx.x >= (uint32_t)kThreads;
   const GLane gl = glane_make();
-  const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
-  uint8_t *stage = lds + kLdsDecStage + wave * kEscStage;
-  const uint32_t stride = gridDim.x * kDecWaves;
+  const Lane l0 = lane_info();
+  uint8_t *stage = lds + kLdsDecEsc + l0.wave * kDecEscBytes;
+  const uint32_t G = gridDim.x;
+  const uint32_t my_n = blockIdx.x < n_rec ? (n_rec - 1 - blockIdx.x) / G + 1 : 0;
+  auto rec_of = [&](uint32_t i) { return blockIdx.x + i * G; };
 
-  for (uint32_t r = blockIdx.x * kDecWaves + wave; r < n_rec; r += stride) {
-    // ---- table entry, table-local rules (uniform across the wave)
-    const uint8_t *e = payload + table_off + 16ull * r;
-    const uint4 ent = *reinterpret_cast<const uint4 *>(e);
-    const uint32_t c = ent.x, src_crc = ent.y;
-    const uint64_t off = (uint64_t)ent.z | ((uint64_t)ent.w << 32);
-    uint64_t end = table_off;
-    bool tbad = false;
-    if (r + 1 < n_rec) {
-      const uint4 nx = *reinterpret_cast<const uint4 *>(e + 16);
-      end = (uint64_t)nx.z | ((uint64_t)nx.w << 32);
-      tbad = nx.x <= c;
-    }
-    {
-      uint32_t ew[4] = {ent.x, ent.y, ent.z, ent.w};
-      uint32_t ec = crc_words(ew, 4);
-      if (lane == 0) ecrc[r] = ec;
-    }
-    tbad = tbad || c >= g.n_chunks || (r == 0 && off != 64u) || (off & 15u) || off >= end ||
-           end > table_off;
-    if (tbad) {
-      if (lane == 0) atomicOr(&ctl->table_bad, 1u);
-      continue;
-    }
-    // ---- record header
-    const uint32_t len = chunk_len(g, c), n_words = len / 2;
-    const uint64_t reclen = end - off;
-    const uint8_t *rec = payload + off;
-    uint32_t st = 0, mode = 0, k = 0, base = 0, n_esc = 0;
-    uint64_t code_bytes = 0, n_blocks = 0;
-    if (reclen < 16) {
-      st = 4;
-    } else {
-      const uint4 h4 = *reinterpret_cast<const uint4 *>(rec);
-      uint32_t hw[4] = {h4.x, h4.y, h4.z, h4.w};
-      mode = hw[0] & 255u;
-      k = (hw[0] >> 8) & 255u;
-      base = (hw[0] >> 16) & 255u;
-      n_esc = hw[2];
-      code_bytes = ((uint64_t)n_words * k + 7) / 8;
-      n_blocks = k ? ((uint64_t)n_words + 511) / 512 : 0;
-      if (crc_words(hw, 3) != hw[3] || (hw[0] >> 24) || hw[1] != n_words || mode > 1) {
-        st = 4;
-      } else if (mode == 0) {
-        if (k || base || n_esc || reclen != 16u + pad16(2ull * n_words)) st = 4;
-      } else if (k > 7 || n_esc > n_words || (k == 0 && n_esc) ||
-                 reclen != 16u + pad16(code_bytes) + pad16(2 * n_blocks) + pad16(n_esc) +
-                               pad16(n_words)) {
-        st = 4;
+  if (is_ctl) {
+    for (uint32_t i = 0; i < 2 && i < my_n; ++i)
+      dec_prepare(payload, table_off, n_rec, rec_of(i), g, ecrc, ctl, sh.meta[i]);
+  }
+  __syncthreads();
+  DecBuf cur, nxt;
+  if (!is_ctl && my_n > 0 && uniform(sh.meta[0].st) == 0)
+    dec_load(cur, dec_view(payload, sh.meta[0], l0, g), l0);
+
+  for (uint32_t i = 0; i <= my_n; ++i) {
+    const Lane l = lane_fresh(l0);
+    if (!is_ctl) {
+      if (i + 1 < my_n) {
+        const DecMeta &Mn = sh.meta[(i + 1) % 3];
+        if (uniform(Mn.st) == 0) dec_load(nxt, dec_view(payload, Mn, l, g), l);
       }
-    }
-    if (st == 0) {
-      uint8_t *dst = staging + (uint64_t)r * kChunk;
-      uint32_t v0 = 0, v1 = 0, v2 = 0, v3 = 0;
-      bool bad = false;
-      if (mode == 0) {
-        const uint8_t *body = rec + 16;
-#pragma unroll 8
-        for (int row = 0; row < kChunkRows; ++row) {
-          const uint32_t o = row * kRow + lane * 16u;
-          uint4 d;
-          if (len == kChunk) d = ldg_nt(body + o);
-          else if (o + 16u <= len) d = *reinterpret_cast<const uint4 *>(body + o);
-          else if (o < len) d = load16_partial(body + o, len - o);
-          else d = make_uint4(0, 0, 0, 0);
-          v0 = g_step(v0 ^ d.x, gl);
-          v1 = g_step(v1 ^ d.y, gl);
-          v2 = g_step(v2 ^ d.z, gl);
-          v3 = g_step(v3 ^ d.w, gl);
-          if (o + 16u <= len) {
-            *reinterpret_cast<uint4 *>(dst + o) = d;
-          } else if (o < len) {
-            const uint32_t w[4] = {d.x, d.y, d.z, d.w};
-            for (uint32_t b = 0; b < len - o; ++b) dst[o + b] = (uint8_t)(w[b >> 2] >> (8 * (b & 3)));
+      if (i < my_n) {
+        const DecMeta &M = sh.meta[i % 3];
+        if (uniform(M.st) == 0) {
+          const DecView v = dec_view(payload, M, l, g);
+          uint8_t *dst = staging + (uint64_t)v.r * kChunk;
+          uint32_t cv[4] = {0, 0, 0, 0};
+          bool bad = false;
+          if (v.mode == 0) {
+#pragma unroll
+            for (int h = 0; h < kRows; ++h) {
+              cv[0] = g_step(cv[0] ^ cur.a[h].x, gl);
+              cv[1] = g_step(cv[1] ^ cur.a[h].y, gl);
+              cv[2] = g_step(cv[2] ^ cur.a[h].z, gl);
+              cv[3] = g_step(cv[3] ^ cur.a[h].w, gl);
+            }
+            store_chunk(dst, v.len, l, cur.a, false);
+          } else {
+            switch (v.k) {
+              case 0: bad = dec_packed<0>(cur, v, M, l, stage, dst, cv, gl); break;
+              case 1: bad = dec_packed<1>(cur, v, M, l, stage, dst, cv, gl); break;
+              case 2: bad = dec_packed<2>(cur, v, M, l, stage, dst, cv, gl); break;
+              case 3: bad = dec_packed<3>(cur, v, M, l, stage, dst, cv, gl); break;
+              case 4: bad = dec_packed<4>(cur, v, M, l, stage, dst, cv, gl); break;
+              case 5: bad = dec_packed<5>(cur, v, M, l, stage, dst, cv, gl); break;
+              case 6: bad = dec_packed<6>(cur, v, M, l, stage, dst, cv, gl); break;
+              default: bad = dec_packed<7>(cur, v, M, l, stage, dst, cv, gl); break;
+            }
+          }
+          const uint32_t q = lane_tree(cv[0], cv[1], cv[2], cv[3]);
+          const bool any_bad = __ballot(bad) != 0;
+          if (l.lane == 0) {
+            sh.part[i & 1][l.wave] = mat_apply(T.wave_mat[l.wave], q);
+            sh.bad[i & 1][l.wave] = any_bad ? 1u : 0u;
           }
         }
-        if (lane < 16u) {
-          uint64_t at = 16u + 2ull * n_words + lane;
-          if (at < 16u + pad16(2ull * n_words) && rec[at]) bad = true;
-        }
-      } else {
-        PackRec R;
-        R.rec = rec;
-        R.k = k;
-        R.base = base;
-        R.n_esc = n_esc;
-        R.n_words = n_words;
-        R.n_blocks = (uint32_t)n_blocks;
-        R.esc_code = (1u << k) - 1u;
-        R.code_off = 16;
-        R.idx_off = 16 + pad16(code_bytes);
-        R.esc_off = R.idx_off + pad16(2 * n_blocks);
-        R.sm_off = R.esc_off + pad16(n_esc);
-        R.blk = (k && lane < n_blocks)
-                    ? (uint32_t)(*reinterpret_cast<const uint16_t *>(rec + R.idx_off + 2 * lane))
-                    : n_esc;
-        const int n_batches = (int)((n_words + kBatch * (kRow / 2) - 1) / (kBatch * (kRow / 2)));
-        uint32_t acc = 0;
-        DecBatch A, B2;
-        dec_load(A, R, 0, lane, reclen);
-        for (int j = 0; j < n_batches; j += 2) {
-          if (j + 1 < n_batches) dec_load(B2, R, j + 1, lane, reclen);
-          bad |= dec_process(A, R, j, lane, stage, acc, v0, v1, v2, v3, gl, dst, len);
-          if (j + 1 >= n_batches) break;
-          if (j + 2 < n_batches) dec_load(A, R, j + 2, lane, reclen);
-          bad |= dec_process(B2, R, j + 1, lane, stage, acc, v0, v1, v2, v3, gl, dst, len);
-        }
-        // rows past the chunk: zero data, as in the zero-padded CRC layout
-        for (int row = n_batches * kBatch; row < kChunkRows; ++row) {
-          v0 = g_step(v0, gl);
-          v1 = g_step(v1, gl);
-          v2 = g_step(v2, gl);
-          v3 = g_step(v3, gl);
-        }
-        if (acc != n_esc) bad = true;
-        // padding: codes (whole bytes and unused bits), index, escapes, sm
-        if (lane < 16u) {
-          const uint8_t *codes = rec + R.code_off;
-          if (code_bytes + lane < pad16(code_bytes) && codes[code_bytes + lane]) bad = true;
-          if (2 * n_blocks + lane < pad16(2 * n_blocks) && rec[R.idx_off + 2 * n_blocks + lane]) bad = true;
-          if (n_esc + lane < pad16(n_esc) && rec[R.esc_off + n_esc + lane]) bad = true;
-          if (n_words + lane < pad16(n_words) && rec[R.sm_off + n_words + lane]) bad = true;
-          uint64_t used = (uint64_t)n_words * k;
-          if (lane == 0 && (used & 7u) && (codes[used / 8] >> (used & 7u))) bad = true;
+      }
+    } else {
+      if (i >= 1) {  // settle the previous record
+        const DecMeta &M = sh.meta[(i - 1) % 3];
+        uint32_t st = uniform(M.st);
+        if (st != kMetaSkip) {
+          if (st == 0) {
+            uint32_t raw = 0, bad = 0;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) {
+              raw ^= sh.part[(i - 1) & 1][w];
+              bad |= sh.bad[(i - 1) & 1][w];
+            }
+            const uint32_t c = uniform(M.c);
+            const uint32_t crc = finish_crc(raw, chunk_len(g, c), g, T);
+            st = bad ? 4u : (crc != uniform(M.src_crc) ? 8u : 0u);
+          }
+          if (l.lane == 0) {
+            if (rec_status) rec_status[uniform(M.r)] = st;
+            if (st) atomicOr(&ctl->rec_bits, st);
+          }
         }
       }
-      const uint32_t crc = wave_chunk_crc(v0, v1, v2, v3, len, g, T);
-      if (__ballot(bad)) st = 4;
-      else if ((uint32_t)__shfl((int)crc, 0, 64) != src_crc) st = 8;
+      if (i + 2 < my_n)
+        dec_prepare(payload, table_off, n_rec, rec_of(i + 2), g, ecrc, ctl, sh.meta[(i + 2) % 3]);
     }
-    if (lane == 0) {
-      if (rec_status) rec_status[r] = st;
-      if (st) atomicOr(&ctl->rec_bits, st);
-    }
+    __syncthreads();
+    if (!is_ctl) cur = nxt;
   }
 }
-
 
 // Final verdict after the table CRC has been combined.
 __global__ void k_decode_verdict(const uint8_t *ws, WsLayout L,
@@ -1489,9 +1675,9 @@ int launch_encode(int mode, const void *cur, const void *prev, const ChunkGeom &
   if (g.n_chunks) {
     uint32_t grid = min((uint32_t)n_cu, g.n_chunks);
     if (mode == kModeStep && prev != nullptr)
-      hipLaunchKernelGGL(k_encode<true>, dim3(grid), dim3(kThreads), kLdsEncode, S(stream), a, g);
+      hipLaunchKernelGGL(k_encode<true>, dim3(grid), dim3(kEncThreads), kLdsEncode, S(stream), a, g);
     else
-      hipLaunchKernelGGL(k_encode<false>, dim3(grid), dim3(kThreads), kLdsEncode, S(stream), a, g);
+      hipLaunchKernelGGL(k_encode<false>, dim3(grid), dim3(kEncThreads), kLdsEncode, S(stream), a, g);
     e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
   }
@@ -1529,8 +1715,8 @@ int launch_decode(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
   if (g.n_chunks) {
-    uint32_t grid_d = min((uint32_t)n_cu, (g.n_chunks + kDecWaves - 1) / kDecWaves);
-    hipLaunchKernelGGL(k_decode, dim3(grid_d), dim3(kDecWaves * 64), kLdsDecode, S(stream), pl,
+    uint32_t grid_d = min((uint32_t)n_cu, g.n_chunks);
+    hipLaunchKernelGGL(k_decode, dim3(grid_d), dim3(kDecThreads), kLdsDecode, S(stream), pl,
                        g, static_cast<uint8_t *>(staging), rec_status, wsb, L);
     e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
