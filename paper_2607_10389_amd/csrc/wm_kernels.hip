@@ -53,6 +53,37 @@ __device__ __forceinline__ uint4 ldg_nt(const void *p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// Buffer loads through a descriptor that covers [base, base + bytes): reads
+// past the range return zero instead of touching memory, so a loop can issue
+// the same loads whatever the length (a zero range turns them into no-ops).
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kNt = 2;  // buffer-load cache policy: non-temporal
+__device__ __forceinline__ Rsrc rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, bytes, 0x00020000);
+}
+template <int AUX = 0>
+__device__ __forceinline__ uint4 buf16(Rsrc r, uint32_t off) {
+  const v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint2 buf8(Rsrc r, uint32_t off) {
+  typedef uint32_t v2u __attribute__((ext_vector_type(2)));
+  const v2u v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+  return make_uint2(v.x, v.y);
+}
+__device__ __forceinline__ uint3 buf12(Rsrc r, uint32_t off) {
+  typedef uint32_t v3u __attribute__((ext_vector_type(3)));
+  const v3u v = __builtin_amdgcn_raw_buffer_load_b96(r, off, 0, 0);
+  return make_uint3(v.x, v.y, v.z);
+}
+
+// Uniform read-only kernel inputs through the constant address space, which
+// the compiler serves with scalar loads (no vector-memory wait).
+__device__ __forceinline__ uint32_t ld_const(const uint32_t *p) {
+  typedef const __attribute__((address_space(4))) uint32_t cu32;
+  return *(cu32 *)(uintptr_t)p;
+}
+
 __device__ __forceinline__ uint32_t lds_u32(uint32_t off) {
   return *reinterpret_cast<const uint32_t *>(lds + off);
 }
@@ -191,23 +222,21 @@ __device__ __forceinline__ uint4 load16_partial(const uint8_t *p, uint32_t n) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// Load a wave's 8 rows of a chunk of `len` bytes; bytes past len read 0.
+// Load a wave's 8 rows of a chunk of `len` bytes (0 for none: the loads are
+// still issued, so every path has the same number in flight); bytes past len
+// read 0.  Only a tail chunk's 16-byte piece that straddles len is refetched
+// bytewise.
 __device__ __forceinline__ void load_chunk(const uint8_t *__restrict__ base,
                                            uint32_t len, const Lane &l,
                                            uint4 (&d)[kRows]) {
-  if (len == kChunk) {
+  const Rsrc r = rsrc(base, len);
 #pragma unroll
-    for (int h = 0; h < kRows; ++h) d[h] = ldg_nt(base + l.off0 + h * kRow);
-  } else {
+  for (int h = 0; h < kRows; ++h) d[h] = buf16<kNt>(r, l.off0 + h * kRow);
+  if (len & 15u) {
 #pragma unroll
     for (int h = 0; h < kRows; ++h) {
-      uint32_t off = l.off0 + h * kRow;
-      if (off + 16u <= len)
-        d[h] = *reinterpret_cast<const uint4 *>(base + off);
-      else if (off < len)
-        d[h] = load16_partial(base + off, len - off);
-      else
-        d[h] = make_uint4(0, 0, 0, 0);
+      const uint32_t off = l.off0 + h * kRow;
+      if (off < len && off + 16u > len) d[h] = load16_partial(base + off, len - off);
     }
   }
 }
@@ -278,11 +307,12 @@ __global__ __launch_bounds__(kThreads) void k_checksum(
   const Lane l = lane_info();
   uint32_t c = blockIdx.x;
   uint4 d[kRows];
-  if (c < g.n_chunks) load_chunk(data + (uint64_t)c * kChunk, chunk_len(g, c), l, d);
+  load_chunk(data + (uint64_t)c * kChunk, c < g.n_chunks ? chunk_len(g, c) : 0u, l, d);
   while (c < g.n_chunks) {
     const uint32_t cn = c + gridDim.x;
     uint4 dn[kRows];
-    if (cn < g.n_chunks) load_chunk(data + (uint64_t)cn * kChunk, chunk_len(g, cn), l, dn);
+    load_chunk(data + (uint64_t)(cn < g.n_chunks ? cn : c) * kChunk,
+               cn < g.n_chunks ? chunk_len(g, cn) : 0u, l, dn);
     const uint32_t q = wave_q(d, gl);
     if (l.lane == 0) misc()[M_PART + l.wave] = mat_apply(T.wave_mat[l.wave], q);
     __syncthreads();
@@ -483,8 +513,8 @@ struct EncShared {
   uint32_t mode, k, base, n_esc, size, dirty, crc;
   uint32_t first, next;      // tickets
   uint32_t off_lo, off_hi;   // record offset
-  uint32_t H[256];           // histogram
-  uint32_t P[260];           // exclusive prefix of H (P[256] = n)
+  alignas(16) uint32_t H[256];  // histogram
+  alignas(16) uint32_t P[260];  // exclusive prefix of H (P[256] = n)
 };
 static_assert(sizeof(EncShared) <= kLdsMiscBytes, "encoder scratch fits");
 constexpr uint32_t kLdsHistE = kLdsMisc + kLdsMiscBytes;  // 256 bins x 16 copies
@@ -516,14 +546,25 @@ __device__ __forceinline__ uint32_t pk_sub_min(uint32_t ex, uint32_t base2, uint
 }
 
 // The 8 sign/mantissa bytes of a 16-byte piece: byte u = (w_u >> 8 & 0x80) |
-// (w_u & 0x7F).
+// (w_u & 0x7F), from the gathered low and high bytes of the words.
 __device__ __forceinline__ uint2 sm_bytes(const uint4 &x) {
-  uint32_t s0 = (x.x & 0x007F007Fu) | ((x.x >> 8) & 0x00800080u);
-  uint32_t s1 = (x.y & 0x007F007Fu) | ((x.y >> 8) & 0x00800080u);
-  uint32_t s2 = (x.z & 0x007F007Fu) | ((x.z >> 8) & 0x00800080u);
-  uint32_t s3 = (x.w & 0x007F007Fu) | ((x.w >> 8) & 0x00800080u);
-  return make_uint2(__builtin_amdgcn_perm(s1, s0, 0x06040200u),
-                    __builtin_amdgcn_perm(s3, s2, 0x06040200u));
+  const uint32_t lo0 = __builtin_amdgcn_perm(x.y, x.x, 0x06040200u);
+  const uint32_t hi0 = __builtin_amdgcn_perm(x.y, x.x, 0x07050301u);
+  const uint32_t lo1 = __builtin_amdgcn_perm(x.w, x.z, 0x06040200u);
+  const uint32_t hi1 = __builtin_amdgcn_perm(x.w, x.z, 0x07050301u);
+  return make_uint2((lo0 & 0x7F7F7F7Fu) | (hi0 & 0x80808080u),
+                    (lo1 & 0x7F7F7F7Fu) | (hi1 & 0x80808080u));
+}
+
+// Maximum over the wave (DPP row shifts and broadcasts), as a uniform value.
+__device__ __forceinline__ uint32_t wave_max_u(uint32_t v) {
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false));
+  return __builtin_amdgcn_readlane(v, 63);
 }
 
 // Chunk of a work item; a caller's list must be ascending and in range, a
@@ -531,8 +572,8 @@ __device__ __forceinline__ uint2 sm_bytes(const uint4 &x) {
 __device__ __forceinline__ uint32_t item_chunk(const EncArgs &a, uint32_t item,
                                                const ChunkGeom &g) {
   if (a.mode != kModeList) return item;
-  uint32_t c = a.idx[item];
-  if (c >= g.n_chunks || (item > 0 && a.idx[item - 1] >= c)) return 0xFFFFFFFFu;
+  const uint32_t c = ld_const(a.idx + item);
+  if (c >= g.n_chunks || (item > 0 && ld_const(a.idx + item - 1) >= c)) return 0xFFFFFFFFu;
   return c;
 }
 
@@ -602,44 +643,43 @@ __device__ uint64_t lookback_finish(const uint64_t *status, int64_t top, Window 
   return excl;
 }
 
-// k-bit codes of the data wave's 8 rows into LDS staging; escape flags per
-// row (8 bits each) and each row's escape count before it within the wave.
+// K-bit codes of the data wave's 8 rows into LDS staging.  Codes are formed
+// two words at a time in 16-bit lanes: c = min((e - base) mod 2^16, esc), and
+// c + 1 carries into bit K exactly for escapes.  Per row: escm holds the
+// lane's escape flags (bit u = word u, 8 bits per row), lane_r the number of
+// the wave's escapes before the lane's first one in this row.
 template <uint32_t K>
 __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &l,
                                            uint32_t n_words, bool full, uint32_t base,
                                            uint8_t *stage, uint32_t (&escm)[2],
-                                           uint32_t (&row_base)[kRows], uint32_t &wave_esc) {
+                                           uint32_t (&lane_r)[kRows], uint32_t &wave_esc) {
   constexpr uint32_t esc = (1u << K) - 1u;
-  constexpr uint32_t esc2 = esc | (esc << 16);
-  const uint32_t base2 = base | (base << 16);
+  constexpr uint32_t esc2 = esc * 0x00010001u;
+  const uint32_t base2 = base * 0x00010001u;
 #pragma unroll
   for (int h = 0; h < kRows; ++h) {
     const uint32_t w0 = (l.off0 + h * kRow) >> 1;
     const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
-    uint32_t lo[4], hi[4];
-    uint32_t flags = 0;
+    uint32_t pair[4], m = 0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t cp = pk_sub_min((x[j] >> 7) & 0x00FF00FFu, base2, esc2);
-      lo[j] = cp & 0xFFFFu;
-      hi[j] = cp >> 16;
-      if (!full) {  // words past the chunk code as 0 and never escape
-        if (w0 + 2 * j >= n_words) lo[j] = 0;
-        if (w0 + 2 * j + 1 >= n_words) hi[j] = 0;
-      }
-      flags |= (lo[j] == esc ? 1u : 0u) << (2 * j);
-      flags |= (hi[j] == esc ? 1u : 0u) << (2 * j + 1);
+      const uint32_t c2 = pk_sub_min((x[j] >> 7) & 0x00FF00FFu, base2, esc2);
+      m |= (((c2 + 0x00010001u) >> K) & 0x00010001u) << (2 * j);
+      pair[j] = (c2 & 0xFFFFu) | (c2 >> (16 - K));  // lo | hi << K
     }
-    if (!full) {
-      const uint32_t valid = w0 >= n_words ? 0u : (n_words - w0 >= 8 ? 8u : n_words - w0);
-      flags &= (1u << valid) - 1u;
+    uint32_t m8 = (m | (m >> 15)) & 0xFFu;
+    if (!full) {  // words past the chunk code as 0 and never escape
+      const uint32_t vw = w0 >= n_words ? 0u : min(n_words - w0, 8u);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        pair[j] &= vw >= 2u * j + 2u ? ~0u : (vw == 2u * j + 1u ? esc : 0u);
+      m8 &= (1u << vw) - 1u;
     }
     if (w0 < n_words) {
       uint8_t *at = stage + (w0 >> 3) * K;
       if constexpr (K * 8 <= 32) {
-        uint32_t p = 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) p |= (lo[j] << (2 * j * K)) | (hi[j] << ((2 * j + 1) * K));
+        const uint32_t p = pair[0] | (pair[1] << (2 * K)) | (pair[2] << (4 * K)) |
+                           (pair[3] << (6 * K));
         if constexpr (K == 4) *reinterpret_cast<uint32_t *>(at) = p;
         else if constexpr (K == 2) *reinterpret_cast<uint16_t *>(at) = (uint16_t)p;
         else if constexpr (K == 1) *at = (uint8_t)p;
@@ -648,10 +688,8 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
           for (uint32_t b = 0; b < K; ++b) at[b] = (uint8_t)(p >> (8 * b));
         }
       } else {
-        uint64_t p = 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          p |= ((uint64_t)lo[j] << (2 * j * K)) | ((uint64_t)hi[j] << ((2 * j + 1) * K));
+        const uint64_t p = (uint64_t)pair[0] | ((uint64_t)pair[1] << (2 * K)) |
+                           ((uint64_t)pair[2] << (4 * K)) | ((uint64_t)pair[3] << (6 * K));
         if constexpr (K == 6) {
 #pragma unroll
           for (uint32_t b = 0; b < 3; ++b)
@@ -662,11 +700,14 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
         }
       }
     }
-    const uint32_t cnt = __popc(flags);
-    const uint32_t incl = wave_incl_scan(cnt);
-    row_base[h] = wave_esc;
-    wave_esc += __builtin_amdgcn_readlane(incl, 63);
-    escm[h >> 2] |= flags << (8 * (h & 3));
+    lane_r[h] = wave_esc;
+    if (__ballot(m8 != 0)) {
+      const uint32_t cnt = __popc(m8);
+      const uint32_t incl = wave_incl_scan(cnt);
+      lane_r[h] = wave_esc + incl - cnt;
+      wave_esc += __builtin_amdgcn_readlane(incl, 63);
+    }
+    escm[h >> 2] |= m8 << (8 * (h & 3));
   }
 }
 
@@ -677,7 +718,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   uint4 *tab_ws = reinterpret_cast<uint4 *>(a.ws + a.L.table);
   uint32_t *ecrc = reinterpret_cast<uint32_t *>(a.ws + a.L.entry_crc);
   const uint32_t n_items =
-      uniform(a.mode == kModeList ? min(*a.n_idx, g.n_chunks) : g.n_chunks);
+      uniform(a.mode == kModeList ? min(ld_const(a.n_idx), g.n_chunks) : g.n_chunks);
   const bool need_crc = a.crc_in == nullptr;
   const bool is_ctl = threadIdx.x >= (uint32_t)kThreads;
 
@@ -702,9 +743,10 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   const GLane gl = glane_make();
   const Lane l0 = lane_info();
   uint4 d[kRows];
-  if (!is_ctl && item < n_items) {
-    const uint32_t c = uniform(item_chunk(a, item, g));
-    if (c < g.n_chunks) load_chunk(a.cur + (uint64_t)c * kChunk, chunk_len(g, c), l0, d);
+  if (!is_ctl) {
+    const uint32_t c = item < n_items ? uniform(item_chunk(a, item, g)) : 0xFFFFFFFFu;
+    load_chunk(a.cur + (uint64_t)(c < g.n_chunks ? c : 0u) * kChunk,
+               c < g.n_chunks ? chunk_len(g, c) : 0u, l0, d);
   }
   while (item < n_items) {
     Window win;           // control wave: look-back window in flight
@@ -722,10 +764,11 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     // ---- data: prefetch, CRC streams, diff
     if (!is_ctl) {
       uint4 p[kRows];
-      if (HAS_PREV && !bad_index) load_chunk(a.prev + (uint64_t)c * kChunk, len, l, p);
-      if (next < n_items) {
-        const uint32_t cn = uniform(item_chunk(a, next, g));
-        if (cn < g.n_chunks) load_chunk(a.cur + (uint64_t)cn * kChunk, chunk_len(g, cn), l, dn);
+      if (HAS_PREV) load_chunk(a.prev + (uint64_t)c * kChunk, len, l, p);
+      {
+        const uint32_t cn = next < n_items ? uniform(item_chunk(a, next, g)) : 0xFFFFFFFFu;
+        load_chunk(a.cur + (uint64_t)(cn < g.n_chunks ? cn : 0u) * kChunk,
+                   cn < g.n_chunks ? chunk_len(g, cn) : 0u, l, dn);
       }
       if (need_crc) {
         const uint32_t q = wave_q(d, gl);
@@ -787,27 +830,32 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         for (int w = 0; w < kWaves; ++w) raw ^= sh.part[w];
         crc = bad_index ? 0u : finish_crc(raw, len, g, T);
       } else {
-        crc = a.crc_in[c];
+        crc = ld_const(a.crc_in + c);
       }
       uint32_t mode = 0, k = 0, base = 0, n_esc = 0;
       uint64_t size = 0;
       if (dirty) {
+        // Candidates in tie-break order (the first of equal sizes wins): RAW,
+        // a constant exponent, then windows of 2^k - 1 exponents for k = 1..7
+        // placed where they cover the most words (lowest base on ties).
         const uint32_t lane = l.lane, b0 = lane * 4u;
-        const uint32_t h0 = sh.H[b0], h1 = sh.H[b0 + 1], h2 = sh.H[b0 + 2], h3 = sh.H[b0 + 3];
-        const uint32_t t4 = h0 + h1 + h2 + h3;
+        const uint4 hv = *reinterpret_cast<const uint4 *>(&sh.H[b0]);
+        const uint32_t t4 = hv.x + hv.y + hv.z + hv.w;
         const uint32_t ex = wave_incl_scan(t4) - t4;
-        sh.P[b0] = ex;
-        sh.P[b0 + 1] = ex + h0;
-        sh.P[b0 + 2] = ex + h0 + h1;
-        sh.P[b0 + 3] = ex + h0 + h1 + h2;
+        *reinterpret_cast<uint4 *>(&sh.P[b0]) =
+            make_uint4(ex, ex + hv.x, ex + hv.x + hv.y, ex + hv.x + hv.y + hv.z);
         if (lane == 63u) sh.P[256] = ex + t4;
-        const uint32_t nz = (h0 ? 1u : 0u) | (h1 ? 2u : 0u) | (h2 ? 4u : 0u) | (h3 ? 8u : 0u);
+        const uint32_t nz = (hv.x ? 1u : 0u) | (hv.y ? 2u : 0u) | (hv.z ? 4u : 0u) | (hv.w ? 8u : 0u);
         const uint32_t n_distinct = __builtin_amdgcn_readlane(wave_incl_scan(__popc(nz)), 63);
-        const uint32_t only = wave_max(nz ? b0 + 31u - __clz(nz) : 0u);
+        const uint32_t only = wave_max_u(nz ? b0 + 31u - __clz(nz) : 0u);
         const uint64_t n = n_words;
-        // candidates: lane 0 RAW, lane 1 k=0, lanes 2..8 k = lane-1
-        uint64_t cand = ~0ull;
-        uint32_t c_base = 0, c_esc = 0;
+        size = 16u + pad16(2 * n);
+        if (n_distinct == 1 && 16u + pad16(n) < size) {
+          size = 16u + pad16(n);
+          mode = 1;
+          base = only;
+        }
+        const uint64_t fixed = pad16(2 * ((n + 511) / 512)) + pad16(n) + 16u;
 #pragma unroll 1
         for (uint32_t kk = 1; kk <= 7; ++kk) {
           const uint32_t width = (1u << kk) - 1u;
@@ -818,31 +866,17 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
             const uint32_t inside = sh.P[min(b + width, 256u)] - sh.P[b];
             key = max(key, (inside << 8) | (255u - b));
           }
-          key = wave_max(key);
-          if (lane == kk + 1) {
-            c_base = 255u - (key & 255u);
-            c_esc = n_words - (key >> 8);
-            cand = 16u + pad16((n * kk + 7) / 8) + pad16(2 * ((n + 511) / 512)) + pad16(c_esc) +
-                   pad16(n);
+          key = wave_max_u(key);
+          const uint32_t c_esc = n_words - (key >> 8);
+          const uint64_t sz = pad16((n * kk + 7) / 8) + pad16(c_esc) + fixed;
+          if (sz < size) {
+            size = sz;
+            mode = 1;
+            k = kk;
+            base = 255u - (key & 255u);
+            n_esc = c_esc;
           }
         }
-        if (lane == 0) cand = 16u + pad16(2 * n);
-        if (lane == 1 && n_distinct == 1) {
-          cand = 16u + pad16(n);
-          c_base = only;
-        }
-        uint64_t key = (cand << 8) | lane;  // smallest size, then lowest lane
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-          const uint64_t y = __shfl_xor(key, o, 64);
-          key = y < key ? y : key;
-        }
-        const uint32_t win_lane = (uint32_t)(key & 255u);
-        size = key >> 8;
-        mode = win_lane == 0 ? 0u : 1u;
-        k = win_lane <= 1 ? 0u : win_lane - 1u;
-        base = (uint32_t)__shfl((int)c_base, (int)win_lane, 64);
-        n_esc = (uint32_t)__shfl((int)c_esc, (int)win_lane, 64);
       }
       const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((size >> 4) << 26);
       if (l.lane == 0) {
@@ -866,10 +900,37 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     const uint32_t mode = uniform(sh.mode), k = uniform(sh.k), base = uniform(sh.base);
     const uint32_t n_esc = uniform(sh.n_esc);
     const bool pack = dirty && mode == 1u && k > 0u;
+    const uint64_t n = n_words;
+    const uint32_t code_bytes = (uint32_t)((n * k + 7) / 8);
+    const uint32_t n_blocks = k ? (n_words + 511u) / 512u : 0u;
+    const uint32_t s_idx = (uint32_t)pad16(code_bytes);  // staging offsets
+    const uint32_t s_esc = s_idx + (uint32_t)pad16(2 * n_blocks);
+    const uint32_t s_end = s_esc + (uint32_t)pad16(n_esc);
     uint32_t escm[2] = {0, 0};
-    uint32_t row_base[kRows];
+    uint32_t lane_r[kRows];
+    if (!is_ctl && pack) {
+      // ---- data: codes into staging, escape flags and counts
+      if (!full) {  // the wave's own code bytes; lanes past the chunk write none
+        uint4 *s4 = reinterpret_cast<uint4 *>(stage + l.wave * 512u * k);
+        for (uint32_t i = l.lane; i < 32u * k; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
+      }
+      uint32_t wave_esc = 0;
+      switch (k) {
+        case 1: pack_codes<1>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+        case 2: pack_codes<2>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+        case 3: pack_codes<3>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+        case 4: pack_codes<4>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+        case 5: pack_codes<5>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+        case 6: pack_codes<6>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+        default: pack_codes<7>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+      }
+      if (l.lane == 0) sh.esc_w[l.wave] = wave_esc;
+    }
+    __syncthreads();  // B4: codes staged, escape totals known
+
     if (is_ctl) {
-      // ---- control: offset, header, table entry
+      // ---- control: finish the look-back (its reads have had the whole
+      // packing phase to return), publish the prefix, header, table entry
       const uint32_t crc = uniform(sh.crc);
       const uint64_t excl = lookback_finish(status, (int64_t)item - 1, win, ctl);
       const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(sh.size >> 4) << 26);
@@ -899,36 +960,37 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         if (a.crc_out && !bad_index) a.crc_out[c] = crc;
       }
     } else if (pack) {
-      // ---- data: codes into staging, escape flags and counts
-      if (!full) {  // the wave's own code bytes; lanes past the chunk write none
-        uint4 *s4 = reinterpret_cast<uint4 *>(stage + l.wave * 512u * k);
-        for (uint32_t i = l.lane; i < 32u * k; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
+      // ---- data: escape index and escapes into staging behind the codes
+      uint32_t wave_base = 0;
+      for (uint32_t w = 0; w < l.wave; ++w) wave_base += sh.esc_w[w];
+      wave_base = uniform(wave_base);
+#pragma unroll
+      for (int h = 0; h < kRows; ++h) {
+        const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+        if (l.lane == 0 && w0 < n_words)  // this row is escape-index block w0/512
+          *reinterpret_cast<uint16_t *>(stage + s_idx + 2 * (w0 >> 9)) =
+              (uint16_t)(wave_base + lane_r[h]);
+        uint32_t flags = (escm[h >> 2] >> (8 * (h & 3))) & 255u;
+        uint32_t at = s_esc + wave_base + lane_r[h];
+        while (flags) {  // the lane's escaped exponents, in word order
+          const uint32_t u = __builtin_ctz(flags);
+          flags &= flags - 1u;
+          const uint32_t xw = u < 4 ? (u < 2 ? d[h].x : d[h].y) : (u < 6 ? d[h].z : d[h].w);
+          stage[at++] = (uint8_t)(xw >> (7 + 16 * (u & 1)));
+        }
       }
-      uint32_t wave_esc = 0;
-      switch (k) {
-        case 1: pack_codes<1>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
-        case 2: pack_codes<2>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
-        case 3: pack_codes<3>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
-        case 4: pack_codes<4>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
-        case 5: pack_codes<5>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
-        case 6: pack_codes<6>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
-        default: pack_codes<7>(d, l, n_words, full, base, stage, escm, row_base, wave_esc); break;
+      if (threadIdx.x < 16u) {  // zero padding of index and escapes
+        const uint32_t t = threadIdx.x;
+        if (2 * n_blocks + t < s_esc - s_idx) stage[s_idx + 2 * n_blocks + t] = 0;
+        if (n_esc + t < s_end - s_esc) stage[s_esc + n_esc + t] = 0;
       }
-      if (l.lane == 0) sh.esc_w[l.wave] = wave_esc;
     }
-    __syncthreads();  // B4: offset known, codes staged, escape totals known
+    __syncthreads();  // B5: offset known, staging complete
 
-    // ---- data: sign/mantissa plane to the payload; escape index and
-    // escapes into staging behind the codes
-    const uint64_t n = n_words;
-    const uint32_t code_bytes = (uint32_t)((n * k + 7) / 8);
-    const uint32_t n_blocks = k ? (n_words + 511u) / 512u : 0u;
-    const uint32_t s_idx = (uint32_t)pad16(code_bytes);          // staging offsets
-    const uint32_t s_esc = s_idx + (uint32_t)pad16(2 * n_blocks);
-    const uint32_t s_end = s_esc + (uint32_t)pad16(n_esc);
-    const uint64_t rec_off = (uint64_t)uniform(sh.off_lo) | ((uint64_t)uniform(sh.off_hi) << 32);
-    uint8_t *rec = a.payload + rec_off;
+    // ---- data: the record body
     if (!is_ctl && dirty) {
+      const uint64_t rec_off = (uint64_t)uniform(sh.off_lo) | ((uint64_t)uniform(sh.off_hi) << 32);
+      uint8_t *rec = a.payload + rec_off;
       if (mode == 0) {
         store_chunk(rec + 16, len, l, d, true);
       } else {
@@ -938,44 +1000,11 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
           const uint32_t w0 = (l.off0 + h * kRow) >> 1;
           if (w0 < n_words) *reinterpret_cast<uint2 *>(sm_at + w0) = sm_bytes(d[h]);
         }
-        if (pack) {
-          uint32_t wave_base = 0;
-          for (uint32_t w = 0; w < l.wave; ++w) wave_base += sh.esc_w[w];
-          wave_base = uniform(wave_base);
-#pragma unroll
-          for (int h = 0; h < kRows; ++h) {
-            const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-            if (l.lane == 0 && w0 < n_words)  // this row is escape-index block w0/512
-              *reinterpret_cast<uint16_t *>(stage + s_idx + 2 * (w0 >> 9)) =
-                  (uint16_t)(wave_base + row_base[h]);
-            const uint32_t flags = (escm[h >> 2] >> (8 * (h & 3))) & 255u;
-            const uint32_t cnt = __popc(flags);
-            uint32_t rank = wave_base + row_base[h] + wave_incl_scan(cnt) - cnt;
-            if (flags) {
-              const uint32_t xx[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
-#pragma unroll
-              for (int u = 0; u < 8; ++u) {
-                if ((flags >> u) & 1u) {
-                  stage[s_esc + rank] = (uint8_t)((xx[u >> 1] >> (7 + 16 * (u & 1))) & 255u);
-                  ++rank;
-                }
-              }
-            }
-          }
-        }
-        if (threadIdx.x < 16u) {  // zero padding of index, escapes and sm plane
-          const uint32_t t = threadIdx.x;
-          if (2 * n_blocks + t < s_esc - s_idx) stage[s_idx + 2 * n_blocks + t] = 0;
-          if (n_esc + t < s_end - s_esc) stage[s_esc + n_esc + t] = 0;
-          if (n_words + t < pad16(n)) sm_at[n_words + t] = 0;
-        }
+        for (uint32_t i = threadIdx.x; i < s_end / 16u; i += kThreads)
+          *reinterpret_cast<uint4 *>(rec + 16 + 16 * i) =
+              *reinterpret_cast<const uint4 *>(stage + 16 * i);
+        if (threadIdx.x < 16u && n_words + threadIdx.x < pad16(n)) sm_at[n_words + threadIdx.x] = 0;
       }
-    }
-    __syncthreads();  // B5: staging complete
-    if (!is_ctl && dirty && mode == 1u) {
-      for (uint32_t i = threadIdx.x; i < s_end / 16u; i += kThreads)
-        *reinterpret_cast<uint4 *>(rec + 16 + 16 * i) =
-            *reinterpret_cast<const uint4 *>(stage + 16 * i);
     }
     if (!is_ctl) {
 #pragma unroll
@@ -1115,7 +1144,7 @@ constexpr uint32_t kMetaSkip = 0xFFu;    // table entry rejected: no record stat
 struct DecMeta {
   uint32_t st;  // 0 decode, kMetaSkip, else the record's status
   uint32_t mode, k, base, n_words, n_esc, c, src_crc, r;
-  uint32_t off_lo, off_hi, code_off, esc_off, sm_off;
+  uint32_t off_lo, off_hi, rlen, esc_off, sm_off;
   uint32_t pad_[2];
   uint32_t ent[68];  // escape index; entries from n_blocks on read n_esc
 };
@@ -1126,7 +1155,7 @@ struct DecShared {
 };
 static_assert(sizeof(DecShared) <= kLdsMiscBytes, "decoder scratch fits");
 constexpr uint32_t kLdsDecEsc = kLdsMisc + kLdsMiscBytes;
-constexpr uint32_t kLdsDecode = kLdsDecEsc + kWaves * kDecEscBytes;
+constexpr uint32_t kLdsDecode = kLdsDecEsc + kWaves * kDecEscBytes + 16;  // + read slack
 static_assert(kLdsDecode <= 163840, "decoder LDS fits one CU");
 
 __device__ __forceinline__ DecShared &dec_shared() {
@@ -1227,7 +1256,7 @@ __device__ void dec_prepare(const uint8_t *__restrict__ payload, uint64_t table_
     M.r = r;
     M.off_lo = (uint32_t)off;
     M.off_hi = (uint32_t)(off >> 32);
-    M.code_off = 16;
+    M.rlen = st == 0 ? (uint32_t)reclen : 0u;
     M.esc_off = (uint32_t)esc_off;
     M.sm_off = (uint32_t)sm_off;
   }
@@ -1243,6 +1272,7 @@ struct DecBuf {
 
 struct DecView {  // uniform fields of a record as a data wave needs them
   const uint8_t *rec;
+  uint32_t rlen;    // bytes of the record the loads may touch (0: none)
   uint32_t mode, k, base, n_words, n_esc, len;
   uint32_t E0, Ee;  // the wave's escape range from the index
   uint32_t al;      // 16-byte aligned start of the prefetched escape window
@@ -1254,6 +1284,7 @@ __device__ __forceinline__ DecView dec_view(const uint8_t *payload, const DecMet
   DecView v;
   const uint64_t off = (uint64_t)uniform(M.off_lo) | ((uint64_t)uniform(M.off_hi) << 32);
   v.rec = payload + off;
+  v.rlen = uniform(M.rlen);
   v.mode = uniform(M.mode);
   v.k = uniform(M.k);
   v.base = uniform(M.base);
@@ -1270,31 +1301,21 @@ __device__ __forceinline__ DecView dec_view(const uint8_t *payload, const DecMet
   return v;
 }
 
+// The same 17 loads for every record kind (RAW rows in a[]; codes, sign /
+// mantissa bytes and the escape window otherwise), through descriptors that
+// cover the record, so the compiler can count them on every path.
 __device__ __forceinline__ void dec_load(DecBuf &B, const DecView &v, const Lane &l) {
-  if (v.mode == 0) {
-    load_chunk(v.rec + 16, v.len, l, B.a);
-    return;
-  }
+  const bool raw = v.mode == 0;
+  const Rsrc ra = rsrc(v.rec, v.rlen);
+  const Rsrc rb = rsrc(v.rec, raw ? 0u : v.rlen);
 #pragma unroll
   for (int h = 0; h < kRows; ++h) {
     const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-    B.a[h] = make_uint4(0, 0, 0, 0);
-    B.b[h] = make_uint2(0, 0);
-    if (w0 < v.n_words) {
-      if (v.k) {
-        const uint32_t a4 = ((w0 >> 3) * v.k) & ~3u;
-        const uint3 x = *reinterpret_cast<const uint3 *>(v.rec + 16 + a4);
-        B.a[h] = make_uint4(x.x, x.y, x.z, 0);
-      }
-      B.b[h] = *reinterpret_cast<const uint2 *>(v.rec + v.sm_off + w0);
-    }
+    const uint32_t offa = 16u + (raw ? l.off0 + h * kRow : ((w0 >> 3) * v.k) & ~3u);
+    B.a[h] = buf16(ra, offa);
+    B.b[h] = buf8(rb, v.sm_off + w0);
   }
-  B.e = make_uint4(0, 0, 0, 0);
-  if (v.k) {
-    const uint32_t e0c = min(v.E0, v.n_esc), eec = min(max(v.Ee, e0c), v.n_esc);
-    const uint32_t at = v.al + 16u * l.lane;
-    if (at < eec) B.e = *reinterpret_cast<const uint4 *>(v.rec + v.esc_off + at);
-  }
+  B.e = buf16(rb, v.esc_off + v.al + 16u * l.lane);
 }
 
 __device__ __forceinline__ void dec_store(uint8_t *dst, uint32_t o, uint32_t len,
@@ -1403,26 +1424,33 @@ __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, co
         // the index entry of this block equals the escapes before it
         if (uniform(M.ent[row]) != acc) bad = true;
         if (__ballot((f.x | f.y) != 0)) {
-          const uint32_t cnt = __popc(f.x) + __popc(f.y);
+          // The lane's escapes are cnt consecutive bytes from rank r0 on;
+          // byte u of the lane takes escape number (flagged bytes before u).
+          const uint32_t bx = f.x >> K, by = f.y >> K;  // 0x01 per flagged byte
+          const uint32_t cx = __popc(bx), cnt = cx + __popc(by);
           const uint32_t incl = wave_incl_scan(cnt);
-          uint32_t rank = acc + incl - cnt;
+          const uint32_t r0 = acc + incl - cnt;
           acc += __builtin_amdgcn_readlane(incl, 63);
-          uint64_t ff = (uint64_t)f.x | ((uint64_t)f.y << 32);
-          uint64_t ev = (uint64_t)e.x | ((uint64_t)e.y << 32);
-          while (ff) {
-            const uint32_t bit = (uint32_t)__builtin_ctzll(ff) & ~7u;
-            ff &= ff - 1;
-            uint32_t x = 0;
-            if (rank < eec) {
-              const uint32_t at = rank - v.al;
-              x = at < kDecEscBytes ? stage[at] : v.rec[v.esc_off + rank];
-            } else {
-              bad = true;
+          if (cnt) {
+            if (r0 + cnt > eec) bad = true;
+            uint2 ev;
+            const uint32_t at = r0 - v.al;
+            if (at + cnt <= kDecEscBytes) {
+              const uint32_t *w = reinterpret_cast<const uint32_t *>(stage + (at & ~3u));
+              const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], sa = (at & 3u) * 8u;
+              ev = make_uint2(__builtin_amdgcn_alignbit(w1, w0, sa),
+                              __builtin_amdgcn_alignbit(w2, w1, sa));
+            } else {  // past the prefetched window
+              uint32_t t[2] = {0, 0};
+              for (uint32_t j = 0; j < cnt; ++j)
+                if (r0 + j < eec) t[j >> 2] |= (uint32_t)v.rec[v.esc_off + r0 + j] << (8 * (j & 3));
+              ev = make_uint2(t[0], t[1]);
             }
-            ++rank;
-            ev = (ev & ~(0xFFull << bit)) | ((uint64_t)x << bit);
+            const uint32_t px = (bx << 8) + (bx << 16) + (bx << 24);  // exclusive prefix
+            const uint32_t py = (by << 8) + (by << 16) + (by << 24) + cx * 0x01010101u;
+            e.x = bfi((bx << 8) - bx, __builtin_amdgcn_perm(ev.y, ev.x, px), e.x);
+            e.y = bfi((by << 8) - by, __builtin_amdgcn_perm(ev.y, ev.x, py), e.y);
           }
-          e = make_uint2((uint32_t)ev, (uint32_t)(ev >> 32));
         }
       }
       const uint2 lo = assemble4(e.x, B.b[h].x), hi = assemble4(e.y, B.b[h].y);
@@ -1473,15 +1501,20 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
   }
   __syncthreads();
   DecBuf cur, nxt;
-  if (!is_ctl && my_n > 0 && uniform(sh.meta[0].st) == 0)
-    dec_load(cur, dec_view(payload, sh.meta[0], l0, g), l0);
+  if (!is_ctl) {
+    DecView v0 = dec_view(payload, sh.meta[0], l0, g);
+    if (my_n == 0 || uniform(sh.meta[0].st) != 0) v0.rlen = 0;
+    dec_load(cur, v0, l0);
+  }
 
   for (uint32_t i = 0; i <= my_n; ++i) {
     const Lane l = lane_fresh(l0);
     if (!is_ctl) {
-      if (i + 1 < my_n) {
+      {
         const DecMeta &Mn = sh.meta[(i + 1) % 3];
-        if (uniform(Mn.st) == 0) dec_load(nxt, dec_view(payload, Mn, l, g), l);
+        DecView vn = dec_view(payload, Mn, l, g);
+        if (i + 1 >= my_n || uniform(Mn.st) != 0) vn.rlen = 0;  // loads become no-ops
+        dec_load(nxt, vn, l);
       }
       if (i < my_n) {
         const DecMeta &M = sh.meta[i % 3];
