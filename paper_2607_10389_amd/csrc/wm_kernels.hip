@@ -510,11 +510,11 @@ struct EncShared {
   uint32_t part[kWaves];     // wave CRC partials
   uint32_t dirty_w[kWaves];  // per-wave "differs from prev"
   uint32_t esc_w[kWaves];    // escapes per wave
-  uint32_t mode, k, base, n_esc, size, dirty, crc;
+  uint32_t crc;               // the chunk's CRC
   uint32_t first, next;      // tickets
   uint32_t off_lo, off_hi;   // record offset
+  alignas(16) uint4 cand[9];    // plan candidates: size, base | k << 8 | mode << 16, n_esc
   alignas(16) uint32_t H[256];  // histogram
-  alignas(16) uint32_t P[260];  // exclusive prefix of H (P[256] = n)
 };
 static_assert(sizeof(EncShared) <= kLdsMiscBytes, "encoder scratch fits");
 constexpr uint32_t kLdsHistE = kLdsMisc + kLdsMiscBytes;  // 256 bins x 16 copies
@@ -821,7 +821,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     __syncthreads();  // B2: H complete
 
     if (is_ctl) {
-      // ---- control: chunk CRC, plan, aggregate, first look-back window
+      // ---- control: chunk CRC
       if (l.lane == 0) ticket = atomicAdd(&ctl->ticket, 1u);  // handed out after B4
       uint32_t crc;
       if (need_crc) {
@@ -832,73 +832,73 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       } else {
         crc = ld_const(a.crc_in + c);
       }
-      uint32_t mode = 0, k = 0, base = 0, n_esc = 0;
-      uint64_t size = 0;
-      if (dirty) {
-        // Candidates in tie-break order (the first of equal sizes wins): RAW,
-        // a constant exponent, then windows of 2^k - 1 exponents for k = 1..7
-        // placed where they cover the most words (lowest base on ties).
-        const uint32_t lane = l.lane, b0 = lane * 4u;
-        const uint4 hv = *reinterpret_cast<const uint4 *>(&sh.H[b0]);
+      if (l.lane == 0) sh.crc = crc;
+    } else if (dirty) {
+      // ---- data: clear the copies for the next chunk; score the plan
+      // candidates, one per wave: waves 0..6 place a window of 2^k - 1
+      // exponents (k = wave + 1) where it covers the most words (lowest base
+      // on ties), wave 7 prices RAW and a constant exponent
+      uint4 *h4 = reinterpret_cast<uint4 *>(hist);
+      for (uint32_t i = threadIdx.x; i < 1024u; i += kThreads) h4[i] = make_uint4(0, 0, 0, 0);
+      const uint32_t lane = l.lane, b0 = lane * 4u;
+      const uint4 hv = *reinterpret_cast<const uint4 *>(&sh.H[b0]);
+      const uint64_t n = n_words;
+      if (l.wave < 7u) {
         const uint32_t t4 = hv.x + hv.y + hv.z + hv.w;
         const uint32_t ex = wave_incl_scan(t4) - t4;
-        *reinterpret_cast<uint4 *>(&sh.P[b0]) =
-            make_uint4(ex, ex + hv.x, ex + hv.x + hv.y, ex + hv.x + hv.y + hv.z);
-        if (lane == 63u) sh.P[256] = ex + t4;
+        const uint32_t pv[4] = {ex, ex + hv.x, ex + hv.x + hv.y, ex + hv.x + hv.y + hv.z};
+        uint32_t *P = reinterpret_cast<uint32_t *>(stage + l.wave * 1040u);  // free until B3
+        *reinterpret_cast<uint4 *>(P + b0) = make_uint4(pv[0], pv[1], pv[2], pv[3]);
+        if (lane == 63u) P[256] = ex + t4;
+        const uint32_t kk = l.wave + 1u, width = (1u << kk) - 1u;
+        uint32_t key = 0;
+#pragma unroll
+        for (uint32_t j = 0; j < 4; ++j) {
+          const uint32_t inside = P[min(b0 + j + width, 256u)] - pv[j];
+          key = max(key, (inside << 8) | (255u - (b0 + j)));
+        }
+        key = wave_max_u(key);
+        const uint32_t c_esc = n_words - (key >> 8);
+        const uint64_t sz = pad16((n * kk + 7) / 8) + pad16(2 * ((n + 511) / 512)) +
+                            pad16(c_esc) + pad16(n) + 16u;
+        if (lane == 0)
+          sh.cand[2 + l.wave] =
+              make_uint4((uint32_t)sz, (255u - (key & 255u)) | (kk << 8) | (1u << 16), c_esc, 0);
+      } else {
         const uint32_t nz = (hv.x ? 1u : 0u) | (hv.y ? 2u : 0u) | (hv.z ? 4u : 0u) | (hv.w ? 8u : 0u);
         const uint32_t n_distinct = __builtin_amdgcn_readlane(wave_incl_scan(__popc(nz)), 63);
         const uint32_t only = wave_max_u(nz ? b0 + 31u - __clz(nz) : 0u);
-        const uint64_t n = n_words;
-        size = 16u + pad16(2 * n);
-        if (n_distinct == 1 && 16u + pad16(n) < size) {
-          size = 16u + pad16(n);
-          mode = 1;
-          base = only;
-        }
-        const uint64_t fixed = pad16(2 * ((n + 511) / 512)) + pad16(n) + 16u;
-#pragma unroll 1
-        for (uint32_t kk = 1; kk <= 7; ++kk) {
-          const uint32_t width = (1u << kk) - 1u;
-          uint32_t key = 0;
-#pragma unroll
-          for (uint32_t j = 0; j < 4; ++j) {
-            const uint32_t b = b0 + j;
-            const uint32_t inside = sh.P[min(b + width, 256u)] - sh.P[b];
-            key = max(key, (inside << 8) | (255u - b));
-          }
-          key = wave_max_u(key);
-          const uint32_t c_esc = n_words - (key >> 8);
-          const uint64_t sz = pad16((n * kk + 7) / 8) + pad16(c_esc) + fixed;
-          if (sz < size) {
-            size = sz;
-            mode = 1;
-            k = kk;
-            base = 255u - (key & 255u);
-            n_esc = c_esc;
-          }
+        if (lane == 0) {
+          sh.cand[0] = make_uint4((uint32_t)(16u + pad16(2 * n)), 0, 0, 0);
+          sh.cand[1] = make_uint4(n_distinct == 1 ? (uint32_t)(16u + pad16(n)) : ~0u,
+                                  only | (1u << 16), 0, 0);
         }
       }
-      const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((size >> 4) << 26);
-      if (l.lane == 0) {
-        if (item != 0) status_store(&status[item], agg | kFlagAgg);
-        sh.mode = mode;
-        sh.k = k;
-        sh.base = base;
-        sh.n_esc = n_esc;
-        sh.size = (uint32_t)size;
-        sh.dirty = dirty ? 1u : 0u;
-        sh.crc = crc;
-      }
-      win = lookback_issue(status, (int64_t)item - 1);
-    } else if (dirty) {
-      // ---- data: clear the copies for the next chunk
-      uint4 *h4 = reinterpret_cast<uint4 *>(hist);
-      for (uint32_t i = threadIdx.x; i < 1024u; i += kThreads) h4[i] = make_uint4(0, 0, 0, 0);
     }
-    __syncthreads();  // B3: plan known
+    __syncthreads();  // B3: candidates scored
 
-    const uint32_t mode = uniform(sh.mode), k = uniform(sh.k), base = uniform(sh.base);
-    const uint32_t n_esc = uniform(sh.n_esc);
+    // ---- every wave: the plan is the smallest candidate, the first in the
+    // order RAW, constant, k = 1..7 on ties
+    uint32_t mode = 0, k = 0, base = 0, n_esc = 0, size = 0;
+    if (dirty) {
+      uint4 best = sh.cand[0];
+#pragma unroll
+      for (int i = 1; i < 9; ++i) {
+        const uint4 cc = sh.cand[i];
+        if (cc.x < best.x) best = cc;
+      }
+      size = uniform(best.x);
+      base = uniform(best.y) & 255u;
+      k = (uniform(best.y) >> 8) & 255u;
+      mode = uniform(best.y) >> 16;
+      n_esc = uniform(best.z);
+    }
+    if (is_ctl) {
+      // ---- control: aggregate, first look-back window (finished after B4)
+      const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(size >> 4) << 26);
+      if (l.lane == 0 && item != 0) status_store(&status[item], agg | kFlagAgg);
+      win = lookback_issue(status, (int64_t)item - 1);
+    }
     const bool pack = dirty && mode == 1u && k > 0u;
     const uint64_t n = n_words;
     const uint32_t code_bytes = (uint32_t)((n * k + 7) / 8);
@@ -933,7 +933,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       // packing phase to return), publish the prefix, header, table entry
       const uint32_t crc = uniform(sh.crc);
       const uint64_t excl = lookback_finish(status, (int64_t)item - 1, win, ctl);
-      const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(sh.size >> 4) << 26);
+      const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(size >> 4) << 26);
       const uint64_t incl = excl + (agg >> 2);
       const uint32_t rec_idx = (uint32_t)(excl & 0xFFFFFFu);
       const uint64_t rec_off = 64u + ((excl >> 24) << 4);
