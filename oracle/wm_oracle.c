@@ -24,7 +24,7 @@
  *   Record:
  *     0 u8 mode (0 RAW, 1 PACK)  1 u8 k  2 u8 base  3 u8 0
  *     4 u32 n_words  8 u32 n_esc  12 u32 rec_crc = CRC(record bytes 0..11)
- *     RAW : the chunk's bytes
+ *     RAW : exponent plane (n B, e of every word) | sign/mantissa plane (n B)
  *     PACK: codes (ceil(n*k/8) B, LSB-first k-bit codes) | escape index
  *           (ceil(n/512) u16: escaped words before each 512-word block)
  *           | escapes (n_esc B) | sign/mantissa plane (n B); k = 0 has only
@@ -204,7 +204,7 @@ static uint8_t sm_of(uint16_t w) {
   return (uint8_t)(((w >> 15) << 7) | (w & 127u));
 }
 
-static uint64_t raw_size(uint32_t n) { return 16 + pad16(2 * (uint64_t)n); }
+static uint64_t raw_size(uint32_t n) { return 16 + 2 * pad16(n); }
 /* escape-index entries: one per block of 512 words (k >= 1 only) */
 static uint64_t index_bytes(uint32_t n, uint32_t k) {
   return k ? 2 * (((uint64_t)n + 511) / 512) : 0;
@@ -309,7 +309,11 @@ static void write_record(int kind, const uint8_t *chunk, uint32_t len,
   put_u32(out + 12, orc_crc(kind, out, 12));
   uint8_t *body = out + 16;
   if (mode == 0) {
-    memcpy(body, chunk, len);
+    for (uint32_t i = 0; i < n; i++) {
+      uint16_t w = word_at(chunk, i);
+      body[i] = (uint8_t)exponent_of(w);
+      body[pad16(n) + i] = sm_of(w);
+    }
     return;
   }
   uint8_t *codes = body;
@@ -480,9 +484,13 @@ static uint32_t decode_record(int kind, const uint8_t *rec, uint64_t L,
   if (mode == 0) {
     if (k != 0 || base != 0 || n_esc != 0) return ORC_V_RECORD;
     if (L != raw_size(n)) return ORC_V_RECORD;
-    if (!all_zero(body + 2 * (uint64_t)n, pad16(2 * (uint64_t)n) - 2 * n))
+    const uint8_t *ex = body, *sm = body + pad16(n);
+    if (!all_zero(ex + n, pad16(n) - n) || !all_zero(sm + n, pad16(n) - n))
       return ORC_V_RECORD;
-    memcpy(out, body, len);
+    for (uint32_t i = 0; i < n; i++)
+      put_u16(out + 2 * (uint64_t)i,
+              (uint16_t)(((uint32_t)(sm[i] >> 7) << 15) | ((uint32_t)ex[i] << 7) |
+                         (sm[i] & 127u)));
   } else {
     if (k > 7 || n_esc > n || (k == 0 && n_esc != 0)) return ORC_V_RECORD;
     if (L != pack_size(n, k, n_esc)) return ORC_V_RECORD;

@@ -241,25 +241,6 @@ __device__ __forceinline__ void load_chunk(const uint8_t *__restrict__ base,
   }
 }
 
-// Store the first `len` bytes of a wave's rows (pieces that start below len
-// are stored whole when pad_ok; their bytes past len are zero).
-__device__ __forceinline__ void store_chunk(uint8_t *__restrict__ base,
-                                            uint32_t len, const Lane &l,
-                                            const uint4 (&d)[kRows],
-                                            bool pad_ok) {
-#pragma unroll
-  for (int h = 0; h < kRows; ++h) {
-    uint32_t off = l.off0 + h * kRow;
-    if (off + 16u <= len || (pad_ok && off < len)) {
-      *reinterpret_cast<uint4 *>(base + off) = d[h];
-    } else if (off < len) {
-      const uint32_t w[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
-      for (uint32_t b = 0; b < len - off; ++b)
-        base[off + b] = (uint8_t)(w[b >> 2] >> (8 * (b & 3)));
-    }
-  }
-}
-
 // Lane merge of the four column states and the 6-level lane tree; the wave
 // value Q is valid in lane 0.
 __device__ __forceinline__ uint32_t lane_tree(uint32_t v0, uint32_t v1, uint32_t v2,
@@ -653,6 +634,23 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
                                            uint32_t n_words, bool full, uint32_t base,
                                            uint8_t *stage, uint32_t (&escm)[2],
                                            uint32_t (&lane_r)[kRows], uint32_t &wave_esc) {
+  if constexpr (K == 8) {  // RAW: the exponent plane, one byte per word
+#pragma unroll
+    for (int h = 0; h < kRows; ++h) {
+      const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+      const uint4 x = d[h];
+      const uint32_t lo0 = __builtin_amdgcn_perm(x.y, x.x, 0x06040200u);
+      const uint32_t hi0 = __builtin_amdgcn_perm(x.y, x.x, 0x07050301u);
+      const uint32_t lo1 = __builtin_amdgcn_perm(x.w, x.z, 0x06040200u);
+      const uint32_t hi1 = __builtin_amdgcn_perm(x.w, x.z, 0x07050301u);
+      // e = (high byte << 1 | low byte >> 7) & 255, four words at a time
+      uint2 e = make_uint2(((hi0 << 1) & 0xFEFEFEFEu) | ((lo0 >> 7) & 0x01010101u),
+                           ((hi1 << 1) & 0xFEFEFEFEu) | ((lo1 >> 7) & 0x01010101u));
+      if (w0 < n_words) *reinterpret_cast<uint2 *>(stage + w0) = e;
+      lane_r[h] = 0;
+    }
+    return;
+  }
   constexpr uint32_t esc = (1u << K) - 1u;
   constexpr uint32_t esc2 = esc * 0x00010001u;
   const uint32_t base2 = base * 0x00010001u;
@@ -869,7 +867,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         const uint32_t n_distinct = __builtin_amdgcn_readlane(wave_incl_scan(__popc(nz)), 63);
         const uint32_t only = wave_max_u(nz ? b0 + 31u - __clz(nz) : 0u);
         if (lane == 0) {
-          sh.cand[0] = make_uint4((uint32_t)(16u + pad16(2 * n)), 0, 0, 0);
+          sh.cand[0] = make_uint4((uint32_t)(16u + 2 * pad16(n)), 0, 0, 0);  // RAW
           sh.cand[1] = make_uint4(n_distinct == 1 ? (uint32_t)(16u + pad16(n)) : ~0u,
                                   only | (1u << 16), 0, 0);
         }
@@ -899,10 +897,14 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       if (l.lane == 0 && item != 0) status_store(&status[item], agg | kFlagAgg);
       win = lookback_issue(status, (int64_t)item - 1);
     }
-    const bool pack = dirty && mode == 1u && k > 0u;
+    // staged: exponent-derived section of the record (RAW exponent plane, or
+    // codes + escape index + escapes); the sign/mantissa plane follows it
+    const uint32_t kbits = mode == 0 ? 8u : k;
+    const bool pack = dirty && kbits > 0u;
+    const bool has_esc = mode == 1u && k > 0u;
     const uint64_t n = n_words;
-    const uint32_t code_bytes = (uint32_t)((n * k + 7) / 8);
-    const uint32_t n_blocks = k ? (n_words + 511u) / 512u : 0u;
+    const uint32_t code_bytes = (uint32_t)((n * kbits + 7) / 8);
+    const uint32_t n_blocks = has_esc ? (n_words + 511u) / 512u : 0u;
     const uint32_t s_idx = (uint32_t)pad16(code_bytes);  // staging offsets
     const uint32_t s_esc = s_idx + (uint32_t)pad16(2 * n_blocks);
     const uint32_t s_end = s_esc + (uint32_t)pad16(n_esc);
@@ -911,18 +913,19 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     if (!is_ctl && pack) {
       // ---- data: codes into staging, escape flags and counts
       if (!full) {  // the wave's own code bytes; lanes past the chunk write none
-        uint4 *s4 = reinterpret_cast<uint4 *>(stage + l.wave * 512u * k);
-        for (uint32_t i = l.lane; i < 32u * k; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
+        uint4 *s4 = reinterpret_cast<uint4 *>(stage + l.wave * 512u * kbits);
+        for (uint32_t i = l.lane; i < 32u * kbits; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
       }
       uint32_t wave_esc = 0;
-      switch (k) {
+      switch (kbits) {
         case 1: pack_codes<1>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
         case 2: pack_codes<2>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
         case 3: pack_codes<3>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
         case 4: pack_codes<4>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
         case 5: pack_codes<5>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
         case 6: pack_codes<6>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-        default: pack_codes<7>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+        case 7: pack_codes<7>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+        default: pack_codes<8>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
       }
       if (l.lane == 0) sh.esc_w[l.wave] = wave_esc;
     }
@@ -959,7 +962,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         }
         if (a.crc_out && !bad_index) a.crc_out[c] = crc;
       }
-    } else if (pack) {
+    } else if (pack && has_esc) {
       // ---- data: escape index and escapes into staging behind the codes
       uint32_t wave_base = 0;
       for (uint32_t w = 0; w < l.wave; ++w) wave_base += sh.esc_w[w];
@@ -991,9 +994,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     if (!is_ctl && dirty) {
       const uint64_t rec_off = (uint64_t)uniform(sh.off_lo) | ((uint64_t)uniform(sh.off_hi) << 32);
       uint8_t *rec = a.payload + rec_off;
-      if (mode == 0) {
-        store_chunk(rec + 16, len, l, d, true);
-      } else {
+      {
         uint8_t *sm_at = rec + 16 + s_end;
 #pragma unroll
         for (int h = 0; h < kRows; ++h) {
@@ -1206,15 +1207,17 @@ __device__ void dec_prepare(const uint8_t *__restrict__ payload, uint64_t table_
     k = (hw[0] >> 8) & 255u;
     base = (hw[0] >> 16) & 255u;
     n_esc = hw[2];
-    code_bytes = ((uint64_t)n_words * k + 7) / 8;
-    n_blocks = k ? ((uint64_t)n_words + 511) / 512 : 0;
+    // RAW keeps one exponent byte per word where codes would be
+    const uint32_t kbits = mode == 0 ? 8u : k;
+    code_bytes = ((uint64_t)n_words * kbits + 7) / 8;
+    n_blocks = (mode == 1 && k) ? ((uint64_t)n_words + 511) / 512 : 0;
     idx_off = 16 + pad16(code_bytes);
     esc_off = idx_off + pad16(2 * n_blocks);
     sm_off = esc_off + pad16(n_esc);
     if (crc_words(hw, 3) != hw[3] || (hw[0] >> 24) || hw[1] != n_words || mode > 1) {
       st = 4;
     } else if (mode == 0) {
-      if (k || base || n_esc || reclen != 16u + pad16(2ull * n_words)) st = 4;
+      if (k || base || n_esc || reclen != 16u + 2 * pad16(n_words)) st = 4;
     } else if (k > 7 || n_esc > n_words || (k == 0 && n_esc) ||
                reclen != sm_off + pad16(n_words)) {
       st = 4;
@@ -1223,9 +1226,10 @@ __device__ void dec_prepare(const uint8_t *__restrict__ payload, uint64_t table_
   uint32_t entry = n_esc;
   if (st == 0) {
     bool bad = false;
-    if (mode == 0) {
-      const uint64_t at = 16u + 2ull * n_words + lane;
-      if (lane < 16u && at < 16u + pad16(2ull * n_words) && rec[at]) bad = true;
+    if (mode == 0) {  // padding of both planes
+      if (lane < 16u && n_words + lane < pad16(n_words) &&
+          (rec[16 + n_words + lane] | rec[sm_off + n_words + lane]))
+        bad = true;
     } else {
       // padding: whole bytes after each section, code bits past n*k
       if (lane < 16u) {
@@ -1247,7 +1251,7 @@ __device__ void dec_prepare(const uint8_t *__restrict__ payload, uint64_t table_
     M.ent[64] = n_esc;
     M.st = st;
     M.mode = mode;
-    M.k = k;
+    M.k = mode == 0 ? 8u : k;  // code bits per word
     M.base = base;
     M.n_words = n_words;
     M.n_esc = n_esc;
@@ -1301,21 +1305,18 @@ __device__ __forceinline__ DecView dec_view(const uint8_t *payload, const DecMet
   return v;
 }
 
-// The same 17 loads for every record kind (RAW rows in a[]; codes, sign /
-// mantissa bytes and the escape window otherwise), through descriptors that
-// cover the record, so the compiler can count them on every path.
+// The same 17 loads for every record (codes or RAW exponent bytes, sign /
+// mantissa bytes, the head of the wave's escape range) through a descriptor
+// that covers the record, so the compiler can count them on every path.
 __device__ __forceinline__ void dec_load(DecBuf &B, const DecView &v, const Lane &l) {
-  const bool raw = v.mode == 0;
-  const Rsrc ra = rsrc(v.rec, v.rlen);
-  const Rsrc rb = rsrc(v.rec, raw ? 0u : v.rlen);
+  const Rsrc r = rsrc(v.rec, v.rlen);
 #pragma unroll
   for (int h = 0; h < kRows; ++h) {
     const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-    const uint32_t offa = 16u + (raw ? l.off0 + h * kRow : ((w0 >> 3) * v.k) & ~3u);
-    B.a[h] = buf16(ra, offa);
-    B.b[h] = buf8(rb, v.sm_off + w0);
+    B.a[h] = buf16(r, 16u + (((w0 >> 3) * v.k) & ~3u));
+    B.b[h] = buf8(r, v.sm_off + w0);
   }
-  B.e = buf16(rb, v.esc_off + v.al + 16u * l.lane);
+  B.e = buf16(r, v.esc_off + v.al + 16u * l.lane);
 }
 
 __device__ __forceinline__ void dec_store(uint8_t *dst, uint32_t o, uint32_t len,
@@ -1340,7 +1341,9 @@ __device__ __forceinline__ uint2 unpack_codes(const uint4 &a, uint32_t sh) {
     return c;
   } else {
     const uint32_t v0 = __builtin_amdgcn_alignbit(a.y, a.x, sh);
-    if constexpr (K == 4) {
+    if constexpr (K == 8) {
+      c = make_uint2(a.x, a.y);  // byte aligned: sh is 0
+    } else if constexpr (K == 4) {
       const uint32_t t0 = __builtin_amdgcn_perm(0u, v0, 0x01010000u);  // b0 b0 b1 b1
       const uint32_t t1 = __builtin_amdgcn_perm(0u, v0, 0x03030202u);  // b2 b2 b3 b3
       c.x = (t0 & 0x000F000Fu) | ((t0 >> 4) & 0x0F000F00u);
@@ -1380,15 +1383,16 @@ template <uint32_t K>
 __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, const DecMeta &M,
                                            const Lane &l, uint8_t *stage, uint8_t *dst,
                                            uint32_t (&cv)[4], const GLane &gl) {
-  constexpr uint32_t esc = (1u << K) - 1u;
+  constexpr bool kEsc = K > 0 && K < 8;  // K = 8: RAW exponent bytes, no escapes
+  constexpr uint32_t esc = K < 8 ? (1u << K) - 1u : 255u;
   bool bad = false;
   uint32_t acc = v.E0;
   const uint32_t e0c = min(v.E0, v.n_esc), eec = min(max(v.Ee, e0c), v.n_esc);
   const uint32_t sh = ((l.lane * K) & 3u) * 8u;
   const uint32_t base4 = v.base * 0x01010101u;
-  const bool wrap = v.base + esc > 255u;  // a code can carry out of its byte
+  const bool wrap = kEsc && v.base + esc > 255u;  // a code can carry out of its byte
   const bool full = v.n_words == kChunk / 2;
-  if (K) *reinterpret_cast<uint4 *>(stage + 16u * l.lane) = B.e;
+  if (kEsc) *reinterpret_cast<uint4 *>(stage + 16u * l.lane) = B.e;
 #pragma unroll
   for (int h = 0; h < kRows; ++h) {
     const uint32_t row = l.wave * kRows + h;
@@ -1405,7 +1409,7 @@ __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, co
         c.y &= vm1;
       }
       uint2 f = make_uint2(0, 0);  // escape flags at bit 8u+K
-      if (K) {
+      if (kEsc) {
         f.x = (c.x + 0x01010101u) & (0x01010101u << K);
         f.y = (c.y + 0x01010101u) & (0x01010101u << K);
       }
@@ -1417,10 +1421,10 @@ __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, co
         const uint32_t s1 = ((c.y & 0x7F7F7F7Fu) + (base4 & 0x7F7F7F7Fu)) ^ ((c.y ^ base4) & 0x80808080u);
         const uint32_t k0 = ((c.x & base4) | ((c.x | base4) & ~s0)) & 0x80808080u;
         const uint32_t k1 = ((c.y & base4) | ((c.y | base4) & ~s1)) & 0x80808080u;
-        if ((k0 & ~(f.x << (7 - K)) & vm0) | (k1 & ~(f.y << (7 - K)) & vm1)) bad = true;
+        if ((k0 & ~(f.x << (7 - (K & 7))) & vm0) | (k1 & ~(f.y << (7 - (K & 7))) & vm1)) bad = true;
         e = make_uint2(s0, s1);
       }
-      if (K) {
+      if (kEsc) {
         // the index entry of this block equals the escapes before it
         if (uniform(M.ent[row]) != acc) bad = true;
         if (__ballot((f.x | f.y) != 0)) {
@@ -1471,7 +1475,7 @@ __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, co
     cv[3] = g_step(cv[3] ^ out[3], gl);
     dec_store(dst, l.off0 + h * kRow, v.len, out);
   }
-  if (K && acc != v.Ee) bad = true;  // the wave's escapes end where the next block's begin
+  if (kEsc && acc != v.Ee) bad = true;  // the wave's escapes end where the next block's begin
   return bad;
 }
 
@@ -1523,26 +1527,16 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
           uint8_t *dst = staging + (uint64_t)v.r * kChunk;
           uint32_t cv[4] = {0, 0, 0, 0};
           bool bad = false;
-          if (v.mode == 0) {
-#pragma unroll
-            for (int h = 0; h < kRows; ++h) {
-              cv[0] = g_step(cv[0] ^ cur.a[h].x, gl);
-              cv[1] = g_step(cv[1] ^ cur.a[h].y, gl);
-              cv[2] = g_step(cv[2] ^ cur.a[h].z, gl);
-              cv[3] = g_step(cv[3] ^ cur.a[h].w, gl);
-            }
-            store_chunk(dst, v.len, l, cur.a, false);
-          } else {
-            switch (v.k) {
-              case 0: bad = dec_packed<0>(cur, v, M, l, stage, dst, cv, gl); break;
-              case 1: bad = dec_packed<1>(cur, v, M, l, stage, dst, cv, gl); break;
-              case 2: bad = dec_packed<2>(cur, v, M, l, stage, dst, cv, gl); break;
-              case 3: bad = dec_packed<3>(cur, v, M, l, stage, dst, cv, gl); break;
-              case 4: bad = dec_packed<4>(cur, v, M, l, stage, dst, cv, gl); break;
-              case 5: bad = dec_packed<5>(cur, v, M, l, stage, dst, cv, gl); break;
-              case 6: bad = dec_packed<6>(cur, v, M, l, stage, dst, cv, gl); break;
-              default: bad = dec_packed<7>(cur, v, M, l, stage, dst, cv, gl); break;
-            }
+          switch (v.k) {  // 8: RAW exponent plane
+            case 0: bad = dec_packed<0>(cur, v, M, l, stage, dst, cv, gl); break;
+            case 1: bad = dec_packed<1>(cur, v, M, l, stage, dst, cv, gl); break;
+            case 2: bad = dec_packed<2>(cur, v, M, l, stage, dst, cv, gl); break;
+            case 3: bad = dec_packed<3>(cur, v, M, l, stage, dst, cv, gl); break;
+            case 4: bad = dec_packed<4>(cur, v, M, l, stage, dst, cv, gl); break;
+            case 5: bad = dec_packed<5>(cur, v, M, l, stage, dst, cv, gl); break;
+            case 6: bad = dec_packed<6>(cur, v, M, l, stage, dst, cv, gl); break;
+            case 7: bad = dec_packed<7>(cur, v, M, l, stage, dst, cv, gl); break;
+            default: bad = dec_packed<8>(cur, v, M, l, stage, dst, cv, gl); break;
           }
           const uint32_t q = lane_tree(cv[0], cv[1], cv[2], cv[3]);
           const bool any_bad = __ballot(bad) != 0;

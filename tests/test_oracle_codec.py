@@ -9,7 +9,8 @@ code paths:
     16-bit words -> RAW);
   * a brute-force argmin over every (k, base) on tiny chunks;
   * escape-index entries counted word by word;
-  * hand-built expected bytes for a two-chunk payload, with CRCs from zlib.
+  * hand-built expected bytes for a three-chunk payload (PACK k=0, PACK
+    k=2, RAW), with CRCs from zlib.
 """
 import struct
 import zlib
@@ -89,7 +90,7 @@ def brute_force_plan(words):
     and for a given k the smallest base.  Counts escapes word by word."""
     n = len(words)
     e = [(int(w) >> 7) & 255 for w in words]
-    best = (16 + pad16(2 * n), 0, 0, 0, 0)  # size, mode, k, base, n_esc
+    best = (16 + 2 * pad16(n), 0, 0, 0, 0)  # size, mode, k, base, n_esc
     if len(set(e)) == 1:
         s = 16 + pad16(n)
         if s < best[0]:
@@ -132,15 +133,17 @@ def test_plan_matches_brute_force(seed):
 
 
 def test_hand_built_payload():
-    """Two 4 KiB chunks: chunk 0 constant 1.0 (PACK k=0), chunk 1 exponents
-    cycling base..base+2 with k=2.  Expected bytes (header, records, then the
+    """Three 4 KiB chunks: chunk 0 constant 1.0 (PACK k=0), chunk 1 exponents
+    cycling base..base+2 with k=2, chunk 2 random bits (RAW: exponent plane,
+    then sign/mantissa plane).  Expected bytes (header, records, then the
     table) are written out here from the format text, CRCs from zlib."""
     n = CH // 2
     c0 = np.full(n, 0x3F80, np.uint16)
     e1 = 120 + (np.arange(n) % 3)
     sm1 = (np.arange(n) * 37) % 256
     c1 = (((sm1 >> 7) << 15) | (e1 << 7) | (sm1 & 127)).astype(np.uint16)
-    state = np.concatenate([c0, c1]).view(np.uint8)
+    c2 = np.random.default_rng(77).integers(0, 65536, n).astype(np.uint16)
+    state = np.concatenate([c0, c1, c2]).view(np.uint8)
 
     def rec(mode, k, base, n_esc, body):
         h = struct.pack("<BBBBII", mode, k, base, 0, n, n_esc)
@@ -156,14 +159,18 @@ def test_hand_built_payload():
                 codes[j // 8] |= 1 << (j % 8)
     index = bytes(16)  # 4 blocks of 512 words, no escapes: four zero u16
     r1 = rec(1, 2, 120, 0, bytes(codes) + index + sm1.astype(np.uint8).tobytes())
+    e2 = bytes(int((w >> 7) & 255) for w in c2)
+    s2 = bytes(int(((w >> 15) << 7) | (w & 127)) for w in c2)
+    r2 = rec(0, 0, 0, 0, e2 + s2)
     table = struct.pack("<IIQ", 0, zlib.crc32(c0.tobytes()), 64)
     table += struct.pack("<IIQ", 1, zlib.crc32(c1.tobytes()), 64 + len(r0))
-    total = 64 + len(r0) + len(r1) + len(table)
-    head = b"WMV1" + struct.pack("<HBBIIQIIQII", 1, 0, 1, CH, 2, state.size,
-                                 2, 1, total, zlib.crc32(state.tobytes()),
+    table += struct.pack("<IIQ", 2, zlib.crc32(c2.tobytes()), 64 + len(r0) + len(r1))
+    total = 64 + len(r0) + len(r1) + len(r2) + len(table)
+    head = b"WMV1" + struct.pack("<HBBIIQIIQII", 1, 0, 1, CH, 3, state.size,
+                                 3, 1, total, zlib.crc32(state.tobytes()),
                                  zlib.crc32(table)) + bytes(12)
     head += struct.pack("<I", zlib.crc32(head))
-    want = head + r0 + r1 + table
+    want = head + r0 + r1 + r2 + table
     got = oracle.encode(0, state, CH).tobytes()
     assert len(got) == len(want) == total
     assert got == want
