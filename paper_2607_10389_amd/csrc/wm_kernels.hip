@@ -470,7 +470,7 @@ __global__ __launch_bounds__(1024) void k_compact(const uint32_t *__restrict__ f
 
 constexpr int kModeList = 0, kModeAll = 1, kModeStep = 2;
 constexpr uint64_t kFlagAgg = 1, kFlagIncl = 2;
-constexpr uint32_t kLookbackWindow = 256;  // predecessors read per round trip
+constexpr uint32_t kLookbackWindow = 512;  // predecessors read per round trip
 constexpr int kEncThreads = kThreads + 64;
 
 struct EncArgs {
@@ -709,6 +709,21 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
   }
 }
 
+// The encoder runs one chunk behind on output: iteration i computes chunk
+// X_i (CRC, histogram, plan, codes staged in LDS, sign/mantissa bytes kept
+// in registers) and writes the record of X_{i-1}, whose payload offset the
+// control wave resolved by look-back at the start of iteration i.  By then
+// the predecessors of X_{i-1} have published their sizes an iteration ago,
+// so the look-back finishes within the first phase and nothing waits on it.
+//   phase 1 (..B1): data: prefetch X_{i+1}, CRC and histogram of X_i;
+//                   control: look-back of X_{i-1}, its prefix, header and
+//                   table entry; next ticket
+//   phase 2 (..B2): data: reduce the histogram; control: CRC of X_i
+//   phase 3 (..B3): data: write X_{i-1} (staging + sign/mantissa bytes),
+//                   score the plan candidates of X_i
+//   phase 4 (..B4): all: pick X_i's plan; control: publish its size;
+//                   data: codes into staging, escape counts, sign/mantissa
+//   phase 5:        data: escape index and escapes into staging
 template <bool HAS_PREV>
 __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(a.ws + a.L.ctl);
@@ -737,7 +752,6 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   uint32_t item = uniform(sh.first);
   uint32_t next = uniform(sh.next);
 
-  // data-wave state
   const GLane gl = glane_make();
   const Lane l0 = lane_info();
   uint4 d[kRows];
@@ -746,20 +760,31 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     load_chunk(a.cur + (uint64_t)(c < g.n_chunks ? c : 0u) * kChunk,
                c < g.n_chunks ? chunk_len(g, c) : 0u, l0, d);
   }
-  while (item < n_items) {
-    Window win;           // control wave: look-back window in flight
-    uint32_t ticket = 0;  // control wave: the ticket after `next`
+
+  // the chunk whose record is still to be written (uniform), and its
+  // sign/mantissa bytes (data waves)
+  bool pend = false, p_dirty = false, p_bad = false;
+  uint32_t p_item = 0, p_c = 0, p_nw = 0, p_mode = 0, p_k = 0, p_base = 0, p_nesc = 0;
+  uint32_t p_size = 0, p_send = 0, p_crc = 0;
+  uint2 smp[kRows];
+#pragma unroll
+  for (int h = 0; h < kRows; ++h) smp[h] = make_uint2(0, 0);
+
+  while (item < n_items || pend) {
+    const bool cur = item < n_items;
     const Lane l = lane_fresh(l0);
     const uint32_t copy4 = (l.lane & 15u) * 4u;
-    uint32_t c = uniform(item_chunk(a, item, g));
-    const bool bad_index = c >= g.n_chunks;
-    if (bad_index) c = 0;
-    const uint32_t len = bad_index ? 0u : chunk_len(g, c);
+    uint32_t c = cur ? uniform(item_chunk(a, item, g)) : 0u;
+    const bool bad_index = cur && c >= g.n_chunks;
+    if (!cur || bad_index) c = 0;
+    const uint32_t len = (cur && !bad_index) ? chunk_len(g, c) : 0u;
     const uint32_t n_words = len / 2;
     const bool full = len == kChunk;
     uint4 dn[kRows];
+    uint32_t ticket = 0;
 
-    // ---- data: prefetch, CRC streams, diff
+    // ---- phase 1
+    Window win;
     if (!is_ctl) {
       uint4 p[kRows];
       if (HAS_PREV) load_chunk(a.prev + (uint64_t)c * kChunk, len, l, p);
@@ -768,7 +793,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         load_chunk(a.cur + (uint64_t)(cn < g.n_chunks ? cn : 0u) * kChunk,
                    cn < g.n_chunks ? chunk_len(g, cn) : 0u, l, dn);
       }
-      if (need_crc) {
+      if (need_crc && cur) {
         const uint32_t q = wave_q(d, gl);
         if (l.lane == 0) sh.part[l.wave] = mat_apply(T.wave_mat[l.wave], q);
       }
@@ -778,20 +803,52 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         for (int h = 0; h < kRows; ++h)
           diff |= (d[h].x ^ p[h].x) | (d[h].y ^ p[h].y) | (d[h].z ^ p[h].z) | (d[h].w ^ p[h].w);
         const unsigned long long any = __ballot(diff != 0);
-        if (l.lane == 0) sh.dirty_w[l.wave] = (any && !bad_index) ? 1u : 0u;
+        if (l.lane == 0) sh.dirty_w[l.wave] = any ? 1u : 0u;
       }
+    } else {
+      if (cur && l.lane == 0) ticket = atomicAdd(&ctl->ticket, 1u);
+      if (pend) win = lookback_issue(status, (int64_t)p_item - 1);
     }
-    bool dirty = !bad_index;
+    bool dirty = cur && !bad_index;
     if (HAS_PREV) {
       __syncthreads();  // B0: per-wave diff flags
       uint32_t dw = 0;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) dw |= sh.dirty_w[w];
-      dirty = uniform(dw) != 0;
+      dirty = dirty && uniform(dw) != 0;
     }
-
-    // ---- data: exponent histogram (16 copies x 256 bins)
-    if (!is_ctl && dirty) {
+    if (is_ctl) {
+      if (pend) {
+        // ---- control: X_{i-1}'s offset, prefix, header and table entry
+        const uint64_t excl = lookback_finish(status, (int64_t)p_item - 1, win, ctl);
+        const uint64_t agg = ((uint64_t)(p_dirty ? 1u : 0u) << 2) | ((uint64_t)(p_size >> 4) << 26);
+        const uint64_t incl = excl + (agg >> 2);
+        const uint32_t rec_idx = (uint32_t)(excl & 0xFFFFFFu);
+        const uint64_t rec_off = 64u + ((excl >> 24) << 4);
+        uint32_t hw[4] = {p_mode | (p_k << 8) | (p_base << 16), p_nw, p_nesc, 0};
+        hw[3] = crc_words(hw, 3);
+        uint32_t ew[4] = {p_c, p_crc, (uint32_t)rec_off, (uint32_t)(rec_off >> 32)};
+        const uint32_t eck = crc_words(ew, 4);
+        if (l.lane == 0) {
+          status_store(&status[p_item], (incl << 2) | kFlagIncl);
+          if (p_item + 1 == n_items) {
+            ctl->n_rec = (uint32_t)(incl & 0xFFFFFFu);
+            ctl->payload_bytes = (incl >> 24) << 4;  // total record bytes
+          }
+          if (p_bad) atomicOr(&ctl->error, 2u);
+          sh.off_lo = (uint32_t)rec_off;
+          sh.off_hi = (uint32_t)(rec_off >> 32);
+          if (p_dirty) {
+            *reinterpret_cast<uint4 *>(a.payload + rec_off) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+            tab_ws[rec_idx] = make_uint4(ew[0], ew[1], ew[2], ew[3]);
+            ecrc[rec_idx] = eck;
+            if (a.dirty_idx) a.dirty_idx[rec_idx] = p_c;
+          }
+          if (a.crc_out && !p_bad) a.crc_out[p_c] = p_crc;
+        }
+      }
+    } else if (dirty) {
+      // ---- data: exponent histogram (16 copies x 256 bins)
 #pragma unroll
       for (int h = 0; h < kRows; ++h) {
         const uint32_t w0 = (l.off0 + h * kRow) >> 1;
@@ -805,10 +862,24 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         }
       }
     }
-    __syncthreads();  // B1: histogram copies and CRC partials complete
+    __syncthreads();  // B1: histogram copies, CRC partials, X_{i-1}'s offset
 
-    // ---- data: reduce the copies, 32 bins per wave
-    if (!is_ctl && dirty) {
+    // ---- phase 2
+    uint32_t crc = 0;
+    if (is_ctl) {
+      if (cur) {
+        if (need_crc) {
+          uint32_t raw = 0;
+#pragma unroll
+          for (int w = 0; w < kWaves; ++w) raw ^= sh.part[w];
+          crc = bad_index ? 0u : finish_crc(raw, len, g, T);
+        } else {
+          crc = bad_index ? 0u : ld_const(a.crc_in + c);
+        }
+        if (l.lane == 0) sh.next = ticket;
+      }
+    } else if (dirty) {
+      // reduce the copies: wave w sums bins 32w..32w+31 (its own 2 KiB of them)
       const uint32_t bin = l.wave * 32u + (l.lane >> 1), half = l.lane & 1u;
       uint32_t s = 0;
 #pragma unroll
@@ -818,65 +889,72 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     }
     __syncthreads();  // B2: H complete
 
-    if (is_ctl) {
-      // ---- control: chunk CRC
-      if (l.lane == 0) ticket = atomicAdd(&ctl->ticket, 1u);  // handed out after B4
-      uint32_t crc;
-      if (need_crc) {
-        uint32_t raw = 0;
+    // ---- phase 3
+    if (!is_ctl) {
+      if (pend && p_dirty) {
+        // write X_{i-1}: staged section, then its sign/mantissa plane
+        const uint64_t rec_off = (uint64_t)uniform(sh.off_lo) | ((uint64_t)uniform(sh.off_hi) << 32);
+        uint8_t *rec = a.payload + rec_off;
+        for (uint32_t i = threadIdx.x; i < p_send / 16u; i += kThreads)
+          *reinterpret_cast<uint4 *>(rec + 16 + 16 * i) =
+              *reinterpret_cast<const uint4 *>(stage + 16 * i);
+        uint8_t *sm_at = rec + 16 + p_send;
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) raw ^= sh.part[w];
-        crc = bad_index ? 0u : finish_crc(raw, len, g, T);
-      } else {
-        crc = ld_const(a.crc_in + c);
+        for (int h = 0; h < kRows; ++h) {
+          const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+          if (w0 < p_nw) *reinterpret_cast<uint2 *>(sm_at + w0) = smp[h];
+        }
+        if (threadIdx.x < 16u && p_nw + threadIdx.x < pad16(p_nw)) sm_at[p_nw + threadIdx.x] = 0;
       }
-      if (l.lane == 0) sh.crc = crc;
-    } else if (dirty) {
-      // ---- data: clear the copies for the next chunk; score the plan
-      // candidates, one per wave: waves 0..6 place a window of 2^k - 1
-      // exponents (k = wave + 1) where it covers the most words (lowest base
-      // on ties), wave 7 prices RAW and a constant exponent
-      uint4 *h4 = reinterpret_cast<uint4 *>(hist);
-      for (uint32_t i = threadIdx.x; i < 1024u; i += kThreads) h4[i] = make_uint4(0, 0, 0, 0);
-      const uint32_t lane = l.lane, b0 = lane * 4u;
-      const uint4 hv = *reinterpret_cast<const uint4 *>(&sh.H[b0]);
-      const uint64_t n = n_words;
-      if (l.wave < 7u) {
-        const uint32_t t4 = hv.x + hv.y + hv.z + hv.w;
-        const uint32_t ex = wave_incl_scan(t4) - t4;
-        const uint32_t pv[4] = {ex, ex + hv.x, ex + hv.x + hv.y, ex + hv.x + hv.y + hv.z};
-        uint32_t *P = reinterpret_cast<uint32_t *>(stage + l.wave * 1040u);  // free until B3
-        *reinterpret_cast<uint4 *>(P + b0) = make_uint4(pv[0], pv[1], pv[2], pv[3]);
-        if (lane == 63u) P[256] = ex + t4;
-        const uint32_t kk = l.wave + 1u, width = (1u << kk) - 1u;
-        uint32_t key = 0;
+      if (dirty) {
+        // score the plan candidates, one per wave: waves 0..6 place a window
+        // of 2^k - 1 exponents (k = wave + 1) where it covers the most words
+        // (lowest base on ties), wave 7 prices RAW and a constant exponent;
+        // each wave's prefix scratch lives in its own, already reduced, 2 KiB
+        // of the histogram copies, which it clears afterwards
+        const uint32_t lane = l.lane, b0 = lane * 4u;
+        const uint4 hv = *reinterpret_cast<const uint4 *>(&sh.H[b0]);
+        const uint64_t n = n_words;
+        uint32_t *slice = hist + l.wave * 512u;
+        if (l.wave < 7u) {
+          const uint32_t t4 = hv.x + hv.y + hv.z + hv.w;
+          const uint32_t ex = wave_incl_scan(t4) - t4;
+          const uint32_t pv[4] = {ex, ex + hv.x, ex + hv.x + hv.y, ex + hv.x + hv.y + hv.z};
+          uint32_t *P = slice;
+          *reinterpret_cast<uint4 *>(P + b0) = make_uint4(pv[0], pv[1], pv[2], pv[3]);
+          if (lane == 63u) P[256] = ex + t4;
+          const uint32_t kk = l.wave + 1u, width = (1u << kk) - 1u;
+          uint32_t key = 0;
 #pragma unroll
-        for (uint32_t j = 0; j < 4; ++j) {
-          const uint32_t inside = P[min(b0 + j + width, 256u)] - pv[j];
-          key = max(key, (inside << 8) | (255u - (b0 + j)));
+          for (uint32_t j = 0; j < 4; ++j) {
+            const uint32_t inside = P[min(b0 + j + width, 256u)] - pv[j];
+            key = max(key, (inside << 8) | (255u - (b0 + j)));
+          }
+          key = wave_max_u(key);
+          const uint32_t c_esc = n_words - (key >> 8);
+          const uint64_t sz = pad16((n * kk + 7) / 8) + pad16(2 * ((n + 511) / 512)) +
+                              pad16(c_esc) + pad16(n) + 16u;
+          if (lane == 0)
+            sh.cand[2 + l.wave] =
+                make_uint4((uint32_t)sz, (255u - (key & 255u)) | (kk << 8) | (1u << 16), c_esc, 0);
+        } else {
+          const uint32_t nz = (hv.x ? 1u : 0u) | (hv.y ? 2u : 0u) | (hv.z ? 4u : 0u) | (hv.w ? 8u : 0u);
+          const uint32_t n_distinct = __builtin_amdgcn_readlane(wave_incl_scan(__popc(nz)), 63);
+          const uint32_t only = wave_max_u(nz ? b0 + 31u - __clz(nz) : 0u);
+          if (lane == 0) {
+            sh.cand[0] = make_uint4((uint32_t)(16u + 2 * pad16(n)), 0, 0, 0);  // RAW
+            sh.cand[1] = make_uint4(n_distinct == 1 ? (uint32_t)(16u + pad16(n)) : ~0u,
+                                    only | (1u << 16), 0, 0);
+          }
         }
-        key = wave_max_u(key);
-        const uint32_t c_esc = n_words - (key >> 8);
-        const uint64_t sz = pad16((n * kk + 7) / 8) + pad16(2 * ((n + 511) / 512)) +
-                            pad16(c_esc) + pad16(n) + 16u;
-        if (lane == 0)
-          sh.cand[2 + l.wave] =
-              make_uint4((uint32_t)sz, (255u - (key & 255u)) | (kk << 8) | (1u << 16), c_esc, 0);
-      } else {
-        const uint32_t nz = (hv.x ? 1u : 0u) | (hv.y ? 2u : 0u) | (hv.z ? 4u : 0u) | (hv.w ? 8u : 0u);
-        const uint32_t n_distinct = __builtin_amdgcn_readlane(wave_incl_scan(__popc(nz)), 63);
-        const uint32_t only = wave_max_u(nz ? b0 + 31u - __clz(nz) : 0u);
-        if (lane == 0) {
-          sh.cand[0] = make_uint4((uint32_t)(16u + 2 * pad16(n)), 0, 0, 0);  // RAW
-          sh.cand[1] = make_uint4(n_distinct == 1 ? (uint32_t)(16u + pad16(n)) : ~0u,
-                                  only | (1u << 16), 0, 0);
-        }
+        uint4 *s4 = reinterpret_cast<uint4 *>(slice);
+        for (uint32_t i = l.lane; i < 128u; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
       }
     }
-    __syncthreads();  // B3: candidates scored
+    __syncthreads();  // B3: candidates scored, X_{i-1}'s staging read
 
-    // ---- every wave: the plan is the smallest candidate, the first in the
-    // order RAW, constant, k = 1..7 on ties
+    // ---- phase 4: every wave picks the plan, the smallest candidate (the
+    // first in the order RAW, constant, k = 1..7 on ties)
     uint32_t mode = 0, k = 0, base = 0, n_esc = 0, size = 0;
     if (dirty) {
       uint4 best = sh.cand[0];
@@ -891,14 +969,9 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       mode = uniform(best.y) >> 16;
       n_esc = uniform(best.z);
     }
-    if (is_ctl) {
-      // ---- control: aggregate, first look-back window (finished after B4)
-      const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(size >> 4) << 26);
-      if (l.lane == 0 && item != 0) status_store(&status[item], agg | kFlagAgg);
-      win = lookback_issue(status, (int64_t)item - 1);
-    }
-    // staged: exponent-derived section of the record (RAW exponent plane, or
-    // codes + escape index + escapes); the sign/mantissa plane follows it
+    // staged: the exponent-derived section of the record (RAW exponent
+    // plane, or codes + escape index + escapes); the sign/mantissa plane
+    // follows it
     const uint32_t kbits = mode == 0 ? 8u : k;
     const bool pack = dirty && kbits > 0u;
     const bool has_esc = mode == 1u && k > 0u;
@@ -910,60 +983,38 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     const uint32_t s_end = s_esc + (uint32_t)pad16(n_esc);
     uint32_t escm[2] = {0, 0};
     uint32_t lane_r[kRows];
-    if (!is_ctl && pack) {
-      // ---- data: codes into staging, escape flags and counts
-      if (!full) {  // the wave's own code bytes; lanes past the chunk write none
-        uint4 *s4 = reinterpret_cast<uint4 *>(stage + l.wave * 512u * kbits);
-        for (uint32_t i = l.lane; i < 32u * kbits; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
+    if (is_ctl) {
+      if (cur && item != 0 && l.lane == 0) {
+        const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(size >> 4) << 26);
+        status_store(&status[item], agg | kFlagAgg);
       }
-      uint32_t wave_esc = 0;
-      switch (kbits) {
-        case 1: pack_codes<1>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-        case 2: pack_codes<2>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-        case 3: pack_codes<3>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-        case 4: pack_codes<4>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-        case 5: pack_codes<5>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-        case 6: pack_codes<6>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-        case 7: pack_codes<7>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-        default: pack_codes<8>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+    } else if (dirty) {
+      if (pack) {
+        // ---- data: codes into staging, escape flags and counts
+        if (!full) {  // the wave's own code bytes; lanes past the chunk write none
+          uint4 *s4 = reinterpret_cast<uint4 *>(stage + l.wave * 512u * kbits);
+          for (uint32_t i = l.lane; i < 32u * kbits; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
+        }
+        uint32_t wave_esc = 0;
+        switch (kbits) {
+          case 1: pack_codes<1>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+          case 2: pack_codes<2>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+          case 3: pack_codes<3>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+          case 4: pack_codes<4>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+          case 5: pack_codes<5>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+          case 6: pack_codes<6>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+          case 7: pack_codes<7>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+          default: pack_codes<8>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+        }
+        if (l.lane == 0) sh.esc_w[l.wave] = wave_esc;
       }
-      if (l.lane == 0) sh.esc_w[l.wave] = wave_esc;
+#pragma unroll
+      for (int h = 0; h < kRows; ++h) smp[h] = sm_bytes(d[h]);
     }
     __syncthreads();  // B4: codes staged, escape totals known
 
-    if (is_ctl) {
-      // ---- control: finish the look-back (its reads have had the whole
-      // packing phase to return), publish the prefix, header, table entry
-      const uint32_t crc = uniform(sh.crc);
-      const uint64_t excl = lookback_finish(status, (int64_t)item - 1, win, ctl);
-      const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(size >> 4) << 26);
-      const uint64_t incl = excl + (agg >> 2);
-      const uint32_t rec_idx = (uint32_t)(excl & 0xFFFFFFu);
-      const uint64_t rec_off = 64u + ((excl >> 24) << 4);
-      uint32_t hw[4] = {mode | (k << 8) | (base << 16), n_words, n_esc, 0};
-      hw[3] = crc_words(hw, 3);
-      uint32_t ew[4] = {c, crc, (uint32_t)rec_off, (uint32_t)(rec_off >> 32)};
-      const uint32_t eck = crc_words(ew, 4);
-      if (l.lane == 0) {
-        status_store(&status[item], (incl << 2) | kFlagIncl);
-        if (item + 1 == n_items) {
-          ctl->n_rec = (uint32_t)(incl & 0xFFFFFFu);
-          ctl->payload_bytes = (incl >> 24) << 4;  // total record bytes
-        }
-        if (bad_index) atomicOr(&ctl->error, 2u);
-        sh.off_lo = (uint32_t)rec_off;
-        sh.off_hi = (uint32_t)(rec_off >> 32);
-        sh.next = ticket;
-        if (dirty) {
-          *reinterpret_cast<uint4 *>(a.payload + rec_off) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-          tab_ws[rec_idx] = make_uint4(ew[0], ew[1], ew[2], ew[3]);
-          ecrc[rec_idx] = eck;
-          if (a.dirty_idx) a.dirty_idx[rec_idx] = c;
-        }
-        if (a.crc_out && !bad_index) a.crc_out[c] = crc;
-      }
-    } else if (pack && has_esc) {
-      // ---- data: escape index and escapes into staging behind the codes
+    // ---- phase 5
+    if (!is_ctl && pack && has_esc) {
       uint32_t wave_base = 0;
       for (uint32_t w = 0; w < l.wave; ++w) wave_base += sh.esc_w[w];
       wave_base = uniform(wave_base);
@@ -988,34 +1039,29 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         if (n_esc + t < s_end - s_esc) stage[s_esc + n_esc + t] = 0;
       }
     }
-    __syncthreads();  // B5: offset known, staging complete
 
-    // ---- data: the record body
-    if (!is_ctl && dirty) {
-      const uint64_t rec_off = (uint64_t)uniform(sh.off_lo) | ((uint64_t)uniform(sh.off_hi) << 32);
-      uint8_t *rec = a.payload + rec_off;
-      {
-        uint8_t *sm_at = rec + 16 + s_end;
-#pragma unroll
-        for (int h = 0; h < kRows; ++h) {
-          const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-          if (w0 < n_words) *reinterpret_cast<uint2 *>(sm_at + w0) = sm_bytes(d[h]);
-        }
-        for (uint32_t i = threadIdx.x; i < s_end / 16u; i += kThreads)
-          *reinterpret_cast<uint4 *>(rec + 16 + 16 * i) =
-              *reinterpret_cast<const uint4 *>(stage + 16 * i);
-        if (threadIdx.x < 16u && n_words + threadIdx.x < pad16(n)) sm_at[n_words + threadIdx.x] = 0;
-      }
-    }
+    // ---- X_i becomes the pending record
+    pend = cur;
+    p_item = item;
+    p_c = c;
+    p_nw = n_words;
+    p_dirty = dirty;
+    p_bad = bad_index;
+    p_mode = mode;
+    p_k = k;
+    p_base = base;
+    p_nesc = n_esc;
+    p_size = size;
+    p_send = s_end;
+    p_crc = crc;
     if (!is_ctl) {
 #pragma unroll
       for (int h = 0; h < kRows; ++h) d[h] = dn[h];
     }
     item = next;
-    next = uniform(sh.next);
+    if (cur) next = uniform(sh.next);
   }
 }
-
 
 // Zero the control block and the look-back words before an encode.
 __global__ void k_encode_prepare(uint8_t *ws, WsLayout L, uint32_t n) {
