@@ -470,7 +470,7 @@ __global__ __launch_bounds__(1024) void k_compact(const uint32_t *__restrict__ f
 
 constexpr int kModeList = 0, kModeAll = 1, kModeStep = 2;
 constexpr uint64_t kFlagAgg = 1, kFlagIncl = 2;
-constexpr uint32_t kLookbackWindow = 512;  // predecessors read per round trip
+constexpr uint32_t kLookbackWindow = 256;  // predecessors read per round trip
 constexpr int kEncThreads = kThreads + 64;
 
 struct EncArgs {
@@ -560,8 +560,10 @@ __device__ __forceinline__ uint32_t item_chunk(const EncArgs &a, uint32_t item,
 
 // Look-back (control wave).  lookback_issue reads a window of predecessors
 // before other work; lookback_finish consumes it and reads further windows
-// only if needed.  Every item publishes its aggregate before its own
-// look-back and tickets go to running workgroups in order, so each
+// only if needed.  The workgroup's own previous item (`known`, whose
+// inclusive prefix it computed itself) ends the walk, so a look-back never
+// reads further back than the items handed out since that one.  Every item
+// publishes its aggregate before its own look-back and tickets go to running workgroups in order, so each
 // predecessor publishes eventually; the spin bound only guarantees that the
 // kernel terminates if that were ever violated (the call then reports an
 // empty payload).
@@ -569,19 +571,21 @@ struct Window {
   uint64_t s[kLookbackWindow / 64];
 };
 
-__device__ __forceinline__ Window lookback_issue(const uint64_t *status, int64_t top) {
+__device__ __forceinline__ Window lookback_issue(const uint64_t *status, int64_t top,
+                                                 int64_t known, uint64_t known_incl) {
   Window w;
   const uint32_t lane = threadIdx.x & 63u;
 #pragma unroll
   for (int q = 0; q < (int)(kLookbackWindow / 64); ++q) {
-    int64_t j = top - (int64_t)(lane * (kLookbackWindow / 64) + q);
-    w.s[q] = j >= 0 ? status_load(&status[j]) : kFlagIncl;
+    const int64_t j = top - (int64_t)(lane * (kLookbackWindow / 64) + q);
+    w.s[q] = j > known ? status_load(&status[j])
+                       : (j == known ? (known_incl << 2) | kFlagIncl : kFlagIncl);
   }
   return w;
 }
 
 __device__ uint64_t lookback_finish(const uint64_t *status, int64_t top, Window w,
-                                    WsCtl *ctl) {
+                                    int64_t known, uint64_t known_incl, WsCtl *ctl) {
   constexpr int Q = kLookbackWindow / 64;
   const uint32_t lane = threadIdx.x & 63u;
   uint64_t excl = 0;
@@ -611,7 +615,7 @@ __device__ uint64_t lookback_finish(const uint64_t *status, int64_t top, Window 
         break;
       }
       __builtin_amdgcn_s_sleep(2);
-      w = lookback_issue(status, top);
+      w = lookback_issue(status, top, known, known_incl);
       continue;
     }
 #pragma unroll
@@ -619,7 +623,7 @@ __device__ uint64_t lookback_finish(const uint64_t *status, int64_t top, Window 
     excl += v;
     if (stop != 0xFFFFFFFFu) break;
     top -= kLookbackWindow;
-    w = lookback_issue(status, top);
+    w = lookback_issue(status, top, known, known_incl);
   }
   return excl;
 }
@@ -766,6 +770,8 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   bool pend = false, p_dirty = false, p_bad = false;
   uint32_t p_item = 0, p_c = 0, p_nw = 0, p_mode = 0, p_k = 0, p_base = 0, p_nesc = 0;
   uint32_t p_size = 0, p_send = 0, p_crc = 0;
+  int64_t my_last = -1;      // control: this workgroup's last finished item
+  uint64_t my_last_incl = 0; //          and its inclusive prefix
   uint2 smp[kRows];
 #pragma unroll
   for (int h = 0; h < kRows; ++h) smp[h] = make_uint2(0, 0);
@@ -807,7 +813,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       }
     } else {
       if (cur && l.lane == 0) ticket = atomicAdd(&ctl->ticket, 1u);
-      if (pend) win = lookback_issue(status, (int64_t)p_item - 1);
+      if (pend) win = lookback_issue(status, (int64_t)p_item - 1, my_last, my_last_incl);
     }
     bool dirty = cur && !bad_index;
     if (HAS_PREV) {
@@ -820,9 +826,12 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     if (is_ctl) {
       if (pend) {
         // ---- control: X_{i-1}'s offset, prefix, header and table entry
-        const uint64_t excl = lookback_finish(status, (int64_t)p_item - 1, win, ctl);
+        const uint64_t excl =
+            lookback_finish(status, (int64_t)p_item - 1, win, my_last, my_last_incl, ctl);
         const uint64_t agg = ((uint64_t)(p_dirty ? 1u : 0u) << 2) | ((uint64_t)(p_size >> 4) << 26);
         const uint64_t incl = excl + (agg >> 2);
+        my_last = p_item;
+        my_last_incl = incl;
         const uint32_t rec_idx = (uint32_t)(excl & 0xFFFFFFu);
         const uint64_t rec_off = 64u + ((excl >> 24) << 4);
         uint32_t hw[4] = {p_mode | (p_k << 8) | (p_base << 16), p_nw, p_nesc, 0};
