@@ -563,8 +563,9 @@ __device__ __forceinline__ uint32_t item_chunk(const EncArgs &a, uint32_t item,
 // only if needed.  The workgroup's own previous item (`known`, whose
 // inclusive prefix it computed itself) ends the walk, so a look-back never
 // reads further back than the items handed out since that one.  Every item
-// publishes its aggregate before its own look-back and tickets go to running workgroups in order, so each
-// predecessor publishes eventually; the spin bound only guarantees that the
+// publishes its aggregate before its own look-back and tickets go to running
+// workgroups in order, so each predecessor publishes eventually; the spin
+// bound only guarantees that the
 // kernel terminates if that were ever violated (the call then reports an
 // empty payload).
 struct Window {
