@@ -270,6 +270,12 @@ __device__ __forceinline__ uint32_t wave_q(const uint4 (&d)[kRows],
   return lane_tree(v0, v1, v2, v3);
 }
 
+// The wave's share of the chunk's raw CRC: its value Q (lane 0) shifted past
+// the rows of the later waves, computed on the scalar unit.
+__device__ __forceinline__ uint32_t wave_part(const CrcTables &T, uint32_t wave, uint32_t q) {
+  return mat_apply(T.wave_mat[wave], uniform(q));
+}
+
 // Chunk CRC from the raw (zero-init, padded) value of the whole chunk.
 __device__ __forceinline__ uint32_t finish_crc(uint32_t raw, uint32_t len,
                                                const ChunkGeom &g, const CrcTables &T) {
@@ -295,7 +301,8 @@ __global__ __launch_bounds__(kThreads) void k_checksum(
     load_chunk(data + (uint64_t)(cn < g.n_chunks ? cn : c) * kChunk,
                cn < g.n_chunks ? chunk_len(g, cn) : 0u, l, dn);
     const uint32_t q = wave_q(d, gl);
-    if (l.lane == 0) misc()[M_PART + l.wave] = mat_apply(T.wave_mat[l.wave], q);
+    const uint32_t part = wave_part(T, l.wave, q);
+    if (l.lane == 0) misc()[M_PART + l.wave] = part;
     __syncthreads();
     if (threadIdx.x == 0) {
       uint32_t raw = 0;
@@ -565,9 +572,8 @@ __device__ __forceinline__ uint32_t item_chunk(const EncArgs &a, uint32_t item,
 // reads further back than the items handed out since that one.  Every item
 // publishes its aggregate before its own look-back and tickets go to running
 // workgroups in order, so each predecessor publishes eventually; the spin
-// bound only guarantees that the
-// kernel terminates if that were ever violated (the call then reports an
-// empty payload).
+// bound only guarantees that the kernel terminates if that were ever
+// violated (the call then reports an empty payload).
 struct Window {
   uint64_t s[kLookbackWindow / 64];
 };
@@ -802,7 +808,8 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       }
       if (need_crc && cur) {
         const uint32_t q = wave_q(d, gl);
-        if (l.lane == 0) sh.part[l.wave] = mat_apply(T.wave_mat[l.wave], q);
+        const uint32_t part = wave_part(T, l.wave, q);
+        if (l.lane == 0) sh.part[l.wave] = part;
       }
       if (HAS_PREV) {
         uint32_t diff = 0;
@@ -1205,8 +1212,17 @@ struct DecMeta {
   uint32_t pad_[2];
   uint32_t ent[68];  // escape index; entries from n_blocks on read n_esc
 };
+struct CtlRec {  // one record in the control pipeline (LDS, written by lane 0)
+  uint32_t valid;  // record exists and its table entry passed its checks
+  uint32_t r, c, src_crc;
+  uint64_t off, end;
+  uint4 ent;       // the entry as read (for the table CRC)
+  uint4 hdr;       // record header (step 2)
+};
+
 struct DecShared {
   DecMeta meta[3];
+  CtlRec cr[4];  // control pipeline, slot = record step & 3
   uint32_t part[2][kWaves];  // wave CRC partials
   uint32_t bad[2][kWaves];   // wave structure failures
 };
@@ -1219,46 +1235,110 @@ __device__ __forceinline__ DecShared &dec_shared() {
   return *reinterpret_cast<DecShared *>(lds + kLdsMisc);
 }
 
-// Control wave: checks of table entry r and of its record, layout into M.
-__device__ void dec_prepare(const uint8_t *__restrict__ payload, uint64_t table_off,
-                            uint32_t n_rec, uint32_t r, const ChunkGeom &g,
-                            uint32_t *__restrict__ ecrc, WsCtl *ctl, DecMeta &M) {
+// Control wave: record checks in three steps, each a memory round trip that
+// depends on the previous one (table entry, record header, padding and
+// escape index).  The decoder runs them for three different records in each
+// iteration, so the control wave waits for one round trip per record.
+
+// Steps 1 and 2 are split into issue and record halves: the loads go out
+// as vector loads (which complete in order), step 3 of an older record runs
+// while they are in flight, and only then are the results recorded in R.
+struct CtlLoads {
+  uint4 ent, nx, hdr;
+};
+
+// Step 1: table entry r and the next one.
+__device__ __forceinline__ void ctl_entry_issue(const uint8_t *__restrict__ payload,
+                                                uint64_t table_off, uint32_t n_rec, uint32_t r,
+                                                bool exists, CtlLoads &L) {
+  const uint32_t bytes = !exists ? 0u : (r + 1 < n_rec ? 32u : 16u);
+  const Rsrc rs = rsrc(payload + table_off + 16ull * r, bytes);
+  L.ent = buf16(rs, 0);
+  L.nx = buf16(rs, 16);
+}
+
+__device__ __forceinline__ void ctl_entry_record(uint64_t table_off, uint32_t n_rec, uint32_t r,
+                                                 bool exists, const ChunkGeom &g,
+                                                 const CtlLoads &L, CtlRec &R) {
+  uint32_t valid = 0, c = 0, src = 0;
+  uint64_t off = 0, end = 0;
+  uint4 ent = make_uint4(0, 0, 0, 0);
+  if (exists) {
+    ent = make_uint4(uniform(L.ent.x), uniform(L.ent.y), uniform(L.ent.z), uniform(L.ent.w));
+    c = ent.x;
+    src = ent.y;
+    off = (uint64_t)ent.z | ((uint64_t)ent.w << 32);
+    end = table_off;
+    bool tbad = false;
+    if (r + 1 < n_rec) {
+      end = (uint64_t)uniform(L.nx.z) | ((uint64_t)uniform(L.nx.w) << 32);
+      tbad = uniform(L.nx.x) <= c;
+    }
+    tbad = tbad || c >= g.n_chunks || (r == 0 && off != 64u) || (off & 15u) || off >= end ||
+           end > table_off;
+    valid = tbad ? 2u : 1u;  // 2: entry rejected
+  }
+  if ((threadIdx.x & 63u) == 0) {
+    R.valid = valid;
+    R.r = r;
+    R.c = c;
+    R.src_crc = src;
+    R.off = off;
+    R.end = end;
+    R.ent = ent;
+  }
+}
+
+// Step 2: the record header of R.
+__device__ __forceinline__ void ctl_header_issue(const uint8_t *__restrict__ payload,
+                                                 const CtlRec &R, CtlLoads &L) {
+  const uint32_t valid = uniform(R.valid);
+  const uint64_t off = ((uint64_t)uniform((uint32_t)(R.off >> 32)) << 32) | uniform((uint32_t)R.off);
+  const uint64_t end = ((uint64_t)uniform((uint32_t)(R.end >> 32)) << 32) | uniform((uint32_t)R.end);
+  L.hdr = buf16(rsrc(payload + off, valid == 1u && end - off >= 16u ? 16u : 0u), 0);
+}
+
+__device__ __forceinline__ void ctl_header_record(const CtlLoads &L, CtlRec &R) {
+  const uint4 h = make_uint4(uniform(L.hdr.x), uniform(L.hdr.y), uniform(L.hdr.z), uniform(L.hdr.w));
+  if ((threadIdx.x & 63u) == 0) R.hdr = h;
+}
+
+// Step 3: header rules, padding, escape index; the layout goes to M.
+__device__ __forceinline__ void ctl_body(const uint8_t *__restrict__ payload, const CtlRec &RL,
+                                         const ChunkGeom &g, uint32_t *__restrict__ ecrc,
+                                         WsCtl *ctl, DecMeta &M) {
   const uint32_t lane = threadIdx.x & 63u;
-  const uint8_t *e = payload + table_off + 16ull * r;
-  const uint4 ent = *reinterpret_cast<const uint4 *>(e);
-  const uint32_t c = ent.x;
-  const uint64_t off = (uint64_t)ent.z | ((uint64_t)ent.w << 32);
-  uint64_t end = table_off;
-  bool tbad = false;
-  if (r + 1 < n_rec) {
-    const uint4 nx = *reinterpret_cast<const uint4 *>(e + 16);
-    end = (uint64_t)nx.z | ((uint64_t)nx.w << 32);
-    tbad = nx.x <= c;
-  }
+  CtlRec R;  // uniform copy
+  R.valid = uniform(RL.valid);
+  if (R.valid == 0u) return;  // no such record
+  R.r = uniform(RL.r);
+  R.c = uniform(RL.c);
+  R.src_crc = uniform(RL.src_crc);
+  R.off = ((uint64_t)uniform((uint32_t)(RL.off >> 32)) << 32) | uniform((uint32_t)RL.off);
+  R.end = ((uint64_t)uniform((uint32_t)(RL.end >> 32)) << 32) | uniform((uint32_t)RL.end);
+  R.ent = make_uint4(uniform(RL.ent.x), uniform(RL.ent.y), uniform(RL.ent.z), uniform(RL.ent.w));
+  R.hdr = make_uint4(uniform(RL.hdr.x), uniform(RL.hdr.y), uniform(RL.hdr.z), uniform(RL.hdr.w));
   {
-    uint32_t ew[4] = {ent.x, ent.y, ent.z, ent.w};
+    uint32_t ew[4] = {R.ent.x, R.ent.y, R.ent.z, R.ent.w};
     const uint32_t ec = crc_words(ew, 4);
-    if (lane == 0) ecrc[r] = ec;
+    if (lane == 0) ecrc[R.r] = ec;
   }
-  tbad = tbad || c >= g.n_chunks || (r == 0 && off != 64u) || (off & 15u) || off >= end ||
-         end > table_off;
-  if (tbad) {
+  if (R.valid == 2u) {
     if (lane == 0) {
       atomicOr(&ctl->table_bad, 1u);
       M.st = kMetaSkip;
     }
     return;
   }
-  const uint32_t len = chunk_len(g, c), n_words = len / 2;
-  const uint64_t reclen = end - off;
-  const uint8_t *rec = payload + off;
+  const uint32_t len = chunk_len(g, R.c), n_words = len / 2;
+  const uint64_t reclen = R.end - R.off;
+  const uint8_t *rec = payload + R.off;
   uint32_t st = 0, mode = 0, k = 0, base = 0, n_esc = 0;
   uint64_t code_bytes = 0, n_blocks = 0, idx_off = 16, esc_off = 16, sm_off = 16;
   if (reclen < 16) {
     st = 4;
   } else {
-    const uint4 h4 = *reinterpret_cast<const uint4 *>(rec);
-    uint32_t hw[4] = {h4.x, h4.y, h4.z, h4.w};
+    uint32_t hw[4] = {R.hdr.x, R.hdr.y, R.hdr.z, R.hdr.w};
     mode = hw[0] & 255u;
     k = (hw[0] >> 8) & 255u;
     base = (hw[0] >> 16) & 255u;
@@ -1311,11 +1391,11 @@ __device__ void dec_prepare(const uint8_t *__restrict__ payload, uint64_t table_
     M.base = base;
     M.n_words = n_words;
     M.n_esc = n_esc;
-    M.c = c;
-    M.src_crc = ent.y;
-    M.r = r;
-    M.off_lo = (uint32_t)off;
-    M.off_hi = (uint32_t)(off >> 32);
+    M.c = R.c;
+    M.src_crc = R.src_crc;
+    M.r = R.r;
+    M.off_lo = (uint32_t)R.off;
+    M.off_hi = (uint32_t)(R.off >> 32);
     M.rlen = st == 0 ? (uint32_t)reclen : 0u;
     M.esc_off = (uint32_t)esc_off;
     M.sm_off = (uint32_t)sm_off;
@@ -1555,9 +1635,19 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
   const uint32_t my_n = blockIdx.x < n_rec ? (n_rec - 1 - blockIdx.x) / G + 1 : 0;
   auto rec_of = [&](uint32_t i) { return blockIdx.x + i * G; };
 
+  // control pipeline: in step i, records i+2 (body), i+3 (header) and i+4
+  // (entry)
   if (is_ctl) {
-    for (uint32_t i = 0; i < 2 && i < my_n; ++i)
-      dec_prepare(payload, table_off, n_rec, rec_of(i), g, ecrc, ctl, sh.meta[i]);
+    CtlLoads L;
+    for (uint32_t j = 0; j < 4; ++j) {
+      ctl_entry_issue(payload, table_off, n_rec, rec_of(j), j < my_n, L);
+      ctl_entry_record(table_off, n_rec, rec_of(j), j < my_n, g, L, sh.cr[j]);
+    }
+    for (uint32_t j = 0; j < 3; ++j) {
+      ctl_header_issue(payload, sh.cr[j], L);
+      ctl_header_record(L, sh.cr[j]);
+    }
+    for (uint32_t j = 0; j < 2; ++j) ctl_body(payload, sh.cr[j], g, ecrc, ctl, sh.meta[j]);
   }
   __syncthreads();
   DecBuf cur, nxt;
@@ -1595,9 +1685,10 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
             default: bad = dec_packed<8>(cur, v, M, l, stage, dst, cv, gl); break;
           }
           const uint32_t q = lane_tree(cv[0], cv[1], cv[2], cv[3]);
+          const uint32_t part = wave_part(T, l.wave, q);
           const bool any_bad = __ballot(bad) != 0;
           if (l.lane == 0) {
-            sh.part[i & 1][l.wave] = mat_apply(T.wave_mat[l.wave], q);
+            sh.part[i & 1][l.wave] = part;
             sh.bad[i & 1][l.wave] = any_bad ? 1u : 0u;
           }
         }
@@ -1624,8 +1715,12 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
           }
         }
       }
-      if (i + 2 < my_n)
-        dec_prepare(payload, table_off, n_rec, rec_of(i + 2), g, ecrc, ctl, sh.meta[(i + 2) % 3]);
+      CtlLoads L;
+      ctl_header_issue(payload, sh.cr[(i + 3) & 3], L);
+      ctl_entry_issue(payload, table_off, n_rec, rec_of(i + 4), i + 4 < my_n, L);
+      ctl_body(payload, sh.cr[(i + 2) & 3], g, ecrc, ctl, sh.meta[(i + 2) % 3]);
+      ctl_header_record(L, sh.cr[(i + 3) & 3]);
+      ctl_entry_record(table_off, n_rec, rec_of(i + 4), i + 4 < my_n, g, L, sh.cr[(i + 4) & 3]);
     }
     __syncthreads();
     if (!is_ctl) cur = nxt;
