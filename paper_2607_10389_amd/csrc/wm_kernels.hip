@@ -270,10 +270,19 @@ __device__ __forceinline__ uint32_t wave_q(const uint4 (&d)[kRows],
   return lane_tree(v0, v1, v2, v3);
 }
 
+// A uniform pointer the compiler cannot see through: loads through it stay
+// where they are used instead of being hoisted out of a chunk loop, where 32
+// matrix columns would otherwise occupy scalar registers for the whole loop.
+template <typename P>
+__device__ __forceinline__ P *opaque(P *p) {
+  asm volatile("" : "+s"(p));
+  return p;
+}
+
 // The wave's share of the chunk's raw CRC: its value Q (lane 0) shifted past
 // the rows of the later waves, computed on the scalar unit.
 __device__ __forceinline__ uint32_t wave_part(const CrcTables &T, uint32_t wave, uint32_t q) {
-  return mat_apply(T.wave_mat[wave], uniform(q));
+  return mat_apply(opaque(T.wave_mat[wave]), uniform(q));
 }
 
 // Chunk CRC from the raw (zero-init, padded) value of the whole chunk.

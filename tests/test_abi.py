@@ -1,0 +1,137 @@
+"""The C ABI without a GPU: libwm.so loads, exports every function that
+include/wm.h declares, and its host-side argument checks return the documented
+status codes before any device work.  Addresses passed here are never
+dereferenced (every call fails validation first)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+LIB = os.path.join(ROOT, "paper_2607_10389_amd", "libwm.so")
+HEADER = os.path.join(ROOT, "include", "wm.h")
+
+OK, VERIFY_FAILED, INVALID, CAPACITY, HIP, WORKSPACE, UNSUPPORTED = 0, 1, -1, -2, -3, -4, -5
+CH = 65536
+ALIGNED = 0x7f0000001000  # a well-formed 16-byte aligned address, never touched
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("chunk_bytes", ctypes.c_uint32), ("crc_kind", ctypes.c_uint32),
+                ("codec", ctypes.c_uint32), ("flags", ctypes.c_uint32)]
+
+
+def declared():
+    text = open(HEADER).read()
+    return re.findall(r"^\s*(?:const\s+char\s*\*|wm_status|uint64_t)\s*(wm_\w+)\s*\(",
+                      text, flags=re.M)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        pytest.skip("libwm.so is not built")
+    L = ctypes.CDLL(LIB)
+    vp, u64, u32, pp = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.POINTER(Params)
+    L.wm_status_str.restype = ctypes.c_char_p
+    L.wm_status_str.argtypes = [ctypes.c_int32]
+    L.wm_workspace_bytes.restype = u64
+    L.wm_workspace_bytes.argtypes = [u64, pp]
+    L.wm_payload_bound.restype = u64
+    L.wm_payload_bound.argtypes = [u64, u32, pp]
+    L.wm_checksum_chunks.argtypes = [vp, u64, pp, vp, vp, vp]
+    L.wm_diff_dirty.argtypes = [vp, vp, u64, pp, vp, vp, vp, u64, vp]
+    L.wm_encode.argtypes = [vp, u64, pp, vp, vp, vp, vp, u64, vp, vp, u64, vp]
+    L.wm_encode_step.argtypes = [vp, vp, u64, pp, vp, vp, vp, vp, vp, u64, vp, vp, u64, vp]
+    L.wm_decode_verify.argtypes = [vp, u64, u64, pp, vp, u64, vp, vp, vp, u64, vp]
+    L.wm_commit_or_abort.argtypes = [vp, u64, pp, vp, vp, vp, u32, vp]
+    for name in declared():
+        if name not in ("wm_status_str", "wm_workspace_bytes", "wm_payload_bound"):
+            getattr(L, name).restype = ctypes.c_int32
+    return L
+
+
+def P(chunk=CH, kind=0, codec=1, flags=0):
+    return ctypes.byref(Params(chunk, kind, codec, flags))
+
+
+def test_header_declares_the_boundary():
+    names = declared()
+    for must in ("wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_decode_verify",
+                 "wm_commit_or_abort"):
+        assert must in names
+    assert len(names) == len(set(names)) == 10
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared():
+        assert hasattr(lib, name), name
+
+
+def test_binding_lists_the_same_symbols():
+    # the binding's export list is plain text: compare without importing torch
+    src = open(os.path.join(ROOT, "paper_2607_10389_amd", "_wm.py")).read()
+    block = src[src.index("EXPORTS = ("):src.index(")", src.index("EXPORTS = ("))]
+    listed = re.findall(r'"(wm_\w+)"', block)
+    assert sorted(listed) == sorted(declared())
+
+
+def test_status_strings(lib):
+    for code, name in ((OK, b"WM_OK"), (VERIFY_FAILED, b"WM_VERIFY_FAILED"),
+                       (INVALID, b"WM_ERR_INVALID_ARG"), (CAPACITY, b"WM_ERR_CAPACITY"),
+                       (HIP, b"WM_ERR_HIP"), (WORKSPACE, b"WM_ERR_WORKSPACE"),
+                       (UNSUPPORTED, b"WM_ERR_UNSUPPORTED")):
+        assert lib.wm_status_str(code) == name
+
+
+@pytest.mark.parametrize("nbytes", [0, 2, CH, CH + 2, 1673527296, 4294967296])
+def test_payload_bound_matches_the_oracle(lib, nbytes):
+    n = -(-nbytes // CH)
+    assert lib.wm_payload_bound(nbytes, n, P()) == oracle.payload_bound(nbytes, CH, n)
+    # the workspace holds at least the look-back status, table and CRC arrays
+    assert lib.wm_workspace_bytes(nbytes, P()) >= 256 + 32 * max(n, 1)
+
+
+def test_bad_params_are_rejected_before_device_work(lib):
+    a = ALIGNED
+    assert lib.wm_payload_bound(CH, 1, P(chunk=3000)) == 0   # not a power of two
+    assert lib.wm_workspace_bytes(CH, P(kind=2)) == 0        # unknown CRC
+    # a valid power-of-two chunk size other than 64 KiB is not implemented
+    assert lib.wm_checksum_chunks(a, CH, P(chunk=4096), a, None, None) == UNSUPPORTED
+    assert lib.wm_checksum_chunks(a, CH, P(codec=7), a, None, None) == INVALID
+    assert lib.wm_checksum_chunks(a + 4, CH, P(), a, None, None) == INVALID  # misaligned
+    assert lib.wm_checksum_chunks(None, CH, P(), a, None, None) == INVALID
+
+
+def test_encode_argument_checks(lib):
+    a, big = ALIGNED, 1 << 40
+    ws = lib.wm_workspace_bytes(4 * CH, P())
+    bound = lib.wm_payload_bound(4 * CH, 4, P())
+    enc = lib.wm_encode
+    assert enc(a, 4 * CH + 1, P(), None, None, None, a, bound, a, a, ws, None) == INVALID  # odd
+    assert enc(a, 4 * CH, P(), a, None, a, a, bound, a, a, ws, None) == INVALID  # idx w/o n_idx
+    assert enc(a, 4 * CH, P(), a, a, None, a, bound, a, a, ws, None) == INVALID  # list w/o CRCs
+    assert enc(a, 4 * CH, P(), None, None, None, a, bound - 1, a, a, ws, None) == CAPACITY
+    assert enc(a, 4 * CH, P(), None, None, None, a, bound, a, a, ws - 1, None) == WORKSPACE
+    assert enc(a, 4 * CH, P(), None, None, None, a + 8, big, a, a, ws, None) == INVALID
+    step = lib.wm_encode_step
+    assert step(a, a + 2, 4 * CH, P(), None, None, None, None, a, bound, a, a, ws,
+                None) == INVALID
+    assert step(a, None, 4 * CH, P(), None, None, None, None, a, bound - 16, a, a, ws,
+                None) == CAPACITY
+
+
+def test_decode_and_commit_argument_checks(lib):
+    a = ALIGNED
+    ws = lib.wm_workspace_bytes(4 * CH, P())
+    dec = lib.wm_decode_verify
+    assert dec(a, 1 << 20, 4 * CH, P(), a, 4 * CH, None, None, a, ws, None) == INVALID
+    assert dec(a, 1 << 20, 4 * CH, P(), a, 4 * CH, a, None, a, ws - 256, None) == WORKSPACE
+    assert dec(a, 1 << 20, 4 * CH + 1, P(), a, 4 * CH, a, None, a, ws, None) == INVALID
+    com = lib.wm_commit_or_abort
+    assert com(a, 4 * CH, P(), a, a, None, 1, None) == INVALID   # no verdict
+    assert com(a, 4 * CH, P(), a, a, a, 2, None) == INVALID      # unknown mode
+    assert com(a + 1, 4 * CH, P(), a, a, a, 1, None) == INVALID  # misaligned live
