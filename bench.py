@@ -312,7 +312,35 @@ def main():
             "kv_GBps_round_trip": round(nbytes / ((a_src_ms + a_dst_ms) * 1e-3) / 1e9, 1),
             "payload_bytes": pb,
         }
-        del cur, live, ms
+
+        # the same step as separate calls, each against its own bytes
+        mu = Mover(nbytes, args.crc, dev)
+        mu.checksum(cur)
+        mu.diff(cur, prev)
+        mu.encode(cur, dirty_only=True)
+        torch.cuda.synchronize()
+        if not torch.equal(mu.payload[:pb], ms.payload[:pb]):
+            raise RuntimeError("separate calls and the fused step disagree")
+        mu.decode()
+
+        def one(name, fn, moved):
+            t = timed_events(torch, fn, 10)
+            return {"ms": round(t, 4), "bytes": moved,
+                    "GBps": round(moved / (t * 1e-3) / 1e9, 1),
+                    "frac_hbm_peak": round(moved / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+
+        out["separate_calls"] = {
+            "wm_checksum_chunks": one("checksum", lambda: mu.checksum(cur), nbytes),
+            "wm_diff_dirty": one("diff", lambda: mu.diff(cur, prev), 2 * nbytes),
+            "wm_encode_dirty_list": one("encode", lambda: mu.encode(cur, dirty_only=True),
+                                        dirty_b + pb),
+            "wm_commit_scatter": one("commit", lambda: mu.commit(live, scatter=True),
+                                     2 * dirty_b),
+        }
+        # what a plain streaming copy reaches on this device (read S + write S)
+        dst = torch.empty_like(cur)
+        out["copy_ceiling"] = one("copy", lambda: dst.copy_(cur), 2 * nbytes)
+        del cur, live, ms, mu, dst
 
     if not args.no_cpu:
         host = state.view(-1).view(torch.uint8).cpu().numpy()
