@@ -26,13 +26,15 @@ constexpr int kTree = 6;                    // log2(64) lanes
 // Constant tables for one CRC kind (built on the host, uploaded once).
 struct CrcTables {
   uint32_t row[4][256];          // F^kRow   (column-stream step, hot)
+  // f4 .. wave_step are contiguous: they are copied to LDS as one block
   uint32_t f4[4][256];           // F^4      (standard 4-byte step)
   uint32_t f8[4][256];           // F^8
+  uint32_t f12[4][256];          // F^12     (lane merge)
   uint32_t tree[kTree][4][256];  // F^(16 << l): lane-tree levels
+  uint32_t wave_step[4][256];    // F^kSub: one wave's share of a chunk
   uint32_t byte1[256];           // one-byte step of the table method
-  uint32_t wave_mat[kWaves][32]; // F^(kSub*(kWaves-1-w) + 4 - kRow), columns
+  uint32_t wave_mat[kWaves][32]; // F^(kSub*(kWaves-1-w) + 4), columns
   uint32_t pow2[48][32];         // F^(2^i) bytes, columns
-  uint32_t unrow_mat[32];        // F^(4 - kRow): chunk from a one-wave tree
   uint32_t k_full;               // F^kChunk(~0) ^ ~0
   uint32_t pad_[3];
 };

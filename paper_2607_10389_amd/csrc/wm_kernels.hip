@@ -32,13 +32,15 @@ __device__ CrcTables g_tables[2];
 
 // ------------------------------------------------------------ LDS layout --
 constexpr uint32_t kLdsG = 0;                       // 64 KiB, replicated F^1024
-constexpr uint32_t kLdsF4 = 65536;                  // 4 KiB
-constexpr uint32_t kLdsF8 = kLdsF4 + 4096;          // 4 KiB
-constexpr uint32_t kLdsTree = kLdsF8 + 4096;        // 6 x 4 KiB
-constexpr uint32_t kLdsCrcEnd = kLdsTree + kTree * 4096;  // 98304
-constexpr uint32_t kLdsMisc = kLdsCrcEnd;           // 8 KiB of small scratch
-constexpr uint32_t kLdsMiscBytes = 8192;
-constexpr uint32_t kLdsBase = kLdsMisc + kLdsMiscBytes;  // 106496
+constexpr uint32_t kLdsF4 = 65536;                  // 4 KiB each: F^4, F^8, F^12
+constexpr uint32_t kLdsF8 = kLdsF4 + 4096;
+constexpr uint32_t kLdsF12 = kLdsF8 + 4096;
+constexpr uint32_t kLdsTree = kLdsF12 + 4096;       // 6 x 4 KiB
+constexpr uint32_t kLdsWaveStep = kLdsTree + kTree * 4096;  // 4 KiB, F^kSub
+constexpr uint32_t kLdsCrcEnd = kLdsWaveStep + 4096;        // 106496
+constexpr uint32_t kLdsMisc = kLdsCrcEnd;           // 4 KiB of small scratch
+constexpr uint32_t kLdsMiscBytes = 4096;
+constexpr uint32_t kLdsBase = kLdsMisc + kLdsMiscBytes;  // 110592
 
 // checksum-kernel scratch (u32 index into kLdsMisc)
 constexpr uint32_t M_PART = 0;  // [kWaves] wave CRC partials
@@ -135,9 +137,9 @@ __device__ void load_crc_tables(uint32_t kind) {
   uint32_t *g = reinterpret_cast<uint32_t *>(lds + kLdsG);
   for (uint32_t i = threadIdx.x; i < 16384u; i += blockDim.x)
     g[i] = T.row[(i >> 4) & 3u][i >> 6];
-  const uint32_t *src = &T.f4[0][0];  // f4, f8, tree are contiguous
+  const uint32_t *src = &T.f4[0][0];  // f4, f8, f12, tree, wave_step
   uint32_t *dst = reinterpret_cast<uint32_t *>(lds + kLdsF4);
-  for (uint32_t i = threadIdx.x; i < (2u + kTree) * 1024u; i += blockDim.x)
+  for (uint32_t i = threadIdx.x; i < (4u + kTree) * 1024u; i += blockDim.x)
     dst[i] = src[i];
 }
 
@@ -241,33 +243,58 @@ __device__ __forceinline__ void load_chunk(const uint8_t *__restrict__ base,
   }
 }
 
-// Lane merge of the four column states and the 6-level lane tree; the wave
-// value Q is valid in lane 0.
-__device__ __forceinline__ uint32_t lane_tree(uint32_t v0, uint32_t v1, uint32_t v2,
-                                              uint32_t v3) {
-  // u = F^12 v0 ^ F^8 v1 ^ F^4 v2 ^ v3
-  uint32_t u = tab4(kLdsF8, tab4(kLdsF4, v0) ^ v1) ^ tab4(kLdsF4, v2) ^ v3;
-#pragma unroll
-  for (int lv = 0; lv < kTree; ++lv) {
-    uint32_t s = tab4(kLdsTree + lv * 4096u, u);
-    uint32_t o = __shfl_down(u, 1u << lv, 64);
-    u = s ^ o;
-  }
+// How a wave's 8 KiB enter the chunk CRC.  The word at chunk offset o
+// contributes F^(kChunk - o) of itself to the zero-init register R (see
+// wm_internal.h), and for lane l, row h, column j of wave w
+//     kChunk - o = kSub (7 - w) + kRow (7 - h) + 16 (63 - l) + 4 (3 - j) + 4.
+// The four factors are applied in stages: column streams over the rows
+// (w_j = sum_h F^(kRow (7 - h)) word_hj), the lane merge over the columns,
+// the lane tree over the lanes, and a per-wave shift F^(kSub (7 - w) + 4).
+
+// Lane merge of the four column streams: F^12 w0 ^ F^8 w1 ^ F^4 w2 ^ w3.
+__device__ __forceinline__ uint32_t lane_merge(uint32_t v0, uint32_t v1, uint32_t v2,
+                                               uint32_t v3) {
+  return tab4(kLdsF12, v0) ^ tab4(kLdsF8, v1) ^ tab4(kLdsF4, v2) ^ v3;
+}
+
+// Lane tree: sum over lanes of F^(16 (63 - l)) u_l, valid in lane 63.  A
+// Hillis-Steele pass over DPP row shifts and row broadcasts: at level s, the
+// value received from s lanes below covers bytes that precede the receiver's
+// own s lanes, so it is shifted by F^(16 s) before the XOR (a lane with no
+// source receives 0, and F(0) = 0).
+__device__ __forceinline__ uint32_t lane_tree(uint32_t u) {
+  u ^= tab4(kLdsTree + 0 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x111, 0xF, 0xF, false));
+  u ^= tab4(kLdsTree + 1 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x112, 0xF, 0xF, false));
+  u ^= tab4(kLdsTree + 2 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x114, 0xF, 0xF, false));
+  u ^= tab4(kLdsTree + 3 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x118, 0xF, 0xF, false));
+  u ^= tab4(kLdsTree + 4 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x142, 0xA, 0xF, false));
+  u ^= tab4(kLdsTree + 5 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x143, 0xC, 0xF, false));
   return u;
 }
 
-// Wave-level CRC value Q of the wave's 8 rows (valid in lane 0).
+// The lane's merged value of the wave's 8 rows (before the lane tree).
+__device__ __forceinline__ uint32_t lane_value(const uint4 (&d)[kRows], const GLane &gl) {
+  uint32_t v0 = d[0].x, v1 = d[0].y, v2 = d[0].z, v3 = d[0].w;
+#pragma unroll
+  for (int h = 1; h < kRows; ++h) {
+    v0 = g_step(v0, gl) ^ d[h].x;
+    v1 = g_step(v1, gl) ^ d[h].y;
+    v2 = g_step(v2, gl) ^ d[h].z;
+    v3 = g_step(v3, gl) ^ d[h].w;
+  }
+  return lane_merge(v0, v1, v2, v3);
+}
+
+// Wave-level CRC value Q of the wave's 8 rows (valid in lane 63).
 __device__ __forceinline__ uint32_t wave_q(const uint4 (&d)[kRows],
                                            const GLane &gl) {
-  uint32_t v0 = 0, v1 = 0, v2 = 0, v3 = 0;
-#pragma unroll
-  for (int h = 0; h < kRows; ++h) {
-    v0 = g_step(v0 ^ d[h].x, gl);
-    v1 = g_step(v1 ^ d[h].y, gl);
-    v2 = g_step(v2 ^ d[h].z, gl);
-    v3 = g_step(v3 ^ d[h].w, gl);
-  }
-  return lane_tree(v0, v1, v2, v3);
+  return lane_tree(lane_value(d, gl));
 }
 
 // A uniform pointer the compiler cannot see through: loads through it stay
@@ -279,10 +306,10 @@ __device__ __forceinline__ P *opaque(P *p) {
   return p;
 }
 
-// The wave's share of the chunk's raw CRC: its value Q (lane 0) shifted past
-// the rows of the later waves, computed on the scalar unit.
+// The wave's share of the chunk's raw CRC: its value Q (lane 63) shifted
+// past the rows of the later waves, computed on the scalar unit.
 __device__ __forceinline__ uint32_t wave_part(const CrcTables &T, uint32_t wave, uint32_t q) {
-  return mat_apply(opaque(T.wave_mat[wave]), uniform(q));
+  return mat_apply(opaque(T.wave_mat[wave]), __builtin_amdgcn_readlane(q, 63));
 }
 
 // Chunk CRC from the raw (zero-init, padded) value of the whole chunk.
@@ -504,7 +531,7 @@ struct EncArgs {
 };
 
 struct EncShared {
-  uint32_t part[kWaves];     // wave CRC partials
+  uint32_t u[kThreads];      // lane values of the chunk's CRC (lane_value)
   uint32_t dirty_w[kWaves];  // per-wave "differs from prev"
   uint32_t esc_w[kWaves];    // escapes per wave
   uint32_t crc;               // the chunk's CRC
@@ -648,10 +675,11 @@ __device__ uint64_t lookback_finish(const uint64_t *status, int64_t top, Window 
 // two words at a time in 16-bit lanes: c = min((e - base) mod 2^16, esc), and
 // c + 1 carries into bit K exactly for escapes.  Per row: escm holds the
 // lane's escape flags (bit u = word u, 8 bits per row), lane_r the number of
-// the wave's escapes before the lane's first one in this row.
-template <uint32_t K>
+// the wave's escapes before the lane's first one in this row.  FULL: the
+// chunk has kChunk bytes (no word needs a bounds check).
+template <uint32_t K, bool FULL>
 __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &l,
-                                           uint32_t n_words, bool full, uint32_t base,
+                                           uint32_t n_words, uint32_t base,
                                            uint8_t *stage, uint32_t (&escm)[2],
                                            uint32_t (&lane_r)[kRows], uint32_t &wave_esc) {
   if constexpr (K == 8) {  // RAW: the exponent plane, one byte per word
@@ -666,7 +694,7 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
       // e = (high byte << 1 | low byte >> 7) & 255, four words at a time
       uint2 e = make_uint2(((hi0 << 1) & 0xFEFEFEFEu) | ((lo0 >> 7) & 0x01010101u),
                            ((hi1 << 1) & 0xFEFEFEFEu) | ((lo1 >> 7) & 0x01010101u));
-      if (w0 < n_words) *reinterpret_cast<uint2 *>(stage + w0) = e;
+      if (FULL || w0 < n_words) *reinterpret_cast<uint2 *>(stage + w0) = e;
       lane_r[h] = 0;
     }
     return;
@@ -686,14 +714,14 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
       pair[j] = (c2 & 0xFFFFu) | (c2 >> (16 - K));  // lo | hi << K
     }
     uint32_t m8 = (m | (m >> 15)) & 0xFFu;
-    if (!full) {  // words past the chunk code as 0 and never escape
+    if constexpr (!FULL) {  // words past the chunk code as 0 and never escape
       const uint32_t vw = w0 >= n_words ? 0u : min(n_words - w0, 8u);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         pair[j] &= vw >= 2u * j + 2u ? ~0u : (vw == 2u * j + 1u ? esc : 0u);
       m8 &= (1u << vw) - 1u;
     }
-    if (w0 < n_words) {
+    if (FULL || w0 < n_words) {
       uint8_t *at = stage + (w0 >> 3) * K;
       if constexpr (K * 8 <= 32) {
         const uint32_t p = pair[0] | (pair[1] << (2 * K)) | (pair[2] << (4 * K)) |
@@ -729,21 +757,70 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
   }
 }
 
+// A chunk's record fields as the control wave holds them (uniform).
+struct RecFields {
+  uint32_t item, c, n_words, mode, k, base, n_esc, size, crc;
+  bool dirty, bad;
+};
+
+// Control wave: the record's payload offset (finishing the look-back window
+// `win` issued for item - 1), then the item's inclusive prefix, the record
+// header and the table entry; the offset goes to the data waves through LDS.
+__device__ __forceinline__ void ctl_emit(const EncArgs &a, const RecFields &r, const Window &win,
+                                         uint32_t n_items, uint64_t *status, WsCtl *ctl,
+                                         uint4 *tab_ws, uint32_t *ecrc, EncShared &sh,
+                                         int64_t &my_last, uint64_t &my_last_incl) {
+  const uint64_t excl =
+      lookback_finish(status, (int64_t)r.item - 1, win, my_last, my_last_incl, ctl);
+  const uint64_t agg = ((uint64_t)(r.dirty ? 1u : 0u) << 2) | ((uint64_t)(r.size >> 4) << 26);
+  const uint64_t incl = excl + (agg >> 2);
+  my_last = r.item;
+  my_last_incl = incl;
+  const uint32_t rec_idx = (uint32_t)(excl & 0xFFFFFFu);
+  const uint64_t rec_off = 64u + ((excl >> 24) << 4);
+  uint32_t hw[4] = {r.mode | (r.k << 8) | (r.base << 16), r.n_words, r.n_esc, 0};
+  hw[3] = crc_words(hw, 3);
+  uint32_t ew[4] = {r.c, r.crc, (uint32_t)rec_off, (uint32_t)(rec_off >> 32)};
+  const uint32_t eck = crc_words(ew, 4);
+  if ((threadIdx.x & 63u) == 0) {
+    status_store(&status[r.item], (incl << 2) | kFlagIncl);
+    if (r.item + 1 == n_items) {
+      ctl->n_rec = (uint32_t)(incl & 0xFFFFFFu);
+      ctl->payload_bytes = (incl >> 24) << 4;  // total record bytes
+    }
+    if (r.bad) atomicOr(&ctl->error, 2u);
+    sh.off_lo = (uint32_t)rec_off;
+    sh.off_hi = (uint32_t)(rec_off >> 32);
+    if (r.dirty) {
+      *reinterpret_cast<uint4 *>(a.payload + rec_off) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+      tab_ws[rec_idx] = make_uint4(ew[0], ew[1], ew[2], ew[3]);
+      ecrc[rec_idx] = eck;
+      if (a.dirty_idx) a.dirty_idx[rec_idx] = r.c;
+    }
+    if (a.crc_out && !r.bad) a.crc_out[r.c] = r.crc;
+  }
+}
+
 // The encoder runs one chunk behind on output: iteration i computes chunk
 // X_i (CRC, histogram, plan, codes staged in LDS, sign/mantissa bytes kept
 // in registers) and writes the record of X_{i-1}, whose payload offset the
-// control wave resolved by look-back at the start of iteration i.  By then
-// the predecessors of X_{i-1} have published their sizes an iteration ago,
-// so the look-back finishes within the first phase and nothing waits on it.
-//   phase 1 (..B1): data: prefetch X_{i+1}, CRC and histogram of X_i;
-//                   control: look-back of X_{i-1}, its prefix, header and
-//                   table entry; next ticket
-//   phase 2 (..B2): data: reduce the histogram; control: CRC of X_i
+// control wave resolved by look-back: for a full ship at the end of
+// iteration i-1, right after X_{i-1}'s size was published (its predecessors
+// run alongside and have published theirs by then); for a step, whose clean
+// chunks finish early and let workgroups drift apart, in phase 1 of
+// iteration i, issued before B0 and finished after it.
+//   phase 1 (..B1): data: prefetch X_{i+1}, lane CRC values and histogram of
+//                   X_i; control: next ticket
+//   phase 2 (..B2): data: reduce the histogram
 //   phase 3 (..B3): data: write X_{i-1} (staging + sign/mantissa bytes),
-//                   score the plan candidates of X_i
-//   phase 4 (..B4): all: pick X_i's plan; control: publish its size;
-//                   data: codes into staging, escape counts, sign/mantissa
-//   phase 5:        data: escape index and escapes into staging
+//                   score the plan candidates of X_i; control: first step
+//                   of X_i's CRC
+//   phase 4 (..B4): all: pick X_i's plan; control: publish its size, finish
+//                   its CRC; data: codes into staging, escape counts,
+//                   sign/mantissa bytes
+//   phase 5:        control (full ship): look-back of X_i, its prefix,
+//                   header and table entry; data: escape index and escapes
+//                   into staging
 template <bool HAS_PREV>
 __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(a.ws + a.L.ctl);
@@ -783,9 +860,9 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
 
   // the chunk whose record is still to be written (uniform), and its
   // sign/mantissa bytes (data waves)
-  bool pend = false, p_dirty = false, p_bad = false;
-  uint32_t p_item = 0, p_c = 0, p_nw = 0, p_mode = 0, p_k = 0, p_base = 0, p_nesc = 0;
-  uint32_t p_size = 0, p_send = 0, p_crc = 0;
+  bool pend = false, p_dirty = false;
+  uint32_t p_nw = 0, p_send = 0;
+  RecFields pr = {};  // control, step variant: X_{i-1}'s record fields
   int64_t my_last = -1;      // control: this workgroup's last finished item
   uint64_t my_last_incl = 0; //          and its inclusive prefix
   uint2 smp[kRows];
@@ -815,11 +892,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         load_chunk(a.cur + (uint64_t)(cn < g.n_chunks ? cn : 0u) * kChunk,
                    cn < g.n_chunks ? chunk_len(g, cn) : 0u, l, dn);
       }
-      if (need_crc && cur) {
-        const uint32_t q = wave_q(d, gl);
-        const uint32_t part = wave_part(T, l.wave, q);
-        if (l.lane == 0) sh.part[l.wave] = part;
-      }
+      if (need_crc && cur) sh.u[l.wave * 64u + l.lane] = lane_value(d, gl);
       if (HAS_PREV) {
         uint32_t diff = 0;
 #pragma unroll
@@ -830,7 +903,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       }
     } else {
       if (cur && l.lane == 0) ticket = atomicAdd(&ctl->ticket, 1u);
-      if (pend) win = lookback_issue(status, (int64_t)p_item - 1, my_last, my_last_incl);
+      if (HAS_PREV && pend) win = lookback_issue(status, (int64_t)pr.item - 1, my_last, my_last_incl);
     }
     bool dirty = cur && !bad_index;
     if (HAS_PREV) {
@@ -839,52 +912,21 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) dw |= sh.dirty_w[w];
       dirty = dirty && uniform(dw) != 0;
+      if (is_ctl && pend)  // ---- control: X_{i-1}'s offset, header and table entry
+        ctl_emit(a, pr, win, n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
     }
-    if (is_ctl) {
-      if (pend) {
-        // ---- control: X_{i-1}'s offset, prefix, header and table entry
-        const uint64_t excl =
-            lookback_finish(status, (int64_t)p_item - 1, win, my_last, my_last_incl, ctl);
-        const uint64_t agg = ((uint64_t)(p_dirty ? 1u : 0u) << 2) | ((uint64_t)(p_size >> 4) << 26);
-        const uint64_t incl = excl + (agg >> 2);
-        my_last = p_item;
-        my_last_incl = incl;
-        const uint32_t rec_idx = (uint32_t)(excl & 0xFFFFFFu);
-        const uint64_t rec_off = 64u + ((excl >> 24) << 4);
-        uint32_t hw[4] = {p_mode | (p_k << 8) | (p_base << 16), p_nw, p_nesc, 0};
-        hw[3] = crc_words(hw, 3);
-        uint32_t ew[4] = {p_c, p_crc, (uint32_t)rec_off, (uint32_t)(rec_off >> 32)};
-        const uint32_t eck = crc_words(ew, 4);
-        if (l.lane == 0) {
-          status_store(&status[p_item], (incl << 2) | kFlagIncl);
-          if (p_item + 1 == n_items) {
-            ctl->n_rec = (uint32_t)(incl & 0xFFFFFFu);
-            ctl->payload_bytes = (incl >> 24) << 4;  // total record bytes
-          }
-          if (p_bad) atomicOr(&ctl->error, 2u);
-          sh.off_lo = (uint32_t)rec_off;
-          sh.off_hi = (uint32_t)(rec_off >> 32);
-          if (p_dirty) {
-            *reinterpret_cast<uint4 *>(a.payload + rec_off) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-            tab_ws[rec_idx] = make_uint4(ew[0], ew[1], ew[2], ew[3]);
-            ecrc[rec_idx] = eck;
-            if (a.dirty_idx) a.dirty_idx[rec_idx] = p_c;
-          }
-          if (a.crc_out && !p_bad) a.crc_out[p_c] = p_crc;
-        }
-      }
-    } else if (dirty) {
-      // ---- data: exponent histogram (16 copies x 256 bins)
+    if (!is_ctl && dirty) {
+      // ---- data: exponent histogram (16 copies x 256 bins) of all 32768
+      // words; the words past a short chunk load as zero, and the reduce
+      // takes their count off bin 0
+      const uint32_t hb = kLdsHistE + copy4;
 #pragma unroll
       for (int h = 0; h < kRows; ++h) {
-        const uint32_t w0 = (l.off0 + h * kRow) >> 1;
         const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          if (full || w0 + 2 * j < n_words)
-            atomicAdd(reinterpret_cast<uint32_t *>(lds + kLdsHistE + (((x[j] >> 1) & 0x3FC0u) | copy4)), 1u);
-          if (full || w0 + 2 * j + 1 < n_words)
-            atomicAdd(reinterpret_cast<uint32_t *>(lds + kLdsHistE + (((x[j] >> 17) & 0x3FC0u) | copy4)), 1u);
+          atomicAdd(reinterpret_cast<uint32_t *>(lds + hb + (__builtin_amdgcn_ubfe(x[j], 7, 8) << 6)), 1u);
+          atomicAdd(reinterpret_cast<uint32_t *>(lds + hb + (__builtin_amdgcn_ubfe(x[j], 23, 8) << 6)), 1u);
         }
       }
     }
@@ -894,14 +936,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     uint32_t crc = 0;
     if (is_ctl) {
       if (cur) {
-        if (need_crc) {
-          uint32_t raw = 0;
-#pragma unroll
-          for (int w = 0; w < kWaves; ++w) raw ^= sh.part[w];
-          crc = bad_index ? 0u : finish_crc(raw, len, g, T);
-        } else {
-          crc = bad_index ? 0u : ld_const(a.crc_in + c);
-        }
+        if (!need_crc) crc = bad_index ? 0u : ld_const(a.crc_in + c);
         if (l.lane == 0) sh.next = ticket;
       }
     } else if (dirty) {
@@ -911,12 +946,21 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
 #pragma unroll
       for (int cc = 0; cc < 8; ++cc) s += hist[bin * 16u + half * 8u + ((cc + (l.lane >> 1)) & 7u)];
       s += (uint32_t)__shfl_xor((int)s, 1, 64);
-      if (half == 0) sh.H[bin] = s;
+      if (half == 0) sh.H[bin] = bin == 0 ? s - (kChunk / 2 - n_words) : s;
     }
     __syncthreads();  // B2: H complete
 
     // ---- phase 3
-    if (!is_ctl) {
+    uint32_t crc_acc = 0;
+    if (is_ctl) {
+      if (cur && need_crc) {
+        // the chunk CRC from the data waves' lane values, first step: lane l
+        // folds lane l of the eight waves (F^kSub per wave)
+        crc_acc = sh.u[l.lane];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) crc_acc = tab4(kLdsWaveStep, crc_acc) ^ sh.u[w * 64 + l.lane];
+      }
+    } else {
       if (pend && p_dirty) {
         // write X_{i-1}: staged section, then its sign/mantissa plane
         const uint64_t rec_off = (uint64_t)uniform(sh.off_lo) | ((uint64_t)uniform(sh.off_hi) << 32);
@@ -1014,6 +1058,12 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(size >> 4) << 26);
         status_store(&status[item], agg | kFlagAgg);
       }
+      if (cur && need_crc) {
+        // second step: the lane tree, then the F^4 common to every word
+        // (see lane_value)
+        const uint32_t q = uniform(__builtin_amdgcn_readlane(lane_tree(crc_acc), 63));
+        crc = bad_index ? 0u : finish_crc(tab4(kLdsF4, q), len, g, T);
+      }
     } else if (dirty) {
       if (pack) {
         // ---- data: codes into staging, escape flags and counts
@@ -1022,22 +1072,35 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
           for (uint32_t i = l.lane; i < 32u * kbits; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
         }
         uint32_t wave_esc = 0;
+#define WM_PACK(K)                                                                   \
+  (full ? pack_codes<K, true>(d, l, n_words, base, stage, escm, lane_r, wave_esc)      \
+        : pack_codes<K, false>(d, l, n_words, base, stage, escm, lane_r, wave_esc))
         switch (kbits) {
-          case 1: pack_codes<1>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-          case 2: pack_codes<2>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-          case 3: pack_codes<3>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-          case 4: pack_codes<4>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-          case 5: pack_codes<5>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-          case 6: pack_codes<6>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-          case 7: pack_codes<7>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
-          default: pack_codes<8>(d, l, n_words, full, base, stage, escm, lane_r, wave_esc); break;
+          case 1: WM_PACK(1); break;
+          case 2: WM_PACK(2); break;
+          case 3: WM_PACK(3); break;
+          case 4: WM_PACK(4); break;
+          case 5: WM_PACK(5); break;
+          case 6: WM_PACK(6); break;
+          case 7: WM_PACK(7); break;
+          default: WM_PACK(8); break;
         }
+#undef WM_PACK
         if (l.lane == 0) sh.esc_w[l.wave] = wave_esc;
       }
 #pragma unroll
       for (int h = 0; h < kRows; ++h) smp[h] = sm_bytes(d[h]);
     }
     __syncthreads();  // B4: codes staged, escape totals known
+
+    if (!HAS_PREV && is_ctl && cur) {
+      // ---- control: X_i's offset, prefix, header and table entry.  Its size
+      // was published before B4, and the vector-memory pipe is idle here (the
+      // data waves' next loads come after the loop top).
+      const Window win = lookback_issue(status, (int64_t)item - 1, my_last, my_last_incl);
+      const RecFields r = {item, c, n_words, mode, k, base, n_esc, size, crc, dirty, bad_index};
+      ctl_emit(a, r, win, n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
+    }
 
     // ---- phase 5
     if (!is_ctl && pack && has_esc) {
@@ -1067,19 +1130,11 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     }
 
     // ---- X_i becomes the pending record
+    if (HAS_PREV) pr = RecFields{item, c, n_words, mode, k, base, n_esc, size, crc, dirty, bad_index};
     pend = cur;
-    p_item = item;
-    p_c = c;
     p_nw = n_words;
     p_dirty = dirty;
-    p_bad = bad_index;
-    p_mode = mode;
-    p_k = k;
-    p_base = base;
-    p_nesc = n_esc;
-    p_size = size;
     p_send = s_end;
-    p_crc = crc;
     if (!is_ctl) {
 #pragma unroll
       for (int h = 0; h < kRows; ++h) d[h] = dn[h];
@@ -1614,10 +1669,14 @@ __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, co
           out[j] &= vw >= 2 * j + 2 ? ~0u : (vw == 2 * j + 1 ? 0xFFFFu : 0u);
       }
     }
-    cv[0] = g_step(cv[0] ^ out[0], gl);
-    cv[1] = g_step(cv[1] ^ out[1], gl);
-    cv[2] = g_step(cv[2] ^ out[2], gl);
-    cv[3] = g_step(cv[3] ^ out[3], gl);
+    if (h == 0) {
+      cv[0] = out[0], cv[1] = out[1], cv[2] = out[2], cv[3] = out[3];
+    } else {
+      cv[0] = g_step(cv[0], gl) ^ out[0];
+      cv[1] = g_step(cv[1], gl) ^ out[1];
+      cv[2] = g_step(cv[2], gl) ^ out[2];
+      cv[3] = g_step(cv[3], gl) ^ out[3];
+    }
     dec_store(dst, l.off0 + h * kRow, v.len, out);
   }
   if (kEsc && acc != v.Ee) bad = true;  // the wave's escapes end where the next block's begin
@@ -1693,7 +1752,7 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
             case 7: bad = dec_packed<7>(cur, v, M, l, stage, dst, cv, gl); break;
             default: bad = dec_packed<8>(cur, v, M, l, stage, dst, cv, gl); break;
           }
-          const uint32_t q = lane_tree(cv[0], cv[1], cv[2], cv[3]);
+          const uint32_t q = lane_tree(lane_merge(cv[0], cv[1], cv[2], cv[3]));
           const uint32_t part = wave_part(T, l.wave, q);
           const bool any_bad = __ballot(bad) != 0;
           if (l.lane == 0) {

@@ -97,12 +97,14 @@ void build_crc_tables(uint32_t poly, CrcTables *t) {
   byte_tables(byte_shift(poly, kRow), t->row);
   byte_tables(byte_shift(poly, 4), t->f4);
   byte_tables(byte_shift(poly, 8), t->f8);
+  byte_tables(byte_shift(poly, 12), t->f12);
   for (int l = 0; l < kTree; ++l)
     byte_tables(byte_shift(poly, 16 << l), t->tree[l]);
+  byte_tables(byte_shift(poly, kSub), t->wave_step);
   Mat one = byte_shift(poly, 1);
   for (uint32_t b = 0; b < 256; ++b) t->byte1[b] = apply(one, b);
   for (int w = 0; w < kWaves; ++w) {
-    Mat m = byte_shift(poly, (int64_t)kSub * (kWaves - 1 - w) + 4 - kRow);
+    Mat m = byte_shift(poly, (int64_t)kSub * (kWaves - 1 - w) + 4);
     std::memcpy(t->wave_mat[w], m.c, sizeof(m.c));
   }
   Mat p = byte_shift(poly, 1);
@@ -110,8 +112,6 @@ void build_crc_tables(uint32_t poly, CrcTables *t) {
     std::memcpy(t->pow2[i], p.c, sizeof(p.c));
     p = compose(p, p);
   }
-  Mat un = byte_shift(poly, 4 - (int64_t)kRow);
-  std::memcpy(t->unrow_mat, un.c, sizeof(un.c));
   t->k_full = apply(byte_shift(poly, kChunk), 0xFFFFFFFFu) ^ 0xFFFFFFFFu;
 }
 
