@@ -31,21 +31,33 @@ namespace wm {
 __device__ CrcTables g_tables[2];
 
 // ------------------------------------------------------------ LDS layout --
-constexpr uint32_t kLdsG = 0;                       // 64 KiB, replicated F^1024
-constexpr uint32_t kLdsF4 = 65536;                  // 4 KiB each: F^4, F^8, F^12
+// The first 16 KiB are kernel-specific (encoder histogram, decoder escape
+// windows): below 64 KiB, so their base folds into an instruction's offset.
+constexpr uint32_t kLdsLow = 0;
+constexpr uint32_t kLdsLowBytes = 16384;
+constexpr uint32_t kLdsG = kLdsLow + kLdsLowBytes;  // 64 KiB, replicated F^1024
+constexpr uint32_t kLdsF4 = kLdsG + 65536;          // 4 KiB each: F^4, F^8, F^12
 constexpr uint32_t kLdsF8 = kLdsF4 + 4096;
 constexpr uint32_t kLdsF12 = kLdsF8 + 4096;
 constexpr uint32_t kLdsTree = kLdsF12 + 4096;       // 6 x 4 KiB
 constexpr uint32_t kLdsWaveStep = kLdsTree + kTree * 4096;  // 4 KiB, F^kSub
-constexpr uint32_t kLdsCrcEnd = kLdsWaveStep + 4096;        // 106496
+constexpr uint32_t kLdsCrcEnd = kLdsWaveStep + 4096;        // 122880
 constexpr uint32_t kLdsMisc = kLdsCrcEnd;           // 4 KiB of small scratch
 constexpr uint32_t kLdsMiscBytes = 4096;
-constexpr uint32_t kLdsBase = kLdsMisc + kLdsMiscBytes;  // 110592
+constexpr uint32_t kLdsBase = kLdsMisc + kLdsMiscBytes;  // 126976
 
 // checksum-kernel scratch (u32 index into kLdsMisc)
 constexpr uint32_t M_PART = 0;  // [kWaves] wave CRC partials
 
-extern __shared__ __align__(16) uint8_t lds[];
+// Dynamic LDS of the kernels below.  They declare no static LDS (checked at
+// set-up, set_kernel_attributes), so it begins at LDS address 0: addresses
+// are plain numbers, and their constant parts stay in the LDS instructions'
+// offset fields instead of an extern array's base (a link-time value) being
+// added to every address.
+__device__ __forceinline__ uint8_t *lds_at(uint32_t off) {
+  typedef __attribute__((address_space(3))) uint8_t lds_u8;
+  return (uint8_t *)(lds_u8 *)(uintptr_t)off;  // C-style: address-space cast
+}
 
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
@@ -87,20 +99,29 @@ __device__ __forceinline__ uint32_t ld_const(const uint32_t *p) {
 }
 
 __device__ __forceinline__ uint32_t lds_u32(uint32_t off) {
-  return *reinterpret_cast<const uint32_t *>(lds + off);
+  return *reinterpret_cast<const uint32_t *>(lds_at(off));
 }
 __device__ __forceinline__ uint32_t *misc() {
-  return reinterpret_cast<uint32_t *>(lds + kLdsMisc);
+  return reinterpret_cast<uint32_t *>(lds_at(kLdsMisc));
 }
 __device__ __forceinline__ uint32_t uniform(uint32_t v) {
   return __builtin_amdgcn_readfirstlane(v);
 }
 
-// Byte-table application of a shift stored at LDS offset `off`.
+// a ^ b ^ c in one instruction (three-input logic op, truth table 0x96).
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
+// Byte-table application of a shift stored at LDS offset `off`, XORed with y.
+__device__ __forceinline__ uint32_t tab4x(uint32_t off, uint32_t x, uint32_t y) {
+  return xor3(xor3(lds_u32(off + ((x & 255u) << 2)), lds_u32(off + 1024u + (((x >> 8) & 255u) << 2)),
+                   lds_u32(off + 2048u + (((x >> 16) & 255u) << 2))),
+              lds_u32(off + 3072u + ((x >> 24) << 2)), y);
+}
 __device__ __forceinline__ uint32_t tab4(uint32_t off, uint32_t x) {
-  return lds_u32(off + ((x & 255u) << 2)) ^
-         lds_u32(off + 1024u + (((x >> 8) & 255u) << 2)) ^
-         lds_u32(off + 2048u + (((x >> 16) & 255u) << 2)) ^
+  return xor3(lds_u32(off + ((x & 255u) << 2)), lds_u32(off + 1024u + (((x >> 8) & 255u) << 2)),
+              lds_u32(off + 2048u + (((x >> 16) & 255u) << 2))) ^
          lds_u32(off + 3072u + ((x >> 24) << 2));
 }
 
@@ -123,22 +144,23 @@ __device__ __forceinline__ GLane glane_make() {
   return gl;
 }
 
-__device__ __forceinline__ uint32_t g_step(uint32_t x, const GLane &gl) {
+// F^kRow(x) ^ y.
+__device__ __forceinline__ uint32_t g_step(uint32_t x, uint32_t y, const GLane &gl) {
   uint32_t a0 = __builtin_amdgcn_perm(x, gl.k[0], gl.sel[0]);
   uint32_t a1 = __builtin_amdgcn_perm(x, gl.k[1], gl.sel[1]);
   uint32_t a2 = __builtin_amdgcn_perm(x, gl.k[2], gl.sel[2]);
   uint32_t a3 = __builtin_amdgcn_perm(x, gl.k[3], gl.sel[3]);
-  return lds_u32(kLdsG + a0) ^ lds_u32(kLdsG + a1) ^ lds_u32(kLdsG + a2) ^
-         lds_u32(kLdsG + a3);
+  return xor3(xor3(lds_u32(kLdsG + a0), lds_u32(kLdsG + a1), lds_u32(kLdsG + a2)),
+              lds_u32(kLdsG + a3), y);
 }
 
 __device__ void load_crc_tables(uint32_t kind) {
   const CrcTables &T = g_tables[kind];
-  uint32_t *g = reinterpret_cast<uint32_t *>(lds + kLdsG);
+  uint32_t *g = reinterpret_cast<uint32_t *>(lds_at(kLdsG));
   for (uint32_t i = threadIdx.x; i < 16384u; i += blockDim.x)
     g[i] = T.row[(i >> 4) & 3u][i >> 6];
   const uint32_t *src = &T.f4[0][0];  // f4, f8, f12, tree, wave_step
-  uint32_t *dst = reinterpret_cast<uint32_t *>(lds + kLdsF4);
+  uint32_t *dst = reinterpret_cast<uint32_t *>(lds_at(kLdsF4));
   for (uint32_t i = threadIdx.x; i < (4u + kTree) * 1024u; i += blockDim.x)
     dst[i] = src[i];
 }
@@ -161,11 +183,14 @@ __device__ uint32_t shift_bytes(const CrcTables &T, uint64_t m, uint32_t v) {
 }
 
 // Standard CRC (init/xorout ~0) of 4*nw bytes held as words, with F^4 tables
-// in LDS.  Used for headers and table entries.
-__device__ __forceinline__ uint32_t crc_words(const uint32_t *w, int nw) {
-  uint32_t s = 0xFFFFFFFFu;
+// in LDS.  Used for headers and table entries.  crc_feed continues a
+// register state s (start from ~0, finish with ^ ~0).
+__device__ __forceinline__ uint32_t crc_feed(uint32_t s, const uint32_t *w, int nw) {
   for (int i = 0; i < nw; ++i) s = tab4(kLdsF4, s ^ w[i]);
-  return s ^ 0xFFFFFFFFu;
+  return s;
+}
+__device__ __forceinline__ uint32_t crc_words(const uint32_t *w, int nw) {
+  return crc_feed(0xFFFFFFFFu, w, nw) ^ 0xFFFFFFFFu;
 }
 
 __device__ __forceinline__ uint64_t pad16(uint64_t x) { return (x + 15u) & ~15ull; }
@@ -254,7 +279,7 @@ __device__ __forceinline__ void load_chunk(const uint8_t *__restrict__ base,
 // Lane merge of the four column streams: F^12 w0 ^ F^8 w1 ^ F^4 w2 ^ w3.
 __device__ __forceinline__ uint32_t lane_merge(uint32_t v0, uint32_t v1, uint32_t v2,
                                                uint32_t v3) {
-  return tab4(kLdsF12, v0) ^ tab4(kLdsF8, v1) ^ tab4(kLdsF4, v2) ^ v3;
+  return tab4x(kLdsF12, v0, tab4x(kLdsF8, v1, tab4x(kLdsF4, v2, v3)));
 }
 
 // Lane tree: sum over lanes of F^(16 (63 - l)) u_l, valid in lane 63.  A
@@ -262,20 +287,28 @@ __device__ __forceinline__ uint32_t lane_merge(uint32_t v0, uint32_t v1, uint32_
 // value received from s lanes below covers bytes that precede the receiver's
 // own s lanes, so it is shifted by F^(16 s) before the XOR (a lane with no
 // source receives 0, and F(0) = 0).
-__device__ __forceinline__ uint32_t lane_tree(uint32_t u) {
-  u ^= tab4(kLdsTree + 0 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x111, 0xF, 0xF, false));
-  u ^= tab4(kLdsTree + 1 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x112, 0xF, 0xF, false));
-  u ^= tab4(kLdsTree + 2 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x114, 0xF, 0xF, false));
-  u ^= tab4(kLdsTree + 3 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x118, 0xF, 0xF, false));
-  u ^= tab4(kLdsTree + 4 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x142, 0xA, 0xF, false));
-  u ^= tab4(kLdsTree + 5 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x143, 0xC, 0xF, false));
+// Levels 0..3 (within rows of 16 lanes) and 4..5 (across rows) may run
+// apart; lane_tree is both.
+__device__ __forceinline__ uint32_t lane_tree_rows(uint32_t u) {
+  u = tab4x(kLdsTree + 0 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x111, 0xF, 0xF, false), u);
+  u = tab4x(kLdsTree + 1 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x112, 0xF, 0xF, false), u);
+  u = tab4x(kLdsTree + 2 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x114, 0xF, 0xF, false), u);
+  u = tab4x(kLdsTree + 3 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x118, 0xF, 0xF, false), u);
   return u;
+}
+__device__ __forceinline__ uint32_t lane_tree_across(uint32_t u) {
+  u = tab4x(kLdsTree + 4 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x142, 0xA, 0xF, false), u);
+  u = tab4x(kLdsTree + 5 * 4096u,
+            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x143, 0xC, 0xF, false), u);
+  return u;
+}
+__device__ __forceinline__ uint32_t lane_tree(uint32_t u) {
+  return lane_tree_across(lane_tree_rows(u));
 }
 
 // The lane's merged value of the wave's 8 rows (before the lane tree).
@@ -283,10 +316,10 @@ __device__ __forceinline__ uint32_t lane_value(const uint4 (&d)[kRows], const GL
   uint32_t v0 = d[0].x, v1 = d[0].y, v2 = d[0].z, v3 = d[0].w;
 #pragma unroll
   for (int h = 1; h < kRows; ++h) {
-    v0 = g_step(v0, gl) ^ d[h].x;
-    v1 = g_step(v1, gl) ^ d[h].y;
-    v2 = g_step(v2, gl) ^ d[h].z;
-    v3 = g_step(v3, gl) ^ d[h].w;
+    v0 = g_step(v0, d[h].x, gl);
+    v1 = g_step(v1, d[h].y, gl);
+    v2 = g_step(v2, d[h].z, gl);
+    v3 = g_step(v3, d[h].w, gl);
   }
   return lane_merge(v0, v1, v2, v3);
 }
@@ -541,8 +574,8 @@ struct EncShared {
   alignas(16) uint32_t H[256];  // histogram
 };
 static_assert(sizeof(EncShared) <= kLdsMiscBytes, "encoder scratch fits");
-constexpr uint32_t kLdsHistE = kLdsMisc + kLdsMiscBytes;  // 256 bins x 16 copies
-constexpr uint32_t kLdsStage = kLdsHistE + 16384;         // record body staging
+constexpr uint32_t kLdsHistE = kLdsLow;   // 256 bins x 16 copies (16 KiB)
+constexpr uint32_t kLdsStage = kLdsBase;  // record body staging
 // codes + escape index + escapes of a chosen packed record: the plan only
 // packs when the record is smaller than RAW, so they stay below half a chunk
 constexpr uint32_t kLdsStageBytes = kChunk / 2;
@@ -550,7 +583,7 @@ constexpr uint32_t kLdsEncode = kLdsStage + kLdsStageBytes;
 static_assert(kLdsEncode <= 163840, "encoder LDS fits one CU");
 
 __device__ __forceinline__ EncShared &enc_shared() {
-  return *reinterpret_cast<EncShared *>(lds + kLdsMisc);
+  return *reinterpret_cast<EncShared *>(lds_at(kLdsMisc));
 }
 
 __device__ __forceinline__ void status_store(uint64_t *p, uint64_t v) {
@@ -761,6 +794,8 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
 struct RecFields {
   uint32_t item, c, n_words, mode, k, base, n_esc, size, crc;
   bool dirty, bad;
+  uint32_t hcrc;   // CRC of the record header's first 12 bytes
+  uint32_t epart;  // CRC register after the table entry's first 8 bytes
 };
 
 // Control wave: the record's payload offset (finishing the look-back window
@@ -778,10 +813,9 @@ __device__ __forceinline__ void ctl_emit(const EncArgs &a, const RecFields &r, c
   my_last_incl = incl;
   const uint32_t rec_idx = (uint32_t)(excl & 0xFFFFFFu);
   const uint64_t rec_off = 64u + ((excl >> 24) << 4);
-  uint32_t hw[4] = {r.mode | (r.k << 8) | (r.base << 16), r.n_words, r.n_esc, 0};
-  hw[3] = crc_words(hw, 3);
-  uint32_t ew[4] = {r.c, r.crc, (uint32_t)rec_off, (uint32_t)(rec_off >> 32)};
-  const uint32_t eck = crc_words(ew, 4);
+  const uint32_t hw[4] = {r.mode | (r.k << 8) | (r.base << 16), r.n_words, r.n_esc, r.hcrc};
+  const uint32_t ew[4] = {r.c, r.crc, (uint32_t)rec_off, (uint32_t)(rec_off >> 32)};
+  const uint32_t eck = crc_feed(r.epart, ew + 2, 2) ^ 0xFFFFFFFFu;
   if ((threadIdx.x & 63u) == 0) {
     status_store(&status[r.item], (incl << 2) | kFlagIncl);
     if (r.item + 1 == n_items) {
@@ -835,8 +869,8 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   load_crc_tables(g.crc_kind);
   const CrcTables &T = g_tables[g.crc_kind];
   EncShared &sh = enc_shared();
-  uint8_t *stage = lds + kLdsStage;
-  uint32_t *hist = reinterpret_cast<uint32_t *>(lds + kLdsHistE);
+  uint8_t *stage = lds_at(kLdsStage);
+  uint32_t *hist = reinterpret_cast<uint32_t *>(lds_at(kLdsHistE));
   {
     uint4 *h4 = reinterpret_cast<uint4 *>(hist);
     for (uint32_t i = threadIdx.x; i < 1024u; i += kEncThreads) h4[i] = make_uint4(0, 0, 0, 0);
@@ -919,14 +953,17 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       // ---- data: exponent histogram (16 copies x 256 bins) of all 32768
       // words; the words past a short chunk load as zero, and the reduce
       // takes their count off bin 0
-      const uint32_t hb = kLdsHistE + copy4;
+      static_assert(kLdsHistE == 0, "bin address = (e << 6) | copy4");
 #pragma unroll
       for (int h = 0; h < kRows; ++h) {
         const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          atomicAdd(reinterpret_cast<uint32_t *>(lds + hb + (__builtin_amdgcn_ubfe(x[j], 7, 8) << 6)), 1u);
-          atomicAdd(reinterpret_cast<uint32_t *>(lds + hb + (__builtin_amdgcn_ubfe(x[j], 23, 8) << 6)), 1u);
+          // (v & 0x3FC0) | copy4 as one three-input logic op (table 0xEA)
+          atomicAdd(reinterpret_cast<uint32_t *>(
+                        lds_at(__builtin_amdgcn_bitop3_b32(x[j] >> 1, 0x3FC0u, copy4, 0xEA))), 1u);
+          atomicAdd(reinterpret_cast<uint32_t *>(
+                        lds_at(__builtin_amdgcn_bitop3_b32(x[j] >> 17, 0x3FC0u, copy4, 0xEA))), 1u);
         }
       }
     }
@@ -951,14 +988,15 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     __syncthreads();  // B2: H complete
 
     // ---- phase 3
-    uint32_t crc_acc = 0;
+    uint32_t crc_acc = 0, hcrc = 0, epart = 0;
     if (is_ctl) {
       if (cur && need_crc) {
         // the chunk CRC from the data waves' lane values, first step: lane l
         // folds lane l of the eight waves (F^kSub per wave)
         crc_acc = sh.u[l.lane];
 #pragma unroll
-        for (int w = 1; w < kWaves; ++w) crc_acc = tab4(kLdsWaveStep, crc_acc) ^ sh.u[w * 64 + l.lane];
+        for (int w = 1; w < kWaves; ++w) crc_acc = tab4x(kLdsWaveStep, crc_acc, sh.u[w * 64 + l.lane]);
+        crc_acc = lane_tree_rows(crc_acc);
       }
     } else {
       if (pend && p_dirty) {
@@ -1059,9 +1097,9 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         status_store(&status[item], agg | kFlagAgg);
       }
       if (cur && need_crc) {
-        // second step: the lane tree, then the F^4 common to every word
-        // (see lane_value)
-        const uint32_t q = uniform(__builtin_amdgcn_readlane(lane_tree(crc_acc), 63));
+        // second step: the rest of the lane tree, then the F^4 common to
+        // every word (see lane_value)
+        const uint32_t q = uniform(__builtin_amdgcn_readlane(lane_tree_across(crc_acc), 63));
         crc = bad_index ? 0u : finish_crc(tab4(kLdsF4, q), len, g, T);
       }
     } else if (dirty) {
@@ -1093,13 +1131,22 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     }
     __syncthreads();  // B4: codes staged, escape totals known
 
-    if (!HAS_PREV && is_ctl && cur) {
+    if (is_ctl && cur) {
       // ---- control: X_i's offset, prefix, header and table entry.  Its size
       // was published before B4, and the vector-memory pipe is idle here (the
-      // data waves' next loads come after the loop top).
-      const Window win = lookback_issue(status, (int64_t)item - 1, my_last, my_last_incl);
-      const RecFields r = {item, c, n_words, mode, k, base, n_esc, size, crc, dirty, bad_index};
-      ctl_emit(a, r, win, n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
+      // data waves' next loads come after the loop top).  The header CRC and
+      // the entry's CRC prefix are computed while the look-back loads fly.
+      Window win;
+      if (!HAS_PREV) win = lookback_issue(status, (int64_t)item - 1, my_last, my_last_incl);
+      const uint32_t hw[3] = {mode | (k << 8) | (base << 16), n_words, n_esc};
+      hcrc = crc_words(hw, 3);
+      const uint32_t ew[2] = {c, crc};
+      epart = crc_feed(0xFFFFFFFFu, ew, 2);
+      if (!HAS_PREV) {
+        const RecFields r = {item, c, n_words, mode, k, base, n_esc, size, crc, dirty, bad_index,
+                             hcrc, epart};
+        ctl_emit(a, r, win, n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
+      }
     }
 
     // ---- phase 5
@@ -1114,12 +1161,22 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
           *reinterpret_cast<uint16_t *>(stage + s_idx + 2 * (w0 >> 9)) =
               (uint16_t)(wave_base + lane_r[h]);
         uint32_t flags = (escm[h >> 2] >> (8 * (h & 3))) & 255u;
-        uint32_t at = s_esc + wave_base + lane_r[h];
-        while (flags) {  // the lane's escaped exponents, in word order
-          const uint32_t u = __builtin_ctz(flags);
-          flags &= flags - 1u;
-          const uint32_t xw = u < 4 ? (u < 2 ? d[h].x : d[h].y) : (u < 6 ? d[h].z : d[h].w);
-          stage[at++] = (uint8_t)(xw >> (7 + 16 * (u & 1)));
+        if (flags) {  // the lane's escaped exponents, in word order
+          // exponent bytes of the row's eight words: e = high byte << 1 |
+          // low byte >> 7, four words per register
+          const uint4 x = d[h];
+          const uint32_t lo0 = __builtin_amdgcn_perm(x.y, x.x, 0x06040200u);
+          const uint32_t hi0 = __builtin_amdgcn_perm(x.y, x.x, 0x07050301u);
+          const uint32_t lo1 = __builtin_amdgcn_perm(x.w, x.z, 0x06040200u);
+          const uint32_t hi1 = __builtin_amdgcn_perm(x.w, x.z, 0x07050301u);
+          const uint32_t ex = ((hi0 << 1) & 0xFEFEFEFEu) | ((lo0 >> 7) & 0x01010101u);
+          const uint32_t ey = ((hi1 << 1) & 0xFEFEFEFEu) | ((lo1 >> 7) & 0x01010101u);
+          uint32_t at = s_esc + wave_base + lane_r[h];
+          do {  // byte u of (ey:ex) is word u's exponent
+            const uint32_t u = __builtin_ctz(flags);
+            flags &= flags - 1u;
+            stage[at++] = (uint8_t)__builtin_amdgcn_perm(ey, ex, u);
+          } while (flags);
         }
       }
       if (threadIdx.x < 16u) {  // zero padding of index and escapes
@@ -1130,7 +1187,8 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     }
 
     // ---- X_i becomes the pending record
-    if (HAS_PREV) pr = RecFields{item, c, n_words, mode, k, base, n_esc, size, crc, dirty, bad_index};
+    if (HAS_PREV)
+      pr = RecFields{item, c, n_words, mode, k, base, n_esc, size, crc, dirty, bad_index, hcrc, epart};
     pend = cur;
     p_nw = n_words;
     p_dirty = dirty;
@@ -1291,12 +1349,13 @@ struct DecShared {
   uint32_t bad[2][kWaves];   // wave structure failures
 };
 static_assert(sizeof(DecShared) <= kLdsMiscBytes, "decoder scratch fits");
-constexpr uint32_t kLdsDecEsc = kLdsMisc + kLdsMiscBytes;
-constexpr uint32_t kLdsDecode = kLdsDecEsc + kWaves * kDecEscBytes + 16;  // + read slack
+constexpr uint32_t kLdsDecEsc = kLdsLow;  // + 16 B of read slack, inside the region
+static_assert(kWaves * kDecEscBytes + 16 <= kLdsLowBytes, "escape windows fit");
+constexpr uint32_t kLdsDecode = kLdsBase;
 static_assert(kLdsDecode <= 163840, "decoder LDS fits one CU");
 
 __device__ __forceinline__ DecShared &dec_shared() {
-  return *reinterpret_cast<DecShared *>(lds + kLdsMisc);
+  return *reinterpret_cast<DecShared *>(lds_at(kLdsMisc));
 }
 
 // Control wave: record checks in three steps, each a memory round trip that
@@ -1672,10 +1731,10 @@ __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, co
     if (h == 0) {
       cv[0] = out[0], cv[1] = out[1], cv[2] = out[2], cv[3] = out[3];
     } else {
-      cv[0] = g_step(cv[0], gl) ^ out[0];
-      cv[1] = g_step(cv[1], gl) ^ out[1];
-      cv[2] = g_step(cv[2], gl) ^ out[2];
-      cv[3] = g_step(cv[3], gl) ^ out[3];
+      cv[0] = g_step(cv[0], out[0], gl);
+      cv[1] = g_step(cv[1], out[1], gl);
+      cv[2] = g_step(cv[2], out[2], gl);
+      cv[3] = g_step(cv[3], out[3], gl);
     }
     dec_store(dst, l.off0 + h * kRow, v.len, out);
   }
@@ -1698,7 +1757,7 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
   const bool is_ctl = threadIdx.x >= (uint32_t)kThreads;
   const GLane gl = glane_make();
   const Lane l0 = lane_info();
-  uint8_t *stage = lds + kLdsDecEsc + l0.wave * kDecEscBytes;
+  uint8_t *stage = lds_at(kLdsDecEsc + l0.wave * kDecEscBytes);
   const uint32_t G = gridDim.x;
   const uint32_t my_n = blockIdx.x < n_rec ? (n_rec - 1 - blockIdx.x) / G + 1 : 0;
   auto rec_of = [&](uint32_t i) { return blockIdx.x + i * G; };
@@ -1843,20 +1902,24 @@ int upload_tables(int device, const CrcTables tabs[2]) {
   return (int)hipDeviceSynchronize();
 }
 
+// Dynamic LDS limits, and the premise of lds_at: the kernels that address
+// dynamic LDS from 0 have no static LDS.
 int set_kernel_attributes() {
-  hipError_t e;
-  e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_checksum),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBase);
-  if (e != hipSuccess) return (int)e;
-  e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_encode<false>),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kLdsEncode);
-  if (e != hipSuccess) return (int)e;
-  e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_encode<true>),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kLdsEncode);
-  if (e != hipSuccess) return (int)e;
-  e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_decode),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kLdsDecode);
-  return (int)e;
+  const void *kern[4] = {reinterpret_cast<const void *>(&k_checksum),
+                         reinterpret_cast<const void *>(&k_encode<false>),
+                         reinterpret_cast<const void *>(&k_encode<true>),
+                         reinterpret_cast<const void *>(&k_decode)};
+  const uint32_t bytes[4] = {kLdsBase, kLdsEncode, kLdsEncode, kLdsDecode};
+  for (int i = 0; i < 4; ++i) {
+    hipError_t e = hipFuncSetAttribute(kern[i], hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)bytes[i]);
+    if (e != hipSuccess) return (int)e;
+    hipFuncAttributes fa;
+    e = hipFuncGetAttributes(&fa, kern[i]);
+    if (e != hipSuccess) return (int)e;
+    if (fa.sharedSizeBytes != 0) return (int)hipErrorInvalidConfiguration;
+  }
+  return 0;
 }
 
 static int launch_combine(const CombineJobs &jobs, int n_jobs, void *stream) {
