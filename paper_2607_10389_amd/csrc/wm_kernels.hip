@@ -574,7 +574,7 @@ struct EncShared {
   alignas(16) uint32_t H[256];  // histogram
 };
 static_assert(sizeof(EncShared) <= kLdsMiscBytes, "encoder scratch fits");
-constexpr uint32_t kLdsHistE = kLdsLow;   // 256 bins x 16 copies (16 KiB)
+constexpr uint32_t kLdsHistE = kLdsLow;   // 256 bins x 32 copies of u16 (16 KiB)
 constexpr uint32_t kLdsStage = kLdsBase;  // record body staging
 // codes + escape index + escapes of a chosen packed record: the plan only
 // packs when the record is smaller than RAW, so they stay below half a chunk
@@ -790,6 +790,39 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
   }
 }
 
+// A data wave's share of a chunk's exponent histogram in the low LDS
+// region: all 32768 words, the words past a short chunk loaded as zero (the
+// reduce takes their count off bin 0).  32 copies of 16-bit counters, copy =
+// lane mod 32, so the 32 lanes an LDS cycle serves never touch the same bank
+// (nor the same counter); bins 2m and 2m + 1 are the halves of dword
+// m * 32 + copy.  A copy counts at most 16 lanes x 64 words.
+// 1 + b * 0xFFFF (b = 0 or 1) in one instruction: the increment of the low
+// or the high 16-bit counter of a dword.
+__device__ __forceinline__ uint32_t half_inc(uint32_t b) {
+  uint32_t r;
+  asm("v_mad_u32_u24 %0, %1, %2, 1" : "=v"(r) : "v"(b), "s"(0xFFFFu));
+  return r;
+}
+
+__device__ __forceinline__ void hist_add(const uint4 (&d)[kRows], uint32_t copy4) {
+  static_assert(kLdsHistE == 0, "bin pair address = (e >> 1 << 7) | copy4");
+#pragma unroll
+  for (int h = 0; h < kRows; ++h) {
+    const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      // (v & 0x3F80) | copy4 as one three-input logic op (table 0xEA); the
+      // exponent's low bit picks the counter half
+      atomicAdd(reinterpret_cast<uint32_t *>(
+                    lds_at(__builtin_amdgcn_bitop3_b32(x[j] >> 1, 0x3F80u, copy4, 0xEA))),
+                half_inc(__builtin_amdgcn_ubfe(x[j], 7, 1)));
+      atomicAdd(reinterpret_cast<uint32_t *>(
+                    lds_at(__builtin_amdgcn_bitop3_b32(x[j] >> 17, 0x3F80u, copy4, 0xEA))),
+                half_inc(__builtin_amdgcn_ubfe(x[j], 23, 1)));
+    }
+  }
+}
+
 // A chunk's record fields as the control wave holds them (uniform).
 struct RecFields {
   uint32_t item, c, n_words, mode, k, base, n_esc, size, crc;
@@ -843,15 +876,16 @@ __device__ __forceinline__ void ctl_emit(const EncArgs &a, const RecFields &r, c
 // run alongside and have published theirs by then); for a step, whose clean
 // chunks finish early and let workgroups drift apart, in phase 1 of
 // iteration i, issued before B0 and finished after it.
-//   phase 1 (..B1): data: prefetch X_{i+1}, lane CRC values and histogram of
-//                   X_i; control: next ticket
-//   phase 2 (..B2): data: reduce the histogram
+//   phase 1 (..B1): data: prefetch X_{i+1}, lane CRC values of X_i;
+//                   control: next ticket
+//   phase 2 (..B2): data: reduce X_i's histogram (accumulated in phase 4 of
+//                   iteration i-1, or before the loop for the first chunk)
 //   phase 3 (..B3): data: write X_{i-1} (staging + sign/mantissa bytes),
 //                   score the plan candidates of X_i; control: first step
 //                   of X_i's CRC
 //   phase 4 (..B4): all: pick X_i's plan; control: publish its size, finish
-//                   its CRC; data: codes into staging, escape counts,
-//                   sign/mantissa bytes
+//                   its CRC; data: X_{i+1}'s histogram, X_i's codes into
+//                   staging, escape counts, sign/mantissa bytes
 //   phase 5:        control (full ship): look-back of X_i, its prefix,
 //                   header and table entry; data: escape index and escapes
 //                   into staging
@@ -890,6 +924,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     const uint32_t c = item < n_items ? uniform(item_chunk(a, item, g)) : 0xFFFFFFFFu;
     load_chunk(a.cur + (uint64_t)(c < g.n_chunks ? c : 0u) * kChunk,
                c < g.n_chunks ? chunk_len(g, c) : 0u, l0, d);
+    if (c < g.n_chunks) hist_add(d, (l0.lane & 31u) * 4u);  // copies zeroed before the barrier
   }
 
   // the chunk whose record is still to be written (uniform), and its
@@ -906,7 +941,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   while (item < n_items || pend) {
     const bool cur = item < n_items;
     const Lane l = lane_fresh(l0);
-    const uint32_t copy4 = (l.lane & 15u) * 4u;
+    const uint32_t copy4 = (l.lane & 31u) * 4u;
     uint32_t c = cur ? uniform(item_chunk(a, item, g)) : 0u;
     const bool bad_index = cur && c >= g.n_chunks;
     if (!cur || bad_index) c = 0;
@@ -915,6 +950,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     const bool full = len == kChunk;
     uint4 dn[kRows];
     uint32_t ticket = 0;
+    bool next_valid = false;  // X_{i+1} exists and its index is valid
 
     // ---- phase 1
     Window win;
@@ -923,8 +959,9 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       if (HAS_PREV) load_chunk(a.prev + (uint64_t)c * kChunk, len, l, p);
       {
         const uint32_t cn = next < n_items ? uniform(item_chunk(a, next, g)) : 0xFFFFFFFFu;
-        load_chunk(a.cur + (uint64_t)(cn < g.n_chunks ? cn : 0u) * kChunk,
-                   cn < g.n_chunks ? chunk_len(g, cn) : 0u, l, dn);
+        next_valid = cn < g.n_chunks;
+        load_chunk(a.cur + (uint64_t)(next_valid ? cn : 0u) * kChunk,
+                   next_valid ? chunk_len(g, cn) : 0u, l, dn);
       }
       if (need_crc && cur) sh.u[l.wave * 64u + l.lane] = lane_value(d, gl);
       if (HAS_PREV) {
@@ -949,25 +986,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       if (is_ctl && pend)  // ---- control: X_{i-1}'s offset, header and table entry
         ctl_emit(a, pr, win, n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
     }
-    if (!is_ctl && dirty) {
-      // ---- data: exponent histogram (16 copies x 256 bins) of all 32768
-      // words; the words past a short chunk load as zero, and the reduce
-      // takes their count off bin 0
-      static_assert(kLdsHistE == 0, "bin address = (e << 6) | copy4");
-#pragma unroll
-      for (int h = 0; h < kRows; ++h) {
-        const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          // (v & 0x3FC0) | copy4 as one three-input logic op (table 0xEA)
-          atomicAdd(reinterpret_cast<uint32_t *>(
-                        lds_at(__builtin_amdgcn_bitop3_b32(x[j] >> 1, 0x3FC0u, copy4, 0xEA))), 1u);
-          atomicAdd(reinterpret_cast<uint32_t *>(
-                        lds_at(__builtin_amdgcn_bitop3_b32(x[j] >> 17, 0x3FC0u, copy4, 0xEA))), 1u);
-        }
-      }
-    }
-    __syncthreads();  // B1: histogram copies, CRC partials, X_{i-1}'s offset
+    __syncthreads();  // B1: CRC lane values, X_{i-1}'s offset
 
     // ---- phase 2
     uint32_t crc = 0;
@@ -977,13 +996,18 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         if (l.lane == 0) sh.next = ticket;
       }
     } else if (dirty) {
-      // reduce the copies: wave w sums bins 32w..32w+31 (its own 2 KiB of them)
-      const uint32_t bin = l.wave * 32u + (l.lane >> 1), half = l.lane & 1u;
+      // reduce the copies: wave w sums bins 32w..32w+31 (its own 2 KiB of
+      // them); four lanes share a bin pair, eight copies each, the packed
+      // halves adding without carry (each total is at most 32768)
+      const uint32_t pair = l.wave * 16u + (l.lane >> 2), q = l.lane & 3u;
       uint32_t s = 0;
 #pragma unroll
-      for (int cc = 0; cc < 8; ++cc) s += hist[bin * 16u + half * 8u + ((cc + (l.lane >> 1)) & 7u)];
+      for (int cc = 0; cc < 8; ++cc) s += hist[pair * 32u + q * 8u + ((cc + (l.lane >> 2)) & 7u)];
       s += (uint32_t)__shfl_xor((int)s, 1, 64);
-      if (half == 0) sh.H[bin] = bin == 0 ? s - (kChunk / 2 - n_words) : s;
+      s += (uint32_t)__shfl_xor((int)s, 2, 64);
+      if (q == 0)
+        *reinterpret_cast<uint2 *>(&sh.H[2 * pair]) =
+            make_uint2((s & 0xFFFFu) - (pair == 0 ? kChunk / 2 - n_words : 0u), s >> 16);
     }
     __syncthreads();  // B2: H complete
 
@@ -1057,6 +1081,9 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         }
         uint4 *s4 = reinterpret_cast<uint4 *>(slice);
         for (uint32_t i = l.lane; i < 128u; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
+      } else if (HAS_PREV && cur) {  // a clean chunk's histogram, unused
+        uint4 *s4 = reinterpret_cast<uint4 *>(hist + l.wave * 512u);
+        for (uint32_t i = l.lane; i < 128u; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
       }
     }
     __syncthreads();  // B3: candidates scored, X_{i-1}'s staging read
@@ -1102,7 +1129,12 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         const uint32_t q = uniform(__builtin_amdgcn_readlane(lane_tree_across(crc_acc), 63));
         crc = bad_index ? 0u : finish_crc(tab4(kLdsF4, q), len, g, T);
       }
-    } else if (dirty) {
+    } else {
+      // ---- data: X_{i+1}'s histogram (its loads were issued an iteration
+      // ago); the atomics drain while the codes below keep the VALUs busy
+      if (next_valid) hist_add(dn, copy4);
+    }
+    if (!is_ctl && dirty) {
       if (pack) {
         // ---- data: codes into staging, escape flags and counts
         if (!full) {  // the wave's own code bytes; lanes past the chunk write none
