@@ -1377,12 +1377,16 @@ struct CtlRec {  // one record in the control pipeline (LDS, written by lane 0)
 struct DecShared {
   DecMeta meta[3];
   CtlRec cr[4];  // control pipeline, slot = record step & 3
-  uint32_t part[2][kWaves];  // wave CRC partials
   uint32_t bad[2][kWaves];   // wave structure failures
 };
 static_assert(sizeof(DecShared) <= kLdsMiscBytes, "decoder scratch fits");
 constexpr uint32_t kLdsDecEsc = kLdsLow;  // + 16 B of read slack, inside the region
-static_assert(kWaves * kDecEscBytes + 16 <= kLdsLowBytes, "escape windows fit");
+// lane CRC values of a record (lane_value), double-buffered by record step
+constexpr uint32_t kLdsDecU = kLdsDecEsc + kWaves * kDecEscBytes + 256;
+static_assert(kLdsDecU + 2 * kThreads * 4 <= kLdsLow + kLdsLowBytes, "decoder low region fits");
+__device__ __forceinline__ uint32_t *dec_u(uint32_t b) {
+  return reinterpret_cast<uint32_t *>(lds_at(kLdsDecU + b * (kThreads * 4u)));
+}
 constexpr uint32_t kLdsDecode = kLdsBase;
 static_assert(kLdsDecode <= 163840, "decoder LDS fits one CU");
 
@@ -1843,29 +1847,33 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
             case 7: bad = dec_packed<7>(cur, v, M, l, stage, dst, cv, gl); break;
             default: bad = dec_packed<8>(cur, v, M, l, stage, dst, cv, gl); break;
           }
-          const uint32_t q = lane_tree(lane_merge(cv[0], cv[1], cv[2], cv[3]));
-          const uint32_t part = wave_part(T, l.wave, q);
+          dec_u(i & 1)[l.wave * 64u + l.lane] = lane_merge(cv[0], cv[1], cv[2], cv[3]);
           const bool any_bad = __ballot(bad) != 0;
-          if (l.lane == 0) {
-            sh.part[i & 1][l.wave] = part;
-            sh.bad[i & 1][l.wave] = any_bad ? 1u : 0u;
-          }
+          if (l.lane == 0) sh.bad[i & 1][l.wave] = any_bad ? 1u : 0u;
         }
       }
     } else {
-      if (i >= 1) {  // settle the previous record
+      CtlLoads L;
+      ctl_header_issue(payload, sh.cr[(i + 3) & 3], L);
+      ctl_entry_issue(payload, table_off, n_rec, rec_of(i + 4), i + 4 < my_n, L);
+      if (i >= 1) {  // settle the previous record, while those loads fly
         const DecMeta &M = sh.meta[(i - 1) % 3];
         uint32_t st = uniform(M.st);
         if (st != kMetaSkip) {
           if (st == 0) {
-            uint32_t raw = 0, bad = 0;
+            uint32_t bad = 0;
 #pragma unroll
-            for (int w = 0; w < kWaves; ++w) {
-              raw ^= sh.part[(i - 1) & 1][w];
-              bad |= sh.bad[(i - 1) & 1][w];
-            }
+            for (int w = 0; w < kWaves; ++w) bad |= sh.bad[(i - 1) & 1][w];
+            // the record's CRC from the data waves' lane values: lane l folds
+            // lane l of the eight waves (F^kSub per wave), then the lane tree,
+            // then the F^4 common to every word (see lane_value)
+            const uint32_t *u = dec_u((i - 1) & 1);
+            uint32_t acc = u[l.lane];
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) acc = tab4x(kLdsWaveStep, acc, u[w * 64 + l.lane]);
+            const uint32_t q = uniform(__builtin_amdgcn_readlane(lane_tree(acc), 63));
             const uint32_t c = uniform(M.c);
-            const uint32_t crc = finish_crc(raw, chunk_len(g, c), g, T);
+            const uint32_t crc = finish_crc(tab4(kLdsF4, q), chunk_len(g, c), g, T);
             st = bad ? 4u : (crc != uniform(M.src_crc) ? 8u : 0u);
           }
           if (l.lane == 0) {
@@ -1874,9 +1882,6 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
           }
         }
       }
-      CtlLoads L;
-      ctl_header_issue(payload, sh.cr[(i + 3) & 3], L);
-      ctl_entry_issue(payload, table_off, n_rec, rec_of(i + 4), i + 4 < my_n, L);
       ctl_body(payload, sh.cr[(i + 2) & 3], g, ecrc, ctl, sh.meta[(i + 2) % 3]);
       ctl_header_record(L, sh.cr[(i + 3) & 3]);
       ctl_entry_record(table_off, n_rec, rec_of(i + 4), i + 4 < my_n, g, L, sh.cr[(i + 4) & 3]);
