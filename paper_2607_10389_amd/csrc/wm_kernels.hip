@@ -1603,15 +1603,20 @@ __device__ __forceinline__ DecView dec_view(const uint8_t *payload, const DecMet
 // The same 17 loads for every record (codes or RAW exponent bytes, sign /
 // mantissa bytes, the head of the wave's escape range) through a descriptor
 // that covers the record, so the compiler can count them on every path.
+__device__ __forceinline__ void dec_load_row(DecBuf &B, const DecView &v, const Lane &l, Rsrc r,
+                                             int h) {
+  const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+  B.a[h] = buf16(r, 16u + (((w0 >> 3) * v.k) & ~3u));
+  B.b[h] = buf8(r, v.sm_off + w0);
+}
+__device__ __forceinline__ void dec_load_esc(DecBuf &B, const DecView &v, const Lane &l, Rsrc r) {
+  B.e = buf16(r, v.esc_off + v.al + 16u * l.lane);
+}
 __device__ __forceinline__ void dec_load(DecBuf &B, const DecView &v, const Lane &l) {
   const Rsrc r = rsrc(v.rec, v.rlen);
 #pragma unroll
-  for (int h = 0; h < kRows; ++h) {
-    const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-    B.a[h] = buf16(r, 16u + (((w0 >> 3) * v.k) & ~3u));
-    B.b[h] = buf8(r, v.sm_off + w0);
-  }
-  B.e = buf16(r, v.esc_off + v.al + 16u * l.lane);
+  for (int h = 0; h < kRows; ++h) dec_load_row(B, v, l, r, h);
+  dec_load_esc(B, v, l, r);
 }
 
 __device__ __forceinline__ void dec_store(uint8_t *dst, uint32_t o, uint32_t len,
@@ -1677,7 +1682,12 @@ __device__ __forceinline__ uint2 assemble4(uint32_t e, uint32_t s) {
 template <uint32_t K>
 __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, const DecMeta &M,
                                            const Lane &l, uint8_t *stage, uint8_t *dst,
-                                           uint32_t (&cv)[4], const GLane &gl) {
+                                           uint32_t (&cv)[4], const GLane &gl, DecBuf &N,
+                                           const DecView &vn) {
+  // the next record's loads go out one row at a time, between the rows of
+  // this one, so the memory pipe takes them while the VALUs decode
+  const Rsrc rn = rsrc(vn.rec, vn.rlen);
+  dec_load_esc(N, vn, l, rn);
   constexpr bool kEsc = K > 0 && K < 8;  // K = 8: RAW exponent bytes, no escapes
   constexpr uint32_t esc = K < 8 ? (1u << K) - 1u : 255u;
   bool bad = false;
@@ -1690,6 +1700,7 @@ __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, co
   if (kEsc) *reinterpret_cast<uint4 *>(stage + 16u * l.lane) = B.e;
 #pragma unroll
   for (int h = 0; h < kRows; ++h) {
+    dec_load_row(N, vn, l, rn, h);
     const uint32_t row = l.wave * kRows + h;
     const uint32_t w0 = (l.off0 + h * kRow) >> 1;
     uint32_t out[4] = {0, 0, 0, 0};
@@ -1823,29 +1834,28 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
   for (uint32_t i = 0; i <= my_n; ++i) {
     const Lane l = lane_fresh(l0);
     if (!is_ctl) {
-      {
-        const DecMeta &Mn = sh.meta[(i + 1) % 3];
-        DecView vn = dec_view(payload, Mn, l, g);
-        if (i + 1 >= my_n || uniform(Mn.st) != 0) vn.rlen = 0;  // loads become no-ops
-        dec_load(nxt, vn, l);
-      }
-      if (i < my_n) {
-        const DecMeta &M = sh.meta[i % 3];
-        if (uniform(M.st) == 0) {
+      const DecMeta &Mn = sh.meta[(i + 1) % 3];
+      DecView vn = dec_view(payload, Mn, l, g);
+      if (i + 1 >= my_n || uniform(Mn.st) != 0) vn.rlen = 0;  // loads become no-ops
+      const DecMeta &M = sh.meta[i % 3];
+      if (i >= my_n || uniform(M.st) != 0) {
+        dec_load(nxt, vn, l);  // nothing to decode in this step
+      } else {
+        {
           const DecView v = dec_view(payload, M, l, g);
           uint8_t *dst = staging + (uint64_t)v.r * kChunk;
           uint32_t cv[4] = {0, 0, 0, 0};
           bool bad = false;
           switch (v.k) {  // 8: RAW exponent plane
-            case 0: bad = dec_packed<0>(cur, v, M, l, stage, dst, cv, gl); break;
-            case 1: bad = dec_packed<1>(cur, v, M, l, stage, dst, cv, gl); break;
-            case 2: bad = dec_packed<2>(cur, v, M, l, stage, dst, cv, gl); break;
-            case 3: bad = dec_packed<3>(cur, v, M, l, stage, dst, cv, gl); break;
-            case 4: bad = dec_packed<4>(cur, v, M, l, stage, dst, cv, gl); break;
-            case 5: bad = dec_packed<5>(cur, v, M, l, stage, dst, cv, gl); break;
-            case 6: bad = dec_packed<6>(cur, v, M, l, stage, dst, cv, gl); break;
-            case 7: bad = dec_packed<7>(cur, v, M, l, stage, dst, cv, gl); break;
-            default: bad = dec_packed<8>(cur, v, M, l, stage, dst, cv, gl); break;
+            case 0: bad = dec_packed<0>(cur, v, M, l, stage, dst, cv, gl, nxt, vn); break;
+            case 1: bad = dec_packed<1>(cur, v, M, l, stage, dst, cv, gl, nxt, vn); break;
+            case 2: bad = dec_packed<2>(cur, v, M, l, stage, dst, cv, gl, nxt, vn); break;
+            case 3: bad = dec_packed<3>(cur, v, M, l, stage, dst, cv, gl, nxt, vn); break;
+            case 4: bad = dec_packed<4>(cur, v, M, l, stage, dst, cv, gl, nxt, vn); break;
+            case 5: bad = dec_packed<5>(cur, v, M, l, stage, dst, cv, gl, nxt, vn); break;
+            case 6: bad = dec_packed<6>(cur, v, M, l, stage, dst, cv, gl, nxt, vn); break;
+            case 7: bad = dec_packed<7>(cur, v, M, l, stage, dst, cv, gl, nxt, vn); break;
+            default: bad = dec_packed<8>(cur, v, M, l, stage, dst, cv, gl, nxt, vn); break;
           }
           dec_u(i & 1)[l.wave * 64u + l.lane] = lane_merge(cv[0], cv[1], cv[2], cv[3]);
           const bool any_bad = __ballot(bad) != 0;
