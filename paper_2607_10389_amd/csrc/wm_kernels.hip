@@ -324,6 +324,34 @@ __device__ __forceinline__ uint32_t lane_value(const uint4 (&d)[kRows], const GL
   return lane_merge(v0, v1, v2, v3);
 }
 
+// lane_value of d while the next chunk's rows load into dn (one load per
+// row step, so the memory pipe takes them between the LDS rounds); a short
+// chunk's straddling piece is refetched as in load_chunk.
+__device__ __forceinline__ uint32_t lane_value_load(const uint4 (&d)[kRows], const GLane &gl,
+                                                    const uint8_t *__restrict__ nbase,
+                                                    uint32_t nlen, const Lane &l,
+                                                    uint4 (&dn)[kRows]) {
+  const Rsrc r = rsrc(nbase, nlen);
+  dn[0] = buf16<kNt>(r, l.off0);
+  uint32_t v0 = d[0].x, v1 = d[0].y, v2 = d[0].z, v3 = d[0].w;
+#pragma unroll
+  for (int h = 1; h < kRows; ++h) {
+    dn[h] = buf16<kNt>(r, l.off0 + h * kRow);
+    v0 = g_step(v0, d[h].x, gl);
+    v1 = g_step(v1, d[h].y, gl);
+    v2 = g_step(v2, d[h].z, gl);
+    v3 = g_step(v3, d[h].w, gl);
+  }
+  if (nlen & 15u) {
+#pragma unroll
+    for (int h = 0; h < kRows; ++h) {
+      const uint32_t off = l.off0 + h * kRow;
+      if (off < nlen && off + 16u > nlen) dn[h] = load16_partial(nbase + off, nlen - off);
+    }
+  }
+  return lane_merge(v0, v1, v2, v3);
+}
+
 // Wave-level CRC value Q of the wave's 8 rows (valid in lane 63).
 __device__ __forceinline__ uint32_t wave_q(const uint4 (&d)[kRows],
                                            const GLane &gl) {
@@ -960,10 +988,15 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       {
         const uint32_t cn = next < n_items ? uniform(item_chunk(a, next, g)) : 0xFFFFFFFFu;
         next_valid = cn < g.n_chunks;
-        load_chunk(a.cur + (uint64_t)(next_valid ? cn : 0u) * kChunk,
-                   next_valid ? chunk_len(g, cn) : 0u, l, dn);
+        const uint8_t *nbase = a.cur + (uint64_t)(next_valid ? cn : 0u) * kChunk;
+        const uint32_t nlen = next_valid ? chunk_len(g, cn) : 0u;
+        if (!HAS_PREV && need_crc && cur) {  // X_i's lane CRC values while X_{i+1} loads
+          sh.u[l.wave * 64u + l.lane] = lane_value_load(d, gl, nbase, nlen, l, dn);
+        } else {  // (the step variant keeps prev's rows live as well: no room)
+          load_chunk(nbase, nlen, l, dn);
+          if (need_crc && cur) sh.u[l.wave * 64u + l.lane] = lane_value(d, gl);
+        }
       }
-      if (need_crc && cur) sh.u[l.wave * 64u + l.lane] = lane_value(d, gl);
       if (HAS_PREV) {
         uint32_t diff = 0;
 #pragma unroll
