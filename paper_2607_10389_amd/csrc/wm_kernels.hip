@@ -1388,7 +1388,9 @@ __global__ __launch_bounds__(64) void k_decode_prepare(
 // the current record in registers and have the next one's loads in flight
 // while they decode; the control wave also settles the previous record
 // (chunk CRC from the wave partials, status).
-constexpr int kDecThreads = kThreads + 64;
+// 8 data waves, the record-check wave and the settle wave (CRC of the
+// decoded record against its receipt)
+constexpr int kDecThreads = kThreads + 128;
 constexpr uint32_t kDecEscBytes = 1024;  // escape window prefetched per data wave
 constexpr uint32_t kMetaSkip = 0xFFu;    // table entry rejected: no record status
 
@@ -1408,7 +1410,7 @@ struct CtlRec {  // one record in the control pipeline (LDS, written by lane 0)
 };
 
 struct DecShared {
-  DecMeta meta[3];
+  DecMeta meta[4];  // slot = record step & 3
   CtlRec cr[4];  // control pipeline, slot = record step & 3
   uint32_t bad[2][kWaves];   // wave structure failures
 };
@@ -1766,35 +1768,34 @@ __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, co
       if (kEsc) {
         // the index entry of this block equals the escapes before it
         if (uniform(M.ent[row]) != acc) bad = true;
-        if (__ballot((f.x | f.y) != 0)) {
-          // The lane's escapes are cnt consecutive bytes from rank r0 on;
-          // byte u of the lane takes escape number (flagged bytes before u).
-          const uint32_t bx = f.x >> K, by = f.y >> K;  // 0x01 per flagged byte
-          const uint32_t cx = __popc(bx), cnt = cx + __popc(by);
-          const uint32_t incl = wave_incl_scan(cnt);
-          const uint32_t r0 = acc + incl - cnt;
-          acc += __builtin_amdgcn_readlane(incl, 63);
-          if (cnt) {
-            if (r0 + cnt > eec) bad = true;
-            uint2 ev;
-            const uint32_t at = r0 - v.al;
-            if (at + cnt <= kDecEscBytes) {
-              const uint32_t *w = reinterpret_cast<const uint32_t *>(stage + (at & ~3u));
-              const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], sa = (at & 3u) * 8u;
-              ev = make_uint2(__builtin_amdgcn_alignbit(w1, w0, sa),
-                              __builtin_amdgcn_alignbit(w2, w1, sa));
-            } else {  // past the prefetched window
-              uint32_t t[2] = {0, 0};
-              for (uint32_t j = 0; j < cnt; ++j)
-                if (r0 + j < eec) t[j >> 2] |= (uint32_t)v.rec[v.esc_off + r0 + j] << (8 * (j & 3));
-              ev = make_uint2(t[0], t[1]);
-            }
-            const uint32_t px = (bx << 8) + (bx << 16) + (bx << 24);  // exclusive prefix
-            const uint32_t py = (by << 8) + (by << 16) + (by << 24) + cx * 0x01010101u;
-            e.x = bfi((bx << 8) - bx, __builtin_amdgcn_perm(ev.y, ev.x, px), e.x);
-            e.y = bfi((by << 8) - by, __builtin_amdgcn_perm(ev.y, ev.x, py), e.y);
+        // The lane's escapes are cnt consecutive bytes from rank r0 on; byte
+        // u of the lane takes escape number (flagged bytes before u).  No
+        // branch on the flags: a lane without escapes merges nothing.
+        const uint32_t bx = f.x >> K, by = f.y >> K;  // 0x01 per flagged byte
+        const uint32_t cx = __popc(bx), cnt = cx + __popc(by);
+        const uint32_t incl = wave_incl_scan(cnt);
+        const uint32_t r0 = acc + incl - cnt;
+        acc += __builtin_amdgcn_readlane(incl, 63);
+        if (r0 + cnt > eec) bad = true;
+        const uint32_t at = r0 - v.al;
+        const bool in_win = at + cnt <= kDecEscBytes;
+        const uint32_t atw = in_win ? at : 0u;  // an address inside the window
+        const uint32_t *w = reinterpret_cast<const uint32_t *>(stage + (atw & ~3u));
+        const uint32_t sa = (atw & 3u) * 8u;
+        uint2 ev = make_uint2(__builtin_amdgcn_alignbit(w[1], w[0], sa),
+                              __builtin_amdgcn_alignbit(w[2], w[1], sa));
+        if (__ballot(!in_win && cnt != 0)) {  // rare: past the prefetched window
+          if (!in_win && cnt != 0) {
+            uint32_t t[2] = {0, 0};
+            for (uint32_t j = 0; j < cnt; ++j)
+              if (r0 + j < eec) t[j >> 2] |= (uint32_t)v.rec[v.esc_off + r0 + j] << (8 * (j & 3));
+            ev = make_uint2(t[0], t[1]);
           }
         }
+        const uint32_t px = (bx << 8) + (bx << 16) + (bx << 24);  // exclusive prefix
+        const uint32_t py = (by << 8) + (by << 16) + (by << 24) + cx * 0x01010101u;
+        e.x = bfi((bx << 8) - bx, __builtin_amdgcn_perm(ev.y, ev.x, px), e.x);
+        e.y = bfi((by << 8) - by, __builtin_amdgcn_perm(ev.y, ev.x, py), e.y);
       }
       const uint2 lo = assemble4(e.x, B.b[h].x), hi = assemble4(e.y, B.b[h].y);
       out[0] = lo.x;
@@ -1834,7 +1835,8 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
   __syncthreads();
   const CrcTables &T = g_tables[g.crc_kind];
   DecShared &sh = dec_shared();
-  const bool is_ctl = threadIdx.x >= (uint32_t)kThreads;
+  const bool is_ctl = threadIdx.x >= (uint32_t)kThreads;  // either control wave
+  const bool is_settle = threadIdx.x >= (uint32_t)kThreads + 64u;
   const GLane gl = glane_make();
   const Lane l0 = lane_info();
   uint8_t *stage = lds_at(kLdsDecEsc + l0.wave * kDecEscBytes);
@@ -1844,7 +1846,7 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
 
   // control pipeline: in step i, records i+2 (body), i+3 (header) and i+4
   // (entry)
-  if (is_ctl) {
+  if (is_ctl && !is_settle) {
     CtlLoads L;
     for (uint32_t j = 0; j < 4; ++j) {
       ctl_entry_issue(payload, table_off, n_rec, rec_of(j), j < my_n, L);
@@ -1867,10 +1869,10 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
   for (uint32_t i = 0; i <= my_n; ++i) {
     const Lane l = lane_fresh(l0);
     if (!is_ctl) {
-      const DecMeta &Mn = sh.meta[(i + 1) % 3];
+      const DecMeta &Mn = sh.meta[(i + 1) & 3];
       DecView vn = dec_view(payload, Mn, l, g);
       if (i + 1 >= my_n || uniform(Mn.st) != 0) vn.rlen = 0;  // loads become no-ops
-      const DecMeta &M = sh.meta[i % 3];
+      const DecMeta &M = sh.meta[i & 3];
       if (i >= my_n || uniform(M.st) != 0) {
         dec_load(nxt, vn, l);  // nothing to decode in this step
       } else {
@@ -1895,12 +1897,9 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
           if (l.lane == 0) sh.bad[i & 1][l.wave] = any_bad ? 1u : 0u;
         }
       }
-    } else {
-      CtlLoads L;
-      ctl_header_issue(payload, sh.cr[(i + 3) & 3], L);
-      ctl_entry_issue(payload, table_off, n_rec, rec_of(i + 4), i + 4 < my_n, L);
-      if (i >= 1) {  // settle the previous record, while those loads fly
-        const DecMeta &M = sh.meta[(i - 1) % 3];
+    } else if (is_settle) {
+      if (i >= 1) {  // settle the previous record
+        const DecMeta &M = sh.meta[(i - 1) & 3];
         uint32_t st = uniform(M.st);
         if (st != kMetaSkip) {
           if (st == 0) {
@@ -1925,7 +1924,11 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
           }
         }
       }
-      ctl_body(payload, sh.cr[(i + 2) & 3], g, ecrc, ctl, sh.meta[(i + 2) % 3]);
+    } else {
+      CtlLoads L;
+      ctl_header_issue(payload, sh.cr[(i + 3) & 3], L);
+      ctl_entry_issue(payload, table_off, n_rec, rec_of(i + 4), i + 4 < my_n, L);
+      ctl_body(payload, sh.cr[(i + 2) & 3], g, ecrc, ctl, sh.meta[(i + 2) & 3]);
       ctl_header_record(L, sh.cr[(i + 3) & 3]);
       ctl_entry_record(table_off, n_rec, rec_of(i + 4), i + 4 < my_n, g, L, sh.cr[(i + 4) & 3]);
     }
