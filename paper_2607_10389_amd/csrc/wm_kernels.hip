@@ -561,16 +561,9 @@ __global__ __launch_bounds__(1024) void k_compact(const uint32_t *__restrict__ f
 // One 576-thread workgroup per CU: 8 data waves hold a chunk in registers
 // (8 rows each) and a dedicated control wave owns everything that waits on
 // global memory other than the data itself (tickets, the decoupled
-// look-back of record offsets, the plan, headers).  Per chunk:
-//   data   : prefetch next chunk | CRC streams | exponent histogram  [B1]
-//            reduce histogram                                         [B2]
-//            clear histogram                                          [B3]
-//            k-bit codes into LDS, escape flags                       [B4]
-//            write sign/mantissa plane, codes, escape index, escapes
-//   control:                                                          [B1]
-//                                                                     [B2]
-//            chunk CRC, plan, publish aggregate, first look-back read [B3]
-//            finish look-back, publish prefix, header, table entry    [B4]
+// look-back of record offsets, headers, table entries) and folds the chunk
+// CRC from the data waves' lane values.  The per-phase schedule is given
+// above k_encode.
 
 constexpr int kModeList = 0, kModeAll = 1, kModeStep = 2;
 constexpr uint64_t kFlagAgg = 1, kFlagIncl = 2;
@@ -596,7 +589,8 @@ struct EncShared {
   uint32_t dirty_w[kWaves];  // per-wave "differs from prev"
   uint32_t esc_w[kWaves];    // escapes per wave
   uint32_t crc;               // the chunk's CRC
-  uint32_t first, next;      // tickets
+  uint32_t first, next;      // tickets before the loop
+  uint32_t ticket[2];        // in the loop, by iteration parity
   uint32_t off_lo, off_hi;   // record offset
   alignas(16) uint4 cand[9];    // plan candidates: size, base | k << 8 | mode << 16, n_esc
   alignas(16) uint32_t H[256];  // histogram
@@ -954,6 +948,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
                c < g.n_chunks ? chunk_len(g, c) : 0u, l0, d);
     if (c < g.n_chunks) hist_add(d, (l0.lane & 31u) * 4u);  // copies zeroed before the barrier
   }
+  __syncthreads();  // the first chunk's histogram is complete (the loop has no B1)
 
   // the chunk whose record is still to be written (uniform), and its
   // sign/mantissa bytes (data waves)
@@ -966,7 +961,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
 #pragma unroll
   for (int h = 0; h < kRows; ++h) smp[h] = make_uint2(0, 0);
 
-  while (item < n_items || pend) {
+  for (uint32_t it = 0; item < n_items || pend; ++it) {
     const bool cur = item < n_items;
     const Lane l = lane_fresh(l0);
     const uint32_t copy4 = (l.lane & 31u) * 4u;
@@ -1019,14 +1014,19 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       if (is_ctl && pend)  // ---- control: X_{i-1}'s offset, header and table entry
         ctl_emit(a, pr, win, n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
     }
-    __syncthreads();  // B1: CRC lane values, X_{i-1}'s offset
+    // B1 (step only: the control emits X_{i-1} after B0).  Otherwise nothing
+    // here needs it: the histogram being reduced below was completed before
+    // the last B4, the lane values and X_{i-1}'s offset are read after B2,
+    // and the ticket slot alternates so the control cannot overwrite one
+    // still unread.
+    if (HAS_PREV) __syncthreads();
 
     // ---- phase 2
     uint32_t crc = 0;
     if (is_ctl) {
       if (cur) {
         if (!need_crc) crc = bad_index ? 0u : ld_const(a.crc_in + c);
-        if (l.lane == 0) sh.next = ticket;
+        if (l.lane == 0) sh.ticket[it & 1] = ticket;
       }
     } else if (dirty) {
       // reduce the copies: wave w sums bins 32w..32w+31 (its own 2 KiB of
@@ -1263,7 +1263,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       for (int h = 0; h < kRows; ++h) d[h] = dn[h];
     }
     item = next;
-    if (cur) next = uniform(sh.next);
+    if (cur) next = uniform(sh.ticket[it & 1]);
   }
 }
 
