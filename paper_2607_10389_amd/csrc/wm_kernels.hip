@@ -896,10 +896,11 @@ __device__ __forceinline__ void ctl_emit(const EncArgs &a, const RecFields &r, c
 // control wave resolved by look-back: for a full ship at the end of
 // iteration i-1, right after X_{i-1}'s size was published (its predecessors
 // run alongside and have published theirs by then); for a step, whose clean
-// chunks finish early and let workgroups drift apart, in phase 1 of
-// iteration i, issued before B0 and finished after it.
-//   phase 1 (..B1): data: prefetch X_{i+1}, lane CRC values of X_i;
-//                   control: next ticket
+// chunks finish early and let workgroups drift apart, in phases 1-2 of
+// iteration i, issued before B0 and finished after it (nothing waits for it
+// before B2).
+//   phase 1:        data: prefetch X_{i+1}, lane CRC values of X_i (step:
+//                   diff flags, then B0); control: next ticket
 //   phase 2 (..B2): data: reduce X_i's histogram (accumulated in phase 4 of
 //                   iteration i-1, or before the loop for the first chunk)
 //   phase 3 (..B3): data: write X_{i-1} (staging + sign/mantissa bytes),
@@ -1014,12 +1015,10 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       if (is_ctl && pend)  // ---- control: X_{i-1}'s offset, header and table entry
         ctl_emit(a, pr, win, n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
     }
-    // B1 (step only: the control emits X_{i-1} after B0).  Otherwise nothing
-    // here needs it: the histogram being reduced below was completed before
-    // the last B4, the lane values and X_{i-1}'s offset are read after B2,
-    // and the ticket slot alternates so the control cannot overwrite one
-    // still unread.
-    if (HAS_PREV) __syncthreads();
+    // No barrier here: the histogram reduced below was completed before the
+    // last B4, the lane values and X_{i-1}'s offset (step: emitted after B0,
+    // possibly still being resolved) are read after B2, and the ticket slot
+    // alternates so the control cannot overwrite one still unread.
 
     // ---- phase 2
     uint32_t crc = 0;
