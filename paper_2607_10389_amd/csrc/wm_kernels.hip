@@ -1963,9 +1963,16 @@ __global__ __launch_bounds__(256) void k_commit(uint8_t *__restrict__ live, Chun
     const uint8_t *src = staging + (uint64_t)r * kChunk;
     uint8_t *dst = live + (uint64_t)c * kChunk;
     if (len == kChunk) {
-#pragma unroll 4
-      for (uint32_t off = threadIdx.x * 16u; off < kChunk; off += 4096u)
-        *reinterpret_cast<uint4 *>(dst + off) = *reinterpret_cast<const uint4 *>(src + off);
+      // all sixteen 16-byte pieces of the thread in flight at once, streamed
+      // past the caches (neither side is read again here)
+      v4u v[kChunk / 4096u];
+#pragma unroll
+      for (uint32_t i = 0; i < kChunk / 4096u; ++i)
+        v[i] = __builtin_nontemporal_load(
+            reinterpret_cast<const v4u *>(src + threadIdx.x * 16u + i * 4096u));
+#pragma unroll
+      for (uint32_t i = 0; i < kChunk / 4096u; ++i)
+        __builtin_nontemporal_store(v[i], reinterpret_cast<v4u *>(dst + threadIdx.x * 16u + i * 4096u));
     } else {
       for (uint32_t off = threadIdx.x; off < len; off += 256u) dst[off] = src[off];
     }
@@ -2127,7 +2134,7 @@ int launch_decode(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
 int launch_commit(void *live, const ChunkGeom &g, const void *staging, const void *payload,
                   const uint32_t *verdict, int n_cu, void *stream) {
   if (!g.n_chunks) return 0;
-  uint32_t grid = min((uint32_t)n_cu * 4u, g.n_chunks);
+  uint32_t grid = min((uint32_t)n_cu * 8u, g.n_chunks);
   hipLaunchKernelGGL(k_commit, dim3(grid), dim3(256), 0, S(stream),
                      static_cast<uint8_t *>(live), g, static_cast<const uint8_t *>(staging),
                      static_cast<const uint8_t *>(payload), verdict);
