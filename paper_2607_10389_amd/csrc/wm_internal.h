@@ -33,7 +33,6 @@ struct CrcTables {
   uint32_t tree[kTree][4][256];  // F^(16 << l): lane-tree levels
   uint32_t wave_step[4][256];    // F^kSub: one wave's share of a chunk
   uint32_t byte1[256];           // one-byte step of the table method
-  uint32_t wave_mat[kWaves][32]; // F^(kSub*(kWaves-1-w) + 4), columns
   uint32_t pow2[48][32];         // F^(2^i) bytes, columns
   uint32_t k_full;               // F^kChunk(~0) ^ ~0
   uint32_t pad_[3];

@@ -46,8 +46,6 @@ constexpr uint32_t kLdsMisc = kLdsCrcEnd;           // 4 KiB of small scratch
 constexpr uint32_t kLdsMiscBytes = 4096;
 constexpr uint32_t kLdsBase = kLdsMisc + kLdsMiscBytes;  // 126976
 
-// checksum-kernel scratch (u32 index into kLdsMisc)
-constexpr uint32_t M_PART = 0;  // [kWaves] wave CRC partials
 
 // Dynamic LDS of the kernels below.  They declare no static LDS (checked at
 // set-up, set_kernel_attributes), so it begins at LDS address 0: addresses
@@ -100,9 +98,6 @@ __device__ __forceinline__ uint32_t ld_const(const uint32_t *p) {
 
 __device__ __forceinline__ uint32_t lds_u32(uint32_t off) {
   return *reinterpret_cast<const uint32_t *>(lds_at(off));
-}
-__device__ __forceinline__ uint32_t *misc() {
-  return reinterpret_cast<uint32_t *>(lds_at(kLdsMisc));
 }
 __device__ __forceinline__ uint32_t uniform(uint32_t v) {
   return __builtin_amdgcn_readfirstlane(v);
@@ -352,27 +347,6 @@ __device__ __forceinline__ uint32_t lane_value_load(const uint4 (&d)[kRows], con
   return lane_merge(v0, v1, v2, v3);
 }
 
-// Wave-level CRC value Q of the wave's 8 rows (valid in lane 63).
-__device__ __forceinline__ uint32_t wave_q(const uint4 (&d)[kRows],
-                                           const GLane &gl) {
-  return lane_tree(lane_value(d, gl));
-}
-
-// A uniform pointer the compiler cannot see through: loads through it stay
-// where they are used instead of being hoisted out of a chunk loop, where 32
-// matrix columns would otherwise occupy scalar registers for the whole loop.
-template <typename P>
-__device__ __forceinline__ P *opaque(P *p) {
-  asm volatile("" : "+s"(p));
-  return p;
-}
-
-// The wave's share of the chunk's raw CRC: its value Q (lane 63) shifted
-// past the rows of the later waves, computed on the scalar unit.
-__device__ __forceinline__ uint32_t wave_part(const CrcTables &T, uint32_t wave, uint32_t q) {
-  return mat_apply(opaque(T.wave_mat[wave]), __builtin_amdgcn_readlane(q, 63));
-}
-
 // Chunk CRC from the raw (zero-init, padded) value of the whole chunk.
 __device__ __forceinline__ uint32_t finish_crc(uint32_t raw, uint32_t len,
                                                const ChunkGeom &g, const CrcTables &T) {
@@ -381,36 +355,52 @@ __device__ __forceinline__ uint32_t finish_crc(uint32_t raw, uint32_t len,
 
 // -------------------------------------------------------------- checksum --
 
-__global__ __launch_bounds__(kThreads) void k_checksum(
+// Lane CRC values of a chunk, double-buffered by chunk step (low region).
+__device__ __forceinline__ uint32_t *chk_u(uint32_t b) {
+  return reinterpret_cast<uint32_t *>(lds_at(kLdsLow + b * (kThreads * 4u)));
+}
+
+// Chunk CRCs: the eight data waves take chunk i's lane values while chunk
+// i+1 loads; the ninth wave folds chunk i-1's values into its CRC (the
+// Horner step over waves, the lane tree, the common F^4).
+__global__ __launch_bounds__(kThreads + 64) void k_checksum(
     const uint8_t *__restrict__ data, ChunkGeom g,
     uint32_t *__restrict__ crc_out) {
   load_crc_tables(g.crc_kind);
   __syncthreads();
   const CrcTables &T = g_tables[g.crc_kind];
+  const bool is_fold = threadIdx.x >= (uint32_t)kThreads;
   const GLane gl = glane_make();
-  const Lane l = lane_info();
-  uint32_t c = blockIdx.x;
+  const Lane l0 = lane_info();
+  const uint32_t G = gridDim.x;
+  const uint32_t my_n = blockIdx.x < g.n_chunks ? (g.n_chunks - 1 - blockIdx.x) / G + 1 : 0;
   uint4 d[kRows];
-  load_chunk(data + (uint64_t)c * kChunk, c < g.n_chunks ? chunk_len(g, c) : 0u, l, d);
-  while (c < g.n_chunks) {
-    const uint32_t cn = c + gridDim.x;
-    uint4 dn[kRows];
-    load_chunk(data + (uint64_t)(cn < g.n_chunks ? cn : c) * kChunk,
-               cn < g.n_chunks ? chunk_len(g, cn) : 0u, l, dn);
-    const uint32_t q = wave_q(d, gl);
-    const uint32_t part = wave_part(T, l.wave, q);
-    if (l.lane == 0) misc()[M_PART + l.wave] = part;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      uint32_t raw = 0;
+  if (!is_fold)
+    load_chunk(data + (uint64_t)blockIdx.x * kChunk, my_n ? chunk_len(g, blockIdx.x) : 0u, l0, d);
+  for (uint32_t i = 0; i <= my_n; ++i) {
+    const Lane l = lane_fresh(l0);
+    if (!is_fold) {
+      if (i < my_n) {
+        const uint32_t cn = blockIdx.x + (i + 1) * G;
+        const bool nv = i + 1 < my_n;
+        uint4 dn[kRows];
+        chk_u(i & 1)[l.wave * 64u + l.lane] =
+            lane_value_load(d, gl, data + (uint64_t)(nv ? cn : 0u) * kChunk,
+                            nv ? chunk_len(g, cn) : 0u, l, dn);
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) raw ^= misc()[M_PART + w];
-      crc_out[c] = finish_crc(raw, chunk_len(g, c), g, T);
+        for (int h = 0; h < kRows; ++h) d[h] = dn[h];
+      }
+    } else if (i >= 1) {
+      const uint32_t c = blockIdx.x + (i - 1) * G;
+      const uint32_t *u = chk_u((i - 1) & 1);
+      uint32_t acc = u[l.lane];
+#pragma unroll
+      for (int w = 1; w < kWaves; ++w) acc = tab4x(kLdsWaveStep, acc, u[w * 64 + l.lane]);
+      const uint32_t q = uniform(__builtin_amdgcn_readlane(lane_tree(acc), 63));
+      const uint32_t crc = finish_crc(tab4(kLdsF4, q), chunk_len(g, c), g, T);
+      if (l.lane == 0) crc_out[c] = crc;
     }
     __syncthreads();
-#pragma unroll
-    for (int h = 0; h < kRows; ++h) d[h] = dn[h];
-    c = cn;
   }
 }
 
@@ -2020,7 +2010,7 @@ int launch_checksum(const void *data, const ChunkGeom &g, uint32_t *crc_out,
                     uint32_t *global_crc, int n_cu, void *stream) {
   if (g.n_chunks) {
     uint32_t grid = min((uint32_t)n_cu, g.n_chunks);
-    hipLaunchKernelGGL(k_checksum, dim3(grid), dim3(kThreads), kLdsBase, S(stream),
+    hipLaunchKernelGGL(k_checksum, dim3(grid), dim3(kThreads + 64), kLdsBase, S(stream),
                        static_cast<const uint8_t *>(data), g, crc_out);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return (int)e;

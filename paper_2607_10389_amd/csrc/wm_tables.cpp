@@ -103,10 +103,6 @@ void build_crc_tables(uint32_t poly, CrcTables *t) {
   byte_tables(byte_shift(poly, kSub), t->wave_step);
   Mat one = byte_shift(poly, 1);
   for (uint32_t b = 0; b < 256; ++b) t->byte1[b] = apply(one, b);
-  for (int w = 0; w < kWaves; ++w) {
-    Mat m = byte_shift(poly, (int64_t)kSub * (kWaves - 1 - w) + 4);
-    std::memcpy(t->wave_mat[w], m.c, sizeof(m.c));
-  }
   Mat p = byte_shift(poly, 1);
   for (int i = 0; i < 48; ++i) {
     std::memcpy(t->pow2[i], p.c, sizeof(p.c));
