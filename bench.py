@@ -40,6 +40,8 @@ def parse():
                     help="skip the CPU oracle baseline")
     ap.add_argument("--no-step", action="store_true",
                     help="skip the active-generation step measurement")
+    ap.add_argument("--no-manifest", action="store_true",
+                    help="skip the 450-leaf flatten/rehydrate measurement")
     ap.add_argument("--crc", type=int, default=0, help="0 zlib CRC-32, 1 CRC-32C")
     ap.add_argument("--counter-pass", action="store_true",
                     help="one full-ship encode and decode plus a 1 GiB device copy, "
@@ -73,13 +75,14 @@ def measured_traffic(kernel):
 
 
 def counter_pass(args):
-    """Exactly one launch of each hot kernel on the production cache, then a
-    plain device-to-device copy of 1 GiB (the calibration for FETCH_SIZE and
-    WRITE_SIZE)."""
+    """Exactly one launch of each hot kernel on the production cache, a plain
+    device-to-device copy of 1 GiB (the calibration for FETCH_SIZE and
+    WRITE_SIZE), then one flatten and one rehydrate of the 450-leaf
+    manifest."""
     import torch
 
     import wm_inputs
-    from paper_2607_10389_amd import Mover, WM_OK
+    from paper_2607_10389_amd import Mover, WM_OK, _wm
 
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
@@ -92,6 +95,11 @@ def counter_pass(args):
     m.decode()
     ok = m.commit(None, scatter=False) == WM_OK
     dst.copy_(src)
+    leaves = wm_inputs.make_manifest(wm_inputs.PRODUCTION, dev, cache=state)
+    flat = torch.empty(_wm.flat_bytes(leaves), dtype=torch.uint8, device=dev)
+    ws = torch.empty(_wm.manifest_ws_bytes(len(leaves)), dtype=torch.uint8, device=dev)
+    _wm.flatten(leaves, flat, ws)
+    _wm.rehydrate(flat, leaves, ws)
     torch.cuda.synchronize()
     print(json.dumps({"counter_pass": "done", "verified": ok, "copy_bytes": src.numel(),
                       "payload_bytes": int(m.payload_bytes.item()),
@@ -278,6 +286,12 @@ def main():
         },
     }
 
+    def one(name, fn, moved):
+        t = timed_events(torch, fn, 10)
+        return {"ms": round(t, 4), "bytes": moved,
+                "GBps": round(moved / (t * 1e-3) / 1e9, 1),
+                "frac_hbm_peak": round(moved / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+
     if not args.no_step:
         prev = state
         cur, ids = wm_inputs.production_step(prev)
@@ -323,12 +337,6 @@ def main():
             raise RuntimeError("separate calls and the fused step disagree")
         mu.decode()
 
-        def one(name, fn, moved):
-            t = timed_events(torch, fn, 10)
-            return {"ms": round(t, 4), "bytes": moved,
-                    "GBps": round(moved / (t * 1e-3) / 1e9, 1),
-                    "frac_hbm_peak": round(moved / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
-
         out["separate_calls"] = {
             "wm_checksum_chunks": one("checksum", lambda: mu.checksum(cur), nbytes),
             "wm_diff_dirty": one("diff", lambda: mu.diff(cur, prev), 2 * nbytes),
@@ -341,6 +349,30 @@ def main():
         dst = torch.empty_like(cur)
         out["copy_ceiling"] = one("copy", lambda: dst.copy_(cur), 2 * nbytes)
         del cur, live, ms, mu, dst
+
+    if not args.no_manifest:
+        # the step on either side of the move: gather the session's leaves
+        # into the flat buffer, scatter a flat buffer back into the leaves
+        leaves = wm_inputs.make_manifest(spec, dev, cache=state)
+        total = _wm.flat_bytes(leaves)
+        flat = torch.empty(total, dtype=torch.uint8, device=dev)
+        ws = torch.empty(_wm.manifest_ws_bytes(len(leaves)), dtype=torch.uint8, device=dev)
+        back = [torch.empty_like(x) for x in leaves]
+        t_leaves, t_back = _wm.LeafTable(leaves), _wm.LeafTable(back)
+        _wm.flatten(t_leaves, flat, ws)
+        _wm.rehydrate(flat, t_back, ws)
+        torch.cuda.synchronize()
+        if not all(torch.equal(x, y) for x, y in zip(back, leaves)):
+            raise RuntimeError("rehydrated leaves differ from the flattened ones")
+        out["manifest"] = {
+            "workload": f"{len(leaves)} leaves (392 bf16 head-group slabs of the "
+                        "production cache, 28 fp32 [7296] tensors, 30 scalar flags)",
+            "flat_bytes": total,
+            "wm_flatten": one("flatten", lambda: _wm.flatten(t_leaves, flat, ws), 2 * total),
+            "wm_rehydrate": one("rehydrate", lambda: _wm.rehydrate(flat, t_back, ws),
+                                2 * total),
+        }
+        del leaves, flat, back
 
     if not args.no_cpu:
         host = state.view(-1).view(torch.uint8).cpu().numpy()

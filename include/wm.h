@@ -5,9 +5,9 @@
  * KV cache) resident in device memory, the mover's data path from
  * arXiv 2607.10389 ("Stateful Worlds, Stateless Elasticity"):
  *
- *   source side       wm_checksum_chunks -> wm_diff_dirty -> wm_encode
- *                     (or the single-pass wm_encode_step)
- *   destination side  wm_decode_verify -> wm_commit_or_abort
+ *   source side       [wm_flatten] -> wm_checksum_chunks -> wm_diff_dirty
+ *                     -> wm_encode (or the single-pass wm_encode_step)
+ *   destination side  wm_decode_verify -> wm_commit_or_abort -> [wm_rehydrate]
  *
  * under the paper's contract: the destination is bit-identical to the source
  * or nothing is installed (§1; §4 "Sufficiency": commit only on a
@@ -182,6 +182,51 @@ wm_status wm_commit_or_abort(void *live, uint64_t nbytes, const wm_params *p,
                              const void *staging, const void *payload,
                              const uint32_t *verdict, uint32_t mode,
                              void *stream);
+
+/* ---- manifest: flatten and rehydrate --------------------------------------
+ * The mover works on one flat buffer; a session's state is a manifest of
+ * separate device tensors (the paper's suspend manifest: 450 leaves, the 420
+ * movable tensors plus scalar control flags; §5 "Implementation").  The
+ * canonical path flattens the live state, moves and verifies it, and
+ * rehydrates it (§4 "Sufficiency").
+ *
+ * Flat layout: leaf i occupies flat[off_i, off_i + bytes_i) with off_0 = 0
+ * and off_{i+1} = off_i + round_up(bytes_i, 16); flatten writes zeros into
+ * the gaps, so the flat bytes are a function of the leaves alone. */
+typedef struct {
+  const void *ptr; /* device address, 16-byte aligned (any value if bytes is 0) */
+  uint64_t bytes;  /* data bytes of the leaf */
+} wm_leaf;
+
+/* Flat size of a manifest (sum of the leaf sizes rounded up to 16); 0 for a
+ * NULL table with n_leaves > 0 or a sum beyond 64 bits.  leaves: host array. */
+uint64_t wm_flat_bytes(const wm_leaf *leaves, uint32_t n_leaves);
+
+/* Workspace bytes a flatten or rehydrate of n_leaves leaves needs (the
+ * library's device copy of the table: 32 bytes per leaf). */
+uint64_t wm_manifest_ws_bytes(uint32_t n_leaves);
+
+/* Gather the leaves into flat (flatten).  Enqueues on stream a copy of the
+ * table into ws and one kernel; returns without waiting.
+ *   leaves   : host array of n_leaves entries (read before returning)
+ *   flat     : flat_cap bytes, 16-byte aligned, flat_cap >= wm_flat_bytes()
+ *              (bytes past wm_flat_bytes() are not written)
+ *   ws       : ws_bytes >= wm_manifest_ws_bytes(n_leaves), 16-byte aligned;
+ *              in use until the kernel has run
+ * Leaves and flat must not overlap.  A manifest of 0 flat bytes returns
+ * WM_OK without device work.
+ * Errors: WM_ERR_INVALID_ARG (NULL or misaligned pointer, sizes summing past
+ *         64 bits), WM_ERR_CAPACITY, WM_ERR_WORKSPACE, WM_ERR_HIP. */
+wm_status wm_flatten(const wm_leaf *leaves, uint32_t n_leaves, void *flat,
+                     uint64_t flat_cap, void *ws, uint64_t ws_bytes,
+                     void *stream);
+
+/* Scatter flat back into the leaves (rehydrate): the exact inverse of
+ * wm_flatten for the same table (gap bytes of flat are ignored).  Arguments
+ * and errors as wm_flatten. */
+wm_status wm_rehydrate(const void *flat, uint64_t flat_cap,
+                       const wm_leaf *leaves, uint32_t n_leaves, void *ws,
+                       uint64_t ws_bytes, void *stream);
 
 #ifdef __cplusplus
 }

@@ -75,6 +75,14 @@ def lib():
         L.orc_commit.argtypes = [u8p, ctypes.c_uint64, ctypes.c_uint32, u8p,
                                  u8p, ctypes.c_uint32]
         L.orc_commit.restype = ctypes.c_int
+        L.orc_flat_layout.argtypes = [u64p, ctypes.c_uint32, u64p]
+        L.orc_flat_layout.restype = ctypes.c_uint64
+        L.orc_flatten.argtypes = [ctypes.POINTER(u8p), u64p, ctypes.c_uint32,
+                                  u8p]
+        L.orc_flatten.restype = None
+        L.orc_rehydrate.argtypes = [u8p, ctypes.POINTER(u8p), u64p,
+                                    ctypes.c_uint32]
+        L.orc_rehydrate.restype = None
         _lib = L
     return _lib
 
@@ -182,3 +190,45 @@ def commit(live: np.ndarray, chunk: int, staging, payload, verdict: int) -> int:
     s, p = _bytes(staging), _bytes(payload)
     return int(lib().orc_commit(_p8(live), live.size, chunk, _p8(s), _p8(p),
                                 verdict))
+
+
+def _u64p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64))
+
+
+def flat_layout(sizes) -> tuple[np.ndarray, int]:
+    """Offsets of the leaves in the flat buffer and the flat size."""
+    b = np.ascontiguousarray(sizes, dtype=np.uint64)
+    off = np.zeros(max(b.size, 1), np.uint64)
+    total = lib().orc_flat_layout(_u64p(b), b.size, _u64p(off))
+    return off[: b.size], int(total)
+
+
+def _ptr_table(arrays):
+    u8p = ctypes.POINTER(ctypes.c_uint8)
+    t = (u8p * max(len(arrays), 1))()
+    for i, a in enumerate(arrays):
+        t[i] = _p8(a)
+    return t
+
+
+def flatten(leaves) -> np.ndarray:
+    """Flat bytes of a manifest given as a list of arrays (any dtype)."""
+    bs = [_bytes(x) for x in leaves]
+    sizes = np.array([b.size for b in bs], np.uint64)
+    _, total = flat_layout(sizes)
+    flat = np.full(max(total, 1), 0xA5, np.uint8)  # every byte gets written
+    lib().orc_flatten(_ptr_table(bs), _u64p(sizes), len(bs), _p8(flat))
+    return flat[:total]
+
+
+def rehydrate(flat, sizes) -> list[np.ndarray]:
+    """The leaves (uint8 arrays of the given sizes) held by a flat buffer."""
+    f = _bytes(flat)
+    sz = np.ascontiguousarray(sizes, dtype=np.uint64)
+    _, total = flat_layout(sz)
+    if f.size < total:
+        raise ValueError("flat buffer smaller than the manifest")
+    out = [np.zeros(max(int(s), 1), np.uint8) for s in sz]
+    lib().orc_rehydrate(_p8(f), _ptr_table(out), _u64p(sz), sz.size)
+    return [o[: int(s)] for o, s in zip(out, sz)]

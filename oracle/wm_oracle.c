@@ -640,3 +640,35 @@ int orc_commit(uint8_t *live, uint64_t nbytes, uint32_t chunk_bytes,
   }
   return 0;
 }
+
+/* ---- manifest flatten / rehydrate (§4 "Sufficiency", §5 "Implementation") */
+
+uint64_t orc_flat_layout(const uint64_t *bytes, uint32_t n, uint64_t *off) {
+  uint64_t pos = 0;
+  for (uint32_t i = 0; i < n; i++) {
+    off[i] = pos;
+    pos += bytes[i];
+    while (pos % 16 != 0) pos++;
+  }
+  return pos;
+}
+
+void orc_flatten(const uint8_t *const *leaves, const uint64_t *bytes,
+                 uint32_t n, uint8_t *flat) {
+  uint64_t pos = 0;
+  for (uint32_t i = 0; i < n; i++) {
+    if (bytes[i]) memcpy(flat + pos, leaves[i], bytes[i]);
+    pos += bytes[i];
+    while (pos % 16 != 0) flat[pos++] = 0;
+  }
+}
+
+void orc_rehydrate(const uint8_t *flat, uint8_t *const *leaves,
+                   const uint64_t *bytes, uint32_t n) {
+  uint64_t pos = 0;
+  for (uint32_t i = 0; i < n; i++) {
+    if (bytes[i]) memcpy(leaves[i], flat + pos, bytes[i]);
+    pos += bytes[i];
+    while (pos % 16 != 0) pos++;
+  }
+}

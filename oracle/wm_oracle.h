@@ -23,6 +23,12 @@
  *     (§6.4 codec paragraph).  The paper fixes no codec format; the byte
  *     layout implemented here is this project's payload format v1.
  *   - Shadow slot, verify, then commit or roll back (Table 1, session API).
+ *   - Flatten and rehydrate: the mover works on one flat buffer made from the
+ *     session's manifest of leaves, flattened before the move and rehydrated
+ *     after it (§4 "Sufficiency"; §5 "Implementation": 450 leaves).  The
+ *     paper fixes no flat layout; this project's layout places leaf i at the
+ *     sum of the earlier leaves' sizes, each rounded up to 16 bytes, with
+ *     zero bytes in the gaps.
  *
  * Functions return plain integers; no function allocates memory visible to
  * the caller.  Buffers are host memory owned by the caller.
@@ -95,6 +101,19 @@ uint32_t orc_decode_verify(int kind, const uint8_t *payload, uint64_t cap,
 int orc_commit(uint8_t *live, uint64_t nbytes, uint32_t chunk_bytes,
                const uint8_t *staging, const uint8_t *payload,
                uint32_t verdict);
+
+/* Flat layout of a manifest of n leaves of bytes[i] bytes: writes each
+ * leaf's offset into off (n entries) and returns the flat size. */
+uint64_t orc_flat_layout(const uint64_t *bytes, uint32_t n, uint64_t *off);
+
+/* Flatten: copy leaf i to flat + off_i and zero the gap bytes after it.
+ * flat holds orc_flat_layout()'s size. */
+void orc_flatten(const uint8_t *const *leaves, const uint64_t *bytes,
+                 uint32_t n, uint8_t *flat);
+
+/* Rehydrate: copy flat + off_i back into leaf i (gap bytes are not read). */
+void orc_rehydrate(const uint8_t *flat, uint8_t *const *leaves,
+                   const uint64_t *bytes, uint32_t n);
 
 #ifdef __cplusplus
 }

@@ -12,7 +12,7 @@ from . import _wm
 from ._wm import (  # noqa: F401
     CHUNK, WM_CRC32C, WM_CRC32_ZLIB, WM_COMMIT_NONE, WM_COMMIT_SCATTER,
     WM_OK, WM_VERIFY_FAILED, WmError, checksum_chunks, commit_or_abort,
-    decode_verify, diff_dirty, encode, encode_step, params, payload_bound,
-    workspace_bytes,
+    decode_verify, diff_dirty, encode, encode_step, flat_bytes, flatten,
+    manifest_ws_bytes, params, payload_bound, rehydrate, workspace_bytes,
 )
 from .mover import Mover  # noqa: F401

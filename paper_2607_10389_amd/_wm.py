@@ -39,7 +39,8 @@ CHUNK = 65536
 EXPORTS = (
     "wm_status_str", "wm_init", "wm_workspace_bytes", "wm_payload_bound",
     "wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_encode_step",
-    "wm_decode_verify", "wm_commit_or_abort",
+    "wm_decode_verify", "wm_commit_or_abort", "wm_flat_bytes",
+    "wm_manifest_ws_bytes", "wm_flatten", "wm_rehydrate",
 )
 
 
@@ -54,6 +55,10 @@ class Params(ctypes.Structure):
                 ("codec", ctypes.c_uint32), ("flags", ctypes.c_uint32)]
 
 
+class Leaf(ctypes.Structure):
+    _fields_ = [("ptr", ctypes.c_void_p), ("bytes", ctypes.c_uint64)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(
@@ -62,6 +67,7 @@ def _load():
     lib = ctypes.CDLL(LIB_PATH)
     vp, u64, u32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32
     pp = ctypes.POINTER(Params)
+    lp = ctypes.POINTER(Leaf)
     sig = {
         "wm_status_str": ([ctypes.c_int32], ctypes.c_char_p),
         "wm_init": ([ctypes.c_int], ctypes.c_int32),
@@ -77,6 +83,10 @@ def _load():
                              ctypes.c_int32),
         "wm_commit_or_abort": ([vp, u64, pp, vp, vp, vp, u32, vp],
                                ctypes.c_int32),
+        "wm_flat_bytes": ([lp, u32], u64),
+        "wm_manifest_ws_bytes": ([u32], u64),
+        "wm_flatten": ([lp, u32, vp, u64, vp, u64, vp], ctypes.c_int32),
+        "wm_rehydrate": ([vp, u64, lp, u32, vp, u64, vp], ctypes.c_int32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -106,7 +116,7 @@ def _p(t):
 
 
 def _nbytes(t) -> int:
-    return t.numel() * t.element_size()
+    return 0 if t is None else t.numel() * t.element_size()
 
 
 def _stream(stream=None):
@@ -185,3 +195,44 @@ def commit_or_abort(live, nbytes, p, staging, payload, verdict, mode,
                                          _p(staging), _p(payload), _p(verdict),
                                          mode, _stream(stream)),
                   "wm_commit_or_abort")
+
+
+class LeafTable:
+    """Host table of (device pointer, byte size) for a list of contiguous
+    device tensors; build it once to call flatten/rehydrate repeatedly on the
+    same leaves."""
+
+    def __init__(self, leaves):
+        self.n = len(leaves)
+        self.t = (Leaf * max(self.n, 1))()
+        for i, x in enumerate(leaves):
+            if not x.is_cuda or not x.is_contiguous():
+                raise ValueError("manifest leaves are contiguous device tensors")
+            self.t[i].ptr = x.data_ptr()
+            self.t[i].bytes = _nbytes(x)
+
+
+def _table(leaves) -> LeafTable:
+    return leaves if isinstance(leaves, LeafTable) else LeafTable(leaves)
+
+
+def flat_bytes(leaves) -> int:
+    tab = _table(leaves)
+    return int(LIB.wm_flat_bytes(tab.t, tab.n))
+
+
+def manifest_ws_bytes(n_leaves: int) -> int:
+    return int(LIB.wm_manifest_ws_bytes(n_leaves))
+
+
+def flatten(leaves, flat, ws, stream=None):
+    tab = _table(leaves)
+    return _check(LIB.wm_flatten(tab.t, tab.n, _p(flat), _nbytes(flat), _p(ws),
+                                 _nbytes(ws), _stream(stream)), "wm_flatten")
+
+
+def rehydrate(flat, leaves, ws, stream=None):
+    tab = _table(leaves)
+    return _check(LIB.wm_rehydrate(_p(flat), _nbytes(flat), tab.t, tab.n,
+                                   _p(ws), _nbytes(ws), _stream(stream)),
+                  "wm_rehydrate")

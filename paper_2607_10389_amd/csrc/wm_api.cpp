@@ -8,6 +8,7 @@
 #include <cstdint>
 #include <map>
 #include <mutex>
+#include <vector>
 
 #include "wm.h"
 #include "wm_internal.h"
@@ -253,6 +254,67 @@ wm_status wm_commit_or_abort(void *live, uint64_t nbytes, const wm_params *p, co
     return WM_ERR_HIP;
   if (hipStreamSynchronize(st) != hipSuccess) return WM_ERR_HIP;
   return v == 0 ? WM_OK : WM_VERIFY_FAILED;
+}
+
+uint64_t wm_flat_bytes(const wm_leaf *leaves, uint32_t n_leaves) {
+  if (n_leaves && !leaves) return 0;
+  uint64_t total = 0;
+  for (uint32_t i = 0; i < n_leaves; ++i) {
+    if (leaves[i].bytes > UINT64_MAX - 15u - total) return 0;
+    total += (leaves[i].bytes + 15u) & ~15ull;
+  }
+  return total;
+}
+
+uint64_t wm_manifest_ws_bytes(uint32_t n_leaves) { return 32ull * n_leaves; }
+
+}  // extern "C"
+
+namespace {
+
+// Checks the caller's table, writes the device copy (with offsets) into the
+// workspace and launches the copy.
+wm_status manifest_call(bool gather, const wm_leaf *leaves, uint32_t n_leaves, void *flat,
+                        uint64_t flat_cap, void *ws, uint64_t ws_bytes, void *stream) {
+  if (n_leaves && !leaves) return WM_ERR_INVALID_ARG;
+  std::vector<ManifestLeaf> t(n_leaves);
+  uint64_t total = 0;
+  for (uint32_t i = 0; i < n_leaves; ++i) {
+    const uint64_t b = leaves[i].bytes;
+    if (b && (!leaves[i].ptr || !aligned16(leaves[i].ptr))) return WM_ERR_INVALID_ARG;
+    if (b > UINT64_MAX - 15u - total) return WM_ERR_INVALID_ARG;
+    t[i] = ManifestLeaf{reinterpret_cast<uint64_t>(leaves[i].ptr), total, b, 0};
+    total += (b + 15u) & ~15ull;
+  }
+  if (total && (!flat || !aligned16(flat))) return WM_ERR_INVALID_ARG;
+  if (flat_cap < total) return WM_ERR_CAPACITY;
+  if (n_leaves && (!ws || !aligned16(ws) || ws_bytes < 32ull * n_leaves)) return WM_ERR_WORKSPACE;
+  if (!total) return WM_OK;  // nothing to copy
+  int n_cu = 0;
+  wm_status s = ensure_device(&n_cu);
+  if (s != WM_OK) return s;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  // an asynchronous copy from pageable host memory has read its source when
+  // it returns, so the local table may go out of scope
+  if (hipMemcpyAsync(ws, t.data(), 32ull * n_leaves, hipMemcpyHostToDevice, st) != hipSuccess)
+    return WM_ERR_HIP;
+  return hip_status(launch_manifest(gather, flat, total, static_cast<const ManifestLeaf *>(ws),
+                                    n_leaves, n_cu, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+wm_status wm_flatten(const wm_leaf *leaves, uint32_t n_leaves, void *flat, uint64_t flat_cap,
+                     void *ws, uint64_t ws_bytes, void *stream) {
+  return manifest_call(true, leaves, n_leaves, flat, flat_cap, ws, ws_bytes, stream);
+}
+
+wm_status wm_rehydrate(const void *flat, uint64_t flat_cap, const wm_leaf *leaves,
+                       uint32_t n_leaves, void *ws, uint64_t ws_bytes, void *stream) {
+  return manifest_call(false, leaves, n_leaves, const_cast<void *>(flat), flat_cap, ws, ws_bytes,
+                       stream);
 }
 
 }  // extern "C"

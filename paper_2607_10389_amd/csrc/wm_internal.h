@@ -105,6 +105,17 @@ int launch_decode(const void *payload, uint64_t payload_cap,
 int launch_commit(void *live, const ChunkGeom &g, const void *staging,
                   const void *payload, const uint32_t *verdict, int n_cu,
                   void *stream);
+// One leaf of a manifest as the device sees it (the library's copy of the
+// caller's table, with offsets): 32 bytes.
+struct ManifestLeaf {
+  uint64_t ptr;    // device address, 16-byte aligned
+  uint64_t off;    // flat offset, multiple of 16, ascending
+  uint64_t bytes;  // data bytes
+  uint64_t pad_;
+};
+// gather: leaves -> flat (flatten); else flat -> leaves (rehydrate)
+int launch_manifest(bool gather, void *flat, uint64_t flat_bytes, const ManifestLeaf *leaves,
+                    uint32_t n_leaves, int n_cu, void *stream);
 int set_kernel_attributes();
 
 }  // namespace wm

@@ -2121,6 +2121,88 @@ int launch_decode(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
   return (int)hipGetLastError();
 }
 
+// ------------------------------------------------------------- manifest --
+// Flatten (gather the leaves into the flat state) and rehydrate (scatter it
+// back).  Each workgroup takes 64 KiB windows of the flat buffer, so the
+// work is balanced whatever the leaf sizes; a window finds its first leaf by
+// binary search over the leaf offsets (uniform, scalar loads) and copies the
+// pieces of the leaves it overlaps.  Leaf i occupies flat[off_i, off_i +
+// bytes_i), off_i a multiple of 16; on flatten the bytes up to the next leaf
+// are written as zeros.
+template <bool GATHER>
+__global__ __launch_bounds__(256) void k_manifest(uint8_t *__restrict__ flat, uint64_t flat_bytes,
+                                                  const ManifestLeaf *__restrict__ leaves,
+                                                  uint32_t n_leaves) {
+  typedef const __attribute__((address_space(4))) ManifestLeaf cleaf;
+  const cleaf *L = (cleaf *)(uintptr_t)leaves;
+  const uint64_t n_win = (flat_bytes + kChunk - 1) / kChunk;
+  for (uint64_t w = blockIdx.x; w < n_win; w += gridDim.x) {
+    const uint64_t w0 = w * kChunk, w1 = min(w0 + kChunk, flat_bytes);
+    // first leaf whose padded extent reaches past w0: the last with off <= w0
+    uint32_t lo = 0, hi = n_leaves;
+    while (hi - lo > 1) {
+      const uint32_t mid = (lo + hi) >> 1;
+      if (L[mid].off <= w0) lo = mid; else hi = mid;
+    }
+    for (uint32_t i = lo; i < n_leaves; ++i) {
+      const uint64_t off = L[i].off;
+      if (off >= w1) break;
+      const uint64_t bytes = L[i].bytes;
+      const uint64_t end = i + 1 < n_leaves ? L[i + 1].off : flat_bytes;  // padded end
+      const uint64_t s0 = max(off, w0), s1 = min(end, w1);
+      if (s0 >= s1) continue;
+      uint8_t *leaf = reinterpret_cast<uint8_t *>(L[i].ptr);
+      const uint64_t data_end = off + bytes;
+      if (s0 == w0 && s1 == w0 + kChunk && data_end >= s1) {
+        // the whole window inside one leaf's data: sixteen 16-byte pieces
+        // per thread, all in flight
+        const uint8_t *src = GATHER ? leaf + (w0 - off) : flat + w0;
+        uint8_t *dst = GATHER ? flat + w0 : leaf + (w0 - off);
+        v4u v[kChunk / 4096u];
+#pragma unroll
+        for (uint32_t j = 0; j < kChunk / 4096u; ++j)
+          v[j] = __builtin_nontemporal_load(
+              reinterpret_cast<const v4u *>(src + threadIdx.x * 16u + j * 4096u));
+#pragma unroll
+        for (uint32_t j = 0; j < kChunk / 4096u; ++j)
+          __builtin_nontemporal_store(v[j], reinterpret_cast<v4u *>(dst + threadIdx.x * 16u + j * 4096u));
+        continue;
+      }
+      // general piece [s0, s1): 16-byte units; the unit holding the leaf's
+      // last bytes is copied bytewise (flatten zero-fills the rest of it)
+      for (uint64_t a = s0 + threadIdx.x * 16u; a < s1; a += 256u * 16u) {
+        if (a + 16u <= data_end) {
+          if (GATHER)
+            *reinterpret_cast<uint4 *>(flat + a) = *reinterpret_cast<const uint4 *>(leaf + (a - off));
+          else
+            *reinterpret_cast<uint4 *>(leaf + (a - off)) = *reinterpret_cast<const uint4 *>(flat + a);
+        } else if (GATHER) {
+          uint32_t t[4] = {0, 0, 0, 0};
+          for (uint32_t b = 0; a + b < data_end && b < 16u; ++b)
+            t[b >> 2] |= (uint32_t)leaf[a - off + b] << (8 * (b & 3));
+          *reinterpret_cast<uint4 *>(flat + a) = make_uint4(t[0], t[1], t[2], t[3]);
+        } else {
+          for (uint32_t b = 0; a + b < data_end && b < 16u; ++b) leaf[a - off + b] = flat[a + b];
+        }
+      }
+    }
+  }
+}
+
+int launch_manifest(bool gather, void *flat, uint64_t flat_bytes, const ManifestLeaf *leaves,
+                    uint32_t n_leaves, int n_cu, void *stream) {
+  const uint64_t n_win = (flat_bytes + kChunk - 1) / kChunk;
+  if (!n_win) return 0;
+  const uint32_t grid = (uint32_t)min((uint64_t)n_cu * 8u, n_win);
+  if (gather)
+    hipLaunchKernelGGL(k_manifest<true>, dim3(grid), dim3(256), 0, S(stream),
+                       static_cast<uint8_t *>(flat), flat_bytes, leaves, n_leaves);
+  else
+    hipLaunchKernelGGL(k_manifest<false>, dim3(grid), dim3(256), 0, S(stream),
+                       static_cast<uint8_t *>(flat), flat_bytes, leaves, n_leaves);
+  return (int)hipGetLastError();
+}
+
 int launch_commit(void *live, const ChunkGeom &g, const void *staging, const void *payload,
                   const uint32_t *verdict, int n_cu, void *stream) {
   if (!g.n_chunks) return 0;

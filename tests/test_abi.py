@@ -24,6 +24,17 @@ class Params(ctypes.Structure):
                 ("codec", ctypes.c_uint32), ("flags", ctypes.c_uint32)]
 
 
+class Leaf(ctypes.Structure):
+    _fields_ = [("ptr", ctypes.c_void_p), ("bytes", ctypes.c_uint64)]
+
+
+def leaves(*pairs):
+    t = (Leaf * max(len(pairs), 1))()
+    for i, (p, b) in enumerate(pairs):
+        t[i].ptr, t[i].bytes = p, b
+    return t
+
+
 def declared():
     text = open(HEADER).read()
     return re.findall(r"^\s*(?:const\s+char\s*\*|wm_status|uint64_t)\s*(wm_\w+)\s*\(",
@@ -48,8 +59,16 @@ def lib():
     L.wm_encode_step.argtypes = [vp, vp, u64, pp, vp, vp, vp, vp, vp, u64, vp, vp, u64, vp]
     L.wm_decode_verify.argtypes = [vp, u64, u64, pp, vp, u64, vp, vp, vp, u64, vp]
     L.wm_commit_or_abort.argtypes = [vp, u64, pp, vp, vp, vp, u32, vp]
+    lp = ctypes.POINTER(Leaf)
+    L.wm_flat_bytes.restype = u64
+    L.wm_flat_bytes.argtypes = [lp, u32]
+    L.wm_manifest_ws_bytes.restype = u64
+    L.wm_manifest_ws_bytes.argtypes = [u32]
+    L.wm_flatten.argtypes = [lp, u32, vp, u64, vp, u64, vp]
+    L.wm_rehydrate.argtypes = [vp, u64, lp, u32, vp, u64, vp]
     for name in declared():
-        if name not in ("wm_status_str", "wm_workspace_bytes", "wm_payload_bound"):
+        if name not in ("wm_status_str", "wm_workspace_bytes", "wm_payload_bound",
+                        "wm_flat_bytes", "wm_manifest_ws_bytes"):
             getattr(L, name).restype = ctypes.c_int32
     return L
 
@@ -61,9 +80,9 @@ def P(chunk=CH, kind=0, codec=1, flags=0):
 def test_header_declares_the_boundary():
     names = declared()
     for must in ("wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_decode_verify",
-                 "wm_commit_or_abort"):
+                 "wm_commit_or_abort", "wm_flatten", "wm_rehydrate"):
         assert must in names
-    assert len(names) == len(set(names)) == 10
+    assert len(names) == len(set(names)) == 14
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -135,3 +154,38 @@ def test_decode_and_commit_argument_checks(lib):
     assert com(a, 4 * CH, P(), a, a, None, 1, None) == INVALID   # no verdict
     assert com(a, 4 * CH, P(), a, a, a, 2, None) == INVALID      # unknown mode
     assert com(a + 1, 4 * CH, P(), a, a, a, 1, None) == INVALID  # misaligned live
+
+
+def test_flat_bytes_matches_the_oracle(lib):
+    import wm_inputs
+    sizes = wm_inputs.ragged_sizes(100, seed=9)
+    t = leaves(*[(ALIGNED, s) for s in sizes])
+    assert lib.wm_flat_bytes(t, len(sizes)) == oracle.flat_layout(sizes)[1]
+    assert lib.wm_flat_bytes(None, 3) == 0
+    assert lib.wm_flat_bytes(None, 0) == 0
+    assert lib.wm_flat_bytes(leaves((ALIGNED, 1 << 63), (ALIGNED, 1 << 63)), 2) == 0
+    assert lib.wm_manifest_ws_bytes(450) == 32 * 450
+
+
+def test_manifest_argument_checks(lib):
+    a = ALIGNED
+    t = leaves((a, 100), (a + 4096, 17))
+    flat_b, ws_b = 144, 64  # 112 + 32 flat bytes, 2 x 32 table bytes
+    for fn, call in (("flatten", lambda t, n, f, cap, w, wb:
+                      lib.wm_flatten(t, n, f, cap, w, wb, None)),
+                     ("rehydrate", lambda t, n, f, cap, w, wb:
+                      lib.wm_rehydrate(f, cap, t, n, w, wb, None))):
+        assert call(None, 2, a, flat_b, a, ws_b) == INVALID, fn
+        assert call(leaves((a + 8, 100)), 1, a, flat_b, a, ws_b) == INVALID, fn
+        assert call(leaves((None, 100)), 1, a, flat_b, a, ws_b) == INVALID, fn
+        assert call(t, 2, a + 4, flat_b, a, ws_b) == INVALID, fn
+        assert call(t, 2, None, flat_b, a, ws_b) == INVALID, fn
+        assert call(t, 2, a, flat_b - 16, a, ws_b) == CAPACITY, fn
+        assert call(t, 2, a, flat_b, a, ws_b - 1) == WORKSPACE, fn
+        assert call(t, 2, a, flat_b, None, ws_b) == WORKSPACE, fn
+        assert call(t, 2, a, flat_b, a + 2, ws_b) == WORKSPACE, fn
+        big = leaves((a, (1 << 64) - 8), (a, 64))
+        assert call(big, 2, a, 1 << 62, a, ws_b) == INVALID, fn
+        # nothing to copy: no device work, so this returns without a GPU
+        assert call(None, 0, None, 0, None, 0) == OK, fn
+        assert call(leaves((None, 0), (a + 3, 0)), 2, None, 0, a, ws_b) == OK, fn

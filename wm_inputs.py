@@ -164,3 +164,59 @@ def production_step(prev: torch.Tensor, device=None):
 
 def as_bytes(t: torch.Tensor) -> torch.Tensor:
     return t.contiguous().view(-1).view(torch.uint8)
+
+
+# ---- session manifests ------------------------------------------------------
+# The paper's suspend manifest has 450 leaves: the 420 movable tensors plus
+# scalar control flags (§5 "Implementation").  A stand-in of the same
+# structure is cut from a cache of the specs above: per layer, the K and the V
+# slab split into 7 head groups (392 tensors for 28 layers), one fp32 [T]
+# per-layer tensor (28), and 30 scalar control leaves of 1, 4 or 8 bytes.
+
+N_CONTROL_LEAVES = 30
+
+
+def head_groups(n_heads: int) -> tuple:
+    """Split n_heads into min(7, n_heads) groups, the larger groups last
+    (16 heads -> 2,2,2,2,2,3,3)."""
+    g = min(7, n_heads)
+    base, extra = divmod(n_heads, g)
+    return tuple(base + (1 if i >= g - extra else 0) for i in range(g))
+
+
+def make_manifest(spec: CacheSpec, device="cpu", cache=None) -> list:
+    """Leaves of a session manifest built on `spec`'s cache: a list of
+    separate contiguous tensors (bf16 head-group slabs, fp32 per-layer
+    tensors, uint8/int32/int64 control scalars)."""
+    if cache is None:
+        cache = make_cache(spec, device)
+    L, _, H, T, _ = spec.shape
+    g = torch.Generator(device=cache.device).manual_seed(spec.seed + 7000)
+    leaves = []
+    groups = head_groups(H)
+    for layer in range(L):
+        for kv in range(2):
+            h0 = 0
+            for n in groups:
+                leaves.append(cache[layer, kv, h0:h0 + n].clone())
+                h0 += n
+        leaves.append(torch.rand(T, generator=g, device=cache.device))
+    dtypes = (torch.uint8, torch.int32, torch.int64)
+    for i in range(N_CONTROL_LEAVES):
+        leaves.append(torch.randint(0, 1 << 30, (1,), generator=g, device=cache.device,
+                                    dtype=torch.int64).to(dtypes[i % 3]))
+    return leaves
+
+
+def ragged_sizes(n: int, seed: int) -> list:
+    """Leaf sizes mixing the edge cases of a flat layout (0, 1, 15, 16, 17,
+    64 KiB +- 1 ...) with uniform sizes up to 300 KB."""
+    g = torch.Generator().manual_seed(seed)
+    edge = [0, 1, 15, 16, 17, 4095, 4096, 65535, 65536, 65537, 131071, 2]
+    sizes = []
+    for i in range(n):
+        if i % 3 == 0:
+            sizes.append(edge[(i // 3) % len(edge)])
+        else:
+            sizes.append(int(torch.randint(1, 300_000, (1,), generator=g).item()))
+    return sizes
