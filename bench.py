@@ -42,6 +42,8 @@ def parse():
                     help="skip the active-generation step measurement")
     ap.add_argument("--no-manifest", action="store_true",
                     help="skip the 450-leaf flatten/rehydrate measurement")
+    ap.add_argument("--no-precopy", action="store_true",
+                    help="skip the iterative pre-copy measurement")
     ap.add_argument("--crc", type=int, default=0, help="0 zlib CRC-32, 1 CRC-32C")
     ap.add_argument("--counter-pass", action="store_true",
                     help="one full-ship encode and decode plus a 1 GiB device copy, "
@@ -164,6 +166,58 @@ def cpu_baseline(host_state, nbytes_chunk=65536, target_s=12.0):
                       f"cache ({m * nbytes_chunk} B); encode + decode_verify + "
                       f"commit, {dt:.1f} s",
             "cpu_model": cpu}
+
+
+def precopy_runs(torch, wm_inputs, spec, state, crc, dev, rho, max_rounds):
+    """Iterative pre-copy of the production cache into an empty destination
+    while the source writes rho random chunks per chunk shipped (occupancy
+    model), until a round ships at most 64 chunks or max_rounds live rounds
+    ran; then the final (paused) round.  Each round is one synchronous
+    wm_precopy_round, timed with HIP events on its stream."""
+    from paper_2607_10389_amd import Mover, _wm
+    import math
+
+    nbytes, n = spec.nbytes, spec.nbytes // 65536
+    cur = state.clone()
+    shipped = torch.zeros(nbytes, dtype=torch.uint8, device=dev)
+    dest = torch.zeros_like(shipped)
+    m = Mover(nbytes, crc, dev)
+    rounds, paused, k = [], False, 0
+    while True:
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        s.record()
+        st, nd = m.precopy_round(cur, shipped, dest)
+        e.record()
+        e.synchronize()
+        if st != _wm.WM_OK:
+            raise RuntimeError("pre-copy round failed verification")
+        rounds.append({"dirty": nd, "ms": round(s.elapsed_time(e), 4),
+                       "payload_bytes": int(m.payload_bytes.item())})
+        if paused:
+            break
+        ids = wm_inputs.chunk_writes(n, int(round(rho * nd)), seed=5000 + k, device=dev)
+        wm_inputs.rewrite_chunks(cur, spec, ids, seed=6000 + k)
+        k += 1
+        paused = nd <= 64 or k >= max_rounds
+    torch.cuda.synchronize()
+    if not torch.equal(dest, cur.view(-1).view(torch.uint8)):
+        raise RuntimeError("pre-copy destination differs from the source")
+    # occupancy law for each round after the first, given the previous
+    # round's dirty count: w = rho * d writes dirty N (1 - e^(-w/N)) chunks
+    pred = [n * (1 - math.exp(-round(rho * r["dirty"]) / n)) for r in rounds[:-1]]
+    return {
+        "workload": f"production cache into an empty destination, {rho} random chunk "
+                    "writes per chunk shipped, pause at <= 64 dirty chunks or "
+                    f"{max_rounds} live rounds",
+        "rounds": len(rounds),
+        "dirty_per_round": [r["dirty"] for r in rounds],
+        "occupancy_law_expected_from_round_1": [round(x, 1) for x in pred],
+        "ms_per_round": [r["ms"] for r in rounds],
+        "total_ms": round(sum(r["ms"] for r in rounds), 4),
+        "downtime_ms": rounds[-1]["ms"],
+        "final_round_dirty": rounds[-1]["dirty"],
+    }
 
 
 def main():
@@ -373,6 +427,10 @@ def main():
                                 2 * total),
         }
         del leaves, flat, back
+
+    if not args.no_precopy:
+        out["precopy"] = {r: precopy_runs(torch, wm_inputs, spec, state, args.crc, dev, rho, cap)
+                          for r, rho, cap in (("converging", 0.5, 30), ("saturating", 1.93, 6))}
 
     if not args.no_cpu:
         host = state.view(-1).view(torch.uint8).cpu().numpy()

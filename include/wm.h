@@ -9,6 +9,8 @@
  *                     -> wm_encode (or the single-pass wm_encode_step)
  *   destination side  wm_decode_verify -> wm_commit_or_abort -> [wm_rehydrate]
  *
+ * and one round of iterative pre-copy built from them (wm_precopy_round).
+ *
  * under the paper's contract: the destination is bit-identical to the source
  * or nothing is installed (§1; §4 "Sufficiency": commit only on a
  * byte-identical fingerprint; Table 1: migrate stages into a shadow slot,
@@ -20,7 +22,7 @@
  *     pointer after returning.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Calls only enqueue work on it and return without waiting, except
- *     wm_commit_or_abort, which waits for the stream.
+ *     wm_commit_or_abort and wm_precopy_round, which wait for the stream.
  *   - Argument errors are detected on the host before anything is enqueued;
  *     the call then returns a negative status and writes nothing.
  *   - Problems found on the device (a malformed or corrupted payload) are
@@ -227,6 +229,56 @@ wm_status wm_flatten(const wm_leaf *leaves, uint32_t n_leaves, void *flat,
 wm_status wm_rehydrate(const void *flat, uint64_t flat_cap,
                        const wm_leaf *leaves, uint32_t n_leaves, void *ws,
                        uint64_t ws_bytes, void *stream);
+
+/* ---- iterative pre-copy ---------------------------------------------------
+ * Pre-copy ships a state that keeps changing: each round ships the chunks
+ * that differ from what the destination already holds, while the source
+ * goes on writing; when a round's dirty set is small enough the source
+ * pauses and one last round makes the destination exact (§6.2 Exhibit 2;
+ * App. H: the per-round dirty set follows the occupancy law
+ * N(1 - e^(-w/(N C))) for w bytes written in C-byte chunks).
+ *
+ * Device buffers of one move, owned by the caller, with the sizes the
+ * individual calls require (n = ceil(nbytes / chunk_bytes)). */
+typedef struct {
+  uint32_t *crc;            /* n u32: chunk CRCs of the round's cur */
+  uint32_t *global_crc;     /* 1 u32 or NULL */
+  uint32_t *dirty_idx;      /* n u32 */
+  uint32_t *n_dirty;        /* 1 u32 */
+  void *payload;            /* payload_cap >= wm_payload_bound(nbytes, n) */
+  uint64_t payload_cap;
+  uint64_t *payload_bytes;  /* 1 u64 */
+  void *staging;            /* staging_cap >= n * chunk_bytes */
+  uint64_t staging_cap;
+  uint32_t *verdict;        /* 1 u32 */
+  uint32_t *rec_status;     /* n u32 or NULL */
+  void *ws_src;             /* wm_workspace_bytes() each; two different */
+  uint64_t ws_src_bytes;
+  void *ws_dst;
+  uint64_t ws_dst_bytes;
+} wm_move_buffers;
+
+/* One pre-copy round: wm_encode_step(cur, shipped) ships the chunks of cur
+ * that differ from shipped, wm_decode_verify checks them, and only if the
+ * verdict is 0 each verified record is installed into dest (the
+ * destination's state) and into shipped (the source's copy of what the
+ * destination holds).  Waits for the stream; *n_dirty_host (host) receives
+ * the round's dirty count.  Returns WM_OK, or WM_VERIFY_FAILED with dest and
+ * shipped untouched.
+ *   cur      : nbytes (even), 16-byte aligned; the caller may keep writing
+ *              it on other streams during the round: shipped receives the
+ *              bytes that were encoded, so a chunk changed after it was read
+ *              differs from shipped and is dirty in the next round
+ *   shipped, dest : nbytes each, 16-byte aligned, distinct from cur and
+ *              from each other; equal to each other before the first round
+ *              (e.g. both zero) and kept equal by every round
+ * Errors: those of the four calls it makes (WM_ERR_INVALID_ARG for a
+ *         missing buffer, WM_ERR_CAPACITY for a short payload or staging,
+ *         WM_ERR_WORKSPACE, WM_ERR_HIP). */
+wm_status wm_precopy_round(const void *cur, void *shipped, void *dest,
+                           uint64_t nbytes, const wm_params *p,
+                           const wm_move_buffers *b, uint32_t *n_dirty_host,
+                           void *stream);
 
 #ifdef __cplusplus
 }

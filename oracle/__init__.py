@@ -232,3 +232,31 @@ def rehydrate(flat, sizes) -> list[np.ndarray]:
     out = [np.zeros(max(int(s), 1), np.uint8) for s in sz]
     lib().orc_rehydrate(_p8(f), _ptr_table(out), _u64p(sz), sz.size)
     return [o[: int(s)] for o, s in zip(out, sz)]
+
+
+# ---- pre-copy occupancy model (App. H: the coupon-law derivation) ---------
+# w chunk writes, each to one of N chunks drawn uniformly with replacement,
+# leave a dirty set whose size is the number of distinct chunks hit.
+
+
+def occupancy_mean(n: int, w: int) -> float:
+    """Expected distinct chunks: N (1 - (1 - 1/N)^w), which the paper writes
+    in its large-N form N (1 - e^(-w/N)) (w counted in chunks)."""
+    return n * (1.0 - (1.0 - 1.0 / n) ** w)
+
+
+def occupancy_var(n: int, w: int) -> float:
+    """Variance of the distinct count (sum of N dependent indicators)."""
+    q1 = (1.0 - 1.0 / n) ** w
+    q2 = (1.0 - 2.0 / n) ** w if n > 1 else 0.0
+    return n * q1 + n * (n - 1) * q2 - (n * q1) ** 2
+
+
+def precopy_recursion(n: int, rho: float, n0: int, rounds: int) -> list:
+    """Expected dirty chunks per round when the source writes rho chunks per
+    chunk shipped: d_0 = n0, d_(k+1) = N (1 - e^(-rho d_k / N))."""
+    import math
+    d = [float(n0)]
+    for _ in range(rounds - 1):
+        d.append(n * (1.0 - math.exp(-rho * d[-1] / n)))
+    return d

@@ -16,3 +16,4 @@ from ._wm import (  # noqa: F401
     manifest_ws_bytes, params, payload_bound, rehydrate, workspace_bytes,
 )
 from .mover import Mover  # noqa: F401
+from . import precopy  # noqa: F401

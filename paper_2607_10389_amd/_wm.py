@@ -40,7 +40,7 @@ EXPORTS = (
     "wm_status_str", "wm_init", "wm_workspace_bytes", "wm_payload_bound",
     "wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_encode_step",
     "wm_decode_verify", "wm_commit_or_abort", "wm_flat_bytes",
-    "wm_manifest_ws_bytes", "wm_flatten", "wm_rehydrate",
+    "wm_manifest_ws_bytes", "wm_flatten", "wm_rehydrate", "wm_precopy_round",
 )
 
 
@@ -57,6 +57,17 @@ class Params(ctypes.Structure):
 
 class Leaf(ctypes.Structure):
     _fields_ = [("ptr", ctypes.c_void_p), ("bytes", ctypes.c_uint64)]
+
+
+class MoveBuffers(ctypes.Structure):
+    _fields_ = [("crc", ctypes.c_void_p), ("global_crc", ctypes.c_void_p),
+                ("dirty_idx", ctypes.c_void_p), ("n_dirty", ctypes.c_void_p),
+                ("payload", ctypes.c_void_p), ("payload_cap", ctypes.c_uint64),
+                ("payload_bytes", ctypes.c_void_p),
+                ("staging", ctypes.c_void_p), ("staging_cap", ctypes.c_uint64),
+                ("verdict", ctypes.c_void_p), ("rec_status", ctypes.c_void_p),
+                ("ws_src", ctypes.c_void_p), ("ws_src_bytes", ctypes.c_uint64),
+                ("ws_dst", ctypes.c_void_p), ("ws_dst_bytes", ctypes.c_uint64)]
 
 
 def _load():
@@ -87,6 +98,8 @@ def _load():
         "wm_manifest_ws_bytes": ([u32], u64),
         "wm_flatten": ([lp, u32, vp, u64, vp, u64, vp], ctypes.c_int32),
         "wm_rehydrate": ([vp, u64, lp, u32, vp, u64, vp], ctypes.c_int32),
+        "wm_precopy_round": ([vp, vp, vp, u64, pp, ctypes.POINTER(MoveBuffers),
+                              ctypes.POINTER(u32), vp], ctypes.c_int32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -236,3 +249,24 @@ def rehydrate(flat, leaves, ws, stream=None):
     return _check(LIB.wm_rehydrate(_p(flat), _nbytes(flat), tab.t, tab.n,
                                    _p(ws), _nbytes(ws), _stream(stream)),
                   "wm_rehydrate")
+
+
+def move_buffers(crc, global_crc, dirty_idx, n_dirty, payload, payload_bytes,
+                 staging, verdict, rec_status, ws_src, ws_dst) -> MoveBuffers:
+    def a(t):
+        return None if t is None else _p(t).value
+    return MoveBuffers(a(crc), a(global_crc), a(dirty_idx), a(n_dirty),
+                       a(payload), _nbytes(payload), a(payload_bytes),
+                       a(staging), _nbytes(staging), a(verdict), a(rec_status),
+                       a(ws_src), _nbytes(ws_src), a(ws_dst), _nbytes(ws_dst))
+
+
+def precopy_round(cur, shipped, dest, nbytes, p, bufs: MoveBuffers,
+                  stream=None) -> tuple[int, int]:
+    """(status, dirty count) of one pre-copy round; waits for the stream."""
+    n = ctypes.c_uint32(0)
+    st = _check(LIB.wm_precopy_round(_p(cur), _p(shipped), _p(dest), nbytes,
+                                     ctypes.byref(p), ctypes.byref(bufs),
+                                     ctypes.byref(n), _stream(stream)),
+                "wm_precopy_round")
+    return st, int(n.value)

@@ -318,3 +318,50 @@ wm_status wm_rehydrate(const void *flat, uint64_t flat_cap, const wm_leaf *leave
 }
 
 }  // extern "C"
+
+extern "C" {
+
+wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t nbytes,
+                           const wm_params *p, const wm_move_buffers *b,
+                           uint32_t *n_dirty_host, void *stream) {
+  ChunkGeom g;
+  wm_status s = make_geom(nbytes, p, &g);
+  if (s != WM_OK) return s;
+  if (nbytes & 1u) return WM_ERR_INVALID_ARG;
+  if (!b || !n_dirty_host || !b->crc || !b->dirty_idx || !b->n_dirty) return WM_ERR_INVALID_ARG;
+  if (nbytes && (!cur || !shipped || !dest)) return WM_ERR_INVALID_ARG;
+  if (nbytes && (cur == shipped || cur == dest || shipped == dest)) return WM_ERR_INVALID_ARG;
+  if (!aligned16(shipped) || !aligned16(dest)) return WM_ERR_INVALID_ARG;
+  // the checks of the destination-side calls come first, so that an
+  // argument error leaves everything untouched
+  if (!b->verdict || (nbytes && !b->staging) || !aligned16(b->staging)) return WM_ERR_INVALID_ARG;
+  if (b->staging_cap < (uint64_t)g.n_chunks * kChunk) return WM_ERR_CAPACITY;
+  const uint64_t ws_need = ws_layout(g.n_chunks).total;
+  if (!b->ws_dst || !aligned16(b->ws_dst) || b->ws_dst_bytes < ws_need || b->ws_src == b->ws_dst)
+    return WM_ERR_WORKSPACE;
+  s = wm_encode_step(cur, shipped, nbytes, p, b->crc, b->global_crc, b->dirty_idx, b->n_dirty,
+                     b->payload, b->payload_cap, b->payload_bytes, b->ws_src, b->ws_src_bytes,
+                     stream);
+  if (s != WM_OK) return s;
+  s = wm_decode_verify(b->payload, b->payload_cap, nbytes, p, b->staging, b->staging_cap,
+                       b->verdict, b->rec_status, b->ws_dst, b->ws_dst_bytes, stream);
+  if (s != WM_OK) return s;
+  int n_cu = 0;
+  if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  if (nbytes) {
+    // both installs are conditional on the same device verdict word
+    if (launch_commit(dest, g, b->staging, b->payload, b->verdict, n_cu, stream) != 0 ||
+        launch_commit(shipped, g, b->staging, b->payload, b->verdict, n_cu, stream) != 0)
+      return WM_ERR_HIP;
+  }
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  uint32_t v[2] = {0xFFFFFFFFu, 0};
+  if (hipMemcpyAsync(&v[0], b->verdict, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(&v[1], b->n_dirty, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return WM_ERR_HIP;
+  *n_dirty_host = v[1];
+  return v[0] == 0 ? WM_OK : WM_VERIFY_FAILED;
+}
+
+}  // extern "C"

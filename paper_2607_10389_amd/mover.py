@@ -38,6 +38,7 @@ class Mover:
                                    device=self.device)
         self.verdict = torch.zeros(1, **u32)
         self.rec_status = torch.zeros(max(n, 1), **u32)
+        self._bufs = None
 
     # ---- source side
     def checksum(self, state: torch.Tensor):
@@ -77,6 +78,19 @@ class Mover:
         mode = _wm.WM_COMMIT_SCATTER if scatter else _wm.WM_COMMIT_NONE
         return _wm.commit_or_abort(live, self.nbytes, self.p, self.staging, pl,
                                    self.verdict, mode, self.stream)
+
+    # ---- iterative pre-copy
+    def precopy_round(self, cur: torch.Tensor, shipped: torch.Tensor,
+                      dest: torch.Tensor) -> tuple[int, int]:
+        """One round (diff against shipped, encode, decode, verify, install
+        into dest and shipped); returns (status, dirty chunks)."""
+        if self._bufs is None:
+            self._bufs = _wm.move_buffers(
+                self.crc, self.global_crc, self.dirty_idx, self.n_dirty,
+                self.payload, self.payload_bytes, self.staging, self.verdict,
+                self.rec_status, self.ws_src, self.ws_dst)
+        return _wm.precopy_round(cur, shipped, dest, self.nbytes, self.p,
+                                 self._bufs, self.stream)
 
     # ---- host views (synchronising)
     def payload_host(self):

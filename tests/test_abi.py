@@ -28,6 +28,14 @@ class Leaf(ctypes.Structure):
     _fields_ = [("ptr", ctypes.c_void_p), ("bytes", ctypes.c_uint64)]
 
 
+class MoveBuffers(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint64 if n.endswith(("_cap", "_bytes")) and n != "payload_bytes"
+                 else ctypes.c_void_p)
+                for n in ("crc", "global_crc", "dirty_idx", "n_dirty", "payload", "payload_cap",
+                          "payload_bytes", "staging", "staging_cap", "verdict", "rec_status",
+                          "ws_src", "ws_src_bytes", "ws_dst", "ws_dst_bytes")]
+
+
 def leaves(*pairs):
     t = (Leaf * max(len(pairs), 1))()
     for i, (p, b) in enumerate(pairs):
@@ -66,6 +74,8 @@ def lib():
     L.wm_manifest_ws_bytes.argtypes = [u32]
     L.wm_flatten.argtypes = [lp, u32, vp, u64, vp, u64, vp]
     L.wm_rehydrate.argtypes = [vp, u64, lp, u32, vp, u64, vp]
+    L.wm_precopy_round.argtypes = [vp, vp, vp, u64, pp, ctypes.POINTER(MoveBuffers),
+                                   ctypes.POINTER(u32), vp]
     for name in declared():
         if name not in ("wm_status_str", "wm_workspace_bytes", "wm_payload_bound",
                         "wm_flat_bytes", "wm_manifest_ws_bytes"):
@@ -82,7 +92,7 @@ def test_header_declares_the_boundary():
     for must in ("wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_decode_verify",
                  "wm_commit_or_abort", "wm_flatten", "wm_rehydrate"):
         assert must in names
-    assert len(names) == len(set(names)) == 14
+    assert len(names) == len(set(names)) == 15
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -189,3 +199,40 @@ def test_manifest_argument_checks(lib):
         # nothing to copy: no device work, so this returns without a GPU
         assert call(None, 0, None, 0, None, 0) == OK, fn
         assert call(leaves((None, 0), (a + 3, 0)), 2, None, 0, a, ws_b) == OK, fn
+
+
+def test_precopy_round_argument_checks(lib):
+    a = ALIGNED
+    nb = 4 * CH
+    ws = lib.wm_workspace_bytes(nb, P())
+    bound = lib.wm_payload_bound(nb, 4, P())
+
+    def bufs(**kw):
+        d = dict(crc=a, global_crc=None, dirty_idx=a, n_dirty=a, payload=a + 0x100000,
+                 payload_cap=bound, payload_bytes=a, staging=a + 0x200000, staging_cap=nb,
+                 verdict=a, rec_status=None, ws_src=a + 0x300000, ws_src_bytes=ws,
+                 ws_dst=a + 0x400000, ws_dst_bytes=ws)
+        d.update(kw)
+        return ctypes.byref(MoveBuffers(**d))
+
+    n = ctypes.c_uint32(0)
+    cur, shp, dst = a + 0x500000, a + 0x600000, a + 0x700000
+    rnd = lib.wm_precopy_round
+    assert rnd(cur, shp, dst, nb, P(), None, ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, dst, nb, P(), bufs(), None, None) == INVALID
+    assert rnd(cur, shp, shp, nb, P(), bufs(), ctypes.byref(n), None) == INVALID
+    assert rnd(cur, cur, dst, nb, P(), bufs(), ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp + 8, dst, nb, P(), bufs(), ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, None, nb, P(), bufs(), ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, dst, nb, P(), bufs(verdict=None), ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, dst, nb, P(), bufs(n_dirty=None), ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, dst, nb, P(), bufs(staging_cap=nb - CH), ctypes.byref(n),
+               None) == CAPACITY
+    assert rnd(cur, shp, dst, nb, P(), bufs(ws_dst_bytes=ws - 1), ctypes.byref(n),
+               None) == WORKSPACE
+    assert rnd(cur, shp, dst, nb, P(), bufs(ws_dst=a + 0x300000), ctypes.byref(n),
+               None) == WORKSPACE
+    assert rnd(cur, shp, dst, nb, P(), bufs(payload_cap=bound - 1), ctypes.byref(n),
+               None) == CAPACITY
+    assert rnd(cur, shp, dst, nb + 1, P(), bufs(), ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, dst, nb, P(chunk=4096), bufs(), ctypes.byref(n), None) == UNSUPPORTED

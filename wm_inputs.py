@@ -112,15 +112,14 @@ def chunk_scales(spec: CacheSpec, chunk_ids: torch.Tensor,
     return scale[e // (T * D), e % D]
 
 
-def regenerate(prev: torch.Tensor, spec: CacheSpec, chunk_ids: torch.Tensor,
-               seed: int) -> torch.Tensor:
-    """Copy of prev whose listed 64 KiB chunks hold fresh draws from the same
-    per-channel distribution (the active-generation step)."""
-    device = prev.device
-    cur = prev.clone()
-    flat = cur.view(-1)
+def rewrite_chunks(state: torch.Tensor, spec: CacheSpec, chunk_ids: torch.Tensor,
+                   seed: int) -> None:
+    """In place: the listed 64 KiB chunks of state (ids may repeat) get fresh
+    draws from the same per-channel distribution."""
+    device = state.device
+    flat = state.view(-1)
     words = CHUNK // 2
-    ids = torch.sort(chunk_ids.to(device)).values
+    ids = torch.unique(chunk_ids.to(device))
     g = torch.Generator(device=device).manual_seed(seed)
     step = 2048  # chunks per batch, bounds temporary memory
     for b in range(0, ids.numel(), step):
@@ -130,7 +129,22 @@ def regenerate(prev: torch.Tensor, spec: CacheSpec, chunk_ids: torch.Tensor,
         pos = (part.view(-1, 1) * words +
                torch.arange(words, device=device).view(1, -1)).view(-1)
         flat[pos] = z.view(-1).to(torch.bfloat16)
+
+
+def regenerate(prev: torch.Tensor, spec: CacheSpec, chunk_ids: torch.Tensor,
+               seed: int) -> torch.Tensor:
+    """Copy of prev whose listed 64 KiB chunks hold fresh draws from the same
+    per-channel distribution (the active-generation step)."""
+    cur = prev.clone()
+    rewrite_chunks(cur, spec, chunk_ids, seed)
     return cur
+
+
+def chunk_writes(n_chunks: int, count: int, seed: int, device="cpu") -> torch.Tensor:
+    """`count` chunk writes of a generating session, each to a chunk drawn
+    uniformly with replacement (the occupancy model of pre-copy)."""
+    g = torch.Generator(device=device).manual_seed(seed)
+    return torch.randint(0, n_chunks, (count,), generator=g, device=device)
 
 
 def bernoulli_chunks(n_chunks: int, p: float, seed: int,
