@@ -42,6 +42,8 @@ def parse():
                     help="skip the active-generation step measurement")
     ap.add_argument("--no-manifest", action="store_true",
                     help="skip the 450-leaf flatten/rehydrate measurement")
+    ap.add_argument("--no-receive", action="store_true",
+                    help="skip the pipelined receive measurement")
     ap.add_argument("--no-precopy", action="store_true",
                     help="skip the iterative pre-copy measurement")
     ap.add_argument("--crc", type=int, default=0, help="0 zlib CRC-32, 1 CRC-32C")
@@ -166,6 +168,69 @@ def cpu_baseline(host_state, nbytes_chunk=65536, target_s=12.0):
                       f"cache ({m * nbytes_chunk} B); encode + decode_verify + "
                       f"commit, {dt:.1f} s",
             "cpu_model": cpu}
+
+
+def receive_runs(torch, m_src, nbytes, crc, dev):
+    """The full-ship payload of the production cache arriving in pinned host
+    memory: the plain host-to-device copy (the wire), copy then decode on one
+    stream (sequential), and wm_receive_verify with record batches of 16, 64
+    and 256 MiB (copies on a second stream, each batch decoded as it
+    lands).  HIP events on the decode stream bracket each run."""
+    from paper_2607_10389_amd import Mover
+
+    pb = int(m_src.payload_bytes.item())
+    host = torch.empty(pb, dtype=torch.uint8, pin_memory=True)
+    host.copy_(m_src.payload[:pb])
+    m = Mover(nbytes, crc, dev)
+    cs = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+
+    def timed(fn, reps=5):
+        """Mean (total ms, ms from the last copy's end to the end of the
+        decode) over reps; copies run on cs, the decode on main."""
+        fn()
+        torch.cuda.synchronize()
+        tot = tail = 0.0
+        for _ in range(reps):
+            s, ec, e = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            s.record(main)
+            cs.wait_event(s)
+            fn()
+            ec.record(cs)
+            e.record(main)
+            e.synchronize()
+            tot += s.elapsed_time(e)
+            tail += ec.elapsed_time(e)
+        return tot / reps, tail / reps
+
+    def wire():
+        with torch.cuda.stream(cs):
+            m.payload[:pb].copy_(host, non_blocking=True)
+
+    def sequential():
+        wire()
+        main.wait_stream(cs)
+        m.decode()
+
+    wire_ms, _ = timed(wire)
+    seq_ms, seq_tail = timed(sequential)
+    torch.cuda.synchronize()
+    dec_ms = timed_events(torch, lambda: m.decode(), 10)
+    out = {"workload": f"full-ship payload of the production cache ({pb} B) in pinned host memory",
+           "wire_ms": round(wire_ms, 3), "wire_GBps": round(pb / wire_ms / 1e6, 2),
+           "decode_only_ms": round(dec_ms, 4),
+           "sequential": {"ms": round(seq_ms, 3), "exposed_after_last_copy_ms": round(seq_tail, 4)}}
+    for mib in (16, 64, 256):
+        def piped():
+            m.receive(host, pb, mib << 20, cs)
+        t, tail = timed(piped)
+        if int(m.verdict.item()) != 0 or not torch.equal(m.payload[:pb], m_src.payload[:pb]):
+            raise RuntimeError("pipelined receive did not verify")
+        out[f"pipelined_{mib}MiB"] = {
+            "ms": round(t, 3), "verified_GBps": round(pb / t / 1e6, 2),
+            "exposed_after_last_copy_ms": round(tail, 4),
+            "one_batch_decode_ms": round(dec_ms * min(1.0, (mib << 20) / pb), 4)}
+    return out
 
 
 def precopy_runs(torch, wm_inputs, spec, state, crc, dev, rho, max_rounds):
@@ -427,6 +492,9 @@ def main():
                                 2 * total),
         }
         del leaves, flat, back
+
+    if not args.no_receive:
+        out["receive"] = receive_runs(torch, m, nbytes, args.crc, dev)
 
     if not args.no_precopy:
         out["precopy"] = {r: precopy_runs(torch, wm_inputs, spec, state, args.crc, dev, rho, cap)

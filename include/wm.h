@@ -9,7 +9,9 @@
  *                     -> wm_encode (or the single-pass wm_encode_step)
  *   destination side  wm_decode_verify -> wm_commit_or_abort -> [wm_rehydrate]
  *
- * and one round of iterative pre-copy built from them (wm_precopy_round).
+ * a receive that overlaps the payload's copy into device memory with its
+ * decode (wm_receive_verify), and one round of iterative pre-copy built from
+ * them (wm_precopy_round).
  *
  * under the paper's contract: the destination is bit-identical to the source
  * or nothing is installed (§1; §4 "Sufficiency": commit only on a
@@ -229,6 +231,42 @@ wm_status wm_flatten(const wm_leaf *leaves, uint32_t n_leaves, void *flat,
 wm_status wm_rehydrate(const void *flat, uint64_t flat_cap,
                        const wm_leaf *leaves, uint32_t n_leaves, void *ws,
                        uint64_t ws_bytes, void *stream);
+
+/* ---- pipelined receive ----------------------------------------------------
+ * Verification hidden behind the transfer (§6.5: the per-chunk CRC
+ * overlapped with receive and GF(2)-combined leaves one final chunk's check
+ * exposed; §6.4: the exposed tail equals one final-chunk CRC).  The payload
+ * arrives in host memory (a network receive buffer, ideally pinned with
+ * hipHostMalloc so the copies are DMA transfers); its header and table are
+ * copied first, then its records in batches of about batch_bytes, each
+ * batch decoded and verified as soon as it lands, so only the last batch's
+ * decode follows the last copy.
+ *
+ * Outputs equal wm_decode_verify's on the same bytes, whatever batch_bytes.
+ *   host_payload  : payload_bytes of host memory, read by the copies until
+ *                   they have run (the caller keeps it unchanged until then)
+ *   payload       : device buffer of payload_cap >= payload_bytes, 16-byte
+ *                   aligned, receives the payload; device reads stay in
+ *                   [payload, payload + payload_bytes)
+ *   batch_bytes   : target record bytes per batch (0: one record per batch;
+ *                   raised so that there are at most 4096 batches)
+ *   copy_stream   : stream of the copies; stream: stream of the decode,
+ *                   which waits for each batch's copies through events.  Use
+ *                   two different streams (not the legacy null stream) for
+ *                   overlap; the same stream gives the sequential schedule.
+ * Other arguments as wm_decode_verify.  Returns after enqueueing.  The host
+ * reads the header and table only to schedule the copies; a header or table
+ * that does not parse is copied as one batch, and validity is decided on the
+ * device exactly as in wm_decode_verify.
+ * Errors: WM_ERR_INVALID_ARG, WM_ERR_CAPACITY (payload_bytes > payload_cap),
+ *         WM_ERR_WORKSPACE, WM_ERR_UNSUPPORTED, WM_ERR_HIP. */
+wm_status wm_receive_verify(const void *host_payload, uint64_t payload_bytes,
+                            void *payload, uint64_t payload_cap,
+                            uint64_t nbytes, const wm_params *p, void *staging,
+                            uint64_t staging_cap, uint32_t *verdict,
+                            uint32_t *rec_status, void *ws, uint64_t ws_bytes,
+                            uint64_t batch_bytes, void *copy_stream,
+                            void *stream);
 
 /* ---- iterative pre-copy ---------------------------------------------------
  * Pre-copy ships a state that keeps changing: each round ships the chunks

@@ -41,6 +41,7 @@ EXPORTS = (
     "wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_encode_step",
     "wm_decode_verify", "wm_commit_or_abort", "wm_flat_bytes",
     "wm_manifest_ws_bytes", "wm_flatten", "wm_rehydrate", "wm_precopy_round",
+    "wm_receive_verify",
 )
 
 
@@ -98,6 +99,8 @@ def _load():
         "wm_manifest_ws_bytes": ([u32], u64),
         "wm_flatten": ([lp, u32, vp, u64, vp, u64, vp], ctypes.c_int32),
         "wm_rehydrate": ([vp, u64, lp, u32, vp, u64, vp], ctypes.c_int32),
+        "wm_receive_verify": ([vp, u64, vp, u64, u64, pp, vp, u64, vp, vp, vp, u64,
+                               u64, vp, vp], ctypes.c_int32),
         "wm_precopy_round": ([vp, vp, vp, u64, pp, ctypes.POINTER(MoveBuffers),
                               ctypes.POINTER(u32), vp], ctypes.c_int32),
     }
@@ -270,3 +273,17 @@ def precopy_round(cur, shipped, dest, nbytes, p, bufs: MoveBuffers,
                                      ctypes.byref(n), _stream(stream)),
                 "wm_precopy_round")
     return st, int(n.value)
+
+
+def receive_verify(host_payload, payload_bytes, payload, nbytes, p, staging,
+                   verdict, rec_status, ws, batch_bytes, copy_stream, stream=None):
+    """host_payload: a CPU uint8 tensor (pinned for DMA copies)."""
+    if host_payload.is_cuda or not host_payload.is_contiguous():
+        raise ValueError("host_payload is a contiguous host tensor")
+    if payload_bytes > _nbytes(host_payload):
+        raise ValueError("payload_bytes exceeds the host buffer")
+    return _check(LIB.wm_receive_verify(
+        ctypes.c_void_p(host_payload.data_ptr()), payload_bytes, _p(payload),
+        _nbytes(payload), nbytes, ctypes.byref(p), _p(staging), _nbytes(staging),
+        _p(verdict), _p(rec_status), _p(ws), _nbytes(ws), batch_bytes,
+        _stream(copy_stream), _stream(stream)), "wm_receive_verify")

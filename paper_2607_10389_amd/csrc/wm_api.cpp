@@ -5,6 +5,7 @@
 // are built once on the host and uploaded once per device.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 #include <map>
 #include <mutex>
@@ -18,6 +19,7 @@ using namespace wm;
 namespace {
 
 constexpr int kMaxDevices = 64;
+constexpr uint64_t kMaxBatches = 4096;  // record batches of one received payload
 
 struct DeviceState {
   bool ready = false;
@@ -362,6 +364,127 @@ wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t 
     return WM_ERR_HIP;
   *n_dirty_host = v[1];
   return v[0] == 0 ? WM_OK : WM_VERIFY_FAILED;
+}
+
+}  // extern "C"
+
+namespace {
+
+uint32_t host_u32(const uint8_t *p) {
+  return (uint32_t)p[0] | (uint32_t)p[1] << 8 | (uint32_t)p[2] << 16 | (uint32_t)p[3] << 24;
+}
+uint64_t host_u64(const uint8_t *p) { return host_u32(p) | (uint64_t)host_u32(p + 4) << 32; }
+
+struct Batch {
+  uint64_t b0, b1;  // payload bytes [b0, b1)
+  uint32_t r0, r1;  // records [r0, r1)
+};
+
+// Copy schedule of a payload held in host memory: the header and the table
+// first, then the records in batches of about batch_bytes.  Only the order
+// of the copies depends on these host reads; whether the payload is valid is
+// decided on the device.  A header or table that does not parse gives one
+// batch of everything.
+std::vector<Batch> receive_schedule(const uint8_t *h, uint64_t bytes, uint32_t n_chunks,
+                                    uint64_t batch_bytes, uint64_t *table_off) {
+  std::vector<Batch> out;
+  uint32_t n_rec = 0;
+  uint64_t total = 0;
+  bool ok = bytes >= 64;
+  if (ok) {
+    n_rec = host_u32(h + 24);
+    total = host_u64(h + 32);
+    ok = n_rec <= n_chunks && total <= bytes && 64u + 16ull * n_rec <= total;
+  }
+  if (!ok) {
+    *table_off = bytes;
+    out.push_back(Batch{0, bytes, 0, n_chunks});
+    return out;
+  }
+  const uint64_t toff = total - 16ull * n_rec;
+  *table_off = toff;
+  batch_bytes = std::max<uint64_t>(batch_bytes, (toff - 64u) / kMaxBatches + 1u);
+  auto rec_off = [&](uint32_t r) {  // clamped into the record area
+    const uint64_t o = host_u64(h + toff + 16ull * r + 8);
+    return std::min(std::max<uint64_t>(o, 64u), toff);
+  };
+  uint64_t b0 = 64;
+  uint32_t r0 = 0;
+  while (r0 < n_rec) {
+    uint32_t r1 = r0 + 1;
+    uint64_t b1 = r1 < n_rec ? std::max(rec_off(r1), b0) : toff;
+    while (r1 < n_rec && b1 - b0 < batch_bytes) {
+      ++r1;
+      b1 = r1 < n_rec ? std::max(rec_off(r1), b0) : toff;
+    }
+    out.push_back(Batch{b0, b1, r0, r1});
+    b0 = b1;
+    r0 = r1;
+  }
+  return out;
+}
+
+}  // namespace
+
+extern "C" {
+
+wm_status wm_receive_verify(const void *host_payload, uint64_t payload_bytes, void *payload,
+                            uint64_t payload_cap, uint64_t nbytes, const wm_params *p,
+                            void *staging, uint64_t staging_cap, uint32_t *verdict,
+                            uint32_t *rec_status, void *ws, uint64_t ws_bytes,
+                            uint64_t batch_bytes, void *copy_stream, void *stream) {
+  ChunkGeom g;
+  wm_status s = make_geom(nbytes, p, &g);
+  if (s != WM_OK) return s;
+  if (nbytes & 1u) return WM_ERR_INVALID_ARG;
+  if (!payload || !verdict || !aligned16(payload)) return WM_ERR_INVALID_ARG;
+  if (payload_bytes && !host_payload) return WM_ERR_INVALID_ARG;
+  if ((staging_cap && !staging) || !aligned16(staging)) return WM_ERR_INVALID_ARG;
+  if (payload_bytes > payload_cap) return WM_ERR_CAPACITY;
+  WsLayout L = ws_layout(g.n_chunks);
+  if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
+  int n_cu = 0;
+  if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  const uint8_t *h = static_cast<const uint8_t *>(host_payload);
+  uint8_t *d = static_cast<uint8_t *>(payload);
+  uint64_t table_off = payload_bytes;
+  const std::vector<Batch> batches =
+      receive_schedule(h, payload_bytes, g.n_chunks, batch_bytes, &table_off);
+  hipStream_t cs = reinterpret_cast<hipStream_t>(copy_stream);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  std::vector<hipEvent_t> ev;
+  auto arrived = [&]() -> bool {  // stream waits for the copies enqueued so far
+    hipEvent_t e;
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return false;
+    ev.push_back(e);
+    return hipEventRecord(e, cs) == hipSuccess && hipStreamWaitEvent(st, e, 0) == hipSuccess;
+  };
+  auto copy = [&](uint64_t b0, uint64_t b1) {
+    return b1 <= b0 ||
+           hipMemcpyAsync(d + b0, h + b0, b1 - b0, hipMemcpyHostToDevice, cs) == hipSuccess;
+  };
+  bool ok = true;
+  const bool parsed = !(batches.size() == 1 && batches[0].b0 == 0);
+  if (parsed) {
+    // the header and the table (which the checks and every batch read)
+    // first, then the records batch by batch
+    ok = copy(0, 64) && copy(table_off, payload_bytes) && arrived() &&
+         launch_decode_begin(payload, payload_bytes, g, staging_cap, ws, L, stream) == 0;
+    for (size_t i = 0; ok && i < batches.size(); ++i) {
+      const Batch &b = batches[i];
+      ok = copy(b.b0, b.b1) && arrived() &&
+           launch_decode_records(payload, g, staging, rec_status, ws, L, n_cu, b.r0, b.r1,
+                                 stream) == 0;
+    }
+  } else {
+    ok = copy(0, payload_bytes) && arrived() &&
+         launch_decode_begin(payload, payload_bytes, g, staging_cap, ws, L, stream) == 0 &&
+         launch_decode_records(payload, g, staging, rec_status, ws, L, n_cu, 0u, g.n_chunks,
+                               stream) == 0;
+  }
+  ok = ok && launch_decode_end(g, verdict, ws, L, stream) == 0;
+  for (hipEvent_t e : ev) hipEventDestroy(e);  // released once the waits are satisfied
+  return ok ? WM_OK : WM_ERR_HIP;
 }
 
 }  // extern "C"

@@ -102,6 +102,15 @@ int launch_decode(const void *payload, uint64_t payload_cap,
                   const ChunkGeom &g, void *staging, uint64_t staging_cap,
                   uint32_t *verdict, uint32_t *rec_status, void *ws,
                   const WsLayout &L, int n_cu, void *stream);
+// The three parts of launch_decode, for a payload decoded in record batches:
+// header and table checks, records [r0, r1), table CRC and verdict.
+int launch_decode_begin(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
+                        uint64_t staging_cap, void *ws, const WsLayout &L, void *stream);
+int launch_decode_records(const void *payload, const ChunkGeom &g, void *staging,
+                          uint32_t *rec_status, void *ws, const WsLayout &L, int n_cu,
+                          uint32_t r0, uint32_t r1, void *stream);
+int launch_decode_end(const ChunkGeom &g, uint32_t *verdict, void *ws, const WsLayout &L,
+                      void *stream);
 int launch_commit(void *live, const ChunkGeom &g, const void *staging,
                   const void *payload, const uint32_t *verdict, int n_cu,
                   void *stream);

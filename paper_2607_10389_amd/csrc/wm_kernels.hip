@@ -1812,9 +1812,11 @@ __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, co
   return bad;
 }
 
+// Decodes records [r0, r1) of the table (clamped to its length), so that a
+// payload arriving in batches can be decoded batch by batch.
 __global__ __launch_bounds__(kDecThreads) void k_decode(
     const uint8_t *__restrict__ payload, ChunkGeom g, uint8_t *__restrict__ staging,
-    uint32_t *__restrict__ rec_status, uint8_t *ws, WsLayout L) {
+    uint32_t *__restrict__ rec_status, uint8_t *ws, WsLayout L, uint32_t r0, uint32_t r1) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(ws + L.ctl);
   uint32_t *ecrc = reinterpret_cast<uint32_t *>(ws + L.entry_crc);
   if (!uniform(ctl->hdr_ok)) return;
@@ -1830,8 +1832,9 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
   const Lane l0 = lane_info();
   uint8_t *stage = lds_at(kLdsDecEsc + l0.wave * kDecEscBytes);
   const uint32_t G = gridDim.x;
-  const uint32_t my_n = blockIdx.x < n_rec ? (n_rec - 1 - blockIdx.x) / G + 1 : 0;
-  auto rec_of = [&](uint32_t i) { return blockIdx.x + i * G; };
+  const uint32_t lo = min(r0, n_rec), n_in = min(r1, n_rec) - lo;
+  const uint32_t my_n = blockIdx.x < n_in ? (n_in - 1 - blockIdx.x) / G + 1 : 0;
+  auto rec_of = [&](uint32_t i) { return lo + blockIdx.x + i * G; };
 
   // control pipeline: in step i, records i+2 (body), i+3 (header) and i+4
   // (entry)
@@ -2093,28 +2096,44 @@ int launch_encode(int mode, const void *cur, const void *prev, const ChunkGeom &
   return 0;
 }
 
+int launch_decode_begin(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
+                        uint64_t staging_cap, void *ws, const WsLayout &L, void *stream) {
+  hipLaunchKernelGGL(k_decode_prepare, dim3(1), dim3(64), 0, S(stream),
+                     static_cast<const uint8_t *>(payload), payload_cap, g, staging_cap,
+                     static_cast<uint8_t *>(ws), L);
+  return (int)hipGetLastError();
+}
+
+int launch_decode_records(const void *payload, const ChunkGeom &g, void *staging,
+                          uint32_t *rec_status, void *ws, const WsLayout &L, int n_cu,
+                          uint32_t r0, uint32_t r1, void *stream) {
+  if (r1 <= r0 || !g.n_chunks) return 0;
+  const uint32_t grid_d = min((uint32_t)n_cu, min(r1 - r0, g.n_chunks));
+  hipLaunchKernelGGL(k_decode, dim3(grid_d), dim3(kDecThreads), kLdsDecode, S(stream),
+                     static_cast<const uint8_t *>(payload), g, static_cast<uint8_t *>(staging),
+                     rec_status, static_cast<uint8_t *>(ws), L, r0, r1);
+  return (int)hipGetLastError();
+}
+
 int launch_decode(const void *payload, uint64_t payload_cap, const ChunkGeom &g, void *staging,
                   uint64_t staging_cap, uint32_t *verdict, uint32_t *rec_status, void *ws,
                   const WsLayout &L, int n_cu, void *stream) {
+  int rc = launch_decode_begin(payload, payload_cap, g, staging_cap, ws, L, stream);
+  if (rc) return rc;
+  rc = launch_decode_records(payload, g, staging, rec_status, ws, L, n_cu, 0u, g.n_chunks, stream);
+  if (rc) return rc;
+  return launch_decode_end(g, verdict, ws, L, stream);
+}
+
+int launch_decode_end(const ChunkGeom &g, uint32_t *verdict, void *ws, const WsLayout &L,
+                      void *stream) {
   uint8_t *wsb = static_cast<uint8_t *>(ws);
-  const uint8_t *pl = static_cast<const uint8_t *>(payload);
-  hipLaunchKernelGGL(k_decode_prepare, dim3(1), dim3(64), 0, S(stream), pl, payload_cap, g,
-                     staging_cap, wsb, L);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return (int)e;
-  if (g.n_chunks) {
-    uint32_t grid_d = min((uint32_t)n_cu, g.n_chunks);
-    hipLaunchKernelGGL(k_decode, dim3(grid_d), dim3(kDecThreads), kLdsDecode, S(stream), pl,
-                       g, static_cast<uint8_t *>(staging), rec_status, wsb, L);
-    e = hipGetLastError();
-    if (e != hipSuccess) return (int)e;
-  }
   WsCtl *ctl = reinterpret_cast<WsCtl *>(wsb + L.ctl);
   uint32_t *computed = reinterpret_cast<uint32_t *>(wsb + L.ctl) + 60;
   CombineJobs jobs = {};
   jobs.job[0] = CombineJob{reinterpret_cast<const uint32_t *>(wsb + L.entry_crc), &ctl->n_rec,
                            0u, 4u, 16u, g.crc_kind, computed};
-  int rc = launch_combine(jobs, 1, stream);
+  const int rc = launch_combine(jobs, 1, stream);
   if (rc) return rc;
   hipLaunchKernelGGL(k_decode_verdict, dim3(1), dim3(1), 0, S(stream), wsb, L, computed,
                      verdict);

@@ -79,6 +79,15 @@ class Mover:
         return _wm.commit_or_abort(live, self.nbytes, self.p, self.staging, pl,
                                    self.verdict, mode, self.stream)
 
+    def receive(self, host_payload: torch.Tensor, payload_bytes: int,
+                batch_bytes: int, copy_stream):
+        """Copy a payload from host memory into self.payload in batches on
+        copy_stream, decoding and verifying each batch on self.stream as it
+        lands (the verdict as after decode())."""
+        _wm.receive_verify(host_payload, payload_bytes, self.payload, self.nbytes,
+                           self.p, self.staging, self.verdict, self.rec_status,
+                           self.ws_dst, batch_bytes, copy_stream, self.stream)
+
     # ---- iterative pre-copy
     def precopy_round(self, cur: torch.Tensor, shipped: torch.Tensor,
                       dest: torch.Tensor) -> tuple[int, int]:

@@ -74,6 +74,8 @@ def lib():
     L.wm_manifest_ws_bytes.argtypes = [u32]
     L.wm_flatten.argtypes = [lp, u32, vp, u64, vp, u64, vp]
     L.wm_rehydrate.argtypes = [vp, u64, lp, u32, vp, u64, vp]
+    L.wm_receive_verify.argtypes = [vp, u64, vp, u64, u64, pp, vp, u64, vp, vp, vp, u64, u64,
+                                    vp, vp]
     L.wm_precopy_round.argtypes = [vp, vp, vp, u64, pp, ctypes.POINTER(MoveBuffers),
                                    ctypes.POINTER(u32), vp]
     for name in declared():
@@ -92,7 +94,7 @@ def test_header_declares_the_boundary():
     for must in ("wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_decode_verify",
                  "wm_commit_or_abort", "wm_flatten", "wm_rehydrate"):
         assert must in names
-    assert len(names) == len(set(names)) == 15
+    assert len(names) == len(set(names)) == 16
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -236,3 +238,22 @@ def test_precopy_round_argument_checks(lib):
                None) == CAPACITY
     assert rnd(cur, shp, dst, nb + 1, P(), bufs(), ctypes.byref(n), None) == INVALID
     assert rnd(cur, shp, dst, nb, P(chunk=4096), bufs(), ctypes.byref(n), None) == UNSUPPORTED
+
+
+def test_receive_verify_argument_checks(lib):
+    a = ALIGNED
+    nb = 4 * CH
+    ws = lib.wm_workspace_bytes(nb, P())
+    host = ctypes.create_string_buffer(4096)
+    h = ctypes.addressof(host)
+    rv = lib.wm_receive_verify
+    # (host, bytes, payload, cap, nbytes, p, staging, staging_cap, verdict, rec_status,
+    #  ws, ws_bytes, batch, copy_stream, stream)
+    assert rv(h, 4096, a, 4095, nb, P(), a, nb, a, None, a, ws, 0, None, None) == CAPACITY
+    assert rv(None, 4096, a, 4096, nb, P(), a, nb, a, None, a, ws, 0, None, None) == INVALID
+    assert rv(h, 4096, a + 4, 4096, nb, P(), a, nb, a, None, a, ws, 0, None, None) == INVALID
+    assert rv(h, 4096, a, 4096, nb, P(), a, nb, None, None, a, ws, 0, None, None) == INVALID
+    assert rv(h, 4096, a, 4096, nb + 1, P(), a, nb, a, None, a, ws, 0, None, None) == INVALID
+    assert rv(h, 4096, a, 4096, nb, P(), a + 8, nb, a, None, a, ws, 0, None, None) == INVALID
+    assert rv(h, 4096, a, 4096, nb, P(), a, nb, a, None, a, ws - 1, 0, None, None) == WORKSPACE
+    assert rv(h, 4096, a, 4096, nb, P(codec=3), a, nb, a, None, a, ws, 0, None, None) == INVALID
