@@ -199,7 +199,8 @@ def receive_runs(torch, m_src, nbytes, crc, dev):
             ec.record(cs)
             e.record(main)
             e.synchronize()
-            tot += s.elapsed_time(e)
+            ec.synchronize()
+            tot += max(s.elapsed_time(e), s.elapsed_time(ec))
             tail += ec.elapsed_time(e)
         return tot / reps, tail / reps
 
