@@ -310,13 +310,21 @@ typedef struct {
  *   shipped, dest : nbytes each, 16-byte aligned, distinct from cur and
  *              from each other; equal to each other before the first round
  *              (e.g. both zero) and kept equal by every round
+ *   crc_valid  : 0: every chunk of cur is checksummed in the encoding pass
+ *              (wm_encode_step).  1: b->crc holds the CRCs of shipped's
+ *              chunks, as the previous round that returned WM_OK on the same
+ *              buffers left them; the round then runs wm_diff_dirty and
+ *              checksums and encodes only the dirty chunks (each record's
+ *              receipt and bytes from one read), and the header's global CRC
+ *              combines kept and new CRCs.  After a round that did not return
+ *              WM_OK, pass 0.
  * Errors: those of the four calls it makes (WM_ERR_INVALID_ARG for a
  *         missing buffer, WM_ERR_CAPACITY for a short payload or staging,
  *         WM_ERR_WORKSPACE, WM_ERR_HIP). */
 wm_status wm_precopy_round(const void *cur, void *shipped, void *dest,
                            uint64_t nbytes, const wm_params *p,
-                           const wm_move_buffers *b, uint32_t *n_dirty_host,
-                           void *stream);
+                           const wm_move_buffers *b, uint32_t crc_valid,
+                           uint32_t *n_dirty_host, void *stream);
 
 #ifdef __cplusplus
 }

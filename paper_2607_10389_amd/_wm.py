@@ -101,7 +101,7 @@ def _load():
         "wm_rehydrate": ([vp, u64, lp, u32, vp, u64, vp], ctypes.c_int32),
         "wm_receive_verify": ([vp, u64, vp, u64, u64, pp, vp, u64, vp, vp, vp, u64,
                                u64, vp, vp], ctypes.c_int32),
-        "wm_precopy_round": ([vp, vp, vp, u64, pp, ctypes.POINTER(MoveBuffers),
+        "wm_precopy_round": ([vp, vp, vp, u64, pp, ctypes.POINTER(MoveBuffers), u32,
                               ctypes.POINTER(u32), vp], ctypes.c_int32),
     }
     for name, (args, res) in sig.items():
@@ -265,12 +265,13 @@ def move_buffers(crc, global_crc, dirty_idx, n_dirty, payload, payload_bytes,
 
 
 def precopy_round(cur, shipped, dest, nbytes, p, bufs: MoveBuffers,
-                  stream=None) -> tuple[int, int]:
+                  crc_valid: bool = False, stream=None) -> tuple[int, int]:
     """(status, dirty count) of one pre-copy round; waits for the stream."""
     n = ctypes.c_uint32(0)
     st = _check(LIB.wm_precopy_round(_p(cur), _p(shipped), _p(dest), nbytes,
                                      ctypes.byref(p), ctypes.byref(bufs),
-                                     ctypes.byref(n), _stream(stream)),
+                                     1 if crc_valid else 0, ctypes.byref(n),
+                                     _stream(stream)),
                 "wm_precopy_round")
     return st, int(n.value)
 

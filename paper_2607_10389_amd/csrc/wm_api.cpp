@@ -324,27 +324,48 @@ wm_status wm_rehydrate(const void *flat, uint64_t flat_cap, const wm_leaf *leave
 extern "C" {
 
 wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t nbytes,
-                           const wm_params *p, const wm_move_buffers *b,
+                           const wm_params *p, const wm_move_buffers *b, uint32_t crc_valid,
                            uint32_t *n_dirty_host, void *stream) {
   ChunkGeom g;
   wm_status s = make_geom(nbytes, p, &g);
   if (s != WM_OK) return s;
-  if (nbytes & 1u) return WM_ERR_INVALID_ARG;
+  if ((nbytes & 1u) || crc_valid > 1) return WM_ERR_INVALID_ARG;
   if (!b || !n_dirty_host || !b->crc || !b->dirty_idx || !b->n_dirty) return WM_ERR_INVALID_ARG;
   if (nbytes && (!cur || !shipped || !dest)) return WM_ERR_INVALID_ARG;
   if (nbytes && (cur == shipped || cur == dest || shipped == dest)) return WM_ERR_INVALID_ARG;
   if (!aligned16(shipped) || !aligned16(dest)) return WM_ERR_INVALID_ARG;
-  // the checks of the destination-side calls come first, so that an
+  // the checks of every call the round makes come first, so that an
   // argument error leaves everything untouched
+  if (!b->payload || !b->payload_bytes || !aligned16(b->payload) || !aligned16(cur))
+    return WM_ERR_INVALID_ARG;
+  if (b->payload_cap < wm_payload_bound(nbytes, g.n_chunks, p)) return WM_ERR_CAPACITY;
+  if (!b->ws_src || !aligned16(b->ws_src) || b->ws_src_bytes < ws_layout(g.n_chunks).total)
+    return WM_ERR_WORKSPACE;
   if (!b->verdict || (nbytes && !b->staging) || !aligned16(b->staging)) return WM_ERR_INVALID_ARG;
   if (b->staging_cap < (uint64_t)g.n_chunks * kChunk) return WM_ERR_CAPACITY;
   const uint64_t ws_need = ws_layout(g.n_chunks).total;
   if (!b->ws_dst || !aligned16(b->ws_dst) || b->ws_dst_bytes < ws_need || b->ws_src == b->ws_dst)
     return WM_ERR_WORKSPACE;
-  s = wm_encode_step(cur, shipped, nbytes, p, b->crc, b->global_crc, b->dirty_idx, b->n_dirty,
-                     b->payload, b->payload_cap, b->payload_bytes, b->ws_src, b->ws_src_bytes,
-                     stream);
-  if (s != WM_OK) return s;
+  if (!crc_valid) {
+    // every chunk checksummed, the dirty ones encoded, in one pass
+    s = wm_encode_step(cur, shipped, nbytes, p, b->crc, b->global_crc, b->dirty_idx, b->n_dirty,
+                       b->payload, b->payload_cap, b->payload_bytes, b->ws_src, b->ws_src_bytes,
+                       stream);
+    if (s != WM_OK) return s;
+  } else {
+    // the CRCs of clean chunks are those of shipped, kept from earlier
+    // rounds: diff, then checksum and encode only the dirty chunks (each
+    // CRC from the same read as its record)
+    s = wm_diff_dirty(cur, shipped, nbytes, p, b->dirty_idx, b->n_dirty, b->ws_src,
+                      b->ws_src_bytes, stream);
+    if (s != WM_OK) return s;
+    int n_cu0 = 0;
+    if ((s = ensure_device(&n_cu0)) != WM_OK) return s;
+    if (launch_encode(0, cur, nullptr, g, b->dirty_idx, b->n_dirty, nullptr, b->crc,
+                      b->global_crc, nullptr, nullptr, b->payload, b->payload_bytes, b->ws_src,
+                      ws_layout(g.n_chunks), n_cu0, stream) != 0)
+      return WM_ERR_HIP;
+  }
   s = wm_decode_verify(b->payload, b->payload_cap, nbytes, p, b->staging, b->staging_cap,
                        b->verdict, b->rec_status, b->ws_dst, b->ws_dst_bytes, stream);
   if (s != WM_OK) return s;

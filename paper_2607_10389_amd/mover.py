@@ -39,9 +39,14 @@ class Mover:
         self.verdict = torch.zeros(1, **u32)
         self.rec_status = torch.zeros(max(n, 1), **u32)
         self._bufs = None
+        # self.crc holds the CRCs of the last pre-copy round's shipped
+        # snapshot (set by a round that returned WM_OK, cleared by any other
+        # call that writes self.crc)
+        self._crc_of_shipped = None
 
     # ---- source side
     def checksum(self, state: torch.Tensor):
+        self._crc_of_shipped = None
         _wm.checksum_chunks(state, self.nbytes, self.p, self.crc,
                             self.global_crc, self.stream)
 
@@ -54,10 +59,12 @@ class Mover:
         idx = self.dirty_idx if dirty_only else None
         n_idx = self.n_dirty if dirty_only else None
         crc = self.crc if (with_crc or dirty_only) else None
+        self._crc_of_shipped = None
         _wm.encode(state, self.nbytes, self.p, idx, n_idx, crc, self.payload,
                    self.payload_bytes, self.ws_src, self.stream)
 
     def encode_step(self, cur: torch.Tensor, prev: torch.Tensor | None):
+        self._crc_of_shipped = None
         _wm.encode_step(cur, prev, self.nbytes, self.p, self.crc,
                         self.global_crc, self.dirty_idx, self.n_dirty,
                         self.payload, self.payload_bytes, self.ws_src,
@@ -92,14 +99,22 @@ class Mover:
     def precopy_round(self, cur: torch.Tensor, shipped: torch.Tensor,
                       dest: torch.Tensor) -> tuple[int, int]:
         """One round (diff against shipped, encode, decode, verify, install
-        into dest and shipped); returns (status, dirty chunks)."""
+        into dest and shipped); returns (status, dirty chunks).  After a
+        successful round on the same shipped buffer, the next one checksums
+        only its dirty chunks."""
         if self._bufs is None:
             self._bufs = _wm.move_buffers(
                 self.crc, self.global_crc, self.dirty_idx, self.n_dirty,
                 self.payload, self.payload_bytes, self.staging, self.verdict,
                 self.rec_status, self.ws_src, self.ws_dst)
-        return _wm.precopy_round(cur, shipped, dest, self.nbytes, self.p,
-                                 self._bufs, self.stream)
+        valid = self._crc_of_shipped is not None and \
+            self._crc_of_shipped == (shipped.data_ptr(), dest.data_ptr())
+        self._crc_of_shipped = None
+        st, n = _wm.precopy_round(cur, shipped, dest, self.nbytes, self.p,
+                                  self._bufs, valid, self.stream)
+        if st == _wm.WM_OK:
+            self._crc_of_shipped = (shipped.data_ptr(), dest.data_ptr())
+        return st, n
 
     # ---- host views (synchronising)
     def payload_host(self):

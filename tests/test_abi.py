@@ -76,7 +76,7 @@ def lib():
     L.wm_rehydrate.argtypes = [vp, u64, lp, u32, vp, u64, vp]
     L.wm_receive_verify.argtypes = [vp, u64, vp, u64, u64, pp, vp, u64, vp, vp, vp, u64, u64,
                                     vp, vp]
-    L.wm_precopy_round.argtypes = [vp, vp, vp, u64, pp, ctypes.POINTER(MoveBuffers),
+    L.wm_precopy_round.argtypes = [vp, vp, vp, u64, pp, ctypes.POINTER(MoveBuffers), u32,
                                    ctypes.POINTER(u32), vp]
     for name in declared():
         if name not in ("wm_status_str", "wm_workspace_bytes", "wm_payload_bound",
@@ -220,24 +220,27 @@ def test_precopy_round_argument_checks(lib):
     n = ctypes.c_uint32(0)
     cur, shp, dst = a + 0x500000, a + 0x600000, a + 0x700000
     rnd = lib.wm_precopy_round
-    assert rnd(cur, shp, dst, nb, P(), None, ctypes.byref(n), None) == INVALID
-    assert rnd(cur, shp, dst, nb, P(), bufs(), None, None) == INVALID
-    assert rnd(cur, shp, shp, nb, P(), bufs(), ctypes.byref(n), None) == INVALID
-    assert rnd(cur, cur, dst, nb, P(), bufs(), ctypes.byref(n), None) == INVALID
-    assert rnd(cur, shp + 8, dst, nb, P(), bufs(), ctypes.byref(n), None) == INVALID
-    assert rnd(cur, shp, None, nb, P(), bufs(), ctypes.byref(n), None) == INVALID
-    assert rnd(cur, shp, dst, nb, P(), bufs(verdict=None), ctypes.byref(n), None) == INVALID
-    assert rnd(cur, shp, dst, nb, P(), bufs(n_dirty=None), ctypes.byref(n), None) == INVALID
-    assert rnd(cur, shp, dst, nb, P(), bufs(staging_cap=nb - CH), ctypes.byref(n),
+    assert rnd(cur, shp, dst, nb, P(), None, 0, ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, dst, nb, P(), bufs(), 0, None, None) == INVALID
+    assert rnd(cur, shp, shp, nb, P(), bufs(), 0, ctypes.byref(n), None) == INVALID
+    assert rnd(cur, cur, dst, nb, P(), bufs(), 0, ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp + 8, dst, nb, P(), bufs(), 0, ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, None, nb, P(), bufs(), 0, ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, dst, nb, P(), bufs(verdict=None), 0, ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, dst, nb, P(), bufs(n_dirty=None), 0, ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, dst, nb, P(), bufs(staging_cap=nb - CH), 0, ctypes.byref(n),
                None) == CAPACITY
-    assert rnd(cur, shp, dst, nb, P(), bufs(ws_dst_bytes=ws - 1), ctypes.byref(n),
+    assert rnd(cur, shp, dst, nb, P(), bufs(ws_dst_bytes=ws - 1), 0, ctypes.byref(n),
                None) == WORKSPACE
-    assert rnd(cur, shp, dst, nb, P(), bufs(ws_dst=a + 0x300000), ctypes.byref(n),
+    assert rnd(cur, shp, dst, nb, P(), bufs(ws_dst=a + 0x300000), 0, ctypes.byref(n),
                None) == WORKSPACE
-    assert rnd(cur, shp, dst, nb, P(), bufs(payload_cap=bound - 1), ctypes.byref(n),
+    assert rnd(cur, shp, dst, nb, P(), bufs(payload_cap=bound - 1), 0, ctypes.byref(n),
                None) == CAPACITY
-    assert rnd(cur, shp, dst, nb + 1, P(), bufs(), ctypes.byref(n), None) == INVALID
-    assert rnd(cur, shp, dst, nb, P(chunk=4096), bufs(), ctypes.byref(n), None) == UNSUPPORTED
+    assert rnd(cur, shp, dst, nb + 1, P(), bufs(), 0, ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, dst, nb, P(chunk=4096), bufs(), 0, ctypes.byref(n), None) == UNSUPPORTED
+    assert rnd(cur, shp, dst, nb, P(), bufs(), 2, ctypes.byref(n), None) == INVALID
+    assert rnd(cur, shp, dst, nb, P(), bufs(ws_src_bytes=ws - 1), 1, ctypes.byref(n),
+               None) == WORKSPACE
 
 
 def test_receive_verify_argument_checks(lib):

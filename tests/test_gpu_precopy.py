@@ -53,6 +53,11 @@ def test_rounds_match_the_oracle_and_the_law(wm):
             # set of chunks written during the previous round
             assert np.array_equal(got, np.unique(writes.cpu().numpy()).astype(np.uint32)), k
             assert within_law(nd, n, writes.numel()), (k, nd, writes.numel())
+        # round 0 checksums every chunk; later rounds only the dirty ones
+        # and keep the rest: either way the CRCs are those of the state
+        crcs, g = oracle.checksum_chunks(0, cur_h, CH, ORACLE_THREADS)
+        assert np.array_equal(m.crc_host(), crcs), k
+        assert int(m.global_crc.cpu().numpy().view(np.uint32)[0]) == g, k
         if k in (0, 1) or nd <= 8:
             want = oracle.encode(0, cur_h, CH, got, ORACLE_THREADS)
             assert np.array_equal(m.payload_host(), want), k
