@@ -720,13 +720,15 @@ __device__ uint64_t lookback_finish(const uint64_t *status, int64_t top, Window 
 // two words at a time in 16-bit lanes: c = min((e - base) mod 2^16, esc), and
 // c + 1 carries into bit K exactly for escapes.  Per row: escm holds the
 // lane's escape flags (bit u = word u, 8 bits per row), lane_r the number of
-// the wave's escapes before the lane's first one in this row.  FULL: the
+// the wave's escapes before the lane's first one in this row; lane h of
+// row_base receives the wave's escapes before row h (its index entry).  FULL: the
 // chunk has kChunk bytes (no word needs a bounds check).
 template <uint32_t K, bool FULL>
 __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &l,
                                            uint32_t n_words, uint32_t base,
                                            uint8_t *stage, uint32_t (&escm)[2],
-                                           uint32_t (&lane_r)[kRows], uint32_t &wave_esc) {
+                                           uint32_t (&lane_r)[kRows], uint32_t &wave_esc,
+                                           uint32_t &row_base) {
   if constexpr (K == 8) {  // RAW: the exponent plane, one byte per word
 #pragma unroll
     for (int h = 0; h < kRows; ++h) {
@@ -792,6 +794,7 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
       }
     }
     lane_r[h] = wave_esc;
+    row_base = l.lane == (uint32_t)h ? wave_esc : row_base;
     if (__ballot(m8 != 0)) {
       const uint32_t cnt = __popc(m8);
       const uint32_t incl = wave_incl_scan(cnt);
@@ -1140,6 +1143,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     const uint32_t s_end = s_esc + (uint32_t)pad16(n_esc);
     uint32_t escm[2] = {0, 0};
     uint32_t lane_r[kRows];
+    uint32_t row_base = 0;
     if (is_ctl) {
       if (cur && item != 0 && l.lane == 0) {
         const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(size >> 4) << 26);
@@ -1164,9 +1168,9 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
           for (uint32_t i = l.lane; i < 32u * kbits; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
         }
         uint32_t wave_esc = 0;
-#define WM_PACK(K)                                                                   \
-  (full ? pack_codes<K, true>(d, l, n_words, base, stage, escm, lane_r, wave_esc)      \
-        : pack_codes<K, false>(d, l, n_words, base, stage, escm, lane_r, wave_esc))
+#define WM_PACK(K)                                                                        \
+  (full ? pack_codes<K, true>(d, l, n_words, base, stage, escm, lane_r, wave_esc, row_base) \
+        : pack_codes<K, false>(d, l, n_words, base, stage, escm, lane_r, wave_esc, row_base))
         switch (kbits) {
           case 1: WM_PACK(1); break;
           case 2: WM_PACK(2); break;
@@ -1208,12 +1212,14 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       uint32_t wave_base = 0;
       for (uint32_t w = 0; w < l.wave; ++w) wave_base += sh.esc_w[w];
       wave_base = uniform(wave_base);
+      {  // lane h writes the escape-index entry of the wave's row h (block
+         // wave * 8 + h, present when its first word is in the chunk)
+        const uint32_t blk = l.wave * kRows + l.lane;
+        if (l.lane < (uint32_t)kRows && blk * (kRow / 2) < n_words)
+          *reinterpret_cast<uint16_t *>(stage + s_idx + 2 * blk) = (uint16_t)(wave_base + row_base);
+      }
 #pragma unroll
       for (int h = 0; h < kRows; ++h) {
-        const uint32_t w0 = (l.off0 + h * kRow) >> 1;
-        if (l.lane == 0 && w0 < n_words)  // this row is escape-index block w0/512
-          *reinterpret_cast<uint16_t *>(stage + s_idx + 2 * (w0 >> 9)) =
-              (uint16_t)(wave_base + lane_r[h]);
         uint32_t flags = (escm[h >> 2] >> (8 * (h & 3))) & 255u;
         if (flags) {  // the lane's escaped exponents, in word order
           // exponent bytes of the row's eight words: e = high byte << 1 |
