@@ -75,6 +75,19 @@ def lib():
         L.orc_commit.argtypes = [u8p, ctypes.c_uint64, ctypes.c_uint32, u8p,
                                  u8p, ctypes.c_uint32]
         L.orc_commit.restype = ctypes.c_int
+        L.orc_encode_codec.argtypes = [ctypes.c_int, ctypes.c_int, u8p, ctypes.c_uint64,
+                                       ctypes.c_uint32, u32p, ctypes.c_uint32, u8p,
+                                       ctypes.c_uint64, ctypes.c_int]
+        L.orc_encode_codec.restype = ctypes.c_int64
+        L.orc_decode_verify_codec.argtypes = [ctypes.c_int, ctypes.c_int, u8p, ctypes.c_uint64,
+                                              ctypes.c_uint64, ctypes.c_uint32, u8p,
+                                              ctypes.c_uint64, u32p, ctypes.c_uint32,
+                                              ctypes.c_int]
+        L.orc_decode_verify_codec.restype = ctypes.c_uint32
+        L.orc_huffman_lengths.argtypes = [u32p, u8p]
+        L.orc_huffman_lengths.restype = ctypes.c_uint32
+        L.orc_plan_chunk_v2.argtypes = [u8p, ctypes.c_uint32, u32p, u32p, u32p, u32p, u64p]
+        L.orc_plan_chunk_v2.restype = ctypes.c_int
         L.orc_flat_layout.argtypes = [u64p, ctypes.c_uint32, u64p]
         L.orc_flat_layout.restype = ctypes.c_uint64
         L.orc_flatten.argtypes = [ctypes.POINTER(u8p), u64p, ctypes.c_uint32,
@@ -139,8 +152,9 @@ def payload_bound(nbytes: int, chunk: int, n_records: int) -> int:
 
 
 def encode(kind: int, state, chunk: int = 65536, idx=None,
-           threads: int = 1) -> np.ndarray:
-    """Payload bytes (uint8 array of exactly payload_bytes)."""
+           threads: int = 1, codec: int = 1) -> np.ndarray:
+    """Payload bytes (uint8 array of exactly payload_bytes); codec 1 is
+    format v1, codec 2 format v2 (Huffman-coded exponents)."""
     b = _bytes(state)
     if idx is None:
         n_rec, pidx = n_chunks(b.size, chunk), None
@@ -151,11 +165,30 @@ def encode(kind: int, state, chunk: int = 65536, idx=None,
         pidx = _p32(idx_arr) if idx_arr.size else _p32(np.zeros(1, np.uint32))
     cap = payload_bound(b.size, chunk, n_rec)
     out = np.zeros(max(cap, 64), np.uint8)
-    n = lib().orc_encode(kind, _p8(b), b.size, chunk, pidx, n_rec, _p8(out),
-                         out.size, threads)
+    n = lib().orc_encode_codec(kind, codec, _p8(b), b.size, chunk, pidx, n_rec,
+                               _p8(out), out.size, threads)
     if n < 0:
         raise ValueError(f"orc_encode failed ({n})")
     return out[:n].copy()
+
+
+def huffman_lengths(counts) -> tuple[np.ndarray, int]:
+    """Code lengths of format v2 for 256 symbol counts, and the longest."""
+    c = np.ascontiguousarray(counts, dtype=np.uint32)
+    assert c.size == 256
+    out = np.zeros(256, np.uint8)
+    k = lib().orc_huffman_lengths(_p32(c), _p8(out))
+    return out, int(k)
+
+
+def plan_chunk_v2(chunk_bytes) -> dict:
+    b = _bytes(chunk_bytes)
+    m, k, base, sb = (np.zeros(1, np.uint32) for _ in range(4))
+    size = np.zeros(1, np.uint64)
+    lib().orc_plan_chunk_v2(_p8(b), b.size, _p32(m), _p32(k), _p32(base), _p32(sb),
+                            size.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)))
+    return dict(mode=int(m[0]), k=int(k[0]), base=int(base[0]),
+                stream_bytes=int(sb[0]), size=int(size[0]))
 
 
 def plan_chunk(chunk_bytes) -> dict:
@@ -170,7 +203,7 @@ def plan_chunk(chunk_bytes) -> dict:
 
 
 def decode_verify(kind: int, payload, nbytes: int, chunk: int = 65536,
-                  staging_cap: int | None = None, threads: int = 1):
+                  staging_cap: int | None = None, threads: int = 1, codec: int = 1):
     """Returns (verdict, staging uint8 array, per-record status array)."""
     p = _bytes(payload)
     if staging_cap is None:
@@ -178,9 +211,9 @@ def decode_verify(kind: int, payload, nbytes: int, chunk: int = 65536,
     staging = np.zeros(max(staging_cap, 1), np.uint8)
     nst = max(n_chunks(nbytes, chunk), 1)
     status = np.zeros(nst, np.uint32)
-    v = lib().orc_decode_verify(kind, _p8(p), p.size, nbytes, chunk,
-                                _p8(staging), staging_cap, _p32(status), nst,
-                                threads)
+    v = lib().orc_decode_verify_codec(kind, codec, _p8(p), p.size, nbytes, chunk,
+                                      _p8(staging), staging_cap, _p32(status), nst,
+                                      threads)
     return int(v), staging[:staging_cap], status
 
 

@@ -205,6 +205,11 @@ static uint8_t sm_of(uint16_t w) {
 }
 
 static uint64_t raw_size(uint32_t n) { return 16 + 2 * pad16(n); }
+static int all_zero(const uint8_t *p, uint64_t n) {
+  for (uint64_t i = 0; i < n; i++)
+    if (p[i]) return 0;
+  return 1;
+}
 /* escape-index entries: one per block of 512 words (k >= 1 only) */
 static uint64_t index_bytes(uint32_t n, uint32_t k) {
   return k ? 2 * (((uint64_t)n + 511) / 512) : 0;
@@ -344,8 +349,285 @@ static void write_record(int kind, const uint8_t *chunk, uint32_t len,
   }
 }
 
+
+static uint32_t decode_record(int kind, const uint8_t *rec, uint64_t L,
+                              uint32_t len, uint32_t src_crc, uint8_t *out);
+
+/* ------------------------------------------------------ codec 2 (v2) -- */
+/* The paper's codec is an entropy coder over the bf16 words, whose
+ * redundancy sits in the exponent plane (§6.4).  Format v2 codes each
+ * chunk's exponents with that chunk's own canonical Huffman code (lengths at
+ * most ORC_HUF_MAX_LEN) in 512 streams, so that 512 decoders can run side
+ * by side; sign/mantissa bytes stay raw.  Records are RAW (as v1) or HUF. */
+
+#define HUF_STREAMS 512u
+
+/* Word i of stream s (s < 512, i < 64): row 8*(s/64) + i/8 of 512 words,
+ * word 8*(s%64) + i%8 of the row. */
+static uint32_t stream_word(uint32_t s, uint32_t i) {
+  return (8u * (s / 64u) + i / 8u) * 512u + 8u * (s % 64u) + i % 8u;
+}
+
+/* Huffman code lengths for the symbols with nonzero count: leaves sorted by
+ * (count, symbol); the two lightest nodes are merged repeatedly, a leaf
+ * taken before an internal node of equal weight; a symbol's length is its
+ * depth.  While the longest exceeds ORC_HUF_MAX_LEN every nonzero count c
+ * becomes (c + 1) / 2 and the code is rebuilt.  One symbol: length 0.
+ * Returns the longest length. */
+uint32_t orc_huffman_lengths(const uint32_t *count, uint8_t *len) {
+  uint64_t w[256];
+  for (int i = 0; i < 256; i++) w[i] = count[i];
+  for (;;) {
+    uint32_t sym[256], m = 0;
+    for (uint32_t i = 0; i < 256; i++) {
+      len[i] = 0;
+      if (w[i]) sym[m++] = i;
+    }
+    if (m <= 1) return 0;
+    /* insertion sort by (weight, symbol) */
+    for (uint32_t a = 1; a < m; a++) {
+      uint32_t v = sym[a], b = a;
+      while (b > 0 && (w[sym[b - 1]] > w[v] ||
+                       (w[sym[b - 1]] == w[v] && sym[b - 1] > v))) {
+        sym[b] = sym[b - 1];
+        b--;
+      }
+      sym[b] = v;
+    }
+    /* nodes 0..m-1 are the sorted leaves, m..2m-2 the merges in order */
+    uint64_t nw[511];
+    int32_t parent[511];
+    for (uint32_t i = 0; i < m; i++) nw[i] = w[sym[i]];
+    uint32_t li = 0, ii = m, n_int = m;
+    for (uint32_t t = 0; t < m - 1; t++) {
+      uint32_t pick[2];
+      for (int q = 0; q < 2; q++) {
+        if (li < m && (ii >= n_int || nw[li] <= nw[ii]))
+          pick[q] = li++;
+        else
+          pick[q] = ii++;
+      }
+      nw[n_int] = nw[pick[0]] + nw[pick[1]];
+      parent[pick[0]] = parent[pick[1]] = (int32_t)n_int;
+      n_int++;
+    }
+    uint32_t depth[511];
+    depth[n_int - 1] = 0;
+    for (int32_t i = (int32_t)n_int - 2; i >= 0; i--)
+      depth[i] = depth[parent[i]] + 1;
+    uint32_t longest = 0;
+    for (uint32_t i = 0; i < m; i++) {
+      len[sym[i]] = (uint8_t)depth[i];
+      if (depth[i] > longest) longest = depth[i];
+    }
+    if (longest <= ORC_HUF_MAX_LEN) return longest;
+    for (int i = 0; i < 256; i++)
+      if (w[i]) w[i] = (w[i] + 1) / 2;
+  }
+}
+
+/* Canonical codes (symbols ordered by (length, symbol) take consecutive
+ * values): code[s] for every symbol with len[s] > 0. */
+static void canonical_codes(const uint8_t *len, uint32_t *code) {
+  uint32_t bl[ORC_HUF_MAX_LEN + 2] = {0}, next[ORC_HUF_MAX_LEN + 2] = {0};
+  for (int s = 0; s < 256; s++) bl[len[s]]++;
+  bl[0] = 0;
+  uint32_t c = 0;
+  for (uint32_t b = 1; b <= ORC_HUF_MAX_LEN; b++) {
+    c = (c + bl[b - 1]) << 1;
+    next[b] = c;
+  }
+  for (int s = 0; s < 256; s++) code[s] = len[s] ? next[len[s]]++ : 0;
+}
+
+static uint64_t huf_size(uint32_t n, uint32_t k, uint64_t stream_bytes) {
+  if (k == 0) return 16 + pad16(n);
+  return 16 + 128 + HUF_STREAMS + pad16(stream_bytes) + pad16(n);
+}
+
+/* Bits of each stream for the given lengths; returns the total bytes. */
+static uint64_t stream_bytes_of(const uint8_t *chunk, uint32_t n,
+                                const uint8_t *len, uint8_t *sbytes) {
+  uint64_t total = 0;
+  for (uint32_t s = 0; s < HUF_STREAMS; s++) {
+    uint64_t bits = 0;
+    for (uint32_t i = 0; i < 64; i++) {
+      uint32_t wi = stream_word(s, i);
+      if (wi < n) bits += len[exponent_of(word_at(chunk, wi))];
+    }
+    sbytes[s] = (uint8_t)((bits + 7) / 8);
+    total += sbytes[s];
+  }
+  return total;
+}
+
+/* Mode choice of format v2: RAW, or HUF when strictly smaller.  HUF with a
+ * single exponent has k = 0 and base = that exponent; otherwise k is the
+ * longest code length, base 0, and n_esc carries the stream bytes. */
+int orc_plan_chunk_v2(const uint8_t *chunk, uint32_t len, uint32_t *mode,
+                      uint32_t *k, uint32_t *base, uint32_t *n_sb,
+                      uint64_t *size) {
+  uint32_t n = len / 2;
+  uint32_t count[256] = {0};
+  uint8_t lens[256], sbytes[HUF_STREAMS];
+  for (uint32_t i = 0; i < n; i++) count[exponent_of(word_at(chunk, i))]++;
+  uint32_t longest = orc_huffman_lengths(count, lens);
+  uint32_t only = 0, distinct = 0;
+  for (uint32_t e = 0; e < 256; e++)
+    if (count[e]) {
+      distinct++;
+      only = e;
+    }
+  uint64_t sb = longest ? stream_bytes_of(chunk, n, lens, sbytes) : 0;
+  uint64_t hs = huf_size(n, longest, sb);
+  *mode = 0;
+  *k = *base = *n_sb = 0;
+  *size = raw_size(n);
+  if (n && hs < *size) {
+    *mode = 2;
+    *k = longest;
+    *base = distinct == 1 ? only : 0;
+    *n_sb = (uint32_t)sb;
+    *size = hs;
+  }
+  return 0;
+}
+
+/* Write one v2 record (size bytes, already zeroed by the caller). */
+static void write_record_v2(int kind, const uint8_t *chunk, uint32_t len,
+                            uint32_t mode, uint32_t k, uint32_t base,
+                            uint32_t n_sb, uint8_t *out) {
+  uint32_t n = len / 2;
+  if (mode == 0) {
+    write_record(kind, chunk, len, 0, 0, 0, 0, out);
+    return;
+  }
+  out[0] = 2;
+  out[1] = (uint8_t)k;
+  out[2] = (uint8_t)base;
+  out[3] = 0;
+  put_u32(out + 4, n);
+  put_u32(out + 8, n_sb);
+  put_u32(out + 12, orc_crc(kind, out, 12));
+  uint8_t *body = out + 16;
+  uint8_t *sm;
+  if (k == 0) {
+    sm = body;
+  } else {
+    uint32_t count[256] = {0}, code[256];
+    uint8_t lens[256];
+    for (uint32_t i = 0; i < n; i++) count[exponent_of(word_at(chunk, i))]++;
+    orc_huffman_lengths(count, lens);
+    canonical_codes(lens, code);
+    uint8_t *ltab = body, *sbytes = body + 128, *streams = body + 128 + HUF_STREAMS;
+    for (uint32_t e = 0; e < 256; e++) ltab[e / 2] |= (uint8_t)(lens[e] << (4 * (e % 2)));
+    stream_bytes_of(chunk, n, lens, sbytes);
+    uint64_t at = 0;
+    for (uint32_t s = 0; s < HUF_STREAMS; s++) {
+      uint64_t bit = 0;
+      for (uint32_t i = 0; i < 64; i++) {
+        uint32_t wi = stream_word(s, i);
+        if (wi >= n) continue;
+        uint32_t e = exponent_of(word_at(chunk, wi));
+        /* the code's bits, most significant first, go to the stream in
+         * order; stream bit j is bit j % 8 of byte j / 8 */
+        for (int b = lens[e] - 1; b >= 0; b--, bit++)
+          if ((code[e] >> b) & 1u) streams[at + bit / 8] |= (uint8_t)(1u << (bit % 8));
+      }
+      at += sbytes[s];
+    }
+    sm = streams + pad16(at);
+  }
+  for (uint32_t i = 0; i < n; i++) sm[i] = sm_of(word_at(chunk, i));
+}
+
+/* Structure checks and decode of one v2 record (see decode_record). */
+static uint32_t decode_record_v2(int kind, const uint8_t *rec, uint64_t L,
+                                 uint32_t len, uint32_t src_crc, uint8_t *out) {
+  uint32_t n = len / 2;
+  if (L < 16) return ORC_V_RECORD;
+  if (orc_crc(kind, rec, 12) != get_u32(rec + 12)) return ORC_V_RECORD;
+  uint32_t mode = rec[0], k = rec[1], base = rec[2];
+  uint32_t n_words = get_u32(rec + 4), n_sb = get_u32(rec + 8);
+  if (rec[3] != 0 || n_words != n || (mode != 0 && mode != 2))
+    return ORC_V_RECORD;
+  if (mode == 0) return decode_record(kind, rec, L, len, src_crc, out);
+  const uint8_t *body = rec + 16, *sm;
+  uint8_t e_of[32768];
+  if (k > ORC_HUF_MAX_LEN) return ORC_V_RECORD;
+  if (k == 0) {
+    if (n_sb != 0 || L != huf_size(n, 0, 0)) return ORC_V_RECORD;
+    sm = body;
+    for (uint32_t i = 0; i < n; i++) e_of[i] = (uint8_t)base;
+  } else {
+    if (base != 0 || L != huf_size(n, k, n_sb)) return ORC_V_RECORD;
+    const uint8_t *ltab = body, *sbytes = body + 128, *streams = body + 128 + HUF_STREAMS;
+    uint8_t lens[256];
+    uint32_t longest = 0;
+    uint64_t kraft = 0; /* sum of 2^(MAX - len): a complete code fills 2^MAX */
+    for (uint32_t e = 0; e < 256; e++) {
+      lens[e] = (uint8_t)((ltab[e / 2] >> (4 * (e % 2))) & 15u);
+      if (lens[e] > k) return ORC_V_RECORD;
+      if (lens[e] > longest) longest = lens[e];
+      if (lens[e]) kraft += 1u << (ORC_HUF_MAX_LEN - lens[e]);
+    }
+    if (longest != k || kraft != (1u << ORC_HUF_MAX_LEN)) return ORC_V_RECORD;
+    uint32_t code[256];
+    canonical_codes(lens, code);
+    /* canonical decoding: per length, the first code and the symbols in
+     * code order */
+    uint32_t first[ORC_HUF_MAX_LEN + 1], cnt[ORC_HUF_MAX_LEN + 1];
+    uint32_t start[ORC_HUF_MAX_LEN + 1], order[256], m = 0;
+    for (uint32_t b = 1; b <= ORC_HUF_MAX_LEN; b++) {
+      first[b] = 0;
+      cnt[b] = 0;
+      start[b] = m;
+      for (uint32_t e = 0; e < 256; e++)
+        if (lens[e] == b) {
+          if (!cnt[b]) first[b] = code[e];
+          cnt[b]++;
+          order[m++] = e;
+        }
+    }
+    uint64_t sum = 0;
+    for (uint32_t s = 0; s < HUF_STREAMS; s++) sum += sbytes[s];
+    if (sum != n_sb) return ORC_V_RECORD;
+    uint64_t at = 0;
+    for (uint32_t s = 0; s < HUF_STREAMS; s++) {
+      const uint8_t *st = streams + at;
+      uint64_t nbits = 8ull * sbytes[s], bit = 0;
+      for (uint32_t i = 0; i < 64; i++) {
+        uint32_t wi = stream_word(s, i);
+        if (wi >= n) continue;
+        uint32_t c = 0, b = 0;
+        for (;;) {
+          if (bit >= nbits) return ORC_V_RECORD; /* ran past the stream */
+          c = (c << 1) | ((st[bit / 8] >> (bit % 8)) & 1u);
+          bit++;
+          b++;
+          if (b > k) return ORC_V_RECORD; /* cannot happen for a complete code */
+          if (cnt[b] && c - first[b] < cnt[b]) break;
+        }
+        e_of[wi] = (uint8_t)order[start[b] + (c - first[b])];
+      }
+      /* the stream is exactly its bits, rounded up to a byte of zeros */
+      if ((bit + 7) / 8 != sbytes[s]) return ORC_V_RECORD;
+      if (bit % 8 && (st[bit / 8] >> (bit % 8))) return ORC_V_RECORD;
+      at += sbytes[s];
+    }
+    if (!all_zero(streams + at, pad16(at) - at)) return ORC_V_RECORD;
+    sm = streams + pad16(at);
+  }
+  if (!all_zero(sm + n, pad16(n) - n)) return ORC_V_RECORD;
+  for (uint32_t i = 0; i < n; i++)
+    put_u16(out + 2 * (uint64_t)i,
+            (uint16_t)(((uint32_t)(sm[i] >> 7) << 15) | ((uint32_t)e_of[i] << 7) |
+                       (sm[i] & 127u)));
+  return orc_crc(kind, out, len) == src_crc ? 0u : ORC_V_DATA;
+}
+
 typedef struct {
-  int kind;
+  int kind, codec;
   const uint8_t *state;
   uint64_t nbytes;
   uint32_t chunk;
@@ -364,9 +646,14 @@ static void en_plan_range(void *vp, uint64_t lo, uint64_t hi) {
   en_ctx *x = (en_ctx *)vp;
   for (uint64_t r = lo; r < hi; r++) {
     uint64_t c = en_chunk(x, r);
-    orc_plan_chunk(x->state + c * (uint64_t)x->chunk,
-                   chunk_len(x->nbytes, x->chunk, c), &x->mode[r], &x->k[r],
-                   &x->base[r], &x->esc[r], &x->size[r]);
+    const uint8_t *src = x->state + c * (uint64_t)x->chunk;
+    uint32_t len = chunk_len(x->nbytes, x->chunk, c);
+    if (x->codec == 2)
+      orc_plan_chunk_v2(src, len, &x->mode[r], &x->k[r], &x->base[r],
+                        &x->esc[r], &x->size[r]);
+    else
+      orc_plan_chunk(src, len, &x->mode[r], &x->k[r], &x->base[r], &x->esc[r],
+                     &x->size[r]);
   }
 }
 
@@ -380,8 +667,12 @@ static void en_write_range(void *vp, uint64_t lo, uint64_t hi) {
     put_u32(entry, (uint32_t)c);
     put_u32(entry + 4, orc_crc(x->kind, src, len));
     put_u64(entry + 8, x->offset[r]);
-    write_record(x->kind, src, len, x->mode[r], x->k[r], x->base[r],
-                 x->esc[r], x->payload + x->offset[r]);
+    if (x->codec == 2)
+      write_record_v2(x->kind, src, len, x->mode[r], x->k[r], x->base[r],
+                      x->esc[r], x->payload + x->offset[r]);
+    else
+      write_record(x->kind, src, len, x->mode[r], x->k[r], x->base[r],
+                   x->esc[r], x->payload + x->offset[r]);
   }
 }
 
@@ -396,8 +687,17 @@ uint64_t orc_payload_bound(uint64_t nbytes, uint32_t chunk_bytes,
 int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
                    uint32_t chunk_bytes, const uint32_t *idx, uint32_t n_idx,
                    uint8_t *payload, uint64_t cap, int threads) {
+  return orc_encode_codec(kind, 1, state, nbytes, chunk_bytes, idx, n_idx,
+                          payload, cap, threads);
+}
+
+int64_t orc_encode_codec(int kind, int codec, const uint8_t *state,
+                         uint64_t nbytes, uint32_t chunk_bytes,
+                         const uint32_t *idx, uint32_t n_idx, uint8_t *payload,
+                         uint64_t cap, int threads) {
   if (!chunk_ok(chunk_bytes) || (kind != 0 && kind != 1) || (nbytes & 1))
     return -1;
+  if (codec != 1 && !(codec == 2 && chunk_bytes == 65536)) return -1;
   uint64_t n_chunks = n_chunks_of(nbytes, chunk_bytes);
   uint64_t n_rec = idx ? n_idx : n_chunks;
   if (n_rec > n_chunks) return -1;
@@ -408,6 +708,7 @@ int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
   uint64_t m = n_rec ? n_rec : 1;
   en_ctx x;
   x.kind = kind;
+  x.codec = codec;
   x.state = state;
   x.nbytes = nbytes;
   x.chunk = chunk_bytes;
@@ -438,10 +739,10 @@ int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
   h[0] = 'W';
   h[1] = 'M';
   h[2] = 'V';
-  h[3] = '1';
-  put_u16(h + 4, 1);
+  h[3] = codec == 2 ? '2' : '1';
+  put_u16(h + 4, (uint16_t)codec);
   h[6] = (uint8_t)kind;
-  h[7] = 1;
+  h[7] = (uint8_t)codec;
   put_u32(h + 8, chunk_bytes);
   put_u32(h + 12, (uint32_t)n_chunks);
   put_u64(h + 16, nbytes);
@@ -463,11 +764,7 @@ int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
 
 /* --------------------------------------------------------------- decode -- */
 
-static int all_zero(const uint8_t *p, uint64_t n) {
-  for (uint64_t i = 0; i < n; i++)
-    if (p[i]) return 0;
-  return 1;
-}
+
 
 /* Structure checks and decode of one record occupying rec[0..L).  Returns 0,
  * ORC_V_RECORD or ORC_V_DATA; on 0 the chunk's len bytes are in out. */
@@ -544,7 +841,7 @@ static uint32_t decode_record(int kind, const uint8_t *rec, uint64_t L,
 }
 
 typedef struct {
-  int kind;
+  int kind, codec;
   const uint8_t *payload;
   uint64_t table, nbytes;
   uint32_t chunk, n_rec;
@@ -559,10 +856,13 @@ static void de_range(void *vp, uint64_t lo, uint64_t hi) {
     uint32_t c = get_u32(e);
     uint64_t off = get_u64(e + 8);
     uint64_t end = r + 1 < x->n_rec ? get_u64(e + 16 + 8) : x->table;
-    x->status[r] = decode_record(x->kind, x->payload + off, end - off,
-                                 chunk_len(x->nbytes, x->chunk, c),
-                                 get_u32(e + 4),
-                                 x->staging + r * (uint64_t)x->chunk);
+    uint32_t len = chunk_len(x->nbytes, x->chunk, c);
+    uint8_t *out = x->staging + r * (uint64_t)x->chunk;
+    x->status[r] = x->codec == 2
+                       ? decode_record_v2(x->kind, x->payload + off, end - off,
+                                          len, get_u32(e + 4), out)
+                       : decode_record(x->kind, x->payload + off, end - off,
+                                       len, get_u32(e + 4), out);
   }
 }
 
@@ -571,16 +871,29 @@ uint32_t orc_decode_verify(int kind, const uint8_t *payload, uint64_t cap,
                            uint8_t *staging, uint64_t staging_cap,
                            uint32_t *rec_status, uint32_t n_status,
                            int threads) {
+  return orc_decode_verify_codec(kind, 1, payload, cap, nbytes, chunk_bytes,
+                                 staging, staging_cap, rec_status, n_status,
+                                 threads);
+}
+
+uint32_t orc_decode_verify_codec(int kind, int codec, const uint8_t *payload,
+                                 uint64_t cap, uint64_t nbytes,
+                                 uint32_t chunk_bytes, uint8_t *staging,
+                                 uint64_t staging_cap, uint32_t *rec_status,
+                                 uint32_t n_status, int threads) {
   if (!chunk_ok(chunk_bytes) || (kind != 0 && kind != 1)) return ORC_V_HEADER;
+  if (codec != 1 && !(codec == 2 && chunk_bytes == 65536)) return ORC_V_HEADER;
   uint64_t n_chunks = n_chunks_of(nbytes, chunk_bytes);
 
   /* header */
   if (cap < 64) return ORC_V_HEADER;
   const uint8_t *h = payload;
   if (orc_crc(kind, h, 60) != get_u32(h + 60)) return ORC_V_HEADER;
-  if (h[0] != 'W' || h[1] != 'M' || h[2] != 'V' || h[3] != '1')
+  if (h[0] != 'W' || h[1] != 'M' || h[2] != 'V' ||
+      h[3] != (codec == 2 ? '2' : '1'))
     return ORC_V_HEADER;
-  if ((h[4] | (h[5] << 8)) != 1 || h[6] != (uint8_t)kind || h[7] != 1)
+  if ((h[4] | (h[5] << 8)) != codec || h[6] != (uint8_t)kind ||
+      h[7] != (uint8_t)codec)
     return ORC_V_HEADER;
   if (get_u32(h + 8) != chunk_bytes || get_u32(h + 12) != n_chunks ||
       get_u64(h + 16) != nbytes)
@@ -614,8 +927,8 @@ uint32_t orc_decode_verify(int kind, const uint8_t *payload, uint64_t cap,
 
   /* records */
   uint32_t *status = (uint32_t *)calloc(n_rec ? n_rec : 1, 4);
-  de_ctx x = {kind,  payload, table,   nbytes, chunk_bytes,
-              n_rec, staging, status};
+  de_ctx x = {kind,  codec,   payload, table, nbytes,
+              chunk_bytes, n_rec, staging, status};
   parallel_for(n_rec, threads, de_range, &x);
   uint32_t verdict = 0;
   for (uint32_t r = 0; r < n_rec; r++) {

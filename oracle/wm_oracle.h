@@ -81,6 +81,25 @@ int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
                    uint32_t chunk_bytes, const uint32_t *idx, uint32_t n_idx,
                    uint8_t *payload, uint64_t cap, int threads);
 
+/* Format v2 (codec 2, 64 KiB chunks only): as orc_encode with records RAW
+ * or HUF (per-chunk canonical Huffman codes of the exponents in 512 streams).
+ * orc_encode is orc_encode_codec with codec 1. */
+#define ORC_HUF_MAX_LEN 11u
+int64_t orc_encode_codec(int kind, int codec, const uint8_t *state,
+                         uint64_t nbytes, uint32_t chunk_bytes,
+                         const uint32_t *idx, uint32_t n_idx, uint8_t *payload,
+                         uint64_t cap, int threads);
+
+/* Huffman code lengths (at most ORC_HUF_MAX_LEN) of 256 symbol counts;
+ * returns the longest (0 when at most one symbol occurs). */
+uint32_t orc_huffman_lengths(const uint32_t *count, uint8_t *len);
+
+/* Plan of one v2 record: mode (0 RAW, 2 HUF), k (longest code length),
+ * base (the only exponent when k = 0), n_sb (stream bytes), size. */
+int orc_plan_chunk_v2(const uint8_t *chunk, uint32_t len, uint32_t *mode,
+                      uint32_t *k, uint32_t *base, uint32_t *n_sb,
+                      uint64_t *size);
+
 /* Plan of one chunk's record (exposed for tests): mode, k, base, n_esc and
  * record size in bytes. */
 int orc_plan_chunk(const uint8_t *chunk, uint32_t len, uint32_t *mode,
@@ -95,6 +114,13 @@ uint32_t orc_decode_verify(int kind, const uint8_t *payload, uint64_t cap,
                            uint8_t *staging, uint64_t staging_cap,
                            uint32_t *rec_status, uint32_t n_status,
                            int threads);
+
+/* orc_decode_verify for either format (codec 1 or 2). */
+uint32_t orc_decode_verify_codec(int kind, int codec, const uint8_t *payload,
+                                 uint64_t cap, uint64_t nbytes,
+                                 uint32_t chunk_bytes, uint8_t *staging,
+                                 uint64_t staging_cap, uint32_t *rec_status,
+                                 uint32_t n_status, int threads);
 
 /* Install: verdict 0 copies each staged record to its chunk of live and
  * returns 0; any other verdict leaves live untouched and returns 1. */

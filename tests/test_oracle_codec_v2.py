@@ -1,0 +1,162 @@
+"""Pins of the oracle's format v2 (codec 2): per-chunk canonical Huffman
+codes of the bf16 exponent plane (the plane that carries the redundancy,
+§6.4), code lengths at most 11, 512 streams per chunk.  The Huffman lengths
+are checked against an independent optimal-cost computation, the Kraft
+equality and a hand-worked example; payloads round-trip and every single
+flipped bit of a small payload aborts."""
+import heapq
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+
+CH = 65536
+MAXLEN = 11
+
+
+def optimal_cost(counts):
+    """Total bits of an optimal prefix code (sum of all merge weights)."""
+    h = [c for c in counts if c > 0]
+    if len(h) <= 1:
+        return 0
+    heapq.heapify(h)
+    cost = 0
+    while len(h) > 1:
+        a, b = heapq.heappop(h), heapq.heappop(h)
+        cost += a + b
+        heapq.heappush(h, a + b)
+    return cost
+
+
+def test_hand_worked_lengths():
+    # counts a=5 (sym 10), b=2 (sym 20), c=1 (sym 30), d=1 (sym 40): merge
+    # c+d (2); b and that node tie at 2 and the leaf goes first, merge to 4;
+    # then 4 and a=5: lengths a 1, b 2, c 3, d 3
+    counts = np.zeros(256, np.uint32)
+    counts[[10, 20, 30, 40]] = [5, 2, 1, 1]
+    lens, k = oracle.huffman_lengths(counts)
+    assert k == 3
+    assert {i: int(lens[i]) for i in np.nonzero(lens)[0]} == {10: 1, 20: 2, 30: 3, 40: 3}
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_lengths_are_optimal_and_complete(seed):
+    rng = np.random.default_rng(seed)
+    m = int(rng.integers(2, 40))
+    counts = np.zeros(256, np.uint32)
+    syms = rng.choice(256, m, replace=False)
+    counts[syms] = rng.integers(1, 5000, m)
+    lens, k = oracle.huffman_lengths(counts)
+    assert set(np.nonzero(lens)[0]) == set(syms)
+    assert sum(2.0 ** -int(lens[s]) for s in syms) == 1.0  # Kraft equality
+    cost = int((counts.astype(np.int64) * lens).sum())
+    if k < MAXLEN:  # no length limiting happened: the code is optimal
+        assert cost == optimal_cost(counts)
+        assert k == int(lens.max())
+
+
+def test_length_limit():
+    # Fibonacci counts force depth ~ number of symbols in an unlimited code
+    counts = np.zeros(256, np.uint32)
+    fib = [1, 1]
+    while len(fib) < 24:
+        fib.append(fib[-1] + fib[-2])
+    counts[:24] = fib
+    lens, k = oracle.huffman_lengths(counts)
+    assert k == MAXLEN and int(lens.max()) == MAXLEN
+    assert sum(2.0 ** -int(l) for l in lens if l) == 1.0
+
+
+def test_degenerate_counts():
+    counts = np.zeros(256, np.uint32)
+    assert oracle.huffman_lengths(counts)[1] == 0
+    counts[77] = 1000
+    lens, k = oracle.huffman_lengths(counts)
+    assert k == 0 and not lens.any()
+
+
+def bf16_state(rng, n_words, sigma=1.0):
+    x = (rng.standard_normal(n_words) * sigma).astype(np.float32)
+    return (x.view(np.uint32) >> 16).astype(np.uint16).view(np.uint8)
+
+
+@pytest.mark.parametrize("n_chunks_", [1, 3])
+def test_round_trip_and_ratio(n_chunks_):
+    rng = np.random.default_rng(1)
+    st = bf16_state(rng, n_chunks_ * CH // 2 - 2768)  # short last chunk
+    p1 = oracle.encode(0, st, CH, None, 4, codec=1)
+    p2 = oracle.encode(0, st, CH, None, 4, codec=2)
+    v, stg, rs = oracle.decode_verify(0, p2, st.size, CH, None, 4, codec=2)
+    assert v == 0 and not rs.any()
+    assert np.array_equal(stg[: st.size], st)
+    assert p2[:4].tobytes() == b"WMV2" and p2[7] == 2
+    assert p2.size < p1.size
+    # a v2 payload is not a v1 payload and vice versa
+    assert oracle.decode_verify(0, p2, st.size, CH, None, 4, codec=1)[0] == 1
+    assert oracle.decode_verify(0, p1, st.size, CH, None, 4, codec=2)[0] == 1
+
+
+def test_stream_bits_within_entropy_bounds():
+    rng = np.random.default_rng(2)
+    # normal values with magnitudes clipped to [2^-6, 2^6): a dozen
+    # exponents, no code longer than 11 bits
+    x = rng.standard_normal(CH // 2).astype(np.float32) * 3
+    x = np.sign(x) * np.clip(np.abs(x), 2.0 ** -6, 63.0)
+    st = (x.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16).view(np.uint8)
+    w = st.view(np.uint16)
+    e = (w >> 7) & 255
+    counts = np.bincount(e, minlength=256)
+    lens, k = oracle.huffman_lengths(counts)
+    assert k < MAXLEN
+    p = counts[counts > 0] / w.size
+    H = -(p * np.log2(p)).sum()
+    bits = int((counts * lens).sum())
+    assert H * w.size <= bits <= (H + 1) * w.size
+    plan = oracle.plan_chunk_v2(st)
+    # streams are byte-padded each: between the bits and bits + 7 per stream
+    assert bits / 8 <= plan["stream_bytes"] <= bits / 8 + 512
+    assert plan["mode"] == 2 and plan["k"] == k
+    assert plan["size"] == 16 + 128 + 512 + -(-plan["stream_bytes"] // 16) * 16 + w.size
+
+
+def test_constant_and_random_chunks():
+    n = CH // 2
+    const = np.full(n, 0x3F80, np.uint16).view(np.uint8)  # 1.0 everywhere
+    plan = oracle.plan_chunk_v2(const)
+    assert plan == dict(mode=2, k=0, base=127, stream_bytes=0, size=16 + n)
+    rng = np.random.default_rng(3)
+    rnd = rng.integers(0, 1 << 16, n, dtype=np.uint16).view(np.uint8)
+    assert oracle.plan_chunk_v2(rnd) == dict(mode=0, k=0, base=0, stream_bytes=0,
+                                             size=16 + 2 * n)
+    for st in (const, rnd, np.arange(1 << 16, dtype=np.uint16).view(np.uint8)[:CH]):
+        p = oracle.encode(1, st, CH, None, 1, codec=2)
+        v, stg, _ = oracle.decode_verify(1, p, st.size, CH, None, 1, codec=2)
+        assert v == 0 and np.array_equal(stg[: st.size], st)
+
+
+def test_dirty_list_payload():
+    rng = np.random.default_rng(4)
+    st = bf16_state(rng, 5 * CH // 2)
+    idx = np.array([1, 3, 4], np.uint32)
+    p = oracle.encode(0, st, CH, idx, 2, codec=2)
+    v, stg, _ = oracle.decode_verify(0, p, st.size, CH, None, 2, codec=2)
+    assert v == 0
+    for r, c in enumerate(idx):
+        assert np.array_equal(stg[r * CH:(r + 1) * CH], st[c * CH:(c + 1) * CH])
+
+
+def test_every_single_bit_flip_aborts():
+    rng = np.random.default_rng(5)
+    st = bf16_state(rng, 1500, sigma=2.0)  # one short chunk of 3000 bytes
+    p = oracle.encode(0, st, CH, None, 1, codec=2)
+    assert p[64] == 2  # the record is HUF
+    bad = p.copy()
+    missed = []
+    for i in range(p.size * 8):
+        bad[i // 8] ^= 1 << (i % 8)
+        if oracle.decode_verify(0, bad, st.size, CH, None, 1, codec=2)[0] == 0:
+            missed.append(i)
+        bad[i // 8] ^= 1 << (i % 8)
+    assert not missed
