@@ -57,7 +57,17 @@ typedef int32_t wm_status;
 
 #define WM_CRC32_ZLIB 0 /* reflected 0xEDB88320, init/xorout 0xFFFFFFFF */
 #define WM_CRC32C 1     /* reflected 0x82F63B78, init/xorout 0xFFFFFFFF */
+/* Payload formats (codec ids).  EXPFOR, format v1: each chunk's exponents
+ * as k-bit offsets from a base with escapes.  EXPHUF, format v2: each
+ * chunk's exponents in the chunk's own canonical Huffman code (lengths at
+ * most 11) in 512 streams, so that 512 decoders work side by side (§6.4: the
+ * redundancy of a bf16 cache sits in its exponent plane, which the paper's
+ * codec entropy-codes).  Both fall back to RAW per chunk.  Format v2 is
+ * taken by wm_encode, wm_decode_verify and wm_commit_or_abort; the fused and
+ * composed calls (wm_encode_step, wm_receive_verify, wm_precopy_round)
+ * return WM_ERR_UNSUPPORTED for it. */
 #define WM_CODEC_EXPFOR 1
+#define WM_CODEC_EXPHUF 2
 
 /* Bits of the device verdict word written by wm_decode_verify. */
 #define WM_V_HEADER 1u  /* header rejected; nothing else examined */
@@ -73,7 +83,7 @@ typedef int32_t wm_status;
 typedef struct wm_params {
   uint32_t chunk_bytes; /* bytes per chunk; 65536 */
   uint32_t crc_kind;    /* WM_CRC32_ZLIB or WM_CRC32C */
-  uint32_t codec;       /* WM_CODEC_EXPFOR */
+  uint32_t codec;       /* WM_CODEC_EXPFOR or WM_CODEC_EXPHUF */
   uint32_t flags;       /* must be 0 */
 } wm_params;
 
@@ -85,8 +95,8 @@ const char *wm_status_str(wm_status s);
 wm_status wm_init(int device);
 
 /* Bytes of device workspace needed by wm_diff_dirty, wm_encode,
- * wm_encode_step and wm_decode_verify for a state of nbytes.  0 if p is
- * invalid. */
+ * wm_encode_step and wm_decode_verify for a state of nbytes (format v2 adds
+ * 688 bytes per chunk for the record plans).  0 if p is invalid. */
 uint64_t wm_workspace_bytes(uint64_t nbytes, const wm_params *p);
 
 /* Largest payload that n_records records of a state of nbytes can produce

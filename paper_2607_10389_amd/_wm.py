@@ -27,6 +27,7 @@ WM_ERR_UNSUPPORTED = -5
 WM_CRC32_ZLIB = 0
 WM_CRC32C = 1
 WM_CODEC_EXPFOR = 1
+WM_CODEC_EXPHUF = 2
 
 V_HEADER, V_TABLE, V_RECORD, V_DATA, V_STAGING = 1, 2, 4, 8, 16
 
@@ -118,8 +119,9 @@ def status_str(s: int) -> str:
     return LIB.wm_status_str(s).decode()
 
 
-def params(crc_kind: int = WM_CRC32_ZLIB, chunk_bytes: int = CHUNK) -> Params:
-    return Params(chunk_bytes, crc_kind, WM_CODEC_EXPFOR, 0)
+def params(crc_kind: int = WM_CRC32_ZLIB, chunk_bytes: int = CHUNK,
+           codec: int = WM_CODEC_EXPFOR) -> Params:
+    return Params(chunk_bytes, crc_kind, codec, 0)
 
 
 def _p(t):

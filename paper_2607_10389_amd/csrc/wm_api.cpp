@@ -63,7 +63,9 @@ wm_status ensure_device(int *n_cu) {
 
 wm_status check_params(const wm_params *p) {
   if (!p) return WM_ERR_INVALID_ARG;
-  if (p->crc_kind > 1 || p->codec != WM_CODEC_EXPFOR || p->flags != 0) return WM_ERR_INVALID_ARG;
+  if (p->crc_kind > 1 || (p->codec != WM_CODEC_EXPFOR && p->codec != WM_CODEC_EXPHUF) ||
+      p->flags != 0)
+    return WM_ERR_INVALID_ARG;
   uint32_t c = p->chunk_bytes;
   bool pow2 = c >= 4096u && c <= (16u << 20) && (c & (c - 1)) == 0;
   if (!pow2) return WM_ERR_INVALID_ARG;
@@ -80,6 +82,7 @@ wm_status make_geom(uint64_t nbytes, const wm_params *p, ChunkGeom *g) {
   g->n_chunks = (uint32_t)n;
   g->tail_len = n ? (uint32_t)(nbytes - (n - 1) * kChunk) : kChunk;
   g->crc_kind = p->crc_kind;
+  g->codec = p->codec;
   g->k_tail = 0;
   for (int i = 0; i < 32; ++i) g->tail_mat[i] = 1u << i;
   if (g->tail_len != kChunk) {
@@ -100,6 +103,13 @@ wm_status make_geom(uint64_t nbytes, const wm_params *p, ChunkGeom *g) {
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Workspace: the WsLayout part, then (format v2) one plan per chunk.
+uint64_t plans_offset(const WsLayout &L) { return (L.total + 255u) & ~255ull; }
+uint64_t ws_need(const WsLayout &L, uint32_t n_chunks, uint32_t codec) {
+  return codec == WM_CODEC_EXPHUF ? plans_offset(L) + (uint64_t)kHufPlanBytes * n_chunks
+                                  : L.total;
+}
 
 wm_status hip_status(int e) { return e == 0 ? WM_OK : WM_ERR_HIP; }
 
@@ -132,7 +142,7 @@ uint64_t wm_workspace_bytes(uint64_t nbytes, const wm_params *p) {
   uint64_t n = (nbytes + p->chunk_bytes - 1) / p->chunk_bytes;
   if (n >= (1ull << 24)) return 0;
   (void)g;
-  return ws_layout((uint32_t)n).total;
+  return ws_need(ws_layout((uint32_t)n), (uint32_t)n, p->codec);
 }
 
 uint64_t wm_payload_bound(uint64_t nbytes, uint32_t n_records, const wm_params *p) {
@@ -183,11 +193,16 @@ wm_status wm_encode(const void *state, uint64_t nbytes, const wm_params *p, cons
   if (!payload || !payload_bytes || !aligned16(payload)) return WM_ERR_INVALID_ARG;
   if (payload_cap < wm_payload_bound(nbytes, g.n_chunks, p)) return WM_ERR_CAPACITY;
   WsLayout L = ws_layout(g.n_chunks);
-  if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
+  if (!ws || ws_bytes < ws_need(L, g.n_chunks, g.codec) || !aligned16(ws)) return WM_ERR_WORKSPACE;
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
   uint32_t *crc_scratch =
       crc ? nullptr : reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + L.flags);
+  if (g.codec == WM_CODEC_EXPHUF)
+    return hip_status(launch_encode_v2(state, g, idx, n_idx, crc, crc_scratch, nullptr, payload,
+                                       payload_bytes, ws, L,
+                                       static_cast<uint8_t *>(ws) + plans_offset(L), n_cu,
+                                       stream));
   int mode = idx ? 0 : 1;
   return hip_status(launch_encode(mode, state, nullptr, g, idx, n_idx, crc, crc_scratch, nullptr,
                                   nullptr, nullptr, payload, payload_bytes, ws, L, n_cu, stream));
@@ -200,6 +215,7 @@ wm_status wm_encode_step(const void *cur, const void *prev, uint64_t nbytes, con
   ChunkGeom g;
   wm_status s = make_geom(nbytes, p, &g);
   if (s != WM_OK) return s;
+  if (g.codec != WM_CODEC_EXPFOR) return WM_ERR_UNSUPPORTED;
   if (nbytes & 1u) return WM_ERR_INVALID_ARG;
   if ((nbytes && !cur) || !aligned16(cur) || !aligned16(prev)) return WM_ERR_INVALID_ARG;
   if (!payload || !payload_bytes || !aligned16(payload)) return WM_ERR_INVALID_ARG;
@@ -229,6 +245,9 @@ wm_status wm_decode_verify(const void *payload, uint64_t payload_cap, uint64_t n
   if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  if (g.codec == WM_CODEC_EXPHUF)
+    return hip_status(launch_decode_v2(payload, payload_cap, g, staging, staging_cap, verdict,
+                                       rec_status, ws, L, n_cu, stream));
   return hip_status(launch_decode(payload, payload_cap, g, staging, staging_cap, verdict,
                                   rec_status, ws, L, n_cu, stream));
 }
@@ -329,6 +348,7 @@ wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t 
   ChunkGeom g;
   wm_status s = make_geom(nbytes, p, &g);
   if (s != WM_OK) return s;
+  if (g.codec != WM_CODEC_EXPFOR) return WM_ERR_UNSUPPORTED;
   if ((nbytes & 1u) || crc_valid > 1) return WM_ERR_INVALID_ARG;
   if (!b || !n_dirty_host || !b->crc || !b->dirty_idx || !b->n_dirty) return WM_ERR_INVALID_ARG;
   if (nbytes && (!cur || !shipped || !dest)) return WM_ERR_INVALID_ARG;
@@ -457,6 +477,7 @@ wm_status wm_receive_verify(const void *host_payload, uint64_t payload_bytes, vo
   ChunkGeom g;
   wm_status s = make_geom(nbytes, p, &g);
   if (s != WM_OK) return s;
+  if (g.codec != WM_CODEC_EXPFOR) return WM_ERR_UNSUPPORTED;
   if (nbytes & 1u) return WM_ERR_INVALID_ARG;
   if (!payload || !verdict || !aligned16(payload)) return WM_ERR_INVALID_ARG;
   if (payload_bytes && !host_payload) return WM_ERR_INVALID_ARG;

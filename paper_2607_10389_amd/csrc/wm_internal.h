@@ -52,6 +52,7 @@ struct ChunkGeom {
   uint32_t n_chunks;    // ceil(nbytes / kChunk)
   uint32_t tail_len;    // length of the last chunk (kChunk if full)
   uint32_t crc_kind;
+  uint32_t codec;       // payload format: 1 (v1) or 2 (v2, Huffman exponents)
   uint32_t k_tail;      // F^tail_len(~0) ^ ~0
   uint32_t tail_mat[32];// F^-(kChunk - tail_len), columns
 };
@@ -125,6 +126,17 @@ struct ManifestLeaf {
 // gather: leaves -> flat (flatten); else flat -> leaves (rehydrate)
 int launch_manifest(bool gather, void *flat, uint64_t flat_bytes, const ManifestLeaf *leaves,
                     uint32_t n_leaves, int n_cu, void *stream);
+// Format v2: per-record plans in the workspace after the WsLayout part
+// (kHufPlanBytes each: header, code-length nibbles, stream byte counts).
+constexpr uint32_t kHufPlanBytes = 688;
+int launch_encode_v2(const void *state, const ChunkGeom &g, const uint32_t *idx,
+                     const uint32_t *n_idx, const uint32_t *crc_in, uint32_t *crc_scratch,
+                     uint32_t *global_crc, void *payload, uint64_t *payload_bytes, void *ws,
+                     const WsLayout &L, uint8_t *plans, int n_cu, void *stream);
+int launch_decode_v2(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
+                     void *staging, uint64_t staging_cap, uint32_t *verdict,
+                     uint32_t *rec_status, void *ws, const WsLayout &L, int n_cu,
+                     void *stream);
 int set_kernel_attributes();
 
 }  // namespace wm

@@ -1294,8 +1294,8 @@ __global__ __launch_bounds__(256) void k_encode_finish(
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     const uint64_t total = table_off + 16ull * n_rec;
     uint32_t h[16];
-    h[0] = 0x31564D57u;  // "WMV1"
-    h[1] = 1u | (g.crc_kind << 16) | (1u << 24);
+    h[0] = g.codec == 2 ? 0x32564D57u : 0x31564D57u;  // "WMV2" / "WMV1"
+    h[1] = g.codec | (g.crc_kind << 16) | (g.codec << 24);
     h[2] = kChunk;
     h[3] = g.n_chunks;
     h[4] = (uint32_t)g.nbytes;
@@ -1352,8 +1352,8 @@ __global__ __launch_bounds__(64) void k_decode_prepare(
   uint32_t s = 0xFFFFFFFFu;
   for (int i = 0; i < 60; ++i) s = t1[(s ^ payload[i]) & 255u] ^ (s >> 8);
   if ((s ^ 0xFFFFFFFFu) != ld_u32(payload + 60)) return;
-  if (ld_u32(payload) != 0x31564D57u) return;
-  if (ld_u32(payload + 4) != (1u | (g.crc_kind << 16) | (1u << 24))) return;
+  if (ld_u32(payload) != (g.codec == 2 ? 0x32564D57u : 0x31564D57u)) return;
+  if (ld_u32(payload + 4) != (g.codec | (g.crc_kind << 16) | (g.codec << 24))) return;
   if (ld_u32(payload + 8) != kChunk || ld_u32(payload + 12) != g.n_chunks) return;
   if (ld_u64(payload + 16) != g.nbytes) return;
   uint32_t n_rec = ld_u32(payload + 24), flags = ld_u32(payload + 28);
@@ -1992,13 +1992,624 @@ int upload_tables(int device, const CrcTables tabs[2]) {
 
 // Dynamic LDS limits, and the premise of lds_at: the kernels that address
 // dynamic LDS from 0 have no static LDS.
+// -------------------------------------------------------------- format v2 --
+// Records are RAW (as in format v1) or HUF: the chunk's exponents in the
+// chunk's own canonical Huffman code, lengths at most kHufMaxLen, in 512
+// streams.  Stream s holds the words of wave s / 64, lane s % 64 of the
+// kernels' row layout (the lane's 8 words of each of its wave's 8 rows, row
+// by row), each stream padded to a byte; a code goes into its stream most
+// significant bit first, stream bit j being bit j % 8 of byte j / 8.  HUF
+// body with k >= 1: code-length nibbles (128 B) | stream byte counts (512 B)
+// | streams, padded to 16 | sign/mantissa plane, padded to 16.  With k = 0
+// (a single exponent, `base`): the sign/mantissa plane only.  A HUF record
+// must be shorter than the RAW one.  The encoder plans every record (the
+// code and its exact size), scans the sizes into offsets and then writes;
+// the decoder stages a record's streams in LDS and decodes each stream
+// through a table of the code's first kHufMaxLen bits.
+
+constexpr uint32_t kHufMaxLen = 11;
+constexpr uint32_t kHufStreams = 512;
+constexpr uint32_t kHufHead = 16 + 128 + kHufStreams;  // record header and the two tables
+
+struct HufPlan {  // first 48 bytes of a plan; code-length nibbles at +48, stream bytes at +176
+  uint32_t mode, k, base, sb;
+  uint32_t size_lo, size_hi, off_lo, off_hi;
+  uint32_t c, bad, pad_[2];
+};
+static_assert(sizeof(HufPlan) == 48 && 48 + 128 + kHufStreams <= kHufPlanBytes, "plan layout");
+
+__device__ __forceinline__ uint64_t huf_rec_size(uint32_t n, uint32_t k, uint32_t sb) {
+  return k == 0 ? 16u + pad16(n) : kHufHead + pad16(sb) + pad16(n);
+}
+__device__ __forceinline__ uint64_t raw_rec_size(uint32_t n) { return 16u + 2 * pad16(n); }
+
+// CRC of whole words with the byte table in device memory (kernels without
+// the LDS tables).
+__device__ uint32_t crc_words_g(uint32_t kind, const uint32_t *w, int nw) {
+  const uint32_t *t1 = g_tables[kind].byte1;
+  uint32_t s = 0xFFFFFFFFu;
+  for (int i = 0; i < 4 * nw; ++i) s = t1[(s ^ (w[i >> 2] >> (8 * (i & 3)))) & 255u] ^ (s >> 8);
+  return s ^ 0xFFFFFFFFu;
+}
+
+// Word j (0..7) of a 16-byte row piece, its exponent and sign/mantissa byte.
+__device__ __forceinline__ uint32_t word_of(const uint4 &x, int j) {
+  const uint32_t v = j < 2 ? x.x : (j < 4 ? x.y : (j < 6 ? x.z : x.w));
+  return (v >> (16 * (j & 1))) & 0xFFFFu;
+}
+__device__ __forceinline__ uint32_t exp_of(uint32_t w) { return (w >> 7) & 255u; }
+__device__ __forceinline__ uint32_t sm_of(uint32_t w) { return ((w >> 8) & 0x80u) | (w & 0x7Fu); }
+
+// One plan per item: exponent histogram, code lengths (the oracle's
+// construction, run by one thread: leaves sorted by (count, symbol), the two
+// lightest nodes merged with a leaf before an internal node of equal weight,
+// counts halved while a length exceeds kHufMaxLen), stream byte counts and
+// the mode.
+__global__ __launch_bounds__(512) void k_huf_plan(const uint8_t *__restrict__ state, ChunkGeom g,
+                                                  const uint32_t *__restrict__ idx,
+                                                  const uint32_t *__restrict__ n_idx,
+                                                  uint8_t *__restrict__ plans, WsCtl *ctl) {
+  __shared__ uint32_t hist[256], wt[256];
+  __shared__ uint16_t order[256];
+  __shared__ uint32_t nw[511];
+  __shared__ int16_t parent[511];
+  __shared__ uint8_t depth[511];
+  __shared__ uint8_t lens[256];
+  __shared__ uint32_t red[kWaves];
+  __shared__ uint32_t sh_k;
+  const uint32_t t = threadIdx.x;
+  const Lane l = lane_info();
+  const uint32_t n_items = idx ? min(*n_idx, g.n_chunks) : g.n_chunks;
+  for (uint32_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+    uint32_t c = idx ? idx[item] : item;
+    const bool bad = c >= g.n_chunks || (idx && item > 0 && idx[item - 1] >= c);
+    if (bad) c = 0;
+    const uint32_t len = chunk_len(g, c), n = len / 2, w0 = l.off0 >> 1;
+    uint4 d[kRows];
+    load_chunk(state + (uint64_t)c * kChunk, len, l, d);
+    if (t < 256) hist[t] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < kRows; ++h)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (w0 + h * (kRow / 2) + j < n) atomicAdd(&hist[exp_of(word_of(d[h], j))], 1u);
+    __syncthreads();
+    if (t < 256) wt[t] = hist[t];
+    for (;;) {
+      __syncthreads();
+      const uint32_t my = t < 256 ? wt[t] : 0u;
+      if (t < 256) lens[t] = 0;
+      if (my) {
+        uint32_t rank = 0;
+        for (uint32_t s2 = 0; s2 < 256; ++s2) {
+          const uint32_t o = wt[s2];
+          rank += (o != 0u && (o < my || (o == my && s2 < t))) ? 1u : 0u;
+        }
+        order[rank] = (uint16_t)t;
+      }
+      const uint32_t m = (uint32_t)__syncthreads_count(my != 0u);
+      if (t == 0) {
+        uint32_t longest = 0;
+        if (m >= 2) {
+          for (uint32_t i = 0; i < m; ++i) nw[i] = wt[order[i]];
+          uint32_t li = 0, ii = m, n_int = m;
+          for (uint32_t s2 = 0; s2 + 1 < m; ++s2) {
+            uint32_t pick[2];
+            for (int q = 0; q < 2; ++q) {
+              if (li < m && (ii >= n_int || nw[li] <= nw[ii])) pick[q] = li++;
+              else pick[q] = ii++;
+            }
+            nw[n_int] = nw[pick[0]] + nw[pick[1]];
+            parent[pick[0]] = parent[pick[1]] = (int16_t)n_int;
+            ++n_int;
+          }
+          depth[n_int - 1] = 0;
+          for (int32_t i = (int32_t)n_int - 2; i >= 0; --i) depth[i] = (uint8_t)(depth[parent[i]] + 1);
+          for (uint32_t i = 0; i < m; ++i) {
+            lens[order[i]] = depth[i];
+            longest = max(longest, (uint32_t)depth[i]);
+          }
+        }
+        sh_k = longest;
+      }
+      __syncthreads();
+      if (sh_k <= kHufMaxLen) break;
+      if (t < 256 && wt[t]) wt[t] = (wt[t] + 1u) >> 1;
+    }
+    const uint32_t k = sh_k;
+    uint32_t bits = 0;
+    if (k) {
+#pragma unroll
+      for (int h = 0; h < kRows; ++h)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (w0 + h * (kRow / 2) + j < n) bits += lens[exp_of(word_of(d[h], j))];
+    }
+    const uint32_t sb_t = (bits + 7u) >> 3;
+    const uint32_t incl = wave_incl_scan(sb_t);
+    if (l.lane == 63u) red[l.wave] = incl;
+    uint8_t *P = plans + (uint64_t)item * kHufPlanBytes;
+    P[176 + t] = (uint8_t)sb_t;
+    if (t < 128) P[48 + t] = (uint8_t)(lens[2 * t] | (lens[2 * t + 1] << 4));
+    __syncthreads();
+    if (t == 0) {
+      uint32_t sb = 0;
+      for (int w = 0; w < kWaves; ++w) sb += red[w];
+      const uint64_t raw = raw_rec_size(n), hs = huf_rec_size(n, k, sb);
+      const bool huf = hs < raw;
+      const uint64_t size = huf ? hs : raw;
+      HufPlan hp;
+      hp.mode = huf ? 2u : 0u;
+      hp.k = huf ? k : 0u;
+      hp.base = huf && k == 0 ? (uint32_t)order[0] : 0u;
+      hp.sb = huf ? sb : 0u;
+      hp.size_lo = (uint32_t)size;
+      hp.size_hi = (uint32_t)(size >> 32);
+      hp.off_lo = hp.off_hi = 0;
+      hp.c = c;
+      hp.bad = bad ? 1u : 0u;
+      hp.pad_[0] = hp.pad_[1] = 0;
+      *reinterpret_cast<HufPlan *>(P) = hp;
+      if (bad) atomicOr(&ctl->error, 2u);
+    }
+    __syncthreads();
+  }
+}
+
+// Record offsets: 64 + the exclusive prefix of the record sizes (in 16-byte
+// units per tile of 1024 items, the running total in 64 bits).
+__global__ __launch_bounds__(1024) void k_huf_scan(const uint32_t *__restrict__ n_idx,
+                                                   ChunkGeom g, uint8_t *__restrict__ plans,
+                                                   WsCtl *ctl) {
+  __shared__ uint32_t wsum[16];
+  const uint32_t n_items = n_idx ? min(*n_idx, g.n_chunks) : g.n_chunks;
+  uint64_t carry = 64;
+  for (uint32_t base = 0; base < n_items; base += 1024u) {
+    const uint32_t i = base + threadIdx.x;
+    HufPlan *hp = i < n_items ? reinterpret_cast<HufPlan *>(plans + (uint64_t)i * kHufPlanBytes)
+                              : nullptr;
+    const uint32_t units = hp ? hp->size_lo >> 4 : 0u;
+    const uint32_t incl = wave_incl_scan(units);
+    if ((threadIdx.x & 63u) == 63u) wsum[threadIdx.x >> 6] = incl;
+    __syncthreads();
+    uint32_t before = 0, tile = 0;
+    for (uint32_t w = 0; w < 16u; ++w) {
+      const uint32_t v = wsum[w];
+      if (w < (threadIdx.x >> 6)) before += v;
+      tile += v;
+    }
+    if (hp) {
+      const uint64_t off = carry + 16ull * (before + incl - units);
+      hp->off_lo = (uint32_t)off;
+      hp->off_hi = (uint32_t)(off >> 32);
+    }
+    carry += 16ull * tile;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    ctl->n_rec = n_items;
+    ctl->payload_bytes = carry - 64u;
+  }
+}
+
+// Write every planned record, its table entry (staged in the workspace) and
+// the entry's CRC.
+__global__ __launch_bounds__(512) void k_huf_write(const uint8_t *__restrict__ state, ChunkGeom g,
+                                                   const uint32_t *__restrict__ n_idx,
+                                                   const uint32_t *__restrict__ crcs,
+                                                   const uint8_t *__restrict__ plans,
+                                                   uint8_t *__restrict__ payload, uint8_t *ws,
+                                                   WsLayout L) {
+  __shared__ uint8_t lens[256];
+  __shared__ uint16_t code[256];
+  __shared__ uint32_t red[kWaves];
+  const uint32_t t = threadIdx.x;
+  const Lane l = lane_info();
+  uint4 *tab_ws = reinterpret_cast<uint4 *>(ws + L.table);
+  uint32_t *ecrc = reinterpret_cast<uint32_t *>(ws + L.entry_crc);
+  const uint32_t n_items = n_idx ? min(*n_idx, g.n_chunks) : g.n_chunks;
+  for (uint32_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+    const uint8_t *P = plans + (uint64_t)item * kHufPlanBytes;
+    const HufPlan hp = *reinterpret_cast<const HufPlan *>(P);
+    if (hp.bad) continue;  // the payload is discarded (ctl->error)
+    const uint32_t c = hp.c, len = chunk_len(g, c), n = len / 2, w0 = l.off0 >> 1;
+    const uint64_t off = ((uint64_t)hp.off_hi << 32) | hp.off_lo;
+    uint8_t *rec = payload + off;
+    uint4 d[kRows];
+    load_chunk(state + (uint64_t)c * kChunk, len, l, d);
+    if (t == 0) {
+      uint32_t hw[4] = {hp.mode | (hp.k << 8) | (hp.base << 16), n, hp.sb, 0u};
+      hw[3] = crc_words_g(g.crc_kind, hw, 3);
+      *reinterpret_cast<uint4 *>(rec) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+      const uint32_t ew[4] = {c, crcs[c], (uint32_t)off, (uint32_t)(off >> 32)};
+      tab_ws[item] = make_uint4(ew[0], ew[1], ew[2], ew[3]);
+      ecrc[item] = crc_words_g(g.crc_kind, ew, 4);
+    }
+    uint64_t smo;  // sign/mantissa plane offset
+    if (hp.mode == 0) {
+      smo = 16u + pad16(n);
+#pragma unroll
+      for (int h = 0; h < kRows; ++h) {
+        const uint32_t i0 = w0 + h * (kRow / 2);
+        uint32_t e[2] = {0, 0};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) e[j >> 2] |= exp_of(word_of(d[h], j)) << (8 * (j & 3));
+        if (i0 + 8u <= n) {
+          *reinterpret_cast<uint2 *>(rec + 16 + i0) = make_uint2(e[0], e[1]);
+        } else {
+          for (uint32_t b = 0; i0 + b < n; ++b) rec[16 + i0 + b] = (uint8_t)(e[b >> 2] >> (8 * (b & 3)));
+        }
+      }
+      if (t < 16u && n + t < pad16(n)) rec[16 + n + t] = 0;
+    } else if (hp.k == 0) {
+      smo = 16;
+    } else {
+      smo = kHufHead + pad16(hp.sb);
+      if (t < 128u) rec[16 + t] = P[48 + t];
+      rec[16 + 128 + t] = P[176 + t];
+      if (t < 256u) lens[t] = (uint8_t)((P[48 + (t >> 1)] >> (4 * (t & 1))) & 15u);
+      __syncthreads();
+      if (t == 0) {  // canonical codes: consecutive values in (length, symbol) order
+        uint32_t bl[kHufMaxLen + 1] = {0}, nx[kHufMaxLen + 1] = {0};
+        for (uint32_t s2 = 0; s2 < 256; ++s2) bl[lens[s2]]++;
+        bl[0] = 0;
+        uint32_t cd = 0;
+        for (uint32_t b = 1; b <= kHufMaxLen; ++b) {
+          cd = (cd + bl[b - 1]) << 1;
+          nx[b] = cd;
+        }
+        for (uint32_t s2 = 0; s2 < 256; ++s2) code[s2] = (uint16_t)(lens[s2] ? nx[lens[s2]]++ : 0u);
+      }
+      const uint32_t sb_t = P[176 + t];
+      const uint32_t incl = wave_incl_scan(sb_t);
+      if (l.lane == 63u) red[l.wave] = incl;
+      __syncthreads();
+      uint32_t so = incl - sb_t;
+      for (uint32_t w = 0; w < l.wave; ++w) so += red[w];
+      uint8_t *st = rec + kHufHead + so;
+      uint64_t acc = 0;
+      uint32_t nb = 0, ob = 0;
+#pragma unroll
+      for (int h = 0; h < kRows; ++h)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          if (w0 + h * (kRow / 2) + j < n) {
+            const uint32_t e = exp_of(word_of(d[h], j)), ln = lens[e];
+            acc |= (uint64_t)(__builtin_bitreverse32(code[e]) >> (32u - ln)) << nb;
+            nb += ln;
+            while (nb >= 8u) {  // (the plan counted these bytes: ob stays below sb_t)
+              if (ob < sb_t) st[ob] = (uint8_t)acc;
+              ++ob;
+              acc >>= 8;
+              nb -= 8u;
+            }
+          }
+        }
+      if (nb && ob < sb_t) st[ob] = (uint8_t)acc;
+      if (t < 16u && hp.sb + t < pad16(hp.sb)) rec[kHufHead + hp.sb + t] = 0;
+    }
+#pragma unroll
+    for (int h = 0; h < kRows; ++h) {
+      const uint32_t i0 = w0 + h * (kRow / 2);
+      uint32_t sm[2] = {0, 0};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) sm[j >> 2] |= sm_of(word_of(d[h], j)) << (8 * (j & 3));
+      if (i0 + 8u <= n) {
+        *reinterpret_cast<uint2 *>(rec + smo + i0) = make_uint2(sm[0], sm[1]);
+      } else {
+        for (uint32_t b = 0; i0 + b < n; ++b) rec[smo + i0 + b] = (uint8_t)(sm[b >> 2] >> (8 * (b & 3)));
+      }
+    }
+    if (t < 16u && n + t < pad16(n)) rec[smo + n + t] = 0;
+    __syncthreads();
+  }
+}
+
+// Decoder state in the low LDS region: decode table, code lengths, symbols
+// in code order, lane CRC values, and one record's fields.
+constexpr uint32_t kHdTab = 0;                 // 2^kHufMaxLen u16: symbol | length << 8
+constexpr uint32_t kHdLens = 4096;             // u8[256]
+constexpr uint32_t kHdSorted = kHdLens + 256;  // u8[256]
+constexpr uint32_t kHdU = kHdSorted + 256;     // u32[kThreads]
+constexpr uint32_t kHdMeta = kHdU + 4 * kThreads;
+constexpr uint32_t kLdsHufStreams = kLdsBase;  // the record's streams (under 32 KiB)
+constexpr uint32_t kLdsHufDecode = kLdsBase + 32768;
+static_assert(kLdsHufDecode <= 163840, "v2 decoder LDS fits one CU");
+
+struct HufMeta {
+  uint32_t st, mode, k, base, n, sb, c, src, len, off_lo, off_hi;
+  uint32_t kraft, maxlen, bad, hufbad;
+  uint32_t bl[kHufMaxLen + 1], first[kHufMaxLen + 1], start[kHufMaxLen + 1];
+  uint32_t wsum[kWaves];
+};
+static_assert(kHdMeta + sizeof(HufMeta) <= kLdsLowBytes, "v2 decoder scratch fits the low region");
+
+// One record per workgroup step: the control lane checks the table entry and
+// the record header; the data waves build the decode table, decode their
+// streams, assemble the words, store them and take the CRC lane values; the
+// control wave folds the CRC and records the status.
+__global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
+    const uint8_t *__restrict__ payload, ChunkGeom g, uint8_t *__restrict__ staging,
+    uint32_t *__restrict__ rec_status, uint8_t *ws, WsLayout L) {
+  WsCtl *ctl = reinterpret_cast<WsCtl *>(ws + L.ctl);
+  uint32_t *ecrc = reinterpret_cast<uint32_t *>(ws + L.entry_crc);
+  if (!uniform(ctl->hdr_ok)) return;
+  const uint32_t n_rec = uniform(ctl->n_rec);
+  const uint64_t table_off = ctl->table_off;
+  load_crc_tables(g.crc_kind);
+  __syncthreads();
+  const CrcTables &T = g_tables[g.crc_kind];
+  HufMeta &M = *reinterpret_cast<HufMeta *>(lds_at(kHdMeta));
+  uint16_t *tab = reinterpret_cast<uint16_t *>(lds_at(kHdTab));
+  uint8_t *lens = lds_at(kHdLens);
+  uint8_t *sorted = lds_at(kHdSorted);
+  uint32_t *U = reinterpret_cast<uint32_t *>(lds_at(kHdU));
+  const uint32_t *S32 = reinterpret_cast<const uint32_t *>(lds_at(kLdsHufStreams));
+  const uint32_t t = threadIdx.x;
+  const bool is_ctl = t >= (uint32_t)kThreads;
+  const GLane gl = glane_make();
+  const Lane l0 = lane_info();
+  for (uint32_t r = blockIdx.x; r < n_rec; r += gridDim.x) {
+    const Lane l = lane_fresh(l0);
+    if (t == (uint32_t)kThreads) {
+      const uint8_t *e = payload + table_off + 16ull * r;
+      const uint32_t ew[4] = {ld_u32(e), ld_u32(e + 4), ld_u32(e + 8), ld_u32(e + 12)};
+      const uint32_t c = ew[0];
+      const uint64_t off = ew[2] | ((uint64_t)ew[3] << 32);
+      const uint64_t end = r + 1 < n_rec ? ld_u64(e + 24) : table_off;
+      const bool tbad = c >= g.n_chunks || (r > 0 && ld_u32(e - 16) >= c) ||
+                        (r == 0 && off != 64u) || (off & 15u) || off >= end || end > table_off;
+      ecrc[r] = crc_words(ew, 4);
+      M.bad = M.hufbad = M.kraft = M.maxlen = 0;
+      for (uint32_t b = 0; b <= kHufMaxLen; ++b) M.bl[b] = 0;
+      M.st = kMetaSkip;
+      if (tbad) {
+        atomicOr(&ctl->table_bad, 1u);
+      } else {
+        const uint32_t len = chunk_len(g, c), n = len / 2;
+        const uint64_t rl = end - off;
+        uint32_t st = 0, mode = 0, k = 0, base = 0, sb = 0;
+        if (rl < 16) {
+          st = 4;
+        } else {
+          const uint8_t *rec = payload + off;
+          const uint32_t hw[4] = {ld_u32(rec), ld_u32(rec + 4), ld_u32(rec + 8), ld_u32(rec + 12)};
+          mode = hw[0] & 255u;
+          k = (hw[0] >> 8) & 255u;
+          base = (hw[0] >> 16) & 255u;
+          sb = hw[2];
+          if (crc_words(hw, 3) != hw[3] || (hw[0] >> 24) || hw[1] != n) {
+            st = 4;
+          } else if (mode == 0) {
+            if (k || base || sb || rl != raw_rec_size(n)) st = 4;
+          } else if (mode == 2) {
+            if (k > kHufMaxLen || (k == 0 && sb) || (k && base)) st = 4;
+            else if (huf_rec_size(n, k, sb) >= raw_rec_size(n) || rl != huf_rec_size(n, k, sb)) st = 4;
+          } else {
+            st = 4;
+          }
+        }
+        M.st = st;
+        M.mode = mode;
+        M.k = k;
+        M.base = base;
+        M.n = n;
+        M.sb = sb;
+        M.c = c;
+        M.src = ew[1];
+        M.len = len;
+        M.off_lo = (uint32_t)off;
+        M.off_hi = (uint32_t)(off >> 32);
+      }
+    }
+    __syncthreads();
+    const uint32_t st0 = uniform(M.st), mode = uniform(M.mode), k = uniform(M.k);
+    const uint32_t n = uniform(M.n), sb = uniform(M.sb);
+    const uint64_t off = ((uint64_t)uniform(M.off_hi) << 32) | uniform(M.off_lo);
+    const uint8_t *rec = payload + off;
+    const bool huf = st0 == 0 && mode == 2 && k >= 1;
+    // code lengths and stream byte counts
+    uint32_t sb_t = 0;
+    if (huf && !is_ctl) {
+      if (t < 128u) {
+        const uint32_t b = rec[16 + t];
+        lens[2 * t] = (uint8_t)(b & 15u);
+        lens[2 * t + 1] = (uint8_t)(b >> 4);
+      }
+      sb_t = rec[16 + 128 + t];
+    }
+    __syncthreads();
+    uint32_t incl = 0;
+    if (huf && !is_ctl) {
+      if (t < 256u) {
+        const uint32_t ln = lens[t];
+        if (ln > k) atomicOr(&M.hufbad, 1u);
+        if (ln) {
+          atomicAdd(&M.kraft, 1u << (kHufMaxLen - min(ln, kHufMaxLen)));
+          atomicMax(&M.maxlen, ln);
+          atomicAdd(&M.bl[min(ln, kHufMaxLen)], 1u);
+        }
+      }
+      incl = wave_incl_scan(sb_t);
+      if (l.lane == 63u) M.wsum[l.wave] = incl;
+    }
+    __syncthreads();
+    uint32_t so = 0;
+    if (huf && !is_ctl) {
+      uint32_t tot = 0;
+      so = incl - sb_t;
+      for (uint32_t w = 0; w < (uint32_t)kWaves; ++w) {
+        const uint32_t v = M.wsum[w];
+        if (w < l.wave) so += v;
+        tot += v;
+      }
+      if (t == 0) {  // complete code of longest length k; first code and rank base per length
+        if (M.kraft != (1u << kHufMaxLen) || M.maxlen != k || tot != sb) M.hufbad = 1;
+        uint32_t cd = 0, at = 0;
+        for (uint32_t b = 1; b <= kHufMaxLen; ++b) {
+          cd = (cd + (b > 1 ? M.bl[b - 1] : 0u)) << 1;
+          M.first[b] = cd;
+          M.start[b] = at;
+          at += M.bl[b];
+        }
+      }
+    }
+    __syncthreads();
+    const bool hok = huf && uniform(M.hufbad) == 0;
+    if (hok && !is_ctl) {
+      if (t < 256u && lens[t]) {  // symbols in code order
+        const uint32_t ln = lens[t];
+        uint32_t rank = 0;
+        for (uint32_t s2 = 0; s2 < t; ++s2) rank += lens[s2] == ln ? 1u : 0u;
+        sorted[M.start[ln] + rank] = (uint8_t)t;
+      }
+      // the streams into LDS (sb < 32 KiB for a record shorter than RAW)
+      const uint8_t *src = rec + kHufHead;
+      const Rsrc rs = rsrc(src, sb);
+      for (uint32_t q = t; 16u * q < sb; q += kThreads) {
+        uint4 v = 16u * q + 16u <= sb ? buf16(rs, 16u * q) : load16_partial(src + 16u * q, sb - 16u * q);
+        *reinterpret_cast<uint4 *>(lds_at(kLdsHufStreams + 16u * q)) = v;
+      }
+    }
+    __syncthreads();
+    if (hok && !is_ctl) {  // entry p: the code whose bits, first bit lowest, are p's low bits
+      for (uint32_t p = t; p < (1u << kHufMaxLen); p += kThreads) {
+        uint32_t ent = 0;
+        const uint32_t rp = __builtin_bitreverse32(p);
+        for (uint32_t b = 1; b <= k; ++b) {
+          const uint32_t q = (rp >> (32u - b)) - M.first[b];
+          if (q < M.bl[b]) {
+            ent = sorted[M.start[b] + q] | (b << 8);
+            break;
+          }
+        }
+        tab[p] = (uint16_t)ent;
+      }
+    }
+    __syncthreads();
+    if (!is_ctl) {
+      const uint32_t len = uniform(M.len), base = uniform(M.base), w0 = l.off0 >> 1;
+      const bool ok = st0 == 0 && (mode == 0 || (mode == 2 && (k == 0 || hok)));
+      const uint64_t smo = mode == 0 ? 16u + pad16(n) : (k ? kHufHead + pad16(sb) : 16u);
+      const Rsrc rsm = rsrc(rec + smo, ok ? n : 0u);
+      const Rsrc rex = rsrc(rec + 16, ok && mode == 0 ? n : 0u);
+      const bool dec = ok && mode == 2 && k;
+      uint32_t bad = 0;
+      // the lane's stream: bits so far in acc (next bit lowest), bytes [pos, end)
+      uint64_t acc = 0;
+      uint32_t nb = 0, used = 0, pos = so;
+      const uint32_t end = so + (dec ? sb_t : 0u);
+      uint4 d[kRows];
+#pragma unroll
+      for (int h = 0; h < kRows; ++h) {
+        const uint32_t i0 = w0 + h * (kRow / 2);
+        // 8 bytes per plane; the piece that straddles n is read bytewise
+        const bool part = ok && i0 < n && i0 + 8u > n;
+        uint2 smv = buf8(rsm, i0);
+        if (part) {
+          const uint4 v = load16_partial(rec + smo + i0, n - i0);
+          smv = make_uint2(v.x, v.y);
+        }
+        uint32_t e8[2] = {0, 0};
+        if (mode == 0) {
+          uint2 ev = buf8(rex, i0);
+          if (part) {
+            const uint4 v = load16_partial(rec + 16 + i0, n - i0);
+            ev = make_uint2(v.x, v.y);
+          }
+          e8[0] = ev.x;
+          e8[1] = ev.y;
+        } else if (k == 0) {
+          e8[0] = e8[1] = base * 0x01010101u;
+        } else if (dec) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            if (i0 + j < n) {
+              if (nb < kHufMaxLen && pos < end) {  // 32 more bits (zeros past the stream)
+                const uint32_t a = pos >> 2;
+                uint32_t v = __builtin_amdgcn_alignbit(S32[a + 1], S32[a], (pos & 3u) * 8u);
+                const uint32_t take = min(end - pos, 4u);
+                if (take < 4u) v &= (1u << (8u * take)) - 1u;
+                acc |= (uint64_t)v << nb;
+                nb += 8u * take;
+                pos += take;
+              }
+              const uint32_t ent = tab[(uint32_t)acc & ((1u << kHufMaxLen) - 1u)];
+              uint32_t ln = ent >> 8;
+              if (ln == 0 || ln > nb) {  // past the stream (or no such code)
+                bad = 1;
+                ln = min(max(ln, 1u), nb);
+              }
+              acc >>= ln;
+              nb -= ln;
+              used += ln;
+              e8[j >> 2] |= (ent & 255u) << (8 * (j & 3));
+            }
+          }
+        }
+        uint32_t out[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint32_t v = 0;
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const int j = 2 * q + hh;
+            const uint32_t smb = ((j < 4 ? smv.x : smv.y) >> (8 * (j & 3))) & 255u;
+            const uint32_t eb = (e8[j >> 2] >> (8 * (j & 3))) & 255u;
+            const uint32_t w = i0 + j < n ? (((smb & 0x80u) << 8) | (eb << 7) | (smb & 0x7Fu)) : 0u;
+            v |= w << (16 * hh);
+          }
+          out[q] = v;
+        }
+        d[h] = make_uint4(out[0], out[1], out[2], out[3]);
+        dec_store(staging + (uint64_t)r * kChunk, l.off0 + h * kRow, len, out);
+      }
+      if (dec) {  // exactly the stream's bytes, the last one's unused bits zero
+        if ((used + 7u) / 8u != sb_t) bad = 1;
+        if ((used & 7u) && (acc & ((1u << (8u - (used & 7u))) - 1u))) bad = 1;
+      }
+      if (ok) {  // zero padding after each section
+        if (t < 16u && n + t < pad16(n) && rec[smo + n + t]) bad = 1;
+        if (mode == 0 && t >= 16u && t < 32u && n + t - 16u < pad16(n) && rec[16 + n + t - 16u]) bad = 1;
+        if (dec && t >= 32u && t < 48u && sb + t - 32u < pad16(sb) && rec[kHufHead + sb + t - 32u])
+          bad = 1;
+      }
+      if (bad) atomicOr(&M.bad, 1u);
+      U[t] = lane_value(d, gl);
+    }
+    __syncthreads();
+    if (is_ctl) {
+      const uint32_t st = uniform(M.st);
+      if (st != kMetaSkip) {
+        uint32_t stf = st;
+        if (stf == 0) {
+          uint32_t acc2 = U[l.lane];
+#pragma unroll
+          for (int w = 1; w < kWaves; ++w) acc2 = tab4x(kLdsWaveStep, acc2, U[w * 64 + l.lane]);
+          const uint32_t q = uniform(__builtin_amdgcn_readlane(lane_tree(acc2), 63));
+          const uint32_t crc = finish_crc(tab4(kLdsF4, q), uniform(M.len), g, T);
+          const bool bd = uniform(M.bad) != 0 || (mode == 2 && k && uniform(M.hufbad) != 0);
+          stf = bd ? 4u : (crc != uniform(M.src) ? 8u : 0u);
+        }
+        if (l.lane == 0) {
+          if (rec_status) rec_status[r] = stf;
+          if (stf) atomicOr(&ctl->rec_bits, stf);
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
 int set_kernel_attributes() {
-  const void *kern[4] = {reinterpret_cast<const void *>(&k_checksum),
+  const void *kern[5] = {reinterpret_cast<const void *>(&k_checksum),
                          reinterpret_cast<const void *>(&k_encode<false>),
                          reinterpret_cast<const void *>(&k_encode<true>),
-                         reinterpret_cast<const void *>(&k_decode)};
-  const uint32_t bytes[4] = {kLdsBase, kLdsEncode, kLdsEncode, kLdsDecode};
-  for (int i = 0; i < 4; ++i) {
+                         reinterpret_cast<const void *>(&k_decode),
+                         reinterpret_cast<const void *>(&k_huf_decode)};
+  const uint32_t bytes[5] = {kLdsBase, kLdsEncode, kLdsEncode, kLdsDecode, kLdsHufDecode};
+  for (int i = 0; i < 5; ++i) {
     hipError_t e = hipFuncSetAttribute(kern[i], hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)bytes[i]);
     if (e != hipSuccess) return (int)e;
@@ -2236,6 +2847,69 @@ int launch_commit(void *live, const ChunkGeom &g, const void *staging, const voi
                      static_cast<uint8_t *>(live), g, static_cast<const uint8_t *>(staging),
                      static_cast<const uint8_t *>(payload), verdict);
   return (int)hipGetLastError();
+}
+
+int launch_encode_v2(const void *state, const ChunkGeom &g, const uint32_t *idx,
+                     const uint32_t *n_idx, const uint32_t *crc_in, uint32_t *crc_scratch,
+                     uint32_t *global_crc, void *payload, uint64_t *payload_bytes, void *ws,
+                     const WsLayout &L, uint8_t *plans, int n_cu, void *stream) {
+  uint8_t *wsb = static_cast<uint8_t *>(ws);
+  WsCtl *ctl = reinterpret_cast<WsCtl *>(wsb + L.ctl);
+  const uint8_t *st = static_cast<const uint8_t *>(state);
+  hipLaunchKernelGGL(k_encode_prepare, dim3(64), dim3(256), 0, S(stream), wsb, L, g.n_chunks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return (int)e;
+  const uint32_t *crcs = crc_in;
+  if (!crcs) {
+    const int rc = launch_checksum(state, g, crc_scratch, nullptr, n_cu, stream);
+    if (rc) return rc;
+    crcs = crc_scratch;
+  }
+  if (g.n_chunks) {
+    const uint32_t grid = min((uint32_t)n_cu * 4u, g.n_chunks);
+    hipLaunchKernelGGL(k_huf_plan, dim3(grid), dim3(512), 0, S(stream), st, g, idx, n_idx, plans,
+                       ctl);
+    hipLaunchKernelGGL(k_huf_scan, dim3(1), dim3(1024), 0, S(stream), n_idx, g, plans, ctl);
+    hipLaunchKernelGGL(k_huf_write, dim3(grid), dim3(512), 0, S(stream), st, g, n_idx, crcs,
+                       static_cast<const uint8_t *>(plans), static_cast<uint8_t *>(payload), wsb,
+                       L);
+    e = hipGetLastError();
+    if (e != hipSuccess) return (int)e;
+  }
+  uint32_t *sums = reinterpret_cast<uint32_t *>(wsb + L.ctl) + 60;  // global and table CRC
+  CombineJobs jobs = {};
+  jobs.job[0] = CombineJob{crcs, nullptr, g.n_chunks, 16u, g.tail_len, g.crc_kind, sums};
+  jobs.job[1] = CombineJob{reinterpret_cast<const uint32_t *>(wsb + L.entry_crc), &ctl->n_rec,
+                           0u, 4u, 16u, g.crc_kind, sums + 1};
+  const int rc = launch_combine(jobs, 2, stream);
+  if (rc) return rc;
+  hipLaunchKernelGGL(k_encode_finish, dim3(64), dim3(256), 0, S(stream),
+                     static_cast<uint8_t *>(payload), static_cast<const uint8_t *>(ws), L, g,
+                     idx ? 0u : 1u, sums, payload_bytes, nullptr);
+  e = hipGetLastError();
+  if (e != hipSuccess) return (int)e;
+  if (global_crc) {
+    e = hipMemcpyAsync(global_crc, sums, 4, hipMemcpyDeviceToDevice, S(stream));
+    if (e != hipSuccess) return (int)e;
+  }
+  return 0;
+}
+
+int launch_decode_v2(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
+                     void *staging, uint64_t staging_cap, uint32_t *verdict,
+                     uint32_t *rec_status, void *ws, const WsLayout &L, int n_cu,
+                     void *stream) {
+  int rc = launch_decode_begin(payload, payload_cap, g, staging_cap, ws, L, stream);
+  if (rc) return rc;
+  if (g.n_chunks) {
+    const uint32_t grid = min((uint32_t)n_cu, g.n_chunks);
+    hipLaunchKernelGGL(k_huf_decode, dim3(grid), dim3(kThreads + 64), kLdsHufDecode, S(stream),
+                       static_cast<const uint8_t *>(payload), g, static_cast<uint8_t *>(staging),
+                       rec_status, static_cast<uint8_t *>(ws), L);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return (int)e;
+  }
+  return launch_decode_end(g, verdict, ws, L, stream);
 }
 
 }  // namespace wm

@@ -15,9 +15,10 @@ from . import _wm
 class Mover:
     def __init__(self, nbytes: int, crc_kind: int = _wm.WM_CRC32_ZLIB,
                  device: str | torch.device = "cuda", stream=None,
-                 staging_chunks: int | None = None):
+                 staging_chunks: int | None = None,
+                 codec: int = _wm.WM_CODEC_EXPFOR):
         self.nbytes = nbytes
-        self.p = _wm.params(crc_kind)
+        self.p = _wm.params(crc_kind, codec=codec)
         self.device = torch.device(device)
         self.stream = stream
         n = _wm.n_chunks(nbytes)

@@ -260,3 +260,23 @@ def test_receive_verify_argument_checks(lib):
     assert rv(h, 4096, a, 4096, nb, P(), a + 8, nb, a, None, a, ws, 0, None, None) == INVALID
     assert rv(h, 4096, a, 4096, nb, P(), a, nb, a, None, a, ws - 1, 0, None, None) == WORKSPACE
     assert rv(h, 4096, a, 4096, nb, P(codec=3), a, nb, a, None, a, ws, 0, None, None) == INVALID
+
+
+def test_format_v2_calls(lib):
+    a = ALIGNED
+    nb = 4 * CH
+    ws1 = lib.wm_workspace_bytes(nb, P())
+    ws2 = lib.wm_workspace_bytes(nb, P(codec=2))
+    assert ws2 >= ws1 + 688 * 4
+    assert lib.wm_payload_bound(nb, 4, P(codec=2)) == lib.wm_payload_bound(nb, 4, P())
+    assert lib.wm_workspace_bytes(nb, P(codec=3)) == 0
+    bound = lib.wm_payload_bound(nb, 4, P())
+    enc = lib.wm_encode
+    # the plans need the larger workspace
+    assert enc(a, nb, P(codec=2), None, None, None, a, bound, a, a, ws1, None) == WORKSPACE
+    # fused and composed calls take format v1 only
+    assert lib.wm_encode_step(a, None, nb, P(codec=2), None, None, None, None, a, bound, a, a,
+                              ws2, None) == UNSUPPORTED
+    host = ctypes.create_string_buffer(64)
+    assert lib.wm_receive_verify(ctypes.addressof(host), 64, a, 64, nb, P(codec=2), a, nb, a,
+                                 None, a, ws2, 0, None, None) == UNSUPPORTED

@@ -1,0 +1,155 @@
+"""GPU parity of format v2 (codec 2: per-chunk canonical Huffman codes of
+the exponent plane in 512 streams) against the oracle: payload bytes,
+decoded bytes, verdict words and record status are equal (tolerance 0) on
+the tiny cache, dirty lists, edge-case states, flipped bits and the
+production-size cache."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import wm_inputs
+
+from gpu_helpers import ORACLE_THREADS, host_bytes, random_bytes, say, u32
+
+pytestmark = pytest.mark.gpu
+
+CH = 65536
+
+
+@pytest.fixture(scope="module")
+def wm():
+    from paper_2607_10389_amd import _wm
+    _wm.init(-1)
+    return _wm
+
+
+def mover(nbytes, kind=0):
+    from paper_2607_10389_amd import Mover, WM_CODEC_EXPHUF
+    return Mover(nbytes, kind, codec=WM_CODEC_EXPHUF)
+
+
+def dev(a: np.ndarray) -> torch.Tensor:
+    t = torch.empty(max(a.size, 16), dtype=torch.uint8, device="cuda")
+    t[: a.size] = torch.from_numpy(a).cuda()
+    return t
+
+
+def ship(wm, state_h: np.ndarray, kind=0, label=""):
+    """Full v2 ship of a host state through the GPU; checks payload, decode
+    and verdict against the oracle.  Returns the payload."""
+    st = dev(state_h)
+    m = mover(state_h.size, kind)
+    m.encode(st, with_crc=False)
+    torch.cuda.synchronize()
+    got = m.payload_host()
+    want = oracle.encode(kind, state_h, CH, None, ORACLE_THREADS, codec=2)
+    assert got.size == want.size, (label, got.size, want.size)
+    if not np.array_equal(got, want):
+        bad = np.nonzero(got != want)[0]
+        raise AssertionError(f"{label}: {bad.size} payload bytes differ, first {bad[:8].tolist()}")
+    m.decode()
+    assert m.commit(None, scatter=False) == wm.WM_OK, label
+    torch.cuda.synchronize()
+    assert np.array_equal(m.staging[: state_h.size].cpu().numpy(), state_h), label
+    return got, m
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+def test_tiny_full_ship(wm, kind):
+    state = host_bytes(wm_inputs.make_cache(wm_inputs.TINY))
+    got, _ = ship(wm, state, kind, f"tiny kind={kind}")
+    say(f"[v2] tiny ratio {got.size / state.size:.4f}")
+
+
+def _edge_states():
+    rng = np.random.default_rng(7)
+    n = 3 * CH // 2
+    out = {}
+    out["constant"] = np.full(n, 0x3F80, np.uint16).view(np.uint8)
+    out["random_bits"] = rng.integers(0, 1 << 16, n, dtype=np.uint16).view(np.uint8)
+    out["all_patterns"] = np.arange(1 << 16, dtype=np.uint16).view(np.uint8).copy()
+    sp = np.array([0x0000, 0x8000, 0x7F80, 0xFF80, 0x7FC1, 0x0001, 0x8001, 0x3F80], np.uint16)
+    out["special"] = sp[rng.integers(0, sp.size, n)].view(np.uint8)
+    t = (rng.standard_t(3, n) * 10).astype(np.float32)
+    out["student_t"] = (t.view(np.uint32) >> 16).astype(np.uint16).view(np.uint8)
+    x = (rng.standard_normal(n) * 2).astype(np.float32)
+    bf = (x.view(np.uint32) >> 16).astype(np.uint16).view(np.uint8)
+    out["tail_5536"] = bf[: 2 * CH + 5536].copy()
+    out["tail_4098"] = bf[: 2 * CH + 4098].copy()  # a row piece straddles the end
+    out["one_word_tail"] = bf[: CH + 2].copy()
+    out["two_exponents"] = np.where(rng.random(n) < 0.9, 0x3F80, 0x4000).astype(np.uint16).view(np.uint8)
+    return out
+
+
+@pytest.mark.parametrize("name", list(_edge_states().keys()))
+def test_edge_cases(wm, name):
+    state = _edge_states()[name]
+    got, _ = ship(wm, state, 0, name)
+    modes = got[64]
+    say(f"[v2] {name}: {state.size} B -> {got.size} B, first record mode {modes}")
+
+
+def test_dirty_list(wm):
+    prev, cur, ids = wm_inputs.tiny_step("cuda")
+    h = host_bytes(cur)
+    m = mover(h.size)
+    m.checksum(cur)
+    m.diff(cur, prev)
+    m.encode(cur, dirty_only=True)
+    torch.cuda.synchronize()
+    idx = m.dirty_host()
+    want = oracle.encode(0, h, CH, idx, ORACLE_THREADS, codec=2)
+    assert np.array_equal(m.payload_host(), want)
+    live = prev.clone().view(-1).view(torch.uint8)
+    m.decode()
+    assert m.commit(live, scatter=True) == wm.WM_OK
+    torch.cuda.synchronize()
+    assert torch.equal(live, cur.view(-1).view(torch.uint8))
+
+
+def test_bit_flips_match_oracle(wm):
+    state = _edge_states()["tail_4098"]
+    good, m = ship(wm, state, 0, "flips")
+    n_rec = int(good[24:28].view(np.uint32)[0])
+    total = int(good[32:40].view(np.uint64)[0])
+    table = total - 16 * n_rec
+    rng = np.random.default_rng(11)
+    # header, table, every record's header, tables, streams and planes
+    positions = [3, 30, 45, 61, table + 5, table + 16 * (n_rec - 1) + 9]
+    positions += list(rng.integers(64, table, 40))
+    for pos in positions:
+        for bit in (0, 5):
+            bad = good.copy()
+            bad[pos] ^= 1 << bit
+            m.payload[: bad.size] = torch.from_numpy(bad).cuda()
+            m.decode()
+            torch.cuda.synchronize()
+            v = int(m.verdict.item())
+            v_o, _, rs_o = oracle.decode_verify(0, bad, state.size, CH, m.staging.numel(),
+                                                ORACLE_THREADS, codec=2)
+            assert v == v_o and v != 0, (pos, bit, v, v_o)
+            if v_o & 3 == 0:
+                assert np.array_equal(u32(m.rec_status)[:n_rec], rs_o[:n_rec]), (pos, bit)
+
+
+def test_production_full_ship(wm):
+    state = wm_inputs.make_cache(wm_inputs.PRODUCTION, "cuda")
+    nbytes = state.numel() * 2
+    m = mover(nbytes)
+    m.checksum(state)
+    m.encode(state)
+    torch.cuda.synchronize()
+    got = m.payload_host()
+    h = host_bytes(state)
+    want = oracle.encode(0, h, CH, None, ORACLE_THREADS, codec=2)
+    assert got.size == want.size
+    if not np.array_equal(got, want):
+        bad = np.nonzero(got != want)[0]
+        raise AssertionError(f"{bad.size} bytes differ, first {bad[:8].tolist()}")
+    say(f"[v2] production ratio {got.size / nbytes:.5f}")
+    del want, h
+    m.decode()
+    assert m.commit(None, scatter=False) == wm.WM_OK
+    torch.cuda.synchronize()
+    assert torch.equal(m.staging[:nbytes], state.view(-1).view(torch.uint8))
