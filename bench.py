@@ -42,6 +42,8 @@ def parse():
                     help="skip the active-generation step measurement")
     ap.add_argument("--no-manifest", action="store_true",
                     help="skip the 450-leaf flatten/rehydrate measurement")
+    ap.add_argument("--no-v2", action="store_true",
+                    help="skip the format v2 (Huffman exponent codec) measurement")
     ap.add_argument("--no-receive", action="store_true",
                     help="skip the pipelined receive measurement")
     ap.add_argument("--no-precopy", action="store_true",
@@ -168,6 +170,31 @@ def cpu_baseline(host_state, nbytes_chunk=65536, target_s=12.0):
                       f"cache ({m * nbytes_chunk} B); encode + decode_verify + "
                       f"commit, {dt:.1f} s",
             "cpu_model": cpu}
+
+
+def codec_v2_run(torch, state, nbytes, crc, dev, one):
+    """Format v2 (per-chunk Huffman codes of the exponents) on the production
+    cache: full-ship encode with the CRCs computed in the call (checksum,
+    plan, offset scan, write), decode with verification, and the payload
+    ratio next to format v1's."""
+    from paper_2607_10389_amd import Mover, WM_CODEC_EXPHUF, WM_OK
+
+    m = Mover(nbytes, crc, dev, codec=WM_CODEC_EXPHUF)
+    m.encode(state, with_crc=False)
+    m.decode()
+    if m.commit(None, scatter=False) != WM_OK:
+        raise RuntimeError("format v2 payload did not verify")
+    torch.cuda.synchronize()
+    if not torch.equal(m.staging[:nbytes], state.view(-1).view(torch.uint8)):
+        raise RuntimeError("format v2 decode differs from the source")
+    pb = int(m.payload_bytes.item())
+    return {
+        "workload": "production-size cache, full ship, format v2",
+        "payload_bytes": pb,
+        "compression_ratio": round(pb / nbytes, 5),
+        "wm_encode": one("enc", lambda: m.encode(state, with_crc=False), nbytes + pb),
+        "wm_decode_verify": one("dec", lambda: m.decode(), pb + nbytes),
+    }
 
 
 def receive_runs(torch, m_src, nbytes, crc, dev):
@@ -493,6 +520,9 @@ def main():
                                 2 * total),
         }
         del leaves, flat, back
+
+    if not args.no_v2:
+        out["codec_v2"] = codec_v2_run(torch, state, nbytes, args.crc, dev, one)
 
     if not args.no_receive:
         out["receive"] = receive_runs(torch, m, nbytes, args.crc, dev)

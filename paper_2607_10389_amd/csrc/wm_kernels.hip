@@ -2040,110 +2040,209 @@ __device__ __forceinline__ uint32_t word_of(const uint4 &x, int j) {
 __device__ __forceinline__ uint32_t exp_of(uint32_t w) { return (w >> 7) & 255u; }
 __device__ __forceinline__ uint32_t sm_of(uint32_t w) { return ((w >> 8) & 0x80u) | (w & 0x7Fu); }
 
-// One plan per item: exponent histogram, code lengths (the oracle's
-// construction, run by one thread: leaves sorted by (count, symbol), the two
-// lightest nodes merged with a leaf before an internal node of equal weight,
-// counts halved while a length exceeds kHufMaxLen), stream byte counts and
-// the mode.
-__global__ __launch_bounds__(512) void k_huf_plan(const uint8_t *__restrict__ state, ChunkGeom g,
-                                                  const uint32_t *__restrict__ idx,
-                                                  const uint32_t *__restrict__ n_idx,
-                                                  uint8_t *__restrict__ plans, WsCtl *ctl) {
-  __shared__ uint32_t hist[256], wt[256];
-  __shared__ uint16_t order[256];
-  __shared__ uint32_t nw[511];
-  __shared__ int16_t parent[511];
-  __shared__ uint8_t depth[511];
-  __shared__ uint8_t lens[256];
-  __shared__ uint32_t red[kWaves];
-  __shared__ uint32_t sh_k;
-  const uint32_t t = threadIdx.x;
-  const Lane l = lane_info();
+// Ordering of LDS accesses between the lanes of one wave.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The v2 encoder kernels take one chunk per wave, kHufWaves waves per
+// workgroup, each with this scratch (static LDS).
+constexpr int kHufWaves = 8;
+struct HufWave {
+  uint32_t hist[256];
+  uint32_t wt[256];     // weights of the length construction
+  uint32_t nw[512];     // node weights; canonical codes in the write kernel
+  uint32_t key[256];    // weight << 8 | symbol of the nonzero symbols
+  uint16_t sym[256];    // nonzero symbols
+  uint16_t order[256];  // nonzero symbols by (weight, symbol)
+  uint16_t parent[512];
+  uint8_t depth[512];
+  uint8_t lens[256];
+};
+static_assert(sizeof(HufWave) * kHufWaves <= 65536, "v2 encoder scratch");
+
+// Piece p (0..4095) of a chunk of len bytes: its 16 bytes, zero past len.
+__device__ __forceinline__ uint4 huf_piece(const uint8_t *base, Rsrc r, uint32_t len, uint32_t p) {
+  const uint32_t o = 16u * p;
+  if (o + 16u <= len) return buf16<kNt>(r, o);
+  return o < len ? load16_partial(base + o, len - o) : make_uint4(0, 0, 0, 0);
+}
+
+// Pieces p0 + 64 h (h = 0..7) of a chunk of len bytes, all loads in flight
+// together; zero past len.
+__device__ __forceinline__ void huf_pieces8(const uint8_t *base, Rsrc r, uint32_t len, uint32_t p0,
+                                            uint4 (&x)[8]) {
+#pragma unroll
+  for (int h = 0; h < 8; ++h) x[h] = buf16<kNt>(r, 16u * (p0 + 64u * h));
+  if (len & 15u) {
+#pragma unroll
+    for (int h = 0; h < 8; ++h) {
+      const uint32_t o = 16u * (p0 + 64u * h);
+      if (o < len && o + 16u > len) x[h] = load16_partial(base + o, len - o);
+    }
+  }
+}
+
+// Code lengths of the counts in W.hist (the oracle's construction: leaves
+// sorted by (count, symbol), the two lightest nodes merged with a leaf taken
+// before an internal node of equal weight, a symbol's length its depth;
+// counts halved while the longest exceeds kHufMaxLen).  Returns the longest
+// length (0 for a single symbol, which is then W.order[0]).
+__device__ uint32_t huf_lengths_wave(HufWave &W, uint32_t lane) {
+  for (int q = 0; q < 4; ++q) W.wt[q * 64 + lane] = W.hist[q * 64 + lane];
+  for (;;) {
+    wave_sync();
+    uint32_t m = 0;
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t s = q * 64 + lane, w = W.wt[s];
+      const unsigned long long msk = __ballot(w != 0u);
+      if (w) {
+        const uint32_t i = m + lanes_below(msk);
+        W.sym[i] = (uint16_t)s;
+        W.key[i] = (w << 8) | s;
+      }
+      m += (uint32_t)__popcll(msk);
+      W.lens[s] = 0;
+    }
+    wave_sync();
+    for (uint32_t i = lane; i < m; i += 64u) {  // rank by (weight, symbol)
+      const uint32_t ki = W.key[i];
+      uint32_t rank = 0;
+      for (uint32_t j = 0; j < m; ++j) rank += W.key[j] < ki ? 1u : 0u;
+      W.order[rank] = W.sym[i];
+    }
+    wave_sync();
+    uint32_t longest = 0;
+    if (m >= 2 && m <= 64) {
+      // the same construction in registers: leaf i in lane i, internal node
+      // j (node m + j) in lane j; picks read lanes at uniform indices
+      const uint32_t kInf = 0xFFFFFFFFu;
+      const uint32_t leafw = lane < m ? W.wt[W.order[lane]] : kInf;
+      uint32_t intw = kInf, par_leaf = 0, par_int = 0;
+      uint32_t li = 0, ii = 0, n_int = 0;
+      for (uint32_t s2 = 0; s2 + 1 < m; ++s2) {
+        uint32_t wsum = 0;
+        for (int q = 0; q < 2; ++q) {
+          const uint32_t wl = li < m ? (uint32_t)__builtin_amdgcn_readlane((int)leafw, (int)li) : kInf;
+          const uint32_t wi = ii < n_int ? (uint32_t)__builtin_amdgcn_readlane((int)intw, (int)ii) : kInf;
+          if (li < m && (ii >= n_int || wl <= wi)) {
+            par_leaf = lane == li ? n_int : par_leaf;
+            wsum += wl;
+            ++li;
+          } else {
+            par_int = lane == ii ? n_int : par_int;
+            wsum += wi;
+            ++ii;
+          }
+        }
+        intw = lane == n_int ? wsum : intw;
+        ++n_int;
+      }
+      uint32_t dint = 0;  // depth of internal node j; the root (last) is 0
+      for (int32_t j = (int32_t)n_int - 2; j >= 0; --j) {
+        const uint32_t p = (uint32_t)__builtin_amdgcn_readlane((int)par_int, j);
+        const uint32_t dp = (uint32_t)__builtin_amdgcn_readlane((int)dint, (int)p);
+        dint = lane == (uint32_t)j ? dp + 1u : dint;
+      }
+      const uint32_t dleaf = (uint32_t)__shfl((int)dint, (int)(lane < m ? par_leaf : 0u), 64) + 1u;
+      if (lane < m) W.lens[W.order[lane]] = (uint8_t)dleaf;
+      longest = wave_max(lane < m ? dleaf : 0u);
+    } else if (lane == 0 && m >= 2) {
+      for (uint32_t i = 0; i < m; ++i) W.nw[i] = W.wt[W.order[i]];
+      uint32_t li = 0, ii = m, n_int = m;
+      for (uint32_t s2 = 0; s2 + 1 < m; ++s2) {
+        uint32_t pick[2];
+        for (int q = 0; q < 2; ++q) {
+          if (li < m && (ii >= n_int || W.nw[li] <= W.nw[ii])) pick[q] = li++;
+          else pick[q] = ii++;
+        }
+        W.nw[n_int] = W.nw[pick[0]] + W.nw[pick[1]];
+        W.parent[pick[0]] = W.parent[pick[1]] = (uint16_t)n_int;
+        ++n_int;
+      }
+      W.depth[n_int - 1] = 0;
+      for (int32_t i = (int32_t)n_int - 2; i >= 0; --i) W.depth[i] = (uint8_t)(W.depth[W.parent[i]] + 1);
+      for (uint32_t i = 0; i < m; ++i) {
+        W.lens[W.order[i]] = W.depth[i];
+        longest = max(longest, (uint32_t)W.depth[i]);
+      }
+    }
+    longest = uniform(__builtin_amdgcn_readfirstlane(longest));
+    wave_sync();
+    if (longest <= kHufMaxLen) return longest;
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t s = q * 64 + lane;
+      if (W.wt[s]) W.wt[s] = (W.wt[s] + 1u) >> 1;
+    }
+  }
+}
+
+// One plan per item (one wave per chunk): exponent histogram, code lengths,
+// stream byte counts and the mode.  Stream s = q * 64 + lane covers rows
+// 8q..8q+7, words 8 lane..8 lane+7 of each.
+__global__ __launch_bounds__(64 * kHufWaves) void k_huf_plan(
+    const uint8_t *__restrict__ state, ChunkGeom g, const uint32_t *__restrict__ idx,
+    const uint32_t *__restrict__ n_idx, uint8_t *__restrict__ plans, WsCtl *ctl) {
+  __shared__ HufWave sw[kHufWaves];
+  const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
+  HufWave &W = sw[wave];
   const uint32_t n_items = idx ? min(*n_idx, g.n_chunks) : g.n_chunks;
-  for (uint32_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+  for (uint32_t item = blockIdx.x * kHufWaves + wave; item < n_items;
+       item += gridDim.x * kHufWaves) {
     uint32_t c = idx ? idx[item] : item;
     const bool bad = c >= g.n_chunks || (idx && item > 0 && idx[item - 1] >= c);
     if (bad) c = 0;
-    const uint32_t len = chunk_len(g, c), n = len / 2, w0 = l.off0 >> 1;
-    uint4 d[kRows];
-    load_chunk(state + (uint64_t)c * kChunk, len, l, d);
-    if (t < 256) hist[t] = 0;
-    __syncthreads();
+    const uint32_t len = chunk_len(g, c), n = len / 2;
+    const uint8_t *base = state + (uint64_t)c * kChunk;
+    const Rsrc rs = rsrc(base, len);
+    for (int q = 0; q < 4; ++q) W.hist[q * 64 + lane] = 0;
+    wave_sync();
+    for (uint32_t q = 0; q < 8u; ++q) {
+      uint4 x[8];
+      huf_pieces8(base, rs, len, 512u * q + lane, x);
 #pragma unroll
-    for (int h = 0; h < kRows; ++h)
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (w0 + h * (kRow / 2) + j < n) atomicAdd(&hist[exp_of(word_of(d[h], j))], 1u);
-    __syncthreads();
-    if (t < 256) wt[t] = hist[t];
-    for (;;) {
-      __syncthreads();
-      const uint32_t my = t < 256 ? wt[t] : 0u;
-      if (t < 256) lens[t] = 0;
-      if (my) {
-        uint32_t rank = 0;
-        for (uint32_t s2 = 0; s2 < 256; ++s2) {
-          const uint32_t o = wt[s2];
-          rank += (o != 0u && (o < my || (o == my && s2 < t))) ? 1u : 0u;
-        }
-        order[rank] = (uint16_t)t;
-      }
-      const uint32_t m = (uint32_t)__syncthreads_count(my != 0u);
-      if (t == 0) {
-        uint32_t longest = 0;
-        if (m >= 2) {
-          for (uint32_t i = 0; i < m; ++i) nw[i] = wt[order[i]];
-          uint32_t li = 0, ii = m, n_int = m;
-          for (uint32_t s2 = 0; s2 + 1 < m; ++s2) {
-            uint32_t pick[2];
-            for (int q = 0; q < 2; ++q) {
-              if (li < m && (ii >= n_int || nw[li] <= nw[ii])) pick[q] = li++;
-              else pick[q] = ii++;
-            }
-            nw[n_int] = nw[pick[0]] + nw[pick[1]];
-            parent[pick[0]] = parent[pick[1]] = (int16_t)n_int;
-            ++n_int;
-          }
-          depth[n_int - 1] = 0;
-          for (int32_t i = (int32_t)n_int - 2; i >= 0; --i) depth[i] = (uint8_t)(depth[parent[i]] + 1);
-          for (uint32_t i = 0; i < m; ++i) {
-            lens[order[i]] = depth[i];
-            longest = max(longest, (uint32_t)depth[i]);
-          }
-        }
-        sh_k = longest;
-      }
-      __syncthreads();
-      if (sh_k <= kHufMaxLen) break;
-      if (t < 256 && wt[t]) wt[t] = (wt[t] + 1u) >> 1;
-    }
-    const uint32_t k = sh_k;
-    uint32_t bits = 0;
-    if (k) {
-#pragma unroll
-      for (int h = 0; h < kRows; ++h)
+      for (int h = 0; h < 8; ++h) {
+        const uint32_t i0 = 8u * (512u * q + lane + 64u * h);
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-          if (w0 + h * (kRow / 2) + j < n) bits += lens[exp_of(word_of(d[h], j))];
+          if (i0 + j < n) atomicAdd(&W.hist[exp_of(word_of(x[h], j))], 1u);
+      }
     }
-    const uint32_t sb_t = (bits + 7u) >> 3;
-    const uint32_t incl = wave_incl_scan(sb_t);
-    if (l.lane == 63u) red[l.wave] = incl;
+    wave_sync();
+    const uint32_t k = huf_lengths_wave(W, lane);
     uint8_t *P = plans + (uint64_t)item * kHufPlanBytes;
-    P[176 + t] = (uint8_t)sb_t;
-    if (t < 128) P[48 + t] = (uint8_t)(lens[2 * t] | (lens[2 * t + 1] << 4));
-    __syncthreads();
-    if (t == 0) {
-      uint32_t sb = 0;
-      for (int w = 0; w < kWaves; ++w) sb += red[w];
-      const uint64_t raw = raw_rec_size(n), hs = huf_rec_size(n, k, sb);
+    uint32_t tot = 0;
+    for (uint32_t q = 0; q < 8u; ++q) {  // stream q * 64 + lane
+      uint32_t bits = 0;
+      if (k) {
+        uint4 x[8];
+        huf_pieces8(base, rs, len, 512u * q + lane, x);
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+          const uint32_t i0 = 8u * (512u * q + lane + 64u * h);
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            if (i0 + j < n) bits += W.lens[exp_of(word_of(x[h], j))];
+        }
+      }
+      const uint32_t sb = (bits + 7u) >> 3;
+      P[176 + q * 64 + lane] = (uint8_t)sb;
+      tot += sb;
+    }
+    for (int o = 32; o > 0; o >>= 1) tot += (uint32_t)__shfl_xor((int)tot, o, 64);
+    P[48 + 2 * lane] = (uint8_t)(W.lens[4 * lane] | (W.lens[4 * lane + 1] << 4));
+    P[48 + 2 * lane + 1] = (uint8_t)(W.lens[4 * lane + 2] | (W.lens[4 * lane + 3] << 4));
+    if (lane == 0) {
+      const uint64_t raw = raw_rec_size(n), hs = huf_rec_size(n, k, tot);
       const bool huf = hs < raw;
       const uint64_t size = huf ? hs : raw;
       HufPlan hp;
       hp.mode = huf ? 2u : 0u;
       hp.k = huf ? k : 0u;
-      hp.base = huf && k == 0 ? (uint32_t)order[0] : 0u;
-      hp.sb = huf ? sb : 0u;
+      hp.base = huf && k == 0 ? (uint32_t)W.order[0] : 0u;
+      hp.sb = huf ? tot : 0u;
       hp.size_lo = (uint32_t)size;
       hp.size_hi = (uint32_t)(size >> 32);
       hp.off_lo = hp.off_hi = 0;
@@ -2153,7 +2252,7 @@ __global__ __launch_bounds__(512) void k_huf_plan(const uint8_t *__restrict__ st
       *reinterpret_cast<HufPlan *>(P) = hp;
       if (bad) atomicOr(&ctl->error, 2u);
     }
-    __syncthreads();
+    wave_sync();
   }
 }
 
@@ -2193,32 +2292,29 @@ __global__ __launch_bounds__(1024) void k_huf_scan(const uint32_t *__restrict__ 
   }
 }
 
-// Write every planned record, its table entry (staged in the workspace) and
-// the entry's CRC.
-__global__ __launch_bounds__(512) void k_huf_write(const uint8_t *__restrict__ state, ChunkGeom g,
-                                                   const uint32_t *__restrict__ n_idx,
-                                                   const uint32_t *__restrict__ crcs,
-                                                   const uint8_t *__restrict__ plans,
-                                                   uint8_t *__restrict__ payload, uint8_t *ws,
-                                                   WsLayout L) {
-  __shared__ uint8_t lens[256];
-  __shared__ uint16_t code[256];
-  __shared__ uint32_t red[kWaves];
-  const uint32_t t = threadIdx.x;
-  const Lane l = lane_info();
+// Write every planned record (one wave per chunk), its table entry (staged
+// in the workspace) and the entry's CRC.
+__global__ __launch_bounds__(64 * kHufWaves) void k_huf_write(
+    const uint8_t *__restrict__ state, ChunkGeom g, const uint32_t *__restrict__ n_idx,
+    const uint32_t *__restrict__ crcs, const uint8_t *__restrict__ plans,
+    uint8_t *__restrict__ payload, uint8_t *ws, WsLayout L) {
+  __shared__ HufWave sw[kHufWaves];
+  const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
+  HufWave &W = sw[wave];
   uint4 *tab_ws = reinterpret_cast<uint4 *>(ws + L.table);
   uint32_t *ecrc = reinterpret_cast<uint32_t *>(ws + L.entry_crc);
   const uint32_t n_items = n_idx ? min(*n_idx, g.n_chunks) : g.n_chunks;
-  for (uint32_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+  for (uint32_t item = blockIdx.x * kHufWaves + wave; item < n_items;
+       item += gridDim.x * kHufWaves) {
     const uint8_t *P = plans + (uint64_t)item * kHufPlanBytes;
     const HufPlan hp = *reinterpret_cast<const HufPlan *>(P);
     if (hp.bad) continue;  // the payload is discarded (ctl->error)
-    const uint32_t c = hp.c, len = chunk_len(g, c), n = len / 2, w0 = l.off0 >> 1;
+    const uint32_t c = hp.c, len = chunk_len(g, c), n = len / 2;
+    const uint8_t *base = state + (uint64_t)c * kChunk;
+    const Rsrc rs = rsrc(base, len);
     const uint64_t off = ((uint64_t)hp.off_hi << 32) | hp.off_lo;
     uint8_t *rec = payload + off;
-    uint4 d[kRows];
-    load_chunk(state + (uint64_t)c * kChunk, len, l, d);
-    if (t == 0) {
+    if (lane == 0) {
       uint32_t hw[4] = {hp.mode | (hp.k << 8) | (hp.base << 16), n, hp.sb, 0u};
       hw[3] = crc_words_g(g.crc_kind, hw, 3);
       *reinterpret_cast<uint4 *>(rec) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
@@ -2226,83 +2322,119 @@ __global__ __launch_bounds__(512) void k_huf_write(const uint8_t *__restrict__ s
       tab_ws[item] = make_uint4(ew[0], ew[1], ew[2], ew[3]);
       ecrc[item] = crc_words_g(g.crc_kind, ew, 4);
     }
-    uint64_t smo;  // sign/mantissa plane offset
-    if (hp.mode == 0) {
-      smo = 16u + pad16(n);
-#pragma unroll
-      for (int h = 0; h < kRows; ++h) {
-        const uint32_t i0 = w0 + h * (kRow / 2);
-        uint32_t e[2] = {0, 0};
-#pragma unroll
-        for (int j = 0; j < 8; ++j) e[j >> 2] |= exp_of(word_of(d[h], j)) << (8 * (j & 3));
-        if (i0 + 8u <= n) {
-          *reinterpret_cast<uint2 *>(rec + 16 + i0) = make_uint2(e[0], e[1]);
-        } else {
-          for (uint32_t b = 0; i0 + b < n; ++b) rec[16 + i0 + b] = (uint8_t)(e[b >> 2] >> (8 * (b & 3)));
-        }
+    const bool hufk = hp.mode == 2 && hp.k > 0;
+    const uint64_t smo = hp.mode == 0 ? 16u + pad16(n) : (hufk ? kHufHead + pad16(hp.sb) : 16u);
+    if (hufk) {
+      // tables, and the canonical codes: per length, consecutive values in
+      // symbol order, the first one ((previous first + previous count) << 1)
+      rec[16 + 2 * lane] = P[48 + 2 * lane];
+      rec[16 + 2 * lane + 1] = P[48 + 2 * lane + 1];
+      for (int q = 0; q < 8; ++q) rec[16 + 128 + q * 64 + lane] = P[176 + q * 64 + lane];
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t s = q * 64 + lane;
+        W.lens[s] = (uint8_t)((P[48 + (s >> 1)] >> (4 * (s & 1))) & 15u);
       }
-      if (t < 16u && n + t < pad16(n)) rec[16 + n + t] = 0;
-    } else if (hp.k == 0) {
-      smo = 16;
-    } else {
-      smo = kHufHead + pad16(hp.sb);
-      if (t < 128u) rec[16 + t] = P[48 + t];
-      rec[16 + 128 + t] = P[176 + t];
-      if (t < 256u) lens[t] = (uint8_t)((P[48 + (t >> 1)] >> (4 * (t & 1))) & 15u);
-      __syncthreads();
-      if (t == 0) {  // canonical codes: consecutive values in (length, symbol) order
-        uint32_t bl[kHufMaxLen + 1] = {0}, nx[kHufMaxLen + 1] = {0};
-        for (uint32_t s2 = 0; s2 < 256; ++s2) bl[lens[s2]]++;
-        bl[0] = 0;
-        uint32_t cd = 0;
-        for (uint32_t b = 1; b <= kHufMaxLen; ++b) {
-          cd = (cd + bl[b - 1]) << 1;
-          nx[b] = cd;
+      wave_sync();
+      uint32_t first = 0, prev_cnt = 0;
+      for (uint32_t b = 1; b <= hp.k; ++b) {
+        first = (first + prev_cnt) << 1;
+        uint32_t run = 0;
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t s = q * 64 + lane;
+          const bool is = W.lens[s] == b;
+          const unsigned long long msk = __ballot(is);
+          if (is) W.nw[s] = first + run + lanes_below(msk);
+          run += (uint32_t)__popcll(msk);
         }
-        for (uint32_t s2 = 0; s2 < 256; ++s2) code[s2] = (uint16_t)(lens[s2] ? nx[lens[s2]]++ : 0u);
+        prev_cnt = run;
       }
-      const uint32_t sb_t = P[176 + t];
-      const uint32_t incl = wave_incl_scan(sb_t);
-      if (l.lane == 63u) red[l.wave] = incl;
-      __syncthreads();
-      uint32_t so = incl - sb_t;
-      for (uint32_t w = 0; w < l.wave; ++w) so += red[w];
-      uint8_t *st = rec + kHufHead + so;
-      uint64_t acc = 0;
-      uint32_t nb = 0, ob = 0;
-#pragma unroll
-      for (int h = 0; h < kRows; ++h)
+      wave_sync();
+    }
+    if (hp.mode == 0) {  // exponent plane, sign/mantissa plane
+      for (uint32_t it = 0; it < kChunk / 1024u; ++it) {
+        const uint32_t p = it * 64u + lane, i0 = 8u * p;
+        if (i0 >= n) break;
+        const uint4 x = huf_piece(base, rs, len, p);  // (RAW records are rare)
+        uint32_t e[2] = {0, 0}, sm[2] = {0, 0};
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          if (w0 + h * (kRow / 2) + j < n) {
-            const uint32_t e = exp_of(word_of(d[h], j)), ln = lens[e];
-            acc |= (uint64_t)(__builtin_bitreverse32(code[e]) >> (32u - ln)) << nb;
-            nb += ln;
-            while (nb >= 8u) {  // (the plan counted these bytes: ob stays below sb_t)
-              if (ob < sb_t) st[ob] = (uint8_t)acc;
-              ++ob;
-              acc >>= 8;
-              nb -= 8u;
-            }
+          const uint32_t w = word_of(x, j);
+          e[j >> 2] |= exp_of(w) << (8 * (j & 3));
+          sm[j >> 2] |= sm_of(w) << (8 * (j & 3));
+        }
+        if (i0 + 8u <= n) {
+          *reinterpret_cast<uint2 *>(rec + 16 + i0) = make_uint2(e[0], e[1]);
+          *reinterpret_cast<uint2 *>(rec + smo + i0) = make_uint2(sm[0], sm[1]);
+        } else {
+          for (uint32_t b = 0; i0 + b < n; ++b) {
+            rec[16 + i0 + b] = (uint8_t)(e[b >> 2] >> (8 * (b & 3)));
+            rec[smo + i0 + b] = (uint8_t)(sm[b >> 2] >> (8 * (b & 3)));
           }
         }
-      if (nb && ob < sb_t) st[ob] = (uint8_t)acc;
-      if (t < 16u && hp.sb + t < pad16(hp.sb)) rec[kHufHead + hp.sb + t] = 0;
-    }
-#pragma unroll
-    for (int h = 0; h < kRows; ++h) {
-      const uint32_t i0 = w0 + h * (kRow / 2);
-      uint32_t sm[2] = {0, 0};
-#pragma unroll
-      for (int j = 0; j < 8; ++j) sm[j >> 2] |= sm_of(word_of(d[h], j)) << (8 * (j & 3));
-      if (i0 + 8u <= n) {
-        *reinterpret_cast<uint2 *>(rec + smo + i0) = make_uint2(sm[0], sm[1]);
-      } else {
-        for (uint32_t b = 0; i0 + b < n; ++b) rec[smo + i0 + b] = (uint8_t)(sm[b >> 2] >> (8 * (b & 3)));
       }
+      if (lane < 16u && n + lane < pad16(n)) rec[16 + n + lane] = 0;
+    } else {
+      // streams (HUF k >= 1) and the sign/mantissa plane, rows 8q..8q+7 at a
+      // time; stream q * 64 + lane starts after the earlier streams
+      uint32_t sbase = 0;
+      for (uint32_t q = 0; q < 8u; ++q) {
+        const uint32_t sb = hufk ? P[176 + q * 64 + lane] : 0u;
+        const uint32_t incl = wave_incl_scan(sb);
+        uint8_t *st = rec + kHufHead + sbase + (incl - sb);
+        sbase += uniform(__builtin_amdgcn_readlane(incl, 63));
+        // the stream's bytes go out as whole dwords where the payload
+        // address is 4-aligned, bytewise at its two ends (a neighbouring
+        // stream writes the other bytes of a shared dword)
+        const uint32_t lead = (4u - ((uint32_t)(uintptr_t)st & 3u)) & 3u;
+        uint64_t acc = 0;
+        uint32_t nb = 0, ob = 0;
+        uint4 xs[8];
+        huf_pieces8(base, rs, len, 512u * q + lane, xs);
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+          const uint32_t p = (8u * q + h) * 64u + lane, i0 = 8u * p;
+          const uint4 x = xs[h];
+          uint32_t sm[2] = {0, 0};
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const uint32_t w = word_of(x, j);
+            sm[j >> 2] |= sm_of(w) << (8 * (j & 3));
+            if (hufk && i0 + j < n) {
+              const uint32_t e = exp_of(w), ln = W.lens[e];
+              acc |= (uint64_t)(__builtin_bitreverse32(W.nw[e]) >> (32u - ln)) << nb;
+              nb += ln;
+              // (the plan counted these bytes: ob stays below sb)
+              while (ob < lead && nb >= 8u) {
+                if (ob < sb) st[ob] = (uint8_t)acc;
+                ++ob;
+                acc >>= 8;
+                nb -= 8u;
+              }
+              if (ob >= lead && nb >= 32u) {
+                if (ob + 4u <= sb) *reinterpret_cast<uint32_t *>(st + ob) = (uint32_t)acc;
+                ob += 4u;
+                acc >>= 32;
+                nb -= 32u;
+              }
+            }
+          }
+          if (i0 + 8u <= n) {
+            *reinterpret_cast<uint2 *>(rec + smo + i0) = make_uint2(sm[0], sm[1]);
+          } else {
+            for (uint32_t b = 0; i0 + b < n; ++b) rec[smo + i0 + b] = (uint8_t)(sm[b >> 2] >> (8 * (b & 3)));
+          }
+        }
+        while (nb) {  // the last bytes, the final one's unused bits zero
+          if (ob < sb) st[ob] = (uint8_t)acc;
+          ++ob;
+          acc >>= 8;
+          nb = nb > 8u ? nb - 8u : 0u;
+        }
+      }
+      if (hufk && lane < 16u && hp.sb + lane < pad16(hp.sb)) rec[kHufHead + hp.sb + lane] = 0;
     }
-    if (t < 16u && n + t < pad16(n)) rec[smo + n + t] = 0;
-    __syncthreads();
+    if (lane < 16u && n + lane < pad16(n)) rec[smo + n + lane] = 0;
+    wave_sync();
   }
 }
 
@@ -2322,8 +2454,29 @@ struct HufMeta {
   uint32_t kraft, maxlen, bad, hufbad;
   uint32_t bl[kHufMaxLen + 1], first[kHufMaxLen + 1], start[kHufMaxLen + 1];
   uint32_t wsum[kWaves];
+  uint32_t wcnt[4][kHufMaxLen + 1];  // symbols of each length per 64 symbols
 };
 static_assert(kHdMeta + sizeof(HufMeta) <= kLdsLowBytes, "v2 decoder scratch fits the low region");
+
+// What the control lane reads of record r: its table entry, the previous
+// entry's chunk, the record's end, and its header when the entry's offsets
+// leave room for one (read only then).
+struct HufFetch {
+  uint32_t ew[4], prevc, hdr[4], has_hdr;
+  uint64_t end;
+};
+__device__ __forceinline__ HufFetch huf_fetch(const uint8_t *__restrict__ payload, uint64_t table_off,
+                                              uint32_t n_rec, uint32_t r) {
+  HufFetch f;
+  const uint8_t *e = payload + table_off + 16ull * r;
+  for (int i = 0; i < 4; ++i) f.ew[i] = ld_u32(e + 4 * i);
+  f.prevc = r > 0 ? ld_u32(e - 16) : 0u;
+  f.end = r + 1 < n_rec ? ld_u64(e + 24) : table_off;
+  const uint64_t off = f.ew[2] | ((uint64_t)f.ew[3] << 32);
+  f.has_hdr = !(off & 15u) && off < f.end && f.end <= table_off && f.end - off >= 16u;
+  for (int i = 0; i < 4; ++i) f.hdr[i] = f.has_hdr ? ld_u32(payload + off + 4 * i) : 0u;
+  return f;
+}
 
 // One record per workgroup step: the control lane checks the table entry and
 // the record header; the data waves build the decode table, decode their
@@ -2350,15 +2503,17 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
   const bool is_ctl = t >= (uint32_t)kThreads;
   const GLane gl = glane_make();
   const Lane l0 = lane_info();
+  HufFetch fn;  // control lane: the next record's reads, issued a step ahead
+  if (t == (uint32_t)kThreads && blockIdx.x < n_rec) fn = huf_fetch(payload, table_off, n_rec, blockIdx.x);
   for (uint32_t r = blockIdx.x; r < n_rec; r += gridDim.x) {
     const Lane l = lane_fresh(l0);
     if (t == (uint32_t)kThreads) {
-      const uint8_t *e = payload + table_off + 16ull * r;
-      const uint32_t ew[4] = {ld_u32(e), ld_u32(e + 4), ld_u32(e + 8), ld_u32(e + 12)};
+      const HufFetch f = fn;
+      const uint32_t *ew = f.ew;
       const uint32_t c = ew[0];
       const uint64_t off = ew[2] | ((uint64_t)ew[3] << 32);
-      const uint64_t end = r + 1 < n_rec ? ld_u64(e + 24) : table_off;
-      const bool tbad = c >= g.n_chunks || (r > 0 && ld_u32(e - 16) >= c) ||
+      const uint64_t end = f.end;
+      const bool tbad = c >= g.n_chunks || (r > 0 && f.prevc >= c) ||
                         (r == 0 && off != 64u) || (off & 15u) || off >= end || end > table_off;
       ecrc[r] = crc_words(ew, 4);
       M.bad = M.hufbad = M.kraft = M.maxlen = 0;
@@ -2370,11 +2525,10 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
         const uint32_t len = chunk_len(g, c), n = len / 2;
         const uint64_t rl = end - off;
         uint32_t st = 0, mode = 0, k = 0, base = 0, sb = 0;
-        if (rl < 16) {
+        if (rl < 16 || !f.has_hdr) {
           st = 4;
         } else {
-          const uint8_t *rec = payload + off;
-          const uint32_t hw[4] = {ld_u32(rec), ld_u32(rec + 4), ld_u32(rec + 8), ld_u32(rec + 12)};
+          const uint32_t *hw = f.hdr;
           mode = hw[0] & 255u;
           k = (hw[0] >> 8) & 255u;
           base = (hw[0] >> 16) & 255u;
@@ -2404,23 +2558,56 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
       }
     }
     __syncthreads();
+    if (t == (uint32_t)kThreads && r + gridDim.x < n_rec)
+      fn = huf_fetch(payload, table_off, n_rec, r + gridDim.x);
     const uint32_t st0 = uniform(M.st), mode = uniform(M.mode), k = uniform(M.k);
     const uint32_t n = uniform(M.n), sb = uniform(M.sb);
     const uint64_t off = ((uint64_t)uniform(M.off_hi) << 32) | uniform(M.off_lo);
     const uint8_t *rec = payload + off;
     const bool huf = st0 == 0 && mode == 2 && k >= 1;
-    // code lengths and stream byte counts
+    // every load of the record at once: code lengths, stream byte counts,
+    // the streams (into LDS), and the lane's sign/mantissa (RAW: exponent)
+    // bytes, 8 per row
     uint32_t sb_t = 0;
-    if (huf && !is_ctl) {
-      if (t < 128u) {
-        const uint32_t b = rec[16 + t];
-        lens[2 * t] = (uint8_t)(b & 15u);
-        lens[2 * t + 1] = (uint8_t)(b >> 4);
+    uint2 smv[kRows], exv[kRows];
+    const uint64_t smo = mode == 0 ? 16u + pad16(n) : (k ? kHufHead + pad16(sb) : 16u);
+    if (!is_ctl) {
+      if (huf) {
+        if (t < 128u) {
+          const uint32_t b = rec[16 + t];
+          lens[2 * t] = (uint8_t)(b & 15u);
+          lens[2 * t + 1] = (uint8_t)(b >> 4);
+        }
+        sb_t = rec[16 + 128 + t];
+        // (sb < 32 KiB for a record shorter than RAW)
+        const uint8_t *src = rec + kHufHead;
+        const Rsrc rs = rsrc(src, sb);
+        for (uint32_t q = t; 16u * q < sb; q += kThreads) {
+          uint4 v = 16u * q + 16u <= sb ? buf16(rs, 16u * q) : load16_partial(src + 16u * q, sb - 16u * q);
+          *reinterpret_cast<uint4 *>(lds_at(kLdsHufStreams + 16u * q)) = v;
+        }
       }
-      sb_t = rec[16 + 128 + t];
+      const bool ld = st0 == 0 && (mode == 0 || mode == 2);
+      const Rsrc rsm = rsrc(rec + smo, ld ? n : 0u);
+      const Rsrc rex = rsrc(rec + 16, ld && mode == 0 ? n : 0u);
+      const uint32_t w0 = l.off0 >> 1;
+#pragma unroll
+      for (int h = 0; h < kRows; ++h) {
+        const uint32_t i0 = w0 + h * (kRow / 2);
+        smv[h] = buf8(rsm, i0);
+        exv[h] = buf8(rex, i0);
+        if (ld && i0 < n && i0 + 8u > n) {  // the piece that straddles n, bytewise
+          const uint4 v = load16_partial(rec + smo + i0, n - i0);
+          smv[h] = make_uint2(v.x, v.y);
+          if (mode == 0) {
+            const uint4 e = load16_partial(rec + 16 + i0, n - i0);
+            exv[h] = make_uint2(e.x, e.y);
+          }
+        }
+      }
     }
     __syncthreads();
-    uint32_t incl = 0;
+    uint32_t incl = 0, within = 0;
     if (huf && !is_ctl) {
       if (t < 256u) {
         const uint32_t ln = lens[t];
@@ -2429,6 +2616,13 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
           atomicAdd(&M.kraft, 1u << (kHufMaxLen - min(ln, kHufMaxLen)));
           atomicMax(&M.maxlen, ln);
           atomicAdd(&M.bl[min(ln, kHufMaxLen)], 1u);
+        }
+        // the symbol's rank among the same length within its 64 symbols
+#pragma unroll
+        for (uint32_t b = 1; b <= kHufMaxLen; ++b) {
+          const unsigned long long msk = __ballot(ln == b);
+          if (ln == b) within = lanes_below(msk);
+          if (l.lane == 0) M.wcnt[l.wave][b] = (uint32_t)__popcll(msk);
         }
       }
       incl = wave_incl_scan(sb_t);
@@ -2460,40 +2654,35 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
     if (hok && !is_ctl) {
       if (t < 256u && lens[t]) {  // symbols in code order
         const uint32_t ln = lens[t];
-        uint32_t rank = 0;
-        for (uint32_t s2 = 0; s2 < t; ++s2) rank += lens[s2] == ln ? 1u : 0u;
+        uint32_t rank = within;
+        for (uint32_t w = 0; w < l.wave; ++w) rank += M.wcnt[w][ln];
         sorted[M.start[ln] + rank] = (uint8_t)t;
-      }
-      // the streams into LDS (sb < 32 KiB for a record shorter than RAW)
-      const uint8_t *src = rec + kHufHead;
-      const Rsrc rs = rsrc(src, sb);
-      for (uint32_t q = t; 16u * q < sb; q += kThreads) {
-        uint4 v = 16u * q + 16u <= sb ? buf16(rs, 16u * q) : load16_partial(src + 16u * q, sb - 16u * q);
-        *reinterpret_cast<uint4 *>(lds_at(kLdsHufStreams + 16u * q)) = v;
       }
     }
     __syncthreads();
     if (hok && !is_ctl) {  // entry p: the code whose bits, first bit lowest, are p's low bits
+      uint32_t fb[kHufMaxLen + 1], cb[kHufMaxLen + 1], sbx[kHufMaxLen + 1];
+#pragma unroll
+      for (uint32_t b = 1; b <= kHufMaxLen; ++b) {
+        fb[b] = uniform(M.first[b]);
+        cb[b] = b <= k ? uniform(M.bl[b]) : 0u;
+        sbx[b] = uniform(M.start[b]);
+      }
       for (uint32_t p = t; p < (1u << kHufMaxLen); p += kThreads) {
         uint32_t ent = 0;
         const uint32_t rp = __builtin_bitreverse32(p);
-        for (uint32_t b = 1; b <= k; ++b) {
-          const uint32_t q = (rp >> (32u - b)) - M.first[b];
-          if (q < M.bl[b]) {
-            ent = sorted[M.start[b] + q] | (b << 8);
-            break;
-          }
+#pragma unroll
+        for (uint32_t b = kHufMaxLen; b >= 1; --b) {  // the shortest match is the code
+          const uint32_t q = (rp >> (32u - b)) - fb[b];
+          if (q < cb[b]) ent = (sbx[b] + q) | (b << 8) | 0x10000u;
         }
-        tab[p] = (uint16_t)ent;
+        tab[p] = (ent & 0x10000u) ? (uint16_t)(sorted[ent & 255u] | (ent & 0xF00u)) : (uint16_t)0;
       }
     }
     __syncthreads();
     if (!is_ctl) {
       const uint32_t len = uniform(M.len), base = uniform(M.base), w0 = l.off0 >> 1;
       const bool ok = st0 == 0 && (mode == 0 || (mode == 2 && (k == 0 || hok)));
-      const uint64_t smo = mode == 0 ? 16u + pad16(n) : (k ? kHufHead + pad16(sb) : 16u);
-      const Rsrc rsm = rsrc(rec + smo, ok ? n : 0u);
-      const Rsrc rex = rsrc(rec + 16, ok && mode == 0 ? n : 0u);
       const bool dec = ok && mode == 2 && k;
       uint32_t bad = 0;
       // the lane's stream: bits so far in acc (next bit lowest), bytes [pos, end)
@@ -2504,22 +2693,10 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
 #pragma unroll
       for (int h = 0; h < kRows; ++h) {
         const uint32_t i0 = w0 + h * (kRow / 2);
-        // 8 bytes per plane; the piece that straddles n is read bytewise
-        const bool part = ok && i0 < n && i0 + 8u > n;
-        uint2 smv = buf8(rsm, i0);
-        if (part) {
-          const uint4 v = load16_partial(rec + smo + i0, n - i0);
-          smv = make_uint2(v.x, v.y);
-        }
         uint32_t e8[2] = {0, 0};
         if (mode == 0) {
-          uint2 ev = buf8(rex, i0);
-          if (part) {
-            const uint4 v = load16_partial(rec + 16 + i0, n - i0);
-            ev = make_uint2(v.x, v.y);
-          }
-          e8[0] = ev.x;
-          e8[1] = ev.y;
+          e8[0] = exv[h].x;
+          e8[1] = exv[h].y;
         } else if (k == 0) {
           e8[0] = e8[1] = base * 0x01010101u;
         } else if (dec) {
@@ -2555,7 +2732,7 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {
             const int j = 2 * q + hh;
-            const uint32_t smb = ((j < 4 ? smv.x : smv.y) >> (8 * (j & 3))) & 255u;
+            const uint32_t smb = ((j < 4 ? smv[h].x : smv[h].y) >> (8 * (j & 3))) & 255u;
             const uint32_t eb = (e8[j >> 2] >> (8 * (j & 3))) & 255u;
             const uint32_t w = i0 + j < n ? (((smb & 0x80u) << 8) | (eb << 7) | (smb & 0x7Fu)) : 0u;
             v |= w << (16 * hh);
@@ -2866,11 +3043,11 @@ int launch_encode_v2(const void *state, const ChunkGeom &g, const uint32_t *idx,
     crcs = crc_scratch;
   }
   if (g.n_chunks) {
-    const uint32_t grid = min((uint32_t)n_cu * 4u, g.n_chunks);
-    hipLaunchKernelGGL(k_huf_plan, dim3(grid), dim3(512), 0, S(stream), st, g, idx, n_idx, plans,
-                       ctl);
+    const uint32_t grid = min((uint32_t)n_cu * 2u, (g.n_chunks + kHufWaves - 1) / kHufWaves);
+    hipLaunchKernelGGL(k_huf_plan, dim3(grid), dim3(64 * kHufWaves), 0, S(stream), st, g, idx,
+                       n_idx, plans, ctl);
     hipLaunchKernelGGL(k_huf_scan, dim3(1), dim3(1024), 0, S(stream), n_idx, g, plans, ctl);
-    hipLaunchKernelGGL(k_huf_write, dim3(grid), dim3(512), 0, S(stream), st, g, n_idx, crcs,
+    hipLaunchKernelGGL(k_huf_write, dim3(grid), dim3(64 * kHufWaves), 0, S(stream), st, g, n_idx, crcs,
                        static_cast<const uint8_t *>(plans), static_cast<uint8_t *>(payload), wsb,
                        L);
     e = hipGetLastError();
