@@ -83,8 +83,8 @@ def measured_traffic(kernel):
 def counter_pass(args):
     """Exactly one launch of each hot kernel on the production cache, a plain
     device-to-device copy of 1 GiB (the calibration for FETCH_SIZE and
-    WRITE_SIZE), then one flatten and one rehydrate of the 450-leaf
-    manifest."""
+    WRITE_SIZE), one flatten and one rehydrate of the 450-leaf manifest,
+    then one format v2 encode (CRCs given) and decode."""
     import torch
 
     import wm_inputs
@@ -106,6 +106,12 @@ def counter_pass(args):
     ws = torch.empty(_wm.manifest_ws_bytes(len(leaves)), dtype=torch.uint8, device=dev)
     _wm.flatten(leaves, flat, ws)
     _wm.rehydrate(flat, leaves, ws)
+    del leaves, flat
+    m2 = Mover(state.numel() * 2, args.crc, dev, codec=_wm.WM_CODEC_EXPHUF)
+    m2.checksum(state)
+    m2.encode(state)
+    m2.decode()
+    ok = ok and m2.commit(None, scatter=False) == WM_OK
     torch.cuda.synchronize()
     print(json.dumps({"counter_pass": "done", "verified": ok, "copy_bytes": src.numel(),
                       "payload_bytes": int(m.payload_bytes.item()),
