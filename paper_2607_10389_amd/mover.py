@@ -101,8 +101,9 @@ class Mover:
                       dest: torch.Tensor) -> tuple[int, int]:
         """One round (diff against shipped, encode, decode, verify, install
         into dest and shipped); returns (status, dirty chunks).  After a
-        successful round on the same shipped buffer, the next one checksums
-        only its dirty chunks."""
+        successful round on the same shipped and dest buffers, the next one
+        checksums only its dirty chunks: shipped must then change only
+        through these rounds (its chunk CRCs are kept in self.crc)."""
         if self._bufs is None:
             self._bufs = _wm.move_buffers(
                 self.crc, self.global_crc, self.dirty_idx, self.n_dirty,

@@ -280,3 +280,6 @@ def test_format_v2_calls(lib):
     host = ctypes.create_string_buffer(64)
     assert lib.wm_receive_verify(ctypes.addressof(host), 64, a, 64, nb, P(codec=2), a, nb, a,
                                  None, a, ws2, 0, None, None) == UNSUPPORTED
+    n = ctypes.c_uint32(0)
+    assert lib.wm_precopy_round(a, a + 0x100000, a + 0x200000, nb, P(codec=2), None, 0,
+                                ctypes.byref(n), None) == UNSUPPORTED

@@ -90,6 +90,17 @@ def test_edge_cases(wm, name):
     say(f"[v2] {name}: {state.size} B -> {got.size} B, first record mode {modes}")
 
 
+def test_empty_state(wm):
+    m = mover(0)
+    state = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    m.encode(state, with_crc=False)
+    torch.cuda.synchronize()
+    want = oracle.encode(0, np.zeros(0, np.uint8), CH, None, 1, codec=2)
+    assert np.array_equal(m.payload_host(), want)
+    m.decode()
+    assert m.commit(None, scatter=False) == wm.WM_OK
+
+
 def test_dirty_list(wm):
     prev, cur, ids = wm_inputs.tiny_step("cuda")
     h = host_bytes(cur)
