@@ -112,3 +112,33 @@ def test_driver_without_writes_ships_once(wm):
     # round after the pause ships nothing
     assert [r["dirty"] for r in rounds] == [nbytes // CH, 0, 0]
     assert torch.equal(dest, cur.view(-1).view(torch.uint8))
+
+
+def test_rounds_while_the_source_keeps_writing(wm):
+    """The source is rewritten on another stream while rounds run (chunk
+    writes racing the rounds' reads); after the writer stops, one more round
+    makes the destination equal to the source, byte for byte."""
+    from paper_2607_10389_amd import Mover, precopy
+    spec = SPEC
+    cur = wm_inputs.make_cache(spec, "cuda")
+    nbytes, n = spec.nbytes, spec.nbytes // CH
+    shipped = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    dest = torch.zeros_like(shipped)
+    m = Mover(nbytes)
+    writer = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    dirty = []
+    for k in range(6):
+        with torch.cuda.stream(writer):  # enqueued, runs alongside the round
+            for b in range(4):
+                ids = wm_inputs.chunk_writes(n, 256, seed=7000 + 10 * k + b, device="cuda")
+                wm_inputs.rewrite_chunks(cur, spec, ids, seed=8000 + 10 * k + b)
+        st, nd = m.precopy_round(cur, shipped, dest)
+        assert st == wm.WM_OK
+        dirty.append(nd)
+    writer.synchronize()  # the pause
+    rounds = precopy.run(m, cur, shipped, dest, lambda k, nd: None, stop_chunks=0, max_rounds=3)
+    say(f"[precopy] racing rounds: {dirty}, then {[r['dirty'] for r in rounds]}")
+    assert torch.equal(dest, cur.view(-1).view(torch.uint8))
+    assert torch.equal(shipped, dest)
+    assert rounds[-1]["dirty"] == 0
