@@ -42,6 +42,8 @@ def parse():
                     help="skip the active-generation step measurement")
     ap.add_argument("--no-manifest", action="store_true",
                     help="skip the 450-leaf flatten/rehydrate measurement")
+    ap.add_argument("--no-fanin", action="store_true",
+                    help="skip the eight-session fan-in measurement")
     ap.add_argument("--no-v2", action="store_true",
                     help="skip the format v2 (Huffman exponent codec) measurement")
     ap.add_argument("--no-receive", action="store_true",
@@ -176,6 +178,44 @@ def cpu_baseline(host_state, nbytes_chunk=65536, target_s=12.0):
                       f"cache ({m * nbytes_chunk} B); encode + decode_verify + "
                       f"commit, {dt:.1f} s",
             "cpu_model": cpu}
+
+
+def fanin_run(torch, wm_inputs, crc, dev, reps=5):
+    """Eight independent sessions ([24,2,8,4096,128] bf16, 402,653,184 B
+    each, seeds 100..107), each encoded (full ship) and decoded with
+    verification on its own HIP stream, all enqueued together; wall time
+    from a synchronised start to the last stream's end."""
+    from paper_2607_10389_amd import Mover, WM_OK
+
+    states = [wm_inputs.make_cache(s, dev) for s in wm_inputs.FANIN]
+    streams = [torch.cuda.Stream() for _ in states]
+    movers = [Mover(s.numel() * 2, crc, dev, stream=st) for s, st in zip(states, streams)]
+
+    def run():
+        for m, s, st in zip(movers, states, streams):
+            with torch.cuda.stream(st):
+                m.encode_step(s, None)
+                m.decode()
+
+    run()
+    torch.cuda.synchronize()
+    for m, s in zip(movers, states):
+        if m.commit(None, scatter=False) != WM_OK or \
+                not torch.equal(m.staging[: m.nbytes], s.view(-1).view(torch.uint8)):
+            raise RuntimeError("fan-in session did not verify")
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        run()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / reps
+    each = states[0].numel() * 2
+    return {
+        "workload": "8 sessions x [24,2,8,4096,128] bf16 (402,653,184 B each) on 8 streams: "
+                    "full checksum + encode + decode + verify",
+        "ms": round(wall * 1e3, 3),
+        "aggregate_kv_GBps": round(8 * each / wall / 1e9, 1),
+        "per_session_kv_GBps": round(each / wall / 1e9, 1),
+    }
 
 
 def codec_v2_run(torch, state, nbytes, crc, dev, one):
@@ -529,6 +569,9 @@ def main():
 
     if not args.no_v2:
         out["codec_v2"] = codec_v2_run(torch, state, nbytes, args.crc, dev, one)
+
+    if not args.no_fanin:
+        out["fan_in"] = fanin_run(torch, wm_inputs, args.crc, dev)
 
     if not args.no_receive:
         out["receive"] = receive_runs(torch, m, nbytes, args.crc, dev)
