@@ -208,6 +208,20 @@ def fanin_run(torch, wm_inputs, crc, dev, reps=5):
         run()
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / reps
+
+    def run_serial():  # the same work, one session after another on one stream
+        for m, s in zip(movers, states):
+            m.stream = None
+            m.encode_step(s, None)
+            m.decode()
+
+    run_serial()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        run_serial()
+    torch.cuda.synchronize()
+    serial = (time.perf_counter() - t0) / reps
     each = states[0].numel() * 2
     return {
         "workload": "8 sessions x [24,2,8,4096,128] bf16 (402,653,184 B each) on 8 streams: "
@@ -215,6 +229,8 @@ def fanin_run(torch, wm_inputs, crc, dev, reps=5):
         "ms": round(wall * 1e3, 3),
         "aggregate_kv_GBps": round(8 * each / wall / 1e9, 1),
         "per_session_kv_GBps": round(each / wall / 1e9, 1),
+        "one_stream_back_to_back_ms": round(serial * 1e3, 3),
+        "one_stream_back_to_back_kv_GBps": round(8 * each / serial / 1e9, 1),
     }
 
 
