@@ -222,8 +222,34 @@ def fanin_run(torch, wm_inputs, crc, dev, reps=5):
         run_serial()
     torch.cuda.synchronize()
     serial = (time.perf_counter() - t0) / reps
+    # eight streams on disjoint slices of the CUs: each session keeps its own
+    from paper_2607_10389_amd import streams as cu_streams
+    parts = cu_streams.partition(len(states))
+    for m, cs in zip(movers, parts):
+        m.stream = cs.stream
+
+    def run_parts():
+        for m, s in zip(movers, states):
+            m.encode_step(s, None)
+            m.decode()
+
+    run_parts()
+    torch.cuda.synchronize()
+    for m, s in zip(movers, states):
+        if m.commit(None, scatter=False) != WM_OK or \
+                not torch.equal(m.staging[: m.nbytes], s.view(-1).view(torch.uint8)):
+            raise RuntimeError("fan-in session on a CU slice did not verify")
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        run_parts()
+    torch.cuda.synchronize()
+    parted = (time.perf_counter() - t0) / reps
+    for cs in parts:
+        cs.close()
     each = states[0].numel() * 2
     return {
+        "cu_partitioned_ms": round(parted * 1e3, 3),
+        "cu_partitioned_kv_GBps": round(8 * each / parted / 1e9, 1),
         "workload": "8 sessions x [24,2,8,4096,128] bf16 (402,653,184 B each) on 8 streams: "
                     "full checksum + encode + decode + verify",
         "ms": round(wall * 1e3, 3),

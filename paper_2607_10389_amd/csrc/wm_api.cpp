@@ -104,6 +104,19 @@ wm_status make_geom(uint64_t nbytes, const wm_params *p, ChunkGeom *g) {
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// CUs that launches on `stream` can use: the stream's CU mask when it has
+// one (hipExtStreamCreateWithCUMask, e.g. one slice of the GPU per session),
+// all of them otherwise.  The persistent kernels size their grids with it.
+int stream_cus(void *stream, int n_cu) {
+  if (!stream) return n_cu;
+  uint32_t mask[32] = {0};  // up to 1024 CUs
+  if (hipExtStreamGetCUMask(reinterpret_cast<hipStream_t>(stream), 32, mask) != hipSuccess)
+    return n_cu;
+  int c = 0;
+  for (uint32_t m : mask) c += __builtin_popcount(m);
+  return c > 0 && c < n_cu ? c : n_cu;
+}
+
 // Workspace: the WsLayout part, then (format v2) one plan per chunk.
 uint64_t plans_offset(const WsLayout &L) { return (L.total + 255u) & ~255ull; }
 uint64_t ws_need(const WsLayout &L, uint32_t n_chunks, uint32_t codec) {
@@ -161,6 +174,7 @@ wm_status wm_checksum_chunks(const void *data, uint64_t nbytes, const wm_params 
   if (!crc_out && global_crc) return WM_ERR_INVALID_ARG;
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  n_cu = stream_cus(stream, n_cu);
   return hip_status(launch_checksum(data, g, crc_out, global_crc, n_cu, stream));
 }
 
@@ -176,6 +190,7 @@ wm_status wm_diff_dirty(const void *cur, const void *prev, uint64_t nbytes, cons
   if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  n_cu = stream_cus(stream, n_cu);
   return hip_status(launch_diff(cur, prev, g, dirty_idx, n_dirty, ws, L, stream));
 }
 
@@ -196,6 +211,7 @@ wm_status wm_encode(const void *state, uint64_t nbytes, const wm_params *p, cons
   if (!ws || ws_bytes < ws_need(L, g.n_chunks, g.codec) || !aligned16(ws)) return WM_ERR_WORKSPACE;
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  n_cu = stream_cus(stream, n_cu);
   uint32_t *crc_scratch =
       crc ? nullptr : reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + L.flags);
   if (g.codec == WM_CODEC_EXPHUF)
@@ -224,6 +240,7 @@ wm_status wm_encode_step(const void *cur, const void *prev, uint64_t nbytes, con
   if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  n_cu = stream_cus(stream, n_cu);
   uint32_t *crcs =
       crc_out ? crc_out : reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + L.flags);
   return hip_status(launch_encode(2, cur, prev, g, nullptr, nullptr, nullptr, crcs, global_crc,
@@ -245,6 +262,7 @@ wm_status wm_decode_verify(const void *payload, uint64_t payload_cap, uint64_t n
   if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  n_cu = stream_cus(stream, n_cu);
   if (g.codec == WM_CODEC_EXPHUF)
     return hip_status(launch_decode_v2(payload, payload_cap, g, staging, staging_cap, verdict,
                                        rec_status, ws, L, n_cu, stream));
@@ -266,6 +284,7 @@ wm_status wm_commit_or_abort(void *live, uint64_t nbytes, const wm_params *p, co
   }
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  n_cu = stream_cus(stream, n_cu);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   if (mode == WM_COMMIT_SCATTER) {
     if (launch_commit(live, g, staging, payload, verdict, n_cu, stream) != 0) return WM_ERR_HIP;
@@ -314,6 +333,7 @@ wm_status manifest_call(bool gather, const wm_leaf *leaves, uint32_t n_leaves, v
   int n_cu = 0;
   wm_status s = ensure_device(&n_cu);
   if (s != WM_OK) return s;
+  n_cu = stream_cus(stream, n_cu);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   // an asynchronous copy from pageable host memory has read its source when
   // it returns, so the local table may go out of scope
@@ -381,6 +401,7 @@ wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t 
     if (s != WM_OK) return s;
     int n_cu0 = 0;
     if ((s = ensure_device(&n_cu0)) != WM_OK) return s;
+    n_cu0 = stream_cus(stream, n_cu0);
     if (launch_encode(0, cur, nullptr, g, b->dirty_idx, b->n_dirty, nullptr, b->crc,
                       b->global_crc, nullptr, nullptr, b->payload, b->payload_bytes, b->ws_src,
                       ws_layout(g.n_chunks), n_cu0, stream) != 0)
@@ -391,6 +412,7 @@ wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t 
   if (s != WM_OK) return s;
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  n_cu = stream_cus(stream, n_cu);
   if (nbytes) {
     // both installs are conditional on the same device verdict word
     if (launch_commit(dest, g, b->staging, b->payload, b->verdict, n_cu, stream) != 0 ||
@@ -487,6 +509,7 @@ wm_status wm_receive_verify(const void *host_payload, uint64_t payload_bytes, vo
   if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  n_cu = stream_cus(stream, n_cu);
   const uint8_t *h = static_cast<const uint8_t *>(host_payload);
   uint8_t *d = static_cast<uint8_t *>(payload);
   uint64_t table_off = payload_bytes;

@@ -131,3 +131,28 @@ def test_long_context_raw_chunks_and_bit_flip(wm):
     bad[pos] ^= 4
     v_orc, _, _ = oracle.decode_verify(0, bad, nbytes, CH, None, ORACLE_THREADS)
     assert int(m.verdict.item()) == v_orc
+
+
+def test_sessions_on_cu_slices(wm):
+    """Two sessions on streams limited to disjoint halves of the CUs (the
+    library's grids then span a slice): payloads equal the oracle's and the
+    decoded states equal the sources."""
+    from paper_2607_10389_amd import Mover, streams
+    parts = streams.partition(2)
+    try:
+        states = [wm_inputs.make_cache(wm_inputs.TINY, "cuda"),
+                  wm_inputs.make_cache(wm_inputs.FANIN[1], "cuda")]
+        movers = [Mover(s.numel() * 2, 0, stream=p.stream) for s, p in zip(states, parts)]
+        torch.cuda.synchronize()
+        for m, s in zip(movers, states):
+            m.encode_step(s, None)
+            m.decode()
+        torch.cuda.synchronize()
+        for i, (m, s) in enumerate(zip(movers, states)):
+            h = host_bytes(s)
+            _same(m.payload_host(), oracle.encode(0, h, CH, None, ORACLE_THREADS), f"slice {i}")
+            assert m.commit(None, scatter=False) == wm.WM_OK
+            assert torch.equal(m.staging[: m.nbytes], s.view(-1).view(torch.uint8)), i
+    finally:
+        for p in parts:
+            p.close()
