@@ -31,6 +31,9 @@
  *     never crashes: they become bits of the device verdict word.
  *   - Calls on different streams must use different workspaces; calls that
  *     share a workspace must be ordered (same stream).
+ *   - Grids are sized to the CUs the stream may use: its CU mask when it was
+ *     made with hipExtStreamCreateWithCUMask, every CU otherwise, so
+ *     sessions on disjoint CU slices run side by side.
  *   - All functions are thread-safe.  The first call on a device uploads the
  *     library's constant CRC tables to it (wm_init does this eagerly).
  *   - The kernels support chunk_bytes == 65536 only; other values return
