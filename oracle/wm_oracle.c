@@ -555,6 +555,9 @@ static uint32_t decode_record_v2(int kind, const uint8_t *rec, uint64_t L,
   const uint8_t *body = rec + 16, *sm;
   uint8_t e_of[32768];
   if (k > ORC_HUF_MAX_LEN) return ORC_V_RECORD;
+  /* the encoder codes a chunk only when that beats RAW: a longer HUF record
+   * is malformed (this also bounds the stream section a decoder stages) */
+  if (huf_size(n, k, n_sb) >= raw_size(n)) return ORC_V_RECORD;
   if (k == 0) {
     if (n_sb != 0 || L != huf_size(n, 0, 0)) return ORC_V_RECORD;
     sm = body;
