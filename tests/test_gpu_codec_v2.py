@@ -164,3 +164,16 @@ def test_production_full_ship(wm):
     assert m.commit(None, scatter=False) == wm.WM_OK
     torch.cuda.synchronize()
     assert torch.equal(m.staging[:nbytes], state.view(-1).view(torch.uint8))
+
+
+def test_huf_record_longer_than_raw_is_rejected(wm):
+    from test_oracle_codec_v2 import _huf_payload
+    rng = np.random.default_rng(13)
+    st = rng.integers(0, 1 << 16, 3000, dtype=np.uint16).view(np.uint8)
+    p = np.frombuffer(_huf_payload(st), np.uint8)
+    m = mover(st.size)
+    m.payload[: p.size] = torch.from_numpy(p.copy()).cuda()
+    m.decode()
+    torch.cuda.synchronize()
+    assert int(m.verdict.item()) == 4
+    assert int(u32(m.rec_status)[0]) == 4

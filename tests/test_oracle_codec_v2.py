@@ -160,3 +160,86 @@ def test_every_single_bit_flip_aborts():
             missed.append(i)
         bad[i // 8] ^= 1 << (i % 8)
     assert not missed
+
+
+# ---- an independent writer of format v2 HUF records, from the format's
+# definition (header, code-length nibbles, stream byte counts, streams,
+# sign/mantissa plane), used to pin the oracle's encoder and its rules
+
+def _canonical(lens):
+    codes, code, bl = {}, 0, [0] * 16
+    for ln in lens:
+        bl[ln] += 1
+    bl[0] = 0
+    nxt = [0] * 16
+    for b in range(1, 16):
+        code = (code + bl[b - 1]) << 1
+        nxt[b] = code
+    for s in range(256):
+        if lens[s]:
+            codes[s] = nxt[lens[s]]
+            nxt[lens[s]] += 1
+    return codes
+
+
+def _pad16(x):
+    return -(-x // 16) * 16
+
+
+def _huf_payload(state: np.ndarray) -> bytes:
+    """One-chunk v2 payload whose record is HUF whatever its size (CRC-32)."""
+    import struct
+    import zlib
+    w = state.view(np.uint16)
+    n = w.size
+    e = ((w >> 7) & 255).astype(np.int64)
+    sm = (((w >> 8) & 0x80) | (w & 0x7F)).astype(np.uint8)
+    lens, k = oracle.huffman_lengths(np.bincount(e, minlength=256))
+    codes = _canonical([int(x) for x in lens])
+    streams, sbytes = b"", []
+    for s in range(512):
+        bits = []
+        for i in range(64):
+            wi = (8 * (s // 64) + i // 8) * 512 + 8 * (s % 64) + i % 8
+            if wi < n:
+                ln, c = int(lens[e[wi]]), codes[int(e[wi])]
+                bits += [(c >> b) & 1 for b in range(ln - 1, -1, -1)]
+        out = bytearray(-(-len(bits) // 8))
+        for j, bit in enumerate(bits):
+            out[j // 8] |= bit << (j % 8)
+        sbytes.append(len(out))
+        streams += bytes(out)
+    nib = bytearray(128)
+    for s in range(256):
+        nib[s // 2] |= int(lens[s]) << (4 * (s % 2))
+    hdr = struct.pack("<BBBBII", 2, k, 0, 0, n, len(streams))
+    rec = hdr + struct.pack("<I", zlib.crc32(hdr)) + bytes(nib) + bytes(sbytes)
+    rec += streams + bytes(_pad16(len(streams)) - len(streams))
+    rec += sm.tobytes() + bytes(_pad16(n) - n)
+    table = struct.pack("<IIQ", 0, zlib.crc32(state.tobytes()), 64)
+    total = 64 + len(rec) + 16
+    h = b"WMV2" + struct.pack("<HBBIIQIIQII", 2, 0, 2, CH, 1, state.size, 1, 1, total,
+                              zlib.crc32(state.tobytes()), zlib.crc32(table)) + bytes(12)
+    h += struct.pack("<I", zlib.crc32(h))
+    return h + rec + table
+
+
+def test_independent_writer_matches_the_oracle():
+    rng = np.random.default_rng(12)
+    x = np.sign(rng.standard_normal(3000)) * np.clip(np.abs(rng.standard_normal(3000) * 3),
+                                                      2.0 ** -6, 63.0)
+    st = (x.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16).view(np.uint8)
+    want = oracle.encode(0, st, CH, None, 1, codec=2)
+    assert want[64] == 2  # HUF chosen
+    assert _huf_payload(st) == want.tobytes()
+
+
+def test_a_huf_record_longer_than_raw_is_rejected():
+    # uniform random words: the encoder picks RAW; a HUF record of the same
+    # words is well formed in every other respect but longer than RAW
+    rng = np.random.default_rng(13)
+    st = rng.integers(0, 1 << 16, 3000, dtype=np.uint16).view(np.uint8)
+    assert oracle.encode(0, st, CH, None, 1, codec=2)[64] == 0
+    p = np.frombuffer(_huf_payload(st), np.uint8)
+    v, _, status = oracle.decode_verify(0, p, st.size, CH, None, 1, codec=2)
+    assert v == 4 and status[0] == 4
