@@ -190,6 +190,9 @@ def fanin_run(torch, wm_inputs, crc, dev, reps=5):
     states = [wm_inputs.make_cache(s, dev) for s in wm_inputs.FANIN]
     streams = [torch.cuda.Stream() for _ in states]
     movers = [Mover(s.numel() * 2, crc, dev, stream=st) for s, st in zip(states, streams)]
+    # the caches and buffers were made on the current stream, which the
+    # sessions' streams do not wait for
+    torch.cuda.synchronize()
 
     def run():
         for m, s, st in zip(movers, states, streams):
@@ -299,6 +302,7 @@ def receive_runs(torch, m_src, nbytes, crc, dev):
     m = Mover(nbytes, crc, dev)
     cs = torch.cuda.Stream()
     main = torch.cuda.current_stream()
+    torch.cuda.synchronize()  # m's buffers are cleared on main, the copies run on cs
 
     def timed(fn, reps=5):
         """Mean (total ms, ms from the last copy's end to the end of the

@@ -264,8 +264,10 @@ wm_status wm_rehydrate(const void *flat, uint64_t flat_cap,
  *   batch_bytes   : target record bytes per batch (0: one record per batch;
  *                   raised so that there are at most 4096 batches)
  *   copy_stream   : stream of the copies; stream: stream of the decode,
- *                   which waits for each batch's copies through events.  Use
- *                   two different streams (not the legacy null stream) for
+ *                   which waits for each batch's copies through events.  The
+ *                   copies start after the work enqueued on stream before
+ *                   the call (which may still read payload).  Use two
+ *                   different streams (not the legacy null stream) for
  *                   overlap; the same stream gives the sequential schedule.
  * Other arguments as wm_decode_verify.  Returns after enqueueing.  The host
  * reads the header and table only to schedule the copies; a header or table

@@ -518,17 +518,21 @@ wm_status wm_receive_verify(const void *host_payload, uint64_t payload_bytes, vo
   hipStream_t cs = reinterpret_cast<hipStream_t>(copy_stream);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   std::vector<hipEvent_t> ev;
-  auto arrived = [&]() -> bool {  // stream waits for the copies enqueued so far
+  auto order = [&](hipStream_t from, hipStream_t to) -> bool {  // `to` waits for `from`
     hipEvent_t e;
     if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return false;
     ev.push_back(e);
-    return hipEventRecord(e, cs) == hipSuccess && hipStreamWaitEvent(st, e, 0) == hipSuccess;
+    return hipEventRecord(e, from) == hipSuccess && hipStreamWaitEvent(to, e, 0) == hipSuccess;
   };
+  // the decode stream waits for the copies enqueued so far
+  auto arrived = [&]() { return cs == st || order(cs, st); };
   auto copy = [&](uint64_t b0, uint64_t b1) {
     return b1 <= b0 ||
            hipMemcpyAsync(d + b0, h + b0, b1 - b0, hipMemcpyHostToDevice, cs) == hipSuccess;
   };
-  bool ok = true;
+  // the copies overwrite payload: they start after the work enqueued on
+  // stream before this call (an earlier decode of the same buffer)
+  bool ok = cs == st || order(st, cs);
   const bool parsed = !(batches.size() == 1 && batches[0].b0 == 0);
   if (parsed) {
     // the header and the table (which the checks and every batch read)

@@ -124,3 +124,35 @@ def test_production_payload_in_64mb_batches(wm):
     assert torch.equal(dst.staging[:nbytes], state.view(-1).view(torch.uint8))
     # the received bytes are the sent bytes
     assert torch.equal(dst.payload[: payload.size].cpu(), torch.from_numpy(payload))
+
+
+def test_receive_starts_after_earlier_work_on_its_stream(wm):
+    """A decode of payload X from the device buffer, then a receive of
+    payload Y into the same buffer, enqueued back to back with no host
+    synchronisation: the receive's copies wait for the decode, so both
+    verify (X's decode never reads Y's bytes)."""
+    from paper_2607_10389_amd import Mover
+    state = wm_inputs.make_cache(wm_inputs.PRODUCTION, "cuda")
+    nbytes = state.numel() * 2
+    src = Mover(nbytes)
+    src.encode_step(state, None)
+    torch.cuda.synchronize()
+    px = int(src.payload_bytes.item())
+    dst = Mover(nbytes)
+    dst.payload[:px].copy_(src.payload[:px])
+    cur, _ = wm_inputs.production_step(state)
+    src.encode_step(cur, None)
+    y = pinned(src.payload_host())
+    v_x = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    ds, cs = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    wm.decode_verify(dst.payload, dst.payload.numel(), nbytes, dst.p, dst.staging, v_x,
+                     dst.rec_status, dst.ws_dst, ds)
+    wm.receive_verify(y, y.numel(), dst.payload, nbytes, dst.p, dst.staging, dst.verdict,
+                      dst.rec_status, dst.ws_dst, 64 << 20, cs, ds)
+    torch.cuda.synchronize()
+    say(f"[receive] after a decode on the same stream: verdicts {int(v_x.item())} "
+        f"{int(dst.verdict.item())}")
+    assert int(v_x.item()) == 0
+    assert int(dst.verdict.item()) == 0
+    assert torch.equal(dst.staging[:nbytes], cur.view(-1).view(torch.uint8))
