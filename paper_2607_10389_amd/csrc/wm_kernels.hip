@@ -749,6 +749,7 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
   constexpr uint32_t esc = (1u << K) - 1u;
   constexpr uint32_t esc2 = esc * 0x00010001u;
   const uint32_t base2 = base * 0x00010001u;
+  uint32_t cnt3[(kRows + 2) / 3] = {};  // the lane's escapes per row, three rows a word
 #pragma unroll
   for (int h = 0; h < kRows; ++h) {
     const uint32_t w0 = (l.off0 + h * kRow) >> 1;
@@ -793,15 +794,23 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
         }
       }
     }
-    lane_r[h] = wave_esc;
-    row_base = l.lane == (uint32_t)h ? wave_esc : row_base;
-    if (__ballot(m8 != 0)) {
-      const uint32_t cnt = __popc(m8);
-      const uint32_t incl = wave_incl_scan(cnt);
-      lane_r[h] = wave_esc + incl - cnt;
-      wave_esc += __builtin_amdgcn_readlane(incl, 63);
-    }
     escm[h >> 2] |= m8 << (8 * (h & 3));
+    cnt3[h / 3] |= __popc(m8) << (10 * (h % 3));
+  }
+  // escape ranks from the packed counts: one scan per three rows (a wave's
+  // row holds at most 512 escapes, so 10-bit fields never carry)
+#pragma unroll
+  for (int q = 0; q < (kRows + 2) / 3; ++q) {
+    const uint32_t incl = wave_incl_scan(cnt3[q]);
+    const uint32_t excl = incl - cnt3[q];
+    const uint32_t tot = uniform(__builtin_amdgcn_readlane(incl, 63));
+#pragma unroll
+    for (int j = 0; j < 3 && 3 * q + j < kRows; ++j) {
+      const int h = 3 * q + j;
+      lane_r[h] = wave_esc + ((excl >> (10 * j)) & 1023u);
+      row_base = l.lane == (uint32_t)h ? wave_esc : row_base;
+      wave_esc += (tot >> (10 * j)) & 1023u;
+    }
   }
 }
 
