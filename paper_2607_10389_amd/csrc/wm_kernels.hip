@@ -170,6 +170,19 @@ __device__ __forceinline__ uint32_t mat_apply(const uint32_t *__restrict__ m,
   return r;
 }
 
+// mat_apply with the 32 columns in LDS (four per read, the same address in
+// every lane).
+__device__ __forceinline__ uint32_t mat_apply_lds(const uint4 *m, uint32_t v) {
+  uint32_t r = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint4 c = m[i];
+    r ^= (c.x & (0u - ((v >> (4 * i)) & 1u))) ^ (c.y & (0u - ((v >> (4 * i + 1)) & 1u))) ^
+         (c.z & (0u - ((v >> (4 * i + 2)) & 1u))) ^ (c.w & (0u - ((v >> (4 * i + 3)) & 1u)));
+  }
+  return r;
+}
+
 // F^m(v) for any m >= 0, through the power-of-two shift matrices.
 __device__ uint32_t shift_bytes(const CrcTables &T, uint64_t m, uint32_t v) {
   for (int i = 0; m; ++i, m >>= 1)
@@ -417,73 +430,132 @@ struct CombineJob {
   uint32_t last_len;
   uint32_t kind;
   uint32_t *out;
+  // decoder: the table CRC just combined settles the verdict (null: none)
+  const WsCtl *vctl;
+  uint32_t *verdict;
 };
 
 struct CombineJobs {
   CombineJob job[2];
 };
 
+// The decoder's verdict word once the table CRC is known: the header's
+// verdict if the header was rejected, 2 for a bad table, else the records'
+// bits.
+__device__ __forceinline__ uint32_t decode_verdict(const WsCtl *ctl, uint32_t table_crc) {
+  if (!ctl->hdr_ok) return ctl->verdict_pre;
+  if (ctl->table_bad || table_crc != ctl->table_crc) return 2u;
+  return ctl->rec_bits;
+}
+
+// XOR of x over lanes 0..31, valid in every lane (DPP row steps, then the
+// two rows' totals through lane 15 and lane 31).
+__device__ __forceinline__ uint32_t xor_lanes32(uint32_t x) {
+  x ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  return __builtin_amdgcn_readlane(x, 15) ^ __builtin_amdgcn_readlane(x, 31);
+}
+
+// The pieces' CRCs v_0 .. v_{n-2} (span bytes each) fold to
+//     R = sum_i A^(n-2-i) v_i,   A = F^span,
+// and the result is F^last_len(R) ^ v_{n-1}.  Zeros put in front of the
+// pieces change no term, so the count is padded to N = 4096 K and thread t
+// takes the runs of four consecutive (padded) pieces that start at
+// 4 (t + 1024 k), k < K: every load instruction of a wave then reads 1 KiB
+// of consecutive values.  Its Horner steps by A inside a run and by
+// B = A^4096 from run to run, and the threads' results fold as 1024 blocks of
+// four pieces (a perfect tree, shifts A^(4 * 2^level)).
 __global__ __launch_bounds__(1024) void k_combine(CombineJobs jobs) {
   const CombineJob &J = jobs.job[blockIdx.x];
   const CrcTables &T = g_tables[J.kind];
-  uint32_t n = J.n_dev ? *J.n_dev : J.n;
-  __shared__ uint32_t tabF[1024];   // byte tables of F^span
+  const uint32_t n = J.n_dev ? *J.n_dev : J.n;
+  // byte tables of A = F^span and B = F^(4096 span), four copies: entry
+  // (j, b) of copy c at ((j*256 + b) * 4 + c), a lane reading copy lane % 4,
+  // so the random lookups of the steps below spread over more banks
+  __shared__ __attribute__((aligned(16))) uint32_t tabA[4096];
+  __shared__ __attribute__((aligned(16))) uint32_t tabB[4096];
   __shared__ uint32_t v[1024];
-  uint32_t t = threadIdx.x;
-  // build F^span tables: entry (j, b) = F^span(b << 8j)
-  tabF[t] = mat_apply(T.pow2[J.log2span], (t & 255u) << (8 * (t >> 8)));
+  // F^(2^i), columns: every matrix the steps below take (the index stays
+  // below 2 + 10 + 16 + 1)
+  __shared__ uint4 pw[48 * 8];
+  const uint32_t t = threadIdx.x;
+  if (t < 48u * 8u) pw[t] = reinterpret_cast<const uint4 *>(&T.pow2[0][0])[t];
+  {  // entry (j, b) = F^k(b << 8j)
+    const uint32_t x = (t & 255u) << (8 * (t >> 8));
+    const uint32_t a = mat_apply(T.pow2[J.log2span], x);
+    const uint32_t b = mat_apply(T.pow2[J.log2span + 12u], x);
+    reinterpret_cast<uint4 *>(tabA)[t] = make_uint4(a, a, a, a);
+    reinterpret_cast<uint4 *>(tabB)[t] = make_uint4(b, b, b, b);
+  }
   __syncthreads();
   if (n == 0) {
-    if (t == 0) *J.out = 0u;
+    if (t == 0) {
+      *J.out = 0u;
+      if (J.verdict) *J.verdict = decode_verdict(J.vctl, 0u);
+    }
     return;
   }
-  uint32_t np = n - 1;  // all but the last piece, each exactly span bytes
-  uint32_t m = 1, lm = 0;
-  while (m * 1024u < np) {
-    m <<= 1;
-    ++lm;
-  }
-  // per-thread Horner over pieces [t*m, t*m + m) within [0, np)
-  uint32_t lo = t * m, hi = min(lo + m, np);
+  const uint32_t *tA = tabA + (t & 3u), *tB = tabB + (t & 3u);
+  auto step = [](const uint32_t *tb, uint32_t x) {
+    return tb[(x & 255u) * 4u] ^ tb[(256u + ((x >> 8) & 255u)) * 4u] ^
+           tb[(512u + ((x >> 16) & 255u)) * 4u] ^ tb[(768u + (x >> 24)) * 4u];
+  };
+  const uint32_t np = n - 1;                  // the pieces of span bytes
+  const uint32_t K = (np + 4095u) >> 12;      // runs per thread
+  const uint32_t pad = (K << 12) - np;        // zeros in front
   uint32_t acc = 0;
-  for (uint32_t i = lo; i < hi; ++i) {
-    uint32_t x = acc;
-    acc = tabF[x & 255u] ^ tabF[256u + ((x >> 8) & 255u)] ^
-          tabF[512u + ((x >> 16) & 255u)] ^ tabF[768u + (x >> 24)];
-    acc ^= J.vals[i];
+  for (uint32_t k0 = 0; k0 < K; k0 += 4u) {  // four runs' loads in flight at once
+    uint32_t x[16];
+#pragma unroll
+    for (uint32_t r = 0; r < 4u; ++r) {
+#pragma unroll
+      for (uint32_t q = 0; q < 4u; ++q) {
+        // padded index j, piece j - pad (none in front of the pieces or
+        // past the last run)
+        const uint32_t jp = 4u * (t + 1024u * (k0 + r)) + q;
+        const bool in = k0 + r < K && jp >= pad;
+        x[4 * r + q] = J.vals[in ? jp - pad : 0u];
+        x[4 * r + q] = in ? x[4 * r + q] : 0u;
+      }
+    }
+#pragma unroll
+    for (uint32_t r = 0; r < 4u; ++r) {
+      if (k0 + r < K) {
+        uint32_t run = x[4 * r];
+#pragma unroll
+        for (uint32_t q = 1; q < 4u; ++q) run = step(tA, run) ^ x[4 * r + q];
+        acc = step(tB, acc) ^ run;
+      }
+    }
   }
   v[t] = acc;
   __syncthreads();
-  uint32_t gc = np >> lm;           // complete groups (m pieces each)
-  uint32_t rem = np - (gc << lm);   // pieces in the partial group (index gc)
-  // perfect trees over aligned power-of-two blocks of complete groups
-  for (uint32_t lv = 0; (1u << lv) < 1024u; ++lv) {
-    uint32_t stride = 2u << lv;
-    uint32_t i = t * stride;
-    uint32_t x = 0;
-    bool act = i + stride <= gc;
-    if (act) x = mat_apply(T.pow2[lv + lm + J.log2span], v[i]) ^ v[i + (stride >> 1)];
+  // thread t's result precedes 4 (1023 - t) pieces: a perfect tree, whose
+  // level-lv pairs go to the lowest threads (whole waves drop out)
+  for (uint32_t lv = 0; lv < 10u; ++lv) {
+    const uint32_t stride = 2u << lv, i = t * stride;
+    const bool act = i < 1024u;
+    uint32_t y = 0;
+    if (act) y = mat_apply_lds(pw + 8u * (lv + 2u + J.log2span), v[i]) ^ v[i + (stride >> 1)];
     __syncthreads();
-    if (act) v[i] = x;
+    if (act) v[i] = y;
     __syncthreads();
   }
-  if (t == 0) {
-    uint32_t r = 0;
-    bool have = false;
-    uint32_t pos = 0;
-    for (int b = 10; b >= 0; --b) {
-      if (!((gc >> b) & 1u)) continue;
-      r = have ? mat_apply(T.pow2[b + lm + J.log2span], r) ^ v[pos] : v[pos];
-      have = true;
-      pos += 1u << b;
+  if (t < 64u) {
+    // the first wave shifts the result past the last piece; each matrix
+    // product takes the whole wave (lane i < 32 the term of column i)
+    const uint32_t lane = t;
+    const uint32_t *pcol = reinterpret_cast<const uint32_t *>(pw) + (lane & 31u);
+    uint32_t r = v[0];
+    for (uint32_t i = 0, k = J.last_len; k; ++i, k >>= 1)
+      if (k & 1u) r = xor_lanes32(lane < 32u && ((r >> lane) & 1u) ? pcol[32u * i] : 0u);
+    r ^= J.vals[n - 1];
+    if (lane == 0) {
+      *J.out = r;
+      if (J.verdict) *J.verdict = decode_verdict(J.vctl, r);
     }
-    if (rem) {
-      r = have ? shift_bytes(T, (uint64_t)rem << J.log2span, r) ^ v[gc] : v[gc];
-      have = true;
-    }
-    uint32_t last = J.vals[n - 1];
-    r = have ? shift_bytes(T, J.last_len, r) ^ last : last;
-    *J.out = r;
   }
 }
 
@@ -577,7 +649,7 @@ struct EncArgs {
 struct EncShared {
   uint32_t u[kThreads];      // lane values of the chunk's CRC (lane_value)
   uint32_t dirty_w[kWaves];  // per-wave "differs from prev"
-  uint32_t esc_w[kWaves];    // escapes per wave
+  alignas(16) uint32_t esc_w[kWaves];  // escapes per wave
   uint32_t crc;               // the chunk's CRC
   uint32_t first, next;      // tickets before the loop
   uint32_t ticket[2];        // in the loop, by iteration parity
@@ -1218,8 +1290,13 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
 
     // ---- phase 5
     if (!is_ctl && pack && has_esc) {
+      // escapes of the waves before this one: two reads, no dependent chain
+      const uint4 ea = *reinterpret_cast<const uint4 *>(&sh.esc_w[0]);
+      const uint4 eb = *reinterpret_cast<const uint4 *>(&sh.esc_w[4]);
+      const uint32_t ew[kWaves] = {ea.x, ea.y, ea.z, ea.w, eb.x, eb.y, eb.z, eb.w};
       uint32_t wave_base = 0;
-      for (uint32_t w = 0; w < l.wave; ++w) wave_base += sh.esc_w[w];
+#pragma unroll
+      for (uint32_t w = 0; w < (uint32_t)kWaves - 1u; ++w) wave_base += w < l.wave ? ew[w] : 0u;
       wave_base = uniform(wave_base);
       {  // lane h writes the escape-index entry of the wave's row h (block
          // wave * 8 + h, present when its first word is in the chunk)
@@ -1280,12 +1357,32 @@ __global__ void k_encode_prepare(uint8_t *ws, WsLayout L, uint32_t n) {
   for (; i < n; i += gridDim.x * blockDim.x) status[i] = 0;
 }
 
+// CRC of a 60-byte payload header held as 15 little-endian words, with the
+// byte table in LDS (a chain of 60 dependent lookups: LDS keeps each one
+// short).
+__device__ __forceinline__ uint32_t header_crc60(const uint32_t (&h)[15], const uint32_t *t1) {
+  uint32_t s = 0xFFFFFFFFu;
+#pragma unroll
+  for (int i = 0; i < 15; ++i) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b) s = t1[(s ^ (h[i] >> (8 * b))) & 255u] ^ (s >> 8);
+  }
+  return s ^ 0xFFFFFFFFu;
+}
+__device__ __forceinline__ void byte_table_to_lds(uint32_t *t1, uint32_t kind) {
+  for (uint32_t i = threadIdx.x; i < 256u; i += blockDim.x) t1[i] = g_tables[kind].byte1[i];
+}
+
 // Table copy into the payload and the header.
 __global__ __launch_bounds__(256) void k_encode_finish(
     uint8_t *__restrict__ payload, const uint8_t *__restrict__ ws, WsLayout L,
     ChunkGeom g, uint32_t full, const uint32_t *__restrict__ crcs,
-    uint64_t *payload_bytes, uint32_t *n_dirty) {
+    uint64_t *payload_bytes, uint32_t *n_dirty, uint32_t *global_crc) {
   const WsCtl *ctl = reinterpret_cast<const WsCtl *>(ws + L.ctl);
+  __shared__ uint32_t t1[256];
+  if (blockIdx.x == 0) byte_table_to_lds(t1, g.crc_kind);
+  __syncthreads();
+  if (global_crc && blockIdx.x == 0 && threadIdx.x == 0) *global_crc = crcs[0];
   if (ctl->error) {  // invalid index list or an abandoned scan: no payload
     if (blockIdx.x == 0 && threadIdx.x == 0) {
       *reinterpret_cast<uint4 *>(payload) = make_uint4(0, 0, 0, 0);
@@ -1316,14 +1413,7 @@ __global__ __launch_bounds__(256) void k_encode_finish(
     h[10] = crcs[0];  // global CRC
     h[11] = crcs[1];  // table CRC
     h[12] = h[13] = h[14] = 0;
-    // header CRC over bytes 0..59 with the byte-table step
-    const uint32_t *t1 = g_tables[g.crc_kind].byte1;
-    uint32_t s = 0xFFFFFFFFu;
-    for (int i = 0; i < 60; ++i) {
-      uint32_t b = (h[i >> 2] >> (8 * (i & 3))) & 255u;
-      s = t1[(s ^ b) & 255u] ^ (s >> 8);
-    }
-    h[15] = s ^ 0xFFFFFFFFu;
+    h[15] = header_crc60(reinterpret_cast<const uint32_t(&)[15]>(h), t1);
     uint4 *out = reinterpret_cast<uint4 *>(payload);
     for (int i = 0; i < 4; ++i) out[i] = make_uint4(h[4 * i], h[4 * i + 1], h[4 * i + 2], h[4 * i + 3]);
     if (payload_bytes) *payload_bytes = total;
@@ -1346,6 +1436,9 @@ __global__ __launch_bounds__(64) void k_decode_prepare(
     const uint8_t *__restrict__ payload, uint64_t cap, ChunkGeom g,
     uint64_t staging_cap, uint8_t *ws, WsLayout L) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(ws + L.ctl);
+  __shared__ uint32_t t1[256];
+  byte_table_to_lds(t1, g.crc_kind);
+  __syncthreads();
   if (threadIdx.x != 0) return;
   ctl->ticket = 0;
   ctl->hdr_ok = 0;
@@ -1357,10 +1450,10 @@ __global__ __launch_bounds__(64) void k_decode_prepare(
   ctl->table_crc = 0;
   ctl->verdict_pre = 1u;  // header rejected unless every check passes
   if (cap < 64) return;
-  const uint32_t *t1 = g_tables[g.crc_kind].byte1;
-  uint32_t s = 0xFFFFFFFFu;
-  for (int i = 0; i < 60; ++i) s = t1[(s ^ payload[i]) & 255u] ^ (s >> 8);
-  if ((s ^ 0xFFFFFFFFu) != ld_u32(payload + 60)) return;
+  uint32_t hw[15];
+#pragma unroll
+  for (int i = 0; i < 15; ++i) hw[i] = ld_u32(payload + 4 * i);
+  if (header_crc60(hw, t1) != ld_u32(payload + 60)) return;
   if (ld_u32(payload) != (g.codec == 2 ? 0x32564D57u : 0x31564D57u)) return;
   if (ld_u32(payload + 4) != (g.codec | (g.crc_kind << 16) | (g.codec << 24))) return;
   if (ld_u32(payload + 8) != kChunk || ld_u32(payload + 12) != g.n_chunks) return;
@@ -1942,18 +2035,6 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
     __syncthreads();
     if (!is_ctl) cur = nxt;
   }
-}
-
-// Final verdict after the table CRC has been combined.
-__global__ void k_decode_verdict(const uint8_t *ws, WsLayout L,
-                                 const uint32_t *table_crc,
-                                 uint32_t *verdict) {
-  const WsCtl *ctl = reinterpret_cast<const WsCtl *>(ws + L.ctl);
-  uint32_t v;
-  if (!ctl->hdr_ok) v = ctl->verdict_pre;
-  else if (ctl->table_bad || *table_crc != ctl->table_crc) v = 2u;
-  else v = ctl->rec_bits;
-  *verdict = v;
 }
 
 // ---------------------------------------------------------------- commit --
@@ -2663,8 +2744,9 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
     if (hok && !is_ctl) {
       if (t < 256u && lens[t]) {  // symbols in code order
         const uint32_t ln = lens[t];
-        uint32_t rank = within;
-        for (uint32_t w = 0; w < l.wave; ++w) rank += M.wcnt[w][ln];
+        uint32_t rank = within;  // independent reads, not a chain of round trips
+#pragma unroll
+        for (uint32_t w = 0; w < (uint32_t)kWaves - 1u; ++w) rank += w < l.wave ? M.wcnt[w][ln] : 0u;
         sorted[M.start[ln] + rank] = (uint8_t)t;
       }
     }
@@ -2889,14 +2971,8 @@ int launch_encode(int mode, const void *cur, const void *prev, const ChunkGeom &
   uint32_t full = mode == kModeAll || (mode == kModeStep && prev == nullptr) ? 1u : 0u;
   hipLaunchKernelGGL(k_encode_finish, dim3(64), dim3(256), 0, S(stream),
                      static_cast<uint8_t *>(payload), static_cast<const uint8_t *>(ws), L, g,
-                     full, crcs, payload_bytes, n_dirty);
-  e = hipGetLastError();
-  if (e != hipSuccess) return (int)e;
-  if (global_crc) {
-    e = hipMemcpyAsync(global_crc, crcs, 4, hipMemcpyDeviceToDevice, S(stream));
-    if (e != hipSuccess) return (int)e;
-  }
-  return 0;
+                     full, crcs, payload_bytes, n_dirty, global_crc);
+  return (int)hipGetLastError();
 }
 
 int launch_decode_begin(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
@@ -2935,12 +3011,8 @@ int launch_decode_end(const ChunkGeom &g, uint32_t *verdict, void *ws, const WsL
   uint32_t *computed = reinterpret_cast<uint32_t *>(wsb + L.ctl) + 60;
   CombineJobs jobs = {};
   jobs.job[0] = CombineJob{reinterpret_cast<const uint32_t *>(wsb + L.entry_crc), &ctl->n_rec,
-                           0u, 4u, 16u, g.crc_kind, computed};
-  const int rc = launch_combine(jobs, 1, stream);
-  if (rc) return rc;
-  hipLaunchKernelGGL(k_decode_verdict, dim3(1), dim3(1), 0, S(stream), wsb, L, computed,
-                     verdict);
-  return (int)hipGetLastError();
+                           0u, 4u, 16u, g.crc_kind, computed, ctl, verdict};
+  return launch_combine(jobs, 1, stream);
 }
 
 // ------------------------------------------------------------- manifest --
@@ -3071,14 +3143,8 @@ int launch_encode_v2(const void *state, const ChunkGeom &g, const uint32_t *idx,
   if (rc) return rc;
   hipLaunchKernelGGL(k_encode_finish, dim3(64), dim3(256), 0, S(stream),
                      static_cast<uint8_t *>(payload), static_cast<const uint8_t *>(ws), L, g,
-                     idx ? 0u : 1u, sums, payload_bytes, nullptr);
-  e = hipGetLastError();
-  if (e != hipSuccess) return (int)e;
-  if (global_crc) {
-    e = hipMemcpyAsync(global_crc, sums, 4, hipMemcpyDeviceToDevice, S(stream));
-    if (e != hipSuccess) return (int)e;
-  }
-  return 0;
+                     idx ? 0u : 1u, sums, payload_bytes, nullptr, global_crc);
+  return (int)hipGetLastError();
 }
 
 int launch_decode_v2(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
