@@ -468,7 +468,7 @@ def main():
            "wm_encode_step: k_encode_prepare, k_encode, k_combine, k_encode_finish") \
         if src_ms >= dst_ms else \
         ("k_decode", dst_ms, dst_bytes, dst_gbs,
-         "wm_decode_verify: k_decode_prepare, k_decode, k_combine, k_decode_verdict")
+         "wm_decode_verify: k_decode_prepare, k_decode, k_combine (table CRC and verdict)")
 
     out = {
         "metric": "GB/s of KV cache checksummed+encoded and decoded+verified on 1 MI355X",
