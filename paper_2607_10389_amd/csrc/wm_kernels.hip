@@ -1775,6 +1775,13 @@ __device__ __forceinline__ uint2 unpack_codes(const uint4 &a, uint32_t sh) {
     const uint32_t v0 = __builtin_amdgcn_alignbit(a.y, a.x, sh);
     if constexpr (K == 8) {
       c = make_uint2(a.x, a.y);  // byte aligned: sh is 0
+    } else if constexpr (K == 3) {
+      // each 12-bit half (four codes) spreads in two shift-or-mask steps:
+      // codes 2, 3 up by 10 bits, then the odd codes up by 5
+      const uint32_t g0 = v0 & 0xFFFu, g1 = __builtin_amdgcn_ubfe(v0, 12, 12);
+      const uint32_t t0 = ((g0 << 10) | g0) & 0x003F003Fu, t1 = ((g1 << 10) | g1) & 0x003F003Fu;
+      c.x = ((t0 << 5) | t0) & 0x07070707u;
+      c.y = ((t1 << 5) | t1) & 0x07070707u;
     } else if constexpr (K == 4) {
       const uint32_t t0 = __builtin_amdgcn_perm(0u, v0, 0x01010000u);  // b0 b0 b1 b1
       const uint32_t t1 = __builtin_amdgcn_perm(0u, v0, 0x03030202u);  // b2 b2 b3 b3
