@@ -790,7 +790,8 @@ __device__ uint64_t lookback_finish(const uint64_t *status, int64_t top, Window 
 
 // K-bit codes of the data wave's 8 rows into LDS staging.  Codes are formed
 // two words at a time in 16-bit lanes: c = min((e - base) mod 2^16, esc), and
-// c + 1 carries into bit K exactly for escapes.  Per row: escm holds the
+// c + 1 carries into bit K exactly for escapes (K = 3: escapes are found on
+// the row's packed codes instead).  Per row: escm holds the
 // lane's escape flags (bit u = word u, 8 bits per row), lane_r the number of
 // the wave's escapes before the lane's first one in this row; lane h of
 // row_base receives the wave's escapes before row h (its index entry).  FULL: the
@@ -830,7 +831,7 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const uint32_t c2 = pk_sub_min((x[j] >> 7) & 0x00FF00FFu, base2, esc2);
-      m |= (((c2 + 0x00010001u) >> K) & 0x00010001u) << (2 * j);
+      if constexpr (K != 3) m |= (((c2 + 0x00010001u) >> K) & 0x00010001u) << (2 * j);
       pair[j] = (c2 & 0xFFFFu) | (c2 >> (16 - K));  // lo | hi << K
     }
     uint32_t m8 = (m | (m >> 15)) & 0xFFu;
@@ -840,6 +841,15 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
       for (int j = 0; j < 4; ++j)
         pair[j] &= vw >= 2u * j + 2u ? ~0u : (vw == 2u * j + 1u ? esc : 0u);
       m8 &= (1u << vw) - 1u;
+    }
+    if constexpr (K == 3) {
+      // escapes are the all-ones codes of the row's 24 code bits: flag u
+      // at bit 3u, then gathered to bit u in three shift-or-mask steps
+      const uint32_t p3 = pair[0] | (pair[1] << 6) | (pair[2] << 12) | (pair[3] << 18);
+      const uint32_t t = p3 & (p3 >> 1) & (p3 >> 2) & 0x00249249u;
+      const uint32_t s1 = (t | (t >> 2)) & 0x000C30C3u;
+      const uint32_t s2 = (s1 | (s1 >> 4)) & 0x0000F00Fu;
+      m8 = (s2 | (s2 >> 8)) & 0xFFu;
     }
     if (FULL || w0 < n_words) {
       uint8_t *at = stage + (w0 >> 3) * K;
