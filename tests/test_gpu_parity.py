@@ -56,6 +56,34 @@ def test_ragged_checksum(wm, n):
     assert int(u32(m.global_crc)[0]) == g
 
 
+# The global CRC folds the n - 1 full chunks' CRCs in runs of four, 4096
+# pieces per pass over the workgroup (zeros padded in front): these counts
+# sit on either side of one and two passes.
+@pytest.mark.parametrize("chunks,tail", [(4096, CH), (4097, CH), (4098, 777),
+                                         (8193, CH), (8194, 3)])
+def test_global_crc_fold_boundaries(wm, chunks, tail):
+    n = (chunks - 1) * CH + tail
+    say(f"[fold boundaries] chunks={chunks} tail={tail}")
+    data = random_bytes(n, seed=chunks)
+    kind = chunks & 1
+    m = mover(n, kind)
+    m.checksum(data)
+    torch.cuda.synchronize()
+    crcs, g = oracle.checksum_chunks(kind, host_bytes(data), CH, ORACLE_THREADS)
+    assert np.array_equal(m.crc_host(), crcs)
+    assert int(u32(m.global_crc)[0]) == g
+
+
+def test_full_ship_at_a_fold_boundary(wm):
+    """4098 chunks (the last one short) of bf16 values: the global CRC and
+    the table CRC (4098 entries) both take two passes of the fold."""
+    n_words = (4097 * CH + 778) // 2
+    gen = torch.Generator(device="cuda").manual_seed(4098)
+    state = torch.randn(n_words, generator=gen, device="cuda").to(torch.bfloat16)
+    m = mover(n_words * 2)
+    check_full_ship(m, state, 0, "fold boundary")
+
+
 @pytest.mark.parametrize("kind", [0, 1])
 @pytest.mark.parametrize("fused", [True, False])
 def test_tiny_full_ship(wm, kind, fused):
