@@ -1143,9 +1143,16 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         // write X_{i-1}: staged section, then its sign/mantissa plane
         const uint64_t rec_off = (uint64_t)uniform(sh.off_lo) | ((uint64_t)uniform(sh.off_hi) << 32);
         uint8_t *rec = a.payload + rec_off;
-        for (uint32_t i = threadIdx.x; i < p_send / 16u; i += kThreads)
-          *reinterpret_cast<uint4 *>(rec + 16 + 16 * i) =
-              *reinterpret_cast<const uint4 *>(stage + 16 * i);
+        // two staged pieces per thread and step, both read before either is
+        // stored (one LDS round trip per pair)
+        const uint32_t n16 = p_send / 16u;
+        for (uint32_t i = threadIdx.x; i < n16; i += 2u * kThreads) {
+          const uint32_t i2 = i + kThreads;
+          const uint4 q0 = *reinterpret_cast<const uint4 *>(stage + 16 * i);
+          const uint4 q1 = *reinterpret_cast<const uint4 *>(stage + 16 * min(i2, n16 - 1u));
+          *reinterpret_cast<uint4 *>(rec + 16 + 16 * i) = q0;
+          if (i2 < n16) *reinterpret_cast<uint4 *>(rec + 16 + 16 * i2) = q1;
+        }
         uint8_t *sm_at = rec + 16 + p_send;
 #pragma unroll
         for (int h = 0; h < kRows; ++h) {
