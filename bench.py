@@ -120,20 +120,22 @@ def counter_pass(args):
                       "state_bytes": state.numel() * 2}), flush=True)
 
 
-def timed_events(torch, fn, n):
-    """Average duration (ms) of fn() measured with HIP events on the current
-    stream, n repetitions after one untimed call."""
-    fn()
+def timed_events(torch, fn, n, warmup=3):
+    """Median duration (ms) of fn() over n runs, each bracketed by its own
+    pair of HIP events on the current stream, after `warmup` untimed runs."""
+    for _ in range(warmup):
+        fn()
     s = torch.cuda.Event(enable_timing=True)
     e = torch.cuda.Event(enable_timing=True)
-    total = 0.0
+    times = []
     for _ in range(n):
         s.record()
         fn()
         e.record()
         e.synchronize()
-        total += s.elapsed_time(e)
-    return total / n
+        times.append(s.elapsed_time(e))
+    times.sort()
+    return times[n // 2] if n % 2 else 0.5 * (times[n // 2 - 1] + times[n // 2])
 
 
 def cpu_baseline(host_state, nbytes_chunk=65536, target_s=12.0):
@@ -178,6 +180,43 @@ def cpu_baseline(host_state, nbytes_chunk=65536, target_s=12.0):
                       f"cache ({m * nbytes_chunk} B); encode + decode_verify + "
                       f"commit, {dt:.1f} s",
             "cpu_model": cpu}
+
+
+def cpu_oracle_detail(host_prev, host_cur, tiny_prev, tiny_cur, threads):
+    """The oracle per operation, in GB/s of state bytes: checksum, diff,
+    encode (full ship) and decode + verify, on the tiny cache with one
+    thread and with `threads`, and on the production-size cache with
+    `threads` only (one thread would take minutes there)."""
+    import oracle
+    CH = 65536
+
+    def rate(fn, nbytes, min_s):
+        reps, t = 0, 0.0
+        t0 = time.perf_counter()
+        while True:
+            fn()
+            reps += 1
+            t = time.perf_counter() - t0
+            if t >= min_s:
+                return round(nbytes * reps / t / 1e9, 4)
+
+    def ops(prev, cur, T, min_s):
+        payload = oracle.encode(0, cur, CH, None, T)
+        return {
+            "checksum": rate(lambda: oracle.checksum_chunks(0, cur, CH, T), cur.size, min_s),
+            "diff": rate(lambda: oracle.diff_dirty(cur, prev, CH, T), cur.size, min_s),
+            "encode": rate(lambda: oracle.encode(0, cur, CH, None, T), cur.size, min_s),
+            "decode_verify": rate(lambda: oracle.decode_verify(0, payload, cur.size, CH,
+                                                               None, T), cur.size, min_s),
+        }
+
+    return {
+        "unit": "GB/s of state bytes",
+        "threads": threads,
+        "tiny_one_thread": ops(tiny_prev, tiny_cur, 1, 0.3),
+        "tiny_all_threads": ops(tiny_prev, tiny_cur, threads, 0.3),
+        "production_all_threads": ops(host_prev, host_cur, threads, 0.0),
+    }
 
 
 def fanin_run(torch, wm_inputs, crc, dev, reps=5):
@@ -631,6 +670,14 @@ def main():
         out["cpu_baseline"] = cpu_baseline(host)
         out["cpu_baseline"]["paper_context"] = (
             "the paper's 32-thread CPU zlib CRC engine: 52.6 GB/s (CRC only)")
+        # the active-generation step's snapshot pair, and the tiny pair
+        cur, _ = wm_inputs.production_step(state)
+        host_cur = cur.view(-1).view(torch.uint8).cpu().numpy()
+        del cur
+        tp, tc, _ = wm_inputs.tiny_step("cpu")
+        out["cpu_oracle_detail"] = cpu_oracle_detail(
+            host, host_cur, wm_inputs.as_bytes(tp).numpy(), wm_inputs.as_bytes(tc).numpy(),
+            out["cpu_baseline"]["cores"])
 
     print(json.dumps(out), flush=True)
 
