@@ -2311,8 +2311,16 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_plan(
     const uint32_t len = chunk_len(g, c), n = len / 2;
     const uint8_t *base = state + (uint64_t)c * kChunk;
     const Rsrc rs = rsrc(base, len);
-    for (int q = 0; q < 4; ++q) W.hist[q * 64 + lane] = 0;
+    // four interleaved copies of the histogram (bin b of copy c at 4b + c,
+    // copy = lane mod 4) in hist, wt and nw, which the length construction
+    // only uses afterwards: equal exponents of lanes in different copies hit
+    // different banks
+    uint32_t *H4 = W.hist;
+    static_assert(offsetof(HufWave, wt) == 1024 && offsetof(HufWave, nw) == 2048 &&
+                  sizeof(HufWave::nw) == 2048, "hist, wt, nw: 1024 contiguous words");
+    for (int q = 0; q < 4; ++q) reinterpret_cast<uint4 *>(H4)[q * 64 + lane] = make_uint4(0, 0, 0, 0);
     wave_sync();
+    const uint32_t cp = lane & 3u;
     for (uint32_t q = 0; q < 8u; ++q) {
       uint4 x[8];
       huf_pieces8(base, rs, len, 512u * q + lane, x);
@@ -2321,8 +2329,16 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_plan(
         const uint32_t i0 = 8u * (512u * q + lane + 64u * h);
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-          if (i0 + j < n) atomicAdd(&W.hist[exp_of(word_of(x[h], j))], 1u);
+          if (i0 + j < n) atomicAdd(&H4[4u * exp_of(word_of(x[h], j)) + cp], 1u);
       }
+    }
+    wave_sync();
+    {  // fold the copies into hist (every read is issued before any write)
+      uint4 cs[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) cs[q] = reinterpret_cast<const uint4 *>(H4)[q * 64 + lane];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) W.hist[q * 64 + lane] = cs[q].x + cs[q].y + cs[q].z + cs[q].w;
     }
     wave_sync();
     const uint32_t k = huf_lengths_wave(W, lane);
