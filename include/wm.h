@@ -137,7 +137,10 @@ wm_status wm_diff_dirty(const void *cur, const void *prev, uint64_t nbytes,
  * lossless codec whose receipts bind to the decoded bytes).
  *   state      : nbytes (even), 16-byte aligned
  *   idx, n_idx : device list of *n_idx ascending chunk indices to encode, or
- *                both NULL to encode every chunk (sets the FULL flag)
+ *                both NULL to encode every chunk (sets the FULL flag).  The
+ *                list is checked on the device: one that is not strictly
+ *                ascending or holds an index >= n_chunks yields an empty
+ *                payload (*payload_bytes = 0, header zeroed)
  *   crc        : ceil(nbytes/chunk_bytes) u32 chunk CRCs from
  *                wm_checksum_chunks (used as receipts and for the header's
  *                global CRC), or NULL to compute them in the same pass; NULL

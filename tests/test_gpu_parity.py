@@ -92,6 +92,31 @@ def test_tiny_full_ship(wm, kind, fused):
     check_full_ship(m, state, kind, "tiny", fused)
 
 
+@pytest.mark.parametrize("codec", [1, 2])
+def test_invalid_index_list_gives_an_empty_payload(wm, codec):
+    """A list that repeats, goes backwards or leaves the chunk range is
+    rejected on the device (empty payload); a valid list on the same
+    buffers afterwards encodes exactly as the oracle does."""
+    state = wm_inputs.make_cache(wm_inputs.TINY, "cuda")
+    nbytes = state.numel() * 2
+    m = mover(nbytes, 0, codec=codec)
+    m.checksum(state)
+    for bad in ([3, 3, 5], [5, 2, 9], [0, 1, 32], [7, 40]):
+        idx = torch.tensor(bad, dtype=torch.int32, device="cuda")
+        n_idx = torch.tensor([len(bad)], dtype=torch.int32, device="cuda")
+        m.payload_bytes.fill_(123)
+        wm.encode(state, nbytes, m.p, idx, n_idx, m.crc, m.payload, m.payload_bytes, m.ws_src)
+        torch.cuda.synchronize()
+        assert int(m.payload_bytes.item()) == 0, (codec, bad)
+    good = np.array([1, 4, 9, 31], dtype=np.uint32)
+    idx = torch.from_numpy(good.view(np.int32)).cuda()
+    n_idx = torch.tensor([good.size], dtype=torch.int32, device="cuda")
+    wm.encode(state, nbytes, m.p, idx, n_idx, m.crc, m.payload, m.payload_bytes, m.ws_src)
+    torch.cuda.synchronize()
+    want = oracle.encode(0, host_bytes(state), CH, good, ORACLE_THREADS, codec=codec)
+    assert np.array_equal(m.payload_host(), want)
+
+
 def test_tiny_full_ship_crc_in_pass(wm):
     """wm_encode with crc = NULL computes the receipts in the same pass."""
     state = wm_inputs.make_cache(wm_inputs.TINY, "cuda")
