@@ -139,12 +139,16 @@ wm_status wm_diff_dirty(const void *cur, const void *prev, uint64_t nbytes,
  *   idx, n_idx : device list of *n_idx ascending chunk indices to encode, or
  *                both NULL to encode every chunk (sets the FULL flag).  The
  *                list is checked on the device: one that is not strictly
- *                ascending or holds an index >= n_chunks yields an empty
- *                payload (*payload_bytes = 0, header zeroed)
+ *                ascending, holds an index >= n_chunks or has more than
+ *                n_chunks entries yields an empty payload (*payload_bytes =
+ *                0, the 64 header bytes zeroed)
  *   crc        : ceil(nbytes/chunk_bytes) u32 chunk CRCs from
  *                wm_checksum_chunks (used as receipts and for the header's
- *                global CRC), or NULL to compute them in the same pass; NULL
- *                is only allowed when idx is NULL
+ *                global CRC), or NULL to compute them within the call: in
+ *                the encoding pass when idx is NULL; with a list, every
+ *                chunk is checksummed first (the global CRC covers the
+ *                whole state, listed or not) and the workspace holds the
+ *                CRCs
  *   payload    : payload_cap bytes, 16-byte aligned; payload_cap must be at
  *                least wm_payload_bound(nbytes, n_chunks, p)
  *   payload_bytes : 1 u64, the payload size written

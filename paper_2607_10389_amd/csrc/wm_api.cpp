@@ -204,7 +204,6 @@ wm_status wm_encode(const void *state, uint64_t nbytes, const wm_params *p, cons
   if (nbytes & 1u) return WM_ERR_INVALID_ARG;
   if ((nbytes && !state) || !aligned16(state)) return WM_ERR_INVALID_ARG;
   if ((idx == nullptr) != (n_idx == nullptr)) return WM_ERR_INVALID_ARG;
-  if (idx && !crc) return WM_ERR_INVALID_ARG;
   if (!payload || !payload_bytes || !aligned16(payload)) return WM_ERR_INVALID_ARG;
   if (payload_cap < wm_payload_bound(nbytes, g.n_chunks, p)) return WM_ERR_CAPACITY;
   WsLayout L = ws_layout(g.n_chunks);
@@ -219,6 +218,14 @@ wm_status wm_encode(const void *state, uint64_t nbytes, const wm_params *p, cons
                                        payload_bytes, ws, L,
                                        static_cast<uint8_t *>(ws) + plans_offset(L), n_cu,
                                        stream));
+  if (idx && !crc) {
+    // the header's global CRC covers every chunk, listed or not: checksum
+    // the whole state first, then encode the list with those receipts
+    const int rc = launch_checksum(state, g, crc_scratch, nullptr, n_cu, stream);
+    if (rc) return WM_ERR_HIP;
+    crc = crc_scratch;
+    crc_scratch = nullptr;
+  }
   int mode = idx ? 0 : 1;
   return hip_status(launch_encode(mode, state, nullptr, g, idx, n_idx, crc, crc_scratch, nullptr,
                                   nullptr, nullptr, payload, payload_bytes, ws, L, n_cu, stream));

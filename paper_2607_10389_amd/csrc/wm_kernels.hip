@@ -1002,8 +1002,11 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   uint64_t *status = reinterpret_cast<uint64_t *>(a.ws + a.L.status);
   uint4 *tab_ws = reinterpret_cast<uint4 *>(a.ws + a.L.table);
   uint32_t *ecrc = reinterpret_cast<uint32_t *>(a.ws + a.L.entry_crc);
+  // a list longer than the chunk count is invalid (k_encode_prepare flagged
+  // it): nothing is encoded
+  const uint32_t n_list = a.mode == kModeList ? ld_const(a.n_idx) : 0u;
   const uint32_t n_items =
-      uniform(a.mode == kModeList ? min(ld_const(a.n_idx), g.n_chunks) : g.n_chunks);
+      uniform(a.mode == kModeList ? (n_list > g.n_chunks ? 0u : n_list) : g.n_chunks);
   const bool need_crc = a.crc_in == nullptr;
   const bool is_ctl = threadIdx.x >= (uint32_t)kThreads;
 
@@ -1365,12 +1368,16 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   }
 }
 
-// Zero the control block and the look-back words before an encode.
-__global__ void k_encode_prepare(uint8_t *ws, WsLayout L, uint32_t n) {
+// Zero the control block and the look-back words before an encode.  An
+// index list of more than n entries is rejected here (error 2: the payload
+// comes out empty).
+__global__ void k_encode_prepare(uint8_t *ws, WsLayout L, uint32_t n,
+                                 const uint32_t *__restrict__ n_idx) {
   uint64_t *status = reinterpret_cast<uint64_t *>(ws + L.status);
   uint32_t *ctl = reinterpret_cast<uint32_t *>(ws + L.ctl);
   uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < 64u) ctl[i] = 0;
+  static_assert(offsetof(WsCtl, error) == 4, "error is word 1 of the control block");
+  if (i < 64u) ctl[i] = (i == 1u && n_idx && *n_idx > n) ? 2u : 0u;
   for (; i < n; i += gridDim.x * blockDim.x) status[i] = 0;
 }
 
@@ -1402,7 +1409,7 @@ __global__ __launch_bounds__(256) void k_encode_finish(
   if (global_crc && blockIdx.x == 0 && threadIdx.x == 0) *global_crc = crcs[0];
   if (ctl->error) {  // invalid index list or an abandoned scan: no payload
     if (blockIdx.x == 0 && threadIdx.x == 0) {
-      *reinterpret_cast<uint4 *>(payload) = make_uint4(0, 0, 0, 0);
+      for (int i = 0; i < 4; ++i) reinterpret_cast<uint4 *>(payload)[i] = make_uint4(0, 0, 0, 0);
       if (payload_bytes) *payload_bytes = 0;
       if (n_dirty) *n_dirty = 0;
     }
@@ -2302,7 +2309,7 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_plan(
   __shared__ HufWave sw[kHufWaves];
   const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
   HufWave &W = sw[wave];
-  const uint32_t n_items = idx ? min(*n_idx, g.n_chunks) : g.n_chunks;
+  const uint32_t n_items = idx ? (*n_idx > g.n_chunks ? 0u : *n_idx) : g.n_chunks;
   for (uint32_t item = blockIdx.x * kHufWaves + wave; item < n_items;
        item += gridDim.x * kHufWaves) {
     uint32_t c = idx ? idx[item] : item;
@@ -2392,7 +2399,7 @@ __global__ __launch_bounds__(1024) void k_huf_scan(const uint32_t *__restrict__ 
                                                    ChunkGeom g, uint8_t *__restrict__ plans,
                                                    WsCtl *ctl) {
   __shared__ uint32_t wsum[16];
-  const uint32_t n_items = n_idx ? min(*n_idx, g.n_chunks) : g.n_chunks;
+  const uint32_t n_items = n_idx ? (*n_idx > g.n_chunks ? 0u : *n_idx) : g.n_chunks;
   uint64_t carry = 64;
   for (uint32_t base = 0; base < n_items; base += 1024u) {
     const uint32_t i = base + threadIdx.x;
@@ -2433,7 +2440,7 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_write(
   HufWave &W = sw[wave];
   uint4 *tab_ws = reinterpret_cast<uint4 *>(ws + L.table);
   uint32_t *ecrc = reinterpret_cast<uint32_t *>(ws + L.entry_crc);
-  const uint32_t n_items = n_idx ? min(*n_idx, g.n_chunks) : g.n_chunks;
+  const uint32_t n_items = n_idx ? (*n_idx > g.n_chunks ? 0u : *n_idx) : g.n_chunks;
   for (uint32_t item = blockIdx.x * kHufWaves + wave; item < n_items;
        item += gridDim.x * kHufWaves) {
     const uint8_t *P = plans + (uint64_t)item * kHufPlanBytes;
@@ -2973,7 +2980,8 @@ int launch_encode(int mode, const void *cur, const void *prev, const ChunkGeom &
                   uint32_t *n_dirty, void *payload, uint64_t *payload_bytes, void *ws,
                   const WsLayout &L, int n_cu, void *stream) {
   uint8_t *wsb = static_cast<uint8_t *>(ws);
-  hipLaunchKernelGGL(k_encode_prepare, dim3(64), dim3(256), 0, S(stream), wsb, L, g.n_chunks);
+  hipLaunchKernelGGL(k_encode_prepare, dim3(64), dim3(256), 0, S(stream), wsb, L, g.n_chunks,
+                     mode == kModeList ? n_idx : nullptr);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
   EncArgs a;
@@ -3154,7 +3162,8 @@ int launch_encode_v2(const void *state, const ChunkGeom &g, const uint32_t *idx,
   uint8_t *wsb = static_cast<uint8_t *>(ws);
   WsCtl *ctl = reinterpret_cast<WsCtl *>(wsb + L.ctl);
   const uint8_t *st = static_cast<const uint8_t *>(state);
-  hipLaunchKernelGGL(k_encode_prepare, dim3(64), dim3(256), 0, S(stream), wsb, L, g.n_chunks);
+  hipLaunchKernelGGL(k_encode_prepare, dim3(64), dim3(256), 0, S(stream), wsb, L, g.n_chunks,
+                     idx ? n_idx : nullptr);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
   const uint32_t *crcs = crc_in;

@@ -59,7 +59,7 @@ class Mover:
                with_crc: bool = True):
         idx = self.dirty_idx if dirty_only else None
         n_idx = self.n_dirty if dirty_only else None
-        crc = self.crc if (with_crc or dirty_only) else None
+        crc = self.crc if with_crc else None
         self._crc_of_shipped = None
         _wm.encode(state, self.nbytes, self.p, idx, n_idx, crc, self.payload,
                    self.payload_bytes, self.ws_src, self.stream)

@@ -144,7 +144,9 @@ def test_encode_argument_checks(lib):
     enc = lib.wm_encode
     assert enc(a, 4 * CH + 1, P(), None, None, None, a, bound, a, a, ws, None) == INVALID  # odd
     assert enc(a, 4 * CH, P(), a, None, a, a, bound, a, a, ws, None) == INVALID  # idx w/o n_idx
-    assert enc(a, 4 * CH, P(), a, a, None, a, bound, a, a, ws, None) == INVALID  # list w/o CRCs
+    # a list without CRCs is valid (the call checksums every chunk); its
+    # other arguments are checked as usual
+    assert enc(a, 4 * CH, P(), a, a, None, a, bound, a, a, ws - 1, None) == WORKSPACE
     assert enc(a, 4 * CH, P(), None, None, None, a, bound - 1, a, a, ws, None) == CAPACITY
     assert enc(a, 4 * CH, P(), None, None, None, a, bound, a, a, ws - 1, None) == WORKSPACE
     assert enc(a, 4 * CH, P(), None, None, None, a + 8, big, a, a, ws, None) == INVALID

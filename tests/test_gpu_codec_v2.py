@@ -79,7 +79,27 @@ def _edge_states():
     out["tail_4098"] = bf[: 2 * CH + 4098].copy()  # a row piece straddles the end
     out["one_word_tail"] = bf[: CH + 2].copy()
     out["two_exponents"] = np.where(rng.random(n) < 0.9, 0x3F80, 0x4000).astype(np.uint16).view(np.uint8)
+    # more than 64 distinct exponents in a chunk that still codes as HUF (the
+    # plan's code construction past one wave's 64 lanes, and the length cap)
+    for scale in (6, 20):
+        e = np.clip(127 + np.round(rng.laplace(0, scale, n)), 0, 255).astype(np.int64)
+        sm = rng.integers(0, 256, n)
+        w = (((sm >> 7) << 15) | (e << 7) | (sm & 127)).astype(np.uint16)
+        out[f"laplace_{scale}"] = w.view(np.uint8)
     return out
+
+
+@pytest.mark.parametrize("scale,min_distinct", [(6, 100), (20, 240)])
+def test_wide_alphabet_states_plan_huf(scale, min_distinct):
+    """The wide-alphabet edge states really have more than 64 symbols per
+    chunk and plan HUF (so the GPU test of them exercises that path)."""
+    state = _edge_states()[f"laplace_{scale}"]
+    for c in range(0, state.size, CH):
+        ch = state[c:c + CH]
+        e = (ch.view(np.uint16) >> 7) & 255
+        assert np.unique(e).size >= min_distinct
+        plan = oracle.plan_chunk_v2(ch)
+        assert plan["mode"] == 2 and plan["k"] == 11, plan
 
 
 @pytest.mark.parametrize("name", list(_edge_states().keys()))

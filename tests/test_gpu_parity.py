@@ -101,13 +101,17 @@ def test_invalid_index_list_gives_an_empty_payload(wm, codec):
     nbytes = state.numel() * 2
     m = mover(nbytes, 0, codec=codec)
     m.checksum(state)
-    for bad in ([3, 3, 5], [5, 2, 9], [0, 1, 32], [7, 40]):
+    # the last list is one entry longer than the chunk count: its first 32
+    # entries alone would be a valid full list
+    for bad in ([3, 3, 5], [5, 2, 9], [0, 1, 32], [7, 40], list(range(32)) + [32]):
         idx = torch.tensor(bad, dtype=torch.int32, device="cuda")
         n_idx = torch.tensor([len(bad)], dtype=torch.int32, device="cuda")
         m.payload_bytes.fill_(123)
+        m.payload[:64].fill_(0xEE)
         wm.encode(state, nbytes, m.p, idx, n_idx, m.crc, m.payload, m.payload_bytes, m.ws_src)
         torch.cuda.synchronize()
         assert int(m.payload_bytes.item()) == 0, (codec, bad)
+        assert not m.payload[:64].any(), (codec, bad)
     good = np.array([1, 4, 9, 31], dtype=np.uint32)
     idx = torch.from_numpy(good.view(np.int32)).cuda()
     n_idx = torch.tensor([good.size], dtype=torch.int32, device="cuda")
@@ -272,3 +276,115 @@ def test_production_full_ship(wm):
     m = mover(state.numel() * 2)
     got = check_full_ship(m, state, 0, "production", fused=True)
     say(f"[production] payload {got.size} bytes, ratio {got.size / (state.numel() * 2):.4f}")
+
+
+def _exp_words(rng, n, width, base, esc_frac):
+    """n bf16 words whose exponents are uniform over [base, base + width),
+    a fraction esc_frac of them replaced by uniform exponents over 0..255;
+    sign and mantissa uniform."""
+    e = base + rng.integers(0, width, n)
+    m = rng.random(n) < esc_frac
+    e[m] = rng.integers(0, 256, int(m.sum()))
+    sm = rng.integers(0, 256, n)
+    return ((sm >> 7) << 15) | (e << 7) | (sm & 127)
+
+
+def code_width_state(k: int) -> np.ndarray:
+    """Three chunks whose oracle plan is PACK with code width k: a full chunk
+    with 2% escapes, a full chunk with none (5% escapes for k = 1, where a
+    window of one exponent and no escapes is the constant record), and a
+    5,536-byte tail with 2% escapes."""
+    rng = np.random.default_rng(100 + k)
+    width = (1 << k) - 1
+    base = 128 - width // 2
+    n = CH // 2
+    return np.concatenate([_exp_words(rng, n, width, base, 0.02),
+                           _exp_words(rng, n, width, base, 0.05 if k == 1 else 0.0),
+                           _exp_words(rng, 2768, width, base, 0.02)]).astype(np.uint16)
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+@pytest.mark.parametrize("k", range(1, 8))
+def test_every_code_width(wm, k, kind):
+    """PACK records of every code width k = 1..7 (the k-specialised packing
+    and unpacking paths, including codes that straddle three dwords for k =
+    5..7), on full chunks and a short tail, with and without escapes, through
+    the full ship, the encoder with CRCs given, and the fused step."""
+    words = code_width_state(k)
+    hw = words.view(np.uint8)
+    for c in range(3):
+        plan = oracle.plan_chunk(hw[c * CH:(c + 1) * CH])
+        assert plan["mode"] == 1 and plan["k"] == k, (k, c, plan)
+        assert (plan["n_esc"] > 0) == (c != 1 or k == 1), (k, c, plan)
+    state = _words_state(words)
+    nbytes = state.numel() * 2
+    m = mover(nbytes, kind)
+    check_full_ship(m, state, kind, f"k={k}", fused=(kind == 0))
+    # fused step against a snapshot whose chunk 1 is unchanged
+    prev = state.clone()
+    prev[:10] ^= 1
+    prev[-5:] ^= 0x100
+    m2 = mover(nbytes, kind)
+    m2.encode_step(state, prev)
+    torch.cuda.synchronize()
+    want_idx = np.array([0, 2], np.uint32)
+    assert np.array_equal(m2.dirty_host(), want_idx)
+    want = oracle.encode(kind, host_bytes(state), CH, want_idx)
+    assert np.array_equal(m2.payload_host(), want), k
+    live = prev.clone()
+    m2.decode()
+    assert m2.commit(live, scatter=True) == 0
+    assert torch.equal(live, state)
+
+
+def test_bit_flips_in_wide_code_records(wm):
+    """Flipped bits in PACK k=6 and k=7 records (codes, escape index,
+    escapes, sign/mantissa plane, padding): the GPU verdict word and record
+    status equal the oracle's, and a scatter commit leaves live untouched."""
+    rng = np.random.default_rng(66)
+    n = CH // 2
+    words = np.concatenate([_exp_words(rng, n, 63, 97, 0.02),
+                            _exp_words(rng, 1000, 127, 65, 0.03)]).astype(np.uint16)
+    hw = words.view(np.uint8)
+    assert oracle.plan_chunk(hw[:CH])["k"] == 6
+    assert oracle.plan_chunk(hw[CH:])["k"] == 7
+    state = _words_state(words)
+    nbytes = state.numel() * 2
+    m = mover(nbytes)
+    m.encode_step(state, None)
+    torch.cuda.synchronize()
+    good = m.payload_host()
+    assert np.array_equal(good, oracle.encode(0, host_bytes(state), CH))
+    n_rec = 2
+    positions = rng.integers(64, good.size - 16 * n_rec, 160).tolist()
+    live0 = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    for pos in positions:
+        bit = int(rng.integers(0, 8))
+        bad = good.copy()
+        bad[pos] ^= 1 << bit
+        m.payload[: bad.size].copy_(torch.from_numpy(bad))
+        m.decode(payload_cap=bad.size)
+        live = live0.clone()
+        rc = m.commit(live, scatter=True)
+        v_gpu = int(m.verdict.item())
+        v_orc, _, st = oracle.decode_verify(0, bad, nbytes, CH)
+        assert v_orc != 0 and v_gpu == v_orc, (pos, bit, v_gpu, v_orc)
+        assert rc == 1 and not live.any()
+        assert np.array_equal(u32(m.rec_status)[:n_rec], st[:n_rec]), pos
+
+
+@pytest.mark.parametrize("codec", [1, 2])
+def test_list_encode_without_crcs(wm, codec):
+    """wm_encode of an index list with crc = NULL: the call checksums every
+    chunk itself, so the payload (receipts and the header's global CRC of the
+    whole state) equals the oracle's."""
+    prev, cur, ids = wm_inputs.tiny_step("cuda")
+    nbytes = cur.numel() * 2
+    m = mover(nbytes, 1, codec=codec)
+    m.diff(cur, prev)
+    m.crc.fill_(0x5A5A5A5A)  # not read
+    m.encode(cur, dirty_only=True, with_crc=False)
+    torch.cuda.synchronize()
+    idx = oracle.diff_dirty(host_bytes(cur), host_bytes(prev), CH)
+    want = oracle.encode(1, host_bytes(cur), CH, idx, ORACLE_THREADS, codec=codec)
+    assert np.array_equal(m.payload_host(), want)

@@ -10,7 +10,9 @@ code paths:
   * a brute-force argmin over every (k, base) on tiny chunks;
   * escape-index entries counted word by word;
   * hand-built expected bytes for a three-chunk payload (PACK k=0, PACK
-    k=2, RAW), with CRCs from zlib.
+    k=2, RAW) and for a two-record payload with escapes (PACK k=5 with
+    escapes in four 512-word blocks, PACK k=7 on a short tail), with CRCs
+    from zlib.
 """
 import struct
 import zlib
@@ -248,3 +250,81 @@ def test_escape_index_counts():
     esc = [not (base <= x < base + (1 << k) - 1) for x in e]
     want = [sum(esc[: 512 * b]) for b in range(4)]
     assert index.tolist() == want
+
+
+def _pack_stream(codes, k):
+    """LSB-first k-bit stream: bit b of code i is stream bit i*k + b, stream
+    bit j is bit j mod 8 of byte j div 8 (format v1, PACK body)."""
+    out = bytearray((len(codes) * k + 7) // 8)
+    for i, c in enumerate(codes):
+        for b in range(k):
+            if (c >> b) & 1:
+                j = i * k + b
+                out[j // 8] |= 1 << (j % 8)
+    return bytes(out)
+
+
+def _zpad(b):
+    return b + bytes(pad16(len(b)) - len(b))
+
+
+def _pack_record(words, k, base):
+    """A PACK record written out field by field from the format text: header,
+    codes, escape index (escapes before each 512-word block), escapes in word
+    order, sign/mantissa plane; each section zero-padded to 16 bytes."""
+    words = [int(w) for w in words]
+    n = len(words)
+    esc = (1 << k) - 1
+    e = [(w >> 7) & 255 for w in words]
+    sm = bytes(((w >> 15) << 7) | (w & 127) for w in words)
+    codes = [x - base if 0 <= x - base < esc else esc for x in e]
+    escaped = [x for x, c in zip(e, codes) if c == esc]
+    index = b"".join(struct.pack("<H", sum(1 for c in codes[: 512 * b] if c == esc))
+                     for b in range((n + 511) // 512))
+    h = struct.pack("<BBBBII", 1, k, base, 0, n, len(escaped))
+    h += struct.pack("<I", zlib.crc32(h))
+    body = _zpad(_pack_stream(codes, k)) + _zpad(index) + _zpad(bytes(escaped)) + _zpad(sm)
+    return h + body, len(escaped)
+
+
+def test_hand_built_payload_with_escapes():
+    """Two records with escapes, expected bytes written here from the format
+    text (CRCs from zlib): chunk 0 is PACK k=5 (exponents 100..130, escapes
+    three in block 0 and one in each of blocks 1, 2 and 3, so the index
+    entries are 0, 3, 4, 5), chunk 1
+    a 1,000-byte tail that is PACK k=7 (exponents 60..186 and two escapes).
+    The dirty list ships both, so the FULL flag stays clear."""
+    n0 = CH // 2
+    rng = np.random.default_rng(31)
+    e0 = 100 + (np.arange(n0) * 7) % 31
+    for pos, val in [(5, 20), (300, 255), (511, 0), (512, 99), (1100, 131), (1900, 7)]:
+        e0[pos] = val
+    sm0 = rng.integers(0, 256, n0)
+    c0 = (((sm0 >> 7) << 15) | (e0 << 7) | (sm0 & 127)).astype(np.uint16)
+    n1 = 500
+    e1 = 60 + (np.arange(n1) * 5) % 127
+    e1[17], e1[499] = 0, 255
+    sm1 = rng.integers(0, 256, n1)
+    c1 = (((sm1 >> 7) << 15) | (e1 << 7) | (sm1 & 127)).astype(np.uint16)
+    state = np.concatenate([c0, c1]).view(np.uint8)
+    assert state.size == CH + 1000
+
+    r0, esc0 = _pack_record(c0, 5, 100)
+    r1, esc1 = _pack_record(c1, 7, 60)
+    assert esc0 == 6 and esc1 == 2
+    assert r0[16 + pad16(n0 * 5 // 8): 16 + pad16(n0 * 5 // 8) + 8] == \
+        struct.pack("<HHHH", 0, 3, 4, 5)
+    assert len(r1) == 16 + pad16((n1 * 7 + 7) // 8) + 16 + 16 + pad16(n1)
+    table = struct.pack("<IIQ", 0, zlib.crc32(c0.tobytes()), 64)
+    table += struct.pack("<IIQ", 1, zlib.crc32(c1.tobytes()), 64 + len(r0))
+    total = 64 + len(r0) + len(r1) + len(table)
+    head = b"WMV1" + struct.pack("<HBBIIQIIQII", 1, 0, 1, CH, 2, state.size,
+                                 2, 0, total, zlib.crc32(state.tobytes()),
+                                 zlib.crc32(table)) + bytes(12)
+    head += struct.pack("<I", zlib.crc32(head))
+    want = head + r0 + r1 + table
+    got = oracle.encode(0, state, CH, np.array([0, 1], np.uint32)).tobytes()
+    assert len(got) == len(want) == total
+    assert got == want
+    v, staging, _ = oracle.decode_verify(0, got, state.size, CH)
+    assert v == 0 and np.array_equal(staging[: state.size], state)
