@@ -176,6 +176,27 @@ wm_status wm_encode_step(const void *cur, const void *prev, uint64_t nbytes,
                          uint64_t *payload_bytes, void *ws, uint64_t ws_bytes,
                          void *stream);
 
+/* wm_encode_step for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * outputs, byte for byte, with the workspace taken from a built-in device
+ * array instead of the caller.  The call allocates nothing, on the host or
+ * on the device.
+ *   Limit: states of at most 65,536 chunks (4 GiB in 64 KiB chunks); a larger
+ *   state returns WM_ERR_WORKSPACE before anything is enqueued.
+ *   Sharing: each device holds one built-in workspace (2 MiB + 256 B, kept
+ *   until the process ends) used by every call of this function on that
+ *   device, whatever the stream.  Calls that overlap in time on one device
+ *   race on it and give undefined results: order them (one stream, or
+ *   events).  A call clears what it needs zeroed itself; the workspace keeps
+ *   the last call's contents.
+ * Other arguments, outputs and errors as wm_encode_step. */
+wm_status wm_encode_step_static(const void *cur, const void *prev,
+                                uint64_t nbytes, const wm_params *p,
+                                uint32_t *crc_out, uint32_t *global_crc,
+                                uint32_t *dirty_idx, uint32_t *n_dirty,
+                                void *payload, uint64_t payload_cap,
+                                uint64_t *payload_bytes, void *stream);
+
 /* Validate and decode a payload into staging, re-checksumming every decoded
  * chunk against its receipt (§6.4: decode sits inside the verified
  * envelope; Table 1: verify).  Reads never leave [payload, payload +

@@ -42,7 +42,7 @@ EXPORTS = (
     "wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_encode_step",
     "wm_decode_verify", "wm_commit_or_abort", "wm_flat_bytes",
     "wm_manifest_ws_bytes", "wm_flatten", "wm_rehydrate", "wm_precopy_round",
-    "wm_receive_verify",
+    "wm_receive_verify", "wm_encode_step_static",
 )
 
 
@@ -92,6 +92,8 @@ def _load():
                       ctypes.c_int32),
         "wm_encode_step": ([vp, vp, u64, pp, vp, vp, vp, vp, vp, u64, vp, vp,
                             u64, vp], ctypes.c_int32),
+        "wm_encode_step_static": ([vp, vp, u64, pp, vp, vp, vp, vp, vp, u64, vp,
+                                   vp], ctypes.c_int32),
         "wm_decode_verify": ([vp, u64, u64, pp, vp, u64, vp, vp, vp, u64, vp],
                              ctypes.c_int32),
         "wm_commit_or_abort": ([vp, u64, pp, vp, vp, vp, u32, vp],
@@ -195,6 +197,16 @@ def encode_step(cur, prev, nbytes, p, crc_out, global_crc, dirty_idx, n_dirty,
                                      _nbytes(payload), _p(payload_bytes),
                                      _p(ws), _nbytes(ws), _stream(stream)),
                   "wm_encode_step")
+
+
+def encode_step_static(cur, prev, nbytes, p, crc_out, global_crc, dirty_idx,
+                       n_dirty, payload, payload_bytes, stream=None):
+    """wm_encode_step on the device's built-in workspace (allocates
+    nothing; calls on one device must not overlap)."""
+    return _check(LIB.wm_encode_step_static(
+        _p(cur), _p(prev), nbytes, ctypes.byref(p), _p(crc_out), _p(global_crc),
+        _p(dirty_idx), _p(n_dirty), _p(payload), _nbytes(payload),
+        _p(payload_bytes), _stream(stream)), "wm_encode_step_static")
 
 
 def decode_verify(payload, payload_cap, nbytes, p, staging, verdict,

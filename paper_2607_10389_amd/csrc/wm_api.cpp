@@ -20,10 +20,15 @@ namespace {
 
 constexpr int kMaxDevices = 64;
 constexpr uint64_t kMaxBatches = 4096;  // record batches of one received payload
+// Size of the built-in workspace (kScratchBytes of the device array): the
+// layout of 65,536 chunks.
+constexpr uint64_t kBuiltinWsBytes = 256 + 32ull * 65536;
 
 struct DeviceState {
   bool ready = false;
   int n_cu = 0;
+  void *scratch = nullptr;  // device address of the built-in workspace
+  uint64_t scratch_bytes = 0;
 };
 
 std::mutex g_mu;
@@ -37,7 +42,7 @@ struct TailGeom {
 };
 std::map<uint64_t, TailGeom> g_tail_cache;
 
-wm_status ensure_device(int *n_cu) {
+wm_status ensure_device(int *n_cu, void **scratch = nullptr, uint64_t *scratch_bytes = nullptr) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return WM_ERR_HIP;
   std::lock_guard<std::mutex> lock(g_mu);
@@ -54,10 +59,18 @@ wm_status ensure_device(int *n_cu) {
     if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         cu <= 0)
       return WM_ERR_HIP;
+    // the built-in workspace's address on this device (the current one)
+    void *sp = nullptr;
+    uint64_t sb = 0;
+    if (scratch_address(&sp, &sb) != 0 || !sp) return WM_ERR_HIP;
     st.n_cu = cu;
+    st.scratch = sp;
+    st.scratch_bytes = sb;
     st.ready = true;
   }
   *n_cu = st.n_cu;
+  if (scratch) *scratch = st.scratch;
+  if (scratch_bytes) *scratch_bytes = st.scratch_bytes;
   return WM_OK;
 }
 
@@ -73,7 +86,9 @@ wm_status check_params(const wm_params *p) {
   return WM_OK;
 }
 
-wm_status make_geom(uint64_t nbytes, const wm_params *p, ChunkGeom *g) {
+// cache_tail: keep the short last chunk's shift matrix in a host map for
+// later calls (false: compute it in place, allocating nothing).
+wm_status make_geom(uint64_t nbytes, const wm_params *p, ChunkGeom *g, bool cache_tail = true) {
   wm_status s = check_params(p);
   if (s != WM_OK) return s;
   uint64_t n = (nbytes + kChunk - 1) / kChunk;
@@ -85,7 +100,11 @@ wm_status make_geom(uint64_t nbytes, const wm_params *p, ChunkGeom *g) {
   g->codec = p->codec;
   g->k_tail = 0;
   for (int i = 0; i < 32; ++i) g->tail_mat[i] = 1u << i;
-  if (g->tail_len != kChunk) {
+  if (g->tail_len != kChunk && !cache_tail) {
+    const uint32_t poly = poly_of(p->crc_kind);
+    g->k_tail = shift_apply(poly, g->tail_len, 0xFFFFFFFFu) ^ 0xFFFFFFFFu;
+    shift_matrix(poly, -(int64_t)(kChunk - g->tail_len), g->tail_mat);
+  } else if (g->tail_len != kChunk) {
     uint64_t key = ((uint64_t)p->crc_kind << 32) | g->tail_len;
     std::lock_guard<std::mutex> lock(g_mu);
     auto it = g_tail_cache.find(key);
@@ -231,12 +250,19 @@ wm_status wm_encode(const void *state, uint64_t nbytes, const wm_params *p, cons
                                   nullptr, nullptr, payload, payload_bytes, ws, L, n_cu, stream));
 }
 
-wm_status wm_encode_step(const void *cur, const void *prev, uint64_t nbytes, const wm_params *p,
-                         uint32_t *crc_out, uint32_t *global_crc, uint32_t *dirty_idx,
-                         uint32_t *n_dirty, void *payload, uint64_t payload_cap,
-                         uint64_t *payload_bytes, void *ws, uint64_t ws_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// wm_encode_step on a caller's workspace, or (builtin) on the device's
+// built-in one: then nothing is allocated on the way, host or device.
+wm_status encode_step_call(const void *cur, const void *prev, uint64_t nbytes,
+                           const wm_params *p, uint32_t *crc_out, uint32_t *global_crc,
+                           uint32_t *dirty_idx, uint32_t *n_dirty, void *payload,
+                           uint64_t payload_cap, uint64_t *payload_bytes, void *ws,
+                           uint64_t ws_bytes, bool builtin, void *stream) {
   ChunkGeom g;
-  wm_status s = make_geom(nbytes, p, &g);
+  wm_status s = make_geom(nbytes, p, &g, !builtin);
   if (s != WM_OK) return s;
   if (g.codec != WM_CODEC_EXPFOR) return WM_ERR_UNSUPPORTED;
   if (nbytes & 1u) return WM_ERR_INVALID_ARG;
@@ -244,15 +270,42 @@ wm_status wm_encode_step(const void *cur, const void *prev, uint64_t nbytes, con
   if (!payload || !payload_bytes || !aligned16(payload)) return WM_ERR_INVALID_ARG;
   if (payload_cap < wm_payload_bound(nbytes, g.n_chunks, p)) return WM_ERR_CAPACITY;
   WsLayout L = ws_layout(g.n_chunks);
-  if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
   int n_cu = 0;
-  if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  if (builtin) {
+    // the size limit is checked before the device is touched
+    if (L.total > kBuiltinWsBytes) return WM_ERR_WORKSPACE;
+    if ((s = ensure_device(&n_cu, &ws, &ws_bytes)) != WM_OK) return s;
+    if (L.total > ws_bytes) return WM_ERR_WORKSPACE;
+  } else {
+    if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
+    if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  }
   n_cu = stream_cus(stream, n_cu);
   uint32_t *crcs =
       crc_out ? crc_out : reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + L.flags);
   return hip_status(launch_encode(2, cur, prev, g, nullptr, nullptr, nullptr, crcs, global_crc,
                                   dirty_idx, n_dirty, payload, payload_bytes, ws, L, n_cu,
                                   stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+wm_status wm_encode_step(const void *cur, const void *prev, uint64_t nbytes, const wm_params *p,
+                         uint32_t *crc_out, uint32_t *global_crc, uint32_t *dirty_idx,
+                         uint32_t *n_dirty, void *payload, uint64_t payload_cap,
+                         uint64_t *payload_bytes, void *ws, uint64_t ws_bytes, void *stream) {
+  return encode_step_call(cur, prev, nbytes, p, crc_out, global_crc, dirty_idx, n_dirty, payload,
+                          payload_cap, payload_bytes, ws, ws_bytes, false, stream);
+}
+
+wm_status wm_encode_step_static(const void *cur, const void *prev, uint64_t nbytes,
+                                const wm_params *p, uint32_t *crc_out, uint32_t *global_crc,
+                                uint32_t *dirty_idx, uint32_t *n_dirty, void *payload,
+                                uint64_t payload_cap, uint64_t *payload_bytes, void *stream) {
+  return encode_step_call(cur, prev, nbytes, p, crc_out, global_crc, dirty_idx, n_dirty, payload,
+                          payload_cap, payload_bytes, nullptr, 0, true, stream);
 }
 
 wm_status wm_decode_verify(const void *payload, uint64_t payload_cap, uint64_t nbytes,

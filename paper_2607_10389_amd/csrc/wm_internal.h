@@ -138,5 +138,8 @@ int launch_decode_v2(const void *payload, uint64_t payload_cap, const ChunkGeom 
                      uint32_t *rec_status, void *ws, const WsLayout &L, int n_cu,
                      void *stream);
 int set_kernel_attributes();
+// Device address and size of the built-in workspace (a file-scope device
+// array) on the current device.
+int scratch_address(void **ptr, uint64_t *bytes);
 
 }  // namespace wm

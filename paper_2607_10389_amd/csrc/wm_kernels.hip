@@ -2936,6 +2936,20 @@ int set_kernel_attributes() {
   return 0;
 }
 
+// Built-in workspace of wm_encode_step_static, for callers that cannot
+// allocate: the workspace layout of 65,536 chunks (a 4 GiB state in 64 KiB
+// chunks).  Each device holds its own copy at its own address, shared by
+// every call on that device.  Host code must never pass `scratch` itself to
+// a kernel (on the host it is only a stand-in for the symbol): launches take
+// the device address that scratch_address returns.
+constexpr uint64_t kScratchBytes = 256 + 32ull * 65536;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+int scratch_address(void **ptr, uint64_t *bytes) {
+  *bytes = kScratchBytes;
+  return (int)hipGetSymbolAddress(ptr, HIP_SYMBOL(scratch));
+}
+
 static int launch_combine(const CombineJobs &jobs, int n_jobs, void *stream) {
   hipLaunchKernelGGL(k_combine, dim3(n_jobs), dim3(1024), 0, S(stream), jobs);
   return (int)hipGetLastError();

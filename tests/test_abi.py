@@ -65,6 +65,7 @@ def lib():
     L.wm_diff_dirty.argtypes = [vp, vp, u64, pp, vp, vp, vp, u64, vp]
     L.wm_encode.argtypes = [vp, u64, pp, vp, vp, vp, vp, u64, vp, vp, u64, vp]
     L.wm_encode_step.argtypes = [vp, vp, u64, pp, vp, vp, vp, vp, vp, u64, vp, vp, u64, vp]
+    L.wm_encode_step_static.argtypes = [vp, vp, u64, pp, vp, vp, vp, vp, vp, u64, vp, vp]
     L.wm_decode_verify.argtypes = [vp, u64, u64, pp, vp, u64, vp, vp, vp, u64, vp]
     L.wm_commit_or_abort.argtypes = [vp, u64, pp, vp, vp, vp, u32, vp]
     lp = ctypes.POINTER(Leaf)
@@ -94,7 +95,7 @@ def test_header_declares_the_boundary():
     for must in ("wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_decode_verify",
                  "wm_commit_or_abort", "wm_flatten", "wm_rehydrate"):
         assert must in names
-    assert len(names) == len(set(names)) == 16
+    assert len(names) == len(set(names)) == 17
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -285,3 +286,16 @@ def test_format_v2_calls(lib):
     n = ctypes.c_uint32(0)
     assert lib.wm_precopy_round(a, a + 0x100000, a + 0x200000, nb, P(codec=2), None, 0,
                                 ctypes.byref(n), None) == UNSUPPORTED
+
+
+def test_static_step_refuses_a_state_beyond_its_workspace(lib):
+    """wm_encode_step_static's built-in workspace holds 65,536 chunks; a
+    larger state is refused on the host before any device work."""
+    a = ALIGNED
+    nbytes = 65537 * CH
+    bound = lib.wm_payload_bound(nbytes, 65537, P())
+    fn = lib.wm_encode_step_static
+    assert fn(a, None, nbytes, P(), None, None, None, None, a, bound, a, None) == WORKSPACE
+    # the usual argument checks come first
+    assert fn(a, None, nbytes + 1, P(), None, None, None, None, a, bound, a, None) == INVALID
+    assert fn(a, None, nbytes, P(), None, None, None, None, a, bound - 1, a, None) == CAPACITY
