@@ -21,7 +21,6 @@ constexpr int kThreads = kWaves * 64;
 constexpr uint32_t kRow = 1024;             // bytes per wave row: 64 lanes x 16 B
 constexpr uint32_t kSub = kChunk / kWaves;  // bytes of a chunk per wave
 constexpr int kRows = kSub / kRow;          // rows per lane
-constexpr int kTree = 6;                    // log2(64) lanes
 
 // Constant tables for one CRC kind (built on the host, uploaded once).
 struct CrcTables {
@@ -30,7 +29,9 @@ struct CrcTables {
   uint32_t f4[4][256];           // F^4      (standard 4-byte step)
   uint32_t f8[4][256];           // F^8
   uint32_t f12[4][256];          // F^12     (lane merge)
-  uint32_t tree[kTree][4][256];  // F^(16 << l): lane-tree levels
+  // F^(16 (63 - l) + 4), lane l's shift: columns 4q..4q+3 at lane_mat[q][l]
+  // (a 16-byte read of the 64 lanes covers 1 KiB of consecutive banks)
+  uint32_t lane_mat[8][64][4];
   uint32_t wave_step[4][256];    // F^kSub: one wave's share of a chunk
   uint32_t byte1[256];           // one-byte step of the table method
   uint32_t pow2[48][32];         // F^(2^i) bytes, columns

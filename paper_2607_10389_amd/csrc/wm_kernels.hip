@@ -10,9 +10,10 @@
 // runs four independent dword "column" streams down its rows:
 //     v <- F^1024(v ^ d)
 // (the next dword of the column is 1 KiB further on).  A lane's four columns
-// merge into one value, the 64 lane values of a wave merge through a 6-level
-// shuffle tree of byte-table shifts, and wave values merge through one GF(2)
-// matrix per wave.  The F^1024 tables are the hot ones: 16 copies in LDS,
+// merge into one value, the lane values of the eight waves fold together
+// through one byte-table shift per wave, and each lane's fold enters the chunk
+// value through a GF(2) matrix of its own (its distance from the chunk end),
+// the 64 results XORed across the wave.  The F^1024 tables are the hot ones: 16 copies in LDS,
 // addressed as byte*256 + slot*64 + copy*4 with v_perm, where each group of
 // 16 lanes starts at a different table slot so that one ds_read touches every
 // bank once.  All other shift tables are read rarely and kept single.
@@ -31,16 +32,16 @@ namespace wm {
 __device__ CrcTables g_tables[2];
 
 // ------------------------------------------------------------ LDS layout --
-// The first 16 KiB are kernel-specific (encoder histogram, decoder escape
+// The first 32 KiB are kernel-specific (encoder histogram, decoder escape
 // windows): below 64 KiB, so their base folds into an instruction's offset.
 constexpr uint32_t kLdsLow = 0;
-constexpr uint32_t kLdsLowBytes = 16384;
+constexpr uint32_t kLdsLowBytes = 32768;
 constexpr uint32_t kLdsG = kLdsLow + kLdsLowBytes;  // 64 KiB, replicated F^1024
 constexpr uint32_t kLdsF4 = kLdsG + 65536;          // 4 KiB each: F^4, F^8, F^12
 constexpr uint32_t kLdsF8 = kLdsF4 + 4096;
 constexpr uint32_t kLdsF12 = kLdsF8 + 4096;
-constexpr uint32_t kLdsTree = kLdsF12 + 4096;       // 6 x 4 KiB
-constexpr uint32_t kLdsWaveStep = kLdsTree + kTree * 4096;  // 4 KiB, F^kSub
+constexpr uint32_t kLdsLaneMat = kLdsF12 + 4096;    // 64 lanes x 32 columns (8 KiB)
+constexpr uint32_t kLdsWaveStep = kLdsLaneMat + 8192;  // 4 KiB, F^kSub
 constexpr uint32_t kLdsCrcEnd = kLdsWaveStep + 4096;        // 122880
 constexpr uint32_t kLdsMisc = kLdsCrcEnd;           // 4 KiB of small scratch
 constexpr uint32_t kLdsMiscBytes = 4096;
@@ -154,10 +155,12 @@ __device__ void load_crc_tables(uint32_t kind) {
   uint32_t *g = reinterpret_cast<uint32_t *>(lds_at(kLdsG));
   for (uint32_t i = threadIdx.x; i < 16384u; i += blockDim.x)
     g[i] = T.row[(i >> 4) & 3u][i >> 6];
-  const uint32_t *src = &T.f4[0][0];  // f4, f8, f12, tree, wave_step
+  const uint32_t *src = &T.f4[0][0];  // f4, f8, f12, lane_mat, wave_step
   uint32_t *dst = reinterpret_cast<uint32_t *>(lds_at(kLdsF4));
-  for (uint32_t i = threadIdx.x; i < (4u + kTree) * 1024u; i += blockDim.x)
-    dst[i] = src[i];
+  static_assert(offsetof(CrcTables, wave_step) - offsetof(CrcTables, f4) == 5 * 4096u &&
+                    kLdsWaveStep - kLdsF4 == 5 * 4096u,
+                "f4 .. wave_step copied as one block");
+  for (uint32_t i = threadIdx.x; i < 6u * 1024u; i += blockDim.x) dst[i] = src[i];
 }
 
 // Columns applied to v; `m` must be wave-uniform (the columns then arrive
@@ -282,7 +285,7 @@ __device__ __forceinline__ void load_chunk(const uint8_t *__restrict__ base,
 //     kChunk - o = kSub (7 - w) + kRow (7 - h) + 16 (63 - l) + 4 (3 - j) + 4.
 // The four factors are applied in stages: column streams over the rows
 // (w_j = sum_h F^(kRow (7 - h)) word_hj), the lane merge over the columns,
-// the lane tree over the lanes, and a per-wave shift F^(kSub (7 - w) + 4).
+// a per-lane shift matrix over the lanes, and a per-wave shift F^(kSub (7 - w)).
 
 // Lane merge of the four column streams: F^12 w0 ^ F^8 w1 ^ F^4 w2 ^ w3.
 __device__ __forceinline__ uint32_t lane_merge(uint32_t v0, uint32_t v1, uint32_t v2,
@@ -290,36 +293,42 @@ __device__ __forceinline__ uint32_t lane_merge(uint32_t v0, uint32_t v1, uint32_
   return tab4x(kLdsF12, v0, tab4x(kLdsF8, v1, tab4x(kLdsF4, v2, v3)));
 }
 
-// Lane tree: sum over lanes of F^(16 (63 - l)) u_l, valid in lane 63.  A
-// Hillis-Steele pass over DPP row shifts and row broadcasts: at level s, the
-// value received from s lanes below covers bytes that precede the receiver's
-// own s lanes, so it is shifted by F^(16 s) before the XOR (a lane with no
-// source receives 0, and F(0) = 0).
-// Levels 0..3 (within rows of 16 lanes) and 4..5 (across rows) may run
-// apart; lane_tree is both.
-__device__ __forceinline__ uint32_t lane_tree_rows(uint32_t u) {
-  u = tab4x(kLdsTree + 0 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x111, 0xF, 0xF, false), u);
-  u = tab4x(kLdsTree + 1 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x112, 0xF, 0xF, false), u);
-  u = tab4x(kLdsTree + 2 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x114, 0xF, 0xF, false), u);
-  u = tab4x(kLdsTree + 3 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x118, 0xF, 0xF, false), u);
-  return u;
+// Lane shift: lane l's merged value covers bytes that lie 16 (63 - l) + 4
+// bytes before the end of its wave's share (see lane_value), so it enters the
+// wave's value shifted by F^(16 (63 - l) + 4): a GF(2) matrix of its own,
+// applied from its 32 columns in LDS (eight 16-byte reads issued together;
+// columns 4q..4q+3 of lane l at kLdsLaneMat + 1024 q + 16 l).
+// lane_fold XORs the shifted values of the 64 lanes: the wave's contribution,
+// the common F^4 included, as a uniform value.
+__device__ __forceinline__ uint32_t lane_shift(uint32_t u) {
+  const uint4 *m = reinterpret_cast<const uint4 *>(lds_at(kLdsLaneMat + (threadIdx.x & 63u) * 16u));
+  uint4 c[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) c[i] = m[64 * i];
+  uint32_t r = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    // (column & -bit) ^ r, one three-input logic op per column
+    r = __builtin_amdgcn_bitop3_b32(c[i].x, (uint32_t)__builtin_amdgcn_sbfe((int)u, 4 * i, 1), r, 0x6A);
+    r = __builtin_amdgcn_bitop3_b32(c[i].y, (uint32_t)__builtin_amdgcn_sbfe((int)u, 4 * i + 1, 1), r, 0x6A);
+    r = __builtin_amdgcn_bitop3_b32(c[i].z, (uint32_t)__builtin_amdgcn_sbfe((int)u, 4 * i + 2, 1), r, 0x6A);
+    r = __builtin_amdgcn_bitop3_b32(c[i].w, (uint32_t)__builtin_amdgcn_sbfe((int)u, 4 * i + 3, 1), r, 0x6A);
+  }
+  return r;
 }
-__device__ __forceinline__ uint32_t lane_tree_across(uint32_t u) {
-  u = tab4x(kLdsTree + 4 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x142, 0xA, 0xF, false), u);
-  u = tab4x(kLdsTree + 5 * 4096u,
-            (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u, 0x143, 0xC, 0xF, false), u);
-  return u;
+// XOR over the wave's lanes (DPP row shifts and broadcasts), as a uniform value.
+__device__ __forceinline__ uint32_t wave_xor(uint32_t v) {
+  v ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);
+  v ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);
+  v ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);
+  v ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);
+  v ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);
+  v ^= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);
+  return uniform(__builtin_amdgcn_readlane(v, 63));
 }
-__device__ __forceinline__ uint32_t lane_tree(uint32_t u) {
-  return lane_tree_across(lane_tree_rows(u));
-}
+__device__ __forceinline__ uint32_t lane_fold(uint32_t u) { return wave_xor(lane_shift(u)); }
 
-// The lane's merged value of the wave's 8 rows (before the lane tree).
+// The lane's merged value of the wave's 8 rows (before its lane shift).
 __device__ __forceinline__ uint32_t lane_value(const uint4 (&d)[kRows], const GLane &gl) {
   uint32_t v0 = d[0].x, v1 = d[0].y, v2 = d[0].z, v3 = d[0].w;
 #pragma unroll
@@ -375,7 +384,7 @@ __device__ __forceinline__ uint32_t *chk_u(uint32_t b) {
 
 // Chunk CRCs: the eight data waves take chunk i's lane values while chunk
 // i+1 loads; the ninth wave folds chunk i-1's values into its CRC (the
-// Horner step over waves, the lane tree, the common F^4).
+// Horner step over waves, then the lane shifts and their XOR).
 __global__ __launch_bounds__(kThreads + 64) void k_checksum(
     const uint8_t *__restrict__ data, ChunkGeom g,
     uint32_t *__restrict__ crc_out) {
@@ -409,8 +418,7 @@ __global__ __launch_bounds__(kThreads + 64) void k_checksum(
       uint32_t acc = u[l.lane];
 #pragma unroll
       for (int w = 1; w < kWaves; ++w) acc = tab4x(kLdsWaveStep, acc, u[w * 64 + l.lane]);
-      const uint32_t q = uniform(__builtin_amdgcn_readlane(lane_tree(acc), 63));
-      const uint32_t crc = finish_crc(tab4(kLdsF4, q), chunk_len(g, c), g, T);
+      const uint32_t crc = finish_crc(lane_fold(acc), chunk_len(g, c), g, T);
       if (l.lane == 0) crc_out[c] = crc;
     }
     __syncthreads();
@@ -658,12 +666,16 @@ struct EncShared {
   alignas(16) uint32_t H[256];  // histogram
 };
 static_assert(sizeof(EncShared) <= kLdsMiscBytes, "encoder scratch fits");
-constexpr uint32_t kLdsHistE = kLdsLow;   // 256 bins x 32 copies of u16 (16 KiB)
+constexpr uint32_t kLdsHistE = kLdsLow;   // 256 bins x 32 copies of 2 x u16 (32 KiB)
 constexpr uint32_t kLdsStage = kLdsBase;  // record body staging
 // codes + escape index + escapes of a chosen packed record: the plan only
 // packs when the record is smaller than RAW, so they stay below half a chunk
 constexpr uint32_t kLdsStageBytes = kChunk / 2;
-constexpr uint32_t kLdsEncode = kLdsStage + kLdsStageBytes;
+// 256 x 8 bytes: for an 8-bit set of escaped words, the v_perm selectors
+// that gather their exponent bytes, in word order, from the row's eight
+// exponent bytes (0x0C, a zero byte, past the last one)
+constexpr uint32_t kLdsEscLut = kLdsStage + kLdsStageBytes;
+constexpr uint32_t kLdsEncode = kLdsEscLut + 256 * 8;
 static_assert(kLdsEncode <= 163840, "encoder LDS fits one CU");
 
 __device__ __forceinline__ EncShared &enc_shared() {
@@ -807,13 +819,12 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
     for (int h = 0; h < kRows; ++h) {
       const uint32_t w0 = (l.off0 + h * kRow) >> 1;
       const uint4 x = d[h];
-      const uint32_t lo0 = __builtin_amdgcn_perm(x.y, x.x, 0x06040200u);
-      const uint32_t hi0 = __builtin_amdgcn_perm(x.y, x.x, 0x07050301u);
-      const uint32_t lo1 = __builtin_amdgcn_perm(x.w, x.z, 0x06040200u);
-      const uint32_t hi1 = __builtin_amdgcn_perm(x.w, x.z, 0x07050301u);
-      // e = (high byte << 1 | low byte >> 7) & 255, four words at a time
-      uint2 e = make_uint2(((hi0 << 1) & 0xFEFEFEFEu) | ((lo0 >> 7) & 0x01010101u),
-                           ((hi1 << 1) & 0xFEFEFEFEu) | ((lo1 >> 7) & 0x01010101u));
+      // a dword rotated left by one bit holds its low word's exponent in
+      // byte 1 and its high word's in byte 3
+      const uint32_t r0 = __builtin_amdgcn_alignbit(x.x, x.x, 31), r1 = __builtin_amdgcn_alignbit(x.y, x.y, 31);
+      const uint32_t r2 = __builtin_amdgcn_alignbit(x.z, x.z, 31), r3 = __builtin_amdgcn_alignbit(x.w, x.w, 31);
+      uint2 e = make_uint2(__builtin_amdgcn_perm(r1, r0, 0x07050301u),
+                           __builtin_amdgcn_perm(r3, r2, 0x07050301u));
       if (FULL || w0 < n_words) *reinterpret_cast<uint2 *>(stage + w0) = e;
       lane_r[h] = 0;
     }
@@ -898,33 +909,27 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
 
 // A data wave's share of a chunk's exponent histogram in the low LDS
 // region: all 32768 words, the words past a short chunk loaded as zero (the
-// reduce takes their count off bin 0).  32 copies of 16-bit counters, copy =
-// lane mod 32, so the 32 lanes an LDS cycle serves never touch the same bank
-// (nor the same counter); bins 2m and 2m + 1 are the halves of dword
-// m * 32 + copy.  A copy counts at most 16 lanes x 64 words.
-// 1 + b * 0xFFFF (b = 0 or 1) in one instruction: the increment of the low
-// or the high 16-bit counter of a dword.
-__device__ __forceinline__ uint32_t half_inc(uint32_t b) {
-  uint32_t r;
-  asm("v_mad_u32_u24 %0, %1, %2, 1" : "=v"(r) : "v"(b), "s"(0xFFFFu));
-  return r;
-}
-
+// reduce takes their count off bin 0).  Bin e is 32 dwords at e * 128, one
+// per copy (copy = lane mod 32, so the 32 lanes an LDS cycle serves never
+// touch the same bank nor the same counter); the low 16 bits of a dword count
+// the low words of the lanes' dwords, the high 16 bits their high words.  The
+// low word's exponent sits at bits 7..14 already, so its counter's address is
+// one three-input logic op, (x & 0x7F80) | copy4, and both increments are
+// constants.  A counter counts at most 16 lanes x 32 words.
 __device__ __forceinline__ void hist_add(const uint4 (&d)[kRows], uint32_t copy4) {
-  static_assert(kLdsHistE == 0, "bin pair address = (e >> 1 << 7) | copy4");
+  static_assert(kLdsHistE == 0, "bin address = e << 7 | copy4");
+  uint32_t one = 1u, one_hi = 0x10000u;
+  asm volatile("" : "+v"(one), "+v"(one_hi));  // kept in registers across the loop
 #pragma unroll
   for (int h = 0; h < kRows; ++h) {
     const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      // (v & 0x3F80) | copy4 as one three-input logic op (table 0xEA); the
-      // exponent's low bit picks the counter half
+      atomicAdd(reinterpret_cast<uint32_t *>(lds_at(__builtin_amdgcn_bitop3_b32(x[j], 0x7F80u, copy4, 0xEA))),
+                one);
       atomicAdd(reinterpret_cast<uint32_t *>(
-                    lds_at(__builtin_amdgcn_bitop3_b32(x[j] >> 1, 0x3F80u, copy4, 0xEA))),
-                half_inc(__builtin_amdgcn_ubfe(x[j], 7, 1)));
-      atomicAdd(reinterpret_cast<uint32_t *>(
-                    lds_at(__builtin_amdgcn_bitop3_b32(x[j] >> 17, 0x3F80u, copy4, 0xEA))),
-                half_inc(__builtin_amdgcn_ubfe(x[j], 23, 1)));
+                    lds_at(__builtin_amdgcn_bitop3_b32(x[j] >> 16, 0x7F80u, copy4, 0xEA))),
+                one_hi);
     }
   }
 }
@@ -1017,7 +1022,13 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   uint32_t *hist = reinterpret_cast<uint32_t *>(lds_at(kLdsHistE));
   {
     uint4 *h4 = reinterpret_cast<uint4 *>(hist);
-    for (uint32_t i = threadIdx.x; i < 1024u; i += kEncThreads) h4[i] = make_uint4(0, 0, 0, 0);
+    for (uint32_t i = threadIdx.x; i < 2048u; i += kEncThreads) h4[i] = make_uint4(0, 0, 0, 0);
+    if (threadIdx.x < 256u) {
+      uint32_t f = threadIdx.x, sel[2] = {0x0C0C0C0Cu, 0x0C0C0C0Cu};
+      for (uint32_t j = 0; f; ++j, f &= f - 1u)
+        sel[j >> 2] = (sel[j >> 2] & ~(0xFFu << (8 * (j & 3)))) | ((uint32_t)__builtin_ctz(f) << (8 * (j & 3)));
+      *reinterpret_cast<uint2 *>(lds_at(kLdsEscLut + 8 * threadIdx.x)) = make_uint2(sel[0], sel[1]);
+    }
   }
   if (threadIdx.x == (uint32_t)kThreads) {
     sh.first = atomicAdd(&ctl->ticket, 1u);
@@ -1115,18 +1126,17 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         if (l.lane == 0) sh.ticket[it & 1] = ticket;
       }
     } else if (dirty) {
-      // reduce the copies: wave w sums bins 32w..32w+31 (its own 2 KiB of
-      // them); four lanes share a bin pair, eight copies each, the packed
-      // halves adding without carry (each total is at most 32768)
-      const uint32_t pair = l.wave * 16u + (l.lane >> 2), q = l.lane & 3u;
-      uint32_t s = 0;
-#pragma unroll
-      for (int cc = 0; cc < 8; ++cc) s += hist[pair * 32u + q * 8u + ((cc + (l.lane >> 2)) & 7u)];
+      // reduce the copies: wave w sums bins 32w..32w+31 (its own 4 KiB of
+      // them); two lanes share a bin, 16 copies each (four 16-byte reads),
+      // the packed halves adding without carry (each half at most 16384)
+      const uint32_t bin = l.wave * 32u + (l.lane >> 1);
+      const uint4 *src = reinterpret_cast<const uint4 *>(hist + bin * 32u + (l.lane & 1u) * 16u);
+      const uint4 q0 = src[0], q1 = src[1], q2 = src[2], q3 = src[3];
+      uint32_t s = (q0.x + q0.y + q0.z + q0.w) + (q1.x + q1.y + q1.z + q1.w) +
+                   (q2.x + q2.y + q2.z + q2.w) + (q3.x + q3.y + q3.z + q3.w);
       s += (uint32_t)__shfl_xor((int)s, 1, 64);
-      s += (uint32_t)__shfl_xor((int)s, 2, 64);
-      if (q == 0)
-        *reinterpret_cast<uint2 *>(&sh.H[2 * pair]) =
-            make_uint2((s & 0xFFFFu) - (pair == 0 ? kChunk / 2 - n_words : 0u), s >> 16);
+      if ((l.lane & 1u) == 0)
+        sh.H[bin] = (s & 0xFFFFu) + (s >> 16) - (bin == 0 ? kChunk / 2 - n_words : 0u);
     }
     __syncthreads();  // B2: H complete
 
@@ -1139,7 +1149,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         crc_acc = sh.u[l.lane];
 #pragma unroll
         for (int w = 1; w < kWaves; ++w) crc_acc = tab4x(kLdsWaveStep, crc_acc, sh.u[w * 64 + l.lane]);
-        crc_acc = lane_tree_rows(crc_acc);
+        crc_acc = lane_shift(crc_acc);
       }
     } else {
       if (pend && p_dirty) {
@@ -1168,12 +1178,12 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         // score the plan candidates, one per wave: waves 0..6 place a window
         // of 2^k - 1 exponents (k = wave + 1) where it covers the most words
         // (lowest base on ties), wave 7 prices RAW and a constant exponent;
-        // each wave's prefix scratch lives in its own, already reduced, 2 KiB
+        // each wave's prefix scratch lives in its own, already reduced, 4 KiB
         // of the histogram copies, which it clears afterwards
         const uint32_t lane = l.lane, b0 = lane * 4u;
         const uint4 hv = *reinterpret_cast<const uint4 *>(&sh.H[b0]);
         const uint64_t n = n_words;
-        uint32_t *slice = hist + l.wave * 512u;
+        uint32_t *slice = hist + l.wave * 1024u;
         if (l.wave < 7u) {
           const uint32_t t4 = hv.x + hv.y + hv.z + hv.w;
           const uint32_t ex = wave_incl_scan(t4) - t4;
@@ -1206,10 +1216,12 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
           }
         }
         uint4 *s4 = reinterpret_cast<uint4 *>(slice);
-        for (uint32_t i = l.lane; i < 128u; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (uint32_t i = 0; i < 4u; ++i) s4[l.lane + 64u * i] = make_uint4(0, 0, 0, 0);
       } else if (HAS_PREV && cur) {  // a clean chunk's histogram, unused
-        uint4 *s4 = reinterpret_cast<uint4 *>(hist + l.wave * 512u);
-        for (uint32_t i = l.lane; i < 128u; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
+        uint4 *s4 = reinterpret_cast<uint4 *>(hist + l.wave * 1024u);
+#pragma unroll
+        for (uint32_t i = 0; i < 4u; ++i) s4[l.lane + 64u * i] = make_uint4(0, 0, 0, 0);
       }
     }
     __syncthreads();  // B3: candidates scored, X_{i-1}'s staging read
@@ -1251,10 +1263,8 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         status_store(&status[item], agg | kFlagAgg);
       }
       if (cur && need_crc) {
-        // second step: the rest of the lane tree, then the F^4 common to
-        // every word (see lane_value)
-        const uint32_t q = uniform(__builtin_amdgcn_readlane(lane_tree_across(crc_acc), 63));
-        crc = bad_index ? 0u : finish_crc(tab4(kLdsF4, q), len, g, T);
+        // second step: the XOR of the shifted lane values (F^4 included)
+        crc = bad_index ? 0u : finish_crc(wave_xor(crc_acc), len, g, T);
       }
     } else {
       // ---- data: X_{i+1}'s histogram (its loads were issued an iteration
@@ -1284,6 +1294,10 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         }
 #undef WM_PACK
         if (l.lane == 0) sh.esc_w[l.wave] = wave_esc;
+        // the escape section (with its padding) starts as zeros: phase 5
+        // ORs the escaped exponents in
+        for (uint32_t i = s_esc + 16u * threadIdx.x; i < s_end; i += 16u * kThreads)
+          *reinterpret_cast<uint4 *>(stage + i) = make_uint4(0, 0, 0, 0);
       }
 #pragma unroll
       for (int h = 0; h < kRows; ++h) smp[h] = sm_bytes(d[h]);
@@ -1324,31 +1338,38 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         if (l.lane < (uint32_t)kRows && blk * (kRow / 2) < n_words)
           *reinterpret_cast<uint16_t *>(stage + s_idx + 2 * blk) = (uint16_t)(wave_base + row_base);
       }
+      // the lane's escaped exponents of each row, in word order, at byte
+      // `at` of the zeroed escape section: gathered by one table lookup and
+      // two byte permutes, shifted to at's byte within its dword and ORed in
+      // by the lanes that have any
 #pragma unroll
       for (int h = 0; h < kRows; ++h) {
-        uint32_t flags = (escm[h >> 2] >> (8 * (h & 3))) & 255u;
-        if (flags) {  // the lane's escaped exponents, in word order
-          // exponent bytes of the row's eight words: e = high byte << 1 |
-          // low byte >> 7, four words per register
-          const uint4 x = d[h];
-          const uint32_t lo0 = __builtin_amdgcn_perm(x.y, x.x, 0x06040200u);
-          const uint32_t hi0 = __builtin_amdgcn_perm(x.y, x.x, 0x07050301u);
-          const uint32_t lo1 = __builtin_amdgcn_perm(x.w, x.z, 0x06040200u);
-          const uint32_t hi1 = __builtin_amdgcn_perm(x.w, x.z, 0x07050301u);
-          const uint32_t ex = ((hi0 << 1) & 0xFEFEFEFEu) | ((lo0 >> 7) & 0x01010101u);
-          const uint32_t ey = ((hi1 << 1) & 0xFEFEFEFEu) | ((lo1 >> 7) & 0x01010101u);
-          uint32_t at = s_esc + wave_base + lane_r[h];
-          do {  // byte u of (ey:ex) is word u's exponent
-            const uint32_t u = __builtin_ctz(flags);
-            flags &= flags - 1u;
-            stage[at++] = (uint8_t)__builtin_amdgcn_perm(ey, ex, u);
-          } while (flags);
+        const uint32_t flags = (escm[h >> 2] >> (8 * (h & 3))) & 255u;
+        const uint2 sel = *reinterpret_cast<const uint2 *>(lds_at(kLdsEscLut + 8u * flags));
+        // each dword rotated left by one bit puts the low word's exponent in
+        // byte 1 and the high word's in byte 3
+        const uint4 x = d[h];
+        const uint32_t r0 = __builtin_amdgcn_alignbit(x.x, x.x, 31), r1 = __builtin_amdgcn_alignbit(x.y, x.y, 31);
+        const uint32_t r2 = __builtin_amdgcn_alignbit(x.z, x.z, 31), r3 = __builtin_amdgcn_alignbit(x.w, x.w, 31);
+        const uint32_t ex = __builtin_amdgcn_perm(r1, r0, 0x07050301u);  // words 0..3
+        const uint32_t ey = __builtin_amdgcn_perm(r3, r2, 0x07050301u);  // words 4..7
+        const uint64_t cb = (uint64_t)__builtin_amdgcn_perm(ey, ex, sel.x) |
+                            ((uint64_t)__builtin_amdgcn_perm(ey, ex, sel.y) << 32);
+        const uint32_t at = s_esc + wave_base + lane_r[h];
+        const uint32_t shb = (at & 3u) * 8u;
+        const uint64_t lo = cb << shb;
+        const uint32_t hi = (uint32_t)(((cb >> 32) << shb) >> 32);
+        uint32_t *w = reinterpret_cast<uint32_t *>(stage + (at & ~3u));
+        const uint32_t span = (at & 3u) + __popc(flags);  // bytes from w to the last escape
+        if (flags) {
+          atomicOr(w, (uint32_t)lo);
+          if (span > 4u) atomicOr(w + 1, (uint32_t)(lo >> 32));
+          if (span > 8u) atomicOr(w + 2, hi);
         }
       }
-      if (threadIdx.x < 16u) {  // zero padding of index and escapes
+      if (threadIdx.x < 16u) {  // zero padding of the index
         const uint32_t t = threadIdx.x;
         if (2 * n_blocks + t < s_esc - s_idx) stage[s_idx + 2 * n_blocks + t] = 0;
-        if (n_esc + t < s_end - s_esc) stage[s_esc + n_esc + t] = 0;
       }
     }
 
@@ -2038,15 +2059,14 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
 #pragma unroll
             for (int w = 0; w < kWaves; ++w) bad |= sh.bad[(i - 1) & 1][w];
             // the record's CRC from the data waves' lane values: lane l folds
-            // lane l of the eight waves (F^kSub per wave), then the lane tree,
-            // then the F^4 common to every word (see lane_value)
+            // lane l of the eight waves (F^kSub per wave), then the lane
+            // shifts (F^4 included) and their XOR (see lane_value)
             const uint32_t *u = dec_u((i - 1) & 1);
             uint32_t acc = u[l.lane];
 #pragma unroll
             for (int w = 1; w < kWaves; ++w) acc = tab4x(kLdsWaveStep, acc, u[w * 64 + l.lane]);
-            const uint32_t q = uniform(__builtin_amdgcn_readlane(lane_tree(acc), 63));
             const uint32_t c = uniform(M.c);
-            const uint32_t crc = finish_crc(tab4(kLdsF4, q), chunk_len(g, c), g, T);
+            const uint32_t crc = finish_crc(lane_fold(acc), chunk_len(g, c), g, T);
             st = bad ? 4u : (crc != uniform(M.src_crc) ? 8u : 0u);
           }
           if (l.lane == 0) {
@@ -2902,8 +2922,7 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
           uint32_t acc2 = U[l.lane];
 #pragma unroll
           for (int w = 1; w < kWaves; ++w) acc2 = tab4x(kLdsWaveStep, acc2, U[w * 64 + l.lane]);
-          const uint32_t q = uniform(__builtin_amdgcn_readlane(lane_tree(acc2), 63));
-          const uint32_t crc = finish_crc(tab4(kLdsF4, q), uniform(M.len), g, T);
+          const uint32_t crc = finish_crc(lane_fold(acc2), uniform(M.len), g, T);
           const bool bd = uniform(M.bad) != 0 || (mode == 2 && k && uniform(M.hufbad) != 0);
           stf = bd ? 4u : (crc != uniform(M.src) ? 8u : 0u);
         }

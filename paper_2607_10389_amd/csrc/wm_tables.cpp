@@ -98,8 +98,10 @@ void build_crc_tables(uint32_t poly, CrcTables *t) {
   byte_tables(byte_shift(poly, 4), t->f4);
   byte_tables(byte_shift(poly, 8), t->f8);
   byte_tables(byte_shift(poly, 12), t->f12);
-  for (int l = 0; l < kTree; ++l)
-    byte_tables(byte_shift(poly, 16 << l), t->tree[l]);
+  for (int l = 0; l < 64; ++l) {
+    const Mat m = byte_shift(poly, 16 * (63 - l) + 4);
+    for (int i = 0; i < 32; ++i) t->lane_mat[i / 4][l][i % 4] = m.c[i];
+  }
   byte_tables(byte_shift(poly, kSub), t->wave_step);
   Mat one = byte_shift(poly, 1);
   for (uint32_t b = 0; b < 256; ++b) t->byte1[b] = apply(one, b);
