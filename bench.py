@@ -50,6 +50,8 @@ def parse():
                     help="skip the pipelined receive measurement")
     ap.add_argument("--no-precopy", action="store_true",
                     help="skip the iterative pre-copy measurement")
+    ap.add_argument("--no-long", action="store_true",
+                    help="skip the 4.3 GB long-context ship and its abort path")
     ap.add_argument("--crc", type=int, default=0, help="0 zlib CRC-32, 1 CRC-32C")
     ap.add_argument("--counter-pass", action="store_true",
                     help="one full-ship encode and decode plus a 1 GiB device copy, "
@@ -138,6 +140,26 @@ def timed_events(torch, fn, n, warmup=3):
     return times[n // 2] if n % 2 else 0.5 * (times[n // 2 - 1] + times[n // 2])
 
 
+def cpu_threads() -> int:
+    """Threads the CPU oracle runs with: every CPU this process may run on
+    (its affinity mask), capped by OMP_NUM_THREADS when that is set (the
+    share of the host a GPU job is given)."""
+    n = len(os.sched_getaffinity(0))
+    cap = os.environ.get("OMP_NUM_THREADS", "")
+    return min(n, int(cap)) if cap.isdigit() and int(cap) > 0 else n
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(host_state, nbytes_chunk=65536, target_s=12.0):
     """The oracle (as it stands) on the first m chunks of the cache, m sized
     for about target_s seconds of work; round trip = encode (per-chunk CRCs,
@@ -145,7 +167,7 @@ def cpu_baseline(host_state, nbytes_chunk=65536, target_s=12.0):
     import numpy as np
 
     import oracle
-    threads = min(16, len(os.sched_getaffinity(0)))
+    threads = cpu_threads()
 
     def run(m):
         sample = host_state[: m * nbytes_chunk]
@@ -165,57 +187,72 @@ def cpu_baseline(host_state, nbytes_chunk=65536, target_s=12.0):
     m = int(min(n_total, max(64, m * target_s / max(dt, 1e-3))))
     dt = run(m)
     gbs = m * nbytes_chunk / dt / 1e9
-    cpu = "unknown"
-    try:
-        with open("/proc/cpuinfo") as f:
-            for line in f:
-                if line.startswith("model name"):
-                    cpu = line.split(":", 1)[1].strip()
-                    break
-    except OSError:
-        pass
+    cpu = cpu_model()
     return {"value": round(gbs, 4), "unit": "GB/s", "cores": threads,
             "kind": "oracle",
             "sample": f"first {m} of {n_total} 64 KiB chunks of the production "
                       f"cache ({m * nbytes_chunk} B); encode + decode_verify + "
                       f"commit, {dt:.1f} s",
-            "cpu_model": cpu}
+            "cpu_model": cpu,
+            "threads_rule": "len(os.sched_getaffinity(0)), capped by OMP_NUM_THREADS if set",
+            "affinity_cpus": len(os.sched_getaffinity(0))}
 
 
-def cpu_oracle_detail(host_prev, host_cur, tiny_prev, tiny_cur, threads):
+def cpu_oracle_detail(host_prev, host_cur, tiny_prev, tiny_cur, host_long, threads):
     """The oracle per operation, in GB/s of state bytes: checksum, diff,
-    encode (full ship) and decode + verify, on the tiny cache with one
-    thread and with `threads`, and on the production-size cache with
-    `threads` only (one thread would take minutes there)."""
+    encode (full ship) and decode + verify.  Each rate is the median of at
+    least three timed runs (with their minimum and maximum).  Tiny cache:
+    whole, one thread and `threads`.  Production cache: a labelled sample of
+    its first chunks with one thread and with `threads` (the whole cache
+    takes minutes per operation at one thread).  Long-context cache: a
+    labelled sample with `threads` only."""
+    import statistics
+
     import oracle
     CH = 65536
 
-    def rate(fn, nbytes, min_s):
-        reps, t = 0, 0.0
-        t0 = time.perf_counter()
-        while True:
+    def rate(fn, nbytes, min_s=0.3, reps_min=3):
+        ts = []
+        t_all = time.perf_counter()
+        while len(ts) < reps_min or time.perf_counter() - t_all < min_s:
+            t0 = time.perf_counter()
             fn()
-            reps += 1
-            t = time.perf_counter() - t0
-            if t >= min_s:
-                return round(nbytes * reps / t / 1e9, 4)
+            ts.append(time.perf_counter() - t0)
+        return {"median": round(nbytes / statistics.median(ts) / 1e9, 4),
+                "min": round(nbytes / max(ts) / 1e9, 4),
+                "max": round(nbytes / min(ts) / 1e9, 4), "runs": len(ts)}
 
-    def ops(prev, cur, T, min_s):
+    def ops(prev, cur, T, with_diff=True):
         payload = oracle.encode(0, cur, CH, None, T)
-        return {
-            "checksum": rate(lambda: oracle.checksum_chunks(0, cur, CH, T), cur.size, min_s),
-            "diff": rate(lambda: oracle.diff_dirty(cur, prev, CH, T), cur.size, min_s),
-            "encode": rate(lambda: oracle.encode(0, cur, CH, None, T), cur.size, min_s),
+        out = {
+            "checksum": rate(lambda: oracle.checksum_chunks(0, cur, CH, T), cur.size),
+            "encode": rate(lambda: oracle.encode(0, cur, CH, None, T), cur.size),
             "decode_verify": rate(lambda: oracle.decode_verify(0, payload, cur.size, CH,
-                                                               None, T), cur.size, min_s),
+                                                               None, T), cur.size),
         }
+        if with_diff:
+            out["diff"] = rate(lambda: oracle.diff_dirty(cur, prev, CH, T), cur.size)
+        return out
 
+    prod_n = 1024  # chunks of the sample: 64 MiB
+    sp, sc = host_prev[: prod_n * CH], host_cur[: prod_n * CH]
+    long_n = 1024
+    sl = host_long[: long_n * CH]
     return {
-        "unit": "GB/s of state bytes",
+        "unit": "GB/s of state bytes (median of >= 3 runs; min and max)",
         "threads": threads,
-        "tiny_one_thread": ops(tiny_prev, tiny_cur, 1, 0.3),
-        "tiny_all_threads": ops(tiny_prev, tiny_cur, threads, 0.3),
-        "production_all_threads": ops(host_prev, host_cur, threads, 0.0),
+        "cpu_model": cpu_model(),
+        "tiny_one_thread": ops(tiny_prev, tiny_cur, 1),
+        "tiny_all_threads": ops(tiny_prev, tiny_cur, threads),
+        "production_sample": f"first {prod_n} of {host_cur.size // CH} 64 KiB chunks "
+                             f"({prod_n * CH} B) of the production cache and of its "
+                             "75%-dirty step",
+        "production_one_thread": ops(sp, sc, 1),
+        "production_all_threads": ops(sp, sc, threads),
+        "long_context_sample": f"first {long_n} of 65536 64 KiB chunks "
+                               f"({long_n * CH} B) of the long-context cache (Student-t(3), "
+                               "10% of chunks uniform random bits)",
+        "long_context_all_threads": ops(None, sl, threads, with_diff=False),
     }
 
 
@@ -233,11 +270,20 @@ def fanin_run(torch, wm_inputs, crc, dev, reps=5):
     # sessions' streams do not wait for
     torch.cuda.synchronize()
 
-    def run():
-        for m, s, st in zip(movers, states, streams):
+    # each session's own time: a pair of events on its stream around its
+    # encode and decode
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in states]
+
+    def run(timed=False):
+        for i, (m, s, st) in enumerate(zip(movers, states, streams)):
             with torch.cuda.stream(st):
+                if timed:
+                    ev[i][0].record(st)
                 m.encode_step(s, None)
                 m.decode()
+                if timed:
+                    ev[i][1].record(st)
 
     run()
     torch.cuda.synchronize()
@@ -250,6 +296,13 @@ def fanin_run(torch, wm_inputs, crc, dev, reps=5):
         run()
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / reps
+    per_session_ms = [[] for _ in states]
+    for _ in range(reps):
+        run(timed=True)
+        torch.cuda.synchronize()
+        for i, (e0, e1) in enumerate(ev):
+            per_session_ms[i].append(e0.elapsed_time(e1))
+    sess_ms = [sorted(x)[len(x) // 2] for x in per_session_ms]
 
     def run_serial():  # the same work, one session after another on one stream
         for m, s in zip(movers, states):
@@ -270,10 +323,14 @@ def fanin_run(torch, wm_inputs, crc, dev, reps=5):
     for m, cs in zip(movers, parts):
         m.stream = cs.stream
 
-    def run_parts():
-        for m, s in zip(movers, states):
+    def run_parts(timed=False):
+        for i, (m, s) in enumerate(zip(movers, states)):
+            if timed:
+                ev[i][0].record(m.stream)
             m.encode_step(s, None)
             m.decode()
+            if timed:
+                ev[i][1].record(m.stream)
 
     run_parts()
     torch.cuda.synchronize()
@@ -286,20 +343,94 @@ def fanin_run(torch, wm_inputs, crc, dev, reps=5):
         run_parts()
     torch.cuda.synchronize()
     parted = (time.perf_counter() - t0) / reps
+    part_ms = [[] for _ in states]
+    for _ in range(reps):
+        run_parts(timed=True)
+        torch.cuda.synchronize()
+        for i, (e0, e1) in enumerate(ev):
+            part_ms[i].append(e0.elapsed_time(e1))
+    part_sess_ms = [sorted(x)[len(x) // 2] for x in part_ms]
     for cs in parts:
         cs.close()
     each = states[0].numel() * 2
     return {
         "cu_partitioned_ms": round(parted * 1e3, 3),
         "cu_partitioned_kv_GBps": round(8 * each / parted / 1e9, 1),
+        "cu_partitioned_per_session_ms": [round(t, 3) for t in part_sess_ms],
+        "cu_partitioned_per_session_kv_GBps": [round(each / (t * 1e-3) / 1e9, 1)
+                                               for t in part_sess_ms],
         "workload": "8 sessions x [24,2,8,4096,128] bf16 (402,653,184 B each) on 8 streams: "
                     "full checksum + encode + decode + verify",
         "ms": round(wall * 1e3, 3),
         "aggregate_kv_GBps": round(8 * each / wall / 1e9, 1),
-        "per_session_kv_GBps": round(each / wall / 1e9, 1),
+        "per_session_ms": [round(t, 3) for t in sess_ms],
+        "per_session_kv_GBps": [round(each / (t * 1e-3) / 1e9, 1) for t in sess_ms],
+        "per_session_note": "each session's S_i / t_i, t_i between events on its own "
+                            "stream around its encode and decode (median of the runs)",
         "one_stream_back_to_back_ms": round(serial * 1e3, 3),
         "one_stream_back_to_back_kv_GBps": round(8 * each / serial / 1e9, 1),
     }
+
+
+def long_context_run(torch, wm_inputs, crc, dev, one):
+    """The long-context cache ([32,2,8,32768,128] bf16, 4,294,967,296 B,
+    Student-t(3), 10% of chunks uniform random bits): full ship (encode,
+    decode + verify), then the abort path: one payload bit flipped (position
+    uniform over the payload's bits, seed 6), decode + verify + scatter
+    commit, which must return WM_VERIFY_FAILED with live untouched.  Also
+    returns the first 1,024 chunks in host memory for the CPU oracle."""
+    import numpy as np
+
+    from paper_2607_10389_amd import Mover, WM_OK, WM_VERIFY_FAILED
+
+    state = wm_inputs.make_cache(wm_inputs.LONG, dev)
+    nbytes = state.numel() * 2
+    m = Mover(nbytes, crc, dev)
+    live = torch.zeros(nbytes, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    m.encode_step(state, None)
+    m.decode()
+    if m.commit(None, scatter=False) != WM_OK or \
+            not torch.equal(m.staging[:nbytes], state.view(-1).view(torch.uint8)):
+        raise RuntimeError("long-context ship did not verify")
+    pb = int(m.payload_bytes.item())
+    src = one("source", lambda: m.encode_step(state, None), nbytes + pb)
+    dst = one("destination", lambda: m.decode(), pb + nbytes)
+    # modes of the records (byte 0 of each record header), read from the table
+    n_rec = nbytes // 65536
+    table = m.payload[pb - 16 * n_rec: pb].cpu().numpy().view(np.uint64).reshape(-1, 2)
+    offs = torch.from_numpy(table[:, 1].astype(np.int64)).to(dev)
+    n_raw = int((m.payload[offs] == 0).sum().item())
+    bit = int(np.random.default_rng(6).integers(0, pb * 8))
+    m.payload[bit // 8] ^= 1 << (bit % 8)
+
+    def abort():
+        m.decode()
+        if m.commit(live, scatter=True) != WM_VERIFY_FAILED:
+            raise RuntimeError("a flipped payload bit was not rejected")
+
+    t_abort = timed_events(torch, abort, 5, warmup=1)
+    verdict = int(m.verdict.item())
+    untouched = not bool(live.any())
+    m.payload[bit // 8] ^= 1 << (bit % 8)
+    if not untouched or verdict == 0:
+        raise RuntimeError("the abort path installed something")
+    host_sample = state.view(-1).view(torch.uint8)[: 1024 * 65536].cpu().numpy()
+    del state, m, live
+    torch.cuda.synchronize()
+    return {
+        "workload": "long-context cache [32,2,8,32768,128] bf16 (4,294,967,296 B), "
+                    "Student-t(3), 10% of chunks uniform random 16-bit patterns",
+        "payload_bytes": pb, "compression_ratio": round(pb / nbytes, 5),
+        "raw_records": n_raw, "records": n_rec,
+        "source_wm_encode_step": src,
+        "destination_wm_decode_verify": dst,
+        "kv_GBps_round_trip": round(nbytes / ((src["ms"] + dst["ms"]) * 1e-3) / 1e9, 1),
+        "abort": {"flipped_bit": bit, "verdict": verdict, "live_untouched": untouched,
+                  "ms": round(t_abort, 4),
+                  "timed": "wm_decode_verify + wm_commit_or_abort (scatter) returning "
+                           "WM_VERIFY_FAILED; the commit waits for the stream"},
+    }, host_sample
 
 
 def codec_v2_run(torch, state, nbytes, crc, dev, one):
@@ -623,9 +754,20 @@ def main():
             "wm_commit_scatter": one("commit", lambda: mu.commit(live, scatter=True),
                                      2 * dirty_b),
         }
-        # what a plain streaming copy reaches on this device (read S + write S)
-        dst = torch.empty_like(cur)
-        out["copy_ceiling"] = one("copy", lambda: dst.copy_(cur), 2 * nbytes)
+        # what a streaming copy reaches on this device (read S + write S):
+        # the library's own copy kernel (a flatten of one leaf, the whole
+        # state: 64 KiB windows, 512 threads x 8 x 16 B in flight,
+        # non-temporal; the scatter install copies the same way), and
+        # torch's copy_
+        dst = torch.empty_like(cur).view(-1).view(torch.uint8)
+        one_leaf = _wm.LeafTable([cur])
+        ws1 = torch.empty(_wm.manifest_ws_bytes(1), dtype=torch.uint8, device=dev)
+        out["copy_ceiling"] = one("copy", lambda: _wm.flatten(one_leaf, dst, ws1), 2 * nbytes)
+        out["copy_ceiling"]["kernel"] = "k_manifest<gather>, one leaf of the whole state"
+        torch.cuda.synchronize()
+        if not torch.equal(dst, cur.view(-1).view(torch.uint8)):
+            raise RuntimeError("the one-leaf flatten did not copy the state")
+        out["copy_ceiling"]["torch_copy_"] = one("copy", lambda: dst.copy_(cur.view(-1).view(torch.uint8)), 2 * nbytes)
         del cur, live, ms, mu, dst
 
     if not args.no_manifest:
@@ -655,6 +797,10 @@ def main():
     if not args.no_v2:
         out["codec_v2"] = codec_v2_run(torch, state, nbytes, args.crc, dev, one)
 
+    host_long = None
+    if not args.no_long:
+        out["long_context"], host_long = long_context_run(torch, wm_inputs, args.crc, dev, one)
+
     if not args.no_fanin:
         out["fan_in"] = fanin_run(torch, wm_inputs, args.crc, dev)
 
@@ -675,9 +821,12 @@ def main():
         host_cur = cur.view(-1).view(torch.uint8).cpu().numpy()
         del cur
         tp, tc, _ = wm_inputs.tiny_step("cpu")
+        if host_long is None:
+            host_long = wm_inputs.make_cache(wm_inputs.LONG, dev).view(-1).view(
+                torch.uint8)[: 1024 * 65536].cpu().numpy()
         out["cpu_oracle_detail"] = cpu_oracle_detail(
             host, host_cur, wm_inputs.as_bytes(tp).numpy(), wm_inputs.as_bytes(tc).numpy(),
-            out["cpu_baseline"]["cores"])
+            host_long, out["cpu_baseline"]["cores"])
 
     print(json.dumps(out), flush=True)
 
