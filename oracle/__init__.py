@@ -20,7 +20,7 @@ SOURCES = [os.path.join(HERE, "wm_oracle.c")]
 CRC32_ZLIB = 0
 CRC32C = 1
 
-V_HEADER, V_TABLE, V_RECORD, V_DATA, V_STAGING = 1, 2, 4, 8, 16
+V_HEADER, V_TABLE, V_RECORD, V_DATA, V_STAGING, V_REVERIFY = 1, 2, 4, 8, 16, 32
 
 _lib = None
 
@@ -75,6 +75,9 @@ def lib():
         L.orc_commit.argtypes = [u8p, ctypes.c_uint64, ctypes.c_uint32, u8p,
                                  u8p, ctypes.c_uint32]
         L.orc_commit.restype = ctypes.c_int
+        L.orc_commit_reverify.argtypes = [ctypes.c_int, u8p, ctypes.c_uint64, ctypes.c_uint32,
+                                          u8p, u8p, ctypes.c_uint32]
+        L.orc_commit_reverify.restype = ctypes.c_uint32
         L.orc_encode_codec.argtypes = [ctypes.c_int, ctypes.c_int, u8p, ctypes.c_uint64,
                                        ctypes.c_uint32, u32p, ctypes.c_uint32, u8p,
                                        ctypes.c_uint64, ctypes.c_int]
@@ -223,6 +226,17 @@ def commit(live: np.ndarray, chunk: int, staging, payload, verdict: int) -> int:
     s, p = _bytes(staging), _bytes(payload)
     return int(lib().orc_commit(_p8(live), live.size, chunk, _p8(s), _p8(p),
                                 verdict))
+
+
+def commit_reverify(kind: int, live: np.ndarray, chunk: int, staging, payload,
+                    verdict: int) -> int:
+    """Re-verifying install into `live` (uint8 array): returns the verdict
+    (the given one if nonzero, else 0 = installed or V_REVERIFY = refused,
+    live untouched)."""
+    assert live.dtype == np.uint8 and live.flags.c_contiguous
+    s, p = _bytes(staging), _bytes(payload)
+    return int(lib().orc_commit_reverify(kind, _p8(live), live.size, chunk, _p8(s), _p8(p),
+                                         verdict))
 
 
 def _u64p(a: np.ndarray):

@@ -957,6 +957,37 @@ int orc_commit(uint8_t *live, uint64_t nbytes, uint32_t chunk_bytes,
   return 0;
 }
 
+/* Re-verifying install (Table 1: commit re-verifies, then swaps).  With a
+ * zero verdict, the staged records are checked again against their
+ * receipts, and the state the install would produce (live with every
+ * staged record in place) is checksummed whole and compared with the
+ * header's global CRC, the CRC of the source state.  Only if both hold is
+ * the install done.  Returns the verdict: the one given if nonzero, else 0
+ * or ORC_V_REVERIFY; live is untouched unless 0 is returned. */
+uint32_t orc_commit_reverify(int kind, uint8_t *live, uint64_t nbytes,
+                             uint32_t chunk_bytes, const uint8_t *staging,
+                             const uint8_t *payload, uint32_t verdict) {
+  if (verdict != 0) return verdict;
+  uint32_t n_rec = get_u32(payload + 24);
+  uint64_t table = get_u64(payload + 32) - 16 * (uint64_t)n_rec;
+  int bad = 0;
+  uint8_t *result = malloc(nbytes ? nbytes : 1);
+  if (!result) return ORC_V_REVERIFY;
+  memcpy(result, live, nbytes);
+  for (uint32_t r = 0; r < n_rec; r++) {
+    uint32_t c = get_u32(payload + table + 16 * (uint64_t)r);
+    uint32_t receipt = get_u32(payload + table + 16 * (uint64_t)r + 4);
+    uint32_t len = chunk_len(nbytes, chunk_bytes, c);
+    const uint8_t *src = staging + (uint64_t)r * chunk_bytes;
+    if (orc_crc(kind, src, len) != receipt) bad = 1;
+    memcpy(result + (uint64_t)c * chunk_bytes, src, len);
+  }
+  if (orc_crc(kind, result, nbytes) != get_u32(payload + 40)) bad = 1;
+  if (!bad) memcpy(live, result, nbytes);
+  free(result);
+  return bad ? ORC_V_REVERIFY : 0u;
+}
+
 /* ---- manifest flatten / rehydrate (§4 "Sufficiency", §5 "Implementation") */
 
 uint64_t orc_flat_layout(const uint64_t *bytes, uint32_t n, uint64_t *off) {

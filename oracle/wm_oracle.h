@@ -52,6 +52,8 @@ extern "C" {
 #define ORC_V_RECORD 4u   /* a record's structure is invalid */
 #define ORC_V_DATA 8u     /* a decoded chunk's CRC differs from its receipt */
 #define ORC_V_STAGING 16u /* receiver staging too small for the records */
+#define ORC_V_REVERIFY 32u /* re-verifying install: a staged record or the
+                              resulting state's global CRC disagrees */
 
 /* CRC by its definition: one bit at a time. */
 uint32_t orc_crc_bitwise(int kind, const uint8_t *p, uint64_t n);
@@ -127,6 +129,15 @@ uint32_t orc_decode_verify_codec(int kind, int codec, const uint8_t *payload,
 int orc_commit(uint8_t *live, uint64_t nbytes, uint32_t chunk_bytes,
                const uint8_t *staging, const uint8_t *payload,
                uint32_t verdict);
+
+/* Re-verifying install: with verdict 0, re-checks every staged record
+ * against its receipt and the CRC of the state the install would produce
+ * against the header's global CRC; installs only if both hold.  Returns
+ * the given verdict if nonzero, else 0 (installed) or ORC_V_REVERIFY (live
+ * untouched). */
+uint32_t orc_commit_reverify(int kind, uint8_t *live, uint64_t nbytes,
+                             uint32_t chunk_bytes, const uint8_t *staging,
+                             const uint8_t *payload, uint32_t verdict);
 
 /* Flat layout of a manifest of n leaves of bytes[i] bytes: writes each
  * leaf's offset into off (n entries) and returns the flat size. */

@@ -328,3 +328,54 @@ def test_hand_built_payload_with_escapes():
     assert got == want
     v, staging, _ = oracle.decode_verify(0, got, state.size, CH)
     assert v == 0 and np.array_equal(staging[: state.size], state)
+
+
+def test_reverifying_commit():
+    """The re-verifying install checks the state it would produce against
+    the source's global CRC: installed (bit-identical to the source) when
+    the destination holds the source's previous snapshot, refused with live
+    untouched when the destination's base differs in a chunk the payload
+    does not carry, or when a staged record changed after verification."""
+    rng = np.random.default_rng(9)
+    n = 6 * CH + 1000
+    prev = rng.integers(0, 256, n, dtype=np.uint8)
+    cur = prev.copy()
+    for c in (1, 4, 6):  # chunk 6 is the 1,000-byte tail
+        lo = c * CH
+        cur[lo:min(lo + CH, n)] = rng.integers(0, 256, min(CH, n - lo), dtype=np.uint8)
+    idx = oracle.diff_dirty(cur, prev, CH)
+    assert idx.tolist() == [1, 4, 6]
+    payload = oracle.encode(1, cur, CH, idx)
+    v, staging, _ = oracle.decode_verify(1, payload, n, CH, staging_cap=3 * CH)
+    assert v == 0
+    # the right base: installed, equal to the source
+    live = prev.copy()
+    assert oracle.commit_reverify(1, live, CH, staging, payload, v) == 0
+    assert np.array_equal(live, cur)
+    # a base that differs in a clean chunk: the plain commit would report
+    # success on a state that is not the source's; the re-verifying one refuses
+    live = prev.copy()
+    live[2 * CH + 7] ^= 1
+    before = live.copy()
+    assert oracle.commit_reverify(1, live, CH, staging, payload, v) == oracle.V_REVERIFY
+    assert np.array_equal(live, before)
+    plain = prev.copy()
+    plain[2 * CH + 7] ^= 1
+    assert oracle.commit(plain, CH, staging, payload, v) == 0
+    assert not np.array_equal(plain, cur)
+    # a staged record changed after verification: refused
+    bad_staging = staging.copy()
+    bad_staging[CH + 5] ^= 0x80
+    live = prev.copy()
+    assert oracle.commit_reverify(1, live, CH, bad_staging, payload, v) == oracle.V_REVERIFY
+    assert np.array_equal(live, prev)
+    # a nonzero verdict passes through, nothing installed
+    live = prev.copy()
+    assert oracle.commit_reverify(1, live, CH, staging, payload, oracle.V_DATA) == oracle.V_DATA
+    assert np.array_equal(live, prev)
+    # a full ship re-verifies into any live buffer
+    full = oracle.encode(0, cur, CH)
+    v, st_full, _ = oracle.decode_verify(0, full, n, CH)
+    live = np.zeros(n, np.uint8)
+    assert oracle.commit_reverify(0, live, CH, st_full, full, v) == 0
+    assert np.array_equal(live, cur)
