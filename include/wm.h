@@ -78,6 +78,9 @@ typedef int32_t wm_status;
 #define WM_V_RECORD 4u  /* some record's structure is invalid */
 #define WM_V_DATA 8u    /* some decoded chunk's CRC differs from its receipt */
 #define WM_V_STAGING 16u /* staging_cap too small for the payload's records */
+#define WM_V_REVERIFY 32u /* wm_commit_reverify: a staged record no longer
+                             matches its receipt, or the installed state
+                             would not have the source's global CRC */
 
 /* wm_commit_or_abort modes */
 #define WM_COMMIT_NONE 0    /* only read the verdict (full ship: caller swaps) */
@@ -226,6 +229,29 @@ wm_status wm_decode_verify(const void *payload, uint64_t payload_cap,
 wm_status wm_commit_or_abort(void *live, uint64_t nbytes, const wm_params *p,
                              const void *staging, const void *payload,
                              const uint32_t *verdict, uint32_t mode,
+                             void *stream);
+
+/* Install with re-verification (Table 1: commit re-verifies, then swaps;
+ * §4 "Sufficiency": commit only on a byte-identical fingerprint).  A scatter
+ * install (as WM_COMMIT_SCATTER) that runs only if, besides a zero verdict
+ * from wm_decode_verify:
+ *   - every staged record still has its receipt's CRC (staging unchanged
+ *     since it was verified), and
+ *   - the state the install would produce (live's other chunks plus the
+ *     staged records) has the header's global CRC, the CRC of the source
+ *     state: the destination's base is the source's last shipped snapshot.
+ * Without it the guarantee of a dirty ship holds only relative to the base
+ * the destination already had.  On failure WM_V_REVERIFY is ORed into
+ * *verdict and live is untouched.  Costs a read of live and of the staged
+ * records (their CRCs) before the install.  Waits for the stream; returns
+ * WM_OK (installed) or WM_VERIFY_FAILED.
+ *   live, staging, payload, verdict : as for wm_commit_or_abort (SCATTER)
+ *   ws : workspace of ws_bytes >= wm_workspace_bytes() (chunk CRCs)
+ * Errors: WM_ERR_INVALID_ARG, WM_ERR_WORKSPACE, WM_ERR_UNSUPPORTED,
+ *         WM_ERR_HIP. */
+wm_status wm_commit_reverify(void *live, uint64_t nbytes, const wm_params *p,
+                             const void *staging, const void *payload,
+                             uint32_t *verdict, void *ws, uint64_t ws_bytes,
                              void *stream);
 
 /* ---- manifest: flatten and rehydrate --------------------------------------

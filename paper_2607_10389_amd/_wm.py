@@ -29,7 +29,7 @@ WM_CRC32C = 1
 WM_CODEC_EXPFOR = 1
 WM_CODEC_EXPHUF = 2
 
-V_HEADER, V_TABLE, V_RECORD, V_DATA, V_STAGING = 1, 2, 4, 8, 16
+V_HEADER, V_TABLE, V_RECORD, V_DATA, V_STAGING, V_REVERIFY = 1, 2, 4, 8, 16, 32
 
 WM_COMMIT_NONE = 0
 WM_COMMIT_SCATTER = 1
@@ -42,7 +42,7 @@ EXPORTS = (
     "wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_encode_step",
     "wm_decode_verify", "wm_commit_or_abort", "wm_flat_bytes",
     "wm_manifest_ws_bytes", "wm_flatten", "wm_rehydrate", "wm_precopy_round",
-    "wm_receive_verify", "wm_encode_step_static",
+    "wm_receive_verify", "wm_encode_step_static", "wm_commit_reverify",
 )
 
 
@@ -98,6 +98,7 @@ def _load():
                              ctypes.c_int32),
         "wm_commit_or_abort": ([vp, u64, pp, vp, vp, vp, u32, vp],
                                ctypes.c_int32),
+        "wm_commit_reverify": ([vp, u64, pp, vp, vp, vp, vp, u64, vp], ctypes.c_int32),
         "wm_flat_bytes": ([lp, u32], u64),
         "wm_manifest_ws_bytes": ([u32], u64),
         "wm_flatten": ([lp, u32, vp, u64, vp, u64, vp], ctypes.c_int32),
@@ -225,6 +226,14 @@ def commit_or_abort(live, nbytes, p, staging, payload, verdict, mode,
                                          _p(staging), _p(payload), _p(verdict),
                                          mode, _stream(stream)),
                   "wm_commit_or_abort")
+
+
+def commit_reverify(live, nbytes, p, staging, payload, verdict, ws, stream=None):
+    """Scatter install after re-verifying the staged records and the global
+    CRC of the state it would produce; returns WM_OK or WM_VERIFY_FAILED."""
+    return _check(LIB.wm_commit_reverify(_p(live), nbytes, ctypes.byref(p), _p(staging),
+                                         _p(payload), _p(verdict), _p(ws), _nbytes(ws),
+                                         _stream(stream)), "wm_commit_reverify")
 
 
 class LeafTable:

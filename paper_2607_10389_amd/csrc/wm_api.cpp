@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstring>
 #include <cstdint>
 #include <map>
 #include <mutex>
@@ -353,6 +354,68 @@ wm_status wm_commit_or_abort(void *live, uint64_t nbytes, const wm_params *p, co
   if (hipMemcpyAsync(&v, verdict, sizeof(v), hipMemcpyDeviceToHost, st) != hipSuccess)
     return WM_ERR_HIP;
   if (hipStreamSynchronize(st) != hipSuccess) return WM_ERR_HIP;
+  return v == 0 ? WM_OK : WM_VERIFY_FAILED;
+}
+
+wm_status wm_commit_reverify(void *live, uint64_t nbytes, const wm_params *p,
+                             const void *staging, const void *payload, uint32_t *verdict,
+                             void *ws, uint64_t ws_bytes, void *stream) {
+  ChunkGeom g;
+  wm_status s = make_geom(nbytes, p, &g);
+  if (s != WM_OK) return s;
+  if (!verdict || !payload || !aligned16(payload)) return WM_ERR_INVALID_ARG;
+  if ((nbytes && (!live || !staging)) || !aligned16(live) || !aligned16(staging))
+    return WM_ERR_INVALID_ARG;
+  const WsLayout L = ws_layout(g.n_chunks);
+  if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
+  int n_cu = 0;
+  if ((s = ensure_device(&n_cu)) != WM_OK) return s;
+  n_cu = stream_cus(stream, n_cu);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  // a failed verification needs no further work: nothing is installed
+  uint32_t v = 0xFFFFFFFFu;
+  if (hipMemcpyAsync(&v, verdict, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return WM_ERR_HIP;
+  if (v != 0) return WM_VERIFY_FAILED;
+  // a zero verdict means the header and table passed their checks: the
+  // staged records are chunks table[0..n_rec) in ascending order, each a
+  // full chunk except possibly the last (the state's short last chunk)
+  uint8_t head[64];
+  uint8_t last[16] = {0};
+  if (hipMemcpyAsync(head, payload, 64, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return WM_ERR_HIP;
+  uint32_t n_rec = 0;
+  uint64_t total = 0, state = 0;
+  std::memcpy(&n_rec, head + 24, 4);
+  std::memcpy(&total, head + 32, 8);
+  std::memcpy(&state, head + 16, 8);
+  // the payload a zero verdict was given for has these properties; another
+  // payload is a caller error
+  if (state != nbytes || n_rec > g.n_chunks || total < 64u + 16ull * n_rec)
+    return WM_ERR_INVALID_ARG;
+  uint64_t staged = 0;
+  if (n_rec) {
+    const uint8_t *entry = static_cast<const uint8_t *>(payload) + total - 16u;
+    if (hipMemcpyAsync(last, entry, 16, hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+      return WM_ERR_HIP;
+    uint32_t c_last = 0;
+    std::memcpy(&c_last, last, 4);
+    if (c_last >= g.n_chunks) return WM_ERR_INVALID_ARG;
+    const uint64_t len_last = c_last + 1 == g.n_chunks ? g.tail_len : kChunk;
+    staged = (uint64_t)(n_rec - 1) * kChunk + len_last;
+  }
+  ChunkGeom gs;
+  if ((s = make_geom(staged, p, &gs)) != WM_OK) return s;
+  if (launch_reverify(live, g, staging, gs, payload, verdict, ws, L, n_cu, stream) != 0)
+    return WM_ERR_HIP;
+  if (nbytes && launch_commit(live, g, staging, payload, verdict, n_cu, stream) != 0)
+    return WM_ERR_HIP;
+  if (hipMemcpyAsync(&v, verdict, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return WM_ERR_HIP;
   return v == 0 ? WM_OK : WM_VERIFY_FAILED;
 }
 

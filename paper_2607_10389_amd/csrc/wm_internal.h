@@ -116,6 +116,14 @@ int launch_decode_end(const ChunkGeom &g, uint32_t *verdict, void *ws, const WsL
 int launch_commit(void *live, const ChunkGeom &g, const void *staging,
                   const void *payload, const uint32_t *verdict, int n_cu,
                   void *stream);
+// Re-verification before an install: CRCs of live's chunks (geometry g) and
+// of the staged records (gs: the staged bytes as one state), receipts in
+// place of the chunks the install overwrites, their combined global CRC
+// against the header's; a failure ORs 32 into the verdict.  Uses the
+// workspace's control block, entry CRC and flag arrays.
+int launch_reverify(const void *live, const ChunkGeom &g, const void *staging,
+                    const ChunkGeom &gs, const void *payload, uint32_t *verdict, void *ws,
+                    const WsLayout &L, int n_cu, void *stream);
 // One leaf of a manifest as the device sees it (the library's copy of the
 // caller's table, with offsets): 32 bytes.
 struct ManifestLeaf {

@@ -3200,6 +3200,67 @@ int launch_commit(void *live, const ChunkGeom &g, const void *staging, const voi
   return (int)hipGetLastError();
 }
 
+// ------------------------------------------------------------- reverify --
+// Re-verifying install (Table 1: commit re-verifies, then swaps).  live_crc
+// holds the CRC of every chunk of live, staged_crc that of every staged
+// record.  One workgroup walks the payload's table: a staged record whose
+// CRC differs from its receipt sets the flag, and the record's receipt
+// replaces the CRC of the chunk it will overwrite, so that live_crc becomes
+// the chunk CRCs of the state the install would produce.
+__global__ __launch_bounds__(1024) void k_reverify_records(const uint8_t *__restrict__ payload,
+                                                           uint32_t *__restrict__ live_crc,
+                                                           const uint32_t *__restrict__ staged_crc,
+                                                           uint32_t *__restrict__ flag,
+                                                           uint32_t n_chunks) {
+  __shared__ uint32_t any;
+  if (threadIdx.x == 0) any = 0;
+  __syncthreads();
+  const uint32_t n_rec = ld_u32(payload + 24);
+  const uint64_t table_off = ld_u64(payload + 32) - 16ull * n_rec;
+  uint32_t bad = 0;
+  for (uint32_t r = threadIdx.x; r < n_rec; r += blockDim.x) {
+    const uint2 e = *reinterpret_cast<const uint2 *>(payload + table_off + 16ull * r);
+    bad |= staged_crc[r] != e.y || e.x >= n_chunks ? 1u : 0u;
+    if (e.x < n_chunks) live_crc[e.x] = e.y;
+  }
+  if (bad) atomicOr(&any, 1u);
+  __syncthreads();
+  if (threadIdx.x == 0) *flag = any;
+}
+
+// The resulting state's global CRC (combined from live_crc) against the
+// header's: any disagreement, or a flagged record, adds WM_V_REVERIFY to the
+// verdict, so that the install that follows copies nothing.
+__global__ void k_reverify_end(const uint8_t *__restrict__ payload, const uint32_t *flag,
+                               const uint32_t *global, uint32_t *verdict) {
+  if (threadIdx.x == 0 && (*flag != 0u || *global != ld_u32(payload + 40))) *verdict |= 32u;
+}
+
+int launch_reverify(const void *live, const ChunkGeom &g, const void *staging,
+                    const ChunkGeom &gs, const void *payload, uint32_t *verdict, void *ws,
+                    const WsLayout &L, int n_cu, void *stream) {
+  uint8_t *wsb = static_cast<uint8_t *>(ws);
+  uint32_t *live_crc = reinterpret_cast<uint32_t *>(wsb + L.flags);
+  uint32_t *staged_crc = reinterpret_cast<uint32_t *>(wsb + L.entry_crc);
+  uint32_t *words = reinterpret_cast<uint32_t *>(wsb + L.ctl);  // [0] flag, [1] global
+  int rc = launch_checksum(live, g, live_crc, nullptr, n_cu, stream);
+  if (rc) return rc;
+  rc = launch_checksum(staging, gs, staged_crc, nullptr, n_cu, stream);
+  if (rc) return rc;
+  hipLaunchKernelGGL(k_reverify_records, dim3(1), dim3(1024), 0, S(stream),
+                     static_cast<const uint8_t *>(payload), live_crc,
+                     static_cast<const uint32_t *>(staged_crc), words, g.n_chunks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return (int)e;
+  CombineJobs jobs = {};
+  jobs.job[0] = CombineJob{live_crc, nullptr, g.n_chunks, 16u, g.tail_len, g.crc_kind, words + 1};
+  rc = launch_combine(jobs, 1, stream);
+  if (rc) return rc;
+  hipLaunchKernelGGL(k_reverify_end, dim3(1), dim3(64), 0, S(stream),
+                     static_cast<const uint8_t *>(payload), words, words + 1, verdict);
+  return (int)hipGetLastError();
+}
+
 int launch_encode_v2(const void *state, const ChunkGeom &g, const uint32_t *idx,
                      const uint32_t *n_idx, const uint32_t *crc_in, uint32_t *crc_scratch,
                      uint32_t *global_crc, void *payload, uint64_t *payload_bytes, void *ws,

@@ -87,6 +87,14 @@ class Mover:
         return _wm.commit_or_abort(live, self.nbytes, self.p, self.staging, pl,
                                    self.verdict, mode, self.stream)
 
+    def commit_reverify(self, live: torch.Tensor,
+                        payload: torch.Tensor | None = None) -> int:
+        """Scatter install after re-verifying the staged records and the
+        global CRC of the state the install would produce."""
+        pl = self.payload if payload is None else payload
+        return _wm.commit_reverify(live, self.nbytes, self.p, self.staging, pl,
+                                   self.verdict, self.ws_dst, self.stream)
+
     def receive(self, host_payload: torch.Tensor, payload_bytes: int,
                 batch_bytes: int, copy_stream):
         """Copy a payload from host memory into self.payload in batches on

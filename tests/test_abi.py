@@ -68,6 +68,7 @@ def lib():
     L.wm_encode_step_static.argtypes = [vp, vp, u64, pp, vp, vp, vp, vp, vp, u64, vp, vp]
     L.wm_decode_verify.argtypes = [vp, u64, u64, pp, vp, u64, vp, vp, vp, u64, vp]
     L.wm_commit_or_abort.argtypes = [vp, u64, pp, vp, vp, vp, u32, vp]
+    L.wm_commit_reverify.argtypes = [vp, u64, pp, vp, vp, vp, vp, u64, vp]
     lp = ctypes.POINTER(Leaf)
     L.wm_flat_bytes.restype = u64
     L.wm_flat_bytes.argtypes = [lp, u32]
@@ -95,7 +96,7 @@ def test_header_declares_the_boundary():
     for must in ("wm_checksum_chunks", "wm_diff_dirty", "wm_encode", "wm_decode_verify",
                  "wm_commit_or_abort", "wm_flatten", "wm_rehydrate"):
         assert must in names
-    assert len(names) == len(set(names)) == 17
+    assert len(names) == len(set(names)) == 18
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -299,3 +300,14 @@ def test_static_step_refuses_a_state_beyond_its_workspace(lib):
     # the usual argument checks come first
     assert fn(a, None, nbytes + 1, P(), None, None, None, None, a, bound, a, None) == INVALID
     assert fn(a, None, nbytes, P(), None, None, None, None, a, bound - 1, a, None) == CAPACITY
+
+
+def test_reverify_argument_checks(lib):
+    a = ALIGNED
+    ws = lib.wm_workspace_bytes(4 * CH, P())
+    rv = lib.wm_commit_reverify
+    assert rv(a, 4 * CH, P(), a, a, None, a, ws, None) == INVALID        # no verdict
+    assert rv(a + 8, 4 * CH, P(), a, a, a, a, ws, None) == INVALID       # misaligned live
+    assert rv(a, 4 * CH, P(), a, a + 4, a, a, ws, None) == INVALID       # misaligned payload
+    assert rv(a, 4 * CH, P(), a, a, a, a, ws - 1, None) == WORKSPACE
+    assert rv(a, 4 * CH, P(chunk=3000), a, a, a, a, ws, None) == INVALID
