@@ -65,10 +65,11 @@ typedef int32_t wm_status;
  * chunk's exponents in the chunk's own canonical Huffman code (lengths at
  * most 11) in 512 streams, so that 512 decoders work side by side (§6.4: the
  * redundancy of a bf16 cache sits in its exponent plane, which the paper's
- * codec entropy-codes).  Both fall back to RAW per chunk.  Format v2 is
- * taken by wm_encode, wm_decode_verify and wm_commit_or_abort; the fused and
- * composed calls (wm_encode_step, wm_receive_verify, wm_precopy_round)
- * return WM_ERR_UNSUPPORTED for it. */
+ * codec entropy-codes).  Both fall back to RAW per chunk.  Every call takes
+ * either format, except wm_encode_step_static (format v1 only).  Format v2
+ * has no single-pass encoder: its wm_encode_step runs the diff, a checksum
+ * of every chunk and the list encoder (same outputs), and its pre-copy
+ * rounds checksum every chunk. */
 #define WM_CODEC_EXPFOR 1
 #define WM_CODEC_EXPHUF 2
 
@@ -102,7 +103,8 @@ wm_status wm_init(int device);
 
 /* Bytes of device workspace needed by wm_diff_dirty, wm_encode,
  * wm_encode_step and wm_decode_verify for a state of nbytes (format v2 adds
- * 688 bytes per chunk for the record plans).  0 if p is invalid. */
+ * 692 bytes per chunk and a few hundred more: the record plans and a dirty
+ * list).  0 if p is invalid. */
 uint64_t wm_workspace_bytes(uint64_t nbytes, const wm_params *p);
 
 /* Largest payload that n_records records of a state of nbytes can produce
@@ -185,7 +187,8 @@ wm_status wm_encode_step(const void *cur, const void *prev, uint64_t nbytes,
  * array instead of the caller.  The call allocates nothing, on the host or
  * on the device.
  *   Limit: states of at most 65,536 chunks (4 GiB in 64 KiB chunks); a larger
- *   state returns WM_ERR_WORKSPACE before anything is enqueued.
+ *   state returns WM_ERR_WORKSPACE before anything is enqueued.  Format v1
+ *   only (format v2 returns WM_ERR_UNSUPPORTED).
  *   Sharing: each device holds one built-in workspace (2 MiB + 256 B, kept
  *   until the process ends) used by every call of this function on that
  *   device, whatever the stream.  Calls that overlap in time on one device

@@ -139,9 +139,13 @@ int stream_cus(void *stream, int n_cu) {
 
 // Workspace: the WsLayout part, then (format v2) one plan per chunk.
 uint64_t plans_offset(const WsLayout &L) { return (L.total + 255u) & ~255ull; }
+// Format v2 also keeps, after the plans, a dirty list and its length for
+// a fused step whose caller passes no dirty_idx.
+uint64_t list_offset(const WsLayout &L, uint32_t n_chunks) {
+  return (plans_offset(L) + (uint64_t)kHufPlanBytes * n_chunks + 255u) & ~255ull;
+}
 uint64_t ws_need(const WsLayout &L, uint32_t n_chunks, uint32_t codec) {
-  return codec == WM_CODEC_EXPHUF ? plans_offset(L) + (uint64_t)kHufPlanBytes * n_chunks
-                                  : L.total;
+  return codec == WM_CODEC_EXPHUF ? list_offset(L, n_chunks) + 4ull * n_chunks + 16u : L.total;
 }
 
 wm_status hip_status(int e) { return e == 0 ? WM_OK : WM_ERR_HIP; }
@@ -265,7 +269,8 @@ wm_status encode_step_call(const void *cur, const void *prev, uint64_t nbytes,
   ChunkGeom g;
   wm_status s = make_geom(nbytes, p, &g, !builtin);
   if (s != WM_OK) return s;
-  if (g.codec != WM_CODEC_EXPFOR) return WM_ERR_UNSUPPORTED;
+  // the built-in workspace has the format v1 layout only
+  if (builtin && g.codec != WM_CODEC_EXPFOR) return WM_ERR_UNSUPPORTED;
   if (nbytes & 1u) return WM_ERR_INVALID_ARG;
   if ((nbytes && !cur) || !aligned16(cur) || !aligned16(prev)) return WM_ERR_INVALID_ARG;
   if (!payload || !payload_bytes || !aligned16(payload)) return WM_ERR_INVALID_ARG;
@@ -278,12 +283,28 @@ wm_status encode_step_call(const void *cur, const void *prev, uint64_t nbytes,
     if ((s = ensure_device(&n_cu, &ws, &ws_bytes)) != WM_OK) return s;
     if (L.total > ws_bytes) return WM_ERR_WORKSPACE;
   } else {
-    if (!ws || ws_bytes < L.total || !aligned16(ws)) return WM_ERR_WORKSPACE;
+    if (!ws || ws_bytes < ws_need(L, g.n_chunks, g.codec) || !aligned16(ws))
+      return WM_ERR_WORKSPACE;
     if ((s = ensure_device(&n_cu)) != WM_OK) return s;
   }
   n_cu = stream_cus(stream, n_cu);
-  uint32_t *crcs =
-      crc_out ? crc_out : reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + L.flags);
+  uint8_t *wsb = static_cast<uint8_t *>(ws);
+  uint32_t *crcs = crc_out ? crc_out : reinterpret_cast<uint32_t *>(wsb + L.flags);
+  if (g.codec == WM_CODEC_EXPHUF) {
+    // format v2 has no single-pass encoder: the same outputs from the diff
+    // (whose flags it consumes first), a checksum of every chunk and the
+    // list encoder, each reading the state once
+    uint32_t *list = dirty_idx ? dirty_idx : reinterpret_cast<uint32_t *>(wsb + list_offset(L, g.n_chunks));
+    uint32_t *n_list = n_dirty ? n_dirty : list + g.n_chunks;
+    if (prev && launch_diff(cur, prev, g, list, n_list, ws, L, stream) != 0) return WM_ERR_HIP;
+    if (!prev && (dirty_idx || n_dirty) &&
+        launch_fill_all(dirty_idx, n_dirty, g.n_chunks, stream) != 0)
+      return WM_ERR_HIP;
+    if (launch_checksum(cur, g, crcs, nullptr, n_cu, stream) != 0) return WM_ERR_HIP;
+    return hip_status(launch_encode_v2(cur, g, prev ? list : nullptr, prev ? n_list : nullptr,
+                                       crcs, nullptr, global_crc, payload, payload_bytes, ws, L,
+                                       wsb + plans_offset(L), n_cu, stream));
+  }
   return hip_status(launch_encode(2, cur, prev, g, nullptr, nullptr, nullptr, crcs, global_crc,
                                   dirty_idx, n_dirty, payload, payload_bytes, ws, L, n_cu,
                                   stream));
@@ -491,7 +512,6 @@ wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t 
   ChunkGeom g;
   wm_status s = make_geom(nbytes, p, &g);
   if (s != WM_OK) return s;
-  if (g.codec != WM_CODEC_EXPFOR) return WM_ERR_UNSUPPORTED;
   if ((nbytes & 1u) || crc_valid > 1) return WM_ERR_INVALID_ARG;
   if (!b || !n_dirty_host || !b->crc || !b->dirty_idx || !b->n_dirty) return WM_ERR_INVALID_ARG;
   if (nbytes && (!cur || !shipped || !dest)) return WM_ERR_INVALID_ARG;
@@ -502,7 +522,8 @@ wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t 
   if (!b->payload || !b->payload_bytes || !aligned16(b->payload) || !aligned16(cur))
     return WM_ERR_INVALID_ARG;
   if (b->payload_cap < wm_payload_bound(nbytes, g.n_chunks, p)) return WM_ERR_CAPACITY;
-  if (!b->ws_src || !aligned16(b->ws_src) || b->ws_src_bytes < ws_layout(g.n_chunks).total)
+  if (!b->ws_src || !aligned16(b->ws_src) ||
+      b->ws_src_bytes < ws_need(ws_layout(g.n_chunks), g.n_chunks, g.codec))
     return WM_ERR_WORKSPACE;
   if (!b->verdict || (nbytes && !b->staging) || !aligned16(b->staging)) return WM_ERR_INVALID_ARG;
   if (b->staging_cap < (uint64_t)g.n_chunks * kChunk) return WM_ERR_CAPACITY;
@@ -525,10 +546,20 @@ wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t 
     int n_cu0 = 0;
     if ((s = ensure_device(&n_cu0)) != WM_OK) return s;
     n_cu0 = stream_cus(stream, n_cu0);
-    if (launch_encode(0, cur, nullptr, g, b->dirty_idx, b->n_dirty, nullptr, b->crc,
-                      b->global_crc, nullptr, nullptr, b->payload, b->payload_bytes, b->ws_src,
-                      ws_layout(g.n_chunks), n_cu0, stream) != 0)
+    const WsLayout L = ws_layout(g.n_chunks);
+    if (g.codec == WM_CODEC_EXPHUF) {
+      // format v2 takes its receipts from a checksum of every chunk
+      if (launch_checksum(cur, g, b->crc, nullptr, n_cu0, stream) != 0 ||
+          launch_encode_v2(cur, g, b->dirty_idx, b->n_dirty, b->crc, nullptr, b->global_crc,
+                           b->payload, b->payload_bytes, b->ws_src, L,
+                           static_cast<uint8_t *>(b->ws_src) + plans_offset(L), n_cu0,
+                           stream) != 0)
+        return WM_ERR_HIP;
+    } else if (launch_encode(0, cur, nullptr, g, b->dirty_idx, b->n_dirty, nullptr, b->crc,
+                             b->global_crc, nullptr, nullptr, b->payload, b->payload_bytes,
+                             b->ws_src, L, n_cu0, stream) != 0) {
       return WM_ERR_HIP;
+    }
   }
   s = wm_decode_verify(b->payload, b->payload_cap, nbytes, p, b->staging, b->staging_cap,
                        b->verdict, b->rec_status, b->ws_dst, b->ws_dst_bytes, stream);
@@ -560,6 +591,27 @@ uint32_t host_u32(const uint8_t *p) {
   return (uint32_t)p[0] | (uint32_t)p[1] << 8 | (uint32_t)p[2] << 16 | (uint32_t)p[3] << 24;
 }
 uint64_t host_u64(const uint8_t *p) { return host_u32(p) | (uint64_t)host_u32(p + 4) << 32; }
+
+// Two events (copy stream -> decode stream, and back) per thread and
+// device, made on first use and kept for the process: one thread's calls
+// are sequential, and a stream wait binds to the event's record at the time
+// of the wait, so the same two serve every batch of every call.
+hipEvent_t *order_events() {
+  struct PerThread {
+    hipEvent_t e[kMaxDevices][2];
+    bool made[kMaxDevices];
+  };
+  thread_local PerThread t = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  if (!t.made[dev]) {
+    for (int i = 0; i < 2; ++i)
+      if (hipEventCreateWithFlags(&t.e[dev][i], hipEventDisableTiming) != hipSuccess)
+        return nullptr;
+    t.made[dev] = true;
+  }
+  return t.e[dev];
+}
 
 struct Batch {
   uint64_t b0, b1;  // payload bytes [b0, b1)
@@ -622,7 +674,6 @@ wm_status wm_receive_verify(const void *host_payload, uint64_t payload_bytes, vo
   ChunkGeom g;
   wm_status s = make_geom(nbytes, p, &g);
   if (s != WM_OK) return s;
-  if (g.codec != WM_CODEC_EXPFOR) return WM_ERR_UNSUPPORTED;
   if (nbytes & 1u) return WM_ERR_INVALID_ARG;
   if (!payload || !verdict || !aligned16(payload)) return WM_ERR_INVALID_ARG;
   if (payload_bytes && !host_payload) return WM_ERR_INVALID_ARG;
@@ -640,11 +691,13 @@ wm_status wm_receive_verify(const void *host_payload, uint64_t payload_bytes, vo
       receive_schedule(h, payload_bytes, g.n_chunks, batch_bytes, &table_off);
   hipStream_t cs = reinterpret_cast<hipStream_t>(copy_stream);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  std::vector<hipEvent_t> ev;
-  auto order = [&](hipStream_t from, hipStream_t to) -> bool {  // `to` waits for `from`
-    hipEvent_t e;
-    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return false;
-    ev.push_back(e);
+  auto records = g.codec == WM_CODEC_EXPHUF ? launch_decode_records_v2 : launch_decode_records;
+  hipEvent_t *ev = order_events();
+  if (!ev) return WM_ERR_HIP;
+  // `to` waits for the work enqueued on `from` so far (the wait binds to
+  // the event's latest record, so the event is reused for every batch)
+  auto order = [&](hipStream_t from, hipStream_t to) -> bool {
+    hipEvent_t e = ev[from == cs ? 0 : 1];
     return hipEventRecord(e, from) == hipSuccess && hipStreamWaitEvent(to, e, 0) == hipSuccess;
   };
   // the decode stream waits for the copies enqueued so far
@@ -665,17 +718,14 @@ wm_status wm_receive_verify(const void *host_payload, uint64_t payload_bytes, vo
     for (size_t i = 0; ok && i < batches.size(); ++i) {
       const Batch &b = batches[i];
       ok = copy(b.b0, b.b1) && arrived() &&
-           launch_decode_records(payload, g, staging, rec_status, ws, L, n_cu, b.r0, b.r1,
-                                 stream) == 0;
+           records(payload, g, staging, rec_status, ws, L, n_cu, b.r0, b.r1, stream) == 0;
     }
   } else {
     ok = copy(0, payload_bytes) && arrived() &&
          launch_decode_begin(payload, payload_bytes, g, staging_cap, ws, L, stream) == 0 &&
-         launch_decode_records(payload, g, staging, rec_status, ws, L, n_cu, 0u, g.n_chunks,
-                               stream) == 0;
+         records(payload, g, staging, rec_status, ws, L, n_cu, 0u, g.n_chunks, stream) == 0;
   }
   ok = ok && launch_decode_end(g, verdict, ws, L, stream) == 0;
-  for (hipEvent_t e : ev) hipEventDestroy(e);  // released once the waits are satisfied
   return ok ? WM_OK : WM_ERR_HIP;
 }
 

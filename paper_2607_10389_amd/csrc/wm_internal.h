@@ -116,6 +116,8 @@ int launch_decode_end(const ChunkGeom &g, uint32_t *verdict, void *ws, const WsL
 int launch_commit(void *live, const ChunkGeom &g, const void *staging,
                   const void *payload, const uint32_t *verdict, int n_cu,
                   void *stream);
+// idx[i] = i for i < n (idx may be NULL) and *n_out = n (n_out may be NULL).
+int launch_fill_all(uint32_t *idx, uint32_t *n_out, uint32_t n, void *stream);
 // Re-verification before an install: CRCs of live's chunks (geometry g) and
 // of the staged records (gs: the staged bytes as one state), receipts in
 // place of the chunks the install overwrites, their combined global CRC
@@ -142,6 +144,10 @@ int launch_encode_v2(const void *state, const ChunkGeom &g, const uint32_t *idx,
                      const uint32_t *n_idx, const uint32_t *crc_in, uint32_t *crc_scratch,
                      uint32_t *global_crc, void *payload, uint64_t *payload_bytes, void *ws,
                      const WsLayout &L, uint8_t *plans, int n_cu, void *stream);
+// Format v2 records [r0, r1) (as launch_decode_records).
+int launch_decode_records_v2(const void *payload, const ChunkGeom &g, void *staging,
+                             uint32_t *rec_status, void *ws, const WsLayout &L, int n_cu,
+                             uint32_t r0, uint32_t r1, void *stream);
 int launch_decode_v2(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
                      void *staging, uint64_t staging_cap, uint32_t *verdict,
                      uint32_t *rec_status, void *ws, const WsLayout &L, int n_cu,

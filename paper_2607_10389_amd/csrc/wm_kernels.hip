@@ -2652,11 +2652,14 @@ __device__ __forceinline__ HufFetch huf_fetch(const uint8_t *__restrict__ payloa
 // control wave folds the CRC and records the status.
 __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
     const uint8_t *__restrict__ payload, ChunkGeom g, uint8_t *__restrict__ staging,
-    uint32_t *__restrict__ rec_status, uint8_t *ws, WsLayout L) {
+    uint32_t *__restrict__ rec_status, uint8_t *ws, WsLayout L, uint32_t r0, uint32_t r1) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(ws + L.ctl);
   uint32_t *ecrc = reinterpret_cast<uint32_t *>(ws + L.entry_crc);
   if (!uniform(ctl->hdr_ok)) return;
+  // records [r0, r1) of the table, clamped to its length (a payload decoded
+  // in batches as it arrives)
   const uint32_t n_rec = uniform(ctl->n_rec);
+  const uint32_t r_hi = min(r1, n_rec), r_lo = min(r0, r_hi);
   const uint64_t table_off = ctl->table_off;
   load_crc_tables(g.crc_kind);
   __syncthreads();
@@ -2672,8 +2675,9 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
   const GLane gl = glane_make();
   const Lane l0 = lane_info();
   HufFetch fn;  // control lane: the next record's reads, issued a step ahead
-  if (t == (uint32_t)kThreads && blockIdx.x < n_rec) fn = huf_fetch(payload, table_off, n_rec, blockIdx.x);
-  for (uint32_t r = blockIdx.x; r < n_rec; r += gridDim.x) {
+  if (t == (uint32_t)kThreads && r_lo + blockIdx.x < r_hi)
+    fn = huf_fetch(payload, table_off, n_rec, r_lo + blockIdx.x);
+  for (uint32_t r = r_lo + blockIdx.x; r < r_hi; r += gridDim.x) {
     const Lane l = lane_fresh(l0);
     if (t == (uint32_t)kThreads) {
       const HufFetch f = fn;
@@ -2726,7 +2730,7 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
       }
     }
     __syncthreads();
-    if (t == (uint32_t)kThreads && r + gridDim.x < n_rec)
+    if (t == (uint32_t)kThreads && r + gridDim.x < r_hi)
       fn = huf_fetch(payload, table_off, n_rec, r + gridDim.x);
     const uint32_t st0 = uniform(M.st), mode = uniform(M.mode), k = uniform(M.k);
     const uint32_t n = uniform(M.n), sb = uniform(M.sb);
@@ -3200,6 +3204,19 @@ int launch_commit(void *live, const ChunkGeom &g, const void *staging, const voi
   return (int)hipGetLastError();
 }
 
+// A full ship's dirty list: every chunk, in order.
+__global__ void k_fill_all(uint32_t *__restrict__ idx, uint32_t *__restrict__ n_out, uint32_t n) {
+  if (idx)
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+      idx[i] = i;
+  if (n_out && blockIdx.x == 0 && threadIdx.x == 0) *n_out = n;
+}
+
+int launch_fill_all(uint32_t *idx, uint32_t *n_out, uint32_t n, void *stream) {
+  hipLaunchKernelGGL(k_fill_all, dim3(64), dim3(256), 0, S(stream), idx, n_out, n);
+  return (int)hipGetLastError();
+}
+
 // ------------------------------------------------------------- reverify --
 // Re-verifying install (Table 1: commit re-verifies, then swaps).  live_crc
 // holds the CRC of every chunk of live, staged_crc that of every staged
@@ -3302,20 +3319,26 @@ int launch_encode_v2(const void *state, const ChunkGeom &g, const uint32_t *idx,
   return (int)hipGetLastError();
 }
 
+int launch_decode_records_v2(const void *payload, const ChunkGeom &g, void *staging,
+                             uint32_t *rec_status, void *ws, const WsLayout &L, int n_cu,
+                             uint32_t r0, uint32_t r1, void *stream) {
+  if (r1 <= r0 || !g.n_chunks) return 0;
+  const uint32_t grid = min((uint32_t)n_cu, min(r1 - r0, g.n_chunks));
+  hipLaunchKernelGGL(k_huf_decode, dim3(grid), dim3(kThreads + 64), kLdsHufDecode, S(stream),
+                     static_cast<const uint8_t *>(payload), g, static_cast<uint8_t *>(staging),
+                     rec_status, static_cast<uint8_t *>(ws), L, r0, r1);
+  return (int)hipGetLastError();
+}
+
 int launch_decode_v2(const void *payload, uint64_t payload_cap, const ChunkGeom &g,
                      void *staging, uint64_t staging_cap, uint32_t *verdict,
                      uint32_t *rec_status, void *ws, const WsLayout &L, int n_cu,
                      void *stream) {
   int rc = launch_decode_begin(payload, payload_cap, g, staging_cap, ws, L, stream);
   if (rc) return rc;
-  if (g.n_chunks) {
-    const uint32_t grid = min((uint32_t)n_cu, g.n_chunks);
-    hipLaunchKernelGGL(k_huf_decode, dim3(grid), dim3(kThreads + 64), kLdsHufDecode, S(stream),
-                       static_cast<const uint8_t *>(payload), g, static_cast<uint8_t *>(staging),
-                       rec_status, static_cast<uint8_t *>(ws), L);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return (int)e;
-  }
+  rc = launch_decode_records_v2(payload, g, staging, rec_status, ws, L, n_cu, 0u, g.n_chunks,
+                                stream);
+  if (rc) return rc;
   return launch_decode_end(g, verdict, ws, L, stream);
 }
 

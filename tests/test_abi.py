@@ -278,15 +278,16 @@ def test_format_v2_calls(lib):
     enc = lib.wm_encode
     # the plans need the larger workspace
     assert enc(a, nb, P(codec=2), None, None, None, a, bound, a, a, ws1, None) == WORKSPACE
-    # fused and composed calls take format v1 only
+    # the fused step and pre-copy take format v2 too: a v1-sized workspace
+    # is too small for them (checked before any device work)
     assert lib.wm_encode_step(a, None, nb, P(codec=2), None, None, None, None, a, bound, a, a,
-                              ws2, None) == UNSUPPORTED
-    host = ctypes.create_string_buffer(64)
-    assert lib.wm_receive_verify(ctypes.addressof(host), 64, a, 64, nb, P(codec=2), a, nb, a,
-                                 None, a, ws2, 0, None, None) == UNSUPPORTED
+                              ws1, None) == WORKSPACE
     n = ctypes.c_uint32(0)
     assert lib.wm_precopy_round(a, a + 0x100000, a + 0x200000, nb, P(codec=2), None, 0,
-                                ctypes.byref(n), None) == UNSUPPORTED
+                                ctypes.byref(n), None) == INVALID  # no buffers
+    # only the allocation-free step is format v1 only
+    assert lib.wm_encode_step_static(a, None, nb, P(codec=2), None, None, None, None, a, bound,
+                                     a, None) == UNSUPPORTED
 
 
 def test_static_step_refuses_a_state_beyond_its_workspace(lib):

@@ -197,3 +197,98 @@ def test_huf_record_longer_than_raw_is_rejected(wm):
     torch.cuda.synchronize()
     assert int(m.verdict.item()) == 4
     assert int(u32(m.rec_status)[0]) == 4
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+def test_v2_encode_step(wm, kind):
+    """Format v2 through the fused call: full ship and the tiny 75%-dirty
+    step give the oracle's CRCs, global CRC, dirty list and payload, and the
+    step's scatter install leaves live equal to the source."""
+    prev, cur, ids = wm_inputs.tiny_step("cuda")
+    hc, hp = host_bytes(cur), host_bytes(prev)
+    n = hc.size
+    m = mover(n, kind)
+    m.encode_step(cur, None)
+    torch.cuda.synchronize()
+    assert np.array_equal(m.payload_host(), oracle.encode(kind, hc, CH, None, 1, codec=2))
+    assert np.array_equal(m.dirty_host(), np.arange(n // CH, dtype=np.uint32))
+    crcs, g = oracle.checksum_chunks(kind, hc, CH)
+    assert np.array_equal(m.crc_host(), crcs)
+    assert int(u32(m.global_crc)[0]) == g
+    m.encode_step(cur, prev)
+    torch.cuda.synchronize()
+    idx = oracle.diff_dirty(hc, hp, CH)
+    assert np.array_equal(m.dirty_host(), idx)
+    assert np.array_equal(m.crc_host(), crcs)
+    assert np.array_equal(m.payload_host(), oracle.encode(kind, hc, CH, idx, 1, codec=2))
+    live = prev.clone()
+    m.decode()
+    assert m.commit(live, scatter=True) == wm.WM_OK
+    assert torch.equal(live, cur)
+    # no dirty_idx, n_dirty or crc_out from the caller: the workspace holds them
+    m2 = mover(n, kind)
+    wm.encode_step(cur, prev, n, m2.p, None, None, None, None, m2.payload, m2.payload_bytes,
+                   m2.ws_src)
+    torch.cuda.synchronize()
+    assert np.array_equal(m2.payload_host(), m.payload_host())
+
+
+@pytest.mark.parametrize("batch", [0, 200_000, 1 << 40])
+def test_v2_pipelined_receive(wm, batch):
+    """Format v2 received in record batches: verdict, record status and
+    staging equal the oracle's decode of the same bytes, also with a flipped
+    bit in a record and in the table."""
+    prev, cur, _ = wm_inputs.tiny_step("cuda")
+    hc, hp = host_bytes(cur), host_bytes(prev)
+    idx = oracle.diff_dirty(hc, hp, CH)
+    good = oracle.encode(0, hc, CH, idx, 1, codec=2)
+    n = hc.size
+    m = mover(n)
+    for label, flip in (("clean", None), ("record", 64 + 300), ("table", good.size - 20)):
+        bad = good.copy()
+        if flip is not None:
+            bad[flip] ^= 0x10
+        host = torch.empty(bad.size, dtype=torch.uint8, pin_memory=True)
+        host[:] = torch.from_numpy(bad)
+        cs = torch.cuda.Stream()
+        m.payload.fill_(0xA7)
+        torch.cuda.synchronize()
+        m.receive(host, bad.size, batch, cs)
+        torch.cuda.synchronize()
+        v = int(m.verdict.item())
+        v_o, st_o, rs_o = oracle.decode_verify(0, bad, n, CH, m.staging.numel(), 1, codec=2)
+        assert v == v_o, (label, v, v_o)
+        if v_o & 3 == 0:
+            k = idx.size
+            assert np.array_equal(u32(m.rec_status)[:k], rs_o[:k]), label
+        if v_o == 0:
+            got = m.staging[: idx.size * CH].cpu().numpy()
+            assert np.array_equal(got, st_o[: idx.size * CH]), label
+        else:
+            assert flip is not None
+
+
+def test_v2_precopy_rounds(wm):
+    """Pre-copy rounds in format v2: each round's dirty list and payload
+    equal the oracle's, and the destination ends equal to the source."""
+    spec = wm_inputs.TINY
+    cur = wm_inputs.make_cache(spec, "cuda")
+    n = spec.nbytes
+    shipped = torch.zeros(n, dtype=torch.uint8, device="cuda")
+    dest = torch.zeros_like(shipped)
+    m = mover(n)
+    for k in range(4):
+        cur_h, shp_h = host_bytes(cur), shipped.cpu().numpy()
+        st, nd = m.precopy_round(cur, shipped, dest)
+        assert st == wm.WM_OK, k
+        got = m.dirty_host()
+        assert np.array_equal(got, oracle.diff_dirty(cur_h, shp_h, CH)), k
+        assert np.array_equal(m.payload_host(), oracle.encode(0, cur_h, CH, got, 1, codec=2)), k
+        crcs, g = oracle.checksum_chunks(0, cur_h, CH)
+        assert np.array_equal(m.crc_host(), crcs), k
+        assert torch.equal(dest, shipped)
+        writes = wm_inputs.chunk_writes(n // CH, 9, seed=70 + k, device="cuda")
+        wm_inputs.rewrite_chunks(cur, spec, writes, seed=80 + k)
+    st, nd = m.precopy_round(cur, shipped, dest)
+    assert st == wm.WM_OK
+    assert torch.equal(dest, cur.view(-1).view(torch.uint8))
