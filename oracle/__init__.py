@@ -130,6 +130,11 @@ def n_chunks(nbytes: int, chunk: int) -> int:
     return (nbytes + chunk - 1) // chunk
 
 
+def unit(chunk: int) -> int:
+    """Bytes per record: the chunk up to 64 KiB, else a 64 KiB tile."""
+    return min(chunk, 65536)
+
+
 def checksum_chunks(kind: int, data, chunk: int = 65536, threads: int = 1):
     """Per-chunk CRCs (uint32 array) and the whole-buffer CRC."""
     b = _bytes(data)
@@ -210,9 +215,9 @@ def decode_verify(kind: int, payload, nbytes: int, chunk: int = 65536,
     """Returns (verdict, staging uint8 array, per-record status array)."""
     p = _bytes(payload)
     if staging_cap is None:
-        staging_cap = n_chunks(nbytes, chunk) * chunk
+        staging_cap = n_chunks(nbytes, unit(chunk)) * unit(chunk)
     staging = np.zeros(max(staging_cap, 1), np.uint8)
-    nst = max(n_chunks(nbytes, chunk), 1)
+    nst = max(n_chunks(nbytes, unit(chunk)), 1)
     status = np.zeros(nst, np.uint32)
     v = lib().orc_decode_verify_codec(kind, codec, _p8(p), p.size, nbytes, chunk,
                                       _p8(staging), staging_cap, _p32(status), nst,

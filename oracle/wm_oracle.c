@@ -18,9 +18,15 @@
  *    40 u32 global_crc (CRC of the whole source state)
  *    44 u32 table_crc  (CRC of the 16*n_records table bytes)
  *    48..59 zero                     60 u32 header_crc = CRC(bytes 0..59)
- *   records, contiguous from offset 64, in ascending chunk order
+ *   records, contiguous from offset 64, in ascending unit order
  *   table (16 B per record, after the last record, ending at payload_bytes):
- *     u32 chunk_idx, u32 src_crc, u64 record_offset
+ *     u32 unit_idx, u32 src_crc, u64 record_offset
+ *   The record unit is the chunk for chunks of at most 64 KiB.  A larger
+ *   chunk is shipped as its 64 KiB tiles (unit i = bytes [64Ki*i, 64Ki*(i+1))
+ *   of the state), one record and one receipt each, and a table lists every
+ *   tile of each chunk it ships; n_records counts units.  This keeps a
+ *   record's escape counts within 16 bits and its words within one
+ *   decoder's reach whatever the chunk size.
  *   Record:
  *     0 u8 mode (0 RAW, 1 PACK)  1 u8 k  2 u8 base  3 u8 0
  *     4 u32 n_words  8 u32 n_esc  12 u32 rec_crc = CRC(record bytes 0..11)
@@ -132,6 +138,10 @@ static int chunk_ok(uint32_t chunk) {
   return chunk >= 4096u && chunk <= (16u << 20) && (chunk & (chunk - 1)) == 0;
 }
 static uint64_t pad16(uint64_t x) { return (x + 15u) & ~(uint64_t)15u; }
+/* the record unit of a chunk size: the chunk itself up to 64 KiB, else a
+ * 64 KiB tile */
+#define ORC_TILE 65536u
+static uint32_t unit_of(uint32_t chunk) { return chunk < ORC_TILE ? chunk : ORC_TILE; }
 
 /* --------------------------------------------------------- checksumming -- */
 
@@ -680,11 +690,12 @@ static void en_write_range(void *vp, uint64_t lo, uint64_t hi) {
 }
 
 uint64_t orc_payload_bound(uint64_t nbytes, uint32_t chunk_bytes,
-                           uint32_t n_records) {
-  (void)nbytes; /* every record is bounded by a full RAW chunk */
+                           uint32_t n_ship) {
+  (void)nbytes; /* every record is bounded by a full RAW unit */
   if (!chunk_ok(chunk_bytes)) return 0;
-  return 64 + 16 * (uint64_t)n_records +
-         (uint64_t)n_records * raw_size(chunk_bytes / 2);
+  uint32_t u = unit_of(chunk_bytes);
+  uint64_t units = (uint64_t)n_ship * (chunk_bytes / u);
+  return 64 + units * (16 + raw_size(u / 2));
 }
 
 int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
@@ -700,13 +711,25 @@ int64_t orc_encode_codec(int kind, int codec, const uint8_t *state,
                          uint64_t cap, int threads) {
   if (!chunk_ok(chunk_bytes) || (kind != 0 && kind != 1) || (nbytes & 1))
     return -1;
-  if (codec != 1 && !(codec == 2 && chunk_bytes == 65536)) return -1;
+  if (codec != 1 && !(codec == 2 && chunk_bytes >= ORC_TILE)) return -1;
   uint64_t n_chunks = n_chunks_of(nbytes, chunk_bytes);
-  uint64_t n_rec = idx ? n_idx : n_chunks;
-  if (n_rec > n_chunks) return -1;
-  for (uint64_t r = 0; idx && r < n_rec; r++)
+  uint64_t n_ship = idx ? n_idx : n_chunks;
+  if (n_ship > n_chunks) return -1;
+  for (uint64_t r = 0; idx && r < n_ship; r++)
     if (idx[r] >= n_chunks || (r && idx[r] <= idx[r - 1])) return -1;
-  if (cap < orc_payload_bound(nbytes, chunk_bytes, (uint32_t)n_rec)) return -2;
+  if (cap < orc_payload_bound(nbytes, chunk_bytes, (uint32_t)n_ship)) return -2;
+
+  /* the units shipped: every unit of each listed chunk, in order */
+  uint32_t u = unit_of(chunk_bytes);
+  uint64_t per = chunk_bytes / u, n_units = n_chunks_of(nbytes, u);
+  uint64_t n_rec = idx ? 0 : n_units;
+  uint32_t *units = NULL;
+  if (idx) {
+    units = (uint32_t *)malloc((n_ship * per > 0 ? n_ship * per : 1) * 4);
+    for (uint64_t r = 0; r < n_ship; r++)
+      for (uint64_t j = 0; j < per; j++)
+        if (idx[r] * per + j < n_units) units[n_rec++] = (uint32_t)(idx[r] * per + j);
+  }
 
   uint64_t m = n_rec ? n_rec : 1;
   en_ctx x;
@@ -714,8 +737,8 @@ int64_t orc_encode_codec(int kind, int codec, const uint8_t *state,
   x.codec = codec;
   x.state = state;
   x.nbytes = nbytes;
-  x.chunk = chunk_bytes;
-  x.idx = idx;
+  x.chunk = u;
+  x.idx = units;
   x.mode = (uint32_t *)calloc(m, 4);
   x.k = (uint32_t *)calloc(m, 4);
   x.base = (uint32_t *)calloc(m, 4);
@@ -756,6 +779,7 @@ int64_t orc_encode_codec(int kind, int codec, const uint8_t *state,
   put_u32(h + 44, orc_crc(kind, payload + x.table, 16 * n_rec));
   put_u32(h + 60, orc_crc(kind, h, 60));
 
+  free(units);
   free(x.mode);
   free(x.k);
   free(x.base);
@@ -885,8 +909,10 @@ uint32_t orc_decode_verify_codec(int kind, int codec, const uint8_t *payload,
                                  uint64_t staging_cap, uint32_t *rec_status,
                                  uint32_t n_status, int threads) {
   if (!chunk_ok(chunk_bytes) || (kind != 0 && kind != 1)) return ORC_V_HEADER;
-  if (codec != 1 && !(codec == 2 && chunk_bytes == 65536)) return ORC_V_HEADER;
+  if (codec != 1 && !(codec == 2 && chunk_bytes >= ORC_TILE)) return ORC_V_HEADER;
   uint64_t n_chunks = n_chunks_of(nbytes, chunk_bytes);
+  uint32_t u = unit_of(chunk_bytes);
+  uint64_t per = chunk_bytes / u, n_units = n_chunks_of(nbytes, u);
 
   /* header */
   if (cap < 64) return ORC_V_HEADER;
@@ -904,12 +930,12 @@ uint32_t orc_decode_verify_codec(int kind, int codec, const uint8_t *payload,
   uint32_t n_rec = get_u32(h + 24), flags = get_u32(h + 28);
   uint64_t payload_bytes = get_u64(h + 32);
   if ((flags & ~1u) || !all_zero(h + 48, 12)) return ORC_V_HEADER;
-  if (n_rec > n_chunks) return ORC_V_HEADER;
+  if (n_rec > n_units) return ORC_V_HEADER;
   if (64 + 16 * (uint64_t)n_rec > payload_bytes || payload_bytes > cap ||
       payload_bytes % 16)
     return ORC_V_HEADER;
-  if ((flags & 1u) && n_rec != n_chunks) return ORC_V_HEADER;
-  if ((uint64_t)n_rec * chunk_bytes > staging_cap) return ORC_V_STAGING;
+  if ((flags & 1u) && n_rec != n_units) return ORC_V_HEADER;
+  if ((uint64_t)n_rec * u > staging_cap) return ORC_V_STAGING;
 
   /* table: the last 16*n_records bytes of the payload */
   uint64_t table = payload_bytes - 16 * (uint64_t)n_rec;
@@ -922,16 +948,23 @@ uint32_t orc_decode_verify_codec(int kind, int codec, const uint8_t *payload,
     uint64_t off = get_u64(t + 16 * (uint64_t)r + 8);
     uint64_t end =
         r + 1 < n_rec ? get_u64(t + 16 * (uint64_t)(r + 1) + 8) : table;
-    if (c >= n_chunks) return ORC_V_TABLE;
+    if (c >= n_units) return ORC_V_TABLE;
     if (r && c <= get_u32(t + 16 * (uint64_t)(r - 1))) return ORC_V_TABLE;
     if (r == 0 && off != 64) return ORC_V_TABLE;
     if (off % 16 || off >= end) return ORC_V_TABLE;
+    /* whole chunks: a tile other than its chunk's first comes right after
+     * the tile before it, and one other than its chunk's last (and not the
+     * state's last) right before the tile after it */
+    if (c % per && (r == 0 || get_u32(t + 16 * (uint64_t)(r - 1)) != c - 1))
+      return ORC_V_TABLE;
+    if ((c + 1) % per && c + 1 < n_units &&
+        (r + 1 == n_rec || get_u32(t + 16 * (uint64_t)(r + 1)) != c + 1))
+      return ORC_V_TABLE;
   }
 
   /* records */
   uint32_t *status = (uint32_t *)calloc(n_rec ? n_rec : 1, 4);
-  de_ctx x = {kind,  codec,   payload, table, nbytes,
-              chunk_bytes, n_rec, staging, status};
+  de_ctx x = {kind, codec, payload, table, nbytes, u, n_rec, staging, status};
   parallel_for(n_rec, threads, de_range, &x);
   uint32_t verdict = 0;
   for (uint32_t r = 0; r < n_rec; r++) {
@@ -946,13 +979,12 @@ int orc_commit(uint8_t *live, uint64_t nbytes, uint32_t chunk_bytes,
                const uint8_t *staging, const uint8_t *payload,
                uint32_t verdict) {
   if (verdict != 0) return 1;
+  uint32_t u = unit_of(chunk_bytes);
   uint32_t n_rec = get_u32(payload + 24);
   uint64_t table = get_u64(payload + 32) - 16 * (uint64_t)n_rec;
   for (uint32_t r = 0; r < n_rec; r++) {
     uint32_t c = get_u32(payload + table + 16 * (uint64_t)r);
-    memcpy(live + (uint64_t)c * chunk_bytes,
-           staging + (uint64_t)r * chunk_bytes,
-           chunk_len(nbytes, chunk_bytes, c));
+    memcpy(live + (uint64_t)c * u, staging + (uint64_t)r * u, chunk_len(nbytes, u, c));
   }
   return 0;
 }
@@ -968,6 +1000,7 @@ uint32_t orc_commit_reverify(int kind, uint8_t *live, uint64_t nbytes,
                              uint32_t chunk_bytes, const uint8_t *staging,
                              const uint8_t *payload, uint32_t verdict) {
   if (verdict != 0) return verdict;
+  uint32_t u = unit_of(chunk_bytes);
   uint32_t n_rec = get_u32(payload + 24);
   uint64_t table = get_u64(payload + 32) - 16 * (uint64_t)n_rec;
   int bad = 0;
@@ -977,10 +1010,10 @@ uint32_t orc_commit_reverify(int kind, uint8_t *live, uint64_t nbytes,
   for (uint32_t r = 0; r < n_rec; r++) {
     uint32_t c = get_u32(payload + table + 16 * (uint64_t)r);
     uint32_t receipt = get_u32(payload + table + 16 * (uint64_t)r + 4);
-    uint32_t len = chunk_len(nbytes, chunk_bytes, c);
-    const uint8_t *src = staging + (uint64_t)r * chunk_bytes;
+    uint32_t len = chunk_len(nbytes, u, c);
+    const uint8_t *src = staging + (uint64_t)r * u;
     if (orc_crc(kind, src, len) != receipt) bad = 1;
-    memcpy(result + (uint64_t)c * chunk_bytes, src, len);
+    memcpy(result + (uint64_t)c * u, src, len);
   }
   if (orc_crc(kind, result, nbytes) != get_u32(payload + 40)) bad = 1;
   if (!bad) memcpy(live, result, nbytes);

@@ -72,9 +72,10 @@ uint32_t orc_diff_dirty(const uint8_t *cur, const uint8_t *prev,
                         uint64_t nbytes, uint32_t chunk_bytes,
                         uint32_t *idx_out, int threads);
 
-/* Upper bound on the payload size for n_records records. */
+/* Upper bound on the payload size when n_ship chunks are shipped (each
+ * chunk above 64 KiB as its 64 KiB tiles, one record per tile). */
 uint64_t orc_payload_bound(uint64_t nbytes, uint32_t chunk_bytes,
-                           uint32_t n_records);
+                           uint32_t n_ship);
 
 /* Encode the chunks listed in idx (ascending; idx == NULL means every chunk,
  * which also sets the FULL flag) into payload.  Returns payload bytes, or
@@ -83,7 +84,7 @@ int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
                    uint32_t chunk_bytes, const uint32_t *idx, uint32_t n_idx,
                    uint8_t *payload, uint64_t cap, int threads);
 
-/* Format v2 (codec 2, 64 KiB chunks only): as orc_encode with records RAW
+/* Format v2 (codec 2, chunks of 64 KiB or more): as orc_encode with records RAW
  * or HUF (per-chunk canonical Huffman codes of the exponents in 512 streams).
  * orc_encode is orc_encode_codec with codec 1. */
 #define ORC_HUF_MAX_LEN 11u
@@ -108,7 +109,8 @@ int orc_plan_chunk(const uint8_t *chunk, uint32_t len, uint32_t *mode,
                    uint32_t *k, uint32_t *base, uint32_t *n_esc,
                    uint64_t *size);
 
-/* Validate and decode a payload into staging (record i at i*chunk_bytes).
+/* Validate and decode a payload into staging (record i at i*unit, the unit
+ * being the chunk up to 64 KiB and a 64 KiB tile of a larger chunk).
  * rec_status (may be NULL) receives 0, ORC_V_RECORD or ORC_V_DATA per
  * record when the header and table are valid.  Returns the verdict. */
 uint32_t orc_decode_verify(int kind, const uint8_t *payload, uint64_t cap,
@@ -124,7 +126,7 @@ uint32_t orc_decode_verify_codec(int kind, int codec, const uint8_t *payload,
                                  uint64_t staging_cap, uint32_t *rec_status,
                                  uint32_t n_status, int threads);
 
-/* Install: verdict 0 copies each staged record to its chunk of live and
+/* Install: verdict 0 copies each staged record to its unit of live and
  * returns 0; any other verdict leaves live untouched and returns 1. */
 int orc_commit(uint8_t *live, uint64_t nbytes, uint32_t chunk_bytes,
                const uint8_t *staging, const uint8_t *payload,
