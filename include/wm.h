@@ -36,8 +36,14 @@
  *     sessions on disjoint CU slices run side by side.
  *   - All functions are thread-safe.  The first call on a device uploads the
  *     library's constant CRC tables to it (wm_init does this eagerly).
- *   - The kernels support chunk_bytes == 65536 only; other values return
- *     WM_ERR_UNSUPPORTED.
+ *   - Chunk sizes: chunk_bytes is a power of two in [4 KiB, 16 MiB]; the
+ *     kernels take 64 KiB and above (smaller sizes return
+ *     WM_ERR_UNSUPPORTED).  A chunk is the unit of dirtiness and of the
+ *     per-chunk CRCs; a chunk above 64 KiB (the paper's pre-copy unit is
+ *     4 MB, §6.2 Exhibit 2, App. H) is shipped as its 64 KiB tiles, one
+ *     record and one receipt per tile, so "record" below means a 64 KiB
+ *     unit: the chunk itself at 64 KiB, else one tile of it.  A table that
+ *     ships only part of a chunk is rejected (WM_V_TABLE).
  */
 #ifndef WM_H
 #define WM_H
@@ -88,7 +94,7 @@ typedef int32_t wm_status;
 #define WM_COMMIT_SCATTER 1 /* copy each staged record into its chunk of live */
 
 typedef struct wm_params {
-  uint32_t chunk_bytes; /* bytes per chunk; 65536 */
+  uint32_t chunk_bytes; /* bytes per chunk: a power of two, 64 KiB..16 MiB */
   uint32_t crc_kind;    /* WM_CRC32_ZLIB or WM_CRC32C */
   uint32_t codec;       /* WM_CODEC_EXPFOR or WM_CODEC_EXPHUF */
   uint32_t flags;       /* must be 0 */
@@ -107,8 +113,9 @@ wm_status wm_init(int device);
  * list).  0 if p is invalid. */
 uint64_t wm_workspace_bytes(uint64_t nbytes, const wm_params *p);
 
-/* Largest payload that n_records records of a state of nbytes can produce
- * (header + every record RAW + table).  0 if p is invalid. */
+/* Largest payload that shipping n_records chunks of a state of nbytes can
+ * produce (header + every record RAW + table; a chunk above 64 KiB counts
+ * as its tiles).  0 if p is invalid. */
 uint64_t wm_payload_bound(uint64_t nbytes, uint32_t n_records,
                           const wm_params *p);
 
@@ -153,7 +160,10 @@ wm_status wm_diff_dirty(const void *cur, const void *prev, uint64_t nbytes,
  *                the encoding pass when idx is NULL; with a list, every
  *                chunk is checksummed first (the global CRC covers the
  *                whole state, listed or not) and the workspace holds the
- *                CRCs
+ *                CRCs.  Chunks above 64 KiB: the receipts are tile CRCs,
+ *                which chunk CRCs cannot give, so they are computed within
+ *                the call whether crc is given or not; a given crc then
+ *                serves only a list's global CRC
  *   payload    : payload_cap bytes, 16-byte aligned; payload_cap must be at
  *                least wm_payload_bound(nbytes, n_chunks, p)
  *   payload_bytes : 1 u64, the payload size written
@@ -173,6 +183,9 @@ wm_status wm_encode(const void *state, uint64_t nbytes, const wm_params *p,
  *   crc_out    : n_chunks u32, or NULL
  *   global_crc : 1 u32, or NULL
  *   dirty_idx  : n_chunks u32, or NULL;  n_dirty : 1 u32, or NULL
+ * Chunks above 64 KiB: a chunk is dirty when any of its tiles differs and
+ * then ships whole, so with prev the call runs the diff, a checksum of every
+ * tile and the list encoder (same outputs, more reads) instead of one pass.
  * Other arguments as wm_encode. */
 wm_status wm_encode_step(const void *cur, const void *prev, uint64_t nbytes,
                          const wm_params *p, uint32_t *crc_out,
@@ -188,7 +201,7 @@ wm_status wm_encode_step(const void *cur, const void *prev, uint64_t nbytes,
  * on the device.
  *   Limit: states of at most 65,536 chunks (4 GiB in 64 KiB chunks); a larger
  *   state returns WM_ERR_WORKSPACE before anything is enqueued.  Format v1
- *   only (format v2 returns WM_ERR_UNSUPPORTED).
+ *   and 64 KiB chunks only (anything else returns WM_ERR_UNSUPPORTED).
  *   Sharing: each device holds one built-in workspace (2 MiB + 256 B, kept
  *   until the process ends) used by every call of this function on that
  *   device, whatever the stream.  Calls that overlap in time on one device
@@ -209,11 +222,11 @@ wm_status wm_encode_step_static(const void *cur, const void *prev,
  * payload_cap).
  *   nbytes     : the receiver's state size (must match the header)
  *   staging    : staging_cap bytes, 16-byte aligned; record i is decoded to
- *                staging + i*chunk_bytes (a full ship's staging is therefore
- *                the shadow copy of the state)
+ *                staging + i*65536 (a full ship's staging is therefore the
+ *                shadow copy of the state)
  *   verdict    : 1 u32, 0 when every check passed, else WM_V_* bits
- *   rec_status : n_chunks u32 (0, WM_V_RECORD or WM_V_DATA per record when
- *                header and table are valid), or NULL
+ *   rec_status : ceil(nbytes / 65536) u32 (0, WM_V_RECORD or WM_V_DATA per
+ *                record when header and table are valid), or NULL
  * After a nonzero verdict the staging contents are unspecified. */
 wm_status wm_decode_verify(const void *payload, uint64_t payload_cap,
                            uint64_t nbytes, const wm_params *p, void *staging,
@@ -358,10 +371,10 @@ typedef struct {
   void *payload;            /* payload_cap >= wm_payload_bound(nbytes, n) */
   uint64_t payload_cap;
   uint64_t *payload_bytes;  /* 1 u64 */
-  void *staging;            /* staging_cap >= n * chunk_bytes */
+  void *staging;            /* staging_cap >= ceil(nbytes / 65536) * 65536 */
   uint64_t staging_cap;
   uint32_t *verdict;        /* 1 u32 */
-  uint32_t *rec_status;     /* n u32 or NULL */
+  uint32_t *rec_status;     /* ceil(nbytes / 65536) u32 or NULL */
   void *ws_src;             /* wm_workspace_bytes() each; two different */
   uint64_t ws_src_bytes;
   void *ws_dst;
@@ -389,7 +402,8 @@ typedef struct {
  *              checksums and encodes only the dirty chunks (each record's
  *              receipt and bytes from one read), and the header's global CRC
  *              combines kept and new CRCs.  After a round that did not return
- *              WM_OK, pass 0.
+ *              WM_OK, pass 0.  Chunks above 64 KiB: ignored (the kept chunk
+ *              CRCs cannot give the tile receipts; every tile is checksummed).
  * Errors: those of the four calls it makes (WM_ERR_INVALID_ARG for a
  *         missing buffer, WM_ERR_CAPACITY for a short payload or staging,
  *         WM_ERR_WORKSPACE, WM_ERR_HIP). */

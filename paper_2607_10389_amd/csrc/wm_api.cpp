@@ -83,7 +83,7 @@ wm_status check_params(const wm_params *p) {
   uint32_t c = p->chunk_bytes;
   bool pow2 = c >= 4096u && c <= (16u << 20) && (c & (c - 1)) == 0;
   if (!pow2) return WM_ERR_INVALID_ARG;
-  if (c != kChunk) return WM_ERR_UNSUPPORTED;
+  if (c < kChunk) return WM_ERR_UNSUPPORTED;  // the kernels' unit is 64 KiB
   return WM_OK;
 }
 
@@ -96,6 +96,8 @@ wm_status make_geom(uint64_t nbytes, const wm_params *p, ChunkGeom *g, bool cach
   if (n >= (1ull << 24)) return WM_ERR_INVALID_ARG;  // look-back field width
   g->nbytes = nbytes;
   g->n_chunks = (uint32_t)n;
+  g->tile_log2 = (uint32_t)__builtin_ctz(p->chunk_bytes) - 16u;
+  g->hdr_n = (uint32_t)((nbytes + p->chunk_bytes - 1) / p->chunk_bytes);
   g->tail_len = n ? (uint32_t)(nbytes - (n - 1) * kChunk) : kChunk;
   g->crc_kind = p->crc_kind;
   g->codec = p->codec;
@@ -144,11 +146,108 @@ uint64_t plans_offset(const WsLayout &L) { return (L.total + 255u) & ~255ull; }
 uint64_t list_offset(const WsLayout &L, uint32_t n_chunks) {
   return (plans_offset(L) + (uint64_t)kHufPlanBytes * n_chunks + 255u) & ~255ull;
 }
-uint64_t ws_need(const WsLayout &L, uint32_t n_chunks, uint32_t codec) {
+uint64_t ws_base(const WsLayout &L, uint32_t n_chunks, uint32_t codec) {
   return codec == WM_CODEC_EXPHUF ? list_offset(L, n_chunks) + 4ull * n_chunks + 16u : L.total;
+}
+// Chunks above 64 KiB also keep, after that, the tile list of a chunk list
+// with its length, and a chunk list with its length.
+uint64_t tiles_offset(const WsLayout &L, uint32_t n_units, uint32_t codec) {
+  return (ws_base(L, n_units, codec) + 255u) & ~255ull;
+}
+uint64_t ws_need(const ChunkGeom &g, const WsLayout &L) {
+  if (!g.tile_log2) return ws_base(L, g.n_chunks, g.codec);
+  return tiles_offset(L, g.n_chunks, g.codec) + 4ull * (g.n_chunks + g.hdr_n) + 32u;
+}
+struct TileLists {
+  uint32_t *tiles, *n_tiles, *chunks, *n_chunks;
+};
+TileLists tile_lists(void *ws, const ChunkGeom &g, const WsLayout &L) {
+  uint32_t *t = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) +
+                                             tiles_offset(L, g.n_chunks, g.codec));
+  TileLists r;
+  r.tiles = t;
+  r.n_tiles = t + g.n_chunks;
+  r.chunks = t + g.n_chunks + 4;
+  r.n_chunks = r.chunks + g.hdr_n;
+  return r;
 }
 
 wm_status hip_status(int e) { return e == 0 ? WM_OK : WM_ERR_HIP; }
+
+// wm_encode for chunks above 64 KiB: the records are the listed chunks'
+// tiles, so a chunk list is expanded to its tiles first.  Receipts are tile
+// CRCs, which the caller's chunk CRCs cannot give: they are computed in the
+// encoding pass (format v1) or by a checksum of every tile first (format v2,
+// and format v1 with a list and no CRCs, whose global CRC covers unlisted
+// chunks too).  With a list and the caller's CRCs, the global CRC combines
+// those.
+wm_status encode_tiles(const void *state, const ChunkGeom &g, const uint32_t *idx,
+                       const uint32_t *n_idx, const uint32_t *crc, void *payload,
+                       uint64_t *payload_bytes, void *ws, const WsLayout &L, int n_cu,
+                       void *stream) {
+  uint8_t *wsb = static_cast<uint8_t *>(ws);
+  uint32_t *unit_crc = reinterpret_cast<uint32_t *>(wsb + L.flags);
+  const TileLists t = tile_lists(ws, g, L);
+  if (idx && launch_expand_list(idx, n_idx, g, t.tiles, t.n_tiles, stream) != 0) return WM_ERR_HIP;
+  const uint32_t *ul = idx ? t.tiles : nullptr, *un = idx ? t.n_tiles : nullptr;
+  if (g.codec == WM_CODEC_EXPHUF)
+    return hip_status(launch_encode_v2(state, g, ul, un, nullptr, unit_crc, nullptr, payload,
+                                       payload_bytes, ws, L, wsb + plans_offset(L), n_cu,
+                                       stream));
+  if (!idx)
+    return hip_status(launch_encode(1, state, nullptr, g, nullptr, nullptr, nullptr, unit_crc,
+                                    nullptr, nullptr, nullptr, payload, payload_bytes, ws, L,
+                                    n_cu, stream));
+  if (!crc) {
+    if (launch_checksum(state, g, unit_crc, nullptr, n_cu, stream, true) != 0) return WM_ERR_HIP;
+    return hip_status(launch_encode(0, state, nullptr, g, ul, un, unit_crc, nullptr, nullptr,
+                                    nullptr, nullptr, payload, payload_bytes, ws, L, n_cu,
+                                    stream));
+  }
+  return hip_status(launch_encode(0, state, nullptr, g, ul, un, nullptr, unit_crc, nullptr,
+                                  nullptr, nullptr, payload, payload_bytes, ws, L, n_cu, stream,
+                                  crc));
+}
+
+// wm_encode_step for chunks above 64 KiB: dirtiness is the chunk's (any
+// tile differs), so there is no single pass; the diff gives the dirty chunk
+// list, every tile is checksummed (chunk CRCs fold from tile CRCs, and the
+// global CRC covers every tile), and the list encoder ships the dirty
+// chunks' tiles.  Without prev every chunk ships from one encoding pass.
+wm_status encode_step_tiles(const void *cur, const void *prev, const ChunkGeom &g,
+                            uint32_t *crc_out, uint32_t *global_crc, uint32_t *dirty_idx,
+                            uint32_t *n_dirty, void *payload, uint64_t *payload_bytes, void *ws,
+                            const WsLayout &L, int n_cu, void *stream) {
+  uint8_t *wsb = static_cast<uint8_t *>(ws);
+  uint32_t *unit_crc = reinterpret_cast<uint32_t *>(wsb + L.flags);
+  const TileLists t = tile_lists(ws, g, L);
+  if (!prev) {
+    int rc = g.codec == WM_CODEC_EXPHUF
+                 ? launch_encode_v2(cur, g, nullptr, nullptr, nullptr, unit_crc, global_crc,
+                                    payload, payload_bytes, ws, L, wsb + plans_offset(L), n_cu,
+                                    stream)
+                 : launch_encode(1, cur, nullptr, g, nullptr, nullptr, nullptr, unit_crc,
+                                 global_crc, nullptr, nullptr, payload, payload_bytes, ws, L,
+                                 n_cu, stream);
+    if (rc == 0 && crc_out) rc = launch_fold_tiles(unit_crc, g, crc_out, stream);
+    if (rc == 0 && (dirty_idx || n_dirty)) rc = launch_fill_all(dirty_idx, n_dirty, g.hdr_n, stream);
+    return hip_status(rc);
+  }
+  uint32_t *list = dirty_idx ? dirty_idx : t.chunks;
+  uint32_t *n_list = n_dirty ? n_dirty : t.n_chunks;
+  if (launch_diff(cur, prev, g, list, n_list, ws, L, stream) != 0 ||
+      launch_expand_list(list, n_list, g, t.tiles, t.n_tiles, stream) != 0 ||
+      launch_checksum(cur, g, unit_crc, nullptr, n_cu, stream, true) != 0 ||
+      (crc_out && launch_fold_tiles(unit_crc, g, crc_out, stream) != 0))
+    return WM_ERR_HIP;
+  if (g.codec == WM_CODEC_EXPHUF)
+    return hip_status(launch_encode_v2(cur, g, t.tiles, t.n_tiles, unit_crc, nullptr, global_crc,
+                                       payload, payload_bytes, ws, L, wsb + plans_offset(L), n_cu,
+                                       stream));
+  return hip_status(launch_encode(0, cur, nullptr, g, t.tiles, t.n_tiles, unit_crc, nullptr,
+                                  global_crc, nullptr, nullptr, payload, payload_bytes, ws, L,
+                                  n_cu, stream));
+}
 
 }  // namespace
 
@@ -175,17 +274,17 @@ wm_status wm_init(int device) {
 
 uint64_t wm_workspace_bytes(uint64_t nbytes, const wm_params *p) {
   ChunkGeom g;
-  if (check_params(p) != WM_OK) return 0;
-  uint64_t n = (nbytes + p->chunk_bytes - 1) / p->chunk_bytes;
-  if (n >= (1ull << 24)) return 0;
-  (void)g;
-  return ws_need(ws_layout((uint32_t)n), (uint32_t)n, p->codec);
+  if (make_geom(nbytes, p, &g, false) != WM_OK) return 0;
+  return ws_need(g, ws_layout(g.n_chunks));
 }
 
 uint64_t wm_payload_bound(uint64_t nbytes, uint32_t n_records, const wm_params *p) {
   (void)nbytes;
   if (check_params(p) != WM_OK) return 0;
-  return 64u + 16ull * n_records + (uint64_t)n_records * (16u + p->chunk_bytes);
+  // every record RAW: a chunk above 64 KiB ships as its 64 KiB tiles, one
+  // record (16-byte header + body) and one table entry each
+  const uint64_t units = (uint64_t)n_records * (p->chunk_bytes / kChunk);
+  return 64u + units * (32u + kChunk);
 }
 
 wm_status wm_checksum_chunks(const void *data, uint64_t nbytes, const wm_params *p,
@@ -229,12 +328,14 @@ wm_status wm_encode(const void *state, uint64_t nbytes, const wm_params *p, cons
   if ((nbytes && !state) || !aligned16(state)) return WM_ERR_INVALID_ARG;
   if ((idx == nullptr) != (n_idx == nullptr)) return WM_ERR_INVALID_ARG;
   if (!payload || !payload_bytes || !aligned16(payload)) return WM_ERR_INVALID_ARG;
-  if (payload_cap < wm_payload_bound(nbytes, g.n_chunks, p)) return WM_ERR_CAPACITY;
+  if (payload_cap < wm_payload_bound(nbytes, g.hdr_n, p)) return WM_ERR_CAPACITY;
   WsLayout L = ws_layout(g.n_chunks);
-  if (!ws || ws_bytes < ws_need(L, g.n_chunks, g.codec) || !aligned16(ws)) return WM_ERR_WORKSPACE;
+  if (!ws || ws_bytes < ws_need(g, L) || !aligned16(ws)) return WM_ERR_WORKSPACE;
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
   n_cu = stream_cus(stream, n_cu);
+  if (g.tile_log2) return encode_tiles(state, g, idx, n_idx, crc, payload, payload_bytes, ws, L,
+                                       n_cu, stream);
   uint32_t *crc_scratch =
       crc ? nullptr : reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + L.flags);
   if (g.codec == WM_CODEC_EXPHUF)
@@ -269,12 +370,12 @@ wm_status encode_step_call(const void *cur, const void *prev, uint64_t nbytes,
   ChunkGeom g;
   wm_status s = make_geom(nbytes, p, &g, !builtin);
   if (s != WM_OK) return s;
-  // the built-in workspace has the format v1 layout only
-  if (builtin && g.codec != WM_CODEC_EXPFOR) return WM_ERR_UNSUPPORTED;
+  // the built-in workspace has the format v1, 64 KiB chunk layout only
+  if (builtin && (g.codec != WM_CODEC_EXPFOR || g.tile_log2)) return WM_ERR_UNSUPPORTED;
   if (nbytes & 1u) return WM_ERR_INVALID_ARG;
   if ((nbytes && !cur) || !aligned16(cur) || !aligned16(prev)) return WM_ERR_INVALID_ARG;
   if (!payload || !payload_bytes || !aligned16(payload)) return WM_ERR_INVALID_ARG;
-  if (payload_cap < wm_payload_bound(nbytes, g.n_chunks, p)) return WM_ERR_CAPACITY;
+  if (payload_cap < wm_payload_bound(nbytes, g.hdr_n, p)) return WM_ERR_CAPACITY;
   WsLayout L = ws_layout(g.n_chunks);
   int n_cu = 0;
   if (builtin) {
@@ -283,11 +384,13 @@ wm_status encode_step_call(const void *cur, const void *prev, uint64_t nbytes,
     if ((s = ensure_device(&n_cu, &ws, &ws_bytes)) != WM_OK) return s;
     if (L.total > ws_bytes) return WM_ERR_WORKSPACE;
   } else {
-    if (!ws || ws_bytes < ws_need(L, g.n_chunks, g.codec) || !aligned16(ws))
-      return WM_ERR_WORKSPACE;
+    if (!ws || ws_bytes < ws_need(g, L) || !aligned16(ws)) return WM_ERR_WORKSPACE;
     if ((s = ensure_device(&n_cu)) != WM_OK) return s;
   }
   n_cu = stream_cus(stream, n_cu);
+  if (g.tile_log2)
+    return encode_step_tiles(cur, prev, g, crc_out, global_crc, dirty_idx, n_dirty, payload,
+                             payload_bytes, ws, L, n_cu, stream);
   uint8_t *wsb = static_cast<uint8_t *>(ws);
   uint32_t *crcs = crc_out ? crc_out : reinterpret_cast<uint32_t *>(wsb + L.flags);
   if (g.codec == WM_CODEC_EXPHUF) {
@@ -521,17 +624,18 @@ wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t 
   // argument error leaves everything untouched
   if (!b->payload || !b->payload_bytes || !aligned16(b->payload) || !aligned16(cur))
     return WM_ERR_INVALID_ARG;
-  if (b->payload_cap < wm_payload_bound(nbytes, g.n_chunks, p)) return WM_ERR_CAPACITY;
-  if (!b->ws_src || !aligned16(b->ws_src) ||
-      b->ws_src_bytes < ws_need(ws_layout(g.n_chunks), g.n_chunks, g.codec))
+  if (b->payload_cap < wm_payload_bound(nbytes, g.hdr_n, p)) return WM_ERR_CAPACITY;
+  if (!b->ws_src || !aligned16(b->ws_src) || b->ws_src_bytes < ws_need(g, ws_layout(g.n_chunks)))
     return WM_ERR_WORKSPACE;
   if (!b->verdict || (nbytes && !b->staging) || !aligned16(b->staging)) return WM_ERR_INVALID_ARG;
   if (b->staging_cap < (uint64_t)g.n_chunks * kChunk) return WM_ERR_CAPACITY;
   const uint64_t ws_need = ws_layout(g.n_chunks).total;
   if (!b->ws_dst || !aligned16(b->ws_dst) || b->ws_dst_bytes < ws_need || b->ws_src == b->ws_dst)
     return WM_ERR_WORKSPACE;
-  if (!crc_valid) {
-    // every chunk checksummed, the dirty ones encoded, in one pass
+  if (!crc_valid || g.tile_log2) {
+    // every chunk checksummed, the dirty ones encoded, in one pass (chunks
+    // above 64 KiB: the kept CRCs are chunk CRCs, not the tile receipts the
+    // records need, so every tile is checksummed)
     s = wm_encode_step(cur, shipped, nbytes, p, b->crc, b->global_crc, b->dirty_idx, b->n_dirty,
                        b->payload, b->payload_cap, b->payload_bytes, b->ws_src, b->ws_src_bytes,
                        stream);

@@ -47,16 +47,25 @@ void shift_matrix(uint32_t poly, int64_t m, uint32_t cols[32]);
 uint32_t shift_apply(uint32_t poly, int64_t m, uint32_t v);
 uint32_t poly_of(uint32_t crc_kind);
 
-// Per-call parameters passed by value to every kernel.
+// Per-call parameters passed by value to every kernel.  The kernels work on
+// 64 KiB units: a chunk of at most 64 KiB, or a 64 KiB tile of a larger
+// chunk (the payload then holds one record and one receipt per tile, and a
+// table ships every tile of each chunk it lists).  n_chunks, tail_len and
+// the tail shift describe the units; tile_log2 and hdr_n the caller's
+// chunks.
 struct ChunkGeom {
   uint64_t nbytes;      // state bytes
-  uint32_t n_chunks;    // ceil(nbytes / kChunk)
-  uint32_t tail_len;    // length of the last chunk (kChunk if full)
+  uint32_t n_chunks;    // units: ceil(nbytes / kChunk)
+  uint32_t tail_len;    // length of the last unit (kChunk if full)
   uint32_t crc_kind;
   uint32_t codec;       // payload format: 1 (v1) or 2 (v2, Huffman exponents)
   uint32_t k_tail;      // F^tail_len(~0) ^ ~0
   uint32_t tail_mat[32];// F^-(kChunk - tail_len), columns
+  uint32_t tile_log2;   // log2(chunk_bytes / kChunk): 0 for 64 KiB chunks
+  uint32_t hdr_n;       // chunks: ceil(nbytes / chunk_bytes)
 };
+// Bytes of the caller's chunk.
+inline uint32_t geom_chunk_bytes(const ChunkGeom &g) { return kChunk << g.tile_log2; }
 
 // Workspace layout (bytes from the workspace base).
 struct WsLayout {
@@ -87,19 +96,31 @@ static_assert(sizeof(WsCtl) == 256, "control block is 256 bytes");
 
 // Kernel launchers (wm_kernels.hip).  All return a hipError_t as int.
 int upload_tables(int device, const CrcTables tabs[2]);
+// CRC of each of the caller's chunks (hdr_n of them), or with `units` of
+// each 64 KiB unit (n_chunks); the global CRC from them.
 int launch_checksum(const void *data, const ChunkGeom &g, uint32_t *crc_out,
-                    uint32_t *global_crc, int n_cu, void *stream);
+                    uint32_t *global_crc, int n_cu, void *stream, bool units = false);
+// Dirty chunks (the caller's chunks: one is dirty when any of its tiles is).
 int launch_diff(const void *cur, const void *prev, const ChunkGeom &g,
                 uint32_t *dirty_idx, uint32_t *n_dirty, void *ws,
                 const WsLayout &L, void *stream);
-// mode: 0 = list (idx/n_idx), 1 = all chunks, 2 = step (prev may be NULL)
+// Chunks above 64 KiB: a device list of the caller's chunks as the list of
+// their tiles (an invalid list as an over-long one), and chunk CRCs from
+// tile CRCs.
+int launch_expand_list(const uint32_t *idx, const uint32_t *n_idx, const ChunkGeom &g,
+                       uint32_t *out, uint32_t *n_out, void *stream);
+int launch_fold_tiles(const uint32_t *tile_crc, const ChunkGeom &g, uint32_t *out, void *stream);
+// mode: 0 = list (idx/n_idx), 1 = all chunks, 2 = step (prev may be NULL);
+// the encoder works on units (idx lists units, CRCs are units').  The
+// header's global CRC combines the unit CRCs (crc_in, else crc_out), or
+// global_from: the caller's chunk CRCs.
 int launch_encode(int mode, const void *cur, const void *prev,
                   const ChunkGeom &g, const uint32_t *idx,
                   const uint32_t *n_idx, const uint32_t *crc_in,
                   uint32_t *crc_out, uint32_t *global_crc,
                   uint32_t *dirty_idx, uint32_t *n_dirty, void *payload,
                   uint64_t *payload_bytes, void *ws, const WsLayout &L,
-                  int n_cu, void *stream);
+                  int n_cu, void *stream, const uint32_t *global_from = nullptr);
 int launch_decode(const void *payload, uint64_t payload_cap,
                   const ChunkGeom &g, void *staging, uint64_t staging_cap,
                   uint32_t *verdict, uint32_t *rec_status, void *ws,

@@ -385,9 +385,12 @@ __device__ __forceinline__ uint32_t *chk_u(uint32_t b) {
 // Chunk CRCs: the eight data waves take chunk i's lane values while chunk
 // i+1 loads; the ninth wave folds chunk i-1's values into its CRC (the
 // Horner step over waves, then the lane shifts and their XOR).
+// With `per_chunk` and chunks above 64 KiB, each tile's CRC is shifted past
+// the rest of its chunk and XORed into its chunk's entry (zeroed before the
+// launch): CRC(A|B) = F^|B|(CRC(A)) ^ CRC(B) is linear in the pieces' CRCs.
 __global__ __launch_bounds__(kThreads + 64) void k_checksum(
     const uint8_t *__restrict__ data, ChunkGeom g,
-    uint32_t *__restrict__ crc_out) {
+    uint32_t *__restrict__ crc_out, uint32_t per_chunk) {
   load_crc_tables(g.crc_kind);
   __syncthreads();
   const CrcTables &T = g_tables[g.crc_kind];
@@ -419,7 +422,15 @@ __global__ __launch_bounds__(kThreads + 64) void k_checksum(
 #pragma unroll
       for (int w = 1; w < kWaves; ++w) acc = tab4x(kLdsWaveStep, acc, u[w * 64 + l.lane]);
       const uint32_t crc = finish_crc(lane_fold(acc), chunk_len(g, c), g, T);
-      if (l.lane == 0) crc_out[c] = crc;
+      if (per_chunk && g.tile_log2) {
+        const uint32_t big = c >> g.tile_log2;
+        const uint64_t big_end = min((uint64_t)(big + 1) << (16 + g.tile_log2), g.nbytes);
+        const uint64_t tile_end = min((uint64_t)(c + 1) * kChunk, g.nbytes);
+        const uint32_t part = shift_bytes(T, big_end - tile_end, crc);
+        if (l.lane == 0) atomicXor(&crc_out[big], part);
+      } else if (l.lane == 0) {
+        crc_out[c] = crc;
+      }
     }
     __syncthreads();
   }
@@ -593,9 +604,12 @@ __global__ __launch_bounds__(256) void k_diff(const uint8_t *__restrict__ cur,
   }
 }
 
-// Single-workgroup stream compaction of flags into ascending indices.
+// Single-workgroup stream compaction of flags into ascending indices.  Item
+// i is set when any of flags[i << log2per .. (i + 1) << log2per) (below
+// n_flags) is: chunks above 64 KiB from their tiles' flags.
 __global__ __launch_bounds__(1024) void k_compact(const uint32_t *__restrict__ flags,
-                                                  uint32_t n,
+                                                  uint32_t n, uint32_t log2per,
+                                                  uint32_t n_flags,
                                                   uint32_t *__restrict__ idx,
                                                   uint32_t *__restrict__ count) {
   __shared__ uint32_t wsum[16];
@@ -605,7 +619,11 @@ __global__ __launch_bounds__(1024) void k_compact(const uint32_t *__restrict__ f
   uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
   for (uint32_t base = 0; base < n; base += 1024u) {
     uint32_t i = base + threadIdx.x;
-    bool f = i < n && flags[i];
+    bool f = false;
+    if (i < n) {
+      const uint32_t t0 = i << log2per, t1 = min((i + 1) << log2per, n_flags);
+      for (uint32_t t = t0; t < t1 && !f; ++t) f = flags[t] != 0;
+    }
     unsigned long long m = __ballot(f);
     uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
                                                __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
@@ -1447,8 +1465,8 @@ __global__ __launch_bounds__(256) void k_encode_finish(
     uint32_t h[16];
     h[0] = g.codec == 2 ? 0x32564D57u : 0x31564D57u;  // "WMV2" / "WMV1"
     h[1] = g.codec | (g.crc_kind << 16) | (g.codec << 24);
-    h[2] = kChunk;
-    h[3] = g.n_chunks;
+    h[2] = kChunk << g.tile_log2;  // the caller's chunk size and count
+    h[3] = g.hdr_n;
     h[4] = (uint32_t)g.nbytes;
     h[5] = (uint32_t)(g.nbytes >> 32);
     h[6] = n_rec;
@@ -1501,7 +1519,7 @@ __global__ __launch_bounds__(64) void k_decode_prepare(
   if (header_crc60(hw, t1) != ld_u32(payload + 60)) return;
   if (ld_u32(payload) != (g.codec == 2 ? 0x32564D57u : 0x31564D57u)) return;
   if (ld_u32(payload + 4) != (g.codec | (g.crc_kind << 16) | (g.codec << 24))) return;
-  if (ld_u32(payload + 8) != kChunk || ld_u32(payload + 12) != g.n_chunks) return;
+  if (ld_u32(payload + 8) != (kChunk << g.tile_log2) || ld_u32(payload + 12) != g.hdr_n) return;
   if (ld_u64(payload + 16) != g.nbytes) return;
   uint32_t n_rec = ld_u32(payload + 24), flags = ld_u32(payload + 28);
   uint64_t total = ld_u64(payload + 32);
@@ -1583,6 +1601,23 @@ struct CtlLoads {
   uint4 ent, nx, hdr;
 };
 
+// Chunks above 64 KiB ship whole: a table of tiles lists, for each chunk it
+// ships, every tile of it in order.  Per entry (tile c, whether it is the
+// first entry, the next entry's tile if there is one): the first entry
+// starts a chunk, a tile that does not end its chunk (nor the state) is
+// followed by the next tile, and the next entry, unless it starts a chunk,
+// is the next tile.  Over all entries these are exactly the rules that no
+// tile lacks the tile before or after it in its chunk.
+__device__ __forceinline__ bool tile_order_bad(const ChunkGeom &g, uint32_t c, bool first,
+                                               bool has_next, uint32_t next) {
+  if (!g.tile_log2) return false;
+  const uint32_t m = (1u << g.tile_log2) - 1u;
+  bool bad = first && (c & m) != 0u;
+  if (((c + 1u) & m) != 0u && c + 1u < g.n_chunks) bad = bad || !has_next || next != c + 1u;
+  if (has_next && (next & m) != 0u) bad = bad || next != c + 1u;
+  return bad;
+}
+
 // Step 1: table entry r and the next one.
 __device__ __forceinline__ void ctl_entry_issue(const uint8_t *__restrict__ payload,
                                                 uint64_t table_off, uint32_t n_rec, uint32_t r,
@@ -1606,10 +1641,12 @@ __device__ __forceinline__ void ctl_entry_record(uint64_t table_off, uint32_t n_
     off = (uint64_t)ent.z | ((uint64_t)ent.w << 32);
     end = table_off;
     bool tbad = false;
+    const uint32_t nxc = uniform(L.nx.x);
     if (r + 1 < n_rec) {
       end = (uint64_t)uniform(L.nx.z) | ((uint64_t)uniform(L.nx.w) << 32);
-      tbad = uniform(L.nx.x) <= c;
+      tbad = nxc <= c;
     }
+    tbad = tbad || tile_order_bad(g, c, r == 0, r + 1 < n_rec, nxc);
     tbad = tbad || c >= g.n_chunks || (r == 0 && off != 64u) || (off & 15u) || off >= end ||
            end > table_off;
     valid = tbad ? 2u : 1u;  // 2: entry rejected
@@ -2630,7 +2667,7 @@ static_assert(kHdMeta + sizeof(HufMeta) <= kLdsLowBytes, "v2 decoder scratch fit
 // entry's chunk, the record's end, and its header when the entry's offsets
 // leave room for one (read only then).
 struct HufFetch {
-  uint32_t ew[4], prevc, hdr[4], has_hdr;
+  uint32_t ew[4], prevc, nextc, hdr[4], has_hdr;
   uint64_t end;
 };
 __device__ __forceinline__ HufFetch huf_fetch(const uint8_t *__restrict__ payload, uint64_t table_off,
@@ -2640,6 +2677,7 @@ __device__ __forceinline__ HufFetch huf_fetch(const uint8_t *__restrict__ payloa
   for (int i = 0; i < 4; ++i) f.ew[i] = ld_u32(e + 4 * i);
   f.prevc = r > 0 ? ld_u32(e - 16) : 0u;
   f.end = r + 1 < n_rec ? ld_u64(e + 24) : table_off;
+  f.nextc = r + 1 < n_rec ? ld_u32(e + 16) : 0u;
   const uint64_t off = f.ew[2] | ((uint64_t)f.ew[3] << 32);
   f.has_hdr = !(off & 15u) && off < f.end && f.end <= table_off && f.end - off >= 16u;
   for (int i = 0; i < 4; ++i) f.hdr[i] = f.has_hdr ? ld_u32(payload + off + 4 * i) : 0u;
@@ -2686,7 +2724,8 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
       const uint64_t off = ew[2] | ((uint64_t)ew[3] << 32);
       const uint64_t end = f.end;
       const bool tbad = c >= g.n_chunks || (r > 0 && f.prevc >= c) ||
-                        (r == 0 && off != 64u) || (off & 15u) || off >= end || end > table_off;
+                        (r == 0 && off != 64u) || (off & 15u) || off >= end || end > table_off ||
+                        tile_order_bad(g, c, r == 0, r + 1 < n_rec, f.nextc);
       ecrc[r] = crc_words(ew, 4);
       M.bad = M.hufbad = M.kraft = M.maxlen = 0;
       for (uint32_t b = 0; b <= kHufMaxLen; ++b) M.bl[b] = 0;
@@ -2989,21 +3028,100 @@ static int launch_combine(const CombineJobs &jobs, int n_jobs, void *stream) {
   return (int)hipGetLastError();
 }
 
+__global__ void k_zero_u32(uint32_t *__restrict__ p, uint32_t n) {
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    p[i] = 0;
+}
+
+// The combine job of the global CRC from per-chunk CRCs (the caller's
+// chunks) or per-unit CRCs.
+static CombineJob global_job(const ChunkGeom &g, const uint32_t *vals, bool units, uint32_t *out) {
+  if (units || !g.tile_log2)
+    return CombineJob{vals, nullptr, g.n_chunks, 16u, g.tail_len, g.crc_kind, out};
+  const uint64_t last = g.hdr_n ? g.nbytes - ((uint64_t)(g.hdr_n - 1) << (16 + g.tile_log2)) : 0;
+  return CombineJob{vals, nullptr, g.hdr_n, 16u + g.tile_log2, (uint32_t)last, g.crc_kind, out};
+}
+
 int launch_checksum(const void *data, const ChunkGeom &g, uint32_t *crc_out,
-                    uint32_t *global_crc, int n_cu, void *stream) {
+                    uint32_t *global_crc, int n_cu, void *stream, bool units) {
+  const bool per_chunk = !units && g.tile_log2;
+  if (per_chunk && g.hdr_n) {
+    hipLaunchKernelGGL(k_zero_u32, dim3(min((g.hdr_n + 255u) / 256u, 64u)), dim3(256), 0,
+                       S(stream), crc_out, g.hdr_n);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return (int)e;
+  }
   if (g.n_chunks) {
     uint32_t grid = min((uint32_t)n_cu, g.n_chunks);
     hipLaunchKernelGGL(k_checksum, dim3(grid), dim3(kThreads + 64), kLdsBase, S(stream),
-                       static_cast<const uint8_t *>(data), g, crc_out);
+                       static_cast<const uint8_t *>(data), g, crc_out, per_chunk ? 1u : 0u);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
   }
   if (global_crc) {
     CombineJobs jobs = {};
-    jobs.job[0] = CombineJob{crc_out, nullptr, g.n_chunks, 16u, g.tail_len, g.crc_kind, global_crc};
+    jobs.job[0] = global_job(g, crc_out, units, global_crc);
     return launch_combine(jobs, 1, stream);
   }
   return 0;
+}
+
+// A caller's list of chunks above 64 KiB as the list of their tiles (each
+// chunk's tiles in order; the state's last chunk may have fewer).  A list
+// that is longer than the chunk count, not strictly ascending or out of
+// range becomes a tile list longer than the tile count, which the encoder
+// rejects (an empty payload).  One workgroup.
+__global__ __launch_bounds__(1024) void k_expand_list(const uint32_t *__restrict__ idx,
+                                                      const uint32_t *__restrict__ n_idx,
+                                                      ChunkGeom g, uint32_t *__restrict__ out,
+                                                      uint32_t *__restrict__ n_out) {
+  const uint32_t n = *n_idx, per = 1u << g.tile_log2;
+  bool bad = n > g.hdr_n;
+  const uint32_t m = bad ? 0u : n;
+  for (uint32_t r = threadIdx.x; r < m; r += blockDim.x) {
+    const uint32_t c = idx[r];
+    bad = bad || c >= g.hdr_n || (r > 0 && idx[r - 1] >= c);
+    // (a valid list writes slots below its tile count, hence below n_chunks)
+    if (c < g.hdr_n)
+      for (uint32_t j = 0; j < per; ++j)
+        if ((c << g.tile_log2) + j < g.n_chunks && r * per + j < g.n_chunks)
+          out[r * per + j] = (c << g.tile_log2) + j;
+  }
+  bad = __syncthreads_or(bad);
+  if (threadIdx.x == 0) {
+    uint32_t tiles = m * per;
+    // only the last entry can be the state's last chunk, with fewer tiles
+    if (m && idx[m - 1] + 1u == g.hdr_n) tiles -= (g.hdr_n << g.tile_log2) - g.n_chunks;
+    *n_out = bad ? g.n_chunks + 1u : tiles;
+  }
+}
+
+int launch_expand_list(const uint32_t *idx, const uint32_t *n_idx, const ChunkGeom &g,
+                       uint32_t *out, uint32_t *n_out, void *stream) {
+  hipLaunchKernelGGL(k_expand_list, dim3(1), dim3(1024), 0, S(stream), idx, n_idx, g, out, n_out);
+  return (int)hipGetLastError();
+}
+
+// Chunk CRCs from their tiles' CRCs, CRC(A|B) = F^|B|(CRC(A)) ^ CRC(B) tile by
+// tile; one thread per chunk.
+__global__ void k_fold_tiles(const uint32_t *__restrict__ tile_crc, ChunkGeom g,
+                             uint32_t *__restrict__ out) {
+  const CrcTables &T = g_tables[g.crc_kind];
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < g.hdr_n;
+       i += gridDim.x * blockDim.x) {
+    const uint32_t t0 = i << g.tile_log2, t1 = min((i + 1) << g.tile_log2, g.n_chunks);
+    uint32_t acc = tile_crc[t0];
+    for (uint32_t t = t0 + 1; t < t1; ++t)
+      acc = shift_bytes(T, t + 1 == g.n_chunks ? g.tail_len : kChunk, acc) ^ tile_crc[t];
+    out[i] = acc;
+  }
+}
+
+int launch_fold_tiles(const uint32_t *tile_crc, const ChunkGeom &g, uint32_t *out, void *stream) {
+  if (!g.hdr_n) return 0;
+  hipLaunchKernelGGL(k_fold_tiles, dim3(min((g.hdr_n + 63u) / 64u, 1024u)), dim3(64), 0,
+                     S(stream), tile_crc, g, out);
+  return (int)hipGetLastError();
 }
 
 int launch_diff(const void *cur, const void *prev, const ChunkGeom &g, uint32_t *dirty_idx,
@@ -3017,8 +3135,8 @@ int launch_diff(const void *cur, const void *prev, const ChunkGeom &g, uint32_t 
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
   }
-  hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, S(stream), flags, g.n_chunks, dirty_idx,
-                     n_dirty);
+  hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, S(stream), flags, g.hdr_n, g.tile_log2,
+                     g.n_chunks, dirty_idx, n_dirty);
   return (int)hipGetLastError();
 }
 
@@ -3026,7 +3144,7 @@ int launch_encode(int mode, const void *cur, const void *prev, const ChunkGeom &
                   const uint32_t *idx, const uint32_t *n_idx, const uint32_t *crc_in,
                   uint32_t *crc_out, uint32_t *global_crc, uint32_t *dirty_idx,
                   uint32_t *n_dirty, void *payload, uint64_t *payload_bytes, void *ws,
-                  const WsLayout &L, int n_cu, void *stream) {
+                  const WsLayout &L, int n_cu, void *stream, const uint32_t *global_from) {
   uint8_t *wsb = static_cast<uint8_t *>(ws);
   hipLaunchKernelGGL(k_encode_prepare, dim3(64), dim3(256), 0, S(stream), wsb, L, g.n_chunks,
                      mode == kModeList ? n_idx : nullptr);
@@ -3058,7 +3176,8 @@ int launch_encode(int mode, const void *cur, const void *prev, const ChunkGeom &
   uint32_t *crcs = ctl32 + 60;  // two spare words of the control block
   const uint32_t *all_crc = crc_in ? crc_in : crc_out;
   CombineJobs jobs = {};
-  jobs.job[0] = CombineJob{all_crc, nullptr, g.n_chunks, 16u, g.tail_len, g.crc_kind, crcs};
+  jobs.job[0] = global_from ? global_job(g, global_from, false, crcs)
+                            : global_job(g, all_crc, true, crcs);
   jobs.job[1] = CombineJob{reinterpret_cast<const uint32_t *>(wsb + L.entry_crc),
                            &reinterpret_cast<WsCtl *>(wsb + L.ctl)->n_rec, 0u, 4u, 16u,
                            g.crc_kind, crcs + 1};
@@ -3260,9 +3379,9 @@ int launch_reverify(const void *live, const ChunkGeom &g, const void *staging,
   uint32_t *live_crc = reinterpret_cast<uint32_t *>(wsb + L.flags);
   uint32_t *staged_crc = reinterpret_cast<uint32_t *>(wsb + L.entry_crc);
   uint32_t *words = reinterpret_cast<uint32_t *>(wsb + L.ctl);  // [0] flag, [1] global
-  int rc = launch_checksum(live, g, live_crc, nullptr, n_cu, stream);
+  int rc = launch_checksum(live, g, live_crc, nullptr, n_cu, stream, true);
   if (rc) return rc;
-  rc = launch_checksum(staging, gs, staged_crc, nullptr, n_cu, stream);
+  rc = launch_checksum(staging, gs, staged_crc, nullptr, n_cu, stream, true);
   if (rc) return rc;
   hipLaunchKernelGGL(k_reverify_records, dim3(1), dim3(1024), 0, S(stream),
                      static_cast<const uint8_t *>(payload), live_crc,
@@ -3291,7 +3410,7 @@ int launch_encode_v2(const void *state, const ChunkGeom &g, const uint32_t *idx,
   if (e != hipSuccess) return (int)e;
   const uint32_t *crcs = crc_in;
   if (!crcs) {
-    const int rc = launch_checksum(state, g, crc_scratch, nullptr, n_cu, stream);
+    const int rc = launch_checksum(state, g, crc_scratch, nullptr, n_cu, stream, true);
     if (rc) return rc;
     crcs = crc_scratch;
   }

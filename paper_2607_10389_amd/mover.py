@@ -16,13 +16,17 @@ class Mover:
     def __init__(self, nbytes: int, crc_kind: int = _wm.WM_CRC32_ZLIB,
                  device: str | torch.device = "cuda", stream=None,
                  staging_chunks: int | None = None,
-                 codec: int = _wm.WM_CODEC_EXPFOR):
+                 codec: int = _wm.WM_CODEC_EXPFOR,
+                 chunk_bytes: int = _wm.CHUNK):
         self.nbytes = nbytes
-        self.p = _wm.params(crc_kind, codec=codec)
+        self.p = _wm.params(crc_kind, chunk_bytes=chunk_bytes, codec=codec)
         self.device = torch.device(device)
         self.stream = stream
-        n = _wm.n_chunks(nbytes)
+        n = _wm.n_chunks(nbytes, chunk_bytes)
         self.n_chunks = n
+        # records are 64 KiB units: the chunks, or the tiles of larger ones
+        n_units = _wm.n_chunks(nbytes)
+        self.n_units = n_units
         u32 = dict(dtype=torch.int32, device=self.device)
         self.crc = torch.zeros(max(n, 1), **u32)
         self.global_crc = torch.zeros(1, **u32)
@@ -34,11 +38,11 @@ class Mover:
         ws = _wm.workspace_bytes(nbytes, self.p)
         self.ws_src = torch.zeros(ws, dtype=torch.uint8, device=self.device)
         self.ws_dst = torch.zeros(ws, dtype=torch.uint8, device=self.device)
-        sc = n if staging_chunks is None else staging_chunks
+        sc = n_units if staging_chunks is None else staging_chunks
         self.staging = torch.zeros(max(sc, 1) * _wm.CHUNK, dtype=torch.uint8,
                                    device=self.device)
         self.verdict = torch.zeros(1, **u32)
-        self.rec_status = torch.zeros(max(n, 1), **u32)
+        self.rec_status = torch.zeros(max(n_units, 1), **u32)
         self._bufs = None
         # self.crc holds the CRCs of the last pre-copy round's shipped
         # snapshot (set by a round that returned WM_OK, cleared by any other
