@@ -91,6 +91,9 @@ def lib():
         L.orc_huffman_lengths.restype = ctypes.c_uint32
         L.orc_plan_chunk_v2.argtypes = [u8p, ctypes.c_uint32, u32p, u32p, u32p, u32p, u64p]
         L.orc_plan_chunk_v2.restype = ctypes.c_int
+        L.orc_plan_chunk_huf.argtypes = [ctypes.c_int, u8p, ctypes.c_uint32, u32p, u32p, u32p,
+                                         u32p, u64p]
+        L.orc_plan_chunk_huf.restype = ctypes.c_int
         L.orc_flat_layout.argtypes = [u64p, ctypes.c_uint32, u64p]
         L.orc_flat_layout.restype = ctypes.c_uint64
         L.orc_flatten.argtypes = [ctypes.POINTER(u8p), u64p, ctypes.c_uint32,
@@ -189,12 +192,14 @@ def huffman_lengths(counts) -> tuple[np.ndarray, int]:
     return out, int(k)
 
 
-def plan_chunk_v2(chunk_bytes) -> dict:
+def plan_chunk_v2(chunk_bytes, codec: int = 2) -> dict:
+    """Plan of one chunk's record in format v2 (codec 2: Huffman-coded
+    exponents) or v3 (codec 3: Huffman-coded high bytes)."""
     b = _bytes(chunk_bytes)
     m, k, base, sb = (np.zeros(1, np.uint32) for _ in range(4))
     size = np.zeros(1, np.uint64)
-    lib().orc_plan_chunk_v2(_p8(b), b.size, _p32(m), _p32(k), _p32(base), _p32(sb),
-                            size.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)))
+    lib().orc_plan_chunk_huf(codec, _p8(b), b.size, _p32(m), _p32(k), _p32(base), _p32(sb),
+                             size.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)))
     return dict(mode=int(m[0]), k=int(k[0]), base=int(base[0]),
                 stream_bytes=int(sb[0]), size=int(size[0]))
 

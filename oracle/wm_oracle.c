@@ -39,6 +39,9 @@
  *   mantissa w&127; sm = sign<<7 | mantissa.  PACK with k >= 1 codes e as
  *   e - base when 0 <= e - base < 2^k - 1, else as ESC = 2^k - 1 with e
  *   appended to the escapes; PACK with k = 0 means every e equals base.
+ *
+ * Formats v2 (codec 2, magic 'WMV2') and v3 (codec 3, 'WMV3') share this
+ * header, table and tiling, with RAW or Huffman records (below).
  */
 #include "wm_oracle.h"
 
@@ -372,6 +375,23 @@ static uint32_t decode_record(int kind, const uint8_t *rec, uint64_t L,
 
 #define HUF_STREAMS 512u
 
+/* The two byte planes of a word in the Huffman formats: plane A is coded,
+ * plane B kept raw.  Codec 2 (v2): A is the exponent, B the sign/mantissa
+ * byte.  Codec 3 (v3, the paper's bf16 byte-plane split, §6.4 codec
+ * paragraph): A is the high byte (sign and the exponent's upper seven bits),
+ * B the low byte (the exponent's lowest bit and the mantissa), which is close
+ * to 8 bits of entropy and stays raw. */
+static uint32_t plane_a(int codec, uint16_t w) {
+  return codec == 3 ? (uint32_t)(w >> 8) : exponent_of(w);
+}
+static uint8_t plane_b(int codec, uint16_t w) {
+  return codec == 3 ? (uint8_t)(w & 255u) : sm_of(w);
+}
+static uint16_t from_planes(int codec, uint32_t a, uint32_t b) {
+  if (codec == 3) return (uint16_t)((a << 8) | b);
+  return (uint16_t)(((b >> 7) << 15) | (a << 7) | (b & 127u));
+}
+
 /* Word i of stream s (s < 512, i < 64): row 8*(s/64) + i/8 of 512 words,
  * word 8*(s%64) + i%8 of the row. */
 static uint32_t stream_word(uint32_t s, uint32_t i) {
@@ -456,14 +476,14 @@ static uint64_t huf_size(uint32_t n, uint32_t k, uint64_t stream_bytes) {
 }
 
 /* Bits of each stream for the given lengths; returns the total bytes. */
-static uint64_t stream_bytes_of(const uint8_t *chunk, uint32_t n,
+static uint64_t stream_bytes_of(int codec, const uint8_t *chunk, uint32_t n,
                                 const uint8_t *len, uint8_t *sbytes) {
   uint64_t total = 0;
   for (uint32_t s = 0; s < HUF_STREAMS; s++) {
     uint64_t bits = 0;
     for (uint32_t i = 0; i < 64; i++) {
       uint32_t wi = stream_word(s, i);
-      if (wi < n) bits += len[exponent_of(word_at(chunk, wi))];
+      if (wi < n) bits += len[plane_a(codec, word_at(chunk, wi))];
     }
     sbytes[s] = (uint8_t)((bits + 7) / 8);
     total += sbytes[s];
@@ -471,16 +491,16 @@ static uint64_t stream_bytes_of(const uint8_t *chunk, uint32_t n,
   return total;
 }
 
-/* Mode choice of format v2: RAW, or HUF when strictly smaller.  HUF with a
- * single exponent has k = 0 and base = that exponent; otherwise k is the
- * longest code length, base 0, and n_esc carries the stream bytes. */
-int orc_plan_chunk_v2(const uint8_t *chunk, uint32_t len, uint32_t *mode,
-                      uint32_t *k, uint32_t *base, uint32_t *n_sb,
-                      uint64_t *size) {
+/* Mode choice of formats v2 and v3: RAW, or HUF when strictly smaller.  HUF
+ * with a single plane-A symbol has k = 0 and base = that symbol; otherwise k
+ * is the longest code length, base 0, and n_esc carries the stream bytes. */
+int orc_plan_chunk_huf(int codec, const uint8_t *chunk, uint32_t len,
+                       uint32_t *mode, uint32_t *k, uint32_t *base,
+                       uint32_t *n_sb, uint64_t *size) {
   uint32_t n = len / 2;
   uint32_t count[256] = {0};
   uint8_t lens[256], sbytes[HUF_STREAMS];
-  for (uint32_t i = 0; i < n; i++) count[exponent_of(word_at(chunk, i))]++;
+  for (uint32_t i = 0; i < n; i++) count[plane_a(codec, word_at(chunk, i))]++;
   uint32_t longest = orc_huffman_lengths(count, lens);
   uint32_t only = 0, distinct = 0;
   for (uint32_t e = 0; e < 256; e++)
@@ -488,7 +508,7 @@ int orc_plan_chunk_v2(const uint8_t *chunk, uint32_t len, uint32_t *mode,
       distinct++;
       only = e;
     }
-  uint64_t sb = longest ? stream_bytes_of(chunk, n, lens, sbytes) : 0;
+  uint64_t sb = longest ? stream_bytes_of(codec, chunk, n, lens, sbytes) : 0;
   uint64_t hs = huf_size(n, longest, sb);
   *mode = 0;
   *k = *base = *n_sb = 0;
@@ -503,13 +523,27 @@ int orc_plan_chunk_v2(const uint8_t *chunk, uint32_t len, uint32_t *mode,
   return 0;
 }
 
-/* Write one v2 record (size bytes, already zeroed by the caller). */
-static void write_record_v2(int kind, const uint8_t *chunk, uint32_t len,
+int orc_plan_chunk_v2(const uint8_t *chunk, uint32_t len, uint32_t *mode,
+                      uint32_t *k, uint32_t *base, uint32_t *n_sb,
+                      uint64_t *size) {
+  return orc_plan_chunk_huf(2, chunk, len, mode, k, base, n_sb, size);
+}
+
+/* Write one v2/v3 record (size bytes, already zeroed by the caller).  RAW is
+ * plane A (n B) then plane B (n B), each padded: for codec 2 exactly the
+ * RAW record of format v1. */
+static void write_record_v2(int kind, int codec, const uint8_t *chunk, uint32_t len,
                             uint32_t mode, uint32_t k, uint32_t base,
                             uint32_t n_sb, uint8_t *out) {
   uint32_t n = len / 2;
   if (mode == 0) {
-    write_record(kind, chunk, len, 0, 0, 0, 0, out);
+    put_u32(out + 4, n);
+    put_u32(out + 12, orc_crc(kind, out, 12));
+    for (uint32_t i = 0; i < n; i++) {
+      uint16_t w = word_at(chunk, i);
+      out[16 + i] = (uint8_t)plane_a(codec, w);
+      out[16 + pad16(n) + i] = plane_b(codec, w);
+    }
     return;
   }
   out[0] = 2;
@@ -526,19 +560,19 @@ static void write_record_v2(int kind, const uint8_t *chunk, uint32_t len,
   } else {
     uint32_t count[256] = {0}, code[256];
     uint8_t lens[256];
-    for (uint32_t i = 0; i < n; i++) count[exponent_of(word_at(chunk, i))]++;
+    for (uint32_t i = 0; i < n; i++) count[plane_a(codec, word_at(chunk, i))]++;
     orc_huffman_lengths(count, lens);
     canonical_codes(lens, code);
     uint8_t *ltab = body, *sbytes = body + 128, *streams = body + 128 + HUF_STREAMS;
     for (uint32_t e = 0; e < 256; e++) ltab[e / 2] |= (uint8_t)(lens[e] << (4 * (e % 2)));
-    stream_bytes_of(chunk, n, lens, sbytes);
+    stream_bytes_of(codec, chunk, n, lens, sbytes);
     uint64_t at = 0;
     for (uint32_t s = 0; s < HUF_STREAMS; s++) {
       uint64_t bit = 0;
       for (uint32_t i = 0; i < 64; i++) {
         uint32_t wi = stream_word(s, i);
         if (wi >= n) continue;
-        uint32_t e = exponent_of(word_at(chunk, wi));
+        uint32_t e = plane_a(codec, word_at(chunk, wi));
         /* the code's bits, most significant first, go to the stream in
          * order; stream bit j is bit j % 8 of byte j / 8 */
         for (int b = lens[e] - 1; b >= 0; b--, bit++)
@@ -548,11 +582,11 @@ static void write_record_v2(int kind, const uint8_t *chunk, uint32_t len,
     }
     sm = streams + pad16(at);
   }
-  for (uint32_t i = 0; i < n; i++) sm[i] = sm_of(word_at(chunk, i));
+  for (uint32_t i = 0; i < n; i++) sm[i] = plane_b(codec, word_at(chunk, i));
 }
 
-/* Structure checks and decode of one v2 record (see decode_record). */
-static uint32_t decode_record_v2(int kind, const uint8_t *rec, uint64_t L,
+/* Structure checks and decode of one v2/v3 record (see decode_record). */
+static uint32_t decode_record_v2(int kind, int codec, const uint8_t *rec, uint64_t L,
                                  uint32_t len, uint32_t src_crc, uint8_t *out) {
   uint32_t n = len / 2;
   if (L < 16) return ORC_V_RECORD;
@@ -561,8 +595,16 @@ static uint32_t decode_record_v2(int kind, const uint8_t *rec, uint64_t L,
   uint32_t n_words = get_u32(rec + 4), n_sb = get_u32(rec + 8);
   if (rec[3] != 0 || n_words != n || (mode != 0 && mode != 2))
     return ORC_V_RECORD;
-  if (mode == 0) return decode_record(kind, rec, L, len, src_crc, out);
   const uint8_t *body = rec + 16, *sm;
+  if (mode == 0) {
+    if (k != 0 || base != 0 || n_sb != 0 || L != raw_size(n)) return ORC_V_RECORD;
+    const uint8_t *pa = body, *pb = body + pad16(n);
+    if (!all_zero(pa + n, pad16(n) - n) || !all_zero(pb + n, pad16(n) - n))
+      return ORC_V_RECORD;
+    for (uint32_t i = 0; i < n; i++)
+      put_u16(out + 2 * (uint64_t)i, from_planes(codec, pa[i], pb[i]));
+    return orc_crc(kind, out, len) == src_crc ? 0u : ORC_V_DATA;
+  }
   uint8_t e_of[32768];
   if (k > ORC_HUF_MAX_LEN) return ORC_V_RECORD;
   /* the encoder codes a chunk only when that beats RAW: a longer HUF record
@@ -633,9 +675,7 @@ static uint32_t decode_record_v2(int kind, const uint8_t *rec, uint64_t L,
   }
   if (!all_zero(sm + n, pad16(n) - n)) return ORC_V_RECORD;
   for (uint32_t i = 0; i < n; i++)
-    put_u16(out + 2 * (uint64_t)i,
-            (uint16_t)(((uint32_t)(sm[i] >> 7) << 15) | ((uint32_t)e_of[i] << 7) |
-                       (sm[i] & 127u)));
+    put_u16(out + 2 * (uint64_t)i, from_planes(codec, e_of[i], sm[i]));
   return orc_crc(kind, out, len) == src_crc ? 0u : ORC_V_DATA;
 }
 
@@ -661,9 +701,9 @@ static void en_plan_range(void *vp, uint64_t lo, uint64_t hi) {
     uint64_t c = en_chunk(x, r);
     const uint8_t *src = x->state + c * (uint64_t)x->chunk;
     uint32_t len = chunk_len(x->nbytes, x->chunk, c);
-    if (x->codec == 2)
-      orc_plan_chunk_v2(src, len, &x->mode[r], &x->k[r], &x->base[r],
-                        &x->esc[r], &x->size[r]);
+    if (x->codec >= 2)
+      orc_plan_chunk_huf(x->codec, src, len, &x->mode[r], &x->k[r], &x->base[r],
+                         &x->esc[r], &x->size[r]);
     else
       orc_plan_chunk(src, len, &x->mode[r], &x->k[r], &x->base[r], &x->esc[r],
                      &x->size[r]);
@@ -680,8 +720,8 @@ static void en_write_range(void *vp, uint64_t lo, uint64_t hi) {
     put_u32(entry, (uint32_t)c);
     put_u32(entry + 4, orc_crc(x->kind, src, len));
     put_u64(entry + 8, x->offset[r]);
-    if (x->codec == 2)
-      write_record_v2(x->kind, src, len, x->mode[r], x->k[r], x->base[r],
+    if (x->codec >= 2)
+      write_record_v2(x->kind, x->codec, src, len, x->mode[r], x->k[r], x->base[r],
                       x->esc[r], x->payload + x->offset[r]);
     else
       write_record(x->kind, src, len, x->mode[r], x->k[r], x->base[r],
@@ -711,7 +751,7 @@ int64_t orc_encode_codec(int kind, int codec, const uint8_t *state,
                          uint64_t cap, int threads) {
   if (!chunk_ok(chunk_bytes) || (kind != 0 && kind != 1) || (nbytes & 1))
     return -1;
-  if (codec != 1 && !(codec == 2 && chunk_bytes >= ORC_TILE)) return -1;
+  if (codec != 1 && !((codec == 2 || codec == 3) && chunk_bytes >= ORC_TILE)) return -1;
   uint64_t n_chunks = n_chunks_of(nbytes, chunk_bytes);
   uint64_t n_ship = idx ? n_idx : n_chunks;
   if (n_ship > n_chunks) return -1;
@@ -765,7 +805,7 @@ int64_t orc_encode_codec(int kind, int codec, const uint8_t *state,
   h[0] = 'W';
   h[1] = 'M';
   h[2] = 'V';
-  h[3] = codec == 2 ? '2' : '1';
+  h[3] = (uint8_t)('0' + codec);
   put_u16(h + 4, (uint16_t)codec);
   h[6] = (uint8_t)kind;
   h[7] = (uint8_t)codec;
@@ -885,8 +925,8 @@ static void de_range(void *vp, uint64_t lo, uint64_t hi) {
     uint64_t end = r + 1 < x->n_rec ? get_u64(e + 16 + 8) : x->table;
     uint32_t len = chunk_len(x->nbytes, x->chunk, c);
     uint8_t *out = x->staging + r * (uint64_t)x->chunk;
-    x->status[r] = x->codec == 2
-                       ? decode_record_v2(x->kind, x->payload + off, end - off,
+    x->status[r] = x->codec >= 2
+                       ? decode_record_v2(x->kind, x->codec, x->payload + off, end - off,
                                           len, get_u32(e + 4), out)
                        : decode_record(x->kind, x->payload + off, end - off,
                                        len, get_u32(e + 4), out);
@@ -909,7 +949,8 @@ uint32_t orc_decode_verify_codec(int kind, int codec, const uint8_t *payload,
                                  uint64_t staging_cap, uint32_t *rec_status,
                                  uint32_t n_status, int threads) {
   if (!chunk_ok(chunk_bytes) || (kind != 0 && kind != 1)) return ORC_V_HEADER;
-  if (codec != 1 && !(codec == 2 && chunk_bytes >= ORC_TILE)) return ORC_V_HEADER;
+  if (codec != 1 && !((codec == 2 || codec == 3) && chunk_bytes >= ORC_TILE))
+    return ORC_V_HEADER;
   uint64_t n_chunks = n_chunks_of(nbytes, chunk_bytes);
   uint32_t u = unit_of(chunk_bytes);
   uint64_t per = chunk_bytes / u, n_units = n_chunks_of(nbytes, u);
@@ -919,7 +960,7 @@ uint32_t orc_decode_verify_codec(int kind, int codec, const uint8_t *payload,
   const uint8_t *h = payload;
   if (orc_crc(kind, h, 60) != get_u32(h + 60)) return ORC_V_HEADER;
   if (h[0] != 'W' || h[1] != 'M' || h[2] != 'V' ||
-      h[3] != (codec == 2 ? '2' : '1'))
+      h[3] != (uint8_t)('0' + codec))
     return ORC_V_HEADER;
   if ((h[4] | (h[5] << 8)) != codec || h[6] != (uint8_t)kind ||
       h[7] != (uint8_t)codec)

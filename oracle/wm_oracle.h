@@ -84,9 +84,11 @@ int64_t orc_encode(int kind, const uint8_t *state, uint64_t nbytes,
                    uint32_t chunk_bytes, const uint32_t *idx, uint32_t n_idx,
                    uint8_t *payload, uint64_t cap, int threads);
 
-/* Format v2 (codec 2, chunks of 64 KiB or more): as orc_encode with records RAW
- * or HUF (per-chunk canonical Huffman codes of the exponents in 512 streams).
- * orc_encode is orc_encode_codec with codec 1. */
+/* Formats v2 and v3 (codecs 2 and 3, chunks of 64 KiB or more): as
+ * orc_encode with records RAW or HUF (a per-chunk canonical Huffman code of
+ * one byte plane in 512 streams, the other plane raw): v2 codes the
+ * exponents, v3 the high bytes (the bf16 byte-plane split).  orc_encode is
+ * orc_encode_codec with codec 1. */
 #define ORC_HUF_MAX_LEN 11u
 int64_t orc_encode_codec(int kind, int codec, const uint8_t *state,
                          uint64_t nbytes, uint32_t chunk_bytes,
@@ -102,6 +104,10 @@ uint32_t orc_huffman_lengths(const uint32_t *count, uint8_t *len);
 int orc_plan_chunk_v2(const uint8_t *chunk, uint32_t len, uint32_t *mode,
                       uint32_t *k, uint32_t *base, uint32_t *n_sb,
                       uint64_t *size);
+/* The same for codec 2 or 3 (base: the only coded-plane symbol). */
+int orc_plan_chunk_huf(int codec, const uint8_t *chunk, uint32_t len,
+                       uint32_t *mode, uint32_t *k, uint32_t *base,
+                       uint32_t *n_sb, uint64_t *size);
 
 /* Plan of one chunk's record (exposed for tests): mode, k, base, n_esc and
  * record size in bytes. */

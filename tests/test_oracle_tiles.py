@@ -52,7 +52,7 @@ def rebuilt_header(kind, head64, chunk, n_chunks):
     return bytes(h)
 
 
-@pytest.mark.parametrize("codec", [1, 2])
+@pytest.mark.parametrize("codec", [1, 2, 3])
 @pytest.mark.parametrize("kind", [0, 1])
 @pytest.mark.parametrize("chunk", [1 << 17, 1 << 18])
 def test_payload_is_the_tiles_payload(chunk, kind, codec):
