@@ -71,13 +71,18 @@ typedef int32_t wm_status;
  * chunk's exponents in the chunk's own canonical Huffman code (lengths at
  * most 11) in 512 streams, so that 512 decoders work side by side (§6.4: the
  * redundancy of a bf16 cache sits in its exponent plane, which the paper's
- * codec entropy-codes).  Both fall back to RAW per chunk.  Every call takes
- * either format, except wm_encode_step_static (format v1 only).  Format v2
- * has no single-pass encoder: its wm_encode_step runs the diff, a checksum
- * of every chunk and the list encoder (same outputs), and its pre-copy
- * rounds checksum every chunk. */
+ * codec entropy-codes).  BYTEPLANE, format v3: the paper's bf16 byte-plane
+ * split (§6.4 codec paragraph) in format v2's layout, the high byte (sign and
+ * the exponent's upper seven bits) Huffman-coded and the low byte (the
+ * exponent's lowest bit and the mantissa, close to 8 bits of entropy) raw.
+ * All fall back to RAW per chunk.  Every call takes any format, except
+ * wm_encode_step_static (format v1 only).  Formats v2 and v3 have no
+ * single-pass encoder: their wm_encode_step runs the diff, a checksum of
+ * every chunk and the list encoder (same outputs), and their pre-copy rounds
+ * checksum every chunk. */
 #define WM_CODEC_EXPFOR 1
 #define WM_CODEC_EXPHUF 2
+#define WM_CODEC_BYTEPLANE 3
 
 /* Bits of the device verdict word written by wm_decode_verify. */
 #define WM_V_HEADER 1u  /* header rejected; nothing else examined */
@@ -96,7 +101,7 @@ typedef int32_t wm_status;
 typedef struct wm_params {
   uint32_t chunk_bytes; /* bytes per chunk: a power of two, 64 KiB..16 MiB */
   uint32_t crc_kind;    /* WM_CRC32_ZLIB or WM_CRC32C */
-  uint32_t codec;       /* WM_CODEC_EXPFOR or WM_CODEC_EXPHUF */
+  uint32_t codec;       /* WM_CODEC_EXPFOR, WM_CODEC_EXPHUF or WM_CODEC_BYTEPLANE */
   uint32_t flags;       /* must be 0 */
 } wm_params;
 
@@ -108,7 +113,7 @@ const char *wm_status_str(wm_status s);
 wm_status wm_init(int device);
 
 /* Bytes of device workspace needed by wm_diff_dirty, wm_encode,
- * wm_encode_step and wm_decode_verify for a state of nbytes (format v2 adds
+ * wm_encode_step and wm_decode_verify for a state of nbytes (formats v2 and v3 add
  * 692 bytes per chunk and a few hundred more: the record plans and a dirty
  * list).  0 if p is invalid. */
 uint64_t wm_workspace_bytes(uint64_t nbytes, const wm_params *p);

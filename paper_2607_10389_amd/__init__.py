@@ -10,7 +10,7 @@ is its Python binding (``_wm``) plus a small buffer-owning helper
 """
 from . import _wm
 from ._wm import (  # noqa: F401
-    CHUNK, WM_CODEC_EXPFOR, WM_CODEC_EXPHUF, WM_CRC32C, WM_CRC32_ZLIB, WM_COMMIT_NONE,
+    CHUNK, WM_CODEC_BYTEPLANE, WM_CODEC_EXPFOR, WM_CODEC_EXPHUF, WM_CRC32C, WM_CRC32_ZLIB, WM_COMMIT_NONE,
     WM_COMMIT_SCATTER,
     WM_OK, WM_VERIFY_FAILED, WmError, checksum_chunks, commit_or_abort,
     decode_verify, diff_dirty, encode, encode_step, flat_bytes, flatten,

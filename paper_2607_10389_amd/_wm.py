@@ -28,6 +28,7 @@ WM_CRC32_ZLIB = 0
 WM_CRC32C = 1
 WM_CODEC_EXPFOR = 1
 WM_CODEC_EXPHUF = 2
+WM_CODEC_BYTEPLANE = 3
 
 V_HEADER, V_TABLE, V_RECORD, V_DATA, V_STAGING, V_REVERIFY = 1, 2, 4, 8, 16, 32
 

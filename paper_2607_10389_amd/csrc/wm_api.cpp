@@ -77,7 +77,9 @@ wm_status ensure_device(int *n_cu, void **scratch = nullptr, uint64_t *scratch_b
 
 wm_status check_params(const wm_params *p) {
   if (!p) return WM_ERR_INVALID_ARG;
-  if (p->crc_kind > 1 || (p->codec != WM_CODEC_EXPFOR && p->codec != WM_CODEC_EXPHUF) ||
+  if (p->crc_kind > 1 ||
+      (p->codec != WM_CODEC_EXPFOR && p->codec != WM_CODEC_EXPHUF &&
+       p->codec != WM_CODEC_BYTEPLANE) ||
       p->flags != 0)
     return WM_ERR_INVALID_ARG;
   uint32_t c = p->chunk_bytes;
@@ -147,7 +149,7 @@ uint64_t list_offset(const WsLayout &L, uint32_t n_chunks) {
   return (plans_offset(L) + (uint64_t)kHufPlanBytes * n_chunks + 255u) & ~255ull;
 }
 uint64_t ws_base(const WsLayout &L, uint32_t n_chunks, uint32_t codec) {
-  return codec == WM_CODEC_EXPHUF ? list_offset(L, n_chunks) + 4ull * n_chunks + 16u : L.total;
+  return codec != WM_CODEC_EXPFOR ? list_offset(L, n_chunks) + 4ull * n_chunks + 16u : L.total;
 }
 // Chunks above 64 KiB also keep, after that, the tile list of a chunk list
 // with its length, and a chunk list with its length.
@@ -190,7 +192,7 @@ wm_status encode_tiles(const void *state, const ChunkGeom &g, const uint32_t *id
   const TileLists t = tile_lists(ws, g, L);
   if (idx && launch_expand_list(idx, n_idx, g, t.tiles, t.n_tiles, stream) != 0) return WM_ERR_HIP;
   const uint32_t *ul = idx ? t.tiles : nullptr, *un = idx ? t.n_tiles : nullptr;
-  if (g.codec == WM_CODEC_EXPHUF)
+  if (g.codec != WM_CODEC_EXPFOR)
     return hip_status(launch_encode_v2(state, g, ul, un, nullptr, unit_crc, nullptr, payload,
                                        payload_bytes, ws, L, wsb + plans_offset(L), n_cu,
                                        stream));
@@ -222,7 +224,7 @@ wm_status encode_step_tiles(const void *cur, const void *prev, const ChunkGeom &
   uint32_t *unit_crc = reinterpret_cast<uint32_t *>(wsb + L.flags);
   const TileLists t = tile_lists(ws, g, L);
   if (!prev) {
-    int rc = g.codec == WM_CODEC_EXPHUF
+    int rc = g.codec != WM_CODEC_EXPFOR
                  ? launch_encode_v2(cur, g, nullptr, nullptr, nullptr, unit_crc, global_crc,
                                     payload, payload_bytes, ws, L, wsb + plans_offset(L), n_cu,
                                     stream)
@@ -240,7 +242,7 @@ wm_status encode_step_tiles(const void *cur, const void *prev, const ChunkGeom &
       launch_checksum(cur, g, unit_crc, nullptr, n_cu, stream, true) != 0 ||
       (crc_out && launch_fold_tiles(unit_crc, g, crc_out, stream) != 0))
     return WM_ERR_HIP;
-  if (g.codec == WM_CODEC_EXPHUF)
+  if (g.codec != WM_CODEC_EXPFOR)
     return hip_status(launch_encode_v2(cur, g, t.tiles, t.n_tiles, unit_crc, nullptr, global_crc,
                                        payload, payload_bytes, ws, L, wsb + plans_offset(L), n_cu,
                                        stream));
@@ -338,7 +340,7 @@ wm_status wm_encode(const void *state, uint64_t nbytes, const wm_params *p, cons
                                        n_cu, stream);
   uint32_t *crc_scratch =
       crc ? nullptr : reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + L.flags);
-  if (g.codec == WM_CODEC_EXPHUF)
+  if (g.codec != WM_CODEC_EXPFOR)
     return hip_status(launch_encode_v2(state, g, idx, n_idx, crc, crc_scratch, nullptr, payload,
                                        payload_bytes, ws, L,
                                        static_cast<uint8_t *>(ws) + plans_offset(L), n_cu,
@@ -393,7 +395,7 @@ wm_status encode_step_call(const void *cur, const void *prev, uint64_t nbytes,
                              payload_bytes, ws, L, n_cu, stream);
   uint8_t *wsb = static_cast<uint8_t *>(ws);
   uint32_t *crcs = crc_out ? crc_out : reinterpret_cast<uint32_t *>(wsb + L.flags);
-  if (g.codec == WM_CODEC_EXPHUF) {
+  if (g.codec != WM_CODEC_EXPFOR) {
     // format v2 has no single-pass encoder: the same outputs from the diff
     // (whose flags it consumes first), a checksum of every chunk and the
     // list encoder, each reading the state once
@@ -448,7 +450,7 @@ wm_status wm_decode_verify(const void *payload, uint64_t payload_cap, uint64_t n
   int n_cu = 0;
   if ((s = ensure_device(&n_cu)) != WM_OK) return s;
   n_cu = stream_cus(stream, n_cu);
-  if (g.codec == WM_CODEC_EXPHUF)
+  if (g.codec != WM_CODEC_EXPFOR)
     return hip_status(launch_decode_v2(payload, payload_cap, g, staging, staging_cap, verdict,
                                        rec_status, ws, L, n_cu, stream));
   return hip_status(launch_decode(payload, payload_cap, g, staging, staging_cap, verdict,
@@ -651,7 +653,7 @@ wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t 
     if ((s = ensure_device(&n_cu0)) != WM_OK) return s;
     n_cu0 = stream_cus(stream, n_cu0);
     const WsLayout L = ws_layout(g.n_chunks);
-    if (g.codec == WM_CODEC_EXPHUF) {
+    if (g.codec != WM_CODEC_EXPFOR) {
       // format v2 takes its receipts from a checksum of every chunk
       if (launch_checksum(cur, g, b->crc, nullptr, n_cu0, stream) != 0 ||
           launch_encode_v2(cur, g, b->dirty_idx, b->n_dirty, b->crc, nullptr, b->global_crc,
@@ -795,7 +797,7 @@ wm_status wm_receive_verify(const void *host_payload, uint64_t payload_bytes, vo
       receive_schedule(h, payload_bytes, g.n_chunks, batch_bytes, &table_off);
   hipStream_t cs = reinterpret_cast<hipStream_t>(copy_stream);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  auto records = g.codec == WM_CODEC_EXPHUF ? launch_decode_records_v2 : launch_decode_records;
+  auto records = g.codec != WM_CODEC_EXPFOR ? launch_decode_records_v2 : launch_decode_records;
   hipEvent_t *ev = order_events();
   if (!ev) return WM_ERR_HIP;
   // `to` waits for the work enqueued on `from` so far (the wait binds to

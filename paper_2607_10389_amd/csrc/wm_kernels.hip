@@ -1463,7 +1463,7 @@ __global__ __launch_bounds__(256) void k_encode_finish(
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     const uint64_t total = table_off + 16ull * n_rec;
     uint32_t h[16];
-    h[0] = g.codec == 2 ? 0x32564D57u : 0x31564D57u;  // "WMV2" / "WMV1"
+    h[0] = 0x30564D57u + (g.codec << 24);  // "WMV1", "WMV2", "WMV3"
     h[1] = g.codec | (g.crc_kind << 16) | (g.codec << 24);
     h[2] = kChunk << g.tile_log2;  // the caller's chunk size and count
     h[3] = g.hdr_n;
@@ -1517,7 +1517,7 @@ __global__ __launch_bounds__(64) void k_decode_prepare(
 #pragma unroll
   for (int i = 0; i < 15; ++i) hw[i] = ld_u32(payload + 4 * i);
   if (header_crc60(hw, t1) != ld_u32(payload + 60)) return;
-  if (ld_u32(payload) != (g.codec == 2 ? 0x32564D57u : 0x31564D57u)) return;
+  if (ld_u32(payload) != 0x30564D57u + (g.codec << 24)) return;  // "WMV" + codec digit
   if (ld_u32(payload + 4) != (g.codec | (g.crc_kind << 16) | (g.codec << 24))) return;
   if (ld_u32(payload + 8) != (kChunk << g.tile_log2) || ld_u32(payload + 12) != g.hdr_n) return;
   if (ld_u64(payload + 16) != g.nbytes) return;
@@ -2226,8 +2226,19 @@ __device__ __forceinline__ uint32_t word_of(const uint4 &x, int j) {
   const uint32_t v = j < 2 ? x.x : (j < 4 ? x.y : (j < 6 ? x.z : x.w));
   return (v >> (16 * (j & 1))) & 0xFFFFu;
 }
-__device__ __forceinline__ uint32_t exp_of(uint32_t w) { return (w >> 7) & 255u; }
-__device__ __forceinline__ uint32_t sm_of(uint32_t w) { return ((w >> 8) & 0x80u) | (w & 0x7Fu); }
+// Plane A (Huffman-coded) and plane B (kept raw) of a word, and the word
+// from its planes: format v2 codes the exponent and keeps the sign/mantissa
+// byte; format v3, the bf16 byte-plane split, codes the high byte (sign and
+// the exponent's upper seven bits) and keeps the low byte.
+__device__ __forceinline__ uint32_t pa_of(bool v3, uint32_t w) {
+  return v3 ? w >> 8 : (w >> 7) & 255u;
+}
+__device__ __forceinline__ uint32_t pb_of(bool v3, uint32_t w) {
+  return v3 ? w & 255u : ((w >> 8) & 0x80u) | (w & 0x7Fu);
+}
+__device__ __forceinline__ uint32_t word_from(bool v3, uint32_t a, uint32_t b) {
+  return v3 ? (a << 8) | b : ((b & 0x80u) << 8) | (a << 7) | (b & 0x7Fu);
+}
 
 // Ordering of LDS accesses between the lanes of one wave.
 __device__ __forceinline__ void wave_sync() {
@@ -2377,6 +2388,7 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_plan(
   __shared__ HufWave sw[kHufWaves];
   const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
   HufWave &W = sw[wave];
+  const bool v3 = g.codec == 3;
   const uint32_t n_items = idx ? (*n_idx > g.n_chunks ? 0u : *n_idx) : g.n_chunks;
   for (uint32_t item = blockIdx.x * kHufWaves + wave; item < n_items;
        item += gridDim.x * kHufWaves) {
@@ -2404,7 +2416,7 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_plan(
         const uint32_t i0 = 8u * (512u * q + lane + 64u * h);
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-          if (i0 + j < n) atomicAdd(&H4[4u * exp_of(word_of(x[h], j)) + cp], 1u);
+          if (i0 + j < n) atomicAdd(&H4[4u * pa_of(v3, word_of(x[h], j)) + cp], 1u);
       }
     }
     wave_sync();
@@ -2429,7 +2441,7 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_plan(
           const uint32_t i0 = 8u * (512u * q + lane + 64u * h);
 #pragma unroll
           for (int j = 0; j < 8; ++j)
-            if (i0 + j < n) bits += W.lens[exp_of(word_of(x[h], j))];
+            if (i0 + j < n) bits += W.lens[pa_of(v3, word_of(x[h], j))];
         }
       }
       const uint32_t sb = (bits + 7u) >> 3;
@@ -2506,6 +2518,7 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_write(
   __shared__ HufWave sw[kHufWaves];
   const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
   HufWave &W = sw[wave];
+  const bool v3 = g.codec == 3;
   uint4 *tab_ws = reinterpret_cast<uint4 *>(ws + L.table);
   uint32_t *ecrc = reinterpret_cast<uint32_t *>(ws + L.entry_crc);
   const uint32_t n_items = n_idx ? (*n_idx > g.n_chunks ? 0u : *n_idx) : g.n_chunks;
@@ -2564,8 +2577,8 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_write(
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const uint32_t w = word_of(x, j);
-          e[j >> 2] |= exp_of(w) << (8 * (j & 3));
-          sm[j >> 2] |= sm_of(w) << (8 * (j & 3));
+          e[j >> 2] |= pa_of(v3, w) << (8 * (j & 3));
+          sm[j >> 2] |= pb_of(v3, w) << (8 * (j & 3));
         }
         if (i0 + 8u <= n) {
           *reinterpret_cast<uint2 *>(rec + 16 + i0) = make_uint2(e[0], e[1]);
@@ -2603,9 +2616,9 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_write(
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             const uint32_t w = word_of(x, j);
-            sm[j >> 2] |= sm_of(w) << (8 * (j & 3));
+            sm[j >> 2] |= pb_of(v3, w) << (8 * (j & 3));
             if (hufk && i0 + j < n) {
-              const uint32_t e = exp_of(w), ln = W.lens[e];
+              const uint32_t e = pa_of(v3, w), ln = W.lens[e];
               acc |= (uint64_t)(__builtin_bitreverse32(W.nw[e]) >> (32u - ln)) << nb;
               nb += ln;
               // (the plan counted these bytes: ob stays below sb)
@@ -2946,7 +2959,7 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
             const int j = 2 * q + hh;
             const uint32_t smb = ((j < 4 ? smv[h].x : smv[h].y) >> (8 * (j & 3))) & 255u;
             const uint32_t eb = (e8[j >> 2] >> (8 * (j & 3))) & 255u;
-            const uint32_t w = i0 + j < n ? (((smb & 0x80u) << 8) | (eb << 7) | (smb & 0x7Fu)) : 0u;
+            const uint32_t w = i0 + j < n ? word_from(g.codec == 3, eb, smb) : 0u;
             v |= w << (16 * hh);
           }
           out[q] = v;

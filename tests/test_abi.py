@@ -263,7 +263,7 @@ def test_receive_verify_argument_checks(lib):
     assert rv(h, 4096, a, 4096, nb + 1, P(), a, nb, a, None, a, ws, 0, None, None) == INVALID
     assert rv(h, 4096, a, 4096, nb, P(), a + 8, nb, a, None, a, ws, 0, None, None) == INVALID
     assert rv(h, 4096, a, 4096, nb, P(), a, nb, a, None, a, ws - 1, 0, None, None) == WORKSPACE
-    assert rv(h, 4096, a, 4096, nb, P(codec=3), a, nb, a, None, a, ws, 0, None, None) == INVALID
+    assert rv(h, 4096, a, 4096, nb, P(codec=4), a, nb, a, None, a, ws, 0, None, None) == INVALID
 
 
 def test_format_v2_calls(lib):
@@ -273,7 +273,10 @@ def test_format_v2_calls(lib):
     ws2 = lib.wm_workspace_bytes(nb, P(codec=2))
     assert ws2 >= ws1 + 688 * 4
     assert lib.wm_payload_bound(nb, 4, P(codec=2)) == lib.wm_payload_bound(nb, 4, P())
-    assert lib.wm_workspace_bytes(nb, P(codec=3)) == 0
+    assert lib.wm_workspace_bytes(nb, P(codec=4)) == 0
+    # format v3 (the byte-plane split) shares format v2's kernels and layout
+    assert lib.wm_workspace_bytes(nb, P(codec=3)) == ws2
+    assert lib.wm_payload_bound(nb, 4, P(codec=3)) == lib.wm_payload_bound(nb, 4, P())
     bound = lib.wm_payload_bound(nb, 4, P())
     enc = lib.wm_encode
     # the plans need the larger workspace

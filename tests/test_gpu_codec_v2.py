@@ -1,5 +1,6 @@
-"""GPU parity of format v2 (codec 2: per-chunk canonical Huffman codes of
-the exponent plane in 512 streams) against the oracle: payload bytes,
+"""GPU parity of formats v2 and v3 (codec 2: per-chunk canonical Huffman
+codes of the exponent plane in 512 streams; codec 3: the same of the high
+byte plane, the bf16 byte-plane split) against the oracle: payload bytes,
 decoded bytes, verdict words and record status are equal (tolerance 0) on
 the tiny cache, dirty lists, edge-case states, flipped bits and the
 production-size cache."""
@@ -24,9 +25,14 @@ def wm():
     return _wm
 
 
-def mover(nbytes, kind=0):
-    from paper_2607_10389_amd import Mover, WM_CODEC_EXPHUF
-    return Mover(nbytes, kind, codec=WM_CODEC_EXPHUF)
+@pytest.fixture(params=[2, 3], ids=["v2", "v3"])
+def codec(request):
+    return request.param
+
+
+def mover(nbytes, kind=0, codec=2):
+    from paper_2607_10389_amd import Mover
+    return Mover(nbytes, kind, codec=codec)
 
 
 def dev(a: np.ndarray) -> torch.Tensor:
@@ -35,15 +41,15 @@ def dev(a: np.ndarray) -> torch.Tensor:
     return t
 
 
-def ship(wm, state_h: np.ndarray, kind=0, label=""):
+def ship(wm, state_h: np.ndarray, kind=0, label="", codec=2):
     """Full v2 ship of a host state through the GPU; checks payload, decode
     and verdict against the oracle.  Returns the payload."""
     st = dev(state_h)
-    m = mover(state_h.size, kind)
+    m = mover(state_h.size, kind, codec)
     m.encode(st, with_crc=False)
     torch.cuda.synchronize()
     got = m.payload_host()
-    want = oracle.encode(kind, state_h, CH, None, ORACLE_THREADS, codec=2)
+    want = oracle.encode(kind, state_h, CH, None, ORACLE_THREADS, codec=codec)
     assert got.size == want.size, (label, got.size, want.size)
     if not np.array_equal(got, want):
         bad = np.nonzero(got != want)[0]
@@ -56,10 +62,10 @@ def ship(wm, state_h: np.ndarray, kind=0, label=""):
 
 
 @pytest.mark.parametrize("kind", [0, 1])
-def test_tiny_full_ship(wm, kind):
+def test_tiny_full_ship(wm, kind, codec):
     state = host_bytes(wm_inputs.make_cache(wm_inputs.TINY))
-    got, _ = ship(wm, state, kind, f"tiny kind={kind}")
-    say(f"[v2] tiny ratio {got.size / state.size:.4f}")
+    got, _ = ship(wm, state, kind, f"tiny kind={kind}", codec)
+    say(f"[v{codec}] tiny ratio {got.size / state.size:.4f}")
 
 
 def _edge_states():
@@ -103,34 +109,34 @@ def test_wide_alphabet_states_plan_huf(scale, min_distinct):
 
 
 @pytest.mark.parametrize("name", list(_edge_states().keys()))
-def test_edge_cases(wm, name):
+def test_edge_cases(wm, name, codec):
     state = _edge_states()[name]
-    got, _ = ship(wm, state, 0, name)
+    got, _ = ship(wm, state, 0, name, codec)
     modes = got[64]
-    say(f"[v2] {name}: {state.size} B -> {got.size} B, first record mode {modes}")
+    say(f"[v{codec}] {name}: {state.size} B -> {got.size} B, first record mode {modes}")
 
 
-def test_empty_state(wm):
-    m = mover(0)
+def test_empty_state(wm, codec):
+    m = mover(0, 0, codec)
     state = torch.zeros(16, dtype=torch.uint8, device="cuda")
     m.encode(state, with_crc=False)
     torch.cuda.synchronize()
-    want = oracle.encode(0, np.zeros(0, np.uint8), CH, None, 1, codec=2)
+    want = oracle.encode(0, np.zeros(0, np.uint8), CH, None, 1, codec=codec)
     assert np.array_equal(m.payload_host(), want)
     m.decode()
     assert m.commit(None, scatter=False) == wm.WM_OK
 
 
-def test_dirty_list(wm):
+def test_dirty_list(wm, codec):
     prev, cur, ids = wm_inputs.tiny_step("cuda")
     h = host_bytes(cur)
-    m = mover(h.size)
+    m = mover(h.size, 0, codec)
     m.checksum(cur)
     m.diff(cur, prev)
     m.encode(cur, dirty_only=True)
     torch.cuda.synchronize()
     idx = m.dirty_host()
-    want = oracle.encode(0, h, CH, idx, ORACLE_THREADS, codec=2)
+    want = oracle.encode(0, h, CH, idx, ORACLE_THREADS, codec=codec)
     assert np.array_equal(m.payload_host(), want)
     live = prev.clone().view(-1).view(torch.uint8)
     m.decode()
@@ -139,9 +145,9 @@ def test_dirty_list(wm):
     assert torch.equal(live, cur.view(-1).view(torch.uint8))
 
 
-def test_bit_flips_match_oracle(wm):
+def test_bit_flips_match_oracle(wm, codec):
     state = _edge_states()["tail_4098"]
-    good, m = ship(wm, state, 0, "flips")
+    good, m = ship(wm, state, 0, "flips", codec)
     n_rec = int(good[24:28].view(np.uint32)[0])
     total = int(good[32:40].view(np.uint64)[0])
     table = total - 16 * n_rec
@@ -158,27 +164,27 @@ def test_bit_flips_match_oracle(wm):
             torch.cuda.synchronize()
             v = int(m.verdict.item())
             v_o, _, rs_o = oracle.decode_verify(0, bad, state.size, CH, m.staging.numel(),
-                                                ORACLE_THREADS, codec=2)
+                                                ORACLE_THREADS, codec=codec)
             assert v == v_o and v != 0, (pos, bit, v, v_o)
             if v_o & 3 == 0:
                 assert np.array_equal(u32(m.rec_status)[:n_rec], rs_o[:n_rec]), (pos, bit)
 
 
-def test_production_full_ship(wm):
+def test_production_full_ship(wm, codec):
     state = wm_inputs.make_cache(wm_inputs.PRODUCTION, "cuda")
     nbytes = state.numel() * 2
-    m = mover(nbytes)
+    m = mover(nbytes, 0, codec)
     m.checksum(state)
     m.encode(state)
     torch.cuda.synchronize()
     got = m.payload_host()
     h = host_bytes(state)
-    want = oracle.encode(0, h, CH, None, ORACLE_THREADS, codec=2)
+    want = oracle.encode(0, h, CH, None, ORACLE_THREADS, codec=codec)
     assert got.size == want.size
     if not np.array_equal(got, want):
         bad = np.nonzero(got != want)[0]
         raise AssertionError(f"{bad.size} bytes differ, first {bad[:8].tolist()}")
-    say(f"[v2] production ratio {got.size / nbytes:.5f}")
+    say(f"[v{codec}] production ratio {got.size / nbytes:.5f}")
     del want, h
     m.decode()
     assert m.commit(None, scatter=False) == wm.WM_OK
@@ -186,12 +192,13 @@ def test_production_full_ship(wm):
     assert torch.equal(m.staging[:nbytes], state.view(-1).view(torch.uint8))
 
 
-def test_huf_record_longer_than_raw_is_rejected(wm):
+def test_huf_record_longer_than_raw_is_rejected(wm, codec):
     from test_oracle_codec_v2 import _huf_payload
+    from test_oracle_codec_v3 import _payload
     rng = np.random.default_rng(13)
     st = rng.integers(0, 1 << 16, 3000, dtype=np.uint16).view(np.uint8)
-    p = np.frombuffer(_huf_payload(st), np.uint8)
-    m = mover(st.size)
+    p = np.frombuffer(_huf_payload(st) if codec == 2 else _payload(st, True), np.uint8)
+    m = mover(st.size, 0, codec)
     m.payload[: p.size] = torch.from_numpy(p.copy()).cuda()
     m.decode()
     torch.cuda.synchronize()
@@ -200,17 +207,17 @@ def test_huf_record_longer_than_raw_is_rejected(wm):
 
 
 @pytest.mark.parametrize("kind", [0, 1])
-def test_v2_encode_step(wm, kind):
+def test_v2_encode_step(wm, kind, codec):
     """Format v2 through the fused call: full ship and the tiny 75%-dirty
     step give the oracle's CRCs, global CRC, dirty list and payload, and the
     step's scatter install leaves live equal to the source."""
     prev, cur, ids = wm_inputs.tiny_step("cuda")
     hc, hp = host_bytes(cur), host_bytes(prev)
     n = hc.size
-    m = mover(n, kind)
+    m = mover(n, kind, codec)
     m.encode_step(cur, None)
     torch.cuda.synchronize()
-    assert np.array_equal(m.payload_host(), oracle.encode(kind, hc, CH, None, 1, codec=2))
+    assert np.array_equal(m.payload_host(), oracle.encode(kind, hc, CH, None, 1, codec=codec))
     assert np.array_equal(m.dirty_host(), np.arange(n // CH, dtype=np.uint32))
     crcs, g = oracle.checksum_chunks(kind, hc, CH)
     assert np.array_equal(m.crc_host(), crcs)
@@ -220,13 +227,13 @@ def test_v2_encode_step(wm, kind):
     idx = oracle.diff_dirty(hc, hp, CH)
     assert np.array_equal(m.dirty_host(), idx)
     assert np.array_equal(m.crc_host(), crcs)
-    assert np.array_equal(m.payload_host(), oracle.encode(kind, hc, CH, idx, 1, codec=2))
+    assert np.array_equal(m.payload_host(), oracle.encode(kind, hc, CH, idx, 1, codec=codec))
     live = prev.clone()
     m.decode()
     assert m.commit(live, scatter=True) == wm.WM_OK
     assert torch.equal(live, cur)
     # no dirty_idx, n_dirty or crc_out from the caller: the workspace holds them
-    m2 = mover(n, kind)
+    m2 = mover(n, kind, codec)
     wm.encode_step(cur, prev, n, m2.p, None, None, None, None, m2.payload, m2.payload_bytes,
                    m2.ws_src)
     torch.cuda.synchronize()
@@ -234,16 +241,16 @@ def test_v2_encode_step(wm, kind):
 
 
 @pytest.mark.parametrize("batch", [0, 200_000, 1 << 40])
-def test_v2_pipelined_receive(wm, batch):
+def test_v2_pipelined_receive(wm, batch, codec):
     """Format v2 received in record batches: verdict, record status and
     staging equal the oracle's decode of the same bytes, also with a flipped
     bit in a record and in the table."""
     prev, cur, _ = wm_inputs.tiny_step("cuda")
     hc, hp = host_bytes(cur), host_bytes(prev)
     idx = oracle.diff_dirty(hc, hp, CH)
-    good = oracle.encode(0, hc, CH, idx, 1, codec=2)
+    good = oracle.encode(0, hc, CH, idx, 1, codec=codec)
     n = hc.size
-    m = mover(n)
+    m = mover(n, 0, codec)
     for label, flip in (("clean", None), ("record", 64 + 300), ("table", good.size - 20)):
         bad = good.copy()
         if flip is not None:
@@ -256,7 +263,7 @@ def test_v2_pipelined_receive(wm, batch):
         m.receive(host, bad.size, batch, cs)
         torch.cuda.synchronize()
         v = int(m.verdict.item())
-        v_o, st_o, rs_o = oracle.decode_verify(0, bad, n, CH, m.staging.numel(), 1, codec=2)
+        v_o, st_o, rs_o = oracle.decode_verify(0, bad, n, CH, m.staging.numel(), 1, codec=codec)
         assert v == v_o, (label, v, v_o)
         if v_o & 3 == 0:
             k = idx.size
@@ -268,7 +275,7 @@ def test_v2_pipelined_receive(wm, batch):
             assert flip is not None
 
 
-def test_v2_precopy_rounds(wm):
+def test_v2_precopy_rounds(wm, codec):
     """Pre-copy rounds in format v2: each round's dirty list and payload
     equal the oracle's, and the destination ends equal to the source."""
     spec = wm_inputs.TINY
@@ -276,14 +283,14 @@ def test_v2_precopy_rounds(wm):
     n = spec.nbytes
     shipped = torch.zeros(n, dtype=torch.uint8, device="cuda")
     dest = torch.zeros_like(shipped)
-    m = mover(n)
+    m = mover(n, 0, codec)
     for k in range(4):
         cur_h, shp_h = host_bytes(cur), shipped.cpu().numpy()
         st, nd = m.precopy_round(cur, shipped, dest)
         assert st == wm.WM_OK, k
         got = m.dirty_host()
         assert np.array_equal(got, oracle.diff_dirty(cur_h, shp_h, CH)), k
-        assert np.array_equal(m.payload_host(), oracle.encode(0, cur_h, CH, got, 1, codec=2)), k
+        assert np.array_equal(m.payload_host(), oracle.encode(0, cur_h, CH, got, 1, codec=codec)), k
         crcs, g = oracle.checksum_chunks(0, cur_h, CH)
         assert np.array_equal(m.crc_host(), crcs), k
         assert torch.equal(dest, shipped)

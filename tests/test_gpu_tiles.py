@@ -62,7 +62,7 @@ CASES = [(1 << 17, 3 * (1 << 17) + 100_000),  # short last chunk of two tiles
          (1 << 18, 2 * (1 << 18) + 4 * TILE - 6)]  # last tile short, last chunk 4 tiles
 
 
-@pytest.mark.parametrize("codec", [1, 2])
+@pytest.mark.parametrize("codec", [1, 2, 3])
 @pytest.mark.parametrize("kind", [0, 1])
 @pytest.mark.parametrize("chunk,nbytes", CASES)
 def test_tiles_full_ship_and_lists(wm, chunk, nbytes, kind, codec):
@@ -102,7 +102,7 @@ def test_tiles_full_ship_and_lists(wm, chunk, nbytes, kind, codec):
     assert torch.equal(live, state)
 
 
-@pytest.mark.parametrize("codec", [1, 2])
+@pytest.mark.parametrize("codec", [1, 2, 3])
 @pytest.mark.parametrize("kind", [0, 1])
 def test_tiles_step(wm, kind, codec):
     """Dirtiness is the chunk's: a chunk with one rewritten tile ships all of
