@@ -3003,14 +3003,414 @@ __global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
   }
 }
 
+// ---------------------------------------------- format v2/v3, one record per wave --
+// The Huffman-format decoder with a record per wave: kHwWaves records in
+// flight per workgroup, each wave checking, decoding and verifying its own
+// record with no workgroup barrier, so that one record's dependent steps
+// (table checks, code construction, the symbol-by-symbol decode of each
+// stream) overlap the other waves' work.  Lane l decodes streams q * 64 + l
+// (q = 0..7), which are its 16 bytes of rows 8q..8q+7 in the row layout: a
+// lane's output runs down rows 0..63 in order, so its four CRC column
+// streams take all 64 rows and the lane shifts and the XOR over the wave give
+// the record's CRC without a per-wave step.
+// The 64 streams of group q are contiguous in the record; the wave copies
+// them into an LDS stage with coalesced loads issued one group ahead, and
+// each lane refills its bit buffer from the stage, so the decode waits on
+// LDS only (a refill from device memory would wait behind every store and
+// load issued before it).  A group whose streams overflow the stage, and the
+// last, short record, take a per-symbol path.  Checks and verdict bits are
+// the same as the per-workgroup decoders'.
+constexpr int kHwWaves = 8;
+constexpr uint32_t kHwTab = 4096;    // per wave: decode table, 2^11 u16 entries
+constexpr uint32_t kHwStage = 4096;  // per wave: a group's streams (code order first)
+constexpr uint32_t kHwScratch = kHwTab + kHwStage;
+// waves 0..3 in the low region, waves 4..7 after the CRC tables; tables at
+// multiples of 4096, so an entry's address is the table's base ORed with it
+__device__ __forceinline__ uint32_t hw_scratch(uint32_t wave) {
+  return wave < 4u ? kLdsLow + wave * kHwScratch : kLdsBase + (wave - 4u) * kHwScratch;
+}
+constexpr uint32_t kLdsHufDecodeW = kLdsBase + 4u * kHwScratch;
+static_assert(4u * kHwScratch <= kLdsLowBytes && kLdsHufDecodeW <= 163840 &&
+                  kLdsBase % 4096u == 0 && kHwScratch % 4096u == 0,
+              "record-per-wave decoder LDS fits one CU");
+
+__device__ __forceinline__ uint32_t buf4(Rsrc r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+// The low `take` bytes (0..4) of d.
+__device__ __forceinline__ uint32_t low_bytes(uint32_t d, uint32_t take) {
+  return take >= 4u ? d : d & ((1u << (8u * take)) - 1u);
+}
+
+// Eight words from their plane bytes: byte j of a and b makes word j
+// (words 0..3 from .x, 4..7 from .y), two words per output dword.
+__device__ __forceinline__ void words_from_planes(bool v3, const uint2 &a, const uint2 &b,
+                                                  uint32_t (&out)[4]) {
+#pragma unroll
+  for (int qq = 0; qq < 4; ++qq) {
+    // bytes b_j, a_j, b_j+1, a_j+1: the v3 words as they are
+    const uint32_t p = __builtin_amdgcn_perm(qq < 2 ? a.x : a.y, qq < 2 ? b.x : b.y,
+                                             (qq & 1) ? 0x07030602u : 0x05010400u);
+    // v2: sign bit 7 of b to bit 15, the exponent a to bits 7..14, b's low
+    // seven bits stay (both halves at once)
+    out[qq] = v3 ? p : bfi(0x80008000u, p << 8, bfi(0x007F007Fu, p, p >> 1));
+  }
+}
+
+// One row's words, CRC column steps and store.
+__device__ __forceinline__ void hw_row_out(bool v3, const uint2 &pa, const uint2 &pb,
+                                           uint32_t w0, uint32_t n, bool full, uint32_t len,
+                                           uint8_t *dst, uint32_t (&cv)[4], const GLane &gl) {
+  uint32_t out[4];
+  words_from_planes(v3, pa, pb, out);
+  if (!full && w0 + 8u > n) {  // words past the chunk's end are zero
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (w0 + j >= n) out[j >> 1] &= (j & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+  }
+#pragma unroll
+  for (int c = 0; c < 4; ++c) cv[c] = g_step(cv[c], out[c], gl);
+  dec_store(dst, 2u * w0, len, out);
+}
+
+__global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
+    const uint8_t *__restrict__ payload, ChunkGeom g, uint8_t *__restrict__ staging,
+    uint32_t *__restrict__ rec_status, uint8_t *ws, WsLayout L, uint32_t r0, uint32_t r1) {
+  WsCtl *ctl = reinterpret_cast<WsCtl *>(ws + L.ctl);
+  uint32_t *ecrc = reinterpret_cast<uint32_t *>(ws + L.entry_crc);
+  if (!uniform(ctl->hdr_ok)) return;
+  const uint32_t n_rec = uniform(ctl->n_rec);
+  const uint32_t r_hi = min(r1, n_rec), r_lo = min(r0, r_hi);
+  const uint64_t table_off = ((uint64_t)uniform((uint32_t)(ctl->table_off >> 32)) << 32) |
+                             uniform((uint32_t)ctl->table_off);
+  load_crc_tables(g.crc_kind);
+  __syncthreads();  // the only barrier: the tables are in LDS
+  const CrcTables &T = g_tables[g.crc_kind];
+  const bool v3 = g.codec == 3;
+  const uint32_t wave = uniform(threadIdx.x >> 6), lane = threadIdx.x & 63u;
+  const uint32_t tbase = hw_scratch(wave), sbase = tbase + kHwTab;
+  uint16_t *tab = reinterpret_cast<uint16_t *>(lds_at(tbase));
+  uint8_t *sorted = lds_at(sbase);  // symbols in code order, while the table is built
+  const GLane gl = glane_make();
+  const unsigned long long below = (1ull << lane) - 1ull;
+  for (uint32_t r = r_lo + blockIdx.x * kHwWaves + wave; r < r_hi; r += gridDim.x * kHwWaves) {
+    // ---- table entry (and its neighbours' chunk and offset) and header
+    const uint8_t *e = payload + table_off + 16ull * r;
+    uint32_t ew[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ew[i] = uniform(ld_u32(e + 4 * i));
+    const uint32_t prevc = r > 0 ? uniform(ld_u32(e - 16)) : 0u;
+    const bool has_next = r + 1 < n_rec;
+    const uint32_t nextc = has_next ? uniform(ld_u32(e + 16)) : 0u;
+    const uint64_t end = has_next ? ((uint64_t)uniform(ld_u32(e + 28)) << 32) | uniform(ld_u32(e + 24))
+                                  : table_off;
+    const uint32_t c = ew[0];
+    const uint64_t off = ew[2] | ((uint64_t)ew[3] << 32);
+    const bool tbad = c >= g.n_chunks || (r > 0 && prevc >= c) || (r == 0 && off != 64u) ||
+                      (off & 15u) || off >= end || end > table_off ||
+                      tile_order_bad(g, c, r == 0, has_next, nextc);
+    const uint32_t ec = crc_words(ew, 4);
+    if (lane == 0) ecrc[r] = ec;
+    if (tbad) {
+      if (lane == 0) atomicOr(&ctl->table_bad, 1u);
+      continue;  // no record status for a rejected entry
+    }
+    const uint32_t len = chunk_len(g, c), n = len / 2;
+    const uint64_t rl = end - off;
+    const uint8_t *rec = payload + off;
+    uint32_t st = 0, mode = 0, k = 0, base = 0, sb = 0;
+    if (rl < 16) {
+      st = 4;
+    } else {
+      uint32_t hw[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) hw[i] = uniform(ld_u32(rec + 4 * i));
+      mode = hw[0] & 255u;
+      k = (hw[0] >> 8) & 255u;
+      base = (hw[0] >> 16) & 255u;
+      sb = hw[2];
+      if (crc_words(hw, 3) != hw[3] || (hw[0] >> 24) || hw[1] != n) {
+        st = 4;
+      } else if (mode == 0) {
+        if (k || base || sb || rl != raw_rec_size(n)) st = 4;
+      } else if (mode == 2) {
+        if (k > kHufMaxLen || (k == 0 && sb) || (k && base)) st = 4;
+        else if (huf_rec_size(n, k, sb) >= raw_rec_size(n) || rl != huf_rec_size(n, k, sb)) st = 4;
+      } else {
+        st = 4;
+      }
+    }
+    if (st) {
+      if (lane == 0) {
+        if (rec_status) rec_status[r] = st;
+        atomicOr(&ctl->rec_bits, st);
+      }
+      continue;
+    }
+    const bool hufk = mode == 2 && k > 0;
+    const uint64_t smo = mode == 0 ? 16u + pad16(n) : (hufk ? kHufHead + pad16(sb) : 16u);
+    bool bad = false;
+    // ---- code lengths, their checks and the decode table (HUF, k >= 1):
+    // lane l holds symbols 2l, 2l+1 (nibble byte l) and 128+2l, 129+2l
+    // (nibble byte 64 + l)
+    uint32_t so[8] = {0, 0, 0, 0, 0, 0, 0, 0}, sbq[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    // the streams section (whole, with its padding: no load straddles its
+    // end) and the first group's stage loads, in flight while the table is
+    // built
+    const Rsrc rs = rsrc(rec + kHufHead, hufk ? (uint32_t)pad16(sb) : 0u);
+    uint4 sq0[4] = {};
+    if (hufk) {
+      const uint32_t nb0 = rec[16 + lane], nb1 = rec[16 + 64 + lane];
+      const uint32_t ln[4] = {nb0 & 15u, nb0 >> 4, nb1 & 15u, nb1 >> 4};
+      const uint32_t sym[4] = {2u * lane, 2u * lane + 1u, 128u + 2u * lane, 129u + 2u * lane};
+      uint32_t kr = 0, mx = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (ln[j] > k) bad = true;
+        if (ln[j]) kr += 1u << (kHufMaxLen - min(ln[j], kHufMaxLen));
+        mx = max(mx, ln[j]);
+      }
+      const uint32_t kraft = uniform(__builtin_amdgcn_readlane(wave_incl_scan(kr), 63));
+      const uint32_t longest = uniform(wave_max(mx));
+      // stream byte counts and offsets: stream q * 64 + lane follows the
+      // streams before it
+      uint32_t tot = 0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        sbq[q] = rec[16 + 128 + q * 64 + lane];
+        const uint32_t incl = wave_incl_scan(sbq[q]);
+        so[q] = tot + incl - sbq[q];
+        tot += uniform(__builtin_amdgcn_readlane(incl, 63));
+      }
+      bool hufbad = uniform(__ballot(bad) != 0) || kraft != (1u << kHufMaxLen) || longest != k ||
+                    tot != sb;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sq0[i] = buf16(rs, 1024u * i + 16u * lane);
+      if (!hufbad) {
+        // canonical codes: per length, consecutive values in symbol order;
+        // the left-aligned 11-bit values of length b fill [lb[b], lb[b+1])
+        uint32_t first = 0, prev = 0, start = 0;
+        uint32_t lb[kHufMaxLen + 1], stb[kHufMaxLen + 1], cnb[kHufMaxLen + 1];
+#pragma unroll
+        for (uint32_t b = 1; b <= kHufMaxLen; ++b) {
+          const unsigned long long m0 = __ballot(ln[0] == b), m1 = __ballot(ln[1] == b);
+          const unsigned long long m2 = __ballot(ln[2] == b), m3 = __ballot(ln[3] == b);
+          const uint32_t half = (uint32_t)(__popcll(m0) + __popcll(m1));
+          const uint32_t cnt = half + (uint32_t)(__popcll(m2) + __popcll(m3));
+          first = (first + prev) << 1;
+          const uint32_t rk0 = (uint32_t)(__popcll(m0 & below) + __popcll(m1 & below));
+          const uint32_t rk2 = half + (uint32_t)(__popcll(m2 & below) + __popcll(m3 & below));
+          if (ln[0] == b) sorted[start + rk0] = (uint8_t)sym[0];
+          if (ln[1] == b) sorted[start + rk0 + (ln[0] == b ? 1u : 0u)] = (uint8_t)sym[1];
+          if (ln[2] == b) sorted[start + rk2] = (uint8_t)sym[2];
+          if (ln[3] == b) sorted[start + rk2 + (ln[2] == b ? 1u : 0u)] = (uint8_t)sym[3];
+          lb[b] = first << (kHufMaxLen - b);
+          stb[b] = start;
+          cnb[b] = cnt;
+          start += cnt;
+          prev = cnt;
+        }
+        wave_sync();
+        // table entry p: the code whose first bits (lowest first) are p's;
+        // the entries of length-b codes, in left-aligned order, take the
+        // symbols of that length 2^(11-b) entries each
+#pragma unroll
+        for (uint32_t b = 1; b <= kHufMaxLen; ++b) {
+          const uint32_t run = uniform(cnb[b] << (kHufMaxLen - b));
+          for (uint32_t t = lane; t < run; t += 64u) {
+            const uint32_t v = lb[b] + t;
+            tab[__builtin_bitreverse32(v) >> (32u - kHufMaxLen)] =
+                (uint16_t)(sorted[stb[b] + (t >> (kHufMaxLen - b))] | (b << 8));
+          }
+        }
+        wave_sync();
+      }
+      if (hufbad) bad = true;
+    }
+    const bool hok = !hufk || uniform(__ballot(bad) == 0);
+    // plane ranges cover whole sections with their padding (part of the
+    // record), so no piece straddles a range end; padding bytes are checked
+    // below
+    const Rsrc rb = rsrc(rec + smo, (uint32_t)pad16(n));                       // plane B
+    const Rsrc ra = rsrc(rec + 16, mode == 0 ? (uint32_t)pad16(n) : 0u);       // RAW plane A
+    uint8_t *dst = staging + (uint64_t)r * kChunk;
+    uint32_t cv[4] = {0, 0, 0, 0};
+    const bool dec = hufk && hok;
+    const bool full = n == kChunk / 2;
+    if (!dec) {
+      // ---- RAW (plane A stored) or a single exponent / high byte
+#pragma unroll 1
+      for (uint32_t q = 0; q < 8u; ++q) {
+        uint2 pa[8], pb[8];
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+          const uint32_t w0 = (8u * q + h) * 512u + 8u * lane;
+          pb[h] = buf8(rb, w0);
+          pa[h] = mode == 0 ? buf8(ra, w0) : make_uint2(base * 0x01010101u, base * 0x01010101u);
+        }
+#pragma unroll
+        for (int h = 0; h < 8; ++h)
+          hw_row_out(v3, pa[h], pb[h], (8u * q + h) * 512u + 8u * lane, n, full, len, dst, cv, gl);
+      }
+    } else {
+      // ---- Huffman streams: group q's bytes [A, A + 4096) staged as 4 KiB
+      // (lane l's 16 bytes of each KiB); the next group's loads are in
+      // flight while this one decodes and enter the stage after it
+      const uint32_t s4 = k <= 8u ? 1u : 0u;  // 4 symbols per refill check, else 2
+      const uint32_t *stg = reinterpret_cast<const uint32_t *>(lds_at(sbase));
+      uint32_t A = 0;  // group 0 starts the section
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<uint4 *>(lds_at(sbase + 1024u * i + 16u * lane)) = sq0[i];
+      wave_sync();
+#pragma unroll 1
+      for (uint32_t q = 0; q < 8u; ++q) {
+        const uint32_t soq = so[q], sbl = sbq[q];
+        const bool fits = uniform(__builtin_amdgcn_readlane(soq + sbl, 63)) - A <= kHwStage;
+        const bool more = q < 7u;
+        uint2 pb[8], pa[8];
+#pragma unroll
+        for (int h = 0; h < 8; ++h) pb[h] = buf8(rb, (8u * q + h) * 512u + 8u * lane);
+        uint4 sq[4];
+        uint32_t an = 0;
+        if (more) {
+          an = uniform(__builtin_amdgcn_readlane(so[q + 1u], 0)) & ~15u;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) sq[i] = buf16(rs, an + 1024u * i + 16u * lane);
+        }
+        // the lane's stream: bits in acc (next bit lowest, nb of them),
+        // whole dwords taken while fewer than 32 bits are held, so the bytes
+        // after the stream's end may enter acc but are never decoded from a
+        // well-formed stream: the bits used, 8 (pos - pos0) - nb, must fill
+        // exactly the stream's bytes
+        uint64_t acc;
+        int32_t nb;
+        uint32_t pos = soq - A;
+        const uint32_t pos0 = pos;
+        if (fits && full) {
+          auto rd = [&](uint32_t p) -> uint32_t { return stg[min(p, kHwStage - 4u) >> 2]; };
+          acc = rd(pos) >> (8u * (pos & 3u));  // up to the first dword boundary
+          nb = (int32_t)(32u - 8u * (pos & 3u));
+          pos = (pos & ~3u) + 4u;
+          uint32_t nxt = rd(pos);
+          // branch-free: some lane of the wave needs bits at nearly every check
+          auto refill = [&]() {
+            const bool rf = nb < 32;
+            acc |= (uint64_t)(rf ? nxt : 0u) << nb;
+            nb += rf ? 32 : 0;
+            pos += rf ? 4u : 0u;
+            nxt = rd(pos);
+          };
+          auto symbol = [&]() -> uint32_t {
+            const uint32_t ent = tab[(uint32_t)acc & ((1u << kHufMaxLen) - 1u)];
+            const uint32_t ln = ent >> 8;
+            acc >>= ln;
+            nb -= (int32_t)ln;
+            return ent & 255u;
+          };
+          if (s4) {
+#pragma unroll
+            for (int h = 0; h < 8; ++h) {
+              uint32_t a8[2];
+#pragma unroll
+              for (int j = 0; j < 2; ++j) {
+                refill();
+                const uint32_t x0 = symbol(), x1 = symbol(), x2 = symbol(), x3 = symbol();
+                a8[j] = x0 | (x1 << 8) | (x2 << 16) | (x3 << 24);
+              }
+              pa[h] = make_uint2(a8[0], a8[1]);
+            }
+          } else {
+#pragma unroll
+            for (int h = 0; h < 8; ++h) {
+              uint32_t a8[2];
+#pragma unroll
+              for (int j = 0; j < 2; ++j) {
+                refill();
+                const uint32_t x0 = symbol(), x1 = symbol();
+                refill();
+                const uint32_t x2 = symbol(), x3 = symbol();
+                a8[j] = x0 | (x1 << 8) | (x2 << 16) | (x3 << 24);
+              }
+              pa[h] = make_uint2(a8[0], a8[1]);
+            }
+          }
+        } else {
+          // per symbol: words past the chunk's end have none; bytes from the
+          // stage, or from the record where the group overflows it
+          auto rd = [&](uint32_t p) -> uint32_t {
+            return fits ? stg[min(p, kHwStage - 4u) >> 2] : buf4(rs, A + (p & ~3u));
+          };
+          acc = rd(pos) >> (8u * (pos & 3u));
+          nb = (int32_t)(32u - 8u * (pos & 3u));
+          pos = (pos & ~3u) + 4u;
+#pragma unroll
+          for (int h = 0; h < 8; ++h) {
+            const uint32_t w0 = (8u * q + h) * 512u + 8u * lane;
+            uint32_t a8[2] = {0, 0};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              if (w0 + j < n) {
+                if (nb < 32) {
+                  acc |= (uint64_t)rd(pos) << nb;
+                  nb += 32;
+                  pos += 4u;
+                }
+                const uint32_t ent = tab[(uint32_t)acc & ((1u << kHufMaxLen) - 1u)];
+                const uint32_t ln = ent >> 8;
+                acc >>= ln;
+                nb -= (int32_t)ln;
+                a8[j >> 2] |= (ent & 255u) << (8 * (j & 3));
+              }
+            }
+            pa[h] = make_uint2(a8[0], a8[1]);
+          }
+        }
+        // exactly the stream's bytes, the last one's unused bits zero
+        const uint32_t used = 8u * (pos - pos0) - (uint32_t)nb;
+        if ((used + 7u) / 8u != sbl) bad = true;
+        if ((used & 7u) && ((uint32_t)acc & ((1u << (8u - (used & 7u))) - 1u))) bad = true;
+        if (more) {  // the next group enters the stage once this one is read
+          wave_sync();
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            *reinterpret_cast<uint4 *>(lds_at(sbase + 1024u * i + 16u * lane)) = sq[i];
+          wave_sync();
+          A = an;
+        }
+#pragma unroll
+        for (int h = 0; h < 8; ++h)
+          hw_row_out(v3, pa[h], pb[h], (8u * q + h) * 512u + 8u * lane, n, full, len, dst, cv, gl);
+      }
+    }
+    // ---- zero padding after each section
+    if (lane < 16u && n + lane < pad16(n) && rec[smo + n + lane]) bad = true;
+    if (mode == 0 && lane >= 16u && lane < 32u && n + lane - 16u < pad16(n) &&
+        rec[16 + n + lane - 16u])
+      bad = true;
+    if (hufk && lane >= 32u && lane < 48u && sb + lane - 32u < pad16(sb) &&
+        rec[kHufHead + sb + lane - 32u])
+      bad = true;
+    // ---- the record's CRC against its receipt
+    const uint32_t crc = finish_crc(lane_fold(lane_merge(cv[0], cv[1], cv[2], cv[3])), len, g, T);
+    const uint32_t stf = __ballot(bad) ? 4u : (crc != ew[1] ? 8u : 0u);
+    if (lane == 0) {
+      if (rec_status) rec_status[r] = stf;
+      if (stf) atomicOr(&ctl->rec_bits, stf);
+    }
+  }
+}
+
 int set_kernel_attributes() {
-  const void *kern[5] = {reinterpret_cast<const void *>(&k_checksum),
+  const void *kern[6] = {reinterpret_cast<const void *>(&k_checksum),
                          reinterpret_cast<const void *>(&k_encode<false>),
                          reinterpret_cast<const void *>(&k_encode<true>),
                          reinterpret_cast<const void *>(&k_decode),
-                         reinterpret_cast<const void *>(&k_huf_decode)};
-  const uint32_t bytes[5] = {kLdsBase, kLdsEncode, kLdsEncode, kLdsDecode, kLdsHufDecode};
-  for (int i = 0; i < 5; ++i) {
+                         reinterpret_cast<const void *>(&k_huf_decode),
+                         reinterpret_cast<const void *>(&k_huf_decode_w)};
+  const uint32_t bytes[6] = {kLdsBase, kLdsEncode, kLdsEncode, kLdsDecode, kLdsHufDecode,
+                             kLdsHufDecodeW};
+  for (int i = 0; i < 6; ++i) {
     hipError_t e = hipFuncSetAttribute(kern[i], hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)bytes[i]);
     if (e != hipSuccess) return (int)e;
@@ -3455,8 +3855,9 @@ int launch_decode_records_v2(const void *payload, const ChunkGeom &g, void *stag
                              uint32_t *rec_status, void *ws, const WsLayout &L, int n_cu,
                              uint32_t r0, uint32_t r1, void *stream) {
   if (r1 <= r0 || !g.n_chunks) return 0;
-  const uint32_t grid = min((uint32_t)n_cu, min(r1 - r0, g.n_chunks));
-  hipLaunchKernelGGL(k_huf_decode, dim3(grid), dim3(kThreads + 64), kLdsHufDecode, S(stream),
+  const uint32_t recs = min(r1 - r0, g.n_chunks);
+  const uint32_t grid = min((uint32_t)n_cu, (recs + kHwWaves - 1u) / kHwWaves);
+  hipLaunchKernelGGL(k_huf_decode_w, dim3(grid), dim3(64 * kHwWaves), kLdsHufDecodeW, S(stream),
                      static_cast<const uint8_t *>(payload), g, static_cast<uint8_t *>(staging),
                      rec_status, static_cast<uint8_t *>(ws), L, r0, r1);
   return (int)hipGetLastError();
