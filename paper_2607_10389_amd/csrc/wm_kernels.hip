@@ -2656,353 +2656,6 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_write(
   }
 }
 
-// Decoder state in the low LDS region: decode table, code lengths, symbols
-// in code order, lane CRC values, and one record's fields.
-constexpr uint32_t kHdTab = 0;                 // 2^kHufMaxLen u16: symbol | length << 8
-constexpr uint32_t kHdLens = 4096;             // u8[256]
-constexpr uint32_t kHdSorted = kHdLens + 256;  // u8[256]
-constexpr uint32_t kHdU = kHdSorted + 256;     // u32[kThreads]
-constexpr uint32_t kHdMeta = kHdU + 4 * kThreads;
-constexpr uint32_t kLdsHufStreams = kLdsBase;  // the record's streams (under 32 KiB)
-constexpr uint32_t kLdsHufDecode = kLdsBase + 32768;
-static_assert(kLdsHufDecode <= 163840, "v2 decoder LDS fits one CU");
-
-struct HufMeta {
-  uint32_t st, mode, k, base, n, sb, c, src, len, off_lo, off_hi;
-  uint32_t kraft, maxlen, bad, hufbad;
-  uint32_t bl[kHufMaxLen + 1], first[kHufMaxLen + 1], start[kHufMaxLen + 1];
-  uint32_t wsum[kWaves];
-  uint32_t wcnt[4][kHufMaxLen + 1];  // symbols of each length per 64 symbols
-};
-static_assert(kHdMeta + sizeof(HufMeta) <= kLdsLowBytes, "v2 decoder scratch fits the low region");
-
-// What the control lane reads of record r: its table entry, the previous
-// entry's chunk, the record's end, and its header when the entry's offsets
-// leave room for one (read only then).
-struct HufFetch {
-  uint32_t ew[4], prevc, nextc, hdr[4], has_hdr;
-  uint64_t end;
-};
-__device__ __forceinline__ HufFetch huf_fetch(const uint8_t *__restrict__ payload, uint64_t table_off,
-                                              uint32_t n_rec, uint32_t r) {
-  HufFetch f;
-  const uint8_t *e = payload + table_off + 16ull * r;
-  for (int i = 0; i < 4; ++i) f.ew[i] = ld_u32(e + 4 * i);
-  f.prevc = r > 0 ? ld_u32(e - 16) : 0u;
-  f.end = r + 1 < n_rec ? ld_u64(e + 24) : table_off;
-  f.nextc = r + 1 < n_rec ? ld_u32(e + 16) : 0u;
-  const uint64_t off = f.ew[2] | ((uint64_t)f.ew[3] << 32);
-  f.has_hdr = !(off & 15u) && off < f.end && f.end <= table_off && f.end - off >= 16u;
-  for (int i = 0; i < 4; ++i) f.hdr[i] = f.has_hdr ? ld_u32(payload + off + 4 * i) : 0u;
-  return f;
-}
-
-// One record per workgroup step: the control lane checks the table entry and
-// the record header; the data waves build the decode table, decode their
-// streams, assemble the words, store them and take the CRC lane values; the
-// control wave folds the CRC and records the status.
-__global__ __launch_bounds__(kThreads + 64) void k_huf_decode(
-    const uint8_t *__restrict__ payload, ChunkGeom g, uint8_t *__restrict__ staging,
-    uint32_t *__restrict__ rec_status, uint8_t *ws, WsLayout L, uint32_t r0, uint32_t r1) {
-  WsCtl *ctl = reinterpret_cast<WsCtl *>(ws + L.ctl);
-  uint32_t *ecrc = reinterpret_cast<uint32_t *>(ws + L.entry_crc);
-  if (!uniform(ctl->hdr_ok)) return;
-  // records [r0, r1) of the table, clamped to its length (a payload decoded
-  // in batches as it arrives)
-  const uint32_t n_rec = uniform(ctl->n_rec);
-  const uint32_t r_hi = min(r1, n_rec), r_lo = min(r0, r_hi);
-  const uint64_t table_off = ctl->table_off;
-  load_crc_tables(g.crc_kind);
-  __syncthreads();
-  const CrcTables &T = g_tables[g.crc_kind];
-  HufMeta &M = *reinterpret_cast<HufMeta *>(lds_at(kHdMeta));
-  uint16_t *tab = reinterpret_cast<uint16_t *>(lds_at(kHdTab));
-  uint8_t *lens = lds_at(kHdLens);
-  uint8_t *sorted = lds_at(kHdSorted);
-  uint32_t *U = reinterpret_cast<uint32_t *>(lds_at(kHdU));
-  const uint32_t *S32 = reinterpret_cast<const uint32_t *>(lds_at(kLdsHufStreams));
-  const uint32_t t = threadIdx.x;
-  const bool is_ctl = t >= (uint32_t)kThreads;
-  const GLane gl = glane_make();
-  const Lane l0 = lane_info();
-  HufFetch fn;  // control lane: the next record's reads, issued a step ahead
-  if (t == (uint32_t)kThreads && r_lo + blockIdx.x < r_hi)
-    fn = huf_fetch(payload, table_off, n_rec, r_lo + blockIdx.x);
-  for (uint32_t r = r_lo + blockIdx.x; r < r_hi; r += gridDim.x) {
-    const Lane l = lane_fresh(l0);
-    if (t == (uint32_t)kThreads) {
-      const HufFetch f = fn;
-      const uint32_t *ew = f.ew;
-      const uint32_t c = ew[0];
-      const uint64_t off = ew[2] | ((uint64_t)ew[3] << 32);
-      const uint64_t end = f.end;
-      const bool tbad = c >= g.n_chunks || (r > 0 && f.prevc >= c) ||
-                        (r == 0 && off != 64u) || (off & 15u) || off >= end || end > table_off ||
-                        tile_order_bad(g, c, r == 0, r + 1 < n_rec, f.nextc);
-      ecrc[r] = crc_words(ew, 4);
-      M.bad = M.hufbad = M.kraft = M.maxlen = 0;
-      for (uint32_t b = 0; b <= kHufMaxLen; ++b) M.bl[b] = 0;
-      M.st = kMetaSkip;
-      if (tbad) {
-        atomicOr(&ctl->table_bad, 1u);
-      } else {
-        const uint32_t len = chunk_len(g, c), n = len / 2;
-        const uint64_t rl = end - off;
-        uint32_t st = 0, mode = 0, k = 0, base = 0, sb = 0;
-        if (rl < 16 || !f.has_hdr) {
-          st = 4;
-        } else {
-          const uint32_t *hw = f.hdr;
-          mode = hw[0] & 255u;
-          k = (hw[0] >> 8) & 255u;
-          base = (hw[0] >> 16) & 255u;
-          sb = hw[2];
-          if (crc_words(hw, 3) != hw[3] || (hw[0] >> 24) || hw[1] != n) {
-            st = 4;
-          } else if (mode == 0) {
-            if (k || base || sb || rl != raw_rec_size(n)) st = 4;
-          } else if (mode == 2) {
-            if (k > kHufMaxLen || (k == 0 && sb) || (k && base)) st = 4;
-            else if (huf_rec_size(n, k, sb) >= raw_rec_size(n) || rl != huf_rec_size(n, k, sb)) st = 4;
-          } else {
-            st = 4;
-          }
-        }
-        M.st = st;
-        M.mode = mode;
-        M.k = k;
-        M.base = base;
-        M.n = n;
-        M.sb = sb;
-        M.c = c;
-        M.src = ew[1];
-        M.len = len;
-        M.off_lo = (uint32_t)off;
-        M.off_hi = (uint32_t)(off >> 32);
-      }
-    }
-    __syncthreads();
-    if (t == (uint32_t)kThreads && r + gridDim.x < r_hi)
-      fn = huf_fetch(payload, table_off, n_rec, r + gridDim.x);
-    const uint32_t st0 = uniform(M.st), mode = uniform(M.mode), k = uniform(M.k);
-    const uint32_t n = uniform(M.n), sb = uniform(M.sb);
-    const uint64_t off = ((uint64_t)uniform(M.off_hi) << 32) | uniform(M.off_lo);
-    const uint8_t *rec = payload + off;
-    const bool huf = st0 == 0 && mode == 2 && k >= 1;
-    // every load of the record at once: code lengths, stream byte counts,
-    // the streams (into LDS), and the lane's sign/mantissa (RAW: exponent)
-    // bytes, 8 per row
-    uint32_t sb_t = 0;
-    uint2 smv[kRows], exv[kRows];
-    const uint64_t smo = mode == 0 ? 16u + pad16(n) : (k ? kHufHead + pad16(sb) : 16u);
-    if (!is_ctl) {
-      if (huf) {
-        if (t < 128u) {
-          const uint32_t b = rec[16 + t];
-          lens[2 * t] = (uint8_t)(b & 15u);
-          lens[2 * t + 1] = (uint8_t)(b >> 4);
-        }
-        sb_t = rec[16 + 128 + t];
-        // (sb < 32 KiB for a record shorter than RAW)
-        const uint8_t *src = rec + kHufHead;
-        const Rsrc rs = rsrc(src, sb);
-        for (uint32_t q = t; 16u * q < sb; q += kThreads) {
-          uint4 v = 16u * q + 16u <= sb ? buf16(rs, 16u * q) : load16_partial(src + 16u * q, sb - 16u * q);
-          *reinterpret_cast<uint4 *>(lds_at(kLdsHufStreams + 16u * q)) = v;
-        }
-      }
-      const bool ld = st0 == 0 && (mode == 0 || mode == 2);
-      const Rsrc rsm = rsrc(rec + smo, ld ? n : 0u);
-      const Rsrc rex = rsrc(rec + 16, ld && mode == 0 ? n : 0u);
-      const uint32_t w0 = l.off0 >> 1;
-#pragma unroll
-      for (int h = 0; h < kRows; ++h) {
-        const uint32_t i0 = w0 + h * (kRow / 2);
-        smv[h] = buf8(rsm, i0);
-        exv[h] = buf8(rex, i0);
-        if (ld && i0 < n && i0 + 8u > n) {  // the piece that straddles n, bytewise
-          const uint4 v = load16_partial(rec + smo + i0, n - i0);
-          smv[h] = make_uint2(v.x, v.y);
-          if (mode == 0) {
-            const uint4 e = load16_partial(rec + 16 + i0, n - i0);
-            exv[h] = make_uint2(e.x, e.y);
-          }
-        }
-      }
-    }
-    __syncthreads();
-    uint32_t incl = 0, within = 0;
-    if (huf && !is_ctl) {
-      if (t < 256u) {
-        const uint32_t ln = lens[t];
-        if (ln > k) atomicOr(&M.hufbad, 1u);
-        if (ln) {
-          atomicAdd(&M.kraft, 1u << (kHufMaxLen - min(ln, kHufMaxLen)));
-          atomicMax(&M.maxlen, ln);
-          atomicAdd(&M.bl[min(ln, kHufMaxLen)], 1u);
-        }
-        // the symbol's rank among the same length within its 64 symbols
-#pragma unroll
-        for (uint32_t b = 1; b <= kHufMaxLen; ++b) {
-          const unsigned long long msk = __ballot(ln == b);
-          if (ln == b) within = lanes_below(msk);
-          if (l.lane == 0) M.wcnt[l.wave][b] = (uint32_t)__popcll(msk);
-        }
-      }
-      incl = wave_incl_scan(sb_t);
-      if (l.lane == 63u) M.wsum[l.wave] = incl;
-    }
-    __syncthreads();
-    uint32_t so = 0;
-    if (huf && !is_ctl) {
-      uint32_t tot = 0;
-      so = incl - sb_t;
-      for (uint32_t w = 0; w < (uint32_t)kWaves; ++w) {
-        const uint32_t v = M.wsum[w];
-        if (w < l.wave) so += v;
-        tot += v;
-      }
-      if (t == 0) {  // complete code of longest length k; first code and rank base per length
-        if (M.kraft != (1u << kHufMaxLen) || M.maxlen != k || tot != sb) M.hufbad = 1;
-        uint32_t cd = 0, at = 0;
-        for (uint32_t b = 1; b <= kHufMaxLen; ++b) {
-          cd = (cd + (b > 1 ? M.bl[b - 1] : 0u)) << 1;
-          M.first[b] = cd;
-          M.start[b] = at;
-          at += M.bl[b];
-        }
-      }
-    }
-    __syncthreads();
-    const bool hok = huf && uniform(M.hufbad) == 0;
-    if (hok && !is_ctl) {
-      if (t < 256u && lens[t]) {  // symbols in code order
-        const uint32_t ln = lens[t];
-        uint32_t rank = within;  // independent reads, not a chain of round trips
-#pragma unroll
-        for (uint32_t w = 0; w < (uint32_t)kWaves - 1u; ++w) rank += w < l.wave ? M.wcnt[w][ln] : 0u;
-        sorted[M.start[ln] + rank] = (uint8_t)t;
-      }
-    }
-    __syncthreads();
-    if (hok && !is_ctl) {  // entry p: the code whose bits, first bit lowest, are p's low bits
-      uint32_t fb[kHufMaxLen + 1], cb[kHufMaxLen + 1], sbx[kHufMaxLen + 1];
-#pragma unroll
-      for (uint32_t b = 1; b <= kHufMaxLen; ++b) {
-        fb[b] = uniform(M.first[b]);
-        cb[b] = b <= k ? uniform(M.bl[b]) : 0u;
-        sbx[b] = uniform(M.start[b]);
-      }
-      for (uint32_t p = t; p < (1u << kHufMaxLen); p += kThreads) {
-        uint32_t ent = 0;
-        const uint32_t rp = __builtin_bitreverse32(p);
-#pragma unroll
-        for (uint32_t b = kHufMaxLen; b >= 1; --b) {  // the shortest match is the code
-          const uint32_t q = (rp >> (32u - b)) - fb[b];
-          if (q < cb[b]) ent = (sbx[b] + q) | (b << 8) | 0x10000u;
-        }
-        tab[p] = (ent & 0x10000u) ? (uint16_t)(sorted[ent & 255u] | (ent & 0xF00u)) : (uint16_t)0;
-      }
-    }
-    __syncthreads();
-    if (!is_ctl) {
-      const uint32_t len = uniform(M.len), base = uniform(M.base), w0 = l.off0 >> 1;
-      const bool ok = st0 == 0 && (mode == 0 || (mode == 2 && (k == 0 || hok)));
-      const bool dec = ok && mode == 2 && k;
-      uint32_t bad = 0;
-      // the lane's stream: bits so far in acc (next bit lowest), bytes [pos, end)
-      uint64_t acc = 0;
-      uint32_t nb = 0, used = 0, pos = so;
-      const uint32_t end = so + (dec ? sb_t : 0u);
-      uint4 d[kRows];
-#pragma unroll
-      for (int h = 0; h < kRows; ++h) {
-        const uint32_t i0 = w0 + h * (kRow / 2);
-        uint32_t e8[2] = {0, 0};
-        if (mode == 0) {
-          e8[0] = exv[h].x;
-          e8[1] = exv[h].y;
-        } else if (k == 0) {
-          e8[0] = e8[1] = base * 0x01010101u;
-        } else if (dec) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            if (i0 + j < n) {
-              if (nb < kHufMaxLen && pos < end) {  // 32 more bits (zeros past the stream)
-                const uint32_t a = pos >> 2;
-                uint32_t v = __builtin_amdgcn_alignbit(S32[a + 1], S32[a], (pos & 3u) * 8u);
-                const uint32_t take = min(end - pos, 4u);
-                if (take < 4u) v &= (1u << (8u * take)) - 1u;
-                acc |= (uint64_t)v << nb;
-                nb += 8u * take;
-                pos += take;
-              }
-              const uint32_t ent = tab[(uint32_t)acc & ((1u << kHufMaxLen) - 1u)];
-              uint32_t ln = ent >> 8;
-              if (ln == 0 || ln > nb) {  // past the stream (or no such code)
-                bad = 1;
-                ln = min(max(ln, 1u), nb);
-              }
-              acc >>= ln;
-              nb -= ln;
-              used += ln;
-              e8[j >> 2] |= (ent & 255u) << (8 * (j & 3));
-            }
-          }
-        }
-        uint32_t out[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          uint32_t v = 0;
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const int j = 2 * q + hh;
-            const uint32_t smb = ((j < 4 ? smv[h].x : smv[h].y) >> (8 * (j & 3))) & 255u;
-            const uint32_t eb = (e8[j >> 2] >> (8 * (j & 3))) & 255u;
-            const uint32_t w = i0 + j < n ? word_from(g.codec == 3, eb, smb) : 0u;
-            v |= w << (16 * hh);
-          }
-          out[q] = v;
-        }
-        d[h] = make_uint4(out[0], out[1], out[2], out[3]);
-        dec_store(staging + (uint64_t)r * kChunk, l.off0 + h * kRow, len, out);
-      }
-      if (dec) {  // exactly the stream's bytes, the last one's unused bits zero
-        if ((used + 7u) / 8u != sb_t) bad = 1;
-        if ((used & 7u) && (acc & ((1u << (8u - (used & 7u))) - 1u))) bad = 1;
-      }
-      if (ok) {  // zero padding after each section
-        if (t < 16u && n + t < pad16(n) && rec[smo + n + t]) bad = 1;
-        if (mode == 0 && t >= 16u && t < 32u && n + t - 16u < pad16(n) && rec[16 + n + t - 16u]) bad = 1;
-        if (dec && t >= 32u && t < 48u && sb + t - 32u < pad16(sb) && rec[kHufHead + sb + t - 32u])
-          bad = 1;
-      }
-      if (bad) atomicOr(&M.bad, 1u);
-      U[t] = lane_value(d, gl);
-    }
-    __syncthreads();
-    if (is_ctl) {
-      const uint32_t st = uniform(M.st);
-      if (st != kMetaSkip) {
-        uint32_t stf = st;
-        if (stf == 0) {
-          uint32_t acc2 = U[l.lane];
-#pragma unroll
-          for (int w = 1; w < kWaves; ++w) acc2 = tab4x(kLdsWaveStep, acc2, U[w * 64 + l.lane]);
-          const uint32_t crc = finish_crc(lane_fold(acc2), uniform(M.len), g, T);
-          const bool bd = uniform(M.bad) != 0 || (mode == 2 && k && uniform(M.hufbad) != 0);
-          stf = bd ? 4u : (crc != uniform(M.src) ? 8u : 0u);
-        }
-        if (l.lane == 0) {
-          if (rec_status) rec_status[r] = stf;
-          if (stf) atomicOr(&ctl->rec_bits, stf);
-        }
-      }
-    }
-    __syncthreads();
-  }
-}
-
 // ---------------------------------------------- format v2/v3, one record per wave --
 // The Huffman-format decoder with a record per wave: kHwWaves records in
 // flight per workgroup, each wave checking, decoding and verifying its own
@@ -3024,6 +2677,7 @@ constexpr int kHwWaves = 8;
 constexpr uint32_t kHwTab = 4096;    // per wave: decode table, 2^11 u16 entries
 constexpr uint32_t kHwStage = 4096;  // per wave: a group's streams (code order first)
 constexpr uint32_t kHwScratch = kHwTab + kHwStage;
+constexpr uint32_t kHwOverrun = 64u * 11u / 8u + 8u;  // bytes a stream's reads may pass its end
 // waves 0..3 in the low region, waves 4..7 after the CRC tables; tables at
 // multiples of 4096, so an entry's address is the table's base ORed with it
 __device__ __forceinline__ uint32_t hw_scratch(uint32_t wave) {
@@ -3042,9 +2696,15 @@ __device__ __forceinline__ uint32_t low_bytes(uint32_t d, uint32_t take) {
   return take >= 4u ? d : d & ((1u << (8u * take)) - 1u);
 }
 
+// (m & a) | (~m & b) in one three-input logic op (truth table 0xCA).
+__device__ __forceinline__ uint32_t bitsel(uint32_t m, uint32_t a, uint32_t b) {
+  return __builtin_amdgcn_bitop3_b32(m, a, b, 0xCA);
+}
+
 // Eight words from their plane bytes: byte j of a and b makes word j
 // (words 0..3 from .x, 4..7 from .y), two words per output dword.
-__device__ __forceinline__ void words_from_planes(bool v3, const uint2 &a, const uint2 &b,
+template <bool V3>
+__device__ __forceinline__ void words_from_planes(const uint2 &a, const uint2 &b,
                                                   uint32_t (&out)[4]) {
 #pragma unroll
   for (int qq = 0; qq < 4; ++qq) {
@@ -3053,16 +2713,19 @@ __device__ __forceinline__ void words_from_planes(bool v3, const uint2 &a, const
                                              (qq & 1) ? 0x07030602u : 0x05010400u);
     // v2: sign bit 7 of b to bit 15, the exponent a to bits 7..14, b's low
     // seven bits stay (both halves at once)
-    out[qq] = v3 ? p : bfi(0x80008000u, p << 8, bfi(0x007F007Fu, p, p >> 1));
+    if constexpr (V3) out[qq] = p;
+    else out[qq] = bitsel(0x80008000u, p << 8, bitsel(0x007F007Fu, p, p >> 1));
   }
 }
 
-// One row's words, CRC column steps and store.
-__device__ __forceinline__ void hw_row_out(bool v3, const uint2 &pa, const uint2 &pb,
-                                           uint32_t w0, uint32_t n, bool full, uint32_t len,
-                                           uint8_t *dst, uint32_t (&cv)[4], const GLane &gl) {
+// One row's words, CRC column steps and store, for rows that may pass the
+// chunk's end.
+template <bool V3>
+__device__ __forceinline__ void hw_row_out(const uint2 &pa, const uint2 &pb, uint32_t w0,
+                                           uint32_t n, bool full, uint32_t len, uint8_t *dst,
+                                           uint32_t (&cv)[4], const GLane &gl) {
   uint32_t out[4];
-  words_from_planes(v3, pa, pb, out);
+  words_from_planes<V3>(pa, pb, out);
   if (!full && w0 + 8u > n) {  // words past the chunk's end are zero
 #pragma unroll
     for (int j = 0; j < 8; ++j)
@@ -3073,6 +2736,7 @@ __device__ __forceinline__ void hw_row_out(bool v3, const uint2 &pa, const uint2
   dec_store(dst, 2u * w0, len, out);
 }
 
+template <bool V3>
 __global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
     const uint8_t *__restrict__ payload, ChunkGeom g, uint8_t *__restrict__ staging,
     uint32_t *__restrict__ rec_status, uint8_t *ws, WsLayout L, uint32_t r0, uint32_t r1) {
@@ -3086,7 +2750,6 @@ __global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
   load_crc_tables(g.crc_kind);
   __syncthreads();  // the only barrier: the tables are in LDS
   const CrcTables &T = g_tables[g.crc_kind];
-  const bool v3 = g.codec == 3;
   const uint32_t wave = uniform(threadIdx.x >> 6), lane = threadIdx.x & 63u;
   const uint32_t tbase = hw_scratch(wave), sbase = tbase + kHwTab;
   uint16_t *tab = reinterpret_cast<uint16_t *>(lds_at(tbase));
@@ -3211,16 +2874,17 @@ __global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
           prev = cnt;
         }
         wave_sync();
-        // table entry p: the code whose first bits (lowest first) are p's;
-        // the entries of length-b codes, in left-aligned order, take the
-        // symbols of that length 2^(11-b) entries each
+        // table entry v (code length | symbol << 8): the code whose bits,
+        // first bit as the most significant of 11, begin v (the left-aligned
+        // order: length-b codes take 2^(11-b) consecutive entries each, so
+        // lanes reading the entries of one short code spread over the LDS
+        // banks)
 #pragma unroll
         for (uint32_t b = 1; b <= kHufMaxLen; ++b) {
           const uint32_t run = uniform(cnb[b] << (kHufMaxLen - b));
           for (uint32_t t = lane; t < run; t += 64u) {
             const uint32_t v = lb[b] + t;
-            tab[__builtin_bitreverse32(v) >> (32u - kHufMaxLen)] =
-                (uint16_t)(sorted[stb[b] + (t >> (kHufMaxLen - b))] | (b << 8));
+            tab[v] = (uint16_t)(b | ((uint32_t)sorted[stb[b] + (t >> (kHufMaxLen - b))] << 8));
           }
         }
         wave_sync();
@@ -3250,7 +2914,7 @@ __global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
         }
 #pragma unroll
         for (int h = 0; h < 8; ++h)
-          hw_row_out(v3, pa[h], pb[h], (8u * q + h) * 512u + 8u * lane, n, full, len, dst, cv, gl);
+          hw_row_out<V3>(pa[h], pb[h], (8u * q + h) * 512u + 8u * lane, n, full, len, dst, cv, gl);
       }
     } else {
       // ---- Huffman streams: group q's bytes [A, A + 4096) staged as 4 KiB
@@ -3266,9 +2930,12 @@ __global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
 #pragma unroll 1
       for (uint32_t q = 0; q < 8u; ++q) {
         const uint32_t soq = so[q], sbl = sbq[q];
-        const bool fits = uniform(__builtin_amdgcn_readlane(soq + sbl, 63)) - A <= kHwStage;
+        // in the stage, with room for the reads of a stream that overruns
+        // its bytes (64 codes of at most 11 bits and a dword ahead)
+        const bool fits =
+            uniform(__builtin_amdgcn_readlane(soq + sbl, 63)) - A <= kHwStage - kHwOverrun;
         const bool more = q < 7u;
-        uint2 pb[8], pa[8];
+        uint2 pb[8];
 #pragma unroll
         for (int h = 0; h < 8; ++h) pb[h] = buf8(rb, (8u * q + h) * 512u + 8u * lane);
         uint4 sq[4];
@@ -3278,35 +2945,63 @@ __global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
 #pragma unroll
           for (int i = 0; i < 4; ++i) sq[i] = buf16(rs, an + 1024u * i + 16u * lane);
         }
-        // the lane's stream: bits in acc (next bit lowest, nb of them),
-        // whole dwords taken while fewer than 32 bits are held, so the bytes
-        // after the stream's end may enter acc but are never decoded from a
-        // well-formed stream: the bits used, 8 (pos - pos0) - nb, must fill
-        // exactly the stream's bytes
+        // the lane's stream: bits in acc (next bit the most significant, nb
+        // of them), whole dwords taken, bit-reversed (a stream's first bit
+        // is bit 0 of its first byte), while fewer than 32 bits are held;
+        // bytes after the stream's end may enter acc but are never decoded
+        // from a well-formed stream: the bits used, 8 (pos - pos0) - nb,
+        // must fill exactly the stream's bytes
         uint64_t acc;
         int32_t nb;
         uint32_t pos = soq - A;
         const uint32_t pos0 = pos;
         if (fits && full) {
-          auto rd = [&](uint32_t p) -> uint32_t { return stg[min(p, kHwStage - 4u) >> 2]; };
-          acc = rd(pos) >> (8u * (pos & 3u));  // up to the first dword boundary
+          // one block without branches per group: each row's symbols, its
+          // words, CRC steps and store, so that the table lookups' latency is
+          // filled with the rows around them.  The stage is read at the LDS
+          // address `ra` of the next whole dword (inside the stage: `fits`).
+          const uint32_t tb = tbase;
+          uint32_t ra = sbase + (pos & ~3u);
+          acc = (uint64_t)__builtin_bitreverse32(lds_u32(ra) >> (8u * (pos & 3u))) << 32;
           nb = (int32_t)(32u - 8u * (pos & 3u));
-          pos = (pos & ~3u) + 4u;
-          uint32_t nxt = rd(pos);
-          // branch-free: some lane of the wave needs bits at nearly every check
+          ra += 4u;
+          uint32_t nxt = lds_u32(ra);
+          // nb is kept in the low byte of nbx, from which whole entries
+          // (length | symbol << 8) are subtracted; the next dword enters below
+          // the nb bits held when fewer than 32 are
+          int32_t nbx = nb;
           auto refill = [&]() {
-            const bool rf = nb < 32;
-            acc |= (uint64_t)(rf ? nxt : 0u) << nb;
-            nb += rf ? 32 : 0;
-            pos += rf ? 4u : 0u;
-            nxt = rd(pos);
+            const int32_t nbv = nbx & 255;
+            nbx = nbv;
+            if (nbv < 32) {
+              const uint32_t x = __builtin_bitreverse32(nxt);
+              acc |= ((uint64_t)(x >> nbv) << 32) | __builtin_amdgcn_alignbit(x, 0u, (uint32_t)nbv);
+              nbx += 32;
+              ra += 4u;
+              nxt = lds_u32(ra);
+            }
           };
+          // one code: its entry, the length in the low bits (a 64-bit shift
+          // takes the low six bits of its count)
           auto symbol = [&]() -> uint32_t {
-            const uint32_t ent = tab[(uint32_t)acc & ((1u << kHufMaxLen) - 1u)];
-            const uint32_t ln = ent >> 8;
-            acc >>= ln;
-            nb -= (int32_t)ln;
-            return ent & 255u;
+            const uint32_t ent = *reinterpret_cast<const uint16_t *>(
+                lds_at(tb + 2u * ((uint32_t)(acc >> 32) >> (32 - kHufMaxLen))));
+            acc <<= (ent & 63u);
+            nbx -= (int32_t)ent;
+            return ent;
+          };
+          // symbols (byte 1 of four entries) into one dword
+          auto pack4 = [](uint32_t e0, uint32_t e1, uint32_t e2, uint32_t e3) -> uint32_t {
+            return __builtin_amdgcn_perm(e1, e0, 0x0C0C0501u) |
+                   (__builtin_amdgcn_perm(e3, e2, 0x0C0C0501u) << 16);
+          };
+          auto row = [&](int h, const uint32_t (&a8)[2]) {
+            uint32_t out[4];
+            words_from_planes<V3>(make_uint2(a8[0], a8[1]), pb[h], out);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) cv[c] = g_step(cv[c], out[c], gl);
+            *reinterpret_cast<uint4 *>(dst + 2u * ((8u * q + h) * 512u + 8u * lane)) =
+                make_uint4(out[0], out[1], out[2], out[3]);
           };
           if (s4) {
 #pragma unroll
@@ -3316,9 +3011,9 @@ __global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
               for (int j = 0; j < 2; ++j) {
                 refill();
                 const uint32_t x0 = symbol(), x1 = symbol(), x2 = symbol(), x3 = symbol();
-                a8[j] = x0 | (x1 << 8) | (x2 << 16) | (x3 << 24);
+                a8[j] = pack4(x0, x1, x2, x3);
               }
-              pa[h] = make_uint2(a8[0], a8[1]);
+              row(h, a8);
             }
           } else {
 #pragma unroll
@@ -3330,18 +3025,20 @@ __global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
                 const uint32_t x0 = symbol(), x1 = symbol();
                 refill();
                 const uint32_t x2 = symbol(), x3 = symbol();
-                a8[j] = x0 | (x1 << 8) | (x2 << 16) | (x3 << 24);
+                a8[j] = pack4(x0, x1, x2, x3);
               }
-              pa[h] = make_uint2(a8[0], a8[1]);
+              row(h, a8);
             }
           }
+          pos = ra - sbase;
+          nb = nbx & 255;
         } else {
           // per symbol: words past the chunk's end have none; bytes from the
           // stage, or from the record where the group overflows it
           auto rd = [&](uint32_t p) -> uint32_t {
             return fits ? stg[min(p, kHwStage - 4u) >> 2] : buf4(rs, A + (p & ~3u));
           };
-          acc = rd(pos) >> (8u * (pos & 3u));
+          acc = (uint64_t)__builtin_bitreverse32(rd(pos) >> (8u * (pos & 3u))) << 32;
           nb = (int32_t)(32u - 8u * (pos & 3u));
           pos = (pos & ~3u) + 4u;
 #pragma unroll
@@ -3352,24 +3049,24 @@ __global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
             for (int j = 0; j < 8; ++j) {
               if (w0 + j < n) {
                 if (nb < 32) {
-                  acc |= (uint64_t)rd(pos) << nb;
+                  acc |= (uint64_t)__builtin_bitreverse32(rd(pos)) << (32 - nb);
                   nb += 32;
                   pos += 4u;
                 }
-                const uint32_t ent = tab[(uint32_t)acc & ((1u << kHufMaxLen) - 1u)];
-                const uint32_t ln = ent >> 8;
-                acc >>= ln;
+                const uint32_t ent = tab[(uint32_t)(acc >> (64 - kHufMaxLen))];
+                const uint32_t ln = ent & 15u;
+                acc <<= ln;
                 nb -= (int32_t)ln;
-                a8[j >> 2] |= (ent & 255u) << (8 * (j & 3));
+                a8[j >> 2] |= (ent >> 8) << (8 * (j & 3));
               }
             }
-            pa[h] = make_uint2(a8[0], a8[1]);
+            hw_row_out<V3>(make_uint2(a8[0], a8[1]), pb[h], w0, n, full, len, dst, cv, gl);
           }
         }
         // exactly the stream's bytes, the last one's unused bits zero
         const uint32_t used = 8u * (pos - pos0) - (uint32_t)nb;
         if ((used + 7u) / 8u != sbl) bad = true;
-        if ((used & 7u) && ((uint32_t)acc & ((1u << (8u - (used & 7u))) - 1u))) bad = true;
+        if ((used & 7u) && (uint32_t)(acc >> (56u + (used & 7u)))) bad = true;
         if (more) {  // the next group enters the stage once this one is read
           wave_sync();
 #pragma unroll
@@ -3378,9 +3075,6 @@ __global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
           wave_sync();
           A = an;
         }
-#pragma unroll
-        for (int h = 0; h < 8; ++h)
-          hw_row_out(v3, pa[h], pb[h], (8u * q + h) * 512u + 8u * lane, n, full, len, dst, cv, gl);
       }
     }
     // ---- zero padding after each section
@@ -3406,9 +3100,9 @@ int set_kernel_attributes() {
                          reinterpret_cast<const void *>(&k_encode<false>),
                          reinterpret_cast<const void *>(&k_encode<true>),
                          reinterpret_cast<const void *>(&k_decode),
-                         reinterpret_cast<const void *>(&k_huf_decode),
-                         reinterpret_cast<const void *>(&k_huf_decode_w)};
-  const uint32_t bytes[6] = {kLdsBase, kLdsEncode, kLdsEncode, kLdsDecode, kLdsHufDecode,
+                         reinterpret_cast<const void *>(&k_huf_decode_w<false>),
+                         reinterpret_cast<const void *>(&k_huf_decode_w<true>)};
+  const uint32_t bytes[6] = {kLdsBase, kLdsEncode, kLdsEncode, kLdsDecode, kLdsHufDecodeW,
                              kLdsHufDecodeW};
   for (int i = 0; i < 6; ++i) {
     hipError_t e = hipFuncSetAttribute(kern[i], hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -3857,9 +3551,16 @@ int launch_decode_records_v2(const void *payload, const ChunkGeom &g, void *stag
   if (r1 <= r0 || !g.n_chunks) return 0;
   const uint32_t recs = min(r1 - r0, g.n_chunks);
   const uint32_t grid = min((uint32_t)n_cu, (recs + kHwWaves - 1u) / kHwWaves);
-  hipLaunchKernelGGL(k_huf_decode_w, dim3(grid), dim3(64 * kHwWaves), kLdsHufDecodeW, S(stream),
-                     static_cast<const uint8_t *>(payload), g, static_cast<uint8_t *>(staging),
-                     rec_status, static_cast<uint8_t *>(ws), L, r0, r1);
+  if (g.codec == 3)
+    hipLaunchKernelGGL(k_huf_decode_w<true>, dim3(grid), dim3(64 * kHwWaves), kLdsHufDecodeW,
+                       S(stream), static_cast<const uint8_t *>(payload), g,
+                       static_cast<uint8_t *>(staging), rec_status, static_cast<uint8_t *>(ws), L, r0,
+                       r1);
+  else
+    hipLaunchKernelGGL(k_huf_decode_w<false>, dim3(grid), dim3(64 * kHwWaves), kLdsHufDecodeW,
+                       S(stream), static_cast<const uint8_t *>(payload), g,
+                       static_cast<uint8_t *>(staging), rec_status, static_cast<uint8_t *>(ws), L, r0,
+                       r1);
   return (int)hipGetLastError();
 }
 
