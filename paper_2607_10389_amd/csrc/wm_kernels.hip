@@ -1093,33 +1093,69 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     bool next_valid = false;  // X_{i+1} exists and its index is valid
 
     // ---- phase 1
-    Window win;
     if (!is_ctl) {
-      uint4 p[kRows];
-      if (HAS_PREV) load_chunk(a.prev + (uint64_t)c * kChunk, len, l, p);
-      {
-        const uint32_t cn = next < n_items ? uniform(item_chunk(a, next, g)) : 0xFFFFFFFFu;
-        next_valid = cn < g.n_chunks;
-        const uint8_t *nbase = a.cur + (uint64_t)(next_valid ? cn : 0u) * kChunk;
-        const uint32_t nlen = next_valid ? chunk_len(g, cn) : 0u;
-        if (!HAS_PREV && need_crc && cur) {  // X_i's lane CRC values while X_{i+1} loads
-          sh.u[l.wave * 64u + l.lane] = lane_value_load(d, gl, nbase, nlen, l, dn);
-        } else {  // (the step variant keeps prev's rows live as well: no room)
-          load_chunk(nbase, nlen, l, dn);
-          if (need_crc && cur) sh.u[l.wave * 64u + l.lane] = lane_value(d, gl);
-        }
-      }
+      const uint32_t cn =
+          !HAS_PREV && next < n_items ? uniform(item_chunk(a, next, g)) : 0xFFFFFFFFu;
+      if (!HAS_PREV) next_valid = cn < g.n_chunks;
+      const uint8_t *nbase = a.cur + (uint64_t)(next_valid ? cn : 0u) * kChunk;
+      const uint32_t nlen = next_valid ? chunk_len(g, cn) : 0u;
       if (HAS_PREV) {
-        uint32_t diff = 0;
+        // prev's rows land four at a time while X_i's lane CRC values are
+        // taken (rows 0..3 under the first half of the column steps, rows
+        // 4..7 under the second), each half compared once the steps are done;
+        // X_{i+1}'s loads wait for phase 2, so no more than a chunk and a half
+        // of rows are ever live
+        const uint8_t *pbase = a.prev + (uint64_t)c * kChunk;
+        const Rsrc rp = rsrc(pbase, len);
+        auto prev_rows = [&](int h0, uint4 (&p)[4]) {
 #pragma unroll
-        for (int h = 0; h < kRows; ++h)
-          diff |= (d[h].x ^ p[h].x) | (d[h].y ^ p[h].y) | (d[h].z ^ p[h].z) | (d[h].w ^ p[h].w);
+          for (int i = 0; i < 4; ++i) p[i] = buf16<kNt>(rp, l.off0 + (h0 + i) * kRow);
+          if (len & 15u) {  // a tail chunk's straddling piece, as in load_chunk
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const uint32_t off = l.off0 + (h0 + i) * kRow;
+              if (off < len && off + 16u > len) p[i] = load16_partial(pbase + off, len - off);
+            }
+          }
+        };
+        auto diff_rows = [&](int h0, const uint4 (&p)[4]) {
+          uint32_t df = 0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            df |= (d[h0 + i].x ^ p[i].x) | (d[h0 + i].y ^ p[i].y) | (d[h0 + i].z ^ p[i].z) |
+                  (d[h0 + i].w ^ p[i].w);
+          return df;
+        };
+        const bool crc_now = need_crc && cur;
+        uint32_t v0 = d[0].x, v1 = d[0].y, v2 = d[0].z, v3 = d[0].w;
+        auto steps = [&](int h0, int h1) {
+#pragma unroll
+          for (int h = h0; h < h1; ++h) {
+            v0 = g_step(v0, d[h].x, gl);
+            v1 = g_step(v1, d[h].y, gl);
+            v2 = g_step(v2, d[h].z, gl);
+            v3 = g_step(v3, d[h].w, gl);
+          }
+        };
+        uint4 p[4];
+        prev_rows(0, p);
+        if (crc_now) steps(1, 4);
+        uint32_t diff = diff_rows(0, p);
+        prev_rows(4, p);
+        if (crc_now) {
+          steps(4, kRows);
+          sh.u[l.wave * 64u + l.lane] = lane_merge(v0, v1, v2, v3);
+        }
+        diff |= diff_rows(4, p);
         const unsigned long long any = __ballot(diff != 0);
         if (l.lane == 0) sh.dirty_w[l.wave] = any ? 1u : 0u;
+      } else if (need_crc && cur) {  // X_i's lane CRC values while X_{i+1} loads
+        sh.u[l.wave * 64u + l.lane] = lane_value_load(d, gl, nbase, nlen, l, dn);
+      } else {
+        load_chunk(nbase, nlen, l, dn);
       }
     } else {
       if (cur && l.lane == 0) ticket = atomicAdd(&ctl->ticket, 1u);
-      if (HAS_PREV && pend) win = lookback_issue(status, (int64_t)pr.item - 1, my_last, my_last_incl);
     }
     bool dirty = cur && !bad_index;
     if (HAS_PREV) {
@@ -1129,7 +1165,8 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       for (int w = 0; w < kWaves; ++w) dw |= sh.dirty_w[w];
       dirty = dirty && uniform(dw) != 0;
       if (is_ctl && pend)  // ---- control: X_{i-1}'s offset, header and table entry
-        ctl_emit(a, pr, win, n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
+        ctl_emit(a, pr, lookback_issue(status, (int64_t)pr.item - 1, my_last, my_last_incl),
+                 n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
     }
     // No barrier here: the histogram reduced below was completed before the
     // last B4, the lane values and X_{i-1}'s offset (step: emitted after B0,
@@ -1137,6 +1174,12 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     // alternates so the control cannot overwrite one still unread.
 
     // ---- phase 2
+    if (HAS_PREV && !is_ctl) {  // X_{i+1}'s loads (its histogram is taken in phase 4)
+      const uint32_t cn = next < n_items ? uniform(item_chunk(a, next, g)) : 0xFFFFFFFFu;
+      next_valid = cn < g.n_chunks;
+      load_chunk(a.cur + (uint64_t)(next_valid ? cn : 0u) * kChunk, next_valid ? chunk_len(g, cn) : 0u,
+                 l, dn);
+    }
     uint32_t crc = 0;
     if (is_ctl) {
       if (cur) {
