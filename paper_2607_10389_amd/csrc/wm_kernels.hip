@@ -682,6 +682,8 @@ struct EncShared {
   uint32_t off_lo, off_hi;   // record offset
   alignas(16) uint4 cand[9];    // plan candidates: size, base | k << 8 | mode << 16, n_esc
   alignas(16) uint32_t H[256];  // histogram
+  int64_t my_last;              // control: this workgroup's last finished item
+  uint64_t my_last_incl;        //          and its inclusive prefix
 };
 static_assert(sizeof(EncShared) <= kLdsMiscBytes, "encoder scratch fits");
 constexpr uint32_t kLdsHistE = kLdsLow;   // 256 bins x 32 copies of 2 x u16 (32 KiB)
@@ -1051,6 +1053,8 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   if (threadIdx.x == (uint32_t)kThreads) {
     sh.first = atomicAdd(&ctl->ticket, 1u);
     sh.next = atomicAdd(&ctl->ticket, 1u);
+    sh.my_last = -1;
+    sh.my_last_incl = 0;
   }
   __syncthreads();
   uint32_t item = uniform(sh.first);
@@ -1072,8 +1076,13 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   bool pend = false, p_dirty = false;
   uint32_t p_nw = 0, p_send = 0;
   RecFields pr = {};  // control, step variant: X_{i-1}'s record fields
-  int64_t my_last = -1;      // control: this workgroup's last finished item
-  uint64_t my_last_incl = 0; //          and its inclusive prefix
+  // (the step variant keeps them in LDS: only the control wave uses them,
+  // and as registers they would stay allocated through the data waves'
+  // phases, where that variant has none to spare)
+  int64_t my_last_r = -1;
+  uint64_t my_last_incl_r = 0;
+  int64_t &my_last = HAS_PREV ? sh.my_last : my_last_r;
+  uint64_t &my_last_incl = HAS_PREV ? sh.my_last_incl : my_last_incl_r;
   uint2 smp[kRows];
 #pragma unroll
   for (int h = 0; h < kRows; ++h) smp[h] = make_uint2(0, 0);
@@ -1218,9 +1227,13 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         const uint64_t rec_off = (uint64_t)uniform(sh.off_lo) | ((uint64_t)uniform(sh.off_hi) << 32);
         uint8_t *rec = a.payload + rec_off;
         // two staged pieces per thread and step, both read before either is
-        // stored (one LDS round trip per pair)
+        // stored (one LDS round trip per pair); in the step variant the
+        // thread's first address is formed here each time rather than held
+        // across the loop
         const uint32_t n16 = p_send / 16u;
-        for (uint32_t i = threadIdx.x; i < n16; i += 2u * kThreads) {
+        uint32_t tid = threadIdx.x;
+        if (HAS_PREV) asm volatile("" : "+v"(tid));
+        for (uint32_t i = tid; i < n16; i += 2u * kThreads) {
           const uint32_t i2 = i + kThreads;
           const uint4 q0 = *reinterpret_cast<const uint4 *>(stage + 16 * i);
           const uint4 q1 = *reinterpret_cast<const uint4 *>(stage + 16 * min(i2, n16 - 1u));
