@@ -141,10 +141,9 @@ int stream_cus(void *stream, int n_cu) {
   return c > 0 && c < n_cu ? c : n_cu;
 }
 
-// Workspace: the WsLayout part, then (format v2) one plan per chunk.
-uint64_t plans_offset(const WsLayout &L) { return (L.total + 255u) & ~255ull; }
-// Format v2 also keeps, after the plans, a dirty list and its length for
-// a fused step whose caller passes no dirty_idx.
+// Workspace: the WsLayout part, then (format v2) one plan per item and a
+// dirty list with its length for a fused step whose caller passes no
+// dirty_idx.
 uint64_t list_offset(const WsLayout &L, uint32_t n_chunks) {
   return (plans_offset(L) + (uint64_t)kHufPlanBytes * n_chunks + 255u) & ~255ull;
 }
@@ -194,8 +193,7 @@ wm_status encode_tiles(const void *state, const ChunkGeom &g, const uint32_t *id
   const uint32_t *ul = idx ? t.tiles : nullptr, *un = idx ? t.n_tiles : nullptr;
   if (g.codec != WM_CODEC_EXPFOR)
     return hip_status(launch_encode_v2(state, g, ul, un, nullptr, unit_crc, nullptr, payload,
-                                       payload_bytes, ws, L, wsb + plans_offset(L), n_cu,
-                                       stream));
+                                       payload_bytes, ws, L, n_cu, stream));
   if (!idx)
     return hip_status(launch_encode(1, state, nullptr, g, nullptr, nullptr, nullptr, unit_crc,
                                     nullptr, nullptr, nullptr, payload, payload_bytes, ws, L,
@@ -226,8 +224,7 @@ wm_status encode_step_tiles(const void *cur, const void *prev, const ChunkGeom &
   if (!prev) {
     int rc = g.codec != WM_CODEC_EXPFOR
                  ? launch_encode_v2(cur, g, nullptr, nullptr, nullptr, unit_crc, global_crc,
-                                    payload, payload_bytes, ws, L, wsb + plans_offset(L), n_cu,
-                                    stream)
+                                    payload, payload_bytes, ws, L, n_cu, stream)
                  : launch_encode(1, cur, nullptr, g, nullptr, nullptr, nullptr, unit_crc,
                                  global_crc, nullptr, nullptr, payload, payload_bytes, ws, L,
                                  n_cu, stream);
@@ -244,8 +241,7 @@ wm_status encode_step_tiles(const void *cur, const void *prev, const ChunkGeom &
     return WM_ERR_HIP;
   if (g.codec != WM_CODEC_EXPFOR)
     return hip_status(launch_encode_v2(cur, g, t.tiles, t.n_tiles, unit_crc, nullptr, global_crc,
-                                       payload, payload_bytes, ws, L, wsb + plans_offset(L), n_cu,
-                                       stream));
+                                       payload, payload_bytes, ws, L, n_cu, stream));
   return hip_status(launch_encode(0, cur, nullptr, g, t.tiles, t.n_tiles, unit_crc, nullptr,
                                   global_crc, nullptr, nullptr, payload, payload_bytes, ws, L,
                                   n_cu, stream));
@@ -342,9 +338,7 @@ wm_status wm_encode(const void *state, uint64_t nbytes, const wm_params *p, cons
       crc ? nullptr : reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + L.flags);
   if (g.codec != WM_CODEC_EXPFOR)
     return hip_status(launch_encode_v2(state, g, idx, n_idx, crc, crc_scratch, nullptr, payload,
-                                       payload_bytes, ws, L,
-                                       static_cast<uint8_t *>(ws) + plans_offset(L), n_cu,
-                                       stream));
+                                       payload_bytes, ws, L, n_cu, stream));
   if (idx && !crc) {
     // the header's global CRC covers every chunk, listed or not: checksum
     // the whole state first, then encode the list with those receipts
@@ -408,7 +402,7 @@ wm_status encode_step_call(const void *cur, const void *prev, uint64_t nbytes,
     if (launch_checksum(cur, g, crcs, nullptr, n_cu, stream) != 0) return WM_ERR_HIP;
     return hip_status(launch_encode_v2(cur, g, prev ? list : nullptr, prev ? n_list : nullptr,
                                        crcs, nullptr, global_crc, payload, payload_bytes, ws, L,
-                                       wsb + plans_offset(L), n_cu, stream));
+                                       n_cu, stream));
   }
   return hip_status(launch_encode(2, cur, prev, g, nullptr, nullptr, nullptr, crcs, global_crc,
                                   dirty_idx, n_dirty, payload, payload_bytes, ws, L, n_cu,
@@ -657,8 +651,7 @@ wm_status wm_precopy_round(const void *cur, void *shipped, void *dest, uint64_t 
       // format v2 takes its receipts from a checksum of every chunk
       if (launch_checksum(cur, g, b->crc, nullptr, n_cu0, stream) != 0 ||
           launch_encode_v2(cur, g, b->dirty_idx, b->n_dirty, b->crc, nullptr, b->global_crc,
-                           b->payload, b->payload_bytes, b->ws_src, L,
-                           static_cast<uint8_t *>(b->ws_src) + plans_offset(L), n_cu0,
+                           b->payload, b->payload_bytes, b->ws_src, L, n_cu0,
                            stream) != 0)
         return WM_ERR_HIP;
     } else if (launch_encode(0, cur, nullptr, g, b->dirty_idx, b->n_dirty, nullptr, b->crc,

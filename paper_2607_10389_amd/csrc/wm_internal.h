@@ -158,13 +158,16 @@ struct ManifestLeaf {
 // gather: leaves -> flat (flatten); else flat -> leaves (rehydrate)
 int launch_manifest(bool gather, void *flat, uint64_t flat_bytes, const ManifestLeaf *leaves,
                     uint32_t n_leaves, int n_cu, void *stream);
-// Format v2: per-record plans in the workspace after the WsLayout part
-// (kHufPlanBytes each: header, code-length nibbles, stream byte counts).
-constexpr uint32_t kHufPlanBytes = 688;
+// Format v2/v3: per-item plans (code lengths) in the workspace after the
+// WsLayout part, kHufPlanBytes each.
+constexpr uint32_t kHufPlanBytes = 256;
+inline uint64_t plans_offset(const WsLayout &L) { return (L.total + 255u) & ~255ull; }
+// Format v2/v3 encode (full ship or index list): the code lengths, then one
+// pass per chunk.
 int launch_encode_v2(const void *state, const ChunkGeom &g, const uint32_t *idx,
                      const uint32_t *n_idx, const uint32_t *crc_in, uint32_t *crc_scratch,
                      uint32_t *global_crc, void *payload, uint64_t *payload_bytes, void *ws,
-                     const WsLayout &L, uint8_t *plans, int n_cu, void *stream);
+                     const WsLayout &L, int n_cu, void *stream);
 // Format v2 records [r0, r1) (as launch_decode_records).
 int launch_decode_records_v2(const void *payload, const ChunkGeom &g, void *staging,
                              uint32_t *rec_status, void *ws, const WsLayout &L, int n_cu,

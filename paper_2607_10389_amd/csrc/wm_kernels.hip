@@ -670,6 +670,7 @@ struct EncArgs {
   uint8_t *ws;
   WsLayout L;
   int mode;
+  const uint8_t *plans;  // format v2/v3: the items' code lengths (k_huf_lengths)
 };
 
 struct EncShared {
@@ -2247,21 +2248,14 @@ int upload_tables(int device, const CrcTables tabs[2]) {
 // body with k >= 1: code-length nibbles (128 B) | stream byte counts (512 B)
 // | streams, padded to 16 | sign/mantissa plane, padded to 16.  With k = 0
 // (a single exponent, `base`): the sign/mantissa plane only.  A HUF record
-// must be shorter than the RAW one.  The encoder plans every record (the
-// code and its exact size), scans the sizes into offsets and then writes;
-// the decoder stages a record's streams in LDS and decodes each stream
-// through a table of the code's first kHufMaxLen bits.
+// must be shorter than the RAW one.  The encoder codes each chunk in one
+// pass, in the v1 encoder's pipeline (k_huf_encode); the decoder takes a
+// record per wave and decodes each stream through a table of the code's
+// first kHufMaxLen bits (k_huf_decode_w).
 
 constexpr uint32_t kHufMaxLen = 11;
 constexpr uint32_t kHufStreams = 512;
 constexpr uint32_t kHufHead = 16 + 128 + kHufStreams;  // record header and the two tables
-
-struct HufPlan {  // first 48 bytes of a plan; code-length nibbles at +48, stream bytes at +176
-  uint32_t mode, k, base, sb;
-  uint32_t size_lo, size_hi, off_lo, off_hi;
-  uint32_t c, bad, pad_[2];
-};
-static_assert(sizeof(HufPlan) == 48 && 48 + 128 + kHufStreams <= kHufPlanBytes, "plan layout");
 
 __device__ __forceinline__ uint64_t huf_rec_size(uint32_t n, uint32_t k, uint32_t sb) {
   return k == 0 ? 16u + pad16(n) : kHufHead + pad16(sb) + pad16(n);
@@ -2318,28 +2312,6 @@ struct HufWave {
   uint8_t lens[256];
 };
 static_assert(sizeof(HufWave) * kHufWaves <= 65536, "v2 encoder scratch");
-
-// Piece p (0..4095) of a chunk of len bytes: its 16 bytes, zero past len.
-__device__ __forceinline__ uint4 huf_piece(const uint8_t *base, Rsrc r, uint32_t len, uint32_t p) {
-  const uint32_t o = 16u * p;
-  if (o + 16u <= len) return buf16<kNt>(r, o);
-  return o < len ? load16_partial(base + o, len - o) : make_uint4(0, 0, 0, 0);
-}
-
-// Pieces p0 + 64 h (h = 0..7) of a chunk of len bytes, all loads in flight
-// together; zero past len.
-__device__ __forceinline__ void huf_pieces8(const uint8_t *base, Rsrc r, uint32_t len, uint32_t p0,
-                                            uint4 (&x)[8]) {
-#pragma unroll
-  for (int h = 0; h < 8; ++h) x[h] = buf16<kNt>(r, 16u * (p0 + 64u * h));
-  if (len & 15u) {
-#pragma unroll
-    for (int h = 0; h < 8; ++h) {
-      const uint32_t o = 16u * (p0 + 64u * h);
-      if (o < len && o + 16u > len) x[h] = load16_partial(base + o, len - o);
-    }
-  }
-}
 
 // Code lengths of the counts in W.hist (the oracle's construction: leaves
 // sorted by (count, symbol), the two lightest nodes merged with a leaf taken
@@ -2435,29 +2407,50 @@ __device__ uint32_t huf_lengths_wave(HufWave &W, uint32_t lane) {
   }
 }
 
-// One plan per item (one wave per chunk): exponent histogram, code lengths,
-// stream byte counts and the mode.  Stream s = q * 64 + lane covers rows
-// 8q..8q+7, words 8 lane..8 lane+7 of each.
-__global__ __launch_bounds__(64 * kHufWaves) void k_huf_plan(
+// ------------------------------------------------ format v2/v3, fused encoder --
+// The records, from one read of each chunk once k_huf_lengths (below) has
+// found its code lengths, in the v1 encoder's pipeline (one workgroup per
+// CU, 8 data waves holding a chunk in registers, a control wave, tickets and
+// the decoupled look-back; iteration i computes X_i and writes X_{i-1}):
+//   phase 1: data: X_i's lane CRC values while X_{i+1} loads
+//   phase 2: control: X_i's plan (code lengths) loads
+//   phase 3: data: write X_{i-1} (staged section, then plane B from
+//            registers); control: first CRC step, X_i's canonical codes into
+//            LDS from the code lengths k_huf_lengths found (the construction's
+//            serial merges run there, a chunk per wave, so that they overlap)
+//   phase 4: data: X_i's plane-B bytes, each lane's stream byte count;
+//            control: X_i's CRC
+//   phase 5: all: the record's mode and size from the stream totals;
+//            control: publish, look-back, header and table entry; data: the
+//            code-length nibbles, stream byte counts and streams (HUF) or
+//            plane A (RAW) into staging
+// Stream s = wave * 64 + lane holds the lane's 8 words of each of its wave's
+// 8 rows, which are in its registers.
+constexpr uint32_t kLdsHufCode = kLdsStage + kLdsStageBytes;  // 256 x u32: reversed code | len << 24
+constexpr uint32_t kLdsHufEncode = kLdsHufCode + 1024;
+static_assert(kLdsHufEncode <= 163840, "fused format v2 encoder LDS fits one CU");
+
+// Code lengths of format v2/v3, one chunk per wave (kHufWaves per
+// workgroup): the plane-A histogram (four interleaved copies, bin b of copy
+// c at 4b + c, copy = lane mod 4, so equal symbols of neighbouring lanes hit
+// different banks), then the format's construction.  Plan of item i at
+// plans + kHufPlanBytes i: the longest length k, the single symbol (k = 0),
+// and from byte 16 the record's 128 code-length nibble bytes.
+template <bool V3>
+__global__ __launch_bounds__(64 * kHufWaves) void k_huf_lengths(
     const uint8_t *__restrict__ state, ChunkGeom g, const uint32_t *__restrict__ idx,
-    const uint32_t *__restrict__ n_idx, uint8_t *__restrict__ plans, WsCtl *ctl) {
+    const uint32_t *__restrict__ n_idx, uint8_t *__restrict__ plans) {
   __shared__ HufWave sw[kHufWaves];
   const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
   HufWave &W = sw[wave];
-  const bool v3 = g.codec == 3;
   const uint32_t n_items = idx ? (*n_idx > g.n_chunks ? 0u : *n_idx) : g.n_chunks;
   for (uint32_t item = blockIdx.x * kHufWaves + wave; item < n_items;
        item += gridDim.x * kHufWaves) {
-    uint32_t c = idx ? idx[item] : item;
-    const bool bad = c >= g.n_chunks || (idx && item > 0 && idx[item - 1] >= c);
-    if (bad) c = 0;
+    const uint32_t c = idx ? idx[item] : item;
+    if (c >= g.n_chunks) continue;  // (the encoder rejects the list)
     const uint32_t len = chunk_len(g, c), n = len / 2;
     const uint8_t *base = state + (uint64_t)c * kChunk;
     const Rsrc rs = rsrc(base, len);
-    // four interleaved copies of the histogram (bin b of copy c at 4b + c,
-    // copy = lane mod 4) in hist, wt and nw, which the length construction
-    // only uses afterwards: equal exponents of lanes in different copies hit
-    // different banks
     uint32_t *H4 = W.hist;
     static_assert(offsetof(HufWave, wt) == 1024 && offsetof(HufWave, nw) == 2048 &&
                   sizeof(HufWave::nw) == 2048, "hist, wt, nw: 1024 contiguous words");
@@ -2466,13 +2459,21 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_plan(
     const uint32_t cp = lane & 3u;
     for (uint32_t q = 0; q < 8u; ++q) {
       uint4 x[8];
-      huf_pieces8(base, rs, len, 512u * q + lane, x);
+#pragma unroll
+      for (int h = 0; h < 8; ++h) x[h] = buf16<kNt>(rs, 16u * (512u * q + lane + 64u * h));
+      if (len & 15u) {
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+          const uint32_t o = 16u * (512u * q + lane + 64u * h);
+          if (o < len && o + 16u > len) x[h] = load16_partial(base + o, len - o);
+        }
+      }
 #pragma unroll
       for (int h = 0; h < 8; ++h) {
         const uint32_t i0 = 8u * (512u * q + lane + 64u * h);
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-          if (i0 + j < n) atomicAdd(&H4[4u * pa_of(v3, word_of(x[h], j)) + cp], 1u);
+          if (i0 + j < n) atomicAdd(&H4[4u * pa_of(V3, word_of(x[h], j)) + cp], 1u);
       }
     }
     wave_sync();
@@ -2486,229 +2487,313 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_plan(
     wave_sync();
     const uint32_t k = huf_lengths_wave(W, lane);
     uint8_t *P = plans + (uint64_t)item * kHufPlanBytes;
-    uint32_t tot = 0;
-    for (uint32_t q = 0; q < 8u; ++q) {  // stream q * 64 + lane
-      uint32_t bits = 0;
-      if (k) {
-        uint4 x[8];
-        huf_pieces8(base, rs, len, 512u * q + lane, x);
-#pragma unroll
-        for (int h = 0; h < 8; ++h) {
-          const uint32_t i0 = 8u * (512u * q + lane + 64u * h);
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            if (i0 + j < n) bits += W.lens[pa_of(v3, word_of(x[h], j))];
-        }
-      }
-      const uint32_t sb = (bits + 7u) >> 3;
-      P[176 + q * 64 + lane] = (uint8_t)sb;
-      tot += sb;
-    }
-    for (int o = 32; o > 0; o >>= 1) tot += (uint32_t)__shfl_xor((int)tot, o, 64);
-    P[48 + 2 * lane] = (uint8_t)(W.lens[4 * lane] | (W.lens[4 * lane + 1] << 4));
-    P[48 + 2 * lane + 1] = (uint8_t)(W.lens[4 * lane + 2] | (W.lens[4 * lane + 3] << 4));
-    if (lane == 0) {
-      const uint64_t raw = raw_rec_size(n), hs = huf_rec_size(n, k, tot);
-      const bool huf = hs < raw;
-      const uint64_t size = huf ? hs : raw;
-      HufPlan hp;
-      hp.mode = huf ? 2u : 0u;
-      hp.k = huf ? k : 0u;
-      hp.base = huf && k == 0 ? (uint32_t)W.order[0] : 0u;
-      hp.sb = huf ? tot : 0u;
-      hp.size_lo = (uint32_t)size;
-      hp.size_hi = (uint32_t)(size >> 32);
-      hp.off_lo = hp.off_hi = 0;
-      hp.c = c;
-      hp.bad = bad ? 1u : 0u;
-      hp.pad_[0] = hp.pad_[1] = 0;
-      *reinterpret_cast<HufPlan *>(P) = hp;
-      if (bad) atomicOr(&ctl->error, 2u);
-    }
+    const uint32_t s0 = 4u * lane;
+    *reinterpret_cast<uint16_t *>(P + 16 + 2 * lane) =
+        (uint16_t)(W.lens[s0] | (W.lens[s0 + 1] << 4) | (W.lens[s0 + 2] << 8) | (W.lens[s0 + 3] << 12));
+    if (lane == 0)
+      *reinterpret_cast<uint4 *>(P) = make_uint4(k, k == 0 ? (uint32_t)W.order[0] : 0u, 0u, 0u);
     wave_sync();
   }
 }
 
-// Record offsets: 64 + the exclusive prefix of the record sizes (in 16-byte
-// units per tile of 1024 items, the running total in 64 bits).
-__global__ __launch_bounds__(1024) void k_huf_scan(const uint32_t *__restrict__ n_idx,
-                                                   ChunkGeom g, uint8_t *__restrict__ plans,
-                                                   WsCtl *ctl) {
-  __shared__ uint32_t wsum[16];
-  const uint32_t n_items = n_idx ? (*n_idx > g.n_chunks ? 0u : *n_idx) : g.n_chunks;
-  uint64_t carry = 64;
-  for (uint32_t base = 0; base < n_items; base += 1024u) {
-    const uint32_t i = base + threadIdx.x;
-    HufPlan *hp = i < n_items ? reinterpret_cast<HufPlan *>(plans + (uint64_t)i * kHufPlanBytes)
-                              : nullptr;
-    const uint32_t units = hp ? hp->size_lo >> 4 : 0u;
-    const uint32_t incl = wave_incl_scan(units);
-    if ((threadIdx.x & 63u) == 63u) wsum[threadIdx.x >> 6] = incl;
-    __syncthreads();
-    uint32_t before = 0, tile = 0;
-    for (uint32_t w = 0; w < 16u; ++w) {
-      const uint32_t v = wsum[w];
-      if (w < (threadIdx.x >> 6)) before += v;
-      tile += v;
-    }
-    if (hp) {
-      const uint64_t off = carry + 16ull * (before + incl - units);
-      hp->off_lo = (uint32_t)off;
-      hp->off_hi = (uint32_t)(off >> 32);
-    }
-    carry += 16ull * tile;
-    __syncthreads();
+// Plane A (bytes 0..3: words 0..3 of x) and plane B of a 16-byte row piece.
+template <bool V3>
+__device__ __forceinline__ uint2 plane_a8(const uint4 &x) {
+  if constexpr (V3) {
+    return make_uint2(__builtin_amdgcn_perm(x.y, x.x, 0x07050301u),
+                      __builtin_amdgcn_perm(x.w, x.z, 0x07050301u));
+  } else {  // a dword rotated left by one bit: the exponents in bytes 1 and 3
+    const uint32_t r0 = __builtin_amdgcn_alignbit(x.x, x.x, 31), r1 = __builtin_amdgcn_alignbit(x.y, x.y, 31);
+    const uint32_t r2 = __builtin_amdgcn_alignbit(x.z, x.z, 31), r3 = __builtin_amdgcn_alignbit(x.w, x.w, 31);
+    return make_uint2(__builtin_amdgcn_perm(r1, r0, 0x07050301u),
+                      __builtin_amdgcn_perm(r3, r2, 0x07050301u));
   }
-  if (threadIdx.x == 0) {
-    ctl->n_rec = n_items;
-    ctl->payload_bytes = carry - 64u;
+}
+template <bool V3>
+__device__ __forceinline__ uint2 plane_b8(const uint4 &x) {
+  if constexpr (V3) {
+    return make_uint2(__builtin_amdgcn_perm(x.y, x.x, 0x06040200u),
+                      __builtin_amdgcn_perm(x.w, x.z, 0x06040200u));
+  } else {
+    return sm_bytes(x);
   }
 }
 
-// Write every planned record (one wave per chunk), its table entry (staged
-// in the workspace) and the entry's CRC.
-__global__ __launch_bounds__(64 * kHufWaves) void k_huf_write(
-    const uint8_t *__restrict__ state, ChunkGeom g, const uint32_t *__restrict__ n_idx,
-    const uint32_t *__restrict__ crcs, const uint8_t *__restrict__ plans,
-    uint8_t *__restrict__ payload, uint8_t *ws, WsLayout L) {
-  __shared__ HufWave sw[kHufWaves];
-  const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63u;
-  HufWave &W = sw[wave];
-  const bool v3 = g.codec == 3;
-  uint4 *tab_ws = reinterpret_cast<uint4 *>(ws + L.table);
-  uint32_t *ecrc = reinterpret_cast<uint32_t *>(ws + L.entry_crc);
-  const uint32_t n_items = n_idx ? (*n_idx > g.n_chunks ? 0u : *n_idx) : g.n_chunks;
-  for (uint32_t item = blockIdx.x * kHufWaves + wave; item < n_items;
-       item += gridDim.x * kHufWaves) {
-    const uint8_t *P = plans + (uint64_t)item * kHufPlanBytes;
-    const HufPlan hp = *reinterpret_cast<const HufPlan *>(P);
-    if (hp.bad) continue;  // the payload is discarded (ctl->error)
-    const uint32_t c = hp.c, len = chunk_len(g, c), n = len / 2;
-    const uint8_t *base = state + (uint64_t)c * kChunk;
-    const Rsrc rs = rsrc(base, len);
-    const uint64_t off = ((uint64_t)hp.off_hi << 32) | hp.off_lo;
-    uint8_t *rec = payload + off;
-    if (lane == 0) {
-      uint32_t hw[4] = {hp.mode | (hp.k << 8) | (hp.base << 16), n, hp.sb, 0u};
-      hw[3] = crc_words_g(g.crc_kind, hw, 3);
-      *reinterpret_cast<uint4 *>(rec) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-      const uint32_t ew[4] = {c, crcs[c], (uint32_t)off, (uint32_t)(off >> 32)};
-      tab_ws[item] = make_uint4(ew[0], ew[1], ew[2], ew[3]);
-      ecrc[item] = crc_words_g(g.crc_kind, ew, 4);
-    }
-    const bool hufk = hp.mode == 2 && hp.k > 0;
-    const uint64_t smo = hp.mode == 0 ? 16u + pad16(n) : (hufk ? kHufHead + pad16(hp.sb) : 16u);
-    if (hufk) {
-      // tables, and the canonical codes: per length, consecutive values in
-      // symbol order, the first one ((previous first + previous count) << 1)
-      rec[16 + 2 * lane] = P[48 + 2 * lane];
-      rec[16 + 2 * lane + 1] = P[48 + 2 * lane + 1];
-      for (int q = 0; q < 8; ++q) rec[16 + 128 + q * 64 + lane] = P[176 + q * 64 + lane];
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t s = q * 64 + lane;
-        W.lens[s] = (uint8_t)((P[48 + (s >> 1)] >> (4 * (s & 1))) & 15u);
-      }
-      wave_sync();
-      uint32_t first = 0, prev_cnt = 0;
-      for (uint32_t b = 1; b <= hp.k; ++b) {
-        first = (first + prev_cnt) << 1;
-        uint32_t run = 0;
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t s = q * 64 + lane;
-          const bool is = W.lens[s] == b;
-          const unsigned long long msk = __ballot(is);
-          if (is) W.nw[s] = first + run + lanes_below(msk);
-          run += (uint32_t)__popcll(msk);
-        }
-        prev_cnt = run;
-      }
-      wave_sync();
-    }
-    if (hp.mode == 0) {  // exponent plane, sign/mantissa plane
-      for (uint32_t it = 0; it < kChunk / 1024u; ++it) {
-        const uint32_t p = it * 64u + lane, i0 = 8u * p;
-        if (i0 >= n) break;
-        const uint4 x = huf_piece(base, rs, len, p);  // (RAW records are rare)
-        uint32_t e[2] = {0, 0}, sm[2] = {0, 0};
+template <bool V3>
+__global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom g) {
+  WsCtl *ctl = reinterpret_cast<WsCtl *>(a.ws + a.L.ctl);
+  uint64_t *status = reinterpret_cast<uint64_t *>(a.ws + a.L.status);
+  uint4 *tab_ws = reinterpret_cast<uint4 *>(a.ws + a.L.table);
+  uint32_t *ecrc = reinterpret_cast<uint32_t *>(a.ws + a.L.entry_crc);
+  const uint32_t n_list = a.mode == kModeList ? ld_const(a.n_idx) : 0u;
+  const uint32_t n_items =
+      uniform(a.mode == kModeList ? (n_list > g.n_chunks ? 0u : n_list) : g.n_chunks);
+  const bool need_crc = a.crc_in == nullptr;
+  const bool is_ctl = threadIdx.x >= (uint32_t)kThreads;
+
+  load_crc_tables(g.crc_kind);
+  const CrcTables &T = g_tables[g.crc_kind];
+  EncShared &sh = enc_shared();
+  uint8_t *stage = lds_at(kLdsStage);
+  const uint32_t *code = reinterpret_cast<const uint32_t *>(lds_at(kLdsHufCode));
+  if (threadIdx.x == (uint32_t)kThreads) {
+    sh.first = atomicAdd(&ctl->ticket, 1u);
+    sh.next = atomicAdd(&ctl->ticket, 1u);
+  }
+  __syncthreads();
+  uint32_t item = uniform(sh.first);
+  uint32_t next = uniform(sh.next);
+
+  const GLane gl = glane_make();
+  const Lane l0 = lane_info();
+  uint4 d[kRows];
+  if (!is_ctl) {
+    const uint32_t c = item < n_items ? uniform(item_chunk(a, item, g)) : 0xFFFFFFFFu;
+    load_chunk(a.cur + (uint64_t)(c < g.n_chunks ? c : 0u) * kChunk,
+               c < g.n_chunks ? chunk_len(g, c) : 0u, l0, d);
+  }
+
+  bool pend = false, p_dirty = false;
+  uint32_t p_nw = 0, p_send = 0;
+  int64_t my_last = -1;
+  uint64_t my_last_incl = 0;
+  uint2 smp[kRows];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const uint32_t w = word_of(x, j);
-          e[j >> 2] |= pa_of(v3, w) << (8 * (j & 3));
-          sm[j >> 2] |= pb_of(v3, w) << (8 * (j & 3));
-        }
-        if (i0 + 8u <= n) {
-          *reinterpret_cast<uint2 *>(rec + 16 + i0) = make_uint2(e[0], e[1]);
-          *reinterpret_cast<uint2 *>(rec + smo + i0) = make_uint2(sm[0], sm[1]);
-        } else {
-          for (uint32_t b = 0; i0 + b < n; ++b) {
-            rec[16 + i0 + b] = (uint8_t)(e[b >> 2] >> (8 * (b & 3)));
-            rec[smo + i0 + b] = (uint8_t)(sm[b >> 2] >> (8 * (b & 3)));
+  for (int h = 0; h < kRows; ++h) smp[h] = make_uint2(0, 0);
+
+  for (uint32_t it = 0; item < n_items || pend; ++it) {
+    const bool cur = item < n_items;
+    const Lane l = lane_fresh(l0);
+    uint32_t c = cur ? uniform(item_chunk(a, item, g)) : 0u;
+    const bool bad_index = cur && c >= g.n_chunks;
+    if (!cur || bad_index) c = 0;
+    const uint32_t len = (cur && !bad_index) ? chunk_len(g, c) : 0u;
+    const uint32_t n_words = len / 2;
+    const bool dirty = cur && !bad_index;
+    uint4 dn[kRows];
+    uint32_t ticket = 0;
+
+    // ---- phase 1
+    if (!is_ctl) {
+      const uint32_t cn = next < n_items ? uniform(item_chunk(a, next, g)) : 0xFFFFFFFFu;
+      const bool next_valid = cn < g.n_chunks;
+      const uint8_t *nbase = a.cur + (uint64_t)(next_valid ? cn : 0u) * kChunk;
+      const uint32_t nlen = next_valid ? chunk_len(g, cn) : 0u;
+      if (need_crc && cur) sh.u[l.wave * 64u + l.lane] = lane_value_load(d, gl, nbase, nlen, l, dn);
+      else load_chunk(nbase, nlen, l, dn);
+    } else if (cur && l.lane == 0) {
+      ticket = atomicAdd(&ctl->ticket, 1u);
+    }
+
+    // ---- phase 2
+    uint32_t crc = 0;
+    uint32_t pk = 0, pbase = 0, nib = 0;  // control: X_i's plan (k_huf_lengths)
+    if (is_ctl) {
+      if (cur) {
+        if (!need_crc) crc = bad_index ? 0u : ld_const(a.crc_in + c);
+        if (l.lane == 0) sh.ticket[it & 1] = ticket;
+      }
+      if (dirty) {
+        const uint8_t *P = a.plans + (uint64_t)item * kHufPlanBytes;
+        pk = uniform(ld_u32(P));
+        pbase = uniform(ld_u32(P + 4));
+        nib = *reinterpret_cast<const uint16_t *>(P + 16 + 2 * l.lane);
+      }
+    }
+    __syncthreads();  // B2: lane values and X_{i-1}'s offset
+
+    // ---- phase 3
+    uint32_t crc_acc = 0;
+    if (is_ctl) {
+      if (cur && need_crc) {
+        crc_acc = sh.u[l.lane];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) crc_acc = tab4x(kLdsWaveStep, crc_acc, sh.u[w * 64 + l.lane]);
+        crc_acc = lane_shift(crc_acc);
+      }
+      if (dirty) {
+        // canonical codes from the lengths: per length, consecutive values
+        // in symbol order (lane l holds symbols 4l..4l+3)
+        const uint32_t ln[4] = {nib & 15u, (nib >> 4) & 15u, (nib >> 8) & 15u, nib >> 12};
+        const unsigned long long below = (1ull << l.lane) - 1ull;
+        uint32_t ent[4] = {0, 0, 0, 0};
+        uint32_t first = 0, prev_cnt = 0;
+        for (uint32_t b = 1; b <= pk; ++b) {
+          first = (first + prev_cnt) << 1;
+          uint32_t before = 0, cnt = 0;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const unsigned long long m = __ballot(ln[j] == b);
+            before += (uint32_t)__popcll(m & below);
+            cnt += (uint32_t)__popcll(m);
           }
-        }
-      }
-      if (lane < 16u && n + lane < pad16(n)) rec[16 + n + lane] = 0;
-    } else {
-      // streams (HUF k >= 1) and the sign/mantissa plane, rows 8q..8q+7 at a
-      // time; stream q * 64 + lane starts after the earlier streams
-      uint32_t sbase = 0;
-      for (uint32_t q = 0; q < 8u; ++q) {
-        const uint32_t sb = hufk ? P[176 + q * 64 + lane] : 0u;
-        const uint32_t incl = wave_incl_scan(sb);
-        uint8_t *st = rec + kHufHead + sbase + (incl - sb);
-        sbase += uniform(__builtin_amdgcn_readlane(incl, 63));
-        // the stream's bytes go out as whole dwords where the payload
-        // address is 4-aligned, bytewise at its two ends (a neighbouring
-        // stream writes the other bytes of a shared dword)
-        const uint32_t lead = (4u - ((uint32_t)(uintptr_t)st & 3u)) & 3u;
-        uint64_t acc = 0;
-        uint32_t nb = 0, ob = 0;
-        uint4 xs[8];
-        huf_pieces8(base, rs, len, 512u * q + lane, xs);
+          uint32_t r = first + before;
 #pragma unroll
-        for (int h = 0; h < 8; ++h) {
-          const uint32_t p = (8u * q + h) * 64u + lane, i0 = 8u * p;
-          const uint4 x = xs[h];
-          uint32_t sm[2] = {0, 0};
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const uint32_t w = word_of(x, j);
-            sm[j >> 2] |= pb_of(v3, w) << (8 * (j & 3));
-            if (hufk && i0 + j < n) {
-              const uint32_t e = pa_of(v3, w), ln = W.lens[e];
-              acc |= (uint64_t)(__builtin_bitreverse32(W.nw[e]) >> (32u - ln)) << nb;
-              nb += ln;
-              // (the plan counted these bytes: ob stays below sb)
-              while (ob < lead && nb >= 8u) {
-                if (ob < sb) st[ob] = (uint8_t)acc;
-                ++ob;
-                acc >>= 8;
-                nb -= 8u;
-              }
-              if (ob >= lead && nb >= 32u) {
-                if (ob + 4u <= sb) *reinterpret_cast<uint32_t *>(st + ob) = (uint32_t)acc;
-                ob += 4u;
-                acc >>= 32;
-                nb -= 32u;
-              }
+          for (int j = 0; j < 4; ++j) {
+            if (ln[j] == b) {
+              ent[j] = (__builtin_bitreverse32(r) >> (32u - b)) | (b << 24);
+              ++r;
             }
           }
-          if (i0 + 8u <= n) {
-            *reinterpret_cast<uint2 *>(rec + smo + i0) = make_uint2(sm[0], sm[1]);
-          } else {
-            for (uint32_t b = 0; i0 + b < n; ++b) rec[smo + i0 + b] = (uint8_t)(sm[b >> 2] >> (8 * (b & 3)));
+          prev_cnt = cnt;
+        }
+        *reinterpret_cast<uint4 *>(lds_at(kLdsHufCode + 16u * l.lane)) =
+            make_uint4(ent[0], ent[1], ent[2], ent[3]);
+        if (l.lane == 0) sh.cand[0] = make_uint4(pk, pbase, 0u, 0u);
+        sh.u[l.lane] = nib;  // the record's nibbles, for wave 0 in phase 5
+      }
+    } else {
+      if (pend && p_dirty) {
+        // write X_{i-1}: staged section, then its plane B
+        const uint64_t rec_off = (uint64_t)uniform(sh.off_lo) | ((uint64_t)uniform(sh.off_hi) << 32);
+        uint8_t *rec = a.payload + rec_off;
+        const uint32_t n16 = p_send / 16u;
+        for (uint32_t i = threadIdx.x; i < n16; i += 2u * kThreads) {
+          const uint32_t i2 = i + kThreads;
+          const uint4 q0 = *reinterpret_cast<const uint4 *>(stage + 16 * i);
+          const uint4 q1 = *reinterpret_cast<const uint4 *>(stage + 16 * min(i2, n16 - 1u));
+          *reinterpret_cast<uint4 *>(rec + 16 + 16 * i) = q0;
+          if (i2 < n16) *reinterpret_cast<uint4 *>(rec + 16 + 16 * i2) = q1;
+        }
+        uint8_t *pb_at = rec + 16 + p_send;
+#pragma unroll
+        for (int h = 0; h < kRows; ++h) {
+          const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+          if (w0 < p_nw) *reinterpret_cast<uint2 *>(pb_at + w0) = smp[h];
+        }
+        if (threadIdx.x < 16u && p_nw + threadIdx.x < pad16(p_nw)) pb_at[p_nw + threadIdx.x] = 0;
+      }
+    }
+    __syncthreads();  // B3: the code is in LDS, X_{i-1}'s staging read
+
+    // ---- phase 4
+    const uint32_t k = dirty ? uniform(sh.cand[0].x) : 0u;
+    uint32_t sb_lane = 0, lane_excl = 0;
+    if (is_ctl) {
+      if (cur && need_crc) crc = bad_index ? 0u : finish_crc(wave_xor(crc_acc), len, g, T);
+    } else {
+      if (dirty) {
+        // the streams' section of the staging starts as zeros (phase 5 ORs
+        // the streams in; X_{i-1}'s staging was read before B3)
+        for (uint32_t i = (kHufHead - 16u) / 16u + threadIdx.x; i < kLdsStageBytes / 16u; i += kThreads)
+          reinterpret_cast<uint4 *>(stage)[i] = make_uint4(0, 0, 0, 0);
+        if (k) {  // the lane's stream: its words' code lengths
+          uint32_t bits = 0;
+#pragma unroll
+          for (int h = 0; h < kRows; ++h) {
+            const uint2 pa = plane_a8<V3>(d[h]);
+            const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              const uint32_t e = ((j < 4 ? pa.x : pa.y) >> (8 * (j & 3))) & 255u;
+              if (w0 + j < n_words) bits += code[e] >> 24;
+            }
+          }
+          sb_lane = (bits + 7u) >> 3;
+          const uint32_t incl = wave_incl_scan(sb_lane);
+          lane_excl = incl - sb_lane;
+          if (l.lane == 63u) sh.esc_w[l.wave] = incl;
+        }
+#pragma unroll
+        for (int h = 0; h < kRows; ++h) smp[h] = plane_b8<V3>(d[h]);
+      }
+    }
+    __syncthreads();  // B4: stream totals known
+
+    // ---- phase 5: the plan (every wave computes it), then the record
+    uint32_t mode = 0, base = 0, sb = 0, size = 0, s_send = 0;
+    uint32_t wave_base = 0;
+    if (dirty) {
+      const uint4 ea = *reinterpret_cast<const uint4 *>(&sh.esc_w[0]);
+      const uint4 eb = *reinterpret_cast<const uint4 *>(&sh.esc_w[4]);
+      const uint32_t ew[kWaves] = {ea.x, ea.y, ea.z, ea.w, eb.x, eb.y, eb.z, eb.w};
+      if (k) {
+#pragma unroll
+        for (uint32_t w = 0; w < (uint32_t)kWaves; ++w) {
+          if (w < l.wave) wave_base += ew[w];
+          sb += ew[w];
+        }
+        sb = uniform(sb);
+        wave_base = uniform(wave_base);
+      }
+      const uint64_t raw = raw_rec_size(n_words), hs = huf_rec_size(n_words, k, sb);
+      const bool huf = hs < raw;
+      mode = huf ? 2u : 0u;
+      base = huf && k == 0 ? uniform(sh.cand[0].y) : 0u;
+      if (!huf) sb = 0;
+      size = (uint32_t)(huf ? hs : raw);
+      s_send = huf ? (k ? kHufHead - 16u + (uint32_t)pad16(sb) : 0u) : (uint32_t)pad16(n_words);
+    }
+    const uint32_t kr = mode == 2u ? k : 0u;
+    if (is_ctl && cur) {
+      if (item != 0 && l.lane == 0) {
+        const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(size >> 4) << 26);
+        status_store(&status[item], agg | kFlagAgg);
+      }
+      const Window win = lookback_issue(status, (int64_t)item - 1, my_last, my_last_incl);
+      const uint32_t hw[3] = {mode | (kr << 8) | (base << 16), n_words, sb};
+      const uint32_t hcrc = crc_words(hw, 3);
+      const uint32_t ew2[2] = {c, crc};
+      const uint32_t epart = crc_feed(0xFFFFFFFFu, ew2, 2);
+      const RecFields r = {item, c, n_words, mode, kr, base, sb, size, crc, dirty, bad_index,
+                           hcrc, epart};
+      ctl_emit(a, r, win, n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
+    }
+    if (!is_ctl && dirty) {
+      if (mode == 2u && k) {
+        // code-length nibbles (wave 0) and stream byte counts, then the
+        // lane's stream, ORed into the zeroed section 32 bits at a time at
+        // any bit offset (the streams are packed end to end)
+        if (l.wave == 0) *reinterpret_cast<uint16_t *>(stage + 2u * l.lane) = (uint16_t)sh.u[l.lane];
+        stage[128u + l.wave * 64u + l.lane] = (uint8_t)sb_lane;
+        uint32_t *sw = reinterpret_cast<uint32_t *>(stage);
+        uint32_t P = 8u * (kHufHead - 16u + wave_base + lane_excl);  // next bit to place
+        uint64_t acc = 0;
+        uint32_t nb = 0;
+        auto emit = [&](bool whole) {  // the low 32 bits if held (all at the end)
+          const bool e32 = whole || nb >= 32u;
+          const uint64_t v = (uint64_t)(e32 ? (uint32_t)acc : 0u) << (P & 31u);
+          atomicOr(&sw[P >> 5], (uint32_t)v);
+          atomicOr(&sw[(P >> 5) + 1u], (uint32_t)(v >> 32));
+          P += e32 ? 32u : 0u;
+          acc = e32 ? acc >> 32 : acc;
+          nb -= e32 && !whole ? 32u : 0u;
+        };
+#pragma unroll
+        for (int h = 0; h < kRows; ++h) {
+          const uint2 pa = plane_a8<V3>(d[h]);
+          const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const uint32_t e = ((j < 4 ? pa.x : pa.y) >> (8 * (j & 3))) & 255u;
+            const uint32_t cw = w0 + j < n_words ? code[e] : 0u;
+            acc |= (uint64_t)(cw & 0xFFFFFFu) << nb;
+            nb += cw >> 24;
+            if (j & 1) emit(false);  // at most 22 bits since the last emission
           }
         }
-        while (nb) {  // the last bytes, the final one's unused bits zero
-          if (ob < sb) st[ob] = (uint8_t)acc;
-          ++ob;
-          acc >>= 8;
-          nb = nb > 8u ? nb - 8u : 0u;
+        emit(true);  // fewer than 32 bits are left
+      } else if (mode == 0u) {  // RAW: plane A, one byte per word
+#pragma unroll
+        for (int h = 0; h < kRows; ++h) {
+          const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+          if (w0 < n_words) *reinterpret_cast<uint2 *>(stage + w0) = plane_a8<V3>(d[h]);
         }
+        if (threadIdx.x < 16u && n_words + threadIdx.x < pad16(n_words)) stage[n_words + threadIdx.x] = 0;
       }
-      if (hufk && lane < 16u && hp.sb + lane < pad16(hp.sb)) rec[kHufHead + hp.sb + lane] = 0;
     }
-    if (lane < 16u && n + lane < pad16(n)) rec[smo + n + lane] = 0;
-    wave_sync();
+
+    // ---- X_i becomes the pending record
+    pend = cur;
+    p_nw = n_words;
+    p_dirty = dirty;
+    p_send = s_send;
+    if (!is_ctl) {
+#pragma unroll
+      for (int h = 0; h < kRows; ++h) d[h] = dn[h];
+    }
+    item = next;
+    if (cur) next = uniform(sh.ticket[it & 1]);
   }
 }
 
@@ -3152,15 +3237,17 @@ __global__ __launch_bounds__(64 * kHwWaves) void k_huf_decode_w(
 }
 
 int set_kernel_attributes() {
-  const void *kern[6] = {reinterpret_cast<const void *>(&k_checksum),
+  const void *kern[8] = {reinterpret_cast<const void *>(&k_checksum),
                          reinterpret_cast<const void *>(&k_encode<false>),
                          reinterpret_cast<const void *>(&k_encode<true>),
                          reinterpret_cast<const void *>(&k_decode),
+                         reinterpret_cast<const void *>(&k_huf_encode<false>),
+                         reinterpret_cast<const void *>(&k_huf_encode<true>),
                          reinterpret_cast<const void *>(&k_huf_decode_w<false>),
                          reinterpret_cast<const void *>(&k_huf_decode_w<true>)};
-  const uint32_t bytes[6] = {kLdsBase, kLdsEncode, kLdsEncode, kLdsDecode, kLdsHufDecodeW,
-                             kLdsHufDecodeW};
-  for (int i = 0; i < 6; ++i) {
+  const uint32_t bytes[8] = {kLdsBase,      kLdsEncode,     kLdsEncode,     kLdsDecode,
+                             kLdsHufEncode, kLdsHufEncode, kLdsHufDecodeW, kLdsHufDecodeW};
+  for (int i = 0; i < 8; ++i) {
     hipError_t e = hipFuncSetAttribute(kern[i], hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)bytes[i]);
     if (e != hipSuccess) return (int)e;
@@ -3325,6 +3412,7 @@ int launch_encode(int mode, const void *cur, const void *prev, const ChunkGeom &
   a.ws = wsb;
   a.L = L;
   a.mode = mode;
+  a.plans = nullptr;
   if (g.n_chunks) {
     uint32_t grid = min((uint32_t)n_cu, g.n_chunks);
     if (mode == kModeStep && prev != nullptr)
@@ -3563,34 +3651,60 @@ int launch_reverify(const void *live, const ChunkGeom &g, const void *staging,
 int launch_encode_v2(const void *state, const ChunkGeom &g, const uint32_t *idx,
                      const uint32_t *n_idx, const uint32_t *crc_in, uint32_t *crc_scratch,
                      uint32_t *global_crc, void *payload, uint64_t *payload_bytes, void *ws,
-                     const WsLayout &L, uint8_t *plans, int n_cu, void *stream) {
+                     const WsLayout &L, int n_cu, void *stream) {
   uint8_t *wsb = static_cast<uint8_t *>(ws);
   WsCtl *ctl = reinterpret_cast<WsCtl *>(wsb + L.ctl);
-  const uint8_t *st = static_cast<const uint8_t *>(state);
   hipLaunchKernelGGL(k_encode_prepare, dim3(64), dim3(256), 0, S(stream), wsb, L, g.n_chunks,
                      idx ? n_idx : nullptr);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
+  // receipts: given, computed in the pass (every chunk is encoded), or for a
+  // list checksummed first (the global CRC covers every chunk)
   const uint32_t *crcs = crc_in;
-  if (!crcs) {
+  uint32_t *crc_out = nullptr;
+  if (!crcs && idx) {
     const int rc = launch_checksum(state, g, crc_scratch, nullptr, n_cu, stream, true);
     if (rc) return rc;
     crcs = crc_scratch;
+  } else if (!crcs) {
+    crc_out = crc_scratch;
   }
+  EncArgs a;
+  a.cur = static_cast<const uint8_t *>(state);
+  a.prev = nullptr;
+  a.idx = idx;
+  a.n_idx = n_idx;
+  a.crc_in = crcs;
+  a.crc_out = crc_out;
+  a.dirty_idx = nullptr;
+  a.payload = static_cast<uint8_t *>(payload);
+  a.ws = wsb;
+  a.L = L;
+  a.mode = idx ? kModeList : kModeAll;
+  uint8_t *plans = wsb + plans_offset(L);
+  a.plans = plans;
   if (g.n_chunks) {
-    const uint32_t grid = min((uint32_t)n_cu * 2u, (g.n_chunks + kHufWaves - 1) / kHufWaves);
-    hipLaunchKernelGGL(k_huf_plan, dim3(grid), dim3(64 * kHufWaves), 0, S(stream), st, g, idx,
-                       n_idx, plans, ctl);
-    hipLaunchKernelGGL(k_huf_scan, dim3(1), dim3(1024), 0, S(stream), n_idx, g, plans, ctl);
-    hipLaunchKernelGGL(k_huf_write, dim3(grid), dim3(64 * kHufWaves), 0, S(stream), st, g, n_idx, crcs,
-                       static_cast<const uint8_t *>(plans), static_cast<uint8_t *>(payload), wsb,
-                       L);
+    const uint32_t lgrid = min((uint32_t)n_cu * 2u, (g.n_chunks + kHufWaves - 1) / kHufWaves);
+    if (g.codec == 3)
+      hipLaunchKernelGGL(k_huf_lengths<true>, dim3(lgrid), dim3(64 * kHufWaves), 0, S(stream),
+                         static_cast<const uint8_t *>(state), g, idx, n_idx, plans);
+    else
+      hipLaunchKernelGGL(k_huf_lengths<false>, dim3(lgrid), dim3(64 * kHufWaves), 0, S(stream),
+                         static_cast<const uint8_t *>(state), g, idx, n_idx, plans);
+    const uint32_t grid = min((uint32_t)n_cu, g.n_chunks);
+    if (g.codec == 3)
+      hipLaunchKernelGGL(k_huf_encode<true>, dim3(grid), dim3(kEncThreads), kLdsHufEncode,
+                         S(stream), a, g);
+    else
+      hipLaunchKernelGGL(k_huf_encode<false>, dim3(grid), dim3(kEncThreads), kLdsHufEncode,
+                         S(stream), a, g);
     e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
   }
   uint32_t *sums = reinterpret_cast<uint32_t *>(wsb + L.ctl) + 60;  // global and table CRC
   CombineJobs jobs = {};
-  jobs.job[0] = CombineJob{crcs, nullptr, g.n_chunks, 16u, g.tail_len, g.crc_kind, sums};
+  jobs.job[0] = CombineJob{crcs ? crcs : crc_out, nullptr, g.n_chunks, 16u, g.tail_len,
+                           g.crc_kind, sums};
   jobs.job[1] = CombineJob{reinterpret_cast<const uint32_t *>(wsb + L.entry_crc), &ctl->n_rec,
                            0u, 4u, 16u, g.crc_kind, sums + 1};
   const int rc = launch_combine(jobs, 2, stream);
