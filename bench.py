@@ -45,7 +45,7 @@ def parse():
     ap.add_argument("--no-fanin", action="store_true",
                     help="skip the eight-session fan-in measurement")
     ap.add_argument("--no-v2", action="store_true",
-                    help="skip the format v2 (Huffman exponent codec) measurement")
+                    help="skip the format v2 and v3 (Huffman-coded plane) measurements")
     ap.add_argument("--no-receive", action="store_true",
                     help="skip the pipelined receive measurement")
     ap.add_argument("--no-precopy", action="store_true",
@@ -433,24 +433,26 @@ def long_context_run(torch, wm_inputs, crc, dev, one):
     }, host_sample
 
 
-def codec_v2_run(torch, state, nbytes, crc, dev, one):
-    """Format v2 (per-chunk Huffman codes of the exponents) on the production
-    cache: full-ship encode with the CRCs computed in the call (checksum,
-    plan, offset scan, write), decode with verification, and the payload
-    ratio next to format v1's."""
+def codec_v2_run(torch, state, nbytes, crc, dev, one, codec=None):
+    """Format v2 (per-chunk Huffman codes of the exponents) or v3 (of the
+    bf16 high-byte plane) on the production cache: full-ship encode with the
+    CRCs computed in the call, decode with verification, and the payload
+    ratio (next to format v1's in the same line)."""
     from paper_2607_10389_amd import Mover, WM_CODEC_EXPHUF, WM_OK
 
-    m = Mover(nbytes, crc, dev, codec=WM_CODEC_EXPHUF)
+    codec = WM_CODEC_EXPHUF if codec is None else codec
+    name = "v2" if codec == WM_CODEC_EXPHUF else "v3"
+    m = Mover(nbytes, crc, dev, codec=codec)
     m.encode(state, with_crc=False)
     m.decode()
     if m.commit(None, scatter=False) != WM_OK:
-        raise RuntimeError("format v2 payload did not verify")
+        raise RuntimeError(f"format {name} payload did not verify")
     torch.cuda.synchronize()
     if not torch.equal(m.staging[:nbytes], state.view(-1).view(torch.uint8)):
-        raise RuntimeError("format v2 decode differs from the source")
+        raise RuntimeError(f"format {name} decode differs from the source")
     pb = int(m.payload_bytes.item())
     return {
-        "workload": "production-size cache, full ship, format v2",
+        "workload": f"production-size cache, full ship, format {name}",
         "payload_bytes": pb,
         "compression_ratio": round(pb / nbytes, 5),
         "wm_encode": one("enc", lambda: m.encode(state, with_crc=False), nbytes + pb),
@@ -796,6 +798,9 @@ def main():
 
     if not args.no_v2:
         out["codec_v2"] = codec_v2_run(torch, state, nbytes, args.crc, dev, one)
+        from paper_2607_10389_amd import WM_CODEC_BYTEPLANE
+        out["codec_v3"] = codec_v2_run(torch, state, nbytes, args.crc, dev, one,
+                                       codec=WM_CODEC_BYTEPLANE)
 
     host_long = None
     if not args.no_long:
