@@ -1054,6 +1054,9 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
   if (threadIdx.x == (uint32_t)kThreads) {
     sh.first = atomicAdd(&ctl->ticket, 1u);
     sh.next = atomicAdd(&ctl->ticket, 1u);
+    // full ship: the control wave takes each further ticket after B4, an
+    // iteration before it is read; the first one is taken here
+    if (!HAS_PREV) sh.ticket[0] = atomicAdd(&ctl->ticket, 1u);
     sh.my_last = -1;
     sh.my_last_incl = 0;
   }
@@ -1165,7 +1168,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         load_chunk(nbase, nlen, l, dn);
       }
     } else {
-      if (cur && l.lane == 0) ticket = atomicAdd(&ctl->ticket, 1u);
+      if (HAS_PREV && cur && l.lane == 0) ticket = atomicAdd(&ctl->ticket, 1u);
     }
     bool dirty = cur && !bad_index;
     if (HAS_PREV) {
@@ -1194,7 +1197,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
     if (is_ctl) {
       if (cur) {
         if (!need_crc) crc = bad_index ? 0u : ld_const(a.crc_in + c);
-        if (l.lane == 0) sh.ticket[it & 1] = ticket;
+        if (HAS_PREV && l.lane == 0) sh.ticket[it & 1] = ticket;
       }
     } else if (dirty) {
       // reduce the copies: wave w sums bins 32w..32w+31 (its own 4 KiB of
@@ -1228,12 +1231,13 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         const uint64_t rec_off = (uint64_t)uniform(sh.off_lo) | ((uint64_t)uniform(sh.off_hi) << 32);
         uint8_t *rec = a.payload + rec_off;
         // two staged pieces per thread and step, both read before either is
-        // stored (one LDS round trip per pair); in the step variant the
-        // thread's first address is formed here each time rather than held
-        // across the loop
+        // stored (one LDS round trip per pair); the thread's first address
+        // is formed here each time rather than held across the loop (a held
+        // one is spilled, and its reload would wait for the next chunk's
+        // loads)
         const uint32_t n16 = p_send / 16u;
         uint32_t tid = threadIdx.x;
-        if (HAS_PREV) asm volatile("" : "+v"(tid));
+        asm volatile("" : "+v"(tid));
         for (uint32_t i = tid; i < n16; i += 2u * kThreads) {
           const uint32_t i2 = i + kThreads;
           const uint4 q0 = *reinterpret_cast<const uint4 *>(stage + 16 * i);
@@ -1341,6 +1345,14 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         // second step: the XOR of the shifted lane values (F^4 included)
         crc = bad_index ? 0u : finish_crc(wave_xor(crc_acc), len, g, T);
       }
+      if (!HAS_PREV && cur) {
+        // full ship: the record header's CRC and the table entry's CRC
+        // prefix, here where the control wave is idle rather than after B4
+        const uint32_t hw[3] = {mode | (k << 8) | (base << 16), n_words, n_esc};
+        hcrc = crc_words(hw, 3);
+        const uint32_t ew[2] = {c, crc};
+        epart = crc_feed(0xFFFFFFFFu, ew, 2);
+      }
     } else {
       // ---- data: X_{i+1}'s histogram (its loads were issued an iteration
       // ago); the atomics drain while the codes below keep the VALUs busy
@@ -1384,16 +1396,26 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       // was published before B4, and the vector-memory pipe is idle here (the
       // data waves' next loads come after the loop top).  The header CRC and
       // the entry's CRC prefix are computed while the look-back loads fly.
-      Window win;
-      if (!HAS_PREV) win = lookback_issue(status, (int64_t)item - 1, my_last, my_last_incl);
-      const uint32_t hw[3] = {mode | (k << 8) | (base << 16), n_words, n_esc};
-      hcrc = crc_words(hw, 3);
-      const uint32_t ew[2] = {c, crc};
-      epart = crc_feed(0xFFFFFFFFu, ew, 2);
       if (!HAS_PREV) {
+        // full ship: the ticket for the end of the next iteration (its slot
+        // was last read at the end of the previous one), issued with the
+        // look-back window so that their latencies overlap; the address
+        // goes through a register the compiler cannot see into, so the
+        // uniform-address atomic combining (which reads the result back at
+        // once, waiting for it) is not applied
+        uint32_t zero = 0;
+        asm volatile("" : "+v"(zero));
+        if (l.lane == 0) ticket = atomicAdd(&ctl->ticket + zero, 1u);
+        const Window win = lookback_issue(status, (int64_t)item - 1, my_last, my_last_incl);
         const RecFields r = {item, c, n_words, mode, k, base, n_esc, size, crc, dirty, bad_index,
                              hcrc, epart};
         ctl_emit(a, r, win, n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
+        if (l.lane == 0) sh.ticket[(it + 1) & 1] = ticket;
+      } else {
+        const uint32_t hw[3] = {mode | (k << 8) | (base << 16), n_words, n_esc};
+        hcrc = crc_words(hw, 3);
+        const uint32_t ew[2] = {c, crc};
+        epart = crc_feed(0xFFFFFFFFu, ew, 2);
       }
     }
 
