@@ -2000,6 +2000,7 @@ __device__ __forceinline__ bool dec_packed(const DecBuf &B, const DecView &v, co
   if (kEsc) *reinterpret_cast<uint4 *>(stage + 16u * l.lane) = B.e;
 #pragma unroll
   for (int h = 0; h < kRows; ++h) {
+    if (h == kRows / 2) __builtin_amdgcn_s_setprio(0);  // (see k_decode)
     dec_load_row(N, vn, l, rn, h);
     const uint32_t row = l.wave * kRows + h;
     const uint32_t w0 = (l.off0 + h * kRow) >> 1;
@@ -2144,6 +2145,11 @@ __global__ __launch_bounds__(kDecThreads) void k_decode(
       if (i >= my_n || uniform(M.st) != 0) {
         dec_load(nxt, vn, l);  // nothing to decode in this step
       } else {
+        // Each SIMD holds two data waves, and the older one wins issue
+        // slots; left alone the younger one finishes its record last and
+        // runs its tail by itself.  The younger one takes priority for the
+        // first half of its rows, so that the two finish together.
+        if (l.wave >= kWaves / 2) __builtin_amdgcn_s_setprio(1);
         {
           const DecView v = dec_view(payload, M, l, g);
           uint8_t *dst = staging + (uint64_t)v.r * kChunk;
