@@ -353,6 +353,7 @@ __device__ __forceinline__ uint32_t lane_value_load(const uint4 (&d)[kRows], con
   uint32_t v0 = d[0].x, v1 = d[0].y, v2 = d[0].z, v3 = d[0].w;
 #pragma unroll
   for (int h = 1; h < kRows; ++h) {
+    if (h == kRows / 2) __builtin_amdgcn_s_setprio(0);  // (see k_encode)
     dn[h] = buf16<kNt>(r, l.off0 + h * kRow);
     v0 = g_step(v0, d[h].x, gl);
     v1 = g_step(v1, d[h].y, gl);
@@ -838,6 +839,7 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
   if constexpr (K == 8) {  // RAW: the exponent plane, one byte per word
 #pragma unroll
     for (int h = 0; h < kRows; ++h) {
+      if (h == kRows / 2) __builtin_amdgcn_s_setprio(0);  // (see k_encode)
       const uint32_t w0 = (l.off0 + h * kRow) >> 1;
       const uint4 x = d[h];
       // a dword rotated left by one bit holds its low word's exponent in
@@ -857,6 +859,7 @@ __device__ __forceinline__ void pack_codes(const uint4 (&d)[kRows], const Lane &
   uint32_t cnt3[(kRows + 2) / 3] = {};  // the lane's escapes per row, three rows a word
 #pragma unroll
   for (int h = 0; h < kRows; ++h) {
+    if (h == kRows / 2) __builtin_amdgcn_s_setprio(0);  // (see k_encode)
     const uint32_t w0 = (l.off0 + h * kRow) >> 1;
     const uint32_t x[4] = {d[h].x, d[h].y, d[h].z, d[h].w};
     uint32_t pair[4], m = 0;
@@ -1022,6 +1025,11 @@ __device__ __forceinline__ void ctl_emit(const EncArgs &a, const RecFields &r, c
 //   phase 5:        control (full ship): look-back of X_i, its prefix,
 //                   header and table entry; data: escape index and escapes
 //                   into staging
+// Each SIMD holds two data waves, and the older one wins issue slots: left
+// alone, the younger one finishes each phase last and runs its tail by
+// itself.  In the row loops of phases 1 (full ship), 4 and 5 the younger
+// one (waves 4..7) takes priority for the first half of its rows, so that
+// the two finish together.
 template <bool HAS_PREV>
 __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(a.ws + a.L.ctl);
@@ -1163,6 +1171,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
         const unsigned long long any = __ballot(diff != 0);
         if (l.lane == 0) sh.dirty_w[l.wave] = any ? 1u : 0u;
       } else if (need_crc && cur) {  // X_i's lane CRC values while X_{i+1} loads
+        if (l.wave >= kWaves / 2) __builtin_amdgcn_s_setprio(1);  // (see above)
         sh.u[l.wave * 64u + l.lane] = lane_value_load(d, gl, nbase, nlen, l, dn);
       } else {
         load_chunk(nbase, nlen, l, dn);
@@ -1366,6 +1375,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
           for (uint32_t i = l.lane; i < 32u * kbits; i += 64u) s4[i] = make_uint4(0, 0, 0, 0);
         }
         uint32_t wave_esc = 0;
+        if (l.wave >= kWaves / 2) __builtin_amdgcn_s_setprio(1);  // (see above)
 #define WM_PACK(K)                                                                        \
   (full ? pack_codes<K, true>(d, l, n_words, base, stage, escm, lane_r, wave_esc, row_base) \
         : pack_codes<K, false>(d, l, n_words, base, stage, escm, lane_r, wave_esc, row_base))
@@ -1439,8 +1449,10 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
       // `at` of the zeroed escape section: gathered by one table lookup and
       // two byte permutes, shifted to at's byte within its dword and ORed in
       // by the lanes that have any
+      if (l.wave >= kWaves / 2) __builtin_amdgcn_s_setprio(1);  // (see above)
 #pragma unroll
       for (int h = 0; h < kRows; ++h) {
+        if (h == kRows / 2) __builtin_amdgcn_s_setprio(0);
         const uint32_t flags = (escm[h >> 2] >> (8 * (h & 3))) & 255u;
         const uint2 sel = *reinterpret_cast<const uint2 *>(lds_at(kLdsEscLut + 8u * flags));
         // each dword rotated left by one bit puts the low word's exponent in
