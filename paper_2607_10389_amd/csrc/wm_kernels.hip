@@ -1081,6 +1081,12 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs a, ChunkGeom g) 
                c < g.n_chunks ? chunk_len(g, c) : 0u, l0, d);
     if (c < g.n_chunks) hist_add(d, (l0.lane & 31u) * 4u);  // copies zeroed before the barrier
   }
+  // Every path has its first rows in registers before the loop.  Otherwise
+  // the compiler, which merges this entry with the loop's back edge, keeps
+  // them pending and inserts counter waits before each read of d inside the
+  // loop, and those waits also drain the record stores issued after them.
+#pragma unroll
+  for (int h = 0; h < kRows; ++h) asm volatile("" ::"v"(d[h].x), "v"(d[h].y), "v"(d[h].z), "v"(d[h].w));
   __syncthreads();  // the first chunk's histogram is complete (the loop has no B1)
 
   // the chunk whose record is still to be written (uniform), and its
