@@ -122,15 +122,31 @@ def counter_pass(args):
                       "state_bytes": state.numel() * 2}), flush=True)
 
 
-def timed_events(torch, fn, n, warmup=3):
+# GPU clock cycles of the spin that each timed run waits behind (about 0.15
+# ms at the shader clock): long enough for the host to enqueue a whole call
+# before the GPU reaches it.
+PREROLL_CYCLES = 300_000
+
+
+def timed_events(torch, fn, n, warmup=3, preroll=True):
     """Median duration (ms) of fn() over n runs, each bracketed by its own
-    pair of HIP events on the current stream, after `warmup` untimed runs."""
+    pair of HIP events on the current stream, after `warmup` untimed runs.
+
+    With `preroll`, each run is queued behind a short spin kernel, so that
+    the host has enqueued the start event, every launch of the call and the
+    end event before the GPU reaches them: the bracket then holds the call's
+    device time (all of its launches and the device's gaps between them)
+    and not the host's launch latency, which a caller that keeps the GPU
+    busy never sees.  Without it the GPU starts each run idle and waits for
+    the host between launches."""
     for _ in range(warmup):
         fn()
     s = torch.cuda.Event(enable_timing=True)
     e = torch.cuda.Event(enable_timing=True)
     times = []
     for _ in range(n):
+        if preroll:
+            torch.cuda._sleep(PREROLL_CYCLES)
         s.record()
         fn()
         e.record()
@@ -630,12 +646,16 @@ def main():
 
     src_ms = timed_events(torch, source, 10)
     dst_ms = timed_events(torch, destination, 10)
+    # the same calls started on an idle GPU (host launch latency included)
+    src_idle_ms = timed_events(torch, source, 10, preroll=False)
+    dst_idle_ms = timed_events(torch, destination, 10, preroll=False)
     src_bytes = nbytes + payload_bytes
     dst_bytes = payload_bytes + nbytes
     src_gbs = src_bytes / (src_ms * 1e-3) / 1e9
     dst_gbs = dst_bytes / (dst_ms * 1e-3) / 1e9
-    # HIP events bracket one C-ABI call on the stream its kernels run on; the
-    # call's small set-up and finishing launches are timed with the main one
+    # HIP events bracket one C-ABI call on the stream its kernels run on,
+    # queued behind a spin (device time); the call's small set-up and
+    # finishing launches are timed with the main one
     dom = ("k_encode", src_ms, src_bytes, src_gbs,
            "wm_encode_step: k_encode_prepare, k_encode, k_combine, k_encode_finish") \
         if src_ms >= dst_ms else \
@@ -680,11 +700,13 @@ def main():
             "source": {"ms": round(src_ms, 4), "algorithmic_bytes": src_bytes,
                        "GBps": round(src_gbs, 1),
                        "frac_hbm_peak": round(src_gbs / HBM_PEAK_GBS, 4),
-                       "kv_GBps": round(nbytes / (src_ms * 1e-3) / 1e9, 1)},
+                       "kv_GBps": round(nbytes / (src_ms * 1e-3) / 1e9, 1),
+                       "ms_from_idle": round(src_idle_ms, 4)},
             "destination": {"ms": round(dst_ms, 4), "algorithmic_bytes": dst_bytes,
                             "GBps": round(dst_gbs, 1),
                             "frac_hbm_peak": round(dst_gbs / HBM_PEAK_GBS, 4),
-                            "kv_GBps": round(nbytes / (dst_ms * 1e-3) / 1e9, 1)},
+                            "kv_GBps": round(nbytes / (dst_ms * 1e-3) / 1e9, 1),
+                            "ms_from_idle": round(dst_idle_ms, 4)},
         },
         "compression_ratio": round(ratio, 5),
         "payload_bytes": payload_bytes,
