@@ -2598,6 +2598,9 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
     load_chunk(a.cur + (uint64_t)(c < g.n_chunks ? c : 0u) * kChunk,
                c < g.n_chunks ? chunk_len(g, c) : 0u, l0, d);
   }
+  // the first rows are in registers before the loop (as in k_encode)
+#pragma unroll
+  for (int h = 0; h < kRows; ++h) asm volatile("" ::"v"(d[h].x), "v"(d[h].y), "v"(d[h].z), "v"(d[h].w));
 
   bool pend = false, p_dirty = false;
   uint32_t p_nw = 0, p_send = 0;
@@ -2625,8 +2628,14 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
       const bool next_valid = cn < g.n_chunks;
       const uint8_t *nbase = a.cur + (uint64_t)(next_valid ? cn : 0u) * kChunk;
       const uint32_t nlen = next_valid ? chunk_len(g, cn) : 0u;
-      if (need_crc && cur) sh.u[l.wave * 64u + l.lane] = lane_value_load(d, gl, nbase, nlen, l, dn);
-      else load_chunk(nbase, nlen, l, dn);
+      // the younger data wave of each SIMD takes issue priority for the
+      // first half of the rows of each row loop (as in k_encode)
+      if (need_crc && cur) {
+        if (l.wave >= kWaves / 2) __builtin_amdgcn_s_setprio(1);
+        sh.u[l.wave * 64u + l.lane] = lane_value_load(d, gl, nbase, nlen, l, dn);
+      } else {
+        load_chunk(nbase, nlen, l, dn);
+      }
     } else if (cur && l.lane == 0) {
       ticket = atomicAdd(&ctl->ticket, 1u);
     }
@@ -2725,8 +2734,10 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
           reinterpret_cast<uint4 *>(stage)[i] = make_uint4(0, 0, 0, 0);
         if (k) {  // the lane's stream: its words' code lengths
           uint32_t bits = 0;
+          if (l.wave >= kWaves / 2) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
           for (int h = 0; h < kRows; ++h) {
+            if (h == kRows / 2) __builtin_amdgcn_s_setprio(0);
             const uint2 pa = plane_a8<V3>(d[h]);
             const uint32_t w0 = (l.off0 + h * kRow) >> 1;
 #pragma unroll
@@ -2805,8 +2816,10 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
           acc = e32 ? acc >> 32 : acc;
           nb -= e32 && !whole ? 32u : 0u;
         };
+        if (l.wave >= kWaves / 2) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int h = 0; h < kRows; ++h) {
+          if (h == kRows / 2) __builtin_amdgcn_s_setprio(0);
           const uint2 pa = plane_a8<V3>(d[h]);
           const uint32_t w0 = (l.off0 + h * kRow) >> 1;
 #pragma unroll
