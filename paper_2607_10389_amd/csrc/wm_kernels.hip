@@ -2346,16 +2346,22 @@ __device__ __forceinline__ void wave_sync() {
 // The v2 encoder kernels take one chunk per wave, kHufWaves waves per
 // workgroup, each with this scratch (static LDS).
 constexpr int kHufWaves = 8;
+constexpr uint32_t kHufCopies = 8;  // histogram copies while counting
 struct HufWave {
-  uint32_t hist[256];
-  uint32_t wt[256];     // weights of the length construction
-  uint32_t nw[512];     // node weights; canonical codes in the write kernel
-  uint32_t key[256];    // weight << 8 | symbol of the nonzero symbols
-  uint16_t sym[256];    // nonzero symbols
-  uint16_t order[256];  // nonzero symbols by (weight, symbol)
-  uint16_t parent[512];
-  uint8_t depth[512];
-  uint8_t lens[256];
+  union {
+    struct {
+      uint32_t hist[256];
+      uint32_t wt[256];     // weights of the length construction
+      uint32_t nw[512];     // node weights; canonical codes in the write kernel
+      uint32_t key[256];    // weight << 8 | symbol of the nonzero symbols
+      uint16_t sym[256];    // nonzero symbols
+      uint16_t order[256];  // nonzero symbols by (weight, symbol)
+      uint16_t parent[512];
+      uint8_t depth[512];
+      uint8_t lens[256];
+    };
+    uint32_t copies[256 * kHufCopies];  // the count's copies, folded into hist
+  };
 };
 static_assert(sizeof(HufWave) * kHufWaves <= 65536, "v2 encoder scratch");
 
@@ -2477,9 +2483,10 @@ constexpr uint32_t kLdsHufEncode = kLdsHufCode + 1024;
 static_assert(kLdsHufEncode <= 163840, "fused format v2 encoder LDS fits one CU");
 
 // Code lengths of format v2/v3, one chunk per wave (kHufWaves per
-// workgroup): the plane-A histogram (four interleaved copies, bin b of copy
-// c at 4b + c, copy = lane mod 4, so equal symbols of neighbouring lanes hit
-// different banks), then the format's construction.  Plan of item i at
+// workgroup): the plane-A histogram (eight interleaved copies, bin b of copy
+// c at 8b + c, copy = lane mod 8, so equal symbols of neighbouring lanes hit
+// different banks and each address is shared by at most 8 lanes), then the
+// format's construction.  Plan of item i at
 // plans + kHufPlanBytes i: the longest length k, the single symbol (k = 0),
 // and from byte 16 the record's 128 code-length nibble bytes.
 template <bool V3>
@@ -2497,12 +2504,12 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_lengths(
     const uint32_t len = chunk_len(g, c), n = len / 2;
     const uint8_t *base = state + (uint64_t)c * kChunk;
     const Rsrc rs = rsrc(base, len);
-    uint32_t *H4 = W.hist;
-    static_assert(offsetof(HufWave, wt) == 1024 && offsetof(HufWave, nw) == 2048 &&
-                  sizeof(HufWave::nw) == 2048, "hist, wt, nw: 1024 contiguous words");
-    for (int q = 0; q < 4; ++q) reinterpret_cast<uint4 *>(H4)[q * 64 + lane] = make_uint4(0, 0, 0, 0);
+    uint32_t *H8 = W.copies;
+    constexpr uint32_t kQ = 256u * kHufCopies / 256u;  // 16-byte pieces per lane
+#pragma unroll
+    for (uint32_t q = 0; q < kQ; ++q) reinterpret_cast<uint4 *>(H8)[q * 64 + lane] = make_uint4(0, 0, 0, 0);
     wave_sync();
-    const uint32_t cp = lane & 3u;
+    const uint32_t cp = lane & (kHufCopies - 1u);
     for (uint32_t q = 0; q < 8u; ++q) {
       uint4 x[8];
 #pragma unroll
@@ -2519,16 +2526,20 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_lengths(
         const uint32_t i0 = 8u * (512u * q + lane + 64u * h);
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-          if (i0 + j < n) atomicAdd(&H4[4u * pa_of(V3, word_of(x[h], j)) + cp], 1u);
+          if (i0 + j < n) atomicAdd(&H8[kHufCopies * pa_of(V3, word_of(x[h], j)) + cp], 1u);
       }
     }
     wave_sync();
-    {  // fold the copies into hist (every read is issued before any write)
-      uint4 cs[4];
+    {  // fold the copies into hist: lane l sums bins 4l..4l+3 (every read is
+       // issued before any write)
+      static_assert(kHufCopies == 8, "two 16-byte reads per bin");
+      uint4 cs[8];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) cs[q] = reinterpret_cast<const uint4 *>(H4)[q * 64 + lane];
+      for (int q = 0; q < 8; ++q) cs[q] = reinterpret_cast<const uint4 *>(H8)[8 * lane + q];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) W.hist[q * 64 + lane] = cs[q].x + cs[q].y + cs[q].z + cs[q].w;
+      for (int b = 0; b < 4; ++b)
+        W.hist[4 * lane + b] = cs[2 * b].x + cs[2 * b].y + cs[2 * b].z + cs[2 * b].w +
+                               cs[2 * b + 1].x + cs[2 * b + 1].y + cs[2 * b + 1].z + cs[2 * b + 1].w;
     }
     wave_sync();
     const uint32_t k = huf_lengths_wave(W, lane);
