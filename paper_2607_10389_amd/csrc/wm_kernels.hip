@@ -2482,6 +2482,17 @@ constexpr uint32_t kLdsHufCode = kLdsStage + kLdsStageBytes;  // 256 x u32: reve
 constexpr uint32_t kLdsHufEncode = kLdsHufCode + 1024;
 static_assert(kLdsHufEncode <= 163840, "fused format v2 encoder LDS fits one CU");
 
+// Byte offset of the counter of plane A of the low (HI = 0) or high word of
+// dword x, copy cp4 / 4: (symbol * kHufCopies + copy) * 4, from the word's
+// bits with one shift and one mask (the symbol is bits 7..14 of the word in
+// format v2, bits 8..15 in format v3).
+template <bool V3, int HI>
+__device__ __forceinline__ uint32_t huf_bin_off(uint32_t x, uint32_t cp4) {
+  static_assert(kHufCopies == 8, "symbol * 32 bytes");
+  constexpr int sh = (V3 ? 3 : 2) + 16 * HI;
+  return ((x >> sh) & 0x1FE0u) | cp4;
+}
+
 // Code lengths of format v2/v3, one chunk per wave (kHufWaves per
 // workgroup): the plane-A histogram (eight interleaved copies, bin b of copy
 // c at 8b + c, copy = lane mod 8, so equal symbols of neighbouring lanes hit
@@ -2521,12 +2532,25 @@ __global__ __launch_bounds__(64 * kHufWaves) void k_huf_lengths(
           if (o < len && o + 16u > len) x[h] = load16_partial(base + o, len - o);
         }
       }
+      if (len == kChunk) {  // a full chunk: every word counts, no per-word test
+        uint8_t *H8b = reinterpret_cast<uint8_t *>(H8);
 #pragma unroll
-      for (int h = 0; h < 8; ++h) {
-        const uint32_t i0 = 8u * (512u * q + lane + 64u * h);
+        for (int h = 0; h < 8; ++h) {
+          const uint32_t xs[4] = {x[h].x, x[h].y, x[h].z, x[h].w};
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (i0 + j < n) atomicAdd(&H8[kHufCopies * pa_of(V3, word_of(x[h], j)) + cp], 1u);
+          for (int j = 0; j < 4; ++j) {
+            atomicAdd(reinterpret_cast<uint32_t *>(H8b + huf_bin_off<V3, 0>(xs[j], 4u * cp)), 1u);
+            atomicAdd(reinterpret_cast<uint32_t *>(H8b + huf_bin_off<V3, 1>(xs[j], 4u * cp)), 1u);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+          const uint32_t i0 = 8u * (512u * q + lane + 64u * h);
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            if (i0 + j < n) atomicAdd(&H8[kHufCopies * pa_of(V3, word_of(x[h], j)) + cp], 1u);
+        }
       }
     }
     wave_sync();
