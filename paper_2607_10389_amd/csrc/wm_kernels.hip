@@ -2600,6 +2600,12 @@ __device__ __forceinline__ uint2 plane_b8(const uint4 &x) {
   }
 }
 
+// A bool as a type, to pick an instance of a generic lambda.
+template <bool B>
+struct BoolC {
+  static constexpr bool value = B;
+};
+
 template <bool V3>
 __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom g) {
   WsCtl *ctl = reinterpret_cast<WsCtl *>(a.ws + a.L.ctl);
@@ -2768,19 +2774,28 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
         for (uint32_t i = (kHufHead - 16u) / 16u + threadIdx.x; i < kLdsStageBytes / 16u; i += kThreads)
           reinterpret_cast<uint4 *>(stage)[i] = make_uint4(0, 0, 0, 0);
         if (k) {  // the lane's stream: its words' code lengths
-          uint32_t bits = 0;
-          if (l.wave >= kWaves / 2) __builtin_amdgcn_s_setprio(1);
+          // (a full chunk takes an instance without the per-word test, so
+          // that a row's eight table reads go out together instead of one
+          // branch and round trip per word)
+          auto lengths = [&](auto full_c) {
+            constexpr bool kFull = decltype(full_c)::value;
+            uint32_t bits = 0;
+            if (l.wave >= kWaves / 2) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-          for (int h = 0; h < kRows; ++h) {
-            if (h == kRows / 2) __builtin_amdgcn_s_setprio(0);
-            const uint2 pa = plane_a8<V3>(d[h]);
-            const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+            for (int h = 0; h < kRows; ++h) {
+              if (h == kRows / 2) __builtin_amdgcn_s_setprio(0);
+              const uint2 pa = plane_a8<V3>(d[h]);
+              const uint32_t w0 = (l.off0 + h * kRow) >> 1;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-              const uint32_t e = ((j < 4 ? pa.x : pa.y) >> (8 * (j & 3))) & 255u;
-              if (w0 + j < n_words) bits += code[e] >> 24;
+              for (int j = 0; j < 8; ++j) {
+                const uint32_t e = ((j < 4 ? pa.x : pa.y) >> (8 * (j & 3))) & 255u;
+                if (kFull || w0 + j < n_words) bits += code[e] >> 24;
+              }
             }
-          }
+            return bits;
+          };
+          const uint32_t bits =
+              n_words == kChunk / 2 ? lengths(BoolC<true>{}) : lengths(BoolC<false>{});
           sb_lane = (bits + 7u) >> 3;
           const uint32_t incl = wave_incl_scan(sb_lane);
           lane_excl = incl - sb_lane;
@@ -2851,21 +2866,28 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
           acc = e32 ? acc >> 32 : acc;
           nb -= e32 && !whole ? 32u : 0u;
         };
-        if (l.wave >= kWaves / 2) __builtin_amdgcn_s_setprio(1);
+        // (a full chunk takes an instance without the per-word test, as
+        // above)
+        auto pack = [&](auto full_c) {
+          constexpr bool kFull = decltype(full_c)::value;
+          if (l.wave >= kWaves / 2) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-        for (int h = 0; h < kRows; ++h) {
-          if (h == kRows / 2) __builtin_amdgcn_s_setprio(0);
-          const uint2 pa = plane_a8<V3>(d[h]);
-          const uint32_t w0 = (l.off0 + h * kRow) >> 1;
+          for (int h = 0; h < kRows; ++h) {
+            if (h == kRows / 2) __builtin_amdgcn_s_setprio(0);
+            const uint2 pa = plane_a8<V3>(d[h]);
+            const uint32_t w0 = (l.off0 + h * kRow) >> 1;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const uint32_t e = ((j < 4 ? pa.x : pa.y) >> (8 * (j & 3))) & 255u;
-            const uint32_t cw = w0 + j < n_words ? code[e] : 0u;
-            acc |= (uint64_t)(cw & 0xFFFFFFu) << nb;
-            nb += cw >> 24;
-            if (j & 1) emit(false);  // at most 22 bits since the last emission
+            for (int j = 0; j < 8; ++j) {
+              const uint32_t e = ((j < 4 ? pa.x : pa.y) >> (8 * (j & 3))) & 255u;
+              const uint32_t cw = kFull || w0 + j < n_words ? code[e] : 0u;
+              acc |= (uint64_t)(cw & 0xFFFFFFu) << nb;
+              nb += cw >> 24;
+              if (j & 1) emit(false);  // at most 22 bits since the last emission
+            }
           }
-        }
+        };
+        if (n_words == kChunk / 2) pack(BoolC<true>{});
+        else pack(BoolC<false>{});
         emit(true);  // fewer than 32 bits are left
       } else if (mode == 0u) {  // RAW: plane A, one byte per word
 #pragma unroll
