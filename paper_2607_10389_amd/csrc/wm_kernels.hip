@@ -2370,7 +2370,80 @@ static_assert(sizeof(HufWave) * kHufWaves <= 65536, "v2 encoder scratch");
 // before an internal node of equal weight, a symbol's length its depth;
 // counts halved while the longest exceeds kHufMaxLen).  Returns the longest
 // length (0 for a single symbol, which is then W.order[0]).
+// The same construction for 2..64 distinct symbols with every pass in
+// registers: lane l holds the weights of symbols l, 64 + l, 128 + l and
+// 192 + l (wq), the keys (weight << 8 | symbol) are gathered into lanes
+// 0..m-1 through LDS, each lane ranks its key against the m keys read from
+// the other lanes, the sorted keys give the leaves in order, and a pass that
+// needs capping halves wq in place.
+__device__ uint32_t huf_lengths_small(HufWave &W, uint32_t lane, uint32_t (&wq)[4], uint32_t m) {
+  constexpr uint32_t kInf = 0xFFFFFFFFu;
+  for (int q = 0; q < 4; ++q) W.lens[q * 64 + lane] = 0;
+  for (;;) {
+    uint32_t i0 = 0;
+    for (int q = 0; q < 4; ++q) {
+      const unsigned long long msk = __ballot(wq[q] != 0u);
+      if (wq[q]) W.key[i0 + lanes_below(msk)] = (wq[q] << 8) | (q * 64 + lane);
+      i0 += (uint32_t)__popcll(msk);
+    }
+    wave_sync();
+    const uint32_t key = lane < m ? W.key[lane] : kInf;
+    uint32_t rank = 0;  // keys are distinct: ranks 0..m-1 are a permutation
+    for (uint32_t j = 0; j < m; ++j)
+      rank += (uint32_t)__builtin_amdgcn_readlane((int)key, (int)j) < key ? 1u : 0u;
+    if (lane < m) W.nw[rank] = key;
+    wave_sync();
+    const uint32_t skey = lane < m ? W.nw[lane] : kInf;  // lane r: the key of rank r
+    wave_sync();  // (W.key and W.nw are written again by the next pass)
+    // leaf i in lane i, internal node j (node m + j) in lane j; picks read
+    // lanes at uniform indices
+    const uint32_t leafw = lane < m ? skey >> 8 : kInf;
+    uint32_t intw = kInf, par_leaf = 0, par_int = 0;
+    uint32_t li = 0, ii = 0, n_int = 0;
+    for (uint32_t s2 = 0; s2 + 1 < m; ++s2) {
+      uint32_t wsum = 0;
+      for (int q = 0; q < 2; ++q) {
+        const uint32_t wl = li < m ? (uint32_t)__builtin_amdgcn_readlane((int)leafw, (int)li) : kInf;
+        const uint32_t wi = ii < n_int ? (uint32_t)__builtin_amdgcn_readlane((int)intw, (int)ii) : kInf;
+        if (li < m && (ii >= n_int || wl <= wi)) {
+          par_leaf = lane == li ? n_int : par_leaf;
+          wsum += wl;
+          ++li;
+        } else {
+          par_int = lane == ii ? n_int : par_int;
+          wsum += wi;
+          ++ii;
+        }
+      }
+      intw = lane == n_int ? wsum : intw;
+      ++n_int;
+    }
+    uint32_t dint = 0;  // depth of internal node j; the root (last) is 0
+    for (int32_t j = (int32_t)n_int - 2; j >= 0; --j) {
+      const uint32_t p = (uint32_t)__builtin_amdgcn_readlane((int)par_int, j);
+      const uint32_t dp = (uint32_t)__builtin_amdgcn_readlane((int)dint, (int)p);
+      dint = lane == (uint32_t)j ? dp + 1u : dint;
+    }
+    const uint32_t dleaf = (uint32_t)__shfl((int)dint, (int)(lane < m ? par_leaf : 0u), 64) + 1u;
+    const uint32_t longest = uniform(wave_max(lane < m ? dleaf : 0u));
+    if (longest <= kHufMaxLen) {
+      if (lane < m) W.lens[skey & 255u] = (uint8_t)dleaf;
+      wave_sync();
+      return longest;
+    }
+    for (int q = 0; q < 4; ++q) wq[q] = wq[q] ? (wq[q] + 1u) >> 1 : 0u;
+  }
+}
+
 __device__ uint32_t huf_lengths_wave(HufWave &W, uint32_t lane) {
+  {
+    uint32_t wq[4], m = 0;
+    for (int q = 0; q < 4; ++q) {
+      wq[q] = W.hist[q * 64 + lane];
+      m += (uint32_t)__popcll(__ballot(wq[q] != 0u));
+    }
+    if (m >= 2u && m <= 64u) return huf_lengths_small(W, lane, wq, m);
+  }
   for (int q = 0; q < 4; ++q) W.wt[q * 64 + lane] = W.hist[q * 64 + lane];
   for (;;) {
     wave_sync();
