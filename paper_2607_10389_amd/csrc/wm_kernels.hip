@@ -686,6 +686,7 @@ struct EncShared {
   alignas(16) uint32_t H[256];  // histogram
   int64_t my_last;              // control: this workgroup's last finished item
   uint64_t my_last_incl;        //          and its inclusive prefix
+  uint32_t p4_done;             // format v2/v3: data waves through phase 4
 };
 static_assert(sizeof(EncShared) <= kLdsMiscBytes, "encoder scratch fits");
 constexpr uint32_t kLdsHistE = kLdsLow;   // 256 bins x 32 copies of 2 x u16 (32 KiB)
@@ -2537,7 +2538,8 @@ __device__ uint32_t huf_lengths_wave(HufWave &W, uint32_t lane) {
 // found its code lengths, in the v1 encoder's pipeline (one workgroup per
 // CU, 8 data waves holding a chunk in registers, a control wave, tickets and
 // the decoupled look-back; iteration i computes X_i and writes X_{i-1}):
-//   phase 1: data: X_i's lane CRC values while X_{i+1} loads
+//   phase 1: data: X_i's lane CRC values while X_{i+1} loads; control:
+//            X_{i-1}'s look-back, header and table entry, the next ticket
 //   phase 2: control: X_i's plan (code lengths) loads
 //   phase 3: data: write X_{i-1} (staged section, then plane B from
 //            registers); control: first CRC step, X_i's canonical codes into
@@ -2546,13 +2548,14 @@ __device__ uint32_t huf_lengths_wave(HufWave &W, uint32_t lane) {
 //   phase 4: data: X_i's plane-B bytes, each lane's stream byte count;
 //            control: X_i's CRC
 //   phase 5: all: the record's mode and size from the stream totals;
-//            control: publish, look-back, header and table entry; data: the
-//            code-length nibbles, stream byte counts and streams (HUF) or
-//            plane A (RAW) into staging
+//            control: publish X_i's size, its header CRC and the entry's
+//            CRC prefix; data: the code-length nibbles, stream byte counts
+//            and streams (HUF) or plane A (RAW) into staging
 // Stream s = wave * 64 + lane holds the lane's 8 words of each of its wave's
 // 8 rows, which are in its registers.
 constexpr uint32_t kLdsHufCode = kLdsStage + kLdsStageBytes;  // 256 x u32: reversed code | len << 24
-constexpr uint32_t kLdsHufEncode = kLdsHufCode + 1024;
+constexpr uint32_t kLdsHufPend = kLdsHufCode + 1024;  // the control wave's RecFields of X_{i-1}
+constexpr uint32_t kLdsHufEncode = kLdsHufPend + 64;
 static_assert(kLdsHufEncode <= 163840, "fused format v2 encoder LDS fits one CU");
 
 // Byte offset of the counter of plane A of the low (HI = 0) or high word of
@@ -2699,6 +2702,7 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
   if (threadIdx.x == (uint32_t)kThreads) {
     sh.first = atomicAdd(&ctl->ticket, 1u);
     sh.next = atomicAdd(&ctl->ticket, 1u);
+    sh.p4_done = 0;
   }
   __syncthreads();
   uint32_t item = uniform(sh.first);
@@ -2720,6 +2724,10 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
   uint32_t p_nw = 0, p_send = 0;
   int64_t my_last = -1;
   uint64_t my_last_incl = 0;
+  // control: X_{i-1}'s record fields, emitted in phase 1 (in LDS: as
+  // registers they would stay allocated through the data waves' phases)
+  static_assert(sizeof(RecFields) <= 64, "pending record fields fit");
+  RecFields &pr = *reinterpret_cast<RecFields *>(lds_at(kLdsHufPend));
   uint2 smp[kRows];
 #pragma unroll
   for (int h = 0; h < kRows; ++h) smp[h] = make_uint2(0, 0);
@@ -2735,6 +2743,7 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
     const bool dirty = cur && !bad_index;
     uint4 dn[kRows];
     uint32_t ticket = 0;
+    uint32_t pk_v = 0, pbase_v = 0, nib = 0;  // control: X_i's plan as loaded
 
     // ---- phase 1
     if (!is_ctl) {
@@ -2750,23 +2759,43 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
       } else {
         load_chunk(nbase, nlen, l, dn);
       }
-    } else if (cur && l.lane == 0) {
-      ticket = atomicAdd(&ctl->ticket, 1u);
+    } else {
+      // control: X_{i-1}'s look-back and emission, deferred from the end of
+      // iteration i-1.  Its aggregate went out then, as did those of the
+      // items just before it in the other workgroups, so the walk rarely
+      // waits; the next ticket is taken in the same round trip, its address
+      // through a register the compiler cannot see into (no uniform-address
+      // atomic combining, which would wait for the result at once).  The
+      // offset reaches the data waves before B2, where they first use it.
+      // X_i's plan loads go out first, with the ticket and the window, so
+      // that the round trips overlap (read in phase 2)
+      if (dirty) {
+        const uint8_t *P = a.plans + (uint64_t)item * kHufPlanBytes;
+        pk_v = ld_u32(P);
+        pbase_v = ld_u32(P + 4);
+        nib = *reinterpret_cast<const uint16_t *>(P + 16 + 2 * l.lane);
+      }
+      uint32_t zero = 0;
+      asm volatile("" : "+v"(zero));
+      if (cur && l.lane == 0) ticket = atomicAdd(&ctl->ticket + zero, 1u);
+      if (pend) {
+        const RecFields r = pr;
+        ctl_emit(a, r, lookback_issue(status, (int64_t)r.item - 1, my_last, my_last_incl),
+                 n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
+      }
     }
 
     // ---- phase 2
     uint32_t crc = 0;
-    uint32_t pk = 0, pbase = 0, nib = 0;  // control: X_i's plan (k_huf_lengths)
+    uint32_t pk = 0, pbase = 0;  // control: X_i's plan (k_huf_lengths)
     if (is_ctl) {
       if (cur) {
         if (!need_crc) crc = bad_index ? 0u : ld_const(a.crc_in + c);
         if (l.lane == 0) sh.ticket[it & 1] = ticket;
       }
       if (dirty) {
-        const uint8_t *P = a.plans + (uint64_t)item * kHufPlanBytes;
-        pk = uniform(ld_u32(P));
-        pbase = uniform(ld_u32(P + 4));
-        nib = *reinterpret_cast<const uint16_t *>(P + 16 + 2 * l.lane);
+        pk = uniform(pk_v);
+        pbase = uniform(pbase_v);
       }
     }
     __syncthreads();  // B2: lane values and X_{i-1}'s offset
@@ -2877,6 +2906,27 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
 #pragma unroll
         for (int h = 0; h < kRows; ++h) smp[h] = plane_b8<V3>(d[h]);
       }
+      if (cur && item != 0u) {
+        // The last data wave through phase 4 publishes X_i's size (every
+        // wave's stream total is in LDS by then), a phase before the
+        // control wave could: the next items' look-backs, a phase later,
+        // then find it in place instead of waiting for it.
+        __threadfence_block();
+        uint32_t done = 0;
+        if (l.lane == 0) done = atomicAdd(&sh.p4_done, 1u);
+        if (__builtin_amdgcn_readfirstlane(done) == (uint32_t)kWaves - 1u) {
+          __threadfence_block();
+          uint32_t sbt = 0;
+          if (dirty && k) {
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) sbt += uniform(sh.esc_w[w]);
+          }
+          const uint64_t raw = raw_rec_size(n_words), hs = huf_rec_size(n_words, k, sbt);
+          const uint32_t sz = dirty ? (uint32_t)(hs < raw ? hs : raw) : 0u;
+          const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(sz >> 4) << 26);
+          if (l.lane == 0) status_store(&status[item], agg | kFlagAgg);
+        }
+      }
     }
     __syncthreads();  // B4: stream totals known
 
@@ -2906,18 +2956,15 @@ __global__ __launch_bounds__(kEncThreads) void k_huf_encode(EncArgs a, ChunkGeom
     }
     const uint32_t kr = mode == 2u ? k : 0u;
     if (is_ctl && cur) {
-      if (item != 0 && l.lane == 0) {
-        const uint64_t agg = ((uint64_t)(dirty ? 1u : 0u) << 2) | ((uint64_t)(size >> 4) << 26);
-        status_store(&status[item], agg | kFlagAgg);
-      }
-      const Window win = lookback_issue(status, (int64_t)item - 1, my_last, my_last_incl);
+      // X_i's size went out in phase 4; the look-back and emission wait for
+      // the next iteration's phase 1
+      if (l.lane == 0) sh.p4_done = 0;
       const uint32_t hw[3] = {mode | (kr << 8) | (base << 16), n_words, sb};
       const uint32_t hcrc = crc_words(hw, 3);
       const uint32_t ew2[2] = {c, crc};
       const uint32_t epart = crc_feed(0xFFFFFFFFu, ew2, 2);
-      const RecFields r = {item, c, n_words, mode, kr, base, sb, size, crc, dirty, bad_index,
-                           hcrc, epart};
-      ctl_emit(a, r, win, n_items, status, ctl, tab_ws, ecrc, sh, my_last, my_last_incl);
+      if (l.lane == 0)
+        pr = RecFields{item, c, n_words, mode, kr, base, sb, size, crc, dirty, bad_index, hcrc, epart};
     }
     if (!is_ctl && dirty) {
       if (mode == 2u && k) {
