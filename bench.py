@@ -122,10 +122,10 @@ def counter_pass(args):
                       "state_bytes": state.numel() * 2}), flush=True)
 
 
-# GPU clock cycles of the spin that each timed run waits behind (about 0.15
-# ms at the shader clock): long enough for the host to enqueue a whole call
-# before the GPU reaches it.
-PREROLL_CYCLES = 300_000
+# GPU clock cycles of the spin that each timed run waits behind (about 0.45
+# ms at the shader clock): long enough for the host to enqueue a whole call,
+# Python binding included, before the GPU reaches it.
+PREROLL_CYCLES = 1_000_000
 
 
 def timed_events(torch, fn, n, warmup=3, preroll=True):
