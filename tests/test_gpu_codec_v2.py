@@ -92,6 +92,18 @@ def _edge_states():
         sm = rng.integers(0, 256, n)
         w = (((sm >> 7) << 15) | (e << 7) | (sm & 127)).astype(np.uint16)
         out[f"laplace_{scale}"] = w.view(np.uint8)
+    # exactly 64 and 65 distinct exponents in every chunk, with geometric
+    # counts (codes past the length cap, several capping passes): the two
+    # sides of the 64-symbol limit of the register-resident construction
+    rng2 = np.random.default_rng(11)
+    for m_sym in (64, 65):
+        g = np.minimum(rng2.geometric(0.12, n) - 1, m_sym - 1)
+        for cw in range(0, n, CH // 2):
+            g[cw:cw + m_sym] = np.arange(m_sym)
+        e = 60 + g
+        sm = rng2.integers(0, 256, n)
+        w = (((sm >> 7) << 15) | (e << 7) | (sm & 127)).astype(np.uint16)
+        out[f"exact_{m_sym}_exponents"] = w.view(np.uint8)
     return out
 
 
@@ -104,6 +116,19 @@ def test_wide_alphabet_states_plan_huf(scale, min_distinct):
         ch = state[c:c + CH]
         e = (ch.view(np.uint16) >> 7) & 255
         assert np.unique(e).size >= min_distinct
+        plan = oracle.plan_chunk_v2(ch)
+        assert plan["mode"] == 2 and plan["k"] == 11, plan
+
+
+@pytest.mark.parametrize("m_sym", [64, 65])
+def test_boundary_alphabet_states_plan_huf(m_sym):
+    """The boundary states have exactly 64 or 65 exponents in every chunk
+    and plan HUF at the length cap (so their GPU test exercises both sides
+    of the 64-symbol limit, with capping passes)."""
+    state = _edge_states()[f"exact_{m_sym}_exponents"]
+    for c in range(0, state.size, CH):
+        ch = state[c:c + CH]
+        assert np.unique((ch.view(np.uint16) >> 7) & 255).size == m_sym
         plan = oracle.plan_chunk_v2(ch)
         assert plan["mode"] == 2 and plan["k"] == 11, plan
 
