@@ -69,6 +69,61 @@ def test_length_limit():
     assert sum(2.0 ** -int(l) for l in lens if l) == 1.0
 
 
+def min_depth_code(counts):
+    """(cost, longest length) of the optimal prefix code with the smallest
+    longest length: merges taken from a heap ordered by (weight, subtree
+    height, creation order), so among equal weights the shallower subtree
+    goes first."""
+    h = [(int(c), 0, i) for i, c in enumerate(counts) if c > 0]
+    if len(h) <= 1:
+        return 0, 0
+    heapq.heapify(h)
+    seq, cost = len(counts), 0
+    while len(h) > 1:
+        a, b = heapq.heappop(h), heapq.heappop(h)
+        cost += a[0] + b[0]
+        heapq.heappush(h, (a[0] + b[0], max(a[1], b[1]) + 1, seq))
+        seq += 1
+    return cost, h[0][1]
+
+
+@pytest.mark.parametrize("kind", ["geometric", "pareto", "flat", "log_uniform"])
+def test_capped_lengths_match_an_independent_construction(kind):
+    # The length limit: counts are halved (rounding up, so no symbol drops
+    # out) until the code fits in 11 bits.  Independently: halve until the
+    # smallest-longest optimal code fits, then the oracle's lengths must be
+    # an optimal code of exactly those counts, with that longest length.  A
+    # floor halving, a limit off by one or one halving too many fails here.
+    rng = np.random.default_rng({"geometric": 1, "pareto": 2, "flat": 3, "log_uniform": 4}[kind])
+    n_capped = 0
+    for _ in range(60):
+        m = int(rng.integers(2, 120))
+        counts = np.zeros(256, np.int64)
+        syms = rng.choice(256, m, replace=False)
+        if kind == "geometric":
+            counts[syms] = rng.geometric(rng.uniform(0.05, 0.5), m)
+        elif kind == "pareto":
+            counts[syms] = (rng.pareto(rng.uniform(0.3, 1.5), m) * 3 + 1).astype(np.int64)
+        elif kind == "flat":
+            counts[syms] = rng.integers(1, 4, m)
+        else:
+            counts[syms] = (2.0 ** rng.uniform(0, 16, m)).astype(np.int64)
+        counts = np.minimum(counts, 60000)
+        lens, k = oracle.huffman_lengths(counts.astype(np.uint32))
+        c, halvings = counts.copy(), 0
+        while min_depth_code(c)[1] > MAXLEN:
+            c = (c + 1) >> 1
+            halvings += 1
+        n_capped += halvings > 0
+        cost, longest = min_depth_code(c)
+        assert set(np.nonzero(lens)[0]) == set(syms)
+        assert int((c * lens).sum()) == cost
+        assert k == longest == int(lens.max())
+        assert sum(2.0 ** -int(x) for x in lens if x) == 1.0
+    if kind in ("pareto", "log_uniform"):
+        assert n_capped > 10  # the cap is really exercised
+
+
 def test_degenerate_counts():
     counts = np.zeros(256, np.uint32)
     assert oracle.huffman_lengths(counts)[1] == 0
