@@ -154,7 +154,7 @@ def _rebuilt(kind, payload64, chunk, n):
     return p
 
 
-@pytest.mark.parametrize("codec", [1, 2])
+@pytest.mark.parametrize("codec", [1, 2, 3])
 @pytest.mark.parametrize("kind", [0, 1])
 def test_tiles_partial_chunk_tables(wm, kind, codec):
     """Tables that ship part of a chunk are table errors; whole chunks pass
@@ -251,7 +251,7 @@ def test_tiles_precopy_rounds(wm, kind):
         assert torch.equal(dest, src) and torch.equal(shipped, src)
 
 
-@pytest.mark.parametrize("codec", [1, 2])
+@pytest.mark.parametrize("codec", [1, 2, 3])
 def test_production_in_4mib_chunks(wm, codec):
     """The production cache is exactly 399 chunks of 4 MiB: full ship and a
     step whose dirty chunks come from the 75% tile rewrite, against the
@@ -273,7 +273,7 @@ def test_production_in_4mib_chunks(wm, codec):
     assert m.commit(None, scatter=False) == 0
     torch.cuda.synchronize()
     assert torch.equal(m.staging[:nbytes], prev.view(-1).view(torch.uint8))
-    if codec == 2:
+    if codec != 1:
         return
     # a step that rewrites about 2% of the tiles dirties many 4 MiB chunks
     ids = wm_inputs.permuted_chunks(nbytes // TILE, 500, seed=9, device="cuda")
